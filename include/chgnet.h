@@ -1,0 +1,163 @@
+/*
+ * chgnet.h - C interface of the MI355X (gfx950) FastCHGNet training-step library.
+ *
+ * The library computes one training step of the FastCHGNet model (Zhou et al.,
+ * "FastCHGNet: Training one Universal Interatomic Potential to 1.5 Hours with
+ * 32 GPUs"): crystal structures in; energy, forces and stress out (Sec. II-B,
+ * Fig. 1a); gradients of a weighted loss with respect to every weight out
+ * (Sec. IV, "Parameters Setting").
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ *  - Every array argument is a DEVICE pointer owned by the caller. The library
+ *    never allocates device memory: scratch space is the caller's `ws`
+ *    buffer of `ws_bytes` bytes, sized by chgnet_workspace_size().
+ *  - `stream` is a hipStream_t passed as void* (NULL = the null stream). Every
+ *    call only enqueues work on `stream` and returns, except
+ *    chgnet_build_graph, which waits once for the graph's sizes (see there).
+ *  - Floating-point data are IEEE fp32; integer data are int32 unless noted.
+ *  - All matrices are row-major. A lattice is 3x3 with ROWS = lattice vectors,
+ *    so Cartesian = fractional @ lattice.
+ *  - No global state: calls are re-entrant as long as concurrent calls use
+ *    different workspaces. Results are bitwise reproducible run to run (no
+ *    floating-point atomics).
+ *  - Return value: CHGNET_OK (0) or a negative error code below; the text of
+ *    the last error of the calling thread is chgnet_last_error_string().
+ *
+ * Hyperparameters (Sec. IV): feature width d (64; 128 supported), layers T,
+ * 31 radial and 31 angular basis functions, envelope exponent p = 8, atom
+ * graph cutoff 6 A, bond graph cutoff 3 A. Supported: d in {64, 128},
+ * 1 <= T <= 16, 1 <= n_rbf <= 64, n_fourier odd in [1, 63], p in [2, 16],
+ * 0 < r_bond <= r_atom <= 20.
+ */
+#ifndef CHGNET_H
+#define CHGNET_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define CHGNET_OK 0
+#define CHGNET_EINVAL -1    /* bad shape, hyperparameter or input value          */
+#define CHGNET_ECAPACITY -2 /* graph capacity too small; required sizes returned  */
+#define CHGNET_EWORKSPACE -3 /* workspace too small                               */
+#define CHGNET_EHIP -4      /* HIP runtime error                                 */
+
+typedef struct {
+  int32_t d;          /* feature width of atoms, bonds and angles           */
+  int32_t n_layers;   /* number of interaction blocks T                     */
+  int32_t n_rbf;      /* radial basis size (31)                             */
+  int32_t n_fourier;  /* angular basis size, odd (31 = 1 + 15 cos + 15 sin) */
+  int32_t envelope_p; /* polynomial envelope exponent p (8)                 */
+  float r_atom;       /* atom-graph cutoff, Angstrom (6)                    */
+  float r_bond;       /* bond-graph cutoff, Angstrom (3)                    */
+} chgnet_hparams;
+
+/* A batch of S crystals with N atoms in total (Alg. 2: all structures
+ * concatenated). Atoms of structure s are atom_ptr[s] .. atom_ptr[s+1]-1. */
+typedef struct {
+  int32_t n_struct;        /* S >= 1                                             */
+  int32_t n_atoms;         /* N = atom_ptr[S] >= 1                               */
+  const int32_t* atom_ptr; /* [S+1], atom_ptr[0] = 0, non-decreasing           */
+  const float* pos;        /* [N,3] Cartesian positions, Angstrom (not wrapped) */
+  const float* lattice;    /* [S,3,3] rows = lattice vectors, |det| >= 1e-6     */
+  const int32_t* Z;        /* [N] atomic numbers in 1..94                       */
+} chgnet_batch;
+
+/* Atom graph G^a, bond graph G^b and angle list (Sec. II-B (1)).
+ *  Edges: all directed (i, j, n) with i, j in one crystal, n in Z^3,
+ *   (i,j,n) != (i,i,0) and D2 < r_atom^2, where D2 is the fp32 expression
+ *      s_c = ((n1*L1c) + (n2*L2c)) + (n3*L3c);  dl_c = (r_jc + s_c) - r_ic;
+ *      D2  = ((dl_x*dl_x) + (dl_y*dl_y)) + (dl_z*dl_z)
+ *   evaluated with one round-to-nearest per operation (no fused multiply-add).
+ *   Every translation is kept (no truncation). Order: CSR by i, then by j,
+ *   then (n1, n2, n3) lexicographically.
+ *  Bonds: the edges with D2 < r_bond^2, in edge order.
+ *  Angles: at every centre atom with bonds b_1 < ... < b_k, the k(k-1) ordered
+ *   pairs (b, b') with b != b', ordered by (b, b'). */
+typedef struct {
+  int64_t cap_edges, cap_bonds, cap_angles; /* in: capacity of the arrays below   */
+  int64_t n_edges, n_bonds, n_angles;       /* out: E, B, A (also on ECAPACITY)   */
+  int32_t* edge_ptr;  /* [N+1] CSR offsets of edges by source atom                */
+  int32_t* edge_dst;  /* [E]   destination atom j                                 */
+  int32_t* edge_img;  /* [E,3] lattice translation n                              */
+  int32_t* edge_rev;  /* [E]   index of (j, i, -n)                                */
+  int32_t* bond_ptr;  /* [N+1] CSR offsets of bonds by source atom                */
+  int32_t* bond_edge; /* [B]   edge index of each bond                            */
+  int32_t* angle_ptr; /* [B+1] angles whose first bond is b: angle_ptr[b]..[b+1]-1 */
+  int32_t* angle_b2;  /* [A]   second bond of each angle; may be NULL (not built) */
+} chgnet_graph;
+
+/* Number of fp32 parameters in the flat parameter vector for `hp`.
+ * Flat layout, in this order (row-major, "W [a,b]" maps a inputs to b outputs):
+ *   W_Z [94,d] element table; f_a [R], f_b [R] sRBF frequencies (6 A, 3 A);
+ *   W_e [R,2d] columns e^0 | e^a; b_e0 [d]; W_eb [R,d]; W_th [K,d]; b_th [d];
+ *   per layer t = 0..T-1:
+ *     atom conv : W [3d,2d] (input rows v_i | v_j | e_ij, output columns
+ *                 core | gate), b [2d], g_c [d], b_c [d], g_g [d], b_g [d]
+ *                 (LayerNorm scale/shift of core and gate), Wo [d,d], bo [d]
+ *     bond conv : W [4d,2d] (input rows v_i | e_ij | e_ik | a_ijk), b [2d],
+ *                 g_c, b_c, g_g, b_g [d], Wo [d,d], bo [d]
+ *     angle upd.: only if t < T-1: W [4d,2d], b [2d], g_c, b_c, g_g, b_g [d]
+ *   heads E, F, S (energy, force, stress), each:
+ *     W1 [d,d], b1 [d], W2 [d,d], b2 [d], W3 [d,o], b3 [o], o = 1, 1, 9.
+ * d = 64, T = 4, R = K = 31 gives 405,001; d = 128, T = 5 gives 1,975,753. */
+int chgnet_param_count(const chgnet_hparams* hp, int64_t* n);
+
+/* Workspace bytes for a batch of S structures, N atoms and at most E edges,
+ * B bonds and A angles. chgnet_build_graph needs the size for (N, S) with
+ * E = B = A = 0 or more; forward/backward/step need the full size. */
+int chgnet_workspace_size(const chgnet_hparams* hp, int64_t N, int64_t E, int64_t B, int64_t A, int64_t S,
+                          size_t* bytes);
+
+/* Build G^a, G^b and the angle list of `batch` into `graph` (cell-list search).
+ * Waits once on `stream` to read E, B and A back; sets graph->n_edges etc.
+ * If any capacity is too small nothing beyond the counts is written and
+ * CHGNET_ECAPACITY is returned: grow the arrays and call again.
+ * Errors: EINVAL for bad shapes, Z outside 1..94, |det L| < 1e-6, a lattice
+ * too thin for the cutoff (more than 64 cells of images per axis), positions
+ * more than 10^4 A or 200 cells from the origin cell, or more than 8192
+ * edges on one atom. */
+int chgnet_build_graph(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_graph* graph, void* ws,
+                       size_t ws_bytes, void* stream);
+
+/* Forward pass (Eq. 2-9 with the Eq. 11 inputs): energy [S] (total energy of
+ * each crystal), forces [N,3], stress [S,3,3]. `graph` must hold a graph of
+ * `batch` (n_edges/n_bonds/n_angles set; angle_b2 may be NULL). If
+ * save_for_backward != 0 the activations stay in `ws` for chgnet_backward. */
+int chgnet_forward(const chgnet_hparams* hp, const chgnet_batch* batch, const chgnet_graph* graph,
+                   const float* params, float* energy, float* forces, float* stress, int save_for_backward,
+                   void* ws, size_t ws_bytes, void* stream);
+
+/* Backward pass for the weights: grad [P] (overwritten) = d/dparams of
+ * sum(dE*energy) + sum(dF*forces) + sum(dS*stress), using the activations of
+ * the preceding chgnet_forward(save_for_backward=1) on the same ws, batch,
+ * graph and params. Positions and lattices are not differentiated. */
+int chgnet_backward(const chgnet_hparams* hp, const chgnet_batch* batch, const chgnet_graph* graph,
+                    const float* params, const float* dE, const float* dF, const float* dS, float* grad, void* ws,
+                    size_t ws_bytes, void* stream);
+
+/* One training step: build graph, forward, loss, backward, optional Adam.
+ * Loss = w0 * mean_s (E_s/n_s - E_target_s)^2 + w1 * mean (F - F_target)^2
+ *      + w2 * mean (stress - S_target)^2, loss_w = {w0, w1, w2} on the HOST
+ * (the paper's prefactors are 2, 1.5, 0.1). E_target [S] is per atom.
+ * loss [1] is a device scalar. If adam_hp (HOST array {lr, beta1, beta2, eps,
+ * t}, t >= 1 the step number) is non-NULL, params, adam_m and adam_v [P] are
+ * updated in place by bias-corrected Adam; otherwise params are unchanged and
+ * adam_m / adam_v may be NULL. energy/forces/stress outputs are not returned
+ * (use chgnet_forward). Errors as for chgnet_build_graph. */
+int chgnet_step(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_graph* graph, float* params,
+                const float* E_target, const float* F_target, const float* S_target, const float* loss_w,
+                float* loss, float* grad, float* adam_m, float* adam_v, const float* adam_hp, void* ws,
+                size_t ws_bytes, void* stream);
+
+/* Text of the last error on the calling thread ("" if none). */
+const char* chgnet_last_error_string(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* CHGNET_H */

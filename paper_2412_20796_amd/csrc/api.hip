@@ -1,0 +1,148 @@
+// C-ABI entry points, hyperparameter validation and the flat parameter layout.
+#include <hip/hip_runtime.h>
+
+#include <string>
+
+#include "common.hpp"
+
+namespace chg {
+
+size_t graph_scratch_bytes(int64_t N, int64_t S);
+size_t acts_bytes(const chgnet_hparams& hp, int64_t N, int64_t E, int64_t B, int64_t A, int64_t S);
+int build_graph(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_graph* graph, void* ws, size_t ws_bytes,
+                hipStream_t st);
+int forward_entry(const chgnet_hparams* hp, const chgnet_batch* batch, const chgnet_graph* graph, const float* params,
+                  float* energy, float* forces, float* stress, void* ws, size_t ws_bytes, hipStream_t st);
+int backward_entry(const chgnet_hparams* hp, const chgnet_batch* batch, const chgnet_graph* graph, const float* params,
+                   const float* dE, const float* dF, const float* dS, float* grad, void* ws, size_t ws_bytes,
+                   hipStream_t st);
+int step_entry(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_graph* graph, float* params,
+               const float* E_t, const float* F_t, const float* S_t, const float* loss_w, float* loss, float* grad,
+               float* adam_m, float* adam_v, const float* adam_hp, void* ws, size_t ws_bytes, hipStream_t st);
+
+namespace {
+thread_local std::string g_last_error;
+}
+
+void set_error(const std::string& msg) { g_last_error = msg; }
+int fail(int code, const std::string& msg) {
+  g_last_error = msg;
+  return code;
+}
+
+int validate_hparams(const chgnet_hparams* hp) {
+  if (!hp) return fail(CHGNET_EINVAL, "hparams is NULL");
+  if (hp->d != 64 && hp->d != 128) return fail(CHGNET_EINVAL, "d must be 64 or 128");
+  if (hp->n_layers < 1 || hp->n_layers > kMaxLayers) return fail(CHGNET_EINVAL, "n_layers must be in 1..16");
+  if (hp->n_rbf < 1 || hp->n_rbf > 64) return fail(CHGNET_EINVAL, "n_rbf must be in 1..64");
+  if (hp->n_fourier < 1 || hp->n_fourier > 63 || hp->n_fourier % 2 == 0)
+    return fail(CHGNET_EINVAL, "n_fourier must be odd and in 1..63");
+  if (hp->envelope_p < 2 || hp->envelope_p > 16) return fail(CHGNET_EINVAL, "envelope_p must be in 2..16");
+  if (!(hp->r_bond > 0.f) || !(hp->r_bond <= hp->r_atom) || !(hp->r_atom <= 20.f))
+    return fail(CHGNET_EINVAL, "cutoffs must satisfy 0 < r_bond <= r_atom <= 20");
+  return CHGNET_OK;
+}
+
+ParamLayout make_layout(const chgnet_hparams& hp) {
+  ParamLayout L{};
+  const int64_t d = hp.d, R = hp.n_rbf, K = hp.n_fourier;
+  int64_t off = 0;
+  auto take = [&](int64_t n) {
+    int64_t o = off;
+    off += n;
+    return o;
+  };
+  L.W_Z = take(94 * d);
+  L.f_a = take(R);
+  L.f_b = take(R);
+  L.W_e = take(R * 2 * d);
+  L.b_e0 = take(d);
+  L.W_eb = take(R * d);
+  L.W_th = take(K * d);
+  L.b_th = take(d);
+  auto gated = [&](int64_t rows) {
+    GatedOffsets g;
+    g.W = take(rows * 2 * d);
+    g.b = take(2 * d);
+    g.g_c = take(d);
+    g.b_c = take(d);
+    g.g_g = take(d);
+    g.b_g = take(d);
+    return g;
+  };
+  for (int t = 0; t < hp.n_layers; ++t) {
+    LayerOffsets& lo = L.layer[t];
+    lo.av = gated(3 * d);
+    lo.av_Wo = take(d * d);
+    lo.av_bo = take(d);
+    lo.be = gated(4 * d);
+    lo.be_Wo = take(d * d);
+    lo.be_bo = take(d);
+    lo.has_angle = t < hp.n_layers - 1;
+    if (lo.has_angle) lo.an = gated(4 * d);
+    else lo.an = lo.be;
+  }
+  const int outs[3] = {1, 1, 9};
+  for (int h = 0; h < 3; ++h) {
+    HeadOffsets& ho = L.head[h];
+    ho.out = outs[h];
+    ho.W1 = take(d * d);
+    ho.b1 = take(d);
+    ho.W2 = take(d * d);
+    ho.b2 = take(d);
+    ho.W3 = take(d * ho.out);
+    ho.b3 = take(ho.out);
+  }
+  L.total = off;
+  return L;
+}
+
+}  // namespace chg
+
+extern "C" {
+
+int chgnet_param_count(const chgnet_hparams* hp, int64_t* n) {
+  CHG_TRY(chg::validate_hparams(hp));
+  if (!n) return chg::fail(CHGNET_EINVAL, "n is NULL");
+  *n = chg::make_layout(*hp).total;
+  return CHGNET_OK;
+}
+
+int chgnet_workspace_size(const chgnet_hparams* hp, int64_t N, int64_t E, int64_t B, int64_t A, int64_t S,
+                          size_t* bytes) {
+  CHG_TRY(chg::validate_hparams(hp));
+  if (!bytes || N < 0 || E < 0 || B < 0 || A < 0 || S < 0) return chg::fail(CHGNET_EINVAL, "bad sizes");
+  *bytes = chg::graph_scratch_bytes(N, S) + chg::acts_bytes(*hp, N, E, B, A, S);
+  return CHGNET_OK;
+}
+
+int chgnet_build_graph(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_graph* graph, void* ws,
+                       size_t ws_bytes, void* stream) {
+  return chg::build_graph(hp, batch, graph, ws, ws_bytes, static_cast<hipStream_t>(stream));
+}
+
+int chgnet_forward(const chgnet_hparams* hp, const chgnet_batch* batch, const chgnet_graph* graph, const float* params,
+                   float* energy, float* forces, float* stress, int save_for_backward, void* ws, size_t ws_bytes,
+                   void* stream) {
+  (void)save_for_backward;  // activations are always kept in ws
+  return chg::forward_entry(hp, batch, graph, params, energy, forces, stress, ws, ws_bytes,
+                            static_cast<hipStream_t>(stream));
+}
+
+int chgnet_backward(const chgnet_hparams* hp, const chgnet_batch* batch, const chgnet_graph* graph, const float* params,
+                    const float* dE, const float* dF, const float* dS, float* grad, void* ws, size_t ws_bytes,
+                    void* stream) {
+  return chg::backward_entry(hp, batch, graph, params, dE, dF, dS, grad, ws, ws_bytes, static_cast<hipStream_t>(stream));
+}
+
+int chgnet_step(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_graph* graph, float* params,
+                const float* E_target, const float* F_target, const float* S_target, const float* loss_w, float* loss,
+                float* grad, float* adam_m, float* adam_v, const float* adam_hp, void* ws, size_t ws_bytes,
+                void* stream) {
+  return chg::step_entry(hp, batch, graph, params, E_target, F_target, S_target, loss_w, loss, grad, adam_m, adam_v,
+                         adam_hp, ws, ws_bytes, static_cast<hipStream_t>(stream));
+}
+
+const char* chgnet_last_error_string(void) { return chg::g_last_error.c_str(); }
+
+}  // extern "C"

@@ -1,0 +1,87 @@
+// Shared host/device helpers of the gfx950 FastCHGNet library.
+#pragma once
+#include <hip/hip_runtime.h>
+
+#include <cstddef>
+#include <cstdint>
+#include <string>
+
+#include "chgnet.h"
+
+namespace chg {
+
+// ---------------------------------------------------------------------------
+// Error reporting: the last error text per host thread.
+// ---------------------------------------------------------------------------
+void set_error(const std::string& msg);
+int fail(int code, const std::string& msg);
+
+#define CHG_HIP(call)                                                                         \
+  do {                                                                                        \
+    hipError_t _e = (call);                                                                   \
+    if (_e != hipSuccess)                                                                     \
+      return ::chg::fail(CHGNET_EHIP, std::string(#call) + ": " + hipGetErrorString(_e));   \
+  } while (0)
+
+#define CHG_TRY(expr)           \
+  do {                          \
+    int _r = (expr);            \
+    if (_r != CHGNET_OK) return _r; \
+  } while (0)
+
+// Launch-error check after a kernel launch.
+#define CHG_LAUNCHED(name)                                                                    \
+  do {                                                                                        \
+    hipError_t _e = hipGetLastError();                                                        \
+    if (_e != hipSuccess)                                                                     \
+      return ::chg::fail(CHGNET_EHIP, std::string("launch ") + name + ": " + hipGetErrorString(_e)); \
+  } while (0)
+
+inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
+inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+// Bump allocator over the caller's workspace (256-byte aligned slices).
+struct Arena {
+  char* base = nullptr;
+  size_t cap = 0;
+  size_t used = 0;
+  template <class T>
+  T* take(int64_t count) {
+    size_t off = align_up(used, 256);
+    used = off + sizeof(T) * (size_t)(count > 0 ? count : 0);
+    if (base == nullptr || used > cap) return reinterpret_cast<T*>(base ? base + (off < cap ? off : 0) : nullptr);
+    return reinterpret_cast<T*>(base + off);
+  }
+  bool ok() const { return used <= cap; }
+};
+
+int validate_hparams(const chgnet_hparams* hp);
+
+// ---------------------------------------------------------------------------
+// Flat parameter layout (see include/chgnet.h).
+// ---------------------------------------------------------------------------
+struct GatedOffsets {
+  int64_t W, b, g_c, b_c, g_g, b_g;  // W [rows, 2d], b [2d], LayerNorm [d] x 4
+};
+struct LayerOffsets {
+  GatedOffsets av;  // atom conv, W [3d, 2d]
+  int64_t av_Wo, av_bo;
+  GatedOffsets be;  // bond conv, W [4d, 2d]
+  int64_t be_Wo, be_bo;
+  GatedOffsets an;  // angle update (valid if has_angle), W [4d, 2d]
+  bool has_angle;
+};
+struct HeadOffsets {
+  int64_t W1, b1, W2, b2, W3, b3;
+  int out;
+};
+constexpr int kMaxLayers = 16;
+struct ParamLayout {
+  int64_t W_Z, f_a, f_b, W_e, b_e0, W_eb, W_th, b_th;
+  LayerOffsets layer[kMaxLayers];
+  HeadOffsets head[3];  // E, F, S
+  int64_t total;
+};
+ParamLayout make_layout(const chgnet_hparams& hp);
+
+}  // namespace chg

@@ -1,0 +1,565 @@
+// Periodic atom graph, bond graph and angle list on gfx950 (Sec. II-B (1)).
+//
+// Cell-list search: each crystal's cell is cut into n_a slabs per lattice
+// axis, each at least r + margin thick (so the neighbours of an atom lie in
+// the slabs within K_a = floor((r + margin) n_a / h_a) + 1 of its own, with
+// periodic images handled by "virtual" slab indices), atoms are binned by
+// their wrapped fractional coordinates, and one wavefront per atom tests all
+// candidates with the exact fp32 inclusion expression. The accepted (j, n)
+// keys of an atom are then sorted in LDS into the canonical (j, n1, n2, n3)
+// order, so the output does not depend on the order in which atoms landed in
+// their bins. One host wait reads the sizes E, B, A back.
+#include <hip/hip_runtime.h>
+
+#include <climits>
+#include <cmath>
+
+#include "common.hpp"
+
+namespace chg {
+
+namespace {
+
+constexpr double kMargin = 0.05;      // Angstrom added to the cutoff for binning
+constexpr int kMaxK = 64;             // max slab reach per axis
+constexpr int kMaxWrap = 200;         // max |cell index| of an input position
+constexpr float kMaxCoord = 1.0e4f;   // max |Cartesian coordinate|
+constexpr int kMaxEdgesPerAtom = 8192;
+constexpr int kImgBias = 512;         // image components stored as n + 512 in 10 bits
+
+enum ErrBits { ERR_Z = 1, ERR_DET = 2, ERR_THIN = 4, ERR_FAR = 8, ERR_REV = 16, ERR_PTR = 32 };
+
+struct StructInfo {
+  double Linv[9];
+  float L[9];
+  int nb[3];
+  int K[3];
+  int bin_base;
+  int pad;
+};
+
+struct GraphInfo {
+  long long n_edges, n_bonds, n_angles;
+  int max_count;
+  int err;
+};
+
+// ---------------------------------------------------------------------------
+// The exact fp32 cutoff expression: one rounding per operation, no FMA.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ float pair_d2(const float* ri, const float* rj, int n1, int n2, int n3, const float* L) {
+#pragma clang fp contract(off)
+  const float f1 = (float)n1, f2 = (float)n2, f3 = (float)n3;
+  const float sx = (f1 * L[0] + f2 * L[3]) + f3 * L[6];
+  const float sy = (f1 * L[1] + f2 * L[4]) + f3 * L[7];
+  const float sz = (f1 * L[2] + f2 * L[5]) + f3 * L[8];
+  const float dx = (rj[0] + sx) - ri[0];
+  const float dy = (rj[1] + sy) - ri[1];
+  const float dz = (rj[2] + sz) - ri[2];
+  return (dx * dx + dy * dy) + dz * dz;
+}
+
+__device__ __forceinline__ int floor_mod(int v, int n) {
+  int r = v % n;
+  return r < 0 ? r + n : r;
+}
+
+__device__ __forceinline__ int find_struct(const int* atom_ptr, int S, int i) {
+  int lo = 0, hi = S - 1;  // last s with atom_ptr[s] <= i
+  while (lo < hi) {
+    int mid = (lo + hi + 1) >> 1;
+    if (atom_ptr[mid] <= i) lo = mid; else hi = mid - 1;
+  }
+  return lo;
+}
+
+// Per-structure setup: inverse lattice, slab counts and reach. One block.
+__global__ void k_struct_setup(int S, const int* __restrict__ atom_ptr, const float* __restrict__ lattice, float r,
+                               StructInfo* __restrict__ info, int* __restrict__ total_bins, GraphInfo* ginfo) {
+  for (int s = threadIdx.x; s < S; s += blockDim.x) {
+    StructInfo si;
+    double L[9];
+    for (int k = 0; k < 9; ++k) {
+      si.L[k] = lattice[s * 9 + k];
+      L[k] = (double)si.L[k];
+    }
+    // rows a0, a1, a2; cofactor rows give the reciprocal basis
+    double c0[3] = {L[4] * L[8] - L[5] * L[7], L[5] * L[6] - L[3] * L[8], L[3] * L[7] - L[4] * L[6]};
+    double c1[3] = {L[7] * L[2] - L[8] * L[1], L[8] * L[0] - L[6] * L[2], L[6] * L[1] - L[7] * L[0]};
+    double c2[3] = {L[1] * L[5] - L[2] * L[4], L[2] * L[3] - L[0] * L[5], L[0] * L[4] - L[1] * L[3]};
+    double det = L[0] * c0[0] + L[1] * c0[1] + L[2] * c0[2];
+    int n_s = atom_ptr[s + 1] - atom_ptr[s];
+    if (!(fabs(det) >= 1e-6) || n_s < 0) {
+      atomicOr(&ginfo->err, n_s < 0 ? ERR_PTR : ERR_DET);
+      for (int k = 0; k < 9; ++k) si.Linv[k] = 0.0;
+      si.nb[0] = si.nb[1] = si.nb[2] = 1;
+      si.K[0] = si.K[1] = si.K[2] = 0;
+      info[s] = si;
+      continue;
+    }
+    // frac = cart @ Linv, Linv = L^{-1}; column a of Linv = c_a / det
+    for (int row = 0; row < 3; ++row) {
+      si.Linv[row * 3 + 0] = c0[row] / det;
+      si.Linv[row * 3 + 1] = c1[row] / det;
+      si.Linv[row * 3 + 2] = c2[row] / det;
+    }
+    double vol = fabs(det);
+    double h[3];
+    const double* cs[3] = {c0, c1, c2};
+    for (int a = 0; a < 3; ++a) h[a] = vol / sqrt(cs[a][0] * cs[a][0] + cs[a][1] * cs[a][1] + cs[a][2] * cs[a][2]);
+    const double rr = (double)r + kMargin;
+    long long nb[3];
+    for (int a = 0; a < 3; ++a) {
+      double q = floor(h[a] / rr);
+      nb[a] = q < 1.0 ? 1 : (q > 1024.0 ? 1024 : (long long)q);
+    }
+    long long cap = n_s > 1 ? n_s : 1;
+    while (nb[0] * nb[1] * nb[2] > cap) {
+      int a = 0;
+      if (nb[1] > nb[a]) a = 1;
+      if (nb[2] > nb[a]) a = 2;
+      nb[a] -= 1;
+    }
+    bool thin = false;
+    for (int a = 0; a < 3; ++a) {
+      si.nb[a] = (int)nb[a];
+      double kk = floor(rr * (double)nb[a] / h[a]) + 1.0;
+      if (kk > kMaxK) { thin = true; kk = 0; }
+      si.K[a] = (int)kk;
+    }
+    if (thin) atomicOr(&ginfo->err, ERR_THIN);
+    info[s] = si;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int acc = 0;
+    for (int s = 0; s < S; ++s) {
+      info[s].bin_base = acc;
+      acc += info[s].nb[0] * info[s].nb[1] * info[s].nb[2];
+    }
+    *total_bins = acc;
+  }
+}
+
+__global__ void k_atom_bin(int N, int S, const int* __restrict__ atom_ptr, const float* __restrict__ pos,
+                           const int* __restrict__ Z, const StructInfo* __restrict__ info, int* __restrict__ atom_struct,
+                           int* __restrict__ atom_bin, int* __restrict__ atom_cell, int* __restrict__ atom_wrap,
+                           int* __restrict__ bin_count, GraphInfo* ginfo) {
+  int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= N) return;
+  int s = find_struct(atom_ptr, S, i);
+  atom_struct[i] = s;
+  int z = Z[i];
+  if (z < 1 || z > 94) atomicOr(&ginfo->err, ERR_Z);
+  const StructInfo& si = info[s];
+  float p[3] = {pos[i * 3 + 0], pos[i * 3 + 1], pos[i * 3 + 2]};
+  int err = 0;
+  int c[3], w[3];
+  for (int a = 0; a < 3; ++a) {
+    if (!(fabsf(p[a]) <= kMaxCoord)) err |= ERR_FAR;
+    double f = (double)p[0] * si.Linv[0 * 3 + a] + (double)p[1] * si.Linv[1 * 3 + a] + (double)p[2] * si.Linv[2 * 3 + a];
+    double fl = floor(f);
+    if (!(fabs(fl) <= kMaxWrap)) { err |= ERR_FAR; fl = 0.0; }
+    double fr = f - fl;
+    int ca = (int)floor(fr * si.nb[a]);
+    ca = ca < 0 ? 0 : (ca >= si.nb[a] ? si.nb[a] - 1 : ca);
+    c[a] = ca;
+    w[a] = (int)fl;
+  }
+  if (err) atomicOr(&ginfo->err, err);
+  int bin = si.bin_base + (c[0] * si.nb[1] + c[1]) * si.nb[2] + c[2];
+  atom_bin[i] = bin;
+  for (int a = 0; a < 3; ++a) {
+    atom_cell[i * 3 + a] = c[a];
+    atom_wrap[i * 3 + a] = w[a];
+  }
+  atomicAdd(&bin_count[bin], 1);
+}
+
+// Exclusive scan of n ints with one block (any n). out[n] = total.
+__global__ void k_scan_single(int n, const int* __restrict__ in, int* __restrict__ out) {
+  __shared__ int part[1024];
+  __shared__ int carry;
+  if (threadIdx.x == 0) carry = 0;
+  __syncthreads();
+  for (int base = 0; base < n; base += blockDim.x) {
+    int idx = base + threadIdx.x;
+    int v = idx < n ? in[idx] : 0;
+    part[threadIdx.x] = v;
+    __syncthreads();
+    for (int off = 1; off < (int)blockDim.x; off <<= 1) {
+      int t = threadIdx.x >= off ? part[threadIdx.x - off] : 0;
+      __syncthreads();
+      part[threadIdx.x] += t;
+      __syncthreads();
+    }
+    if (idx < n) out[idx] = carry + part[threadIdx.x] - v;
+    __syncthreads();
+    if (threadIdx.x == blockDim.x - 1) carry += part[threadIdx.x];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) out[n] = carry;
+}
+
+__global__ void k_bin_fill(int N, const int* __restrict__ atom_bin, const int* __restrict__ bin_start,
+                           int* __restrict__ bin_cursor, int* __restrict__ bin_atoms) {
+  int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= N) return;
+  int b = atom_bin[i];
+  int slot = atomicAdd(&bin_cursor[b], 1);
+  bin_atoms[bin_start[b] + slot] = i;
+}
+
+struct SearchArgs {
+  int N;
+  float rc2_atom, rc2_bond;
+  const float* pos;
+  const StructInfo* info;
+  const int* atom_struct;
+  const int* atom_cell;
+  const int* atom_wrap;
+  const int* bin_start;
+  const int* bin_atoms;
+};
+
+// Visit every candidate (j, n) of atom i; calls f(j, n1, n2, n3, d2) on the
+// lanes of one wavefront for the candidates that pass the atom cutoff.
+template <class F>
+__device__ __forceinline__ void for_each_neighbour(const SearchArgs& A, int i, F&& f) {
+  const int lane = threadIdx.x & 63;
+  const int s = A.atom_struct[i];
+  const StructInfo& si = A.info[s];
+  float L[9];
+  for (int k = 0; k < 9; ++k) L[k] = si.L[k];
+  const float ri[3] = {A.pos[i * 3 + 0], A.pos[i * 3 + 1], A.pos[i * 3 + 2]};
+  const int ci[3] = {A.atom_cell[i * 3 + 0], A.atom_cell[i * 3 + 1], A.atom_cell[i * 3 + 2]};
+  const int wi[3] = {A.atom_wrap[i * 3 + 0], A.atom_wrap[i * 3 + 1], A.atom_wrap[i * 3 + 2]};
+  for (int d0 = -si.K[0]; d0 <= si.K[0]; ++d0) {
+    const int v0 = ci[0] + d0, b0 = floor_mod(v0, si.nb[0]), m0 = (v0 - b0) / si.nb[0];
+    for (int d1 = -si.K[1]; d1 <= si.K[1]; ++d1) {
+      const int v1 = ci[1] + d1, b1 = floor_mod(v1, si.nb[1]), m1 = (v1 - b1) / si.nb[1];
+      for (int d2 = -si.K[2]; d2 <= si.K[2]; ++d2) {
+        const int v2 = ci[2] + d2, b2 = floor_mod(v2, si.nb[2]), m2 = (v2 - b2) / si.nb[2];
+        const int bin = si.bin_base + (b0 * si.nb[1] + b1) * si.nb[2] + b2;
+        const int lo = A.bin_start[bin], hi = A.bin_start[bin + 1];
+        for (int base = lo; base < hi; base += 64) {
+          const int idx = base + lane;
+          bool pass = false;
+          int j = 0, n1 = 0, n2 = 0, n3 = 0;
+          float dd = 0.f;
+          if (idx < hi) {
+            j = A.bin_atoms[idx];
+            n1 = m0 - A.atom_wrap[j * 3 + 0] + wi[0];
+            n2 = m1 - A.atom_wrap[j * 3 + 1] + wi[1];
+            n3 = m2 - A.atom_wrap[j * 3 + 2] + wi[2];
+            const float rj[3] = {A.pos[j * 3 + 0], A.pos[j * 3 + 1], A.pos[j * 3 + 2]};
+            dd = pair_d2(ri, rj, n1, n2, n3, L);
+            pass = dd < A.rc2_atom && !(j == i && n1 == 0 && n2 == 0 && n3 == 0);
+          }
+          f(pass, j, n1, n2, n3, dd);
+        }
+      }
+    }
+  }
+}
+
+__device__ __forceinline__ int wave_sum(int v) {
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+  return v;
+}
+
+// One wavefront per atom: count edges and bonds.
+__global__ void __launch_bounds__(256) k_count(SearchArgs A, int* __restrict__ edge_count, int* __restrict__ bond_count) {
+  const int i = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (i >= A.N) return;
+  int ne = 0, nb = 0;
+  for_each_neighbour(A, i, [&](bool pass, int, int, int, int, float dd) {
+    ne += pass ? 1 : 0;
+    nb += (pass && dd < A.rc2_bond) ? 1 : 0;
+  });
+  ne = wave_sum(ne);
+  nb = wave_sum(nb);
+  if ((threadIdx.x & 63) == 0) {
+    edge_count[i] = ne;
+    bond_count[i] = nb;
+  }
+}
+
+// Exclusive scans of edge counts, bond counts and k(k-1); totals into ginfo.
+__global__ void k_scan_counts(int N, const int* __restrict__ edge_count, const int* __restrict__ bond_count,
+                              int* __restrict__ edge_ptr, int* __restrict__ bond_ptr, long long* __restrict__ angle_base,
+                              GraphInfo* ginfo) {
+  __shared__ long long pe[1024], pb[1024], pa[1024];
+  __shared__ long long ce, cb, ca;
+  __shared__ int mx[1024];
+  if (threadIdx.x == 0) { ce = cb = ca = 0; }
+  int my_max = 0;
+  __syncthreads();
+  for (int base = 0; base < N; base += blockDim.x) {
+    const int idx = base + threadIdx.x;
+    long long ve = 0, vb = 0, va = 0;
+    if (idx < N) {
+      ve = edge_count[idx];
+      vb = bond_count[idx];
+      va = vb * (vb - 1);
+      my_max = max(my_max, (int)ve);
+    }
+    pe[threadIdx.x] = ve; pb[threadIdx.x] = vb; pa[threadIdx.x] = va;
+    __syncthreads();
+    for (int off = 1; off < (int)blockDim.x; off <<= 1) {
+      long long te = 0, tb = 0, ta = 0;
+      if (threadIdx.x >= off) { te = pe[threadIdx.x - off]; tb = pb[threadIdx.x - off]; ta = pa[threadIdx.x - off]; }
+      __syncthreads();
+      pe[threadIdx.x] += te; pb[threadIdx.x] += tb; pa[threadIdx.x] += ta;
+      __syncthreads();
+    }
+    if (idx < N) {
+      long long e0 = ce + pe[threadIdx.x] - ve, b0 = cb + pb[threadIdx.x] - vb, a0 = ca + pa[threadIdx.x] - va;
+      edge_ptr[idx] = (int)(e0 < INT_MAX ? e0 : INT_MAX);
+      bond_ptr[idx] = (int)(b0 < INT_MAX ? b0 : INT_MAX);
+      angle_base[idx] = a0;
+    }
+    __syncthreads();
+    if (threadIdx.x == blockDim.x - 1) { ce += pe[threadIdx.x]; cb += pb[threadIdx.x]; ca += pa[threadIdx.x]; }
+    __syncthreads();
+  }
+  mx[threadIdx.x] = my_max;
+  __syncthreads();
+  for (int off = blockDim.x / 2; off > 0; off >>= 1) {
+    if ((int)threadIdx.x < off) mx[threadIdx.x] = max(mx[threadIdx.x], mx[threadIdx.x + off]);
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    edge_ptr[N] = (int)(ce < INT_MAX ? ce : INT_MAX);
+    bond_ptr[N] = (int)(cb < INT_MAX ? cb : INT_MAX);
+    angle_base[N] = ca;
+    ginfo->n_edges = ce;
+    ginfo->n_bonds = cb;
+    ginfo->n_angles = ca;
+    ginfo->max_count = mx[0];
+  }
+}
+
+__device__ __forceinline__ unsigned long long make_key(int j, int n1, int n2, int n3, bool bond) {
+  return ((unsigned long long)(unsigned)j << 31) | ((unsigned long long)(n1 + kImgBias) << 21) |
+         ((unsigned long long)(n2 + kImgBias) << 11) | ((unsigned long long)(n3 + kImgBias) << 1) |
+         (bond ? 1ull : 0ull);
+}
+
+// One 64-thread block per atom: gather accepted keys into LDS, bitonic sort,
+// write edges in canonical order and the atom's bond list.
+__global__ void __launch_bounds__(64) k_fill(SearchArgs A, int sort_size, const int* __restrict__ edge_ptr,
+                                             const int* __restrict__ bond_ptr, int* __restrict__ edge_dst,
+                                             int* __restrict__ edge_img, int* __restrict__ bond_edge) {
+  extern __shared__ unsigned long long keys[];
+  const int i = blockIdx.x;
+  const int lane = threadIdx.x;
+  int count = 0;
+  for_each_neighbour(A, i, [&](bool pass, int j, int n1, int n2, int n3, float dd) {
+    const unsigned long long m = __ballot(pass);
+    if (pass) {
+      const int rank = __popcll(m & ((1ull << lane) - 1ull));
+      const int slot = count + rank;
+      if (slot < sort_size) keys[slot] = make_key(j, n1, n2, n3, dd < A.rc2_bond);
+    }
+    count += __popcll(m);
+  });
+  for (int k = count + lane; k < sort_size; k += 64) keys[k] = ~0ull;
+  __syncthreads();
+  // bitonic sort of sort_size (power of two) keys
+  for (int size = 2; size <= sort_size; size <<= 1) {
+    for (int stride = size >> 1; stride > 0; stride >>= 1) {
+      for (int t = lane; t < sort_size / 2; t += 64) {
+        const int lo = 2 * t - (t & (stride - 1));
+        const int hi = lo + stride;
+        const bool up = (lo & size) == 0;
+        const unsigned long long a = keys[lo], b = keys[hi];
+        if ((a > b) == up) { keys[lo] = b; keys[hi] = a; }
+      }
+      __syncthreads();
+    }
+  }
+  const int e0 = edge_ptr[i];
+  const int b0 = bond_ptr[i];
+  int nb = 0;
+  for (int base = 0; base < count; base += 64) {
+    const int k = base + lane;
+    bool bond = false;
+    if (k < count) {
+      const unsigned long long key = keys[k];
+      const int j = (int)(key >> 31);
+      edge_dst[e0 + k] = j;
+      edge_img[(e0 + k) * 3 + 0] = (int)((key >> 21) & 1023) - kImgBias;
+      edge_img[(e0 + k) * 3 + 1] = (int)((key >> 11) & 1023) - kImgBias;
+      edge_img[(e0 + k) * 3 + 2] = (int)((key >> 1) & 1023) - kImgBias;
+      bond = (key & 1ull) != 0;
+    }
+    const unsigned long long m = __ballot(bond);
+    if (bond) bond_edge[b0 + nb + __popcll(m & ((1ull << lane) - 1ull))] = e0 + k;
+    nb += __popcll(m);
+  }
+}
+
+// Reverse map: binary search of (i, -n) in the sorted edge list of j.
+__global__ void k_rev(int N, const int* __restrict__ edge_ptr, const int* __restrict__ edge_dst,
+                      const int* __restrict__ edge_img, int* __restrict__ edge_rev, GraphInfo* ginfo) {
+  const int i = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (i >= N) return;
+  const int lane = threadIdx.x & 63;
+  for (int e = edge_ptr[i] + lane; e < edge_ptr[i + 1]; e += 64) {
+    const int j = edge_dst[e];
+    const int t0 = -edge_img[e * 3 + 0], t1 = -edge_img[e * 3 + 1], t2 = -edge_img[e * 3 + 2];
+    int lo = edge_ptr[j], hi = edge_ptr[j + 1] - 1, found = -1;
+    while (lo <= hi) {
+      const int mid = (lo + hi) >> 1;
+      const int k0 = edge_dst[mid], k1 = edge_img[mid * 3 + 0], k2 = edge_img[mid * 3 + 1], k3 = edge_img[mid * 3 + 2];
+      int cmp = k0 != i ? (k0 < i ? -1 : 1)
+                        : (k1 != t0 ? (k1 < t0 ? -1 : 1) : (k2 != t1 ? (k2 < t1 ? -1 : 1) : (k3 != t2 ? (k3 < t2 ? -1 : 1) : 0)));
+      if (cmp == 0) { found = mid; break; }
+      if (cmp < 0) lo = mid + 1; else hi = mid - 1;
+    }
+    if (found < 0) atomicOr(&ginfo->err, ERR_REV);
+    edge_rev[e] = found < 0 ? e : found;
+  }
+}
+
+__global__ void k_angles(int N, const int* __restrict__ bond_ptr, const long long* __restrict__ angle_base,
+                         int* __restrict__ angle_ptr, int* __restrict__ angle_b2) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= N) return;
+  const int b0 = bond_ptr[i], k = bond_ptr[i + 1] - b0;
+  const long long a0 = angle_base[i];
+  for (int p = 0; p < k; ++p) angle_ptr[b0 + p] = (int)(a0 + (long long)p * (k - 1));
+  if (i == N - 1) angle_ptr[bond_ptr[N]] = (int)angle_base[N];
+  if (angle_b2) {
+    for (int p = 0; p < k; ++p)
+      for (int q = 0; q < k; ++q)
+        if (q != p) angle_b2[a0 + (long long)p * (k - 1) + (q < p ? q : q - 1)] = b0 + q;
+  }
+}
+
+struct GraphScratch {
+  StructInfo* info;
+  GraphInfo* ginfo;
+  int* total_bins;
+  int *atom_struct, *atom_bin, *atom_cell, *atom_wrap;
+  int *bin_count, *bin_start, *bin_cursor, *bin_atoms;
+  int *edge_count, *bond_count;
+  long long* angle_base;
+};
+
+void carve(Arena& ar, int64_t N, int64_t S, GraphScratch& g) {
+  const int64_t nbins = N + S + 1;
+  g.info = ar.take<StructInfo>(S);
+  g.ginfo = ar.take<GraphInfo>(1);
+  g.total_bins = ar.take<int>(1);
+  g.atom_struct = ar.take<int>(N);
+  g.atom_bin = ar.take<int>(N);
+  g.atom_cell = ar.take<int>(3 * N);
+  g.atom_wrap = ar.take<int>(3 * N);
+  g.bin_count = ar.take<int>(nbins + 1);
+  g.bin_start = ar.take<int>(nbins + 1);
+  g.bin_cursor = ar.take<int>(nbins + 1);
+  g.bin_atoms = ar.take<int>(N);
+  g.edge_count = ar.take<int>(N);
+  g.bond_count = ar.take<int>(N);
+  g.angle_base = ar.take<long long>(N + 1);
+}
+
+}  // namespace
+
+size_t graph_scratch_bytes(int64_t N, int64_t S) {
+  Arena ar;
+  GraphScratch g;
+  carve(ar, N, S, g);
+  return align_up(ar.used, 256);
+}
+
+int validate_batch(const chgnet_batch* b) {
+  if (!b || b->n_struct < 1 || b->n_atoms < 1 || !b->atom_ptr || !b->pos || !b->lattice || !b->Z)
+    return fail(CHGNET_EINVAL, "batch: need n_struct >= 1, n_atoms >= 1 and non-null arrays");
+  return CHGNET_OK;
+}
+
+int build_graph(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_graph* graph, void* ws, size_t ws_bytes,
+                hipStream_t st) {
+  CHG_TRY(validate_hparams(hp));
+  CHG_TRY(validate_batch(batch));
+  if (!graph || !graph->edge_ptr || !graph->bond_ptr) return fail(CHGNET_EINVAL, "graph: edge_ptr and bond_ptr are required");
+  const int N = batch->n_atoms, S = batch->n_struct;
+  Arena ar{static_cast<char*>(ws), ws_bytes, 0};
+  GraphScratch g;
+  carve(ar, N, S, g);
+  if (!ws || !ar.ok()) return fail(CHGNET_EWORKSPACE, "workspace too small for the graph build");
+  const int64_t nbins_cap = (int64_t)N + S + 1;
+
+  CHG_HIP(hipMemsetAsync(g.ginfo, 0, sizeof(GraphInfo), st));
+  CHG_HIP(hipMemsetAsync(g.bin_count, 0, sizeof(int) * (nbins_cap + 1), st));
+  CHG_HIP(hipMemsetAsync(g.bin_cursor, 0, sizeof(int) * (nbins_cap + 1), st));
+  k_struct_setup<<<1, 256, 0, st>>>(S, batch->atom_ptr, batch->lattice, hp->r_atom, g.info, g.total_bins, g.ginfo);
+  CHG_LAUNCHED("k_struct_setup");
+  k_atom_bin<<<cdiv(N, 256), 256, 0, st>>>(N, S, batch->atom_ptr, batch->pos, batch->Z, g.info, g.atom_struct, g.atom_bin,
+                                           g.atom_cell, g.atom_wrap, g.bin_count, g.ginfo);
+  CHG_LAUNCHED("k_atom_bin");
+  // total bins <= N + S (each crystal has at most max(1, n_s) bins)
+  k_scan_single<<<1, 1024, 0, st>>>((int)nbins_cap, g.bin_count, g.bin_start);
+  CHG_LAUNCHED("k_scan_single");
+  k_bin_fill<<<cdiv(N, 256), 256, 0, st>>>(N, g.atom_bin, g.bin_start, g.bin_cursor, g.bin_atoms);
+  CHG_LAUNCHED("k_bin_fill");
+
+  SearchArgs A;
+  A.N = N;
+  A.rc2_atom = hp->r_atom * hp->r_atom;
+  A.rc2_bond = hp->r_bond * hp->r_bond;
+  A.pos = batch->pos;
+  A.info = g.info;
+  A.atom_struct = g.atom_struct;
+  A.atom_cell = g.atom_cell;
+  A.atom_wrap = g.atom_wrap;
+  A.bin_start = g.bin_start;
+  A.bin_atoms = g.bin_atoms;
+  k_count<<<cdiv(N, 4), 256, 0, st>>>(A, g.edge_count, g.bond_count);
+  CHG_LAUNCHED("k_count");
+  k_scan_counts<<<1, 1024, 0, st>>>(N, g.edge_count, g.bond_count, graph->edge_ptr, graph->bond_ptr, g.angle_base,
+                                    g.ginfo);
+  CHG_LAUNCHED("k_scan_counts");
+
+  GraphInfo hinfo;
+  CHG_HIP(hipMemcpyAsync(&hinfo, g.ginfo, sizeof(GraphInfo), hipMemcpyDeviceToHost, st));
+  CHG_HIP(hipStreamSynchronize(st));
+  if (hinfo.err) {
+    std::string m = "build_graph: invalid input:";
+    if (hinfo.err & ERR_Z) m += " Z outside 1..94;";
+    if (hinfo.err & ERR_DET) m += " |det L| < 1e-6;";
+    if (hinfo.err & ERR_THIN) m += " lattice too thin for the cutoff;";
+    if (hinfo.err & ERR_FAR) m += " position too far from the origin cell;";
+    if (hinfo.err & ERR_PTR) m += " atom_ptr decreasing;";
+    return fail(CHGNET_EINVAL, m);
+  }
+  graph->n_edges = hinfo.n_edges;
+  graph->n_bonds = hinfo.n_bonds;
+  graph->n_angles = hinfo.n_angles;
+  if (hinfo.max_count > kMaxEdgesPerAtom)
+    return fail(CHGNET_EINVAL, "build_graph: more than 8192 edges on one atom");
+  if (hinfo.n_edges >= INT_MAX || hinfo.n_angles >= INT_MAX)
+    return fail(CHGNET_EINVAL, "build_graph: graph larger than 2^31 entries");
+  if (hinfo.n_edges > graph->cap_edges || hinfo.n_bonds > graph->cap_bonds || hinfo.n_angles > graph->cap_angles)
+    return fail(CHGNET_ECAPACITY, "build_graph: capacity too small (required sizes written to the graph)");
+  if (hinfo.n_edges > 0 && (!graph->edge_dst || !graph->edge_img || !graph->edge_rev))
+    return fail(CHGNET_EINVAL, "graph: edge arrays are required");
+  if (!graph->angle_ptr || (hinfo.n_bonds > 0 && !graph->bond_edge))
+    return fail(CHGNET_EINVAL, "graph: bond_edge and angle_ptr are required");
+
+  int sort_size = 64;
+  while (sort_size < hinfo.max_count) sort_size <<= 1;
+  k_fill<<<N, 64, sizeof(unsigned long long) * sort_size, st>>>(A, sort_size, graph->edge_ptr, graph->bond_ptr,
+                                                                graph->edge_dst, graph->edge_img, graph->bond_edge);
+  CHG_LAUNCHED("k_fill");
+  k_rev<<<cdiv(N, 4), 256, 0, st>>>(N, graph->edge_ptr, graph->edge_dst, graph->edge_img, graph->edge_rev, g.ginfo);
+  CHG_LAUNCHED("k_rev");
+  k_angles<<<cdiv(N, 256), 256, 0, st>>>(N, graph->bond_ptr, g.angle_base, graph->angle_ptr, graph->angle_b2);
+  CHG_LAUNCHED("k_angles");
+  return CHGNET_OK;
+}
+
+}  // namespace chg

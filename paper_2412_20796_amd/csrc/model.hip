@@ -1,0 +1,1333 @@
+// FastCHGNet forward, loss and weight backward on gfx950.
+//
+// Layer t follows Eq. (4)-(6) with the dependency-free inputs of Eq. (11):
+// atom conv, bond conv and angle update all read (v^t, e^t, a^t). The
+// GatedMLP inputs are concatenations [v_i, v_j, e_ij] and
+// [v_i, e_ij, e_ik, a_ijk]; their first linear layer is split by input block
+// so that only the edge term (e W) and the angle term (a W) are computed per
+// edge / per angle, while the atom and bond terms are computed once per atom
+// and per bond and gathered in the GEMM epilogue. Bond conv and angle update
+// share their input (Eq. (11)) and their two weight blocks form one product.
+//
+// Aggregations are segmented sums over CSR ranges (edges by source atom,
+// angles by first bond), one wavefront per segment, in a fixed order: no
+// floating-point atomics anywhere, so results are bitwise reproducible.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <vector>
+
+#include "common.hpp"
+#include "gemm.hpp"
+
+namespace chg {
+
+size_t graph_scratch_bytes(int64_t N, int64_t S);
+int build_graph(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_graph* graph, void* ws, size_t ws_bytes,
+                hipStream_t st);
+int validate_batch(const chgnet_batch* b);
+
+namespace {
+
+constexpr float kLnEps = 1e-5f;
+constexpr int kGateRowsPerBlock = 64;   // rows per block in backward gate kernels
+constexpr int kFreqRowsPerBlock = 256;  // rows per block in frequency-gradient kernel
+constexpr int64_t kTnPartFloats = 16ll << 20;
+
+__device__ __forceinline__ float sigm(float x) { return 1.0f / (1.0f + __expf(-x)); }
+
+__device__ __forceinline__ float wsum(float v) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+  return v;
+}
+
+template <class T>
+__device__ __forceinline__ int upper_bound_idx(const T* ptr, int n, T x) {
+  // largest s in [0, n) with ptr[s] <= x (ptr non-decreasing, ptr[0] <= x)
+  int lo = 0, hi = n - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (ptr[mid] <= x) lo = mid; else hi = mid - 1;
+  }
+  return lo;
+}
+
+__global__ void k_fill(float* __restrict__ p, int64_t n, float v) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = v;
+}
+
+__global__ void k_copy(float* __restrict__ dst, const float* __restrict__ src, int64_t n) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) dst[i] = src[i];
+}
+
+// ---------------------------------------------------------------------------
+// Geometry (fp64) and basis expansions (Eq. 2, Alg. 2: whole batch at once).
+// ---------------------------------------------------------------------------
+__global__ void k_atom_struct(int N, int S, const int* __restrict__ atom_ptr, int* __restrict__ atom_struct) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < N) atom_struct[i] = upper_bound_idx(atom_ptr, S + 1, i);
+}
+
+__global__ void k_prep_edges(int E, int N, const int* __restrict__ edge_ptr, const int* __restrict__ edge_dst,
+                             const int* __restrict__ edge_img, const int* __restrict__ atom_struct,
+                             const float* __restrict__ pos, const float* __restrict__ lattice, int* __restrict__ edge_src,
+                             float* __restrict__ edge_len, float* __restrict__ edge_xhat) {
+  const int e = blockIdx.x * blockDim.x + threadIdx.x;
+  if (e >= E) return;
+  const int i = upper_bound_idx(edge_ptr, N + 1, e);
+  const int j = edge_dst[e];
+  const float* L = lattice + 9 * atom_struct[i];
+  const double n0 = edge_img[3 * e], n1 = edge_img[3 * e + 1], n2 = edge_img[3 * e + 2];
+  double r[3];
+  for (int c = 0; c < 3; ++c)
+    r[c] = (double)pos[3 * j + c] + (n0 * (double)L[c] + n1 * (double)L[3 + c] + n2 * (double)L[6 + c]) - (double)pos[3 * i + c];
+  const double d = sqrt(r[0] * r[0] + r[1] * r[1] + r[2] * r[2]);
+  edge_src[e] = i;
+  edge_len[e] = (float)d;
+  for (int c = 0; c < 3; ++c) edge_xhat[3 * e + c] = (float)(r[c] / d);
+}
+
+__global__ void k_prep_bonds(int B, const int* __restrict__ bond_edge, const int* __restrict__ edge_src,
+                             int* __restrict__ bond_src) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b < B) bond_src[b] = edge_src[bond_edge[b]];
+}
+
+// sRBF_n(r) = sqrt(2/c) sin(f_n r / c) / r * u(r / c), u the polynomial envelope.
+__device__ __forceinline__ float envelope(float x, int p) {
+  const float a = -0.5f * (p + 1) * (p + 2), b = (float)(p * (p + 2)), c = -0.5f * p * (p + 1);
+  float xp = 1.0f;
+  for (int k = 0; k < p; ++k) xp *= x;
+  return 1.0f + xp * (a + x * (b + x * c));
+}
+
+__global__ void k_rbf(int rows, const int* __restrict__ idx, const float* __restrict__ len, const float* __restrict__ freq,
+                      int R, float cutoff, int p, float* __restrict__ out) {
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= (int64_t)rows * R) return;
+  const int row = (int)(t / R), n = (int)(t % R);
+  const float d = len[idx ? idx[row] : row];
+  const float inv_c = 1.0f / cutoff;
+  out[t] = sqrtf(2.0f * inv_c) * sinf(freq[n] * d * inv_c) / d * envelope(d * inv_c, p);
+}
+
+// Angles: first bond b1 (run of angle_ptr), second bond b2, centre atom;
+// cos/sin of theta from (dot, |cross|) in fp64 and the Fourier basis by the
+// complex-power recurrence (cos m t + i sin m t) = (cos t + i sin t)^m.
+__global__ void k_prep_angles(int A, int B, const int* __restrict__ angle_ptr, const int* __restrict__ bond_ptr,
+                              const int* __restrict__ bond_edge, const int* __restrict__ bond_src,
+                              const int* __restrict__ edge_dst, const int* __restrict__ edge_img,
+                              const int* __restrict__ atom_struct, const float* __restrict__ pos,
+                              const float* __restrict__ lattice, int K, int* __restrict__ ang_b1, int* __restrict__ ang_b2,
+                              int* __restrict__ ang_ctr, float* __restrict__ ft) {
+  const int al = blockIdx.x * blockDim.x + threadIdx.x;
+  if (al >= A) return;
+  const int b1 = upper_bound_idx(angle_ptr, B + 1, al);
+  const int i = bond_src[b1];
+  const int k0 = bond_ptr[i];
+  const int p = b1 - k0;
+  const int q0 = al - angle_ptr[b1];
+  const int b2 = k0 + (q0 < p ? q0 : q0 + 1);
+  ang_b1[al] = b1;
+  ang_b2[al] = b2;
+  ang_ctr[al] = i;
+  const float* L = lattice + 9 * atom_struct[i];
+  double r[2][3];
+  const int es[2] = {bond_edge[b1], bond_edge[b2]};
+  for (int s = 0; s < 2; ++s) {
+    const int e = es[s], j = edge_dst[e];
+    const double n0 = edge_img[3 * e], n1 = edge_img[3 * e + 1], n2 = edge_img[3 * e + 2];
+    for (int c = 0; c < 3; ++c)
+      r[s][c] = (double)pos[3 * j + c] + (n0 * (double)L[c] + n1 * (double)L[3 + c] + n2 * (double)L[6 + c]) - (double)pos[3 * i + c];
+  }
+  const double dot = r[0][0] * r[1][0] + r[0][1] * r[1][1] + r[0][2] * r[1][2];
+  const double cx = r[0][1] * r[1][2] - r[0][2] * r[1][1];
+  const double cy = r[0][2] * r[1][0] - r[0][0] * r[1][2];
+  const double cz = r[0][0] * r[1][1] - r[0][1] * r[1][0];
+  const double cr = sqrt(cx * cx + cy * cy + cz * cz);
+  const double h = sqrt(dot * dot + cr * cr);
+  const double c1 = dot / h, s1 = cr / h;
+  const int M = (K - 1) / 2;
+  float* o = ft + (int64_t)al * K;
+  const double inv_sqrt_pi = 0.56418958354775628695;
+  o[0] = (float)(inv_sqrt_pi * 0.70710678118654752440);
+  double cm = 1.0, sm = 0.0;
+  for (int m = 1; m <= M; ++m) {
+    const double cn = cm * c1 - sm * s1, sn = sm * c1 + cm * s1;
+    cm = cn;
+    sm = sn;
+    o[m] = (float)(cm * inv_sqrt_pi);
+    o[M + m] = (float)(sm * inv_sqrt_pi);
+  }
+}
+
+__global__ void k_embed_v0(int N, int D, const int* __restrict__ Z, const float* __restrict__ WZ, float* __restrict__ v0) {
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= (int64_t)N * D) return;
+  const int i = (int)(t / D), c = (int)(t % D);
+  v0[t] = WZ[(int64_t)(Z[i] - 1) * D + c];
+}
+
+// ---------------------------------------------------------------------------
+// GatedMLP rows: phi = SiLU(LN_c(z_c)) * sigmoid(LN_g(z_g)), one row per wave.
+// ---------------------------------------------------------------------------
+template <int V>
+struct GateRow {
+  float xc[V], xg[V];  // normalised core / gate
+  float yc[V], yg[V];  // after scale and shift
+  float rc, rg;        // 1 / std
+};
+
+template <int V>
+__device__ __forceinline__ void gate_forward(const float* __restrict__ z, const float* __restrict__ gc,
+                                             const float* __restrict__ bc, const float* __restrict__ gg,
+                                             const float* __restrict__ bg, int lane, GateRow<V>& g, float* phi) {
+  constexpr int D = 64 * V;
+  float zc[V], zg[V], sc = 0.f, sg = 0.f;
+#pragma unroll
+  for (int k = 0; k < V; ++k) {
+    zc[k] = z[lane + 64 * k];
+    zg[k] = z[D + lane + 64 * k];
+    sc += zc[k];
+    sg += zg[k];
+  }
+  const float mc = wsum(sc) * (1.0f / D), mg = wsum(sg) * (1.0f / D);
+  float vc = 0.f, vg = 0.f;
+#pragma unroll
+  for (int k = 0; k < V; ++k) {
+    zc[k] -= mc;
+    zg[k] -= mg;
+    vc += zc[k] * zc[k];
+    vg += zg[k] * zg[k];
+  }
+  g.rc = rsqrtf(wsum(vc) * (1.0f / D) + kLnEps);
+  g.rg = rsqrtf(wsum(vg) * (1.0f / D) + kLnEps);
+#pragma unroll
+  for (int k = 0; k < V; ++k) {
+    const int c = lane + 64 * k;
+    g.xc[k] = zc[k] * g.rc;
+    g.xg[k] = zg[k] * g.rg;
+    g.yc[k] = gc[c] * g.xc[k] + bc[c];
+    g.yg[k] = gg[c] * g.xg[k] + bg[c];
+    phi[k] = g.yc[k] * sigm(g.yc[k]) * sigm(g.yg[k]);
+  }
+}
+
+// Backward of one gated row given dphi: writes dz (2D values) and
+// accumulates the LayerNorm parameter partials (dgc, dbc, dgg, dbg).
+template <int V>
+__device__ __forceinline__ void gate_backward(const GateRow<V>& g, const float* dphi, const float* __restrict__ gc,
+                                              const float* __restrict__ gg, int lane, float* __restrict__ dz,
+                                              float (&acc)[4][V]) {
+  constexpr int D = 64 * V;
+  float dxc[V], dxg[V], s1c = 0.f, s2c = 0.f, s1g = 0.f, s2g = 0.f;
+#pragma unroll
+  for (int k = 0; k < V; ++k) {
+    const int c = lane + 64 * k;
+    const float sc = sigm(g.yc[k]), sgt = sigm(g.yg[k]);
+    const float silu_c = g.yc[k] * sc;
+    const float dyc = dphi[k] * sgt * sc * (1.0f + g.yc[k] * (1.0f - sc));
+    const float dyg = dphi[k] * silu_c * sgt * (1.0f - sgt);
+    acc[0][k] += dyc * g.xc[k];
+    acc[1][k] += dyc;
+    acc[2][k] += dyg * g.xg[k];
+    acc[3][k] += dyg;
+    dxc[k] = dyc * gc[c];
+    dxg[k] = dyg * gg[c];
+    s1c += dxc[k];
+    s2c += dxc[k] * g.xc[k];
+    s1g += dxg[k];
+    s2g += dxg[k] * g.xg[k];
+  }
+  s1c = wsum(s1c) * (1.0f / D);
+  s2c = wsum(s2c) * (1.0f / D);
+  s1g = wsum(s1g) * (1.0f / D);
+  s2g = wsum(s2g) * (1.0f / D);
+#pragma unroll
+  for (int k = 0; k < V; ++k) {
+    const int c = lane + 64 * k;
+    dz[c] = g.rc * (dxc[k] - s1c - g.xc[k] * s2c);
+    dz[D + c] = g.rg * (dxg[k] - s1g - g.xg[k] * s2g);
+  }
+}
+
+struct LnPtrs {
+  const float *gc, *bc, *gg, *bg;
+};
+
+// Atom conv messages: msg_e = e^a_e * phi_v(z_e).
+template <int V>
+__global__ void __launch_bounds__(256) k_gate_atom_fwd(int E, const float* __restrict__ zv, const float* __restrict__ ea,
+                                                       LnPtrs ln, float* __restrict__ msg) {
+  constexpr int D = 64 * V;
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (row >= E) return;
+  GateRow<V> g;
+  float phi[V];
+  gate_forward<V>(zv + (int64_t)row * 2 * D, ln.gc, ln.bc, ln.gg, ln.bg, lane, g, phi);
+#pragma unroll
+  for (int k = 0; k < V; ++k) {
+    const int64_t o = (int64_t)row * D + lane + 64 * k;
+    msg[o] = ea[o] * phi[k];
+  }
+}
+
+// Bond conv messages eb_{b2} * phi_e and angle update a' = a + phi_a.
+template <int V>
+__global__ void __launch_bounds__(256) k_gate_angle_fwd(int A, const float* __restrict__ zae, int has_angle,
+                                                        const float* __restrict__ eb, const int* __restrict__ ang_b2,
+                                                        LnPtrs lne, LnPtrs lna, const float* __restrict__ a_in,
+                                                        float* __restrict__ a_out, float* __restrict__ msgb) {
+  constexpr int D = 64 * V;
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (row >= A) return;
+  GateRow<V> g;
+  float phi[V];
+  const float* z = zae + (int64_t)row * 4 * D;
+  gate_forward<V>(z, lne.gc, lne.bc, lne.gg, lne.bg, lane, g, phi);
+  const int64_t b2 = ang_b2[row];
+#pragma unroll
+  for (int k = 0; k < V; ++k) msgb[(int64_t)row * D + lane + 64 * k] = eb[b2 * D + lane + 64 * k] * phi[k];
+  if (has_angle) {
+    gate_forward<V>(z + 2 * D, lna.gc, lna.bc, lna.gg, lna.bg, lane, g, phi);
+#pragma unroll
+    for (int k = 0; k < V; ++k) {
+      const int64_t o = (int64_t)row * D + lane + 64 * k;
+      a_out[o] = a_in[o] + phi[k];
+    }
+  }
+}
+
+// Backward of the atom conv gate: dphi = dm_src * e^a, d e^a += dm_src * phi.
+template <int V>
+__global__ void __launch_bounds__(256) k_gate_atom_bwd(int E, const float* __restrict__ zv, const float* __restrict__ ea,
+                                                       const float* __restrict__ dm, const int* __restrict__ edge_src,
+                                                       LnPtrs ln, float* __restrict__ dzv, float* __restrict__ dea,
+                                                       float* __restrict__ lnpart) {
+  constexpr int D = 64 * V;
+  __shared__ float red[4][4 * D];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  float acc[4][V];
+#pragma unroll
+  for (int a = 0; a < 4; ++a)
+#pragma unroll
+    for (int k = 0; k < V; ++k) acc[a][k] = 0.f;
+  const int r0 = blockIdx.x * kGateRowsPerBlock;
+  for (int rr = wave; rr < kGateRowsPerBlock; rr += 4) {
+    const int row = r0 + rr;
+    if (row >= E) break;
+    GateRow<V> g;
+    float phi[V], dphi[V];
+    gate_forward<V>(zv + (int64_t)row * 2 * D, ln.gc, ln.bc, ln.gg, ln.bg, lane, g, phi);
+    const int64_t src = edge_src[row];
+#pragma unroll
+    for (int k = 0; k < V; ++k) {
+      const int c = lane + 64 * k;
+      const float dmv = dm[src * D + c];
+      const int64_t o = (int64_t)row * D + c;
+      dphi[k] = dmv * ea[o];
+      dea[o] += dmv * phi[k];
+    }
+    gate_backward<V>(g, dphi, ln.gc, ln.gg, lane, dzv + (int64_t)row * 2 * D, acc);
+  }
+#pragma unroll
+  for (int a = 0; a < 4; ++a)
+#pragma unroll
+    for (int k = 0; k < V; ++k) red[wave][a * D + lane + 64 * k] = acc[a][k];
+  __syncthreads();
+  for (int c = threadIdx.x; c < 4 * D; c += 256)
+    lnpart[(int64_t)blockIdx.x * 4 * D + c] = ((red[0][c] + red[1][c]) + red[2][c]) + red[3][c];
+}
+
+// Backward of the angle gates. dphi_e = dmu_b1 * eb_b1 * eb_b2;
+// t2 = dmu_b1 * eb_b1 * phi_e (gradient of eb_b2); dphi_a = da'.
+template <int V>
+__global__ void __launch_bounds__(256) k_gate_angle_bwd(int A, const float* __restrict__ zae, int has_angle,
+                                                        const float* __restrict__ eb, const int* __restrict__ ang_b1,
+                                                        const int* __restrict__ ang_b2, const float* __restrict__ dmu,
+                                                        const float* __restrict__ da_next, LnPtrs lne, LnPtrs lna,
+                                                        float* __restrict__ dzae, float* __restrict__ t2,
+                                                        float* __restrict__ lnpart) {
+  constexpr int D = 64 * V;
+  __shared__ float red[4][4 * D];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  float acc_e[4][V], acc_a[4][V];
+#pragma unroll
+  for (int a = 0; a < 4; ++a)
+#pragma unroll
+    for (int k = 0; k < V; ++k) acc_e[a][k] = acc_a[a][k] = 0.f;
+  const int r0 = blockIdx.x * kGateRowsPerBlock;
+  for (int rr = wave; rr < kGateRowsPerBlock; rr += 4) {
+    const int row = r0 + rr;
+    if (row >= A) break;
+    const float* z = zae + (int64_t)row * 4 * D;
+    float* dz = dzae + (int64_t)row * 4 * D;
+    GateRow<V> g;
+    float phi[V], dphi[V];
+    gate_forward<V>(z, lne.gc, lne.bc, lne.gg, lne.bg, lane, g, phi);
+    const int64_t b1 = ang_b1[row], b2 = ang_b2[row];
+#pragma unroll
+    for (int k = 0; k < V; ++k) {
+      const int c = lane + 64 * k;
+      const float w = dmu[b1 * D + c] * eb[b1 * D + c];
+      dphi[k] = w * eb[b2 * D + c];
+      t2[(int64_t)row * D + c] = w * phi[k];
+    }
+    gate_backward<V>(g, dphi, lne.gc, lne.gg, lane, dz, acc_e);
+    if (has_angle) {
+      gate_forward<V>(z + 2 * D, lna.gc, lna.bc, lna.gg, lna.bg, lane, g, phi);
+#pragma unroll
+      for (int k = 0; k < V; ++k) dphi[k] = da_next[(int64_t)row * D + lane + 64 * k];
+      gate_backward<V>(g, dphi, lna.gc, lna.gg, lane, dz + 2 * D, acc_a);
+    }
+  }
+  for (int half = 0; half < 2; ++half) {
+#pragma unroll
+    for (int a = 0; a < 4; ++a)
+#pragma unroll
+      for (int k = 0; k < V; ++k) red[wave][a * D + lane + 64 * k] = half ? acc_a[a][k] : acc_e[a][k];
+    __syncthreads();
+    for (int c = threadIdx.x; c < 4 * D; c += 256)
+      lnpart[(int64_t)blockIdx.x * 8 * D + half * 4 * D + c] = ((red[0][c] + red[1][c]) + red[2][c]) + red[3][c];
+    __syncthreads();
+  }
+}
+
+// Segmented row sums: out[s] (+)= sum_{r in [ptr[s], ptr[s+1])} vals[idx(r)];
+// optionally out2[s] = mul[s] * sum. One wavefront per segment.
+__global__ void __launch_bounds__(256) k_segsum(int nseg, const int* __restrict__ ptr, const int* __restrict__ idx,
+                                                const float* __restrict__ vals, int ld_in, int width, float* __restrict__ out,
+                                                int ld_out, int accumulate, const float* __restrict__ mul, int ld_mul,
+                                                float* __restrict__ out2, int ld_out2) {
+  const int s = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (s >= nseg) return;
+  const int lo = ptr[s], hi = ptr[s + 1];
+  for (int c = lane; c < width; c += 64) {
+    float acc = 0.f;
+    for (int r = lo; r < hi; ++r) acc += vals[(int64_t)(idx ? idx[r] : r) * ld_in + c];
+    float* o = out + (int64_t)s * ld_out + c;
+    *o = accumulate ? *o + acc : acc;
+    if (out2) out2[(int64_t)s * ld_out2 + c] = mul[(int64_t)s * ld_mul + c] * acc;
+  }
+}
+
+// Per bond b (centre i, local index p among k bonds): DZ1 = sum over angles
+// (b, *) of dz, DZ2 = sum over angles (*, b) of dz, and
+// d eb_b += dmu_b * S_b + sum over angles (*, b) of t2.
+__global__ void __launch_bounds__(256) k_bond_bwd_reduce(int B, int D, int W4, const int* __restrict__ bond_src,
+                                                         const int* __restrict__ bond_ptr, const int* __restrict__ angle_ptr,
+                                                         const float* __restrict__ dzae, const float* __restrict__ t2,
+                                                         const float* __restrict__ dmu, const float* __restrict__ ssum,
+                                                         float* __restrict__ DZ12, float* __restrict__ deb) {
+  const int b = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (b >= B) return;
+  const int i = bond_src[b], k0 = bond_ptr[i], k = bond_ptr[i + 1] - k0, q = b - k0;
+  const int lo = angle_ptr[b], hi = angle_ptr[b + 1];
+  for (int c = lane; c < W4; c += 64) {
+    float s1 = 0.f, s2 = 0.f;
+    for (int r = lo; r < hi; ++r) s1 += dzae[(int64_t)r * 4 * D + c];
+    for (int p = 0; p < k; ++p) {
+      if (p == q) continue;
+      const int64_t al = angle_ptr[k0 + p] + (q < p ? q : q - 1);
+      s2 += dzae[al * 4 * D + c];
+    }
+    DZ12[(int64_t)b * 8 * D + c] = s1;
+    DZ12[(int64_t)b * 8 * D + 4 * D + c] = s2;
+  }
+  for (int c = lane; c < D; c += 64) {
+    float s = 0.f;
+    for (int p = 0; p < k; ++p) {
+      if (p == q) continue;
+      const int64_t al = angle_ptr[k0 + p] + (q < p ? q : q - 1);
+      s += t2[al * D + c];
+    }
+    const int64_t o = (int64_t)b * D + c;
+    deb[o] += dmu[o] * ssum[o] + s;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Heads: per-structure energy and stress, per-atom forces (Eq. 7, 9).
+// ---------------------------------------------------------------------------
+__device__ void lattice_units(const float* Lf, double U[9], double& vol) {
+  double L[9];
+  for (int k = 0; k < 9; ++k) L[k] = (double)Lf[k];
+  vol = fabs(L[0] * (L[4] * L[8] - L[5] * L[7]) - L[1] * (L[3] * L[8] - L[5] * L[6]) + L[2] * (L[3] * L[7] - L[4] * L[6]));
+  for (int a = 0; a < 3; ++a) {
+    const double n = sqrt(L[3 * a] * L[3 * a] + L[3 * a + 1] * L[3 * a + 1] + L[3 * a + 2] * L[3 * a + 2]);
+    for (int c = 0; c < 3; ++c) U[3 * a + c] = L[3 * a + c] / n;
+  }
+}
+
+__global__ void __launch_bounds__(256) k_struct_heads(int S, const int* __restrict__ atom_ptr, const float* __restrict__ lattice,
+                                                      const float* __restrict__ oE, const float* __restrict__ oS,
+                                                      float* __restrict__ energy, float* __restrict__ stress) {
+  const int s = blockIdx.x;
+  __shared__ double red[10][256];
+  double acc[10];
+  for (int k = 0; k < 10; ++k) acc[k] = 0.0;
+  for (int i = atom_ptr[s] + threadIdx.x; i < atom_ptr[s + 1]; i += 256) {
+    acc[0] += oE[i];
+    for (int k = 0; k < 9; ++k) acc[1 + k] += oS[(int64_t)i * 9 + k];
+  }
+  for (int k = 0; k < 10; ++k) red[k][threadIdx.x] = acc[k];
+  __syncthreads();
+  for (int off = 128; off > 0; off >>= 1) {
+    if ((int)threadIdx.x < off)
+      for (int k = 0; k < 10; ++k) red[k][threadIdx.x] += red[k][threadIdx.x + off];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    energy[s] = (float)red[0][0];
+    double U[9], vol;
+    lattice_units(lattice + 9 * s, U, vol);
+    for (int x = 0; x < 3; ++x)
+      for (int y = 0; y < 3; ++y) {
+        double v = 0.0;
+        for (int a = 0; a < 3; ++a)
+          for (int b = 0; b < 3; ++b) v += red[1 + 3 * a + b][0] * U[3 * a + x] * U[3 * b + y];
+        stress[9 * s + 3 * x + y] = (float)(v / vol);
+      }
+  }
+}
+
+// F_i = sum_e n_e xhat_e, n_e = (m_e + m_rev(e)) / 2.
+__global__ void k_forces(int N, const int* __restrict__ edge_ptr, const int* __restrict__ edge_rev, const float* __restrict__ oF,
+                         const float* __restrict__ xhat, float* __restrict__ forces) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= N) return;
+  float f[3] = {0.f, 0.f, 0.f};
+  for (int e = edge_ptr[i]; e < edge_ptr[i + 1]; ++e) {
+    const float n = 0.5f * (oF[e] + oF[edge_rev[e]]);
+    for (int c = 0; c < 3; ++c) f[c] += n * xhat[3 * e + c];
+  }
+  for (int c = 0; c < 3; ++c) forces[3 * i + c] = f[c];
+}
+
+// Loss (weighted MSE, per-atom energy) and its gradient; one block.
+__global__ void __launch_bounds__(256) k_loss(int S, int N, const int* __restrict__ atom_ptr, const float* __restrict__ energy,
+                                              const float* __restrict__ forces, const float* __restrict__ stress,
+                                              const float* __restrict__ Et, const float* __restrict__ Ft,
+                                              const float* __restrict__ St, float w0, float w1, float w2,
+                                              float* __restrict__ loss, float* __restrict__ dE, float* __restrict__ dF,
+                                              float* __restrict__ dS) {
+  __shared__ double red[3][256];
+  double le = 0.0, lf = 0.0, ls = 0.0;
+  for (int s = threadIdx.x; s < S; s += 256) {
+    const double n = (double)(atom_ptr[s + 1] - atom_ptr[s]);
+    const double r = (double)energy[s] / n - (double)Et[s];
+    le += r * r;
+    dE[s] = (float)(w0 * 2.0 * r / n / S);
+  }
+  for (int k = threadIdx.x; k < 3 * N; k += 256) {
+    const double r = (double)forces[k] - (double)Ft[k];
+    lf += r * r;
+    dF[k] = (float)(w1 * 2.0 * r / (3.0 * N));
+  }
+  for (int k = threadIdx.x; k < 9 * S; k += 256) {
+    const double r = (double)stress[k] - (double)St[k];
+    ls += r * r;
+    dS[k] = (float)(w2 * 2.0 * r / (9.0 * S));
+  }
+  red[0][threadIdx.x] = le;
+  red[1][threadIdx.x] = lf;
+  red[2][threadIdx.x] = ls;
+  __syncthreads();
+  for (int off = 128; off > 0; off >>= 1) {
+    if ((int)threadIdx.x < off)
+      for (int k = 0; k < 3; ++k) red[k][threadIdx.x] += red[k][threadIdx.x + off];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0)
+    loss[0] = (float)(w0 * red[0][0] / S + w1 * red[1][0] / (3.0 * N) + w2 * red[2][0] / (9.0 * S));
+}
+
+// Upstream gradients of the head outputs.
+__global__ void k_seed_atoms(int N, const int* __restrict__ atom_struct, const float* __restrict__ lattice,
+                             const float* __restrict__ dE, const float* __restrict__ dS, float* __restrict__ doE,
+                             float* __restrict__ doS) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= N) return;
+  const int s = atom_struct[i];
+  doE[i] = dE[s];
+  double U[9], vol;
+  lattice_units(lattice + 9 * s, U, vol);
+  for (int a = 0; a < 3; ++a)
+    for (int b = 0; b < 3; ++b) {
+      double v = 0.0;
+      for (int x = 0; x < 3; ++x)
+        for (int y = 0; y < 3; ++y) v += (double)dS[9 * s + 3 * x + y] * U[3 * a + x] * U[3 * b + y];
+      doS[(int64_t)i * 9 + 3 * a + b] = (float)(v / vol);
+    }
+}
+
+__global__ void k_seed_edges(int E, const int* __restrict__ edge_src, const float* __restrict__ dF,
+                             const float* __restrict__ xhat, float* __restrict__ dn) {
+  const int e = blockIdx.x * blockDim.x + threadIdx.x;
+  if (e >= E) return;
+  const int i = edge_src[e];
+  dn[e] = dF[3 * i] * xhat[3 * e] + dF[3 * i + 1] * xhat[3 * e + 1] + dF[3 * i + 2] * xhat[3 * e + 2];
+}
+
+__global__ void k_seed_edges2(int E, const int* __restrict__ edge_rev, const float* __restrict__ dn, float* __restrict__ doF) {
+  const int e = blockIdx.x * blockDim.x + threadIdx.x;
+  if (e < E) doF[e] = 0.5f * (dn[e] + dn[edge_rev[e]]);
+}
+
+// dW_Z[z] = sum over atoms with Z_i = z+1 of dv0_i (ordered by atom index).
+__global__ void k_embed_bwd_Z(int N, int D, const int* __restrict__ Z, const float* __restrict__ dv0, float* __restrict__ gWZ) {
+  const int z = blockIdx.x + 1;
+  for (int c = threadIdx.x; c < D; c += blockDim.x) {
+    float acc = 0.f;
+    for (int i = 0; i < N; ++i)
+      if (Z[i] == z) acc += dv0[(int64_t)i * D + c];
+    gWZ[(int64_t)(z - 1) * D + c] += acc;
+  }
+}
+
+// Partial sums over rows of d sRBF_n * d sRBF_n / d f_n.
+__global__ void __launch_bounds__(256) k_rbf_fgrad(int rows, const int* __restrict__ idx, const float* __restrict__ len,
+                                                   const float* __restrict__ freq, int R, float cutoff, int p,
+                                                   const float* __restrict__ drbf, float* __restrict__ part) {
+  __shared__ float red[4][64];
+  const int n = threadIdx.x & 63, sub = threadIdx.x >> 6;
+  float acc = 0.f;
+  if (n < R) {
+    const float inv_c = 1.0f / cutoff, pre = sqrtf(2.0f * inv_c) * inv_c, f = freq[n];
+    const int r0 = blockIdx.x * kFreqRowsPerBlock;
+    for (int rr = sub; rr < kFreqRowsPerBlock; rr += 4) {
+      const int row = r0 + rr;
+      if (row >= rows) break;
+      const float d = len[idx ? idx[row] : row];
+      acc += drbf[(int64_t)row * R + n] * pre * cosf(f * d * inv_c) * envelope(d * inv_c, p);
+    }
+  }
+  red[sub][n] = acc;
+  __syncthreads();
+  if (threadIdx.x < 64 && (int)threadIdx.x < R)
+    part[(int64_t)blockIdx.x * R + threadIdx.x] = ((red[0][threadIdx.x] + red[1][threadIdx.x]) + red[2][threadIdx.x]) + red[3][threadIdx.x];
+}
+
+__global__ void k_adam(int64_t P, float* __restrict__ params, const float* __restrict__ grad, float* __restrict__ m,
+                       float* __restrict__ v, float lr, float b1, float b2, float eps, float c1, float c2) {
+  const int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (k >= P) return;
+  const float g = grad[k];
+  const float mk = b1 * m[k] + (1.0f - b1) * g;
+  const float vk = b2 * v[k] + (1.0f - b2) * g * g;
+  m[k] = mk;
+  v[k] = vk;
+  params[k] -= lr * (mk / c1) / (sqrtf(vk / c2) + eps);
+}
+
+// ---------------------------------------------------------------------------
+// Workspace carving.
+// ---------------------------------------------------------------------------
+struct Dims {
+  int64_t N, S, E, B, A;
+  int D, T, R, K;
+};
+
+struct Acts {
+  int *atom_struct, *edge_src, *bond_src, *ang_b1, *ang_b2, *ang_ctr;
+  float *edge_len, *edge_xhat, *rbf_a, *rbf_b, *ft, *ea, *eb;
+  float* v[kMaxLayers + 1];
+  float* e[kMaxLayers + 1];
+  float* a[kMaxLayers];
+  float *zv[kMaxLayers], *zae[kMaxLayers], *m[kMaxLayers], *ssum[kMaxLayers], *mu[kMaxLayers];
+  float *msg, *msgb, *Xa, *Xb;
+  float *hE1, *aE1, *hE2, *aE2, *hS1, *aS1, *hS2, *aS2, *hF1, *aF1, *hF2, *aF2, *oE, *oS, *oF;
+  // backward
+  float *dv[2], *de[2], *da[2], *dm, *dmu, *dzv, *dzae, *t2, *AT, *DZ12, *dea, *deb;
+  float *doE, *doS, *dn, *doF, *dh2E, *dh2S, *dh2F, *dh1ES, *dh1F, *drbf_a, *drbf_b;
+  float *lnpart, *tnpart, *fpart;
+  int64_t tnpart_cap;
+  // loss
+  float *dE, *dF, *dS, *out_E, *out_F, *out_S;
+};
+
+void carve_acts(Arena& ar, const Dims& m, Acts& a) {
+  const int64_t N = m.N, S = m.S, E = m.E, B = m.B, A = m.A, D = m.D, R = m.R, K = m.K;
+  a.atom_struct = ar.take<int>(N);
+  a.edge_src = ar.take<int>(E);
+  a.bond_src = ar.take<int>(B);
+  a.ang_b1 = ar.take<int>(A);
+  a.ang_b2 = ar.take<int>(A);
+  a.ang_ctr = ar.take<int>(A);
+  a.edge_len = ar.take<float>(E);
+  a.edge_xhat = ar.take<float>(3 * E);
+  a.rbf_a = ar.take<float>(E * R);
+  a.rbf_b = ar.take<float>(B * R);
+  a.ft = ar.take<float>(A * K);
+  a.ea = ar.take<float>(E * D);
+  a.eb = ar.take<float>(B * D);
+  for (int t = 0; t <= m.T; ++t) {
+    a.v[t] = ar.take<float>(N * D);
+    a.e[t] = ar.take<float>(E * D);
+  }
+  for (int t = 0; t < m.T; ++t) {
+    a.a[t] = ar.take<float>(A * D);
+    a.zv[t] = ar.take<float>(E * 2 * D);
+    a.zae[t] = ar.take<float>(A * 4 * D);
+    a.m[t] = ar.take<float>(N * D);
+    a.ssum[t] = ar.take<float>(B * D);
+    a.mu[t] = ar.take<float>(B * D);
+  }
+  a.msg = ar.take<float>(E * D);
+  a.msgb = ar.take<float>(A * D);
+  a.Xa = ar.take<float>(N * 8 * D);
+  a.Xb = ar.take<float>(B * 8 * D);
+  float** atom_heads[] = {&a.hE1, &a.aE1, &a.hE2, &a.aE2, &a.hS1, &a.aS1, &a.hS2, &a.aS2};
+  for (auto p : atom_heads) *p = ar.take<float>(N * D);
+  float** edge_heads[] = {&a.hF1, &a.aF1, &a.hF2, &a.aF2};
+  for (auto p : edge_heads) *p = ar.take<float>(E * D);
+  a.oE = ar.take<float>(N);
+  a.oS = ar.take<float>(N * 9);
+  a.oF = ar.take<float>(E);
+  for (int k = 0; k < 2; ++k) {
+    a.dv[k] = ar.take<float>(N * D);
+    a.de[k] = ar.take<float>(E * D);
+    a.da[k] = ar.take<float>(A * D);
+  }
+  a.dm = ar.take<float>(N * D);
+  a.dmu = ar.take<float>(B * D);
+  a.dzv = ar.take<float>(E * 2 * D);
+  a.dzae = ar.take<float>(A * 4 * D);
+  a.t2 = ar.take<float>(A * D);
+  a.AT = ar.take<float>(N * 8 * D);
+  a.DZ12 = ar.take<float>(B * 8 * D);
+  a.dea = ar.take<float>(E * D);
+  a.deb = ar.take<float>(B * D);
+  a.doE = ar.take<float>(N);
+  a.doS = ar.take<float>(N * 9);
+  a.dn = ar.take<float>(E);
+  a.doF = ar.take<float>(E);
+  a.dh2E = ar.take<float>(N * D);
+  a.dh2S = ar.take<float>(N * D);
+  a.dh2F = ar.take<float>(E * D);
+  a.dh1ES = ar.take<float>(N * 2 * D);
+  a.dh1F = ar.take<float>(E * D);
+  a.drbf_a = ar.take<float>(E * R);
+  a.drbf_b = ar.take<float>(B * R);
+  const int64_t gate_blocks = cdiv(std::max<int64_t>(std::max(E, A), 1), kGateRowsPerBlock);
+  a.lnpart = ar.take<float>(gate_blocks * 8 * D);
+  a.tnpart_cap = kTnPartFloats;
+  a.tnpart = ar.take<float>(a.tnpart_cap);
+  a.fpart = ar.take<float>(cdiv(std::max(E, (int64_t)1), kFreqRowsPerBlock) * R);
+  a.dE = ar.take<float>(S);
+  a.dF = ar.take<float>(3 * N);
+  a.dS = ar.take<float>(9 * S);
+  a.out_E = ar.take<float>(S);
+  a.out_F = ar.take<float>(3 * N);
+  a.out_S = ar.take<float>(9 * S);
+}
+
+// ---------------------------------------------------------------------------
+// Host-side helpers for building GEMM problem lists.
+// ---------------------------------------------------------------------------
+GemmProblem gp(int64_t M, int64_t Nc, float* C, int ldc) {
+  GemmProblem p{};
+  p.M = (int)M;
+  p.N = (int)Nc;
+  p.C = C;
+  p.ldc = ldc;
+  return p;
+}
+void seg(GemmProblem& p, const float* A, int lda, int a_col, int K, const float* B, int ldb, int trans) {
+  GemmSeg& s = p.seg[p.nseg++];
+  s.A = A;
+  s.lda = lda;
+  s.a_col = a_col;
+  s.K = K;
+  s.B = B;
+  s.ldb = ldb;
+  s.trans = trans;
+}
+void addend(GemmProblem& p, const float* X, int ld, const int* rows) {
+  p.add[p.nadd] = X;
+  p.add_ld[p.nadd] = ld;
+  p.add_rows[p.nadd] = rows;
+  p.nadd++;
+}
+
+int run_gemms(const std::vector<GemmProblem>& ps, hipStream_t st) {
+  GemmBatch b{};
+  for (const auto& p : ps) {
+    if (p.M <= 0 || p.N <= 0) continue;
+    b.p[b.n++] = p;
+    if (b.n == kMaxGemmProblems) {
+      CHG_TRY(gemm_launch(b, st));
+      b.n = 0;
+    }
+  }
+  if (b.n) CHG_TRY(gemm_launch(b, st));
+  return CHGNET_OK;
+}
+
+TnProblem tp(int64_t R, int M, int Nn, const float* X, int ldx, int x_col, const int* x_rows, const float* Y, int ldy,
+             int y_col, const int* y_rows, float* out, int ld_out) {
+  TnProblem p{};
+  p.R = (int)R;
+  p.M = M;
+  p.N = Nn;
+  p.X = X;
+  p.ldx = ldx;
+  p.x_col = x_col;
+  p.x_rows = x_rows;
+  p.Y = Y;
+  p.ldy = ldy;
+  p.y_col = y_col;
+  p.y_rows = y_rows;
+  p.out = out;
+  p.ld_out = ld_out;
+  return p;
+}
+
+int run_tns(const std::vector<TnProblem>& ps, const Acts& a, hipStream_t st) {
+  TnBatch b{};
+  for (const auto& p : ps) {
+    b.p[b.n++] = p;
+    if (b.n == kMaxTnProblems) {
+      CHG_TRY(tn_launch(b, a.tnpart, a.tnpart_cap, st));
+      b.n = 0;
+    }
+  }
+  if (b.n) CHG_TRY(tn_launch(b, a.tnpart, a.tnpart_cap, st));
+  return CHGNET_OK;
+}
+
+int fill(float* p, int64_t n, float v, hipStream_t st) {
+  if (n <= 0) return CHGNET_OK;
+  k_fill<<<(unsigned)cdiv(n, 256), 256, 0, st>>>(p, n, v);
+  CHG_LAUNCHED("k_fill");
+  return CHGNET_OK;
+}
+
+int segsum(int64_t nseg, const int* ptr, const int* idx, const float* vals, int ld_in, int width, float* out, int ld_out,
+           int accumulate, const float* mul, int ld_mul, float* out2, int ld_out2, hipStream_t st) {
+  if (nseg <= 0) return CHGNET_OK;
+  k_segsum<<<(unsigned)cdiv(nseg, 4), 256, 0, st>>>((int)nseg, ptr, idx, vals, ld_in, width, out, ld_out, accumulate, mul,
+                                                    ld_mul, out2, ld_out2);
+  CHG_LAUNCHED("k_segsum");
+  return CHGNET_OK;
+}
+
+LnPtrs ln_ptrs(const float* P, const GatedOffsets& g) { return LnPtrs{P + g.g_c, P + g.b_c, P + g.g_g, P + g.b_g}; }
+
+struct Ctx {
+  const chgnet_hparams* hp;
+  const chgnet_batch* batch;
+  const chgnet_graph* graph;
+  Dims dm;
+  ParamLayout L;
+  Acts a;
+};
+
+int make_ctx(const chgnet_hparams* hp, const chgnet_batch* batch, const chgnet_graph* graph, void* ws, size_t ws_bytes,
+             Ctx& c) {
+  CHG_TRY(validate_hparams(hp));
+  CHG_TRY(validate_batch(batch));
+  if (!graph) return fail(CHGNET_EINVAL, "graph is NULL");
+  if (graph->n_edges < 0 || graph->n_bonds < 0 || graph->n_angles < 0 || graph->n_bonds > graph->n_edges)
+    return fail(CHGNET_EINVAL, "graph sizes are invalid");
+  if (!graph->edge_ptr || !graph->bond_ptr || !graph->angle_ptr ||
+      (graph->n_edges > 0 && (!graph->edge_dst || !graph->edge_img || !graph->edge_rev)) ||
+      (graph->n_bonds > 0 && !graph->bond_edge))
+    return fail(CHGNET_EINVAL, "graph arrays missing");
+  c.hp = hp;
+  c.batch = batch;
+  c.graph = graph;
+  c.dm = Dims{batch->n_atoms, batch->n_struct, graph->n_edges, graph->n_bonds, graph->n_angles,
+              hp->d, hp->n_layers, hp->n_rbf, hp->n_fourier};
+  c.L = make_layout(*hp);
+  Arena ar{static_cast<char*>(ws), ws_bytes, 0};
+  ar.used = graph_scratch_bytes(c.dm.N, c.dm.S);
+  carve_acts(ar, c.dm, c.a);
+  if (!ws || !ar.ok()) return fail(CHGNET_EWORKSPACE, "workspace too small (query chgnet_workspace_size)");
+  return CHGNET_OK;
+}
+
+#define LAUNCH_V(kern, V, grid, block, st, ...)                                  \
+  do {                                                                           \
+    if ((V) == 1) kern<1><<<(grid), (block), 0, (st)>>>(__VA_ARGS__);            \
+    else kern<2><<<(grid), (block), 0, (st)>>>(__VA_ARGS__);                     \
+    CHG_LAUNCHED(#kern);                                                         \
+  } while (0)
+
+// ---------------------------------------------------------------------------
+// Forward.
+// ---------------------------------------------------------------------------
+int forward_impl(Ctx& c, const float* P, float* energy, float* forces, float* stress, hipStream_t st) {
+  const Dims& m = c.dm;
+  Acts& a = c.a;
+  const ParamLayout& L = c.L;
+  const chgnet_graph& g = *c.graph;
+  const chgnet_batch& bt = *c.batch;
+  const int D = m.D, V = D / 64;
+  const int64_t N = m.N, S = m.S, E = m.E, B = m.B, A = m.A;
+
+  // geometry and bases
+  k_atom_struct<<<(unsigned)cdiv(N, 256), 256, 0, st>>>((int)N, (int)S, bt.atom_ptr, a.atom_struct);
+  CHG_LAUNCHED("k_atom_struct");
+  if (E > 0) {
+    k_prep_edges<<<(unsigned)cdiv(E, 256), 256, 0, st>>>((int)E, (int)N, g.edge_ptr, g.edge_dst, g.edge_img, a.atom_struct,
+                                                         bt.pos, bt.lattice, a.edge_src, a.edge_len, a.edge_xhat);
+    CHG_LAUNCHED("k_prep_edges");
+    k_rbf<<<(unsigned)cdiv(E * m.R, 256), 256, 0, st>>>((int)E, nullptr, a.edge_len, P + L.f_a, m.R, c.hp->r_atom,
+                                                        c.hp->envelope_p, a.rbf_a);
+    CHG_LAUNCHED("k_rbf");
+  }
+  if (B > 0) {
+    k_prep_bonds<<<(unsigned)cdiv(B, 256), 256, 0, st>>>((int)B, g.bond_edge, a.edge_src, a.bond_src);
+    CHG_LAUNCHED("k_prep_bonds");
+    k_rbf<<<(unsigned)cdiv(B * m.R, 256), 256, 0, st>>>((int)B, g.bond_edge, a.edge_len, P + L.f_b, m.R, c.hp->r_bond,
+                                                        c.hp->envelope_p, a.rbf_b);
+    CHG_LAUNCHED("k_rbf");
+  }
+  if (A > 0) {
+    k_prep_angles<<<(unsigned)cdiv(A, 256), 256, 0, st>>>((int)A, (int)B, g.angle_ptr, g.bond_ptr, g.bond_edge, a.bond_src,
+                                                          g.edge_dst, g.edge_img, a.atom_struct, bt.pos, bt.lattice, m.K,
+                                                          a.ang_b1, a.ang_b2, a.ang_ctr, a.ft);
+    CHG_LAUNCHED("k_prep_angles");
+  }
+  // embeddings (Eq. 2)
+  k_embed_v0<<<(unsigned)cdiv(N * D, 256), 256, 0, st>>>((int)N, D, bt.Z, P + L.W_Z, a.v[0]);
+  CHG_LAUNCHED("k_embed_v0");
+  {
+    std::vector<GemmProblem> ps;
+    GemmProblem p = gp(E, D, a.e[0], D);
+    seg(p, a.rbf_a, m.R, 0, m.R, P + L.W_e, 2 * D, 0);
+    p.bias = P + L.b_e0;
+    ps.push_back(p);
+    p = gp(E, D, a.ea, D);
+    seg(p, a.rbf_a, m.R, 0, m.R, P + L.W_e + D, 2 * D, 0);
+    ps.push_back(p);
+    p = gp(B, D, a.eb, D);
+    seg(p, a.rbf_b, m.R, 0, m.R, P + L.W_eb, D, 0);
+    ps.push_back(p);
+    p = gp(A, D, a.a[0], D);
+    seg(p, a.ft, m.K, 0, m.K, P + L.W_th, D, 0);
+    p.bias = P + L.b_th;
+    ps.push_back(p);
+    CHG_TRY(run_gemms(ps, st));
+  }
+
+  for (int t = 0; t < m.T; ++t) {
+    const LayerOffsets& lo = L.layer[t];
+    const bool ang = lo.has_angle;
+    const float* Wav = P + lo.av.W;
+    const float* Wbe = P + lo.be.W;
+    const float* Wan = P + lo.an.W;
+    // atom and bond terms of the split first linear layers
+    std::vector<GemmProblem> ps;
+    for (int k = 0; k < 4; ++k) {
+      if (k == 3 && !ang) break;
+      const float* W = k == 0 ? Wav : k == 1 ? Wav + D * 2 * D : k == 2 ? Wbe : Wan;
+      GemmProblem p = gp(N, 2 * D, a.Xa + k * 2 * D, 8 * D);
+      seg(p, a.v[t], D, 0, D, W, 2 * D, 0);
+      ps.push_back(p);
+    }
+    for (int k = 0; k < 4; ++k) {
+      if ((k & 1) && !ang) continue;
+      // k: 0 bond-conv role b1, 1 angle role b1, 2 bond-conv role b2, 3 angle role b2
+      const float* W = (k & 1 ? Wan : Wbe) + (k < 2 ? 1 : 2) * D * 2 * D;
+      GemmProblem p = gp(B, 2 * D, a.Xb + k * 2 * D, 8 * D);
+      p.a_rows = g.bond_edge;
+      seg(p, a.e[t], D, 0, D, W, 2 * D, 0);
+      ps.push_back(p);
+    }
+    CHG_TRY(run_gemms(ps, st));
+    ps.clear();
+    // edge term + gathered atom terms -> atom conv pre-activation
+    {
+      GemmProblem p = gp(E, 2 * D, a.zv[t], 2 * D);
+      seg(p, a.e[t], D, 0, D, Wav + 2 * D * 2 * D, 2 * D, 0);
+      p.bias = P + lo.av.b;
+      addend(p, a.Xa, 8 * D, a.edge_src);
+      addend(p, a.Xa + 2 * D, 8 * D, g.edge_dst);
+      ps.push_back(p);
+      for (int k = 0; k < (ang ? 2 : 1); ++k) {
+        const float* W = (k ? Wan : Wbe) + 3 * D * 2 * D;
+        GemmProblem q = gp(A, 2 * D, a.zae[t] + k * 2 * D, 4 * D);
+        seg(q, a.a[t], D, 0, D, W, 2 * D, 0);
+        q.bias = P + (k ? lo.an.b : lo.be.b);
+        addend(q, a.Xa + (4 + 2 * k) * D, 8 * D, a.ang_ctr);
+        addend(q, a.Xb + k * 2 * D, 8 * D, a.ang_b1);
+        addend(q, a.Xb + (4 + 2 * k) * D, 8 * D, a.ang_b2);
+        ps.push_back(q);
+      }
+      CHG_TRY(run_gemms(ps, st));
+      ps.clear();
+    }
+    // gates and aggregations
+    if (E > 0) LAUNCH_V(k_gate_atom_fwd, V, (unsigned)cdiv(E, 4), 256, st, (int)E, a.zv[t], a.ea, ln_ptrs(P, lo.av), a.msg);
+    CHG_TRY(segsum(N, g.edge_ptr, nullptr, a.msg, D, D, a.m[t], D, 0, nullptr, 0, nullptr, 0, st));
+    if (A > 0)
+      LAUNCH_V(k_gate_angle_fwd, V, (unsigned)cdiv(A, 4), 256, st, (int)A, a.zae[t], ang ? 1 : 0, a.eb, a.ang_b2,
+               ln_ptrs(P, lo.be), ln_ptrs(P, ang ? lo.an : lo.be), a.a[t], ang ? a.a[t + 1] : a.a[t], a.msgb);
+    CHG_TRY(segsum(B, g.angle_ptr, nullptr, a.msgb, D, D, a.ssum[t], D, 0, a.eb, D, a.mu[t], D, st));
+    // updates: v' = v + m Wo + bo; e' = e (+ mu Wo + bo on bonds)
+    if (E > 0) {
+      k_copy<<<(unsigned)cdiv(E * D, 256), 256, 0, st>>>(a.e[t + 1], a.e[t], E * D);
+      CHG_LAUNCHED("k_copy");
+    }
+    {
+      GemmProblem p = gp(N, D, a.v[t + 1], D);
+      seg(p, a.m[t], D, 0, D, P + lo.av_Wo, D, 0);
+      p.bias = P + lo.av_bo;
+      p.res = a.v[t];
+      p.res_ld = D;
+      ps.push_back(p);
+      p = gp(B, D, a.e[t + 1], D);
+      seg(p, a.mu[t], D, 0, D, P + lo.be_Wo, D, 0);
+      p.bias = P + lo.be_bo;
+      p.res = a.e[t];
+      p.res_ld = D;
+      p.res_rows = g.bond_edge;
+      p.c_rows = g.bond_edge;
+      ps.push_back(p);
+      CHG_TRY(run_gemms(ps, st));
+    }
+  }
+
+  // heads: MLP d -> d -> d -> out with SiLU
+  {
+    const HeadOffsets &hE = L.head[0], &hF = L.head[1], &hS = L.head[2];
+    const float* vT = a.v[m.T];
+    const float* eT = a.e[m.T];
+    std::vector<GemmProblem> ps;
+    struct Lay { const float* in; int64_t M; const HeadOffsets* h; float *h1, *a1, *h2, *a2, *o; };
+    Lay ls[3] = {{vT, N, &hE, a.hE1, a.aE1, a.hE2, a.aE2, a.oE},
+                 {vT, N, &hS, a.hS1, a.aS1, a.hS2, a.aS2, a.oS},
+                 {eT, E, &hF, a.hF1, a.aF1, a.hF2, a.aF2, a.oF}};
+    for (auto& l : ls) {
+      GemmProblem p = gp(l.M, D, l.h1, D);
+      seg(p, l.in, D, 0, D, P + l.h->W1, D, 0);
+      p.bias = P + l.h->b1;
+      p.act = ACT_SILU_OUT;
+      p.C2 = l.a1;
+      p.ldc2 = D;
+      ps.push_back(p);
+    }
+    CHG_TRY(run_gemms(ps, st));
+    ps.clear();
+    for (auto& l : ls) {
+      GemmProblem p = gp(l.M, D, l.h2, D);
+      seg(p, l.a1, D, 0, D, P + l.h->W2, D, 0);
+      p.bias = P + l.h->b2;
+      p.act = ACT_SILU_OUT;
+      p.C2 = l.a2;
+      p.ldc2 = D;
+      ps.push_back(p);
+    }
+    CHG_TRY(run_gemms(ps, st));
+    ps.clear();
+    for (auto& l : ls) {
+      GemmProblem p = gp(l.M, l.h->out, l.o, l.h->out);
+      seg(p, l.a2, D, 0, D, P + l.h->W3, l.h->out, 0);
+      p.bias = P + l.h->b3;
+      ps.push_back(p);
+    }
+    CHG_TRY(run_gemms(ps, st));
+  }
+  k_struct_heads<<<(unsigned)S, 256, 0, st>>>((int)S, bt.atom_ptr, bt.lattice, a.oE, a.oS, energy, stress);
+  CHG_LAUNCHED("k_struct_heads");
+  k_forces<<<(unsigned)cdiv(N, 256), 256, 0, st>>>((int)N, g.edge_ptr, g.edge_rev, a.oF, a.edge_xhat, forces);
+  CHG_LAUNCHED("k_forces");
+  return CHGNET_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Backward (weights only).
+// ---------------------------------------------------------------------------
+int backward_impl(Ctx& c, const float* P, const float* dE, const float* dF, const float* dS, float* G, hipStream_t st) {
+  const Dims& m = c.dm;
+  Acts& a = c.a;
+  const ParamLayout& L = c.L;
+  const chgnet_graph& g = *c.graph;
+  const chgnet_batch& bt = *c.batch;
+  const int D = m.D, V = D / 64;
+  const int64_t N = m.N, E = m.E, B = m.B, A = m.A;
+
+  CHG_TRY(fill(G, L.total, 0.f, st));
+  CHG_TRY(fill(a.dea, E * D, 0.f, st));
+  CHG_TRY(fill(a.deb, B * D, 0.f, st));
+
+  // heads
+  k_seed_atoms<<<(unsigned)cdiv(N, 256), 256, 0, st>>>((int)N, a.atom_struct, bt.lattice, dE, dS, a.doE, a.doS);
+  CHG_LAUNCHED("k_seed_atoms");
+  if (E > 0) {
+    k_seed_edges<<<(unsigned)cdiv(E, 256), 256, 0, st>>>((int)E, a.edge_src, dF, a.edge_xhat, a.dn);
+    CHG_LAUNCHED("k_seed_edges");
+    k_seed_edges2<<<(unsigned)cdiv(E, 256), 256, 0, st>>>((int)E, g.edge_rev, a.dn, a.doF);
+    CHG_LAUNCHED("k_seed_edges2");
+  }
+  int cur = 0;
+  {
+    const HeadOffsets &hE = L.head[0], &hF = L.head[1], &hS = L.head[2];
+    struct Lay {
+      const float* in;
+      int64_t M;
+      const HeadOffsets* h;
+      const float *h1, *a1, *h2, *a2, *dout;
+      float *dh2, *dh1base;
+      int dh1col, ld1;
+    };
+    Lay ls[3] = {{a.v[m.T], N, &hE, a.hE1, a.aE1, a.hE2, a.aE2, a.doE, a.dh2E, a.dh1ES, 0, 2 * D},
+                 {a.v[m.T], N, &hS, a.hS1, a.aS1, a.hS2, a.aS2, a.doS, a.dh2S, a.dh1ES, D, 2 * D},
+                 {a.e[m.T], E, &hF, a.hF1, a.aF1, a.hF2, a.aF2, a.doF, a.dh2F, a.dh1F, 0, D}};
+    std::vector<GemmProblem> ps;
+    for (auto& l : ls) {
+      GemmProblem p = gp(l.M, D, l.dh2, D);
+      seg(p, l.dout, l.h->out, 0, l.h->out, P + l.h->W3, l.h->out, 1);
+      p.act = ACT_DSILU_MUL;
+      p.mul = l.h2;
+      p.mul_ld = D;
+      ps.push_back(p);
+    }
+    CHG_TRY(run_gemms(ps, st));
+    ps.clear();
+    for (auto& l : ls) {
+      GemmProblem p = gp(l.M, D, l.dh1base + l.dh1col, l.ld1);
+      seg(p, l.dh2, D, 0, D, P + l.h->W2, D, 1);
+      p.act = ACT_DSILU_MUL;
+      p.mul = l.h1;
+      p.mul_ld = D;
+      ps.push_back(p);
+    }
+    CHG_TRY(run_gemms(ps, st));
+    ps.clear();
+    {
+      GemmProblem p = gp(N, D, a.dv[cur], D);
+      seg(p, a.dh1ES, 2 * D, 0, D, P + hE.W1, D, 1);
+      seg(p, a.dh1ES, 2 * D, D, D, P + hS.W1, D, 1);
+      ps.push_back(p);
+      p = gp(E, D, a.de[cur], D);
+      seg(p, a.dh1F, D, 0, D, P + hF.W1, D, 1);
+      ps.push_back(p);
+      CHG_TRY(run_gemms(ps, st));
+    }
+    std::vector<TnProblem> ts;
+    for (auto& l : ls) {
+      const int o = l.h->out;
+      const float* dh1_base = l.dh1base;
+      const int dh1_col = l.dh1col;
+      ts.push_back(tp(l.M, D, o, l.a2, D, 0, nullptr, l.dout, o, 0, nullptr, G + l.h->W3, o));
+      ts.push_back(tp(l.M, 1, o, nullptr, 0, 0, nullptr, l.dout, o, 0, nullptr, G + l.h->b3, o));
+      ts.push_back(tp(l.M, D, D, l.a1, D, 0, nullptr, l.dh2, D, 0, nullptr, G + l.h->W2, D));
+      ts.push_back(tp(l.M, 1, D, nullptr, 0, 0, nullptr, l.dh2, D, 0, nullptr, G + l.h->b2, D));
+      ts.push_back(tp(l.M, D, D, l.in, D, 0, nullptr, dh1_base, l.ld1, dh1_col, nullptr, G + l.h->W1, D));
+      ts.push_back(tp(l.M, 1, D, nullptr, 0, 0, nullptr, dh1_base, l.ld1, dh1_col, nullptr, G + l.h->b1, D));
+    }
+    CHG_TRY(run_tns(ts, a, st));
+  }
+
+  // interaction blocks in reverse
+  for (int t = m.T - 1; t >= 0; --t) {
+    const LayerOffsets& lo = L.layer[t];
+    const bool ang = lo.has_angle;
+    const int W4 = ang ? 4 * D : 2 * D;
+    const float* Wav = P + lo.av.W;
+    const float* Wbe = P + lo.be.W;
+    const float* Wan = P + lo.an.W;
+    const int nx = 1 - cur;
+    std::vector<GemmProblem> ps;
+    std::vector<TnProblem> ts;
+    // output linears of the atom and bond updates
+    {
+      GemmProblem p = gp(N, D, a.dm, D);
+      seg(p, a.dv[cur], D, 0, D, P + lo.av_Wo, D, 1);
+      ps.push_back(p);
+      p = gp(B, D, a.dmu, D);
+      p.a_rows = g.bond_edge;
+      seg(p, a.de[cur], D, 0, D, P + lo.be_Wo, D, 1);
+      ps.push_back(p);
+      CHG_TRY(run_gemms(ps, st));
+      ps.clear();
+      ts.push_back(tp(N, D, D, a.m[t], D, 0, nullptr, a.dv[cur], D, 0, nullptr, G + lo.av_Wo, D));
+      ts.push_back(tp(N, 1, D, nullptr, 0, 0, nullptr, a.dv[cur], D, 0, nullptr, G + lo.av_bo, D));
+      ts.push_back(tp(B, D, D, a.mu[t], D, 0, nullptr, a.de[cur], D, 0, g.bond_edge, G + lo.be_Wo, D));
+      ts.push_back(tp(B, 1, D, nullptr, 0, 0, nullptr, a.de[cur], D, 0, g.bond_edge, G + lo.be_bo, D));
+      CHG_TRY(run_tns(ts, a, st));
+      ts.clear();
+    }
+    // angle gates
+    const int64_t ablocks = cdiv(A, kGateRowsPerBlock);
+    if (A > 0) {
+      LAUNCH_V(k_gate_angle_bwd, V, (unsigned)ablocks, 256, st, (int)A, a.zae[t], ang ? 1 : 0, a.eb, a.ang_b1, a.ang_b2,
+               a.dmu, a.da[cur], ln_ptrs(P, lo.be), ln_ptrs(P, ang ? lo.an : lo.be), a.dzae, a.t2, a.lnpart);
+      CHG_TRY(reduce_rows_launch(a.lnpart, (int)ablocks, 8 * D, 4 * D, G + lo.be.g_c, st));
+      if (ang) CHG_TRY(reduce_rows_launch(a.lnpart + 4 * D, (int)ablocks, 8 * D, 4 * D, G + lo.an.g_c, st));
+    }
+    if (B > 0) {
+      k_bond_bwd_reduce<<<(unsigned)cdiv(B, 4), 256, 0, st>>>((int)B, D, W4, a.bond_src, g.bond_ptr, g.angle_ptr, a.dzae,
+                                                              a.t2, a.dmu, a.ssum[t], a.DZ12, a.deb);
+      CHG_LAUNCHED("k_bond_bwd_reduce");
+    }
+    CHG_TRY(segsum(N, g.bond_ptr, nullptr, a.DZ12, 8 * D, W4, a.AT + 4 * D, 8 * D, 0, nullptr, 0, nullptr, 0, st));
+    // atom conv gate
+    const int64_t eblocks = cdiv(E, kGateRowsPerBlock);
+    if (E > 0) {
+      LAUNCH_V(k_gate_atom_bwd, V, (unsigned)eblocks, 256, st, (int)E, a.zv[t], a.ea, a.dm, a.edge_src, ln_ptrs(P, lo.av),
+               a.dzv, a.dea, a.lnpart);
+      CHG_TRY(reduce_rows_launch(a.lnpart, (int)eblocks, 4 * D, 4 * D, G + lo.av.g_c, st));
+    }
+    CHG_TRY(segsum(N, g.edge_ptr, nullptr, a.dzv, 2 * D, 2 * D, a.AT, 8 * D, 0, nullptr, 0, nullptr, 0, st));
+    CHG_TRY(segsum(N, g.edge_ptr, g.edge_rev, a.dzv, 2 * D, 2 * D, a.AT + 2 * D, 8 * D, 0, nullptr, 0, nullptr, 0, st));
+    // input gradients
+    {
+      GemmProblem p = gp(N, D, a.dv[nx], D);
+      seg(p, a.AT, 8 * D, 0, 2 * D, Wav, 2 * D, 1);
+      seg(p, a.AT, 8 * D, 2 * D, 2 * D, Wav + D * 2 * D, 2 * D, 1);
+      seg(p, a.AT, 8 * D, 4 * D, 2 * D, Wbe, 2 * D, 1);
+      if (ang) seg(p, a.AT, 8 * D, 6 * D, 2 * D, Wan, 2 * D, 1);
+      p.res = a.dv[cur];
+      p.res_ld = D;
+      ps.push_back(p);
+      p = gp(E, D, a.de[nx], D);
+      seg(p, a.dzv, 2 * D, 0, 2 * D, Wav + 2 * D * 2 * D, 2 * D, 1);
+      p.res = a.de[cur];
+      p.res_ld = D;
+      ps.push_back(p);
+      p = gp(A, D, a.da[nx], D);
+      seg(p, a.dzae, 4 * D, 0, 2 * D, Wbe + 3 * D * 2 * D, 2 * D, 1);
+      if (ang) {
+        seg(p, a.dzae, 4 * D, 2 * D, 2 * D, Wan + 3 * D * 2 * D, 2 * D, 1);
+        p.res = a.da[cur];
+        p.res_ld = D;
+      }
+      ps.push_back(p);
+      CHG_TRY(run_gemms(ps, st));
+      ps.clear();
+      p = gp(B, D, a.de[nx], D);
+      p.c_rows = g.bond_edge;
+      p.accumulate = 1;
+      seg(p, a.DZ12, 8 * D, 0, 2 * D, Wbe + D * 2 * D, 2 * D, 1);
+      seg(p, a.DZ12, 8 * D, 4 * D, 2 * D, Wbe + 2 * D * 2 * D, 2 * D, 1);
+      if (ang) {
+        seg(p, a.DZ12, 8 * D, 2 * D, 2 * D, Wan + D * 2 * D, 2 * D, 1);
+        seg(p, a.DZ12, 8 * D, 6 * D, 2 * D, Wan + 2 * D * 2 * D, 2 * D, 1);
+      }
+      ps.push_back(p);
+      CHG_TRY(run_gemms(ps, st));
+      ps.clear();
+    }
+    // weight gradients of the first linear layers
+    {
+      const float* vt = a.v[t];
+      const float* et = a.e[t];
+      ts.push_back(tp(N, D, 2 * D, vt, D, 0, nullptr, a.AT, 8 * D, 0, nullptr, G + lo.av.W, 2 * D));
+      ts.push_back(tp(N, D, 2 * D, vt, D, 0, nullptr, a.AT, 8 * D, 2 * D, nullptr, G + lo.av.W + D * 2 * D, 2 * D));
+      ts.push_back(tp(E, D, 2 * D, et, D, 0, nullptr, a.dzv, 2 * D, 0, nullptr, G + lo.av.W + 2 * D * 2 * D, 2 * D));
+      ts.push_back(tp(N, 1, 2 * D, nullptr, 0, 0, nullptr, a.AT, 8 * D, 0, nullptr, G + lo.av.b, 2 * D));
+      for (int k = 0; k < (ang ? 2 : 1); ++k) {
+        const GatedOffsets& go = k ? lo.an : lo.be;
+        ts.push_back(tp(N, D, 2 * D, vt, D, 0, nullptr, a.AT, 8 * D, (4 + 2 * k) * D, nullptr, G + go.W, 2 * D));
+        ts.push_back(tp(B, D, 2 * D, et, D, 0, g.bond_edge, a.DZ12, 8 * D, 2 * k * D, nullptr, G + go.W + D * 2 * D, 2 * D));
+        ts.push_back(tp(B, D, 2 * D, et, D, 0, g.bond_edge, a.DZ12, 8 * D, (4 + 2 * k) * D, nullptr, G + go.W + 2 * D * 2 * D, 2 * D));
+        ts.push_back(tp(A, D, 2 * D, a.a[t], D, 0, nullptr, a.dzae, 4 * D, 2 * k * D, nullptr, G + go.W + 3 * D * 2 * D, 2 * D));
+        ts.push_back(tp(N, 1, 2 * D, nullptr, 0, 0, nullptr, a.AT, 8 * D, (4 + 2 * k) * D, nullptr, G + go.b, 2 * D));
+      }
+      CHG_TRY(run_tns(ts, a, st));
+      ts.clear();
+    }
+    cur = nx;
+  }
+
+  // embeddings
+  k_embed_bwd_Z<<<94, 64, 0, st>>>((int)N, D, bt.Z, a.dv[cur], G + L.W_Z);
+  CHG_LAUNCHED("k_embed_bwd_Z");
+  {
+    std::vector<TnProblem> ts;
+    ts.push_back(tp(E, m.R, D, a.rbf_a, m.R, 0, nullptr, a.de[cur], D, 0, nullptr, G + L.W_e, 2 * D));
+    ts.push_back(tp(E, m.R, D, a.rbf_a, m.R, 0, nullptr, a.dea, D, 0, nullptr, G + L.W_e + D, 2 * D));
+    ts.push_back(tp(E, 1, D, nullptr, 0, 0, nullptr, a.de[cur], D, 0, nullptr, G + L.b_e0, D));
+    ts.push_back(tp(B, m.R, D, a.rbf_b, m.R, 0, nullptr, a.deb, D, 0, nullptr, G + L.W_eb, D));
+    ts.push_back(tp(A, m.K, D, a.ft, m.K, 0, nullptr, a.da[cur], D, 0, nullptr, G + L.W_th, D));
+    ts.push_back(tp(A, 1, D, nullptr, 0, 0, nullptr, a.da[cur], D, 0, nullptr, G + L.b_th, D));
+    CHG_TRY(run_tns(ts, a, st));
+    std::vector<GemmProblem> ps;
+    GemmProblem p = gp(E, m.R, a.drbf_a, m.R);
+    seg(p, a.de[cur], D, 0, D, P + L.W_e, 2 * D, 1);
+    seg(p, a.dea, D, 0, D, P + L.W_e + D, 2 * D, 1);
+    ps.push_back(p);
+    p = gp(B, m.R, a.drbf_b, m.R);
+    seg(p, a.deb, D, 0, D, P + L.W_eb, D, 1);
+    ps.push_back(p);
+    CHG_TRY(run_gemms(ps, st));
+    if (E > 0) {
+      const int64_t nb = cdiv(E, kFreqRowsPerBlock);
+      k_rbf_fgrad<<<(unsigned)nb, 256, 0, st>>>((int)E, nullptr, a.edge_len, P + L.f_a, m.R, c.hp->r_atom,
+                                                c.hp->envelope_p, a.drbf_a, a.fpart);
+      CHG_LAUNCHED("k_rbf_fgrad");
+      CHG_TRY(reduce_rows_launch(a.fpart, (int)nb, m.R, m.R, G + L.f_a, st));
+    }
+    if (B > 0) {
+      const int64_t nb = cdiv(B, kFreqRowsPerBlock);
+      k_rbf_fgrad<<<(unsigned)nb, 256, 0, st>>>((int)B, g.bond_edge, a.edge_len, P + L.f_b, m.R, c.hp->r_bond,
+                                                c.hp->envelope_p, a.drbf_b, a.fpart);
+      CHG_LAUNCHED("k_rbf_fgrad");
+      CHG_TRY(reduce_rows_launch(a.fpart, (int)nb, m.R, m.R, G + L.f_b, st));
+    }
+  }
+  return CHGNET_OK;
+}
+
+}  // namespace
+
+size_t acts_bytes(const chgnet_hparams& hp, int64_t N, int64_t E, int64_t B, int64_t A, int64_t S) {
+  Arena ar;
+  Acts a;
+  Dims m{N, S, E, B, A, hp.d, hp.n_layers, hp.n_rbf, hp.n_fourier};
+  carve_acts(ar, m, a);
+  return align_up(ar.used, 256);
+}
+
+int forward_entry(const chgnet_hparams* hp, const chgnet_batch* batch, const chgnet_graph* graph, const float* params,
+                  float* energy, float* forces, float* stress, void* ws, size_t ws_bytes, hipStream_t st) {
+  Ctx c;
+  CHG_TRY(make_ctx(hp, batch, graph, ws, ws_bytes, c));
+  if (!params || !energy || !forces || !stress) return fail(CHGNET_EINVAL, "forward: null output or params");
+  return forward_impl(c, params, energy, forces, stress, st);
+}
+
+int backward_entry(const chgnet_hparams* hp, const chgnet_batch* batch, const chgnet_graph* graph, const float* params,
+                   const float* dE, const float* dF, const float* dS, float* grad, void* ws, size_t ws_bytes,
+                   hipStream_t st) {
+  Ctx c;
+  CHG_TRY(make_ctx(hp, batch, graph, ws, ws_bytes, c));
+  if (!params || !dE || !dF || !dS || !grad) return fail(CHGNET_EINVAL, "backward: null argument");
+  return backward_impl(c, params, dE, dF, dS, grad, st);
+}
+
+int step_entry(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_graph* graph, float* params,
+               const float* E_t, const float* F_t, const float* S_t, const float* loss_w, float* loss, float* grad,
+               float* adam_m, float* adam_v, const float* adam_hp, void* ws, size_t ws_bytes, hipStream_t st) {
+  if (!params || !E_t || !F_t || !S_t || !loss_w || !loss || !grad) return fail(CHGNET_EINVAL, "step: null argument");
+  if (adam_hp && (!adam_m || !adam_v || !(adam_hp[4] >= 1.0f)))
+    return fail(CHGNET_EINVAL, "step: Adam needs m, v and a step number t >= 1");
+  CHG_TRY(build_graph(hp, batch, graph, ws, ws_bytes, st));
+  Ctx c;
+  CHG_TRY(make_ctx(hp, batch, graph, ws, ws_bytes, c));
+  float* e_out = c.a.out_E;
+  float* f_out = c.a.out_F;
+  float* s_out = c.a.out_S;
+  CHG_TRY(forward_impl(c, params, e_out, f_out, s_out, st));
+  k_loss<<<1, 256, 0, st>>>((int)c.dm.S, (int)c.dm.N, batch->atom_ptr, e_out, f_out, s_out, E_t, F_t, S_t, loss_w[0],
+                            loss_w[1], loss_w[2], loss, c.a.dE, c.a.dF, c.a.dS);
+  CHG_LAUNCHED("k_loss");
+  CHG_TRY(backward_impl(c, params, c.a.dE, c.a.dF, c.a.dS, grad, st));
+  if (adam_hp) {
+    const float lr = adam_hp[0], b1 = adam_hp[1], b2 = adam_hp[2], eps = adam_hp[3], t = adam_hp[4];
+    const float c1 = 1.0f - powf(b1, t), c2 = 1.0f - powf(b2, t);
+    k_adam<<<(unsigned)cdiv(c.L.total, 256), 256, 0, st>>>(c.L.total, params, grad, adam_m, adam_v, lr, b1, b2, eps, c1, c2);
+    CHG_LAUNCHED("k_adam");
+  }
+  return CHGNET_OK;
+}
+
+}  // namespace chg
