@@ -19,7 +19,7 @@ the fp32 expression
 with one IEEE round-to-nearest per operation and no fused multiply-add, and
 an edge exists iff D2 < rc*rc (strict). This makes the edge set exactly
 reproducible. Every translation satisfying the test is kept (no truncation of
-the image range); the enumeration range below is generous.
+the image range); the per-pair enumeration range below is generous.
 
 Canonical order: edges grouped by source atom i (CSR), then by j, then by
 (n1, n2, n3) lexicographically. rev(i, j, n) = (j, i, -n). Bonds keep G^a
@@ -56,19 +56,24 @@ def fp32_d2(ri, rj, n, L):
 
 
 def _edges_of_atom(i, a0, a1, pos32, L32, frac, h, rc):
-    """All (j, n, D2) with D2 < rc^2 for source atom i, in canonical order."""
+    """All (j, n, D2) with D2 < rc^2 for source atom i, in canonical order.
+
+    A translation n can only pass if |df_a + n_a| <= (rc + slack) / h_a on
+    every axis (the component of a displacement along the normal of a lattice
+    plane bounds its length), so each pair (i, j) is tested on every integer
+    n_a in that interval, with 0.5 A of slack for the fp32 rounding."""
     rc2 = np.float32(rc * rc)
     js = np.arange(a0, a1)
     df = frac[a0:a1] - frac[i]  # [n_s, 3], fp64
-    # any accepted translation has |df_a + n_a| <= (rc + slack) / h_a
     reach = (rc + 0.5) / h
-    lo = np.floor(-df.max(axis=0) - reach).astype(np.int64) - 1
-    hi = np.ceil(-df.min(axis=0) + reach).astype(np.int64) + 1
-    grid = np.stack(
-        np.meshgrid(*[np.arange(lo[a], hi[a] + 1) for a in range(3)], indexing="ij"), axis=-1
-    ).reshape(-1, 3)
-    J = np.repeat(js, grid.shape[0])
-    Nimg = np.tile(grid, (js.shape[0], 1))
+    lo = np.ceil(-df - reach).astype(np.int64)  # [n_s, 3]
+    cnt = np.floor(-df + reach).astype(np.int64) - lo + 1
+    kmax = cnt.max(axis=0)
+    grid = np.stack(np.meshgrid(*[np.arange(k) for k in kmax], indexing="ij"), axis=-1).reshape(-1, 3)
+    Nimg = lo[:, None, :] + grid[None, :, :]  # [n_s, G, 3]
+    valid = (grid[None, :, :] < cnt[:, None, :]).all(axis=2)
+    J = np.broadcast_to(js[:, None], valid.shape)[valid]
+    Nimg = Nimg[valid]
     d2 = fp32_d2(pos32[i], pos32[J], Nimg, L32)
     keep = d2 < rc2
     keep &= ~((J == i) & (Nimg == 0).all(axis=1))

@@ -1,0 +1,170 @@
+"""GPU forward, backward and training step against the fp64 oracle:
+|gpu - oracle| <= 1e-5 + 1e-4 |oracle| for energies, forces, stresses, the
+loss and every parameter gradient; bitwise run-to-run reproducibility."""
+import numpy as np
+import pytest
+
+from gpu_helpers import assert_close, assert_graph_equal, subset_batch
+from oracle import graph as og
+from oracle import model as om
+from paper_2412_20796_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def bd():
+    import torch
+
+    from paper_2412_20796_amd import binding
+
+    assert torch.cuda.is_available()
+    binding.lib()
+    return binding
+
+
+def _dev(x):
+    import torch
+
+    return torch.as_tensor(np.ascontiguousarray(x)).to("cuda")
+
+
+def _setup(bd, b, d, T, graph=None):
+    hp = bd.hparams(d=d, n_layers=T)
+    db = bd.DeviceBatch.from_host(b)
+    ws = bd.Workspace()
+    if graph is None:
+        g = bd.DeviceGraph(b.n_atoms, 64, 16, 64)
+        bd.build_graph(hp, db, g, ws)
+    else:
+        g = bd.DeviceGraph.from_host(graph)
+    return hp, db, g, ws
+
+
+def _check_step(bd, b, params, targets, d, T, name):
+    ohp = om.HParams(d=d, n_layers=T)
+    ref_graph = og.build_graph(b.atom_ptr, b.pos, b.lattice)
+    rl, rg, (rE, rF, rS), _ = om.step(ohp, b, params.astype(np.float64), targets, graph=ref_graph)
+    hp, db, g, ws = _setup(bd, b, d, T)
+    p = _dev(params)
+    E, F, S = bd.forward(hp, db, g, p, ws)
+    assert_close(E.cpu().numpy(), rE, name + " energy")
+    assert_close(F.cpu().numpy(), rF, name + " forces")
+    assert_close(S.cpu().numpy(), rS, name + " stress")
+    loss, grad = bd.step(hp, db, g, p, [_dev(x) for x in targets], ws)
+    assert_graph_equal(g.host(), ref_graph)
+    assert_close(loss.cpu().numpy(), [rl], name + " loss")
+    gg = grad.cpu().numpy()
+    lay, _ = om.layout(ohp)
+    for tname, (off, shape) in lay.items():
+        n = int(np.prod(shape))
+        assert_close(gg[off:off + n], rg[off:off + n], "%s grad %s" % (name, tname))
+    return gg
+
+
+@pytest.mark.parametrize("name", ["cubic8", "triclinic40", "heavytail64"])
+def test_step_parity_workloads(bd, name):
+    b, params, targets, d, T = synth.workload_inputs(name)
+    _check_step(bd, b, params, targets, d, T, name)
+
+
+def test_step_parity_random_small_batches(bd):
+    for seed in range(4):
+        b = synth.random_crystals(seed=300 + seed, n_struct=1 + seed, n_lo=2, n_hi=14, rho=(0.06, 0.12))
+        params = synth.make_params(64, 3, seed=(9, 1, seed))
+        targets = synth.make_targets(b, seed=(9, 2, seed))
+        _check_step(bd, b, params, targets, 64, 3, "random%d" % seed)
+
+
+def test_step_parity_sparse_cells(bd):
+    """No bonds at all (B = A = 0), and one isolated atom with no edges (E = 0)."""
+    L = np.eye(3) * 8.5
+    frac = np.array([[0.0, 0.0, 0.0], [0.5, 0.5, 0.5]])
+    b = synth.make_custom_batch([L], [frac], [np.array([3, 17])])
+    params = synth.make_params(64, 2, seed=(8, 1, 0))
+    _check_step(bd, b, params, synth.make_targets(b, seed=(8, 2, 0)), 64, 2, "no-bonds")
+    b1 = synth.make_custom_batch([np.eye(3) * 13.0], [np.zeros((1, 3))], [np.array([26])])
+    _check_step(bd, b1, params, synth.make_targets(b1, seed=(8, 2, 1)), 64, 2, "no-edges")
+
+
+def test_single_layer_and_d128(bd):
+    b = synth.random_crystals(seed=11, n_struct=3, n_lo=4, n_hi=12)
+    _check_step(bd, b, synth.make_params(64, 1, seed=(7, 1, 0)), synth.make_targets(b, seed=(7, 2, 0)), 64, 1, "T1")
+    _check_step(bd, b, synth.make_params(128, 3, seed=(7, 1, 1)), synth.make_targets(b, seed=(7, 2, 1)), 128, 3, "d128")
+
+
+def test_wide128_sampled_structures(bd):
+    """Full-size d=128, T=5 batch on the GPU; the oracle recomputes a sample of
+    structures alone. Forward outputs of those structures must match, and the
+    backward with upstream gradients only on the sample must match the
+    oracle's gradient of the sample (the backward is linear in them)."""
+    b, params, targets, d, T = synth.workload_inputs("wide128")
+    hp, db, g, ws = _setup(bd, b, d, T)
+    p = _dev(params)
+    E, F, S = bd.forward(hp, db, g, p, ws)
+    E, F, S = E.cpu().numpy(), F.cpu().numpy(), S.cpu().numpy()
+    sample = [0, 17, 64, 127]
+    sb = subset_batch(b, sample)
+    ohp = om.HParams(d=d, n_layers=T)
+    sg = og.build_graph(sb.atom_ptr, sb.pos, sb.lattice)
+    rE, rF, rS, cache = om.forward(ohp, sb, sg, params.astype(np.float64))
+    atoms = np.concatenate([np.arange(b.atom_ptr[s], b.atom_ptr[s + 1]) for s in sample])
+    assert_close(E[sample], rE, "wide128 energy")
+    assert_close(F[atoms], rF, "wide128 forces")
+    assert_close(S[sample], rS, "wide128 stress")
+    rng = np.random.default_rng(0)
+    dE = np.zeros(b.n_struct, np.float32)
+    dF = np.zeros((b.n_atoms, 3), np.float32)
+    dS = np.zeros((b.n_struct, 3, 3), np.float32)
+    dE[sample] = rng.standard_normal(len(sample)) * 0.1
+    dF[atoms] = rng.standard_normal((len(atoms), 3)) * 0.1
+    dS[sample] = rng.standard_normal((len(sample), 3, 3)) * 0.1
+    grad = bd.backward(hp, db, g, p, _dev(dE), _dev(dF), _dev(dS), ws).cpu().numpy()
+    rg = om.backward(ohp, cache, dE[sample], dF[atoms], dS[sample])
+    lay, _ = om.layout(ohp)
+    for tname, (off, shape) in lay.items():
+        n = int(np.prod(shape))
+        assert_close(grad[off:off + n], rg[off:off + n], "wide128 grad " + tname)
+
+
+def test_super4096_forward(bd):
+    b, params, targets, d, T = synth.workload_inputs("super4096")
+    hp, db, g, ws = _setup(bd, b, d, T)
+    E, F, S = bd.forward(hp, db, g, _dev(params), ws)
+    ref_graph = og.build_graph(b.atom_ptr, b.pos, b.lattice)
+    assert_graph_equal(g.host(), ref_graph)
+    rE, rF, rS, _ = om.forward(om.HParams(d=d, n_layers=T), b, ref_graph, params.astype(np.float64))
+    assert_close(E.cpu().numpy(), rE, "super4096 energy")
+    assert_close(F.cpu().numpy(), rF, "super4096 forces")
+    assert_close(S.cpu().numpy(), rS, "super4096 stress")
+
+
+def test_adam_update(bd):
+    b, params, targets, d, T = synth.workload_inputs("cubic8")
+    hp, db, g, ws = _setup(bd, b, d, T)
+    p = _dev(params)
+    m = _dev(np.zeros_like(params))
+    v = _dev(np.zeros_like(params))
+    lr, b1, b2, eps = 3e-4, 0.9, 0.999, 1e-8
+    ohp = om.HParams(d=d, n_layers=T)
+    pr = params.astype(np.float64)
+    mr = np.zeros_like(pr)
+    vr = np.zeros_like(pr)
+    for t in (1, 2):
+        _, grad = bd.step(hp, db, g, p, [_dev(x) for x in targets], ws, adam=(m, v, (lr, b1, b2, eps, float(t))))
+        _, rg, _, _ = om.step(ohp, b, pr, targets)
+        pr, mr, vr = om.adam(pr, rg, mr, vr, lr, b1, b2, eps, t)
+        assert_close(p.cpu().numpy(), pr, "adam params step %d" % t)
+        assert_close(m.cpu().numpy(), mr, "adam m step %d" % t)
+
+
+def test_bitwise_reproducible(bd):
+    b, params, targets, d, T = synth.workload_inputs("triclinic40")
+    hp, db, g, ws = _setup(bd, b, d, T)
+    p = _dev(params)
+    tg = [_dev(x) for x in targets]
+    l1, g1 = bd.step(hp, db, g, p, tg, ws)
+    l1, g1 = l1.cpu().numpy().copy(), g1.cpu().numpy().copy()
+    l2, g2 = bd.step(hp, db, g, p, tg, ws)
+    assert np.array_equal(l1, l2.cpu().numpy())
+    assert np.array_equal(g1, g2.cpu().numpy())
