@@ -1,0 +1,230 @@
+"""Benchmark: FastCHGNet training steps per second on one MI355X.
+
+One step = chgnet_step on one batch: periodic graph build, forward (basis,
+embeddings, T interaction blocks, energy/force/stress heads), weighted MSE
+loss, backward for every weight and the Adam update, all in the HIP library.
+Inputs (positions, lattices, atomic numbers, targets, weights) are seeded and
+synthetic (the dataset is not available) and are resident in HBM before the
+timed region.
+
+Prints one JSON line (rank 0). Default workload: 40 random triclinic crystals
+with 8-64 atoms each, d = 64, 4 layers.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+FP32_PEAK_TFLOPS = 157.3
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="triclinic40")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-sample", type=int, default=0, help="structures in the CPU oracle sample (0 = auto)")
+    ap.add_argument("--no-roofline", action="store_true")
+    return ap.parse_args()
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path (run with --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    from paper_2412_20796_amd import binding as bd
+    from paper_2412_20796_amd import synth
+
+    dev = "cuda:0"
+    torch.cuda.set_device(0)
+    b, params, targets, d, T = synth.workload_inputs(args.workload)
+    hp = bd.hparams(d=d, n_layers=T)
+    db = bd.DeviceBatch.from_host(b, dev)
+    g = bd.DeviceGraph(b.n_atoms, 1024, 256, 1024, dev)
+    ws = bd.Workspace(dev)
+    p = torch.tensor(params, device=dev)
+    m = torch.zeros_like(p)
+    v = torch.zeros_like(p)
+    tg = [torch.tensor(x, device=dev) for x in targets]
+    grad = torch.empty_like(p)
+    loss = torch.empty(1, dtype=torch.float32, device=dev)
+    lr, b1, b2, eps = 3e-4, 0.9, 0.999, 1e-8
+
+    step_no = [0]
+
+    def one_step():
+        step_no[0] += 1
+        bd.step(hp, db, g, p, tg, ws, grad=grad, loss=loss, adam=(m, v, (lr, b1, b2, eps, float(step_no[0]))))
+
+    for _ in range(max(args.warmup, 1)):
+        one_step()
+    torch.cuda.synchronize()
+    E, B, A = g.n_edges, g.n_bonds, g.n_angles
+
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    t0.record()
+    for _ in range(args.steps):
+        one_step()
+    t1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    ms = t0.elapsed_time(t1) / args.steps
+    S = b.n_struct
+    value = S / (ms * 1e-3)
+
+    out = {
+        "metric": "training structures/sec (fwd+bwd) on 1 MI355X",
+        "value": round(value, 2),
+        "unit": "structures/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "fp32",
+        "data": "synthetic (seeded crystals shaped like the paper's training set; random-init weights)",
+        "config": {"workload": args.workload, "structures": S, "atoms": b.n_atoms, "edges": E, "bonds": B,
+                   "angles": A, "d": d, "layers": T, "parallelism": "single GPU"},
+        "edges_per_s": round(E / (ms * 1e-3), 1),
+        "angles_per_s": round(A / (ms * 1e-3), 1),
+        "wall_s_timed": round(wall, 3),
+        "final_loss": float(loss.cpu()[0]),
+    }
+    if not args.no_roofline:
+        bd.profile_start(400 * args.steps + 1000)
+        for _ in range(args.steps):
+            one_step()
+        torch.cuda.synchronize()
+        prof = bd.profile_stop()
+        out["roofline"], out["kernels"] = roofline(prof, args.steps, dict(N=b.n_atoms, E=E, B=B, A=A, S=S, D=d, T=T))
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(args.workload, args.cpu_sample)
+    print(json.dumps(out), flush=True)
+
+
+def algorithmic_cost(tag, z):
+    """Algorithmic work of one step's launches of `tag`: ("mfma", flops) for
+    the dense products, ("hbm", bytes) for gather/scatter/elementwise kernels.
+
+    Per-unit figures (fp32, d = D): an angle of a layer with an angle update
+    costs 8d^2 flops in its a-term (a [W_bond | W_angle], d -> 4d), 4d^2 in
+    the last layer (bond conv only); an edge costs 4d^2 (e W, d -> 2d). The
+    backward input gradients cost the same per unit, the weight gradients the
+    same again (A^T B over the rows). Bytes count each array read or written
+    once (gathered rows of small per-atom/per-bond tables excluded)."""
+    N, E, B, A, D, T = z["N"], z["E"], z["B"], z["A"], z["D"], z["T"]
+    Tang = T - 1  # layers with an angle update
+    f = 4  # bytes per fp32
+    if tag == "gemm_z":
+        return "mfma", T * E * 4 * D * D + Tang * A * 8 * D * D + A * 4 * D * D
+    if tag == "gemm_in_bwd":
+        return "mfma", T * (E * 4 * D * D + N * 16 * D * D) - N * 4 * D * D + Tang * A * 8 * D * D + A * 4 * D * D
+    if tag == "tn_in":
+        return "mfma", (T * (E * 4 * D * D + N * 16 * D * D + B * 8 * D * D) - N * 4 * D * D
+                        + Tang * (A * 8 * D * D + B * 8 * D * D) + A * 4 * D * D)
+    if tag == "gemm_proj":
+        return "mfma", T * (N * 16 * D * D + B * 8 * D * D) - N * 4 * D * D - B * 4 * D * D
+    if tag == "gemm_bond_bwd":
+        return "mfma", Tang * B * 16 * D * D + B * 8 * D * D
+    if tag == "k_gate_angle_fwd":  # read z (4d or 2d), read a, write a', write eb-weighted message
+        return "hbm", f * (Tang * A * (4 * D + 3 * D) + A * (2 * D + D))
+    if tag == "k_gate_angle_bwd":  # read z, da'; write dz, t2
+        return "hbm", f * (Tang * A * (4 * D + D + 4 * D + D) + A * (2 * D + 2 * D + D))
+    if tag == "k_gate_atom_fwd":  # read z (2d), e^a; write message
+        return "hbm", f * T * E * (2 * D + 2 * D)
+    if tag == "k_gate_atom_bwd":  # read z, e^a, d e^a; write dz, d e^a
+        return "hbm", f * T * E * (2 * D + D + D + 2 * D + D)
+    if tag == "k_bond_bwd_reduce":  # read dz twice (both roles), t2; write DZ12
+        return "hbm", f * (Tang * A * (8 * D + D) + A * (4 * D + D) + T * B * 8 * D)
+    return None, None
+
+
+def roofline(prof, steps, z):
+    rows = []
+    for tag, (n, ms) in prof.items():
+        bound, work = algorithmic_cost(tag, z)
+        per_step_ms = ms / steps
+        row = {"tag": tag, "launches_per_step": n / steps, "ms_per_step": round(per_step_ms, 4),
+               "avg_launch_us": round(1e3 * ms / max(n, 1), 2)}
+        if bound:
+            sec = ms * 1e-3 / steps
+            if bound == "mfma":
+                ach = work / sec / 1e12
+                row.update(bound="mfma", achieved=round(ach, 3), unit="TFLOP/s", frac=round(ach / FP32_PEAK_TFLOPS, 4))
+            else:
+                ach = work / sec / 1e9
+                row.update(bound="hbm", achieved=round(ach, 1), unit="GB/s", frac=round(ach / HBM_PEAK_GBS, 4))
+        rows.append(row)
+    rows.sort(key=lambda r: -r["ms_per_step"])
+    dom = next(r for r in rows if "bound" in r)
+    bound, work = algorithmic_cost(dom["tag"], z)
+    n_launch = dom["launches_per_step"]
+    per_launch = work / n_launch
+    rl = {"kernel": dom["tag"], "bound": dom["bound"], "achieved": dom["achieved"],
+          "peak": FP32_PEAK_TFLOPS if dom["bound"] == "mfma" else HBM_PEAK_GBS, "unit": dom["unit"],
+          "frac": dom["frac"], "traffic": None,
+          "work_per_launch": per_launch, "work_unit": "flop" if bound == "mfma" else "byte",
+          "avg_launch_us": dom["avg_launch_us"], "launches_per_step": n_launch,
+          "timing": "HIP events around every launch of the kernel on the library's stream, %d steps" % steps}
+    return rl, rows[:14]
+
+
+def cpu_baseline(workload, sample, min_seconds=10.0):
+    """The CPU oracle (fp64 NumPy, untuned) on a bounded sample of the same
+    workload: graph build, forward, loss and backward of the first `sample`
+    structures (default: the whole batch), repeated until min_seconds of CPU
+    work; reported in structures per second."""
+    import numpy as np
+
+    from oracle import model as om
+    from paper_2412_20796_amd import synth
+
+    b, params, targets, d, T = synth.workload_inputs(workload)
+    if sample <= 0:
+        sample = b.n_struct
+    ptr = [0]
+    for s in range(sample):
+        ptr.append(ptr[-1] + int(b.atom_ptr[s + 1] - b.atom_ptr[s]))
+    n = ptr[-1]
+    sb = synth.Batch(np.asarray(ptr, np.int32), b.pos[:n], b.lattice[:sample], b.Z[:n])
+    tgt = (targets[0][:sample], targets[1][:n], targets[2][:sample])
+    hp = om.HParams(d=d, n_layers=T)
+    reps = 0
+    t = time.perf_counter()
+    while True:
+        om.step(hp, sb, params.astype(np.float64), tgt)
+        reps += 1
+        dt = time.perf_counter() - t
+        if dt >= min_seconds or reps >= 20:
+            break
+    try:
+        from threadpoolctl import threadpool_info
+
+        threads = max(int(i.get("num_threads", 1)) for i in threadpool_info()) if threadpool_info() else 1
+    except Exception:  # pragma: no cover - threadpoolctl is optional
+        threads = 1
+    return {"value": round(reps * sample / dt, 4), "unit": "structures/s", "cores": threads, "kind": "oracle",
+            "sample": "%d of the %d structures (%d atoms), %d full step(s) (graph, forward, loss, backward) in %.1f s"
+                      % (sample, b.n_struct, n, reps, dt)}
+
+
+if __name__ == "__main__":
+    main()

@@ -157,6 +157,20 @@ int chgnet_step(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_grap
 /* Text of the last error on the calling thread ("" if none). */
 const char* chgnet_last_error_string(void);
 
+/* Measurement only (benchmarks, profilers). While enabled, the library
+ * records a pair of HIP events around each of its kernel launches (up to
+ * max_launches), on the stream of the call. This is the library's only
+ * global state; it is off by default and not thread-safe.
+ * chgnet_profile_stop waits for the recorded events, disables timing and
+ * writes one line per launch tag into buf (host memory, buflen bytes):
+ * "<tag> <launches> <total milliseconds>\n". Tags are kernel names, or the
+ * role of a GEMM launch (gemm_z: edge and angle GatedMLP pre-activations;
+ * gemm_in_bwd: input gradients of the interaction block; tn_in: weight
+ * gradients of the interaction block; ...). Returns CHGNET_EINVAL if buf is
+ * too small and CHGNET_EWORKSPACE if more than max_launches launches ran. */
+int chgnet_profile_start(int max_launches);
+int chgnet_profile_stop(char* buf, size_t buflen);
+
 #ifdef __cplusplus
 }
 #endif

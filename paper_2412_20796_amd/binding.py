@@ -18,7 +18,8 @@ _lib = None
 
 CHGNET_OK, CHGNET_EINVAL, CHGNET_ECAPACITY, CHGNET_EWORKSPACE, CHGNET_EHIP = 0, -1, -2, -3, -4
 EXPORTED = ("chgnet_param_count", "chgnet_workspace_size", "chgnet_build_graph", "chgnet_forward",
-            "chgnet_backward", "chgnet_step", "chgnet_last_error_string")
+            "chgnet_backward", "chgnet_step", "chgnet_last_error_string", "chgnet_profile_start",
+            "chgnet_profile_stop")
 
 
 class ChgnetError(RuntimeError):
@@ -66,8 +67,11 @@ def lib():
                                   vp, ctypes.POINTER(ctypes.c_float), vp, vp, vp, vp, ctypes.POINTER(ctypes.c_float),
                                   vp, ctypes.c_size_t, vp]
         L.chgnet_last_error_string.restype = ctypes.c_char_p
-        for name in EXPORTED[:-1]:
-            getattr(L, name).restype = ctypes.c_int
+        L.chgnet_profile_start.argtypes = [ctypes.c_int]
+        L.chgnet_profile_stop.argtypes = [ctypes.c_char_p, ctypes.c_size_t]
+        for name in EXPORTED:
+            if name != "chgnet_last_error_string":
+                getattr(L, name).restype = ctypes.c_int
         _lib = L
     return _lib
 
@@ -91,6 +95,21 @@ def workspace_size(hp: HParams, N, E, B, A, S) -> int:
     n = ctypes.c_size_t()
     _check(lib().chgnet_workspace_size(ctypes.byref(hp), N, E, B, A, S, ctypes.byref(n)))
     return n.value
+
+
+def profile_start(max_launches=100000):
+    _check(lib().chgnet_profile_start(max_launches))
+
+
+def profile_stop():
+    """{tag: (launches, total_ms)} of the launches since profile_start."""
+    buf = ctypes.create_string_buffer(1 << 16)
+    _check(lib().chgnet_profile_stop(buf, len(buf)))
+    out = {}
+    for line in buf.value.decode().splitlines():
+        tag, n, ms = line.split()
+        out[tag] = (int(n), float(ms))
+    return out
 
 
 def _ptr(t):

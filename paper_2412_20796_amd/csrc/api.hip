@@ -1,7 +1,10 @@
 // C-ABI entry points, hyperparameter validation and the flat parameter layout.
 #include <hip/hip_runtime.h>
 
+#include <cstdio>
+#include <map>
 #include <string>
+#include <vector>
 
 #include "common.hpp"
 
@@ -22,6 +25,30 @@ int step_entry(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_graph
 
 namespace {
 thread_local std::string g_last_error;
+
+// Per-launch event timing for measurement (chgnet_profile_start/stop).
+struct Profiler {
+  bool on = false;
+  std::vector<hipEvent_t> ev;
+  size_t used = 0;
+  struct Rec { std::string tag; int a, b; };
+  std::vector<Rec> recs;
+};
+Profiler g_prof;
+}  // namespace
+
+int prof_mark(hipStream_t st) {
+  if (!g_prof.on || g_prof.used + 2 > g_prof.ev.size()) return -1;
+  const int i = (int)g_prof.used;
+  if (hipEventRecord(g_prof.ev[i], st) != hipSuccess) return -1;
+  g_prof.used += 2;
+  return i;
+}
+
+void prof_close(hipStream_t st, int first, const char* tag) {
+  if (first < 0) return;
+  hipEventRecord(g_prof.ev[first + 1], st);
+  g_prof.recs.push_back({tag, first, first + 1});
 }
 
 void set_error(const std::string& msg) { g_last_error = msg; }
@@ -144,5 +171,45 @@ int chgnet_step(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_grap
 }
 
 const char* chgnet_last_error_string(void) { return chg::g_last_error.c_str(); }
+
+int chgnet_profile_start(int max_launches) {
+  auto& P = chg::g_prof;
+  if (max_launches < 1) return chg::fail(CHGNET_EINVAL, "max_launches must be >= 1");
+  while ((int)P.ev.size() < 2 * max_launches) {
+    hipEvent_t e;
+    CHG_HIP(hipEventCreate(&e));
+    P.ev.push_back(e);
+  }
+  P.used = 0;
+  P.recs.clear();
+  P.on = true;
+  return CHGNET_OK;
+}
+
+int chgnet_profile_stop(char* buf, size_t buflen) {
+  auto& P = chg::g_prof;
+  P.on = false;
+  std::map<std::string, std::pair<int64_t, double>> agg;
+  for (const auto& r : P.recs) {
+    CHG_HIP(hipEventSynchronize(P.ev[r.b]));
+    float ms = 0.f;
+    CHG_HIP(hipEventElapsedTime(&ms, P.ev[r.a], P.ev[r.b]));
+    auto& x = agg[r.tag];
+    x.first += 1;
+    x.second += ms;
+  }
+  std::string out;
+  char line[256];
+  for (const auto& kv : agg) {
+    std::snprintf(line, sizeof(line), "%s %lld %.6f\n", kv.first.c_str(), (long long)kv.second.first, kv.second.second);
+    out += line;
+  }
+  const bool truncated = P.used + 2 > P.ev.size();
+  P.recs.clear();
+  P.used = 0;
+  if (!buf || buflen <= out.size()) return chg::fail(CHGNET_EINVAL, "profile buffer too small");
+  std::snprintf(buf, buflen, "%s", out.c_str());
+  return truncated ? chg::fail(CHGNET_EWORKSPACE, "more launches than max_launches; later ones not timed") : CHGNET_OK;
+}
 
 }  // extern "C"

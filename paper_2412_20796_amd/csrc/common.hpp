@@ -37,6 +37,21 @@ int fail(int code, const std::string& msg);
       return ::chg::fail(CHGNET_EHIP, std::string("launch ") + name + ": " + hipGetErrorString(_e)); \
   } while (0)
 
+// Optional per-launch timing (measurement only; off unless enabled through
+// chgnet_profile_start). Events bracket each launch on its own stream.
+int prof_mark(hipStream_t st);                       // returns event index or -1
+void prof_close(hipStream_t st, int first, const char* tag);
+
+#define KLAUNCH(st, tag, ...)                                                                 \
+  do {                                                                                        \
+    const int _pf = ::chg::prof_mark(st);                                                     \
+    __VA_ARGS__;                                                                              \
+    hipError_t _e = hipGetLastError();                                                        \
+    if (_e != hipSuccess)                                                                     \
+      return ::chg::fail(CHGNET_EHIP, std::string("launch ") + (tag) + ": " + hipGetErrorString(_e)); \
+    ::chg::prof_close(st, _pf, tag);                                                          \
+  } while (0)
+
 inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 

@@ -174,44 +174,67 @@ __global__ void __launch_bounds__(256) k_tn(TnLaunch L, float* __restrict__ part
     }
 }
 
-__global__ void k_tn_reduce(TnLaunch L, const float* __restrict__ part) {
+// Ordered column sums of chunk partials: 16 wavefronts per block, wave w
+// sums chunks w, w+16, ... (fp64), then the 16 partial sums are added in
+// wave order. The result is independent of scheduling.
+__device__ __forceinline__ double sum_chunks(const float* __restrict__ src, int nchunks, int64_t stride, int w) {
+  double s0 = 0.0, s1 = 0.0;
+  int c = w;
+  for (; c + 16 < nchunks; c += 32) {
+    s0 += (double)src[(int64_t)c * stride];
+    s1 += (double)src[(int64_t)(c + 16) * stride];
+  }
+  if (c < nchunks) s0 += (double)src[(int64_t)c * stride];
+  return s0 + s1;
+}
+
+__global__ void __launch_bounds__(1024) k_tn_reduce(TnLaunch L, const float* __restrict__ part) {
+  __shared__ double red[16][64];
   const TnPlan& Q = L.q[blockIdx.y];
   const TnProblem& P = Q.p;
   const int64_t mn = (int64_t)P.M * P.N;
-  const int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (k >= mn) return;
-  double s = 0.0;
-  const float* src = part + Q.off + k;
-  for (int c = 0; c < Q.nchunks; ++c) s += (double)src[(int64_t)c * mn];
-  const int m = (int)(k / P.N), n = (int)(k % P.N);
-  float* o = P.out + (int64_t)m * P.ld_out + n;
-  *o = (float)((double)*o + s);
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int64_t k = (int64_t)blockIdx.x * 64 + lane;
+  if ((int64_t)blockIdx.x * 64 >= mn) return;
+  red[w][lane] = k < mn ? sum_chunks(part + Q.off + k, Q.nchunks, mn, w) : 0.0;
+  __syncthreads();
+  if (w == 0 && k < mn) {
+    double s = 0.0;
+    for (int q = 0; q < 16; ++q) s += red[q][lane];
+    const int m = (int)(k / P.N), n = (int)(k % P.N);
+    float* o = P.out + (int64_t)m * P.ld_out + n;
+    *o = (float)((double)*o + s);
+  }
 }
 
-__global__ void k_reduce_rows(const float* __restrict__ part, int nchunks, int64_t stride, int count,
-                              float* __restrict__ out) {
-  const int k = blockIdx.x * blockDim.x + threadIdx.x;
-  if (k >= count) return;
-  double s = 0.0;
-  for (int c = 0; c < nchunks; ++c) s += (double)part[(int64_t)c * stride + k];
-  out[k] = (float)((double)out[k] + s);
+__global__ void __launch_bounds__(1024) k_reduce_rows(const float* __restrict__ part, int nchunks, int64_t stride,
+                                                      int count, float* __restrict__ out) {
+  __shared__ double red[16][64];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int k = blockIdx.x * 64 + lane;
+  red[w][lane] = k < count ? sum_chunks(part + k, nchunks, stride, w) : 0.0;
+  __syncthreads();
+  if (w == 0 && k < count) {
+    double s = 0.0;
+    for (int q = 0; q < 16; ++q) s += red[q][lane];
+    out[k] = (float)((double)out[k] + s);
+  }
 }
 
 }  // namespace
 
-int gemm_launch(const GemmBatch& b, hipStream_t st) {
+int gemm_launch(const GemmBatch& b, hipStream_t st, const char* tag) {
   int gx = 0, gy = 0;
   for (int i = 0; i < b.n; ++i) {
     gx = std::max<int>(gx, (int)cdiv(b.p[i].M, 64));
     gy = std::max<int>(gy, (int)cdiv(b.p[i].N, 64));
   }
   if (b.n == 0 || gx == 0 || gy == 0) return CHGNET_OK;
-  k_gemm<<<dim3(gx, gy, b.n), 256, 0, st>>>(b);
-  CHG_LAUNCHED("k_gemm");
+  KLAUNCH(st, tag, k_gemm<<<dim3(gx, gy, b.n), 256, 0, st>>>(b));
   return CHGNET_OK;
 }
 
-int tn_launch(const TnBatch& b, float* part, int64_t part_cap, hipStream_t st) {
+int tn_launch(const TnBatch& b, float* part, int64_t part_cap, hipStream_t st, const char* tag) {
   TnLaunch L;
   L.n = b.n;
   int64_t off = 0;
@@ -224,7 +247,8 @@ int tn_launch(const TnBatch& b, float* part, int64_t part_cap, hipStream_t st) {
     q.tiles_n = (int)cdiv(q.p.N, 64);
     q.tiles = tm * q.tiles_n;
     const int64_t mn = (int64_t)q.p.M * q.p.N;
-    int64_t nch = std::max<int64_t>(1, std::min<int64_t>(cdiv(q.p.R, 64), std::max(1, 1024 / q.tiles)));
+    int64_t nch = std::max<int64_t>(1, std::min<int64_t>(cdiv(q.p.R, 256), std::max(8, 512 / q.tiles)));
+    nch = std::min<int64_t>(nch, 128);
     nch = std::min<int64_t>(nch, std::max<int64_t>(1, budget / std::max<int64_t>(1, mn)));
     int64_t rpc = cdiv(cdiv(q.p.R, nch), 16) * 16;
     if (rpc < 16) rpc = 16;
@@ -238,20 +262,17 @@ int tn_launch(const TnBatch& b, float* part, int64_t part_cap, hipStream_t st) {
   if (off > part_cap) return fail(CHGNET_EWORKSPACE, "split-K partial buffer too small");
   if (b.n == 0) return CHGNET_OK;
   if (gx > 0) {
-    k_tn<<<dim3(gx, gy, b.n), 256, 0, st>>>(L, part);
-    CHG_LAUNCHED("k_tn");
+    KLAUNCH(st, tag, k_tn<<<dim3(gx, gy, b.n), 256, 0, st>>>(L, part));
   }
   int64_t maxmn = 0;
   for (int i = 0; i < b.n; ++i) maxmn = std::max<int64_t>(maxmn, (int64_t)b.p[i].M * b.p[i].N);
-  k_tn_reduce<<<dim3((unsigned)cdiv(maxmn, 256), b.n), 256, 0, st>>>(L, part);
-  CHG_LAUNCHED("k_tn_reduce");
+  KLAUNCH(st, "k_tn_reduce", k_tn_reduce<<<dim3((unsigned)cdiv(maxmn, 64), b.n), 1024, 0, st>>>(L, part));
   return CHGNET_OK;
 }
 
 int reduce_rows_launch(const float* part, int nchunks, int64_t stride, int count, float* out, hipStream_t st) {
   if (count <= 0) return CHGNET_OK;
-  k_reduce_rows<<<(unsigned)cdiv(count, 256), 256, 0, st>>>(part, nchunks, stride, count, out);
-  CHG_LAUNCHED("k_reduce_rows");
+  KLAUNCH(st, "k_reduce_rows", k_reduce_rows<<<(unsigned)cdiv(count, 64), 1024, 0, st>>>(part, nchunks, stride, count, out));
   return CHGNET_OK;
 }
 

@@ -55,7 +55,7 @@ struct GemmBatch {
   GemmProblem p[kMaxGemmProblems];
 };
 
-int gemm_launch(const GemmBatch& b, hipStream_t st);
+int gemm_launch(const GemmBatch& b, hipStream_t st, const char* tag);
 
 // dW[m, n] (+)= sum_r X[x_rows(r), x_col + m] * Y[y_rows(r), y_col + n]
 // over r in [0, R); X == nullptr means a single column of ones (M = 1, the
@@ -79,7 +79,7 @@ struct TnBatch {
 };
 
 // part: scratch of part_cap floats.
-int tn_launch(const TnBatch& b, float* part, int64_t part_cap, hipStream_t st);
+int tn_launch(const TnBatch& b, float* part, int64_t part_cap, hipStream_t st, const char* tag);
 
 // out[k] += sum_c part[c*stride + k] (k < count), ordered, fp64.
 int reduce_rows_launch(const float* part, int nchunks, int64_t stride, int count, float* out, hipStream_t st);

@@ -496,16 +496,12 @@ int build_graph(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_grap
   CHG_HIP(hipMemsetAsync(g.ginfo, 0, sizeof(GraphInfo), st));
   CHG_HIP(hipMemsetAsync(g.bin_count, 0, sizeof(int) * (nbins_cap + 1), st));
   CHG_HIP(hipMemsetAsync(g.bin_cursor, 0, sizeof(int) * (nbins_cap + 1), st));
-  k_struct_setup<<<1, 256, 0, st>>>(S, batch->atom_ptr, batch->lattice, hp->r_atom, g.info, g.total_bins, g.ginfo);
-  CHG_LAUNCHED("k_struct_setup");
-  k_atom_bin<<<cdiv(N, 256), 256, 0, st>>>(N, S, batch->atom_ptr, batch->pos, batch->Z, g.info, g.atom_struct, g.atom_bin,
-                                           g.atom_cell, g.atom_wrap, g.bin_count, g.ginfo);
-  CHG_LAUNCHED("k_atom_bin");
+  KLAUNCH(st, "k_struct_setup", k_struct_setup<<<1, 256, 0, st>>>(S, batch->atom_ptr, batch->lattice, hp->r_atom, g.info, g.total_bins, g.ginfo));
+  KLAUNCH(st, "k_atom_bin", k_atom_bin<<<cdiv(N, 256), 256, 0, st>>>(N, S, batch->atom_ptr, batch->pos, batch->Z, g.info, g.atom_struct, g.atom_bin,
+                                           g.atom_cell, g.atom_wrap, g.bin_count, g.ginfo));
   // total bins <= N + S (each crystal has at most max(1, n_s) bins)
-  k_scan_single<<<1, 1024, 0, st>>>((int)nbins_cap, g.bin_count, g.bin_start);
-  CHG_LAUNCHED("k_scan_single");
-  k_bin_fill<<<cdiv(N, 256), 256, 0, st>>>(N, g.atom_bin, g.bin_start, g.bin_cursor, g.bin_atoms);
-  CHG_LAUNCHED("k_bin_fill");
+  KLAUNCH(st, "k_scan_single", k_scan_single<<<1, 1024, 0, st>>>((int)nbins_cap, g.bin_count, g.bin_start));
+  KLAUNCH(st, "k_bin_fill", k_bin_fill<<<cdiv(N, 256), 256, 0, st>>>(N, g.atom_bin, g.bin_start, g.bin_cursor, g.bin_atoms));
 
   SearchArgs A;
   A.N = N;
@@ -518,11 +514,9 @@ int build_graph(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_grap
   A.atom_wrap = g.atom_wrap;
   A.bin_start = g.bin_start;
   A.bin_atoms = g.bin_atoms;
-  k_count<<<cdiv(N, 4), 256, 0, st>>>(A, g.edge_count, g.bond_count);
-  CHG_LAUNCHED("k_count");
-  k_scan_counts<<<1, 1024, 0, st>>>(N, g.edge_count, g.bond_count, graph->edge_ptr, graph->bond_ptr, g.angle_base,
-                                    g.ginfo);
-  CHG_LAUNCHED("k_scan_counts");
+  KLAUNCH(st, "k_count", k_count<<<cdiv(N, 4), 256, 0, st>>>(A, g.edge_count, g.bond_count));
+  KLAUNCH(st, "k_scan_counts", k_scan_counts<<<1, 1024, 0, st>>>(N, g.edge_count, g.bond_count, graph->edge_ptr, graph->bond_ptr, g.angle_base,
+                                    g.ginfo));
 
   GraphInfo hinfo;
   CHG_HIP(hipMemcpyAsync(&hinfo, g.ginfo, sizeof(GraphInfo), hipMemcpyDeviceToHost, st));
@@ -552,13 +546,10 @@ int build_graph(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_grap
 
   int sort_size = 64;
   while (sort_size < hinfo.max_count) sort_size <<= 1;
-  k_fill<<<N, 64, sizeof(unsigned long long) * sort_size, st>>>(A, sort_size, graph->edge_ptr, graph->bond_ptr,
-                                                                graph->edge_dst, graph->edge_img, graph->bond_edge);
-  CHG_LAUNCHED("k_fill");
-  k_rev<<<cdiv(N, 4), 256, 0, st>>>(N, graph->edge_ptr, graph->edge_dst, graph->edge_img, graph->edge_rev, g.ginfo);
-  CHG_LAUNCHED("k_rev");
-  k_angles<<<cdiv(N, 256), 256, 0, st>>>(N, graph->bond_ptr, g.angle_base, graph->angle_ptr, graph->angle_b2);
-  CHG_LAUNCHED("k_angles");
+  KLAUNCH(st, "k_fill", k_fill<<<N, 64, sizeof(unsigned long long) * sort_size, st>>>(A, sort_size, graph->edge_ptr, graph->bond_ptr,
+                                                                graph->edge_dst, graph->edge_img, graph->bond_edge));
+  KLAUNCH(st, "k_rev", k_rev<<<cdiv(N, 4), 256, 0, st>>>(N, graph->edge_ptr, graph->edge_dst, graph->edge_img, graph->edge_rev, g.ginfo));
+  KLAUNCH(st, "k_angles", k_angles<<<cdiv(N, 256), 256, 0, st>>>(N, graph->bond_ptr, g.angle_base, graph->angle_ptr, graph->angle_b2));
   return CHGNET_OK;
 }
 

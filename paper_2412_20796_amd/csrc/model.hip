@@ -31,7 +31,7 @@ int validate_batch(const chgnet_batch* b);
 namespace {
 
 constexpr float kLnEps = 1e-5f;
-constexpr int kGateRowsPerBlock = 64;   // rows per block in backward gate kernels
+constexpr int kGateRowsPerBlock = 512;  // rows per block (16 wavefronts) in backward gate kernels
 constexpr int kFreqRowsPerBlock = 256;  // rows per block in frequency-gradient kernel
 constexpr int64_t kTnPartFloats = 16ll << 20;
 
@@ -304,12 +304,12 @@ __global__ void __launch_bounds__(256) k_gate_angle_fwd(int A, const float* __re
 
 // Backward of the atom conv gate: dphi = dm_src * e^a, d e^a += dm_src * phi.
 template <int V>
-__global__ void __launch_bounds__(256) k_gate_atom_bwd(int E, const float* __restrict__ zv, const float* __restrict__ ea,
+__global__ void __launch_bounds__(1024) k_gate_atom_bwd(int E, const float* __restrict__ zv, const float* __restrict__ ea,
                                                        const float* __restrict__ dm, const int* __restrict__ edge_src,
                                                        LnPtrs ln, float* __restrict__ dzv, float* __restrict__ dea,
                                                        float* __restrict__ lnpart) {
   constexpr int D = 64 * V;
-  __shared__ float red[4][4 * D];
+  __shared__ float red[16][4 * D];
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   float acc[4][V];
 #pragma unroll
@@ -317,7 +317,7 @@ __global__ void __launch_bounds__(256) k_gate_atom_bwd(int E, const float* __res
 #pragma unroll
     for (int k = 0; k < V; ++k) acc[a][k] = 0.f;
   const int r0 = blockIdx.x * kGateRowsPerBlock;
-  for (int rr = wave; rr < kGateRowsPerBlock; rr += 4) {
+  for (int rr = wave; rr < kGateRowsPerBlock; rr += 16) {
     const int row = r0 + rr;
     if (row >= E) break;
     GateRow<V> g;
@@ -339,21 +339,24 @@ __global__ void __launch_bounds__(256) k_gate_atom_bwd(int E, const float* __res
 #pragma unroll
     for (int k = 0; k < V; ++k) red[wave][a * D + lane + 64 * k] = acc[a][k];
   __syncthreads();
-  for (int c = threadIdx.x; c < 4 * D; c += 256)
-    lnpart[(int64_t)blockIdx.x * 4 * D + c] = ((red[0][c] + red[1][c]) + red[2][c]) + red[3][c];
+  for (int c = threadIdx.x; c < 4 * D; c += 1024) {
+    float s = 0.f;
+    for (int q = 0; q < 16; ++q) s += red[q][c];
+    lnpart[(int64_t)blockIdx.x * 4 * D + c] = s;
+  }
 }
 
 // Backward of the angle gates. dphi_e = dmu_b1 * eb_b1 * eb_b2;
 // t2 = dmu_b1 * eb_b1 * phi_e (gradient of eb_b2); dphi_a = da'.
 template <int V>
-__global__ void __launch_bounds__(256) k_gate_angle_bwd(int A, const float* __restrict__ zae, int has_angle,
+__global__ void __launch_bounds__(1024) k_gate_angle_bwd(int A, const float* __restrict__ zae, int has_angle,
                                                         const float* __restrict__ eb, const int* __restrict__ ang_b1,
                                                         const int* __restrict__ ang_b2, const float* __restrict__ dmu,
                                                         const float* __restrict__ da_next, LnPtrs lne, LnPtrs lna,
                                                         float* __restrict__ dzae, float* __restrict__ t2,
                                                         float* __restrict__ lnpart) {
   constexpr int D = 64 * V;
-  __shared__ float red[4][4 * D];
+  __shared__ float red[16][4 * D];
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   float acc_e[4][V], acc_a[4][V];
 #pragma unroll
@@ -361,7 +364,7 @@ __global__ void __launch_bounds__(256) k_gate_angle_bwd(int A, const float* __re
 #pragma unroll
     for (int k = 0; k < V; ++k) acc_e[a][k] = acc_a[a][k] = 0.f;
   const int r0 = blockIdx.x * kGateRowsPerBlock;
-  for (int rr = wave; rr < kGateRowsPerBlock; rr += 4) {
+  for (int rr = wave; rr < kGateRowsPerBlock; rr += 16) {
     const int row = r0 + rr;
     if (row >= A) break;
     const float* z = zae + (int64_t)row * 4 * D;
@@ -391,28 +394,40 @@ __global__ void __launch_bounds__(256) k_gate_angle_bwd(int A, const float* __re
 #pragma unroll
       for (int k = 0; k < V; ++k) red[wave][a * D + lane + 64 * k] = half ? acc_a[a][k] : acc_e[a][k];
     __syncthreads();
-    for (int c = threadIdx.x; c < 4 * D; c += 256)
-      lnpart[(int64_t)blockIdx.x * 8 * D + half * 4 * D + c] = ((red[0][c] + red[1][c]) + red[2][c]) + red[3][c];
+    for (int c = threadIdx.x; c < 4 * D; c += 1024) {
+      float s = 0.f;
+      for (int q = 0; q < 16; ++q) s += red[q][c];
+      lnpart[(int64_t)blockIdx.x * 8 * D + half * 4 * D + c] = s;
+    }
     __syncthreads();
   }
 }
 
 // Segmented row sums: out[s] (+)= sum_{r in [ptr[s], ptr[s+1])} vals[idx(r)];
 // optionally out2[s] = mul[s] * sum. One wavefront per segment.
-__global__ void __launch_bounds__(256) k_segsum(int nseg, const int* __restrict__ ptr, const int* __restrict__ idx,
+__global__ void __launch_bounds__(256) k_segsum(int nseg, int ncb, const int* __restrict__ ptr, const int* __restrict__ idx,
                                                 const float* __restrict__ vals, int ld_in, int width, float* __restrict__ out,
                                                 int ld_out, int accumulate, const float* __restrict__ mul, int ld_mul,
                                                 float* __restrict__ out2, int ld_out2) {
-  const int s = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
-  if (s >= nseg) return;
+  const int wid = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  const int s = wid / ncb, c = (wid % ncb) * 64 + lane;
+  if (s >= nseg || c >= width) return;
   const int lo = ptr[s], hi = ptr[s + 1];
-  for (int c = lane; c < width; c += 64) {
-    float acc = 0.f;
-    for (int r = lo; r < hi; ++r) acc += vals[(int64_t)(idx ? idx[r] : r) * ld_in + c];
-    float* o = out + (int64_t)s * ld_out + c;
-    *o = accumulate ? *o + acc : acc;
-    if (out2) out2[(int64_t)s * ld_out2 + c] = mul[(int64_t)s * ld_mul + c] * acc;
+  float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
+  int r = lo;
+  for (; r + 3 < hi; r += 4) {
+    const int64_t i0 = idx ? idx[r] : r, i1 = idx ? idx[r + 1] : r + 1, i2 = idx ? idx[r + 2] : r + 2,
+                  i3 = idx ? idx[r + 3] : r + 3;
+    a0 += vals[i0 * ld_in + c];
+    a1 += vals[i1 * ld_in + c];
+    a2 += vals[i2 * ld_in + c];
+    a3 += vals[i3 * ld_in + c];
   }
+  for (; r < hi; ++r) a0 += vals[(int64_t)(idx ? idx[r] : r) * ld_in + c];
+  const float acc = (a0 + a1) + (a2 + a3);
+  float* o = out + (int64_t)s * ld_out + c;
+  *o = accumulate ? *o + acc : acc;
+  if (out2) out2[(int64_t)s * ld_out2 + c] = mul[(int64_t)s * ld_mul + c] * acc;
 }
 
 // Per bond b (centre i, local index p among k bonds): DZ1 = sum over angles
@@ -495,17 +510,28 @@ __global__ void __launch_bounds__(256) k_struct_heads(int S, const int* __restri
   }
 }
 
-// F_i = sum_e n_e xhat_e, n_e = (m_e + m_rev(e)) / 2.
-__global__ void k_forces(int N, const int* __restrict__ edge_ptr, const int* __restrict__ edge_rev, const float* __restrict__ oF,
-                         const float* __restrict__ xhat, float* __restrict__ forces) {
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+// F_i = sum_e n_e xhat_e, n_e = (m_e + m_rev(e)) / 2; one wavefront per atom,
+// lanes stride over its edges, fixed-order wave reduction.
+__global__ void __launch_bounds__(256) k_forces(int N, const int* __restrict__ edge_ptr, const int* __restrict__ edge_rev,
+                                                const float* __restrict__ oF, const float* __restrict__ xhat,
+                                                float* __restrict__ forces) {
+  const int i = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
   if (i >= N) return;
-  float f[3] = {0.f, 0.f, 0.f};
-  for (int e = edge_ptr[i]; e < edge_ptr[i + 1]; ++e) {
+  float f0 = 0.f, f1 = 0.f, f2 = 0.f;
+  for (int e = edge_ptr[i] + lane; e < edge_ptr[i + 1]; e += 64) {
     const float n = 0.5f * (oF[e] + oF[edge_rev[e]]);
-    for (int c = 0; c < 3; ++c) f[c] += n * xhat[3 * e + c];
+    f0 += n * xhat[3 * e];
+    f1 += n * xhat[3 * e + 1];
+    f2 += n * xhat[3 * e + 2];
   }
-  for (int c = 0; c < 3; ++c) forces[3 * i + c] = f[c];
+  f0 = wsum(f0);
+  f1 = wsum(f1);
+  f2 = wsum(f2);
+  if (lane == 0) {
+    forces[3 * i] = f0;
+    forces[3 * i + 1] = f1;
+    forces[3 * i + 2] = f2;
+  }
 }
 
 // Loss (weighted MSE, per-atom energy) and its gradient; one block.
@@ -754,17 +780,17 @@ void addend(GemmProblem& p, const float* X, int ld, const int* rows) {
   p.nadd++;
 }
 
-int run_gemms(const std::vector<GemmProblem>& ps, hipStream_t st) {
+int run_gemms(const std::vector<GemmProblem>& ps, hipStream_t st, const char* tag) {
   GemmBatch b{};
   for (const auto& p : ps) {
     if (p.M <= 0 || p.N <= 0) continue;
     b.p[b.n++] = p;
     if (b.n == kMaxGemmProblems) {
-      CHG_TRY(gemm_launch(b, st));
+      CHG_TRY(gemm_launch(b, st, tag));
       b.n = 0;
     }
   }
-  if (b.n) CHG_TRY(gemm_launch(b, st));
+  if (b.n) CHG_TRY(gemm_launch(b, st, tag));
   return CHGNET_OK;
 }
 
@@ -787,32 +813,31 @@ TnProblem tp(int64_t R, int M, int Nn, const float* X, int ldx, int x_col, const
   return p;
 }
 
-int run_tns(const std::vector<TnProblem>& ps, const Acts& a, hipStream_t st) {
+int run_tns(const std::vector<TnProblem>& ps, const Acts& a, hipStream_t st, const char* tag) {
   TnBatch b{};
   for (const auto& p : ps) {
     b.p[b.n++] = p;
     if (b.n == kMaxTnProblems) {
-      CHG_TRY(tn_launch(b, a.tnpart, a.tnpart_cap, st));
+      CHG_TRY(tn_launch(b, a.tnpart, a.tnpart_cap, st, tag));
       b.n = 0;
     }
   }
-  if (b.n) CHG_TRY(tn_launch(b, a.tnpart, a.tnpart_cap, st));
+  if (b.n) CHG_TRY(tn_launch(b, a.tnpart, a.tnpart_cap, st, tag));
   return CHGNET_OK;
 }
 
 int fill(float* p, int64_t n, float v, hipStream_t st) {
   if (n <= 0) return CHGNET_OK;
-  k_fill<<<(unsigned)cdiv(n, 256), 256, 0, st>>>(p, n, v);
-  CHG_LAUNCHED("k_fill");
+  KLAUNCH(st, "k_fill", k_fill<<<(unsigned)cdiv(n, 256), 256, 0, st>>>(p, n, v));
   return CHGNET_OK;
 }
 
 int segsum(int64_t nseg, const int* ptr, const int* idx, const float* vals, int ld_in, int width, float* out, int ld_out,
            int accumulate, const float* mul, int ld_mul, float* out2, int ld_out2, hipStream_t st) {
   if (nseg <= 0) return CHGNET_OK;
-  k_segsum<<<(unsigned)cdiv(nseg, 4), 256, 0, st>>>((int)nseg, ptr, idx, vals, ld_in, width, out, ld_out, accumulate, mul,
-                                                    ld_mul, out2, ld_out2);
-  CHG_LAUNCHED("k_segsum");
+  const int ncb = (int)cdiv(width, 64);
+  KLAUNCH(st, "k_segsum", k_segsum<<<(unsigned)cdiv(nseg * ncb, 4), 256, 0, st>>>((int)nseg, ncb, ptr, idx, vals, ld_in, width, out, ld_out,
+                                                          accumulate, mul, ld_mul, out2, ld_out2));
   return CHGNET_OK;
 }
 
@@ -851,12 +876,9 @@ int make_ctx(const chgnet_hparams* hp, const chgnet_batch* batch, const chgnet_g
   return CHGNET_OK;
 }
 
-#define LAUNCH_V(kern, V, grid, block, st, ...)                                  \
-  do {                                                                           \
-    if ((V) == 1) kern<1><<<(grid), (block), 0, (st)>>>(__VA_ARGS__);            \
-    else kern<2><<<(grid), (block), 0, (st)>>>(__VA_ARGS__);                     \
-    CHG_LAUNCHED(#kern);                                                         \
-  } while (0)
+#define LAUNCH_V(kern, V, grid, block, st, ...)                                                    \
+  KLAUNCH(st, #kern, if ((V) == 1) kern<1><<<(grid), (block), 0, (st)>>>(__VA_ARGS__);          \
+                     else kern<2><<<(grid), (block), 0, (st)>>>(__VA_ARGS__))
 
 // ---------------------------------------------------------------------------
 // Forward.
@@ -871,32 +893,25 @@ int forward_impl(Ctx& c, const float* P, float* energy, float* forces, float* st
   const int64_t N = m.N, S = m.S, E = m.E, B = m.B, A = m.A;
 
   // geometry and bases
-  k_atom_struct<<<(unsigned)cdiv(N, 256), 256, 0, st>>>((int)N, (int)S, bt.atom_ptr, a.atom_struct);
-  CHG_LAUNCHED("k_atom_struct");
+  KLAUNCH(st, "k_atom_struct", k_atom_struct<<<(unsigned)cdiv(N, 256), 256, 0, st>>>((int)N, (int)S, bt.atom_ptr, a.atom_struct));
   if (E > 0) {
-    k_prep_edges<<<(unsigned)cdiv(E, 256), 256, 0, st>>>((int)E, (int)N, g.edge_ptr, g.edge_dst, g.edge_img, a.atom_struct,
-                                                         bt.pos, bt.lattice, a.edge_src, a.edge_len, a.edge_xhat);
-    CHG_LAUNCHED("k_prep_edges");
-    k_rbf<<<(unsigned)cdiv(E * m.R, 256), 256, 0, st>>>((int)E, nullptr, a.edge_len, P + L.f_a, m.R, c.hp->r_atom,
-                                                        c.hp->envelope_p, a.rbf_a);
-    CHG_LAUNCHED("k_rbf");
+    KLAUNCH(st, "k_prep_edges", k_prep_edges<<<(unsigned)cdiv(E, 256), 256, 0, st>>>((int)E, (int)N, g.edge_ptr, g.edge_dst, g.edge_img, a.atom_struct,
+                                                         bt.pos, bt.lattice, a.edge_src, a.edge_len, a.edge_xhat));
+    KLAUNCH(st, "k_rbf", k_rbf<<<(unsigned)cdiv(E * m.R, 256), 256, 0, st>>>((int)E, nullptr, a.edge_len, P + L.f_a, m.R, c.hp->r_atom,
+                                                        c.hp->envelope_p, a.rbf_a));
   }
   if (B > 0) {
-    k_prep_bonds<<<(unsigned)cdiv(B, 256), 256, 0, st>>>((int)B, g.bond_edge, a.edge_src, a.bond_src);
-    CHG_LAUNCHED("k_prep_bonds");
-    k_rbf<<<(unsigned)cdiv(B * m.R, 256), 256, 0, st>>>((int)B, g.bond_edge, a.edge_len, P + L.f_b, m.R, c.hp->r_bond,
-                                                        c.hp->envelope_p, a.rbf_b);
-    CHG_LAUNCHED("k_rbf");
+    KLAUNCH(st, "k_prep_bonds", k_prep_bonds<<<(unsigned)cdiv(B, 256), 256, 0, st>>>((int)B, g.bond_edge, a.edge_src, a.bond_src));
+    KLAUNCH(st, "k_rbf", k_rbf<<<(unsigned)cdiv(B * m.R, 256), 256, 0, st>>>((int)B, g.bond_edge, a.edge_len, P + L.f_b, m.R, c.hp->r_bond,
+                                                        c.hp->envelope_p, a.rbf_b));
   }
   if (A > 0) {
-    k_prep_angles<<<(unsigned)cdiv(A, 256), 256, 0, st>>>((int)A, (int)B, g.angle_ptr, g.bond_ptr, g.bond_edge, a.bond_src,
+    KLAUNCH(st, "k_prep_angles", k_prep_angles<<<(unsigned)cdiv(A, 256), 256, 0, st>>>((int)A, (int)B, g.angle_ptr, g.bond_ptr, g.bond_edge, a.bond_src,
                                                           g.edge_dst, g.edge_img, a.atom_struct, bt.pos, bt.lattice, m.K,
-                                                          a.ang_b1, a.ang_b2, a.ang_ctr, a.ft);
-    CHG_LAUNCHED("k_prep_angles");
+                                                          a.ang_b1, a.ang_b2, a.ang_ctr, a.ft));
   }
   // embeddings (Eq. 2)
-  k_embed_v0<<<(unsigned)cdiv(N * D, 256), 256, 0, st>>>((int)N, D, bt.Z, P + L.W_Z, a.v[0]);
-  CHG_LAUNCHED("k_embed_v0");
+  KLAUNCH(st, "k_embed_v0", k_embed_v0<<<(unsigned)cdiv(N * D, 256), 256, 0, st>>>((int)N, D, bt.Z, P + L.W_Z, a.v[0]));
   {
     std::vector<GemmProblem> ps;
     GemmProblem p = gp(E, D, a.e[0], D);
@@ -913,7 +928,7 @@ int forward_impl(Ctx& c, const float* P, float* energy, float* forces, float* st
     seg(p, a.ft, m.K, 0, m.K, P + L.W_th, D, 0);
     p.bias = P + L.b_th;
     ps.push_back(p);
-    CHG_TRY(run_gemms(ps, st));
+    CHG_TRY(run_gemms(ps, st, "gemm_embed"));
   }
 
   for (int t = 0; t < m.T; ++t) {
@@ -940,7 +955,7 @@ int forward_impl(Ctx& c, const float* P, float* energy, float* forces, float* st
       seg(p, a.e[t], D, 0, D, W, 2 * D, 0);
       ps.push_back(p);
     }
-    CHG_TRY(run_gemms(ps, st));
+    CHG_TRY(run_gemms(ps, st, "gemm_proj"));
     ps.clear();
     // edge term + gathered atom terms -> atom conv pre-activation
     {
@@ -960,7 +975,7 @@ int forward_impl(Ctx& c, const float* P, float* energy, float* forces, float* st
         addend(q, a.Xb + (4 + 2 * k) * D, 8 * D, a.ang_b2);
         ps.push_back(q);
       }
-      CHG_TRY(run_gemms(ps, st));
+      CHG_TRY(run_gemms(ps, st, "gemm_z"));
       ps.clear();
     }
     // gates and aggregations
@@ -972,8 +987,7 @@ int forward_impl(Ctx& c, const float* P, float* energy, float* forces, float* st
     CHG_TRY(segsum(B, g.angle_ptr, nullptr, a.msgb, D, D, a.ssum[t], D, 0, a.eb, D, a.mu[t], D, st));
     // updates: v' = v + m Wo + bo; e' = e (+ mu Wo + bo on bonds)
     if (E > 0) {
-      k_copy<<<(unsigned)cdiv(E * D, 256), 256, 0, st>>>(a.e[t + 1], a.e[t], E * D);
-      CHG_LAUNCHED("k_copy");
+      KLAUNCH(st, "k_copy", k_copy<<<(unsigned)cdiv(E * D, 256), 256, 0, st>>>(a.e[t + 1], a.e[t], E * D));
     }
     {
       GemmProblem p = gp(N, D, a.v[t + 1], D);
@@ -990,7 +1004,7 @@ int forward_impl(Ctx& c, const float* P, float* energy, float* forces, float* st
       p.res_rows = g.bond_edge;
       p.c_rows = g.bond_edge;
       ps.push_back(p);
-      CHG_TRY(run_gemms(ps, st));
+      CHG_TRY(run_gemms(ps, st, "gemm_update"));
     }
   }
 
@@ -1013,7 +1027,7 @@ int forward_impl(Ctx& c, const float* P, float* energy, float* forces, float* st
       p.ldc2 = D;
       ps.push_back(p);
     }
-    CHG_TRY(run_gemms(ps, st));
+    CHG_TRY(run_gemms(ps, st, "gemm_head1"));
     ps.clear();
     for (auto& l : ls) {
       GemmProblem p = gp(l.M, D, l.h2, D);
@@ -1024,7 +1038,7 @@ int forward_impl(Ctx& c, const float* P, float* energy, float* forces, float* st
       p.ldc2 = D;
       ps.push_back(p);
     }
-    CHG_TRY(run_gemms(ps, st));
+    CHG_TRY(run_gemms(ps, st, "gemm_head2"));
     ps.clear();
     for (auto& l : ls) {
       GemmProblem p = gp(l.M, l.h->out, l.o, l.h->out);
@@ -1032,12 +1046,10 @@ int forward_impl(Ctx& c, const float* P, float* energy, float* forces, float* st
       p.bias = P + l.h->b3;
       ps.push_back(p);
     }
-    CHG_TRY(run_gemms(ps, st));
+    CHG_TRY(run_gemms(ps, st, "gemm_head3"));
   }
-  k_struct_heads<<<(unsigned)S, 256, 0, st>>>((int)S, bt.atom_ptr, bt.lattice, a.oE, a.oS, energy, stress);
-  CHG_LAUNCHED("k_struct_heads");
-  k_forces<<<(unsigned)cdiv(N, 256), 256, 0, st>>>((int)N, g.edge_ptr, g.edge_rev, a.oF, a.edge_xhat, forces);
-  CHG_LAUNCHED("k_forces");
+  KLAUNCH(st, "k_struct_heads", k_struct_heads<<<(unsigned)S, 256, 0, st>>>((int)S, bt.atom_ptr, bt.lattice, a.oE, a.oS, energy, stress));
+  KLAUNCH(st, "k_forces", k_forces<<<(unsigned)cdiv(N, 4), 256, 0, st>>>((int)N, g.edge_ptr, g.edge_rev, a.oF, a.edge_xhat, forces));
   return CHGNET_OK;
 }
 
@@ -1058,13 +1070,10 @@ int backward_impl(Ctx& c, const float* P, const float* dE, const float* dF, cons
   CHG_TRY(fill(a.deb, B * D, 0.f, st));
 
   // heads
-  k_seed_atoms<<<(unsigned)cdiv(N, 256), 256, 0, st>>>((int)N, a.atom_struct, bt.lattice, dE, dS, a.doE, a.doS);
-  CHG_LAUNCHED("k_seed_atoms");
+  KLAUNCH(st, "k_seed_atoms", k_seed_atoms<<<(unsigned)cdiv(N, 256), 256, 0, st>>>((int)N, a.atom_struct, bt.lattice, dE, dS, a.doE, a.doS));
   if (E > 0) {
-    k_seed_edges<<<(unsigned)cdiv(E, 256), 256, 0, st>>>((int)E, a.edge_src, dF, a.edge_xhat, a.dn);
-    CHG_LAUNCHED("k_seed_edges");
-    k_seed_edges2<<<(unsigned)cdiv(E, 256), 256, 0, st>>>((int)E, g.edge_rev, a.dn, a.doF);
-    CHG_LAUNCHED("k_seed_edges2");
+    KLAUNCH(st, "k_seed_edges", k_seed_edges<<<(unsigned)cdiv(E, 256), 256, 0, st>>>((int)E, a.edge_src, dF, a.edge_xhat, a.dn));
+    KLAUNCH(st, "k_seed_edges2", k_seed_edges2<<<(unsigned)cdiv(E, 256), 256, 0, st>>>((int)E, g.edge_rev, a.dn, a.doF));
   }
   int cur = 0;
   {
@@ -1089,7 +1098,7 @@ int backward_impl(Ctx& c, const float* P, const float* dE, const float* dF, cons
       p.mul_ld = D;
       ps.push_back(p);
     }
-    CHG_TRY(run_gemms(ps, st));
+    CHG_TRY(run_gemms(ps, st, "gemm_head_bwd2"));
     ps.clear();
     for (auto& l : ls) {
       GemmProblem p = gp(l.M, D, l.dh1base + l.dh1col, l.ld1);
@@ -1099,7 +1108,7 @@ int backward_impl(Ctx& c, const float* P, const float* dE, const float* dF, cons
       p.mul_ld = D;
       ps.push_back(p);
     }
-    CHG_TRY(run_gemms(ps, st));
+    CHG_TRY(run_gemms(ps, st, "gemm_head_bwd1"));
     ps.clear();
     {
       GemmProblem p = gp(N, D, a.dv[cur], D);
@@ -1109,7 +1118,7 @@ int backward_impl(Ctx& c, const float* P, const float* dE, const float* dF, cons
       p = gp(E, D, a.de[cur], D);
       seg(p, a.dh1F, D, 0, D, P + hF.W1, D, 1);
       ps.push_back(p);
-      CHG_TRY(run_gemms(ps, st));
+      CHG_TRY(run_gemms(ps, st, "gemm_head_bwd0"));
     }
     std::vector<TnProblem> ts;
     for (auto& l : ls) {
@@ -1123,7 +1132,7 @@ int backward_impl(Ctx& c, const float* P, const float* dE, const float* dF, cons
       ts.push_back(tp(l.M, D, D, l.in, D, 0, nullptr, dh1_base, l.ld1, dh1_col, nullptr, G + l.h->W1, D));
       ts.push_back(tp(l.M, 1, D, nullptr, 0, 0, nullptr, dh1_base, l.ld1, dh1_col, nullptr, G + l.h->b1, D));
     }
-    CHG_TRY(run_tns(ts, a, st));
+    CHG_TRY(run_tns(ts, a, st, "tn_heads"));
   }
 
   // interaction blocks in reverse
@@ -1146,33 +1155,32 @@ int backward_impl(Ctx& c, const float* P, const float* dE, const float* dF, cons
       p.a_rows = g.bond_edge;
       seg(p, a.de[cur], D, 0, D, P + lo.be_Wo, D, 1);
       ps.push_back(p);
-      CHG_TRY(run_gemms(ps, st));
+      CHG_TRY(run_gemms(ps, st, "gemm_out_bwd"));
       ps.clear();
       ts.push_back(tp(N, D, D, a.m[t], D, 0, nullptr, a.dv[cur], D, 0, nullptr, G + lo.av_Wo, D));
       ts.push_back(tp(N, 1, D, nullptr, 0, 0, nullptr, a.dv[cur], D, 0, nullptr, G + lo.av_bo, D));
       ts.push_back(tp(B, D, D, a.mu[t], D, 0, nullptr, a.de[cur], D, 0, g.bond_edge, G + lo.be_Wo, D));
       ts.push_back(tp(B, 1, D, nullptr, 0, 0, nullptr, a.de[cur], D, 0, g.bond_edge, G + lo.be_bo, D));
-      CHG_TRY(run_tns(ts, a, st));
+      CHG_TRY(run_tns(ts, a, st, "tn_out"));
       ts.clear();
     }
     // angle gates
     const int64_t ablocks = cdiv(A, kGateRowsPerBlock);
     if (A > 0) {
-      LAUNCH_V(k_gate_angle_bwd, V, (unsigned)ablocks, 256, st, (int)A, a.zae[t], ang ? 1 : 0, a.eb, a.ang_b1, a.ang_b2,
+      LAUNCH_V(k_gate_angle_bwd, V, (unsigned)ablocks, 1024, st, (int)A, a.zae[t], ang ? 1 : 0, a.eb, a.ang_b1, a.ang_b2,
                a.dmu, a.da[cur], ln_ptrs(P, lo.be), ln_ptrs(P, ang ? lo.an : lo.be), a.dzae, a.t2, a.lnpart);
       CHG_TRY(reduce_rows_launch(a.lnpart, (int)ablocks, 8 * D, 4 * D, G + lo.be.g_c, st));
       if (ang) CHG_TRY(reduce_rows_launch(a.lnpart + 4 * D, (int)ablocks, 8 * D, 4 * D, G + lo.an.g_c, st));
     }
     if (B > 0) {
-      k_bond_bwd_reduce<<<(unsigned)cdiv(B, 4), 256, 0, st>>>((int)B, D, W4, a.bond_src, g.bond_ptr, g.angle_ptr, a.dzae,
-                                                              a.t2, a.dmu, a.ssum[t], a.DZ12, a.deb);
-      CHG_LAUNCHED("k_bond_bwd_reduce");
+      KLAUNCH(st, "k_bond_bwd_reduce", k_bond_bwd_reduce<<<(unsigned)cdiv(B, 4), 256, 0, st>>>((int)B, D, W4, a.bond_src, g.bond_ptr, g.angle_ptr, a.dzae,
+                                                              a.t2, a.dmu, a.ssum[t], a.DZ12, a.deb));
     }
     CHG_TRY(segsum(N, g.bond_ptr, nullptr, a.DZ12, 8 * D, W4, a.AT + 4 * D, 8 * D, 0, nullptr, 0, nullptr, 0, st));
     // atom conv gate
     const int64_t eblocks = cdiv(E, kGateRowsPerBlock);
     if (E > 0) {
-      LAUNCH_V(k_gate_atom_bwd, V, (unsigned)eblocks, 256, st, (int)E, a.zv[t], a.ea, a.dm, a.edge_src, ln_ptrs(P, lo.av),
+      LAUNCH_V(k_gate_atom_bwd, V, (unsigned)eblocks, 1024, st, (int)E, a.zv[t], a.ea, a.dm, a.edge_src, ln_ptrs(P, lo.av),
                a.dzv, a.dea, a.lnpart);
       CHG_TRY(reduce_rows_launch(a.lnpart, (int)eblocks, 4 * D, 4 * D, G + lo.av.g_c, st));
     }
@@ -1201,7 +1209,7 @@ int backward_impl(Ctx& c, const float* P, const float* dE, const float* dF, cons
         p.res_ld = D;
       }
       ps.push_back(p);
-      CHG_TRY(run_gemms(ps, st));
+      CHG_TRY(run_gemms(ps, st, "gemm_in_bwd"));
       ps.clear();
       p = gp(B, D, a.de[nx], D);
       p.c_rows = g.bond_edge;
@@ -1213,7 +1221,7 @@ int backward_impl(Ctx& c, const float* P, const float* dE, const float* dF, cons
         seg(p, a.DZ12, 8 * D, 6 * D, 2 * D, Wan + 2 * D * 2 * D, 2 * D, 1);
       }
       ps.push_back(p);
-      CHG_TRY(run_gemms(ps, st));
+      CHG_TRY(run_gemms(ps, st, "gemm_bond_bwd"));
       ps.clear();
     }
     // weight gradients of the first linear layers
@@ -1232,15 +1240,14 @@ int backward_impl(Ctx& c, const float* P, const float* dE, const float* dF, cons
         ts.push_back(tp(A, D, 2 * D, a.a[t], D, 0, nullptr, a.dzae, 4 * D, 2 * k * D, nullptr, G + go.W + 3 * D * 2 * D, 2 * D));
         ts.push_back(tp(N, 1, 2 * D, nullptr, 0, 0, nullptr, a.AT, 8 * D, (4 + 2 * k) * D, nullptr, G + go.b, 2 * D));
       }
-      CHG_TRY(run_tns(ts, a, st));
+      CHG_TRY(run_tns(ts, a, st, "tn_in"));
       ts.clear();
     }
     cur = nx;
   }
 
   // embeddings
-  k_embed_bwd_Z<<<94, 64, 0, st>>>((int)N, D, bt.Z, a.dv[cur], G + L.W_Z);
-  CHG_LAUNCHED("k_embed_bwd_Z");
+  KLAUNCH(st, "k_embed_bwd_Z", k_embed_bwd_Z<<<94, 64, 0, st>>>((int)N, D, bt.Z, a.dv[cur], G + L.W_Z));
   {
     std::vector<TnProblem> ts;
     ts.push_back(tp(E, m.R, D, a.rbf_a, m.R, 0, nullptr, a.de[cur], D, 0, nullptr, G + L.W_e, 2 * D));
@@ -1249,7 +1256,7 @@ int backward_impl(Ctx& c, const float* P, const float* dE, const float* dF, cons
     ts.push_back(tp(B, m.R, D, a.rbf_b, m.R, 0, nullptr, a.deb, D, 0, nullptr, G + L.W_eb, D));
     ts.push_back(tp(A, m.K, D, a.ft, m.K, 0, nullptr, a.da[cur], D, 0, nullptr, G + L.W_th, D));
     ts.push_back(tp(A, 1, D, nullptr, 0, 0, nullptr, a.da[cur], D, 0, nullptr, G + L.b_th, D));
-    CHG_TRY(run_tns(ts, a, st));
+    CHG_TRY(run_tns(ts, a, st, "tn_embed"));
     std::vector<GemmProblem> ps;
     GemmProblem p = gp(E, m.R, a.drbf_a, m.R);
     seg(p, a.de[cur], D, 0, D, P + L.W_e, 2 * D, 1);
@@ -1258,19 +1265,17 @@ int backward_impl(Ctx& c, const float* P, const float* dE, const float* dF, cons
     p = gp(B, m.R, a.drbf_b, m.R);
     seg(p, a.deb, D, 0, D, P + L.W_eb, D, 1);
     ps.push_back(p);
-    CHG_TRY(run_gemms(ps, st));
+    CHG_TRY(run_gemms(ps, st, "gemm_embed_bwd"));
     if (E > 0) {
       const int64_t nb = cdiv(E, kFreqRowsPerBlock);
-      k_rbf_fgrad<<<(unsigned)nb, 256, 0, st>>>((int)E, nullptr, a.edge_len, P + L.f_a, m.R, c.hp->r_atom,
-                                                c.hp->envelope_p, a.drbf_a, a.fpart);
-      CHG_LAUNCHED("k_rbf_fgrad");
+      KLAUNCH(st, "k_rbf_fgrad", k_rbf_fgrad<<<(unsigned)nb, 256, 0, st>>>((int)E, nullptr, a.edge_len, P + L.f_a, m.R, c.hp->r_atom,
+                                                c.hp->envelope_p, a.drbf_a, a.fpart));
       CHG_TRY(reduce_rows_launch(a.fpart, (int)nb, m.R, m.R, G + L.f_a, st));
     }
     if (B > 0) {
       const int64_t nb = cdiv(B, kFreqRowsPerBlock);
-      k_rbf_fgrad<<<(unsigned)nb, 256, 0, st>>>((int)B, g.bond_edge, a.edge_len, P + L.f_b, m.R, c.hp->r_bond,
-                                                c.hp->envelope_p, a.drbf_b, a.fpart);
-      CHG_LAUNCHED("k_rbf_fgrad");
+      KLAUNCH(st, "k_rbf_fgrad", k_rbf_fgrad<<<(unsigned)nb, 256, 0, st>>>((int)B, g.bond_edge, a.edge_len, P + L.f_b, m.R, c.hp->r_bond,
+                                                c.hp->envelope_p, a.drbf_b, a.fpart));
       CHG_TRY(reduce_rows_launch(a.fpart, (int)nb, m.R, m.R, G + L.f_b, st));
     }
   }
@@ -1317,15 +1322,13 @@ int step_entry(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_graph
   float* f_out = c.a.out_F;
   float* s_out = c.a.out_S;
   CHG_TRY(forward_impl(c, params, e_out, f_out, s_out, st));
-  k_loss<<<1, 256, 0, st>>>((int)c.dm.S, (int)c.dm.N, batch->atom_ptr, e_out, f_out, s_out, E_t, F_t, S_t, loss_w[0],
-                            loss_w[1], loss_w[2], loss, c.a.dE, c.a.dF, c.a.dS);
-  CHG_LAUNCHED("k_loss");
+  KLAUNCH(st, "k_loss", k_loss<<<1, 256, 0, st>>>((int)c.dm.S, (int)c.dm.N, batch->atom_ptr, e_out, f_out, s_out, E_t, F_t, S_t, loss_w[0],
+                            loss_w[1], loss_w[2], loss, c.a.dE, c.a.dF, c.a.dS));
   CHG_TRY(backward_impl(c, params, c.a.dE, c.a.dF, c.a.dS, grad, st));
   if (adam_hp) {
     const float lr = adam_hp[0], b1 = adam_hp[1], b2 = adam_hp[2], eps = adam_hp[3], t = adam_hp[4];
     const float c1 = 1.0f - powf(b1, t), c2 = 1.0f - powf(b2, t);
-    k_adam<<<(unsigned)cdiv(c.L.total, 256), 256, 0, st>>>(c.L.total, params, grad, adam_m, adam_v, lr, b1, b2, eps, c1, c2);
-    CHG_LAUNCHED("k_adam");
+    KLAUNCH(st, "k_adam", k_adam<<<(unsigned)cdiv(c.L.total, 256), 256, 0, st>>>(c.L.total, params, grad, adam_m, adam_v, lr, b1, b2, eps, c1, c2));
   }
   return CHGNET_OK;
 }
