@@ -70,13 +70,17 @@ int validate_hparams(const chgnet_hparams* hp) {
   return CHGNET_OK;
 }
 
-ParamLayout make_layout(const chgnet_hparams& hp) {
+ParamLayout make_layout(const chgnet_hparams& hp, int align) {
   ParamLayout L{};
   const int64_t d = hp.d, R = hp.n_rbf, K = hp.n_fourier;
   int64_t off = 0;
   auto take = [&](int64_t n) {
+    off = (off + align - 1) / align * align;
     int64_t o = off;
     off += n;
+    L.toff[L.ntensors] = o;
+    L.tlen[L.ntensors] = n;
+    L.ntensors++;
     return o;
   };
   L.W_Z = take(94 * d);

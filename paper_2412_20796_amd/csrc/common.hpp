@@ -91,12 +91,17 @@ struct HeadOffsets {
   int out;
 };
 constexpr int kMaxLayers = 16;
+constexpr int kMaxTensors = 24 * kMaxLayers + 32;
 struct ParamLayout {
   int64_t W_Z, f_a, f_b, W_e, b_e0, W_eb, W_th, b_th;
   LayerOffsets layer[kMaxLayers];
   HeadOffsets head[3];  // E, F, S
   int64_t total;
+  int ntensors;                 // every tensor in layout order
+  int64_t toff[kMaxTensors], tlen[kMaxTensors];
 };
-ParamLayout make_layout(const chgnet_hparams& hp);
+// align = 1: the public flat layout; align = 4: every tensor starts on a
+// 16-byte boundary (internal copy used for vector loads of the weights).
+ParamLayout make_layout(const chgnet_hparams& hp, int align = 1);
 
 }  // namespace chg

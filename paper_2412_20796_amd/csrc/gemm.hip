@@ -21,83 +21,175 @@ namespace {
 
 __device__ __forceinline__ float sigm(float x) { return 1.0f / (1.0f + __expf(-x)); }
 
-__global__ void __launch_bounds__(256) k_gemm(GemmBatch batch) {
-  const GemmProblem& P = batch.p[blockIdx.z];
-  const int r0 = blockIdx.x * 64, c0 = blockIdx.y * 64;
-  if (r0 >= P.M || c0 >= P.N) return;
-  __shared__ float As[64][17];
-  __shared__ float Bs[16][68];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wr = (wave >> 1) * 32, wc = (wave & 1) * 32;
-  v4f acc[2][2];
-  for (int a = 0; a < 2; ++a)
-    for (int b = 0; b < 2; ++b) acc[a][b] = v4f{0.f, 0.f, 0.f, 0.f};
-  const int lrow = tid >> 2, lk = (tid & 3) * 4;
-  const int grow = r0 + lrow;
-  const bool rvalid = grow < P.M;
-  const int64_t arow = rvalid ? (P.a_rows ? P.a_rows[grow] : grow) : 0;
-  const int bk = tid >> 4, bc = (tid & 15) * 4;
-  for (int s = 0; s < P.nseg; ++s) {
-    const GemmSeg S = P.seg[s];
-    const float* Arow = S.A + arow * S.lda + S.a_col;
-    for (int k0 = 0; k0 < S.K; k0 += 16) {
+typedef float v16f __attribute__((ext_vector_type(16)));
+
+// Load 4 consecutive floats p[k..k+3] of a row of length K (zero past K).
+__device__ __forceinline__ float4 load4(const float* __restrict__ p, int k, int K, bool vec) {
+  if (vec && k + 3 < K) return *reinterpret_cast<const float4*>(p + k);
+  float4 v;
+  v.x = k < K ? p[k] : 0.f;
+  v.y = k + 1 < K ? p[k + 1] : 0.f;
+  v.z = k + 2 < K ? p[k + 2] : 0.f;
+  v.w = k + 3 < K ? p[k + 3] : 0.f;
+  return v;
+}
+
+// NN product, 128 x BN tile per 256-thread block; wave w owns rows
+// [32w, 32w + 32) and all BN columns as BN/32 tiles of 32x32 (fp32 MFMA
+// 32x32x2). K is streamed through LDS in chunks of 32; the global loads of
+// chunk c+1 are issued into registers before the MFMAs of chunk c.
+// NADD gathered addends are summed in the epilogue; their row indices are
+// staged in LDS once per block.
+template <int BN>
+struct GemmStage {
+  float4 a[4];
+  float4 b[BN / 32];
+};
+
+template <int BN>
+__device__ __forceinline__ void gemm_fetch(const GemmProblem& P, const GemmSeg& S, int k0, int c0, int tid,
+                                           const int64_t (&arow)[4], const bool (&aval)[4], GemmStage<BN>& g) {
+  constexpr int KC = 32;
+  const bool avec = ((S.lda | S.a_col) & 3) == 0 && ((uintptr_t)S.A & 15) == 0;
+  const bool bvec = (S.ldb & 3) == 0 && ((uintptr_t)S.B & 15) == 0;
+  const int ak = (tid & 7) * 4;
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int k = k0 + lk + q;
-        As[lrow][lk + q] = (rvalid && k < S.K) ? Arow[k] : 0.f;
-      }
+  for (int q = 0; q < 4; ++q) {
+    g.a[q] = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (aval[q]) g.a[q] = load4(S.A + arow[q] * S.lda + S.a_col + k0, ak, S.K - k0, avec);
+  }
+  if (!S.trans) {
+    constexpr int CPR = BN / 4;
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int k = k0 + bk, n = c0 + bc + q;
-        float v = 0.f;
-        if (k < S.K && n < P.N) v = S.trans ? S.B[(int64_t)n * S.ldb + k] : S.B[(int64_t)k * S.ldb + n];
-        Bs[bk][bc + q] = v;
-      }
-      __syncthreads();
+    for (int q = 0; q < BN / 32; ++q) {
+      const int idx = tid + 256 * q, kr = idx / CPR, cc = (idx % CPR) * 4;
+      const int k = k0 + kr;
+      g.b[q] = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (k < S.K) g.b[q] = load4(S.B + (int64_t)k * S.ldb + c0, cc, P.N - c0, bvec);
+    }
+  } else {
 #pragma unroll
-      for (int kk = 0; kk < 16; kk += 4) {
-        const float a0 = As[wr + (lane & 15)][kk + (lane >> 4)];
-        const float a1 = As[wr + 16 + (lane & 15)][kk + (lane >> 4)];
-        const float b0 = Bs[kk + (lane >> 4)][wc + (lane & 15)];
-        const float b1 = Bs[kk + (lane >> 4)][wc + 16 + (lane & 15)];
-        acc[0][0] = __builtin_amdgcn_mfma_f32_16x16x4f32(a0, b0, acc[0][0], 0, 0, 0);
-        acc[0][1] = __builtin_amdgcn_mfma_f32_16x16x4f32(a0, b1, acc[0][1], 0, 0, 0);
-        acc[1][0] = __builtin_amdgcn_mfma_f32_16x16x4f32(a1, b0, acc[1][0], 0, 0, 0);
-        acc[1][1] = __builtin_amdgcn_mfma_f32_16x16x4f32(a1, b1, acc[1][1], 0, 0, 0);
-      }
-      __syncthreads();
+    for (int q = 0; q < BN / 32; ++q) {
+      const int idx = tid + 256 * q, n = idx / (KC / 4), kk = (idx % (KC / 4)) * 4;
+      g.b[q] = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (c0 + n < P.N) g.b[q] = load4(S.B + (int64_t)(c0 + n) * S.ldb + k0, kk, S.K - k0, bvec);
     }
   }
+}
+
+template <int BN, int NADD>
+__global__ void __launch_bounds__(256) k_gemm(GemmBatch batch) {
+  constexpr int BM = 128, KC = 32, NT = BN / 32;
+  const GemmProblem& P = batch.p[blockIdx.z];
+  const int r0 = blockIdx.x * BM, c0 = blockIdx.y * BN;
+  if (r0 >= P.M || c0 >= P.N) return;
+  __shared__ float As[BM][KC + 1];
+  __shared__ float Bs[KC][BN + 4];
+  __shared__ int64_t ridx[NADD + 2][BM];  // addend rows, residual row, output row
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  if (tid < BM) {
+    const int row = min(r0 + tid, P.M - 1);
 #pragma unroll
-  for (int ti = 0; ti < 2; ++ti) {
+    for (int q = 0; q < NADD; ++q) ridx[q][tid] = (P.add_rows[q] ? P.add_rows[q][row] : row) * (int64_t)P.add_ld[q];
+    ridx[NADD][tid] = P.res ? (P.res_rows ? P.res_rows[row] : row) * (int64_t)P.res_ld : 0;
+    ridx[NADD + 1][tid] = (P.c_rows ? P.c_rows[row] : row) * (int64_t)P.ldc;
+  }
+  v16f acc[NT];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int row = r0 + wr + ti * 16 + 4 * (lane >> 4) + j;
-      if (row >= P.M) continue;
+  for (int t = 0; t < NT; ++t)
 #pragma unroll
-      for (int tj = 0; tj < 2; ++tj) {
-        const int col = c0 + wc + tj * 16 + (lane & 15);
-        if (col >= P.N) continue;
-        float v = acc[ti][tj][j];
-        if (P.act == ACT_DSILU_MUL) {
-          const float x = P.mul[(int64_t)row * P.mul_ld + col];
-          const float sg = sigm(x);
-          v *= sg * (1.0f + x * (1.0f - sg));
-        }
-        if (P.bias) v += P.bias[col];
-        for (int q = 0; q < P.nadd; ++q) {
-          const int64_t ar = P.add_rows[q] ? P.add_rows[q][row] : row;
-          v += P.add[q][ar * P.add_ld[q] + col];
-        }
-        if (P.res) {
-          const int64_t rr = P.res_rows ? P.res_rows[row] : row;
-          v += P.res[rr * P.res_ld + col];
-        }
-        const int64_t cr = P.c_rows ? P.c_rows[row] : row;
-        float* dst = P.C + cr * P.ldc + col;
-        *dst = P.accumulate ? *dst + v : v;
-        if (P.act == ACT_SILU_OUT) P.C2[(int64_t)row * P.ldc2 + col] = v * sigm(v);
+    for (int j = 0; j < 16; ++j) acc[t][j] = 0.f;
+  const int ar = tid >> 3, ak = (tid & 7) * 4;
+  int64_t arow[4];
+  bool aval[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int r = r0 + ar + 32 * q;
+    aval[q] = r < P.M;
+    arow[q] = aval[q] ? (P.a_rows ? P.a_rows[r] : r) : 0;
+  }
+  GemmStage<BN> g;
+  int s = 0, k0 = 0;
+  if (P.nseg > 0) gemm_fetch<BN>(P, P.seg[0], 0, c0, tid, arow, aval, g);
+  while (s < P.nseg) {
+    const bool trans = P.seg[s].trans;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      As[ar + 32 * q][ak + 0] = g.a[q].x;
+      As[ar + 32 * q][ak + 1] = g.a[q].y;
+      As[ar + 32 * q][ak + 2] = g.a[q].z;
+      As[ar + 32 * q][ak + 3] = g.a[q].w;
+    }
+    if (!trans) {
+      constexpr int CPR = BN / 4;
+#pragma unroll
+      for (int q = 0; q < BN / 32; ++q) {
+        const int idx = tid + 256 * q, kr = idx / CPR, cc = (idx % CPR) * 4;
+        *reinterpret_cast<float4*>(&Bs[kr][cc]) = g.b[q];
       }
+    } else {
+#pragma unroll
+      for (int q = 0; q < BN / 32; ++q) {
+        const int idx = tid + 256 * q, n = idx / (KC / 4), kk = (idx % (KC / 4)) * 4;
+        Bs[kk + 0][n] = g.b[q].x;
+        Bs[kk + 1][n] = g.b[q].y;
+        Bs[kk + 2][n] = g.b[q].z;
+        Bs[kk + 3][n] = g.b[q].w;
+      }
+    }
+    __syncthreads();
+    // next chunk
+    k0 += KC;
+    if (k0 >= P.seg[s].K) {
+      k0 = 0;
+      ++s;
+    }
+    if (s < P.nseg) gemm_fetch<BN>(P, P.seg[s], k0, c0, tid, arow, aval, g);
+#pragma unroll
+    for (int kk = 0; kk < KC; kk += 2) {
+      const float a = As[32 * wave + (lane & 31)][kk + (lane >> 5)];
+#pragma unroll
+      for (int t = 0; t < NT; ++t) {
+        const float b = Bs[kk + (lane >> 5)][32 * t + (lane & 31)];
+        acc[t] = __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, acc[t], 0, 0, 0);
+      }
+    }
+    __syncthreads();
+  }
+  __syncthreads();
+  // epilogue: acc[t][j] is C(row, col) with row = 8(j/4) + 4(lane/32) + j%4
+  float bias[NT];
+#pragma unroll
+  for (int t = 0; t < NT; ++t) {
+    const int col = c0 + 32 * t + (lane & 31);
+    bias[t] = (P.bias && col < P.N) ? P.bias[col] : 0.f;
+  }
+#pragma unroll
+  for (int j = 0; j < 16; ++j) {
+    const int lr = 32 * wave + 8 * (j >> 2) + 4 * (lane >> 5) + (j & 3);
+    const int row = r0 + lr;
+    if (row >= P.M) continue;
+    int64_t addr[NADD > 0 ? NADD : 1];
+#pragma unroll
+    for (int q = 0; q < NADD; ++q) addr[q] = ridx[q][lr];
+    const int64_t rr = ridx[NADD][lr], cr = ridx[NADD + 1][lr];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+      const int col = c0 + 32 * t + (lane & 31);
+      if (col >= P.N) continue;
+      float v = acc[t][j];
+      if (P.act == ACT_DSILU_MUL) {
+        const float x = P.mul[(int64_t)row * P.mul_ld + col];
+        const float sg = sigm(x);
+        v *= sg * (1.0f + x * (1.0f - sg));
+      }
+      v += bias[t];
+#pragma unroll
+      for (int q = 0; q < NADD; ++q) v += P.add[q][addr[q] + col];
+      if (P.res) v += P.res[rr + col];
+      float* dst = P.C + cr + col;
+      *dst = P.accumulate ? *dst + v : v;
+      if (P.act == ACT_SILU_OUT) P.C2[(int64_t)row * P.ldc2 + col] = v * sigm(v);
     }
   }
 }
@@ -115,63 +207,90 @@ struct TnLaunch {
   TnPlan q[kMaxTnProblems];
 };
 
+// Split-K X^T Y: a 64 x 128 output tile per block (waves in a 2 x 2 grid,
+// 32 x 64 each as two 32x32 MFMA tiles), rows streamed 32 at a time.
 __global__ void __launch_bounds__(256) k_tn(TnLaunch L, float* __restrict__ part) {
+  constexpr int TM = 64, TN = 128, RC = 32;
   const TnPlan& Q = L.q[blockIdx.z];
   const TnProblem& P = Q.p;
   const int chunk = blockIdx.x;
   if (chunk >= Q.nchunks || (int)blockIdx.y >= Q.tiles) return;
-  const int m0 = (blockIdx.y / Q.tiles_n) * 64, n0 = (blockIdx.y % Q.tiles_n) * 64;
+  const int m0 = (blockIdx.y / Q.tiles_n) * TM, n0 = (blockIdx.y % Q.tiles_n) * TN;
   const int rlo = chunk * Q.rpc;
   const int rhi = min(P.R, rlo + Q.rpc);
-  __shared__ float Xs[16][68];
-  __shared__ float Ys[16][68];
+  __shared__ float Xs[RC][TM + 4];
+  __shared__ float Ys[RC][TN + 4];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = (wave >> 1) * 32, wn = (wave & 1) * 32;
-  v4f acc[2][2];
-  for (int a = 0; a < 2; ++a)
-    for (int b = 0; b < 2; ++b) acc[a][b] = v4f{0.f, 0.f, 0.f, 0.f};
-  const int lr = tid >> 4, lc = (tid & 15) * 4;
-  for (int r0 = rlo; r0 < rhi; r0 += 16) {
-    const int r = r0 + lr;
-    const bool rv = r < rhi;
-    const int64_t xr = rv ? (P.x_rows ? P.x_rows[r] : r) : 0;
-    const int64_t yr = rv ? (P.y_rows ? P.y_rows[r] : r) : 0;
+  const int wm = (wave >> 1) * 32, wn = (wave & 1) * 64;
+  v16f acc[2];
+#pragma unroll
+  for (int t = 0; t < 2; ++t)
+#pragma unroll
+    for (int j = 0; j < 16; ++j) acc[t][j] = 0.f;
+  const bool xvec = P.X && ((P.ldx | P.x_col) & 3) == 0 && ((uintptr_t)P.X & 15) == 0;
+  const bool yvec = ((P.ldy | P.y_col) & 3) == 0 && ((uintptr_t)P.Y & 15) == 0;
+  float4 xs[2], ys[4];
+  auto fetch = [&](int rb) {
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      const int idx = tid + 256 * q, lr = idx >> 4, cc = (idx & 15) * 4, r = rb + lr;
+      float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (r < rhi) {
+        if (P.X) {
+          const int64_t xr = P.x_rows ? P.x_rows[r] : r;
+          v = load4(P.X + xr * P.ldx + P.x_col + m0, cc, P.M - m0, xvec);
+        } else if (m0 == 0 && cc == 0) {
+          v.x = 1.0f;
+        }
+      }
+      xs[q] = v;
+    }
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-      const int m = m0 + lc + q, n = n0 + lc + q;
-      float xv = 0.f, yv = 0.f;
-      if (rv && m < P.M) xv = P.X ? P.X[xr * P.ldx + P.x_col + m] : 1.0f;
-      if (rv && n < P.N) yv = P.Y[yr * P.ldy + P.y_col + n];
-      Xs[lr][lc + q] = xv;
-      Ys[lr][lc + q] = yv;
+      const int idx = tid + 256 * q, lr = idx >> 5, cc = (idx & 31) * 4, r = rb + lr;
+      float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (r < rhi) {
+        const int64_t yr = P.y_rows ? P.y_rows[r] : r;
+        v = load4(P.Y + yr * P.ldy + P.y_col + n0, cc, P.N - n0, yvec);
+      }
+      ys[q] = v;
+    }
+  };
+  if (rlo < rhi) fetch(rlo);
+  for (int rb = rlo; rb < rhi; rb += RC) {
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      const int idx = tid + 256 * q;
+      *reinterpret_cast<float4*>(&Xs[idx >> 4][(idx & 15) * 4]) = xs[q];
+    }
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int idx = tid + 256 * q;
+      *reinterpret_cast<float4*>(&Ys[idx >> 5][(idx & 31) * 4]) = ys[q];
     }
     __syncthreads();
+    if (rb + RC < rhi) fetch(rb + RC);
 #pragma unroll
-    for (int kk = 0; kk < 16; kk += 4) {
-      const float a0 = Xs[kk + (lane >> 4)][wm + (lane & 15)];
-      const float a1 = Xs[kk + (lane >> 4)][wm + 16 + (lane & 15)];
-      const float b0 = Ys[kk + (lane >> 4)][wn + (lane & 15)];
-      const float b1 = Ys[kk + (lane >> 4)][wn + 16 + (lane & 15)];
-      acc[0][0] = __builtin_amdgcn_mfma_f32_16x16x4f32(a0, b0, acc[0][0], 0, 0, 0);
-      acc[0][1] = __builtin_amdgcn_mfma_f32_16x16x4f32(a0, b1, acc[0][1], 0, 0, 0);
-      acc[1][0] = __builtin_amdgcn_mfma_f32_16x16x4f32(a1, b0, acc[1][0], 0, 0, 0);
-      acc[1][1] = __builtin_amdgcn_mfma_f32_16x16x4f32(a1, b1, acc[1][1], 0, 0, 0);
+    for (int kk = 0; kk < RC; kk += 2) {
+      const float a = Xs[kk + (lane >> 5)][wm + (lane & 31)];
+      const float b0 = Ys[kk + (lane >> 5)][wn + (lane & 31)];
+      const float b1 = Ys[kk + (lane >> 5)][wn + 32 + (lane & 31)];
+      acc[0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a, b0, acc[0], 0, 0, 0);
+      acc[1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a, b1, acc[1], 0, 0, 0);
     }
     __syncthreads();
   }
   float* out = part + Q.off + (int64_t)chunk * P.M * P.N;
 #pragma unroll
-  for (int ti = 0; ti < 2; ++ti)
+  for (int j = 0; j < 16; ++j) {
+    const int m = m0 + wm + 8 * (j >> 2) + 4 * (lane >> 5) + (j & 3);
+    if (m >= P.M) continue;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int m = m0 + wm + ti * 16 + 4 * (lane >> 4) + j;
-      if (m >= P.M) continue;
-#pragma unroll
-      for (int tj = 0; tj < 2; ++tj) {
-        const int n = n0 + wn + tj * 16 + (lane & 15);
-        if (n < P.N) out[(int64_t)m * P.N + n] = acc[ti][tj][j];
-      }
+    for (int t = 0; t < 2; ++t) {
+      const int n = n0 + wn + 32 * t + (lane & 31);
+      if (n < P.N) out[(int64_t)m * P.N + n] = acc[t][j];
     }
+  }
 }
 
 // Ordered column sums of chunk partials: 16 wavefronts per block, wave w
@@ -223,14 +342,36 @@ __global__ void __launch_bounds__(1024) k_reduce_rows(const float* __restrict__ 
 
 }  // namespace
 
-int gemm_launch(const GemmBatch& b, hipStream_t st, const char* tag) {
-  int gx = 0, gy = 0;
-  for (int i = 0; i < b.n; ++i) {
-    gx = std::max<int>(gx, (int)cdiv(b.p[i].M, 64));
-    gy = std::max<int>(gy, (int)cdiv(b.p[i].N, 64));
+template <int BN>
+int gemm_launch_bn(const GemmBatch& b, int nadd, dim3 grid, hipStream_t st, const char* tag) {
+  switch (nadd) {
+    case 0: KLAUNCH(st, tag, k_gemm<BN, 0><<<grid, 256, 0, st>>>(b)); break;
+    case 1: KLAUNCH(st, tag, k_gemm<BN, 1><<<grid, 256, 0, st>>>(b)); break;
+    case 2: KLAUNCH(st, tag, k_gemm<BN, 2><<<grid, 256, 0, st>>>(b)); break;
+    default: KLAUNCH(st, tag, k_gemm<BN, 3><<<grid, 256, 0, st>>>(b)); break;
   }
-  if (b.n == 0 || gx == 0 || gy == 0) return CHGNET_OK;
-  KLAUNCH(st, tag, k_gemm<<<dim3(gx, gy, b.n), 256, 0, st>>>(b));
+  return CHGNET_OK;
+}
+
+int gemm_launch(const GemmBatch& b, hipStream_t st, const char* tag) {
+  // problems with different addend counts go to separate launches
+  for (int nadd = 0; nadd <= 3; ++nadd) {
+    GemmBatch g{};
+    for (int i = 0; i < b.n; ++i)
+      if (b.p[i].nadd == nadd) g.p[g.n++] = b.p[i];
+    if (g.n == 0) continue;
+    int minN = 1 << 30;
+    for (int i = 0; i < g.n; ++i) minN = std::min(minN, g.p[i].N);
+    const int BN = minN >= 128 ? 128 : 64;
+    int gx = 0, gy = 0;
+    for (int i = 0; i < g.n; ++i) {
+      gx = std::max<int>(gx, (int)cdiv(g.p[i].M, 128));
+      gy = std::max<int>(gy, (int)cdiv(g.p[i].N, BN));
+    }
+    if (gx == 0 || gy == 0) continue;
+    const dim3 grid(gx, gy, g.n);
+    CHG_TRY(BN == 128 ? gemm_launch_bn<128>(g, nadd, grid, st, tag) : gemm_launch_bn<64>(g, nadd, grid, st, tag));
+  }
   return CHGNET_OK;
 }
 
@@ -244,14 +385,14 @@ int tn_launch(const TnBatch& b, float* part, int64_t part_cap, hipStream_t st, c
     TnPlan& q = L.q[i];
     q.p = b.p[i];
     const int tm = (int)cdiv(q.p.M, 64);
-    q.tiles_n = (int)cdiv(q.p.N, 64);
+    q.tiles_n = (int)cdiv(q.p.N, 128);
     q.tiles = tm * q.tiles_n;
     const int64_t mn = (int64_t)q.p.M * q.p.N;
     int64_t nch = std::max<int64_t>(1, std::min<int64_t>(cdiv(q.p.R, 256), std::max(8, 512 / q.tiles)));
     nch = std::min<int64_t>(nch, 128);
     nch = std::min<int64_t>(nch, std::max<int64_t>(1, budget / std::max<int64_t>(1, mn)));
-    int64_t rpc = cdiv(cdiv(q.p.R, nch), 16) * 16;
-    if (rpc < 16) rpc = 16;
+    int64_t rpc = cdiv(cdiv(q.p.R, nch), 32) * 32;
+    if (rpc < 32) rpc = 32;
     q.rpc = (int)rpc;
     q.nchunks = q.p.R > 0 ? (int)cdiv(q.p.R, rpc) : 0;
     q.off = off;

@@ -59,6 +59,18 @@ __global__ void k_fill(float* __restrict__ p, int64_t n, float v) {
   if (i < n) p[i] = v;
 }
 
+struct PackTable {
+  int n;
+  int src[96], dst[96], len[96];
+};
+
+// Copy of the flat parameters with every tensor on a 16-byte boundary.
+__global__ void k_pack_params(PackTable t, const float* __restrict__ src, float* __restrict__ dst) {
+  if ((int)blockIdx.x >= t.n) return;
+  const int s = t.src[blockIdx.x], d = t.dst[blockIdx.x], n = t.len[blockIdx.x];
+  for (int i = threadIdx.x; i < n; i += blockDim.x) dst[d + i] = src[s + i];
+}
+
 __global__ void k_copy(float* __restrict__ dst, const float* __restrict__ src, int64_t n) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i < n) dst[i] = src[i];
@@ -670,14 +682,15 @@ struct Acts {
   // backward
   float *dv[2], *de[2], *da[2], *dm, *dmu, *dzv, *dzae, *t2, *AT, *DZ12, *dea, *deb;
   float *doE, *doS, *dn, *doF, *dh2E, *dh2S, *dh2F, *dh1ES, *dh1F, *drbf_a, *drbf_b;
-  float *lnpart, *tnpart, *fpart;
+  float *lnpart, *tnpart, *fpart, *Pal;
   int64_t tnpart_cap;
   // loss
   float *dE, *dF, *dS, *out_E, *out_F, *out_S;
 };
 
-void carve_acts(Arena& ar, const Dims& m, Acts& a) {
+void carve_acts(Arena& ar, const Dims& m, Acts& a, int64_t n_params_aligned) {
   const int64_t N = m.N, S = m.S, E = m.E, B = m.B, A = m.A, D = m.D, R = m.R, K = m.K;
+  a.Pal = ar.take<float>(n_params_aligned);
   a.atom_struct = ar.take<int>(N);
   a.edge_src = ar.take<int>(E);
   a.bond_src = ar.take<int>(B);
@@ -841,6 +854,19 @@ int segsum(int64_t nseg, const int* ptr, const int* idx, const float* vals, int 
   return CHGNET_OK;
 }
 
+int pack_params(const ParamLayout& L, const ParamLayout& La, const float* P, float* Pal, hipStream_t st) {
+  for (int k0 = 0; k0 < L.ntensors; k0 += 96) {
+    PackTable t{};
+    for (int k = k0; k < L.ntensors && t.n < 96; ++k, ++t.n) {
+      t.src[t.n] = (int)L.toff[k];
+      t.dst[t.n] = (int)La.toff[k];
+      t.len[t.n] = (int)L.tlen[k];
+    }
+    KLAUNCH(st, "k_pack_params", k_pack_params<<<t.n, 256, 0, st>>>(t, P, Pal));
+  }
+  return CHGNET_OK;
+}
+
 LnPtrs ln_ptrs(const float* P, const GatedOffsets& g) { return LnPtrs{P + g.g_c, P + g.b_c, P + g.g_g, P + g.b_g}; }
 
 struct Ctx {
@@ -848,7 +874,8 @@ struct Ctx {
   const chgnet_batch* batch;
   const chgnet_graph* graph;
   Dims dm;
-  ParamLayout L;
+  ParamLayout L;   // public layout (gradients)
+  ParamLayout La;  // aligned layout of the internal weight copy (reads)
   Acts a;
 };
 
@@ -868,10 +895,11 @@ int make_ctx(const chgnet_hparams* hp, const chgnet_batch* batch, const chgnet_g
   c.graph = graph;
   c.dm = Dims{batch->n_atoms, batch->n_struct, graph->n_edges, graph->n_bonds, graph->n_angles,
               hp->d, hp->n_layers, hp->n_rbf, hp->n_fourier};
-  c.L = make_layout(*hp);
+  c.L = make_layout(*hp, 1);
+  c.La = make_layout(*hp, 4);
   Arena ar{static_cast<char*>(ws), ws_bytes, 0};
   ar.used = graph_scratch_bytes(c.dm.N, c.dm.S);
-  carve_acts(ar, c.dm, c.a);
+  carve_acts(ar, c.dm, c.a, c.La.total);
   if (!ws || !ar.ok()) return fail(CHGNET_EWORKSPACE, "workspace too small (query chgnet_workspace_size)");
   return CHGNET_OK;
 }
@@ -883,10 +911,12 @@ int make_ctx(const chgnet_hparams* hp, const chgnet_batch* batch, const chgnet_g
 // ---------------------------------------------------------------------------
 // Forward.
 // ---------------------------------------------------------------------------
-int forward_impl(Ctx& c, const float* P, float* energy, float* forces, float* stress, hipStream_t st) {
+int forward_impl(Ctx& c, const float* Pflat, float* energy, float* forces, float* stress, hipStream_t st) {
   const Dims& m = c.dm;
   Acts& a = c.a;
-  const ParamLayout& L = c.L;
+  const ParamLayout& L = c.La;
+  CHG_TRY(pack_params(c.L, c.La, Pflat, a.Pal, st));
+  const float* P = a.Pal;
   const chgnet_graph& g = *c.graph;
   const chgnet_batch& bt = *c.batch;
   const int D = m.D, V = D / 64;
@@ -1056,16 +1086,20 @@ int forward_impl(Ctx& c, const float* P, float* energy, float* forces, float* st
 // ---------------------------------------------------------------------------
 // Backward (weights only).
 // ---------------------------------------------------------------------------
-int backward_impl(Ctx& c, const float* P, const float* dE, const float* dF, const float* dS, float* G, hipStream_t st) {
+int backward_impl(Ctx& c, const float* Pflat, bool repack, const float* dE, const float* dF, const float* dS, float* G,
+                  hipStream_t st) {
   const Dims& m = c.dm;
   Acts& a = c.a;
-  const ParamLayout& L = c.L;
+  const ParamLayout& L = c.La;   // reads from the aligned weight copy
+  const ParamLayout& Lg = c.L;   // gradients in the public layout
+  if (repack) CHG_TRY(pack_params(c.L, c.La, Pflat, a.Pal, st));
+  const float* P = a.Pal;
   const chgnet_graph& g = *c.graph;
   const chgnet_batch& bt = *c.batch;
   const int D = m.D, V = D / 64;
   const int64_t N = m.N, E = m.E, B = m.B, A = m.A;
 
-  CHG_TRY(fill(G, L.total, 0.f, st));
+  CHG_TRY(fill(G, Lg.total, 0.f, st));
   CHG_TRY(fill(a.dea, E * D, 0.f, st));
   CHG_TRY(fill(a.deb, B * D, 0.f, st));
 
@@ -1082,13 +1116,14 @@ int backward_impl(Ctx& c, const float* P, const float* dE, const float* dF, cons
       const float* in;
       int64_t M;
       const HeadOffsets* h;
+      const HeadOffsets* hg;
       const float *h1, *a1, *h2, *a2, *dout;
       float *dh2, *dh1base;
       int dh1col, ld1;
     };
-    Lay ls[3] = {{a.v[m.T], N, &hE, a.hE1, a.aE1, a.hE2, a.aE2, a.doE, a.dh2E, a.dh1ES, 0, 2 * D},
-                 {a.v[m.T], N, &hS, a.hS1, a.aS1, a.hS2, a.aS2, a.doS, a.dh2S, a.dh1ES, D, 2 * D},
-                 {a.e[m.T], E, &hF, a.hF1, a.aF1, a.hF2, a.aF2, a.doF, a.dh2F, a.dh1F, 0, D}};
+    Lay ls[3] = {{a.v[m.T], N, &hE, &Lg.head[0], a.hE1, a.aE1, a.hE2, a.aE2, a.doE, a.dh2E, a.dh1ES, 0, 2 * D},
+                 {a.v[m.T], N, &hS, &Lg.head[2], a.hS1, a.aS1, a.hS2, a.aS2, a.doS, a.dh2S, a.dh1ES, D, 2 * D},
+                 {a.e[m.T], E, &hF, &Lg.head[1], a.hF1, a.aF1, a.hF2, a.aF2, a.doF, a.dh2F, a.dh1F, 0, D}};
     std::vector<GemmProblem> ps;
     for (auto& l : ls) {
       GemmProblem p = gp(l.M, D, l.dh2, D);
@@ -1125,12 +1160,12 @@ int backward_impl(Ctx& c, const float* P, const float* dE, const float* dF, cons
       const int o = l.h->out;
       const float* dh1_base = l.dh1base;
       const int dh1_col = l.dh1col;
-      ts.push_back(tp(l.M, D, o, l.a2, D, 0, nullptr, l.dout, o, 0, nullptr, G + l.h->W3, o));
-      ts.push_back(tp(l.M, 1, o, nullptr, 0, 0, nullptr, l.dout, o, 0, nullptr, G + l.h->b3, o));
-      ts.push_back(tp(l.M, D, D, l.a1, D, 0, nullptr, l.dh2, D, 0, nullptr, G + l.h->W2, D));
-      ts.push_back(tp(l.M, 1, D, nullptr, 0, 0, nullptr, l.dh2, D, 0, nullptr, G + l.h->b2, D));
-      ts.push_back(tp(l.M, D, D, l.in, D, 0, nullptr, dh1_base, l.ld1, dh1_col, nullptr, G + l.h->W1, D));
-      ts.push_back(tp(l.M, 1, D, nullptr, 0, 0, nullptr, dh1_base, l.ld1, dh1_col, nullptr, G + l.h->b1, D));
+      ts.push_back(tp(l.M, D, o, l.a2, D, 0, nullptr, l.dout, o, 0, nullptr, G + l.hg->W3, o));
+      ts.push_back(tp(l.M, 1, o, nullptr, 0, 0, nullptr, l.dout, o, 0, nullptr, G + l.hg->b3, o));
+      ts.push_back(tp(l.M, D, D, l.a1, D, 0, nullptr, l.dh2, D, 0, nullptr, G + l.hg->W2, D));
+      ts.push_back(tp(l.M, 1, D, nullptr, 0, 0, nullptr, l.dh2, D, 0, nullptr, G + l.hg->b2, D));
+      ts.push_back(tp(l.M, D, D, l.in, D, 0, nullptr, dh1_base, l.ld1, dh1_col, nullptr, G + l.hg->W1, D));
+      ts.push_back(tp(l.M, 1, D, nullptr, 0, 0, nullptr, dh1_base, l.ld1, dh1_col, nullptr, G + l.hg->b1, D));
     }
     CHG_TRY(run_tns(ts, a, st, "tn_heads"));
   }
@@ -1138,6 +1173,7 @@ int backward_impl(Ctx& c, const float* P, const float* dE, const float* dF, cons
   // interaction blocks in reverse
   for (int t = m.T - 1; t >= 0; --t) {
     const LayerOffsets& lo = L.layer[t];
+    const LayerOffsets& lg = Lg.layer[t];
     const bool ang = lo.has_angle;
     const int W4 = ang ? 4 * D : 2 * D;
     const float* Wav = P + lo.av.W;
@@ -1157,10 +1193,10 @@ int backward_impl(Ctx& c, const float* P, const float* dE, const float* dF, cons
       ps.push_back(p);
       CHG_TRY(run_gemms(ps, st, "gemm_out_bwd"));
       ps.clear();
-      ts.push_back(tp(N, D, D, a.m[t], D, 0, nullptr, a.dv[cur], D, 0, nullptr, G + lo.av_Wo, D));
-      ts.push_back(tp(N, 1, D, nullptr, 0, 0, nullptr, a.dv[cur], D, 0, nullptr, G + lo.av_bo, D));
-      ts.push_back(tp(B, D, D, a.mu[t], D, 0, nullptr, a.de[cur], D, 0, g.bond_edge, G + lo.be_Wo, D));
-      ts.push_back(tp(B, 1, D, nullptr, 0, 0, nullptr, a.de[cur], D, 0, g.bond_edge, G + lo.be_bo, D));
+      ts.push_back(tp(N, D, D, a.m[t], D, 0, nullptr, a.dv[cur], D, 0, nullptr, G + lg.av_Wo, D));
+      ts.push_back(tp(N, 1, D, nullptr, 0, 0, nullptr, a.dv[cur], D, 0, nullptr, G + lg.av_bo, D));
+      ts.push_back(tp(B, D, D, a.mu[t], D, 0, nullptr, a.de[cur], D, 0, g.bond_edge, G + lg.be_Wo, D));
+      ts.push_back(tp(B, 1, D, nullptr, 0, 0, nullptr, a.de[cur], D, 0, g.bond_edge, G + lg.be_bo, D));
       CHG_TRY(run_tns(ts, a, st, "tn_out"));
       ts.clear();
     }
@@ -1169,8 +1205,8 @@ int backward_impl(Ctx& c, const float* P, const float* dE, const float* dF, cons
     if (A > 0) {
       LAUNCH_V(k_gate_angle_bwd, V, (unsigned)ablocks, 1024, st, (int)A, a.zae[t], ang ? 1 : 0, a.eb, a.ang_b1, a.ang_b2,
                a.dmu, a.da[cur], ln_ptrs(P, lo.be), ln_ptrs(P, ang ? lo.an : lo.be), a.dzae, a.t2, a.lnpart);
-      CHG_TRY(reduce_rows_launch(a.lnpart, (int)ablocks, 8 * D, 4 * D, G + lo.be.g_c, st));
-      if (ang) CHG_TRY(reduce_rows_launch(a.lnpart + 4 * D, (int)ablocks, 8 * D, 4 * D, G + lo.an.g_c, st));
+      CHG_TRY(reduce_rows_launch(a.lnpart, (int)ablocks, 8 * D, 4 * D, G + lg.be.g_c, st));
+      if (ang) CHG_TRY(reduce_rows_launch(a.lnpart + 4 * D, (int)ablocks, 8 * D, 4 * D, G + lg.an.g_c, st));
     }
     if (B > 0) {
       KLAUNCH(st, "k_bond_bwd_reduce", k_bond_bwd_reduce<<<(unsigned)cdiv(B, 4), 256, 0, st>>>((int)B, D, W4, a.bond_src, g.bond_ptr, g.angle_ptr, a.dzae,
@@ -1182,7 +1218,7 @@ int backward_impl(Ctx& c, const float* P, const float* dE, const float* dF, cons
     if (E > 0) {
       LAUNCH_V(k_gate_atom_bwd, V, (unsigned)eblocks, 1024, st, (int)E, a.zv[t], a.ea, a.dm, a.edge_src, ln_ptrs(P, lo.av),
                a.dzv, a.dea, a.lnpart);
-      CHG_TRY(reduce_rows_launch(a.lnpart, (int)eblocks, 4 * D, 4 * D, G + lo.av.g_c, st));
+      CHG_TRY(reduce_rows_launch(a.lnpart, (int)eblocks, 4 * D, 4 * D, G + lg.av.g_c, st));
     }
     CHG_TRY(segsum(N, g.edge_ptr, nullptr, a.dzv, 2 * D, 2 * D, a.AT, 8 * D, 0, nullptr, 0, nullptr, 0, st));
     CHG_TRY(segsum(N, g.edge_ptr, g.edge_rev, a.dzv, 2 * D, 2 * D, a.AT + 2 * D, 8 * D, 0, nullptr, 0, nullptr, 0, st));
@@ -1228,12 +1264,12 @@ int backward_impl(Ctx& c, const float* P, const float* dE, const float* dF, cons
     {
       const float* vt = a.v[t];
       const float* et = a.e[t];
-      ts.push_back(tp(N, D, 2 * D, vt, D, 0, nullptr, a.AT, 8 * D, 0, nullptr, G + lo.av.W, 2 * D));
-      ts.push_back(tp(N, D, 2 * D, vt, D, 0, nullptr, a.AT, 8 * D, 2 * D, nullptr, G + lo.av.W + D * 2 * D, 2 * D));
-      ts.push_back(tp(E, D, 2 * D, et, D, 0, nullptr, a.dzv, 2 * D, 0, nullptr, G + lo.av.W + 2 * D * 2 * D, 2 * D));
-      ts.push_back(tp(N, 1, 2 * D, nullptr, 0, 0, nullptr, a.AT, 8 * D, 0, nullptr, G + lo.av.b, 2 * D));
+      ts.push_back(tp(N, D, 2 * D, vt, D, 0, nullptr, a.AT, 8 * D, 0, nullptr, G + lg.av.W, 2 * D));
+      ts.push_back(tp(N, D, 2 * D, vt, D, 0, nullptr, a.AT, 8 * D, 2 * D, nullptr, G + lg.av.W + D * 2 * D, 2 * D));
+      ts.push_back(tp(E, D, 2 * D, et, D, 0, nullptr, a.dzv, 2 * D, 0, nullptr, G + lg.av.W + 2 * D * 2 * D, 2 * D));
+      ts.push_back(tp(N, 1, 2 * D, nullptr, 0, 0, nullptr, a.AT, 8 * D, 0, nullptr, G + lg.av.b, 2 * D));
       for (int k = 0; k < (ang ? 2 : 1); ++k) {
-        const GatedOffsets& go = k ? lo.an : lo.be;
+        const GatedOffsets& go = k ? lg.an : lg.be;
         ts.push_back(tp(N, D, 2 * D, vt, D, 0, nullptr, a.AT, 8 * D, (4 + 2 * k) * D, nullptr, G + go.W, 2 * D));
         ts.push_back(tp(B, D, 2 * D, et, D, 0, g.bond_edge, a.DZ12, 8 * D, 2 * k * D, nullptr, G + go.W + D * 2 * D, 2 * D));
         ts.push_back(tp(B, D, 2 * D, et, D, 0, g.bond_edge, a.DZ12, 8 * D, (4 + 2 * k) * D, nullptr, G + go.W + 2 * D * 2 * D, 2 * D));
@@ -1247,15 +1283,15 @@ int backward_impl(Ctx& c, const float* P, const float* dE, const float* dF, cons
   }
 
   // embeddings
-  KLAUNCH(st, "k_embed_bwd_Z", k_embed_bwd_Z<<<94, 64, 0, st>>>((int)N, D, bt.Z, a.dv[cur], G + L.W_Z));
+  KLAUNCH(st, "k_embed_bwd_Z", k_embed_bwd_Z<<<94, 64, 0, st>>>((int)N, D, bt.Z, a.dv[cur], G + Lg.W_Z));
   {
     std::vector<TnProblem> ts;
-    ts.push_back(tp(E, m.R, D, a.rbf_a, m.R, 0, nullptr, a.de[cur], D, 0, nullptr, G + L.W_e, 2 * D));
-    ts.push_back(tp(E, m.R, D, a.rbf_a, m.R, 0, nullptr, a.dea, D, 0, nullptr, G + L.W_e + D, 2 * D));
-    ts.push_back(tp(E, 1, D, nullptr, 0, 0, nullptr, a.de[cur], D, 0, nullptr, G + L.b_e0, D));
-    ts.push_back(tp(B, m.R, D, a.rbf_b, m.R, 0, nullptr, a.deb, D, 0, nullptr, G + L.W_eb, D));
-    ts.push_back(tp(A, m.K, D, a.ft, m.K, 0, nullptr, a.da[cur], D, 0, nullptr, G + L.W_th, D));
-    ts.push_back(tp(A, 1, D, nullptr, 0, 0, nullptr, a.da[cur], D, 0, nullptr, G + L.b_th, D));
+    ts.push_back(tp(E, m.R, D, a.rbf_a, m.R, 0, nullptr, a.de[cur], D, 0, nullptr, G + Lg.W_e, 2 * D));
+    ts.push_back(tp(E, m.R, D, a.rbf_a, m.R, 0, nullptr, a.dea, D, 0, nullptr, G + Lg.W_e + D, 2 * D));
+    ts.push_back(tp(E, 1, D, nullptr, 0, 0, nullptr, a.de[cur], D, 0, nullptr, G + Lg.b_e0, D));
+    ts.push_back(tp(B, m.R, D, a.rbf_b, m.R, 0, nullptr, a.deb, D, 0, nullptr, G + Lg.W_eb, D));
+    ts.push_back(tp(A, m.K, D, a.ft, m.K, 0, nullptr, a.da[cur], D, 0, nullptr, G + Lg.W_th, D));
+    ts.push_back(tp(A, 1, D, nullptr, 0, 0, nullptr, a.da[cur], D, 0, nullptr, G + Lg.b_th, D));
     CHG_TRY(run_tns(ts, a, st, "tn_embed"));
     std::vector<GemmProblem> ps;
     GemmProblem p = gp(E, m.R, a.drbf_a, m.R);
@@ -1270,13 +1306,13 @@ int backward_impl(Ctx& c, const float* P, const float* dE, const float* dF, cons
       const int64_t nb = cdiv(E, kFreqRowsPerBlock);
       KLAUNCH(st, "k_rbf_fgrad", k_rbf_fgrad<<<(unsigned)nb, 256, 0, st>>>((int)E, nullptr, a.edge_len, P + L.f_a, m.R, c.hp->r_atom,
                                                 c.hp->envelope_p, a.drbf_a, a.fpart));
-      CHG_TRY(reduce_rows_launch(a.fpart, (int)nb, m.R, m.R, G + L.f_a, st));
+      CHG_TRY(reduce_rows_launch(a.fpart, (int)nb, m.R, m.R, G + Lg.f_a, st));
     }
     if (B > 0) {
       const int64_t nb = cdiv(B, kFreqRowsPerBlock);
       KLAUNCH(st, "k_rbf_fgrad", k_rbf_fgrad<<<(unsigned)nb, 256, 0, st>>>((int)B, g.bond_edge, a.edge_len, P + L.f_b, m.R, c.hp->r_bond,
                                                 c.hp->envelope_p, a.drbf_b, a.fpart));
-      CHG_TRY(reduce_rows_launch(a.fpart, (int)nb, m.R, m.R, G + L.f_b, st));
+      CHG_TRY(reduce_rows_launch(a.fpart, (int)nb, m.R, m.R, G + Lg.f_b, st));
     }
   }
   return CHGNET_OK;
@@ -1288,7 +1324,7 @@ size_t acts_bytes(const chgnet_hparams& hp, int64_t N, int64_t E, int64_t B, int
   Arena ar;
   Acts a;
   Dims m{N, S, E, B, A, hp.d, hp.n_layers, hp.n_rbf, hp.n_fourier};
-  carve_acts(ar, m, a);
+  carve_acts(ar, m, a, make_layout(hp, 4).total);
   return align_up(ar.used, 256);
 }
 
@@ -1306,7 +1342,7 @@ int backward_entry(const chgnet_hparams* hp, const chgnet_batch* batch, const ch
   Ctx c;
   CHG_TRY(make_ctx(hp, batch, graph, ws, ws_bytes, c));
   if (!params || !dE || !dF || !dS || !grad) return fail(CHGNET_EINVAL, "backward: null argument");
-  return backward_impl(c, params, dE, dF, dS, grad, st);
+  return backward_impl(c, params, true, dE, dF, dS, grad, st);
 }
 
 int step_entry(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_graph* graph, float* params,
@@ -1324,7 +1360,7 @@ int step_entry(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_graph
   CHG_TRY(forward_impl(c, params, e_out, f_out, s_out, st));
   KLAUNCH(st, "k_loss", k_loss<<<1, 256, 0, st>>>((int)c.dm.S, (int)c.dm.N, batch->atom_ptr, e_out, f_out, s_out, E_t, F_t, S_t, loss_w[0],
                             loss_w[1], loss_w[2], loss, c.a.dE, c.a.dF, c.a.dS));
-  CHG_TRY(backward_impl(c, params, c.a.dE, c.a.dF, c.a.dS, grad, st));
+  CHG_TRY(backward_impl(c, params, false, c.a.dE, c.a.dF, c.a.dS, grad, st));
   if (adam_hp) {
     const float lr = adam_hp[0], b1 = adam_hp[1], b2 = adam_hp[2], eps = adam_hp[3], t = adam_hp[4];
     const float c1 = 1.0f - powf(b1, t), c2 = 1.0f - powf(b2, t);
