@@ -52,6 +52,7 @@ __device__ __forceinline__ void gemm_fetch(const GemmProblem& P, const GemmSeg& 
   constexpr int KC = 32;
   const bool avec = ((S.lda | S.a_col) & 3) == 0 && ((uintptr_t)S.A & 15) == 0;
   const bool bvec = (S.ldb & 3) == 0 && ((uintptr_t)S.B & 15) == 0;
+  (void)bvec;
   const int ak = (tid & 7) * 4;
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
@@ -59,13 +60,20 @@ __device__ __forceinline__ void gemm_fetch(const GemmProblem& P, const GemmSeg& 
     if (aval[q]) g.a[q] = load4(S.A + arow[q] * S.lda + S.a_col + k0, ak, S.K - k0, avec);
   }
   if (!S.trans) {
-    constexpr int CPR = BN / 4;
+    // column strips: thread takes column n = tid % BN and 4 consecutive k
+    constexpr int G = 256 / BN;  // k-groups per pass
+    const int n = tid % BN, kg = tid / BN;
+    const bool nv = c0 + n < P.N;
 #pragma unroll
     for (int q = 0; q < BN / 32; ++q) {
-      const int idx = tid + 256 * q, kr = idx / CPR, cc = (idx % CPR) * 4;
-      const int k = k0 + kr;
-      g.b[q] = make_float4(0.f, 0.f, 0.f, 0.f);
-      if (k < S.K) g.b[q] = load4(S.B + (int64_t)k * S.ldb + c0, cc, P.N - c0, bvec);
+      const int kb = k0 + 4 * (kg + G * q);
+      const float* col = S.B + c0 + n;
+      float4 v;
+      v.x = (nv && kb + 0 < S.K) ? col[(int64_t)(kb + 0) * S.ldb] : 0.f;
+      v.y = (nv && kb + 1 < S.K) ? col[(int64_t)(kb + 1) * S.ldb] : 0.f;
+      v.z = (nv && kb + 2 < S.K) ? col[(int64_t)(kb + 2) * S.ldb] : 0.f;
+      v.w = (nv && kb + 3 < S.K) ? col[(int64_t)(kb + 3) * S.ldb] : 0.f;
+      g.b[q] = v;
     }
   } else {
 #pragma unroll
@@ -79,14 +87,17 @@ __device__ __forceinline__ void gemm_fetch(const GemmProblem& P, const GemmSeg& 
 
 template <int BN, int NADD>
 __global__ void __launch_bounds__(256) k_gemm(GemmBatch batch) {
-  constexpr int BM = 128, KC = 32, NT = BN / 32;
+  constexpr int BM = 128, KC = 32, NT = BN / 32, KP = KC + 4;
   const GemmProblem& P = batch.p[blockIdx.z];
   const int r0 = blockIdx.x * BM, c0 = blockIdx.y * BN;
   if (r0 >= P.M || c0 >= P.N) return;
-  __shared__ float As[BM][KC + 1];
-  __shared__ float Bs[KC][BN + 4];
+  // Tiles are stored k-contiguous: As[row][k], Bs[col][k]. In MFMA k-step i,
+  // lane half h = lane / 32 supplies k = 16 h + i, so each lane reads its 16
+  // A and B values of a chunk with four 16-byte LDS reads.
+  __shared__ __attribute__((aligned(16))) float As[BM][KP];
+  __shared__ __attribute__((aligned(16))) float Bs[BN][KP];
   __shared__ int64_t ridx[NADD + 2][BM];  // addend rows, residual row, output row
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, h = lane >> 5;
   if (tid < BM) {
     const int row = min(r0 + tid, P.M - 1);
 #pragma unroll
@@ -114,46 +125,48 @@ __global__ void __launch_bounds__(256) k_gemm(GemmBatch batch) {
   while (s < P.nseg) {
     const bool trans = P.seg[s].trans;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      As[ar + 32 * q][ak + 0] = g.a[q].x;
-      As[ar + 32 * q][ak + 1] = g.a[q].y;
-      As[ar + 32 * q][ak + 2] = g.a[q].z;
-      As[ar + 32 * q][ak + 3] = g.a[q].w;
-    }
+    for (int q = 0; q < 4; ++q) *reinterpret_cast<float4*>(&As[ar + 32 * q][ak]) = g.a[q];
     if (!trans) {
-      constexpr int CPR = BN / 4;
+      constexpr int G = 256 / BN;
 #pragma unroll
-      for (int q = 0; q < BN / 32; ++q) {
-        const int idx = tid + 256 * q, kr = idx / CPR, cc = (idx % CPR) * 4;
-        *reinterpret_cast<float4*>(&Bs[kr][cc]) = g.b[q];
-      }
+      for (int q = 0; q < BN / 32; ++q)
+        *reinterpret_cast<float4*>(&Bs[tid % BN][4 * (tid / BN + G * q)]) = g.b[q];
     } else {
 #pragma unroll
       for (int q = 0; q < BN / 32; ++q) {
         const int idx = tid + 256 * q, n = idx / (KC / 4), kk = (idx % (KC / 4)) * 4;
-        Bs[kk + 0][n] = g.b[q].x;
-        Bs[kk + 1][n] = g.b[q].y;
-        Bs[kk + 2][n] = g.b[q].z;
-        Bs[kk + 3][n] = g.b[q].w;
+        *reinterpret_cast<float4*>(&Bs[n][kk]) = g.b[q];
       }
     }
     __syncthreads();
-    // next chunk
     k0 += KC;
     if (k0 >= P.seg[s].K) {
       k0 = 0;
       ++s;
     }
     if (s < P.nseg) gemm_fetch<BN>(P, P.seg[s], k0, c0, tid, arow, aval, g);
+    float af[16], bf[NT][16];
+    {
+      const float* ap = &As[32 * wave + (lane & 31)][16 * h];
 #pragma unroll
-    for (int kk = 0; kk < KC; kk += 2) {
-      const float a = As[32 * wave + (lane & 31)][kk + (lane >> 5)];
+      for (int q = 0; q < 4; ++q) {
+        const float4 v = *reinterpret_cast<const float4*>(ap + 4 * q);
+        af[4 * q] = v.x; af[4 * q + 1] = v.y; af[4 * q + 2] = v.z; af[4 * q + 3] = v.w;
+      }
 #pragma unroll
       for (int t = 0; t < NT; ++t) {
-        const float b = Bs[kk + (lane >> 5)][32 * t + (lane & 31)];
-        acc[t] = __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, acc[t], 0, 0, 0);
+        const float* bp = &Bs[32 * t + (lane & 31)][16 * h];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const float4 v = *reinterpret_cast<const float4*>(bp + 4 * q);
+          bf[t][4 * q] = v.x; bf[t][4 * q + 1] = v.y; bf[t][4 * q + 2] = v.z; bf[t][4 * q + 3] = v.w;
+        }
       }
     }
+#pragma unroll
+    for (int i = 0; i < 16; ++i)
+#pragma unroll
+      for (int t = 0; t < NT; ++t) acc[t] = __builtin_amdgcn_mfma_f32_32x32x2f32(af[i], bf[t][i], acc[t], 0, 0, 0);
     __syncthreads();
   }
   __syncthreads();
@@ -326,18 +339,28 @@ __global__ void __launch_bounds__(1024) k_tn_reduce(TnLaunch L, const float* __r
   }
 }
 
-__global__ void __launch_bounds__(1024) k_reduce_rows(const float* __restrict__ part, int nchunks, int64_t stride,
-                                                      int count, float* __restrict__ out) {
-  __shared__ double red[16][64];
+// First level of the ordered row reduction: group g sums chunks
+// [g*per, (g+1)*per) (wave w takes every 4th), in fp64.
+__global__ void __launch_bounds__(256) k_reduce_rows1(const float* __restrict__ part, int nchunks, int per, int64_t stride,
+                                                      int count, double* __restrict__ part2) {
+  __shared__ double red[4][64];
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int k = blockIdx.x * 64 + lane;
-  red[w][lane] = k < count ? sum_chunks(part + k, nchunks, stride, w) : 0.0;
+  const int k = blockIdx.x * 64 + lane, g = blockIdx.y;
+  const int c0 = g * per, c1 = min(nchunks, c0 + per);
+  double s = 0.0;
+  if (k < count)
+    for (int c = c0 + w; c < c1; c += 4) s += (double)part[(int64_t)c * stride + k];
+  red[w][lane] = s;
   __syncthreads();
-  if (w == 0 && k < count) {
-    double s = 0.0;
-    for (int q = 0; q < 16; ++q) s += red[q][lane];
-    out[k] = (float)((double)out[k] + s);
-  }
+  if (w == 0 && k < count) part2[(int64_t)g * count + k] = ((red[0][lane] + red[1][lane]) + red[2][lane]) + red[3][lane];
+}
+
+__global__ void k_reduce_rows2(const double* __restrict__ part2, int groups, int count, float* __restrict__ out) {
+  const int k = blockIdx.x * blockDim.x + threadIdx.x;
+  if (k >= count) return;
+  double s = 0.0;
+  for (int g = 0; g < groups; ++g) s += part2[(int64_t)g * count + k];
+  out[k] = (float)((double)out[k] + s);
 }
 
 }  // namespace
@@ -411,9 +434,14 @@ int tn_launch(const TnBatch& b, float* part, int64_t part_cap, hipStream_t st, c
   return CHGNET_OK;
 }
 
-int reduce_rows_launch(const float* part, int nchunks, int64_t stride, int count, float* out, hipStream_t st) {
+int reduce_rows_launch(const float* part, int nchunks, int64_t stride, int count, float* out, double* scratch,
+                       hipStream_t st) {
   if (count <= 0) return CHGNET_OK;
-  KLAUNCH(st, "k_reduce_rows", k_reduce_rows<<<(unsigned)cdiv(count, 64), 1024, 0, st>>>(part, nchunks, stride, count, out));
+  const int groups = std::max(1, std::min(32, nchunks));
+  const int per = (int)cdiv(std::max(nchunks, 1), groups);
+  KLAUNCH(st, "k_reduce_rows1", k_reduce_rows1<<<dim3((unsigned)cdiv(count, 64), groups), 256, 0, st>>>(
+                                    part, nchunks, per, stride, count, scratch));
+  KLAUNCH(st, "k_reduce_rows2", k_reduce_rows2<<<(unsigned)cdiv(count, 256), 256, 0, st>>>(scratch, groups, count, out));
   return CHGNET_OK;
 }
 

@@ -81,7 +81,9 @@ struct TnBatch {
 // part: scratch of part_cap floats.
 int tn_launch(const TnBatch& b, float* part, int64_t part_cap, hipStream_t st, const char* tag);
 
-// out[k] += sum_c part[c*stride + k] (k < count), ordered, fp64.
-int reduce_rows_launch(const float* part, int nchunks, int64_t stride, int count, float* out, hipStream_t st);
+// out[k] += sum_c part[c*stride + k] (k < count), in a fixed order, in fp64.
+// scratch: 32 * count doubles. count is at most 8 * 128 for the callers here.
+int reduce_rows_launch(const float* part, int nchunks, int64_t stride, int count, float* out, double* scratch,
+                       hipStream_t st);
 
 }  // namespace chg

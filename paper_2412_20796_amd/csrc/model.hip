@@ -31,8 +31,8 @@ int validate_batch(const chgnet_batch* b);
 namespace {
 
 constexpr float kLnEps = 1e-5f;
-constexpr int kGateRowsPerBlock = 512;  // rows per block (16 wavefronts) in backward gate kernels
 constexpr int kFreqRowsPerBlock = 256;  // rows per block in frequency-gradient kernel
+constexpr int kReduceGroups = 32;      // first-level groups of the ordered partial-sum reduction
 constexpr int64_t kTnPartFloats = 16ll << 20;
 
 __device__ __forceinline__ float sigm(float x) { return 1.0f / (1.0f + __expf(-x)); }
@@ -185,85 +185,71 @@ __global__ void k_embed_v0(int N, int D, const int* __restrict__ Z, const float*
 }
 
 // ---------------------------------------------------------------------------
-// GatedMLP rows: phi = SiLU(LN_c(z_c)) * sigmoid(LN_g(z_g)), one row per wave.
+// GatedMLP rows: phi = SiLU(LN_c(z_c)) * sigmoid(LN_g(z_g)).
+// A row is held by LPR = d/16 adjacent lanes, each with 16 contiguous core
+// columns and the 16 matching gate columns; LayerNorm statistics are sums
+// over those LPR lanes by DPP permutes (no LDS traffic). A wavefront works
+// on 64/LPR rows at a time.
 // ---------------------------------------------------------------------------
-template <int V>
-struct GateRow {
-  float xc[V], xg[V];  // normalised core / gate
-  float yc[V], yg[V];  // after scale and shift
-  float rc, rg;        // 1 / std
+template <int CTRL>
+__device__ __forceinline__ float dpp(float v) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+
+template <int LPR>
+__device__ __forceinline__ float rowsum(float v) {
+  v += dpp<0xB1>(v);  // quad_perm [1,0,3,2]
+  v += dpp<0x4E>(v);  // quad_perm [2,3,0,1]
+  if (LPR == 8) v += dpp<0x141>(v);  // row_half_mirror: pairs the two quads
+  return v;
+}
+
+template <int D>
+struct RowShape {
+  static constexpr int LPR = D / 16;    // lanes per row
+  static constexpr int RPW = 64 / LPR;  // rows per wavefront pass
 };
 
-template <int V>
-__device__ __forceinline__ void gate_forward(const float* __restrict__ z, const float* __restrict__ gc,
-                                             const float* __restrict__ bc, const float* __restrict__ gg,
-                                             const float* __restrict__ bg, int lane, GateRow<V>& g, float* phi) {
-  constexpr int D = 64 * V;
-  float zc[V], zg[V], sc = 0.f, sg = 0.f;
+__device__ __forceinline__ void load16(const float* __restrict__ p, float (&v)[16]) {
 #pragma unroll
-  for (int k = 0; k < V; ++k) {
-    zc[k] = z[lane + 64 * k];
-    zg[k] = z[D + lane + 64 * k];
+  for (int q = 0; q < 4; ++q) {
+    const float4 t = *reinterpret_cast<const float4*>(p + 4 * q);
+    v[4 * q] = t.x;
+    v[4 * q + 1] = t.y;
+    v[4 * q + 2] = t.z;
+    v[4 * q + 3] = t.w;
+  }
+}
+__device__ __forceinline__ void store16(float* __restrict__ p, const float (&v)[16]) {
+#pragma unroll
+  for (int q = 0; q < 4; ++q)
+    *reinterpret_cast<float4*>(p + 4 * q) = make_float4(v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]);
+}
+
+// Normalised core/gate (xc, xg) and 1/std (rc, rg) of one row; in place.
+template <int LPR, int D>
+__device__ __forceinline__ void ln_stats(float (&zc)[16], float (&zg)[16], float& rc, float& rg) {
+  float sc = 0.f, sg = 0.f;
+#pragma unroll
+  for (int k = 0; k < 16; ++k) {
     sc += zc[k];
     sg += zg[k];
   }
-  const float mc = wsum(sc) * (1.0f / D), mg = wsum(sg) * (1.0f / D);
+  const float mc = rowsum<LPR>(sc) * (1.0f / D), mg = rowsum<LPR>(sg) * (1.0f / D);
   float vc = 0.f, vg = 0.f;
 #pragma unroll
-  for (int k = 0; k < V; ++k) {
+  for (int k = 0; k < 16; ++k) {
     zc[k] -= mc;
     zg[k] -= mg;
     vc += zc[k] * zc[k];
     vg += zg[k] * zg[k];
   }
-  g.rc = rsqrtf(wsum(vc) * (1.0f / D) + kLnEps);
-  g.rg = rsqrtf(wsum(vg) * (1.0f / D) + kLnEps);
+  rc = rsqrtf(rowsum<LPR>(vc) * (1.0f / D) + kLnEps);
+  rg = rsqrtf(rowsum<LPR>(vg) * (1.0f / D) + kLnEps);
 #pragma unroll
-  for (int k = 0; k < V; ++k) {
-    const int c = lane + 64 * k;
-    g.xc[k] = zc[k] * g.rc;
-    g.xg[k] = zg[k] * g.rg;
-    g.yc[k] = gc[c] * g.xc[k] + bc[c];
-    g.yg[k] = gg[c] * g.xg[k] + bg[c];
-    phi[k] = g.yc[k] * sigm(g.yc[k]) * sigm(g.yg[k]);
-  }
-}
-
-// Backward of one gated row given dphi: writes dz (2D values) and
-// accumulates the LayerNorm parameter partials (dgc, dbc, dgg, dbg).
-template <int V>
-__device__ __forceinline__ void gate_backward(const GateRow<V>& g, const float* dphi, const float* __restrict__ gc,
-                                              const float* __restrict__ gg, int lane, float* __restrict__ dz,
-                                              float (&acc)[4][V]) {
-  constexpr int D = 64 * V;
-  float dxc[V], dxg[V], s1c = 0.f, s2c = 0.f, s1g = 0.f, s2g = 0.f;
-#pragma unroll
-  for (int k = 0; k < V; ++k) {
-    const int c = lane + 64 * k;
-    const float sc = sigm(g.yc[k]), sgt = sigm(g.yg[k]);
-    const float silu_c = g.yc[k] * sc;
-    const float dyc = dphi[k] * sgt * sc * (1.0f + g.yc[k] * (1.0f - sc));
-    const float dyg = dphi[k] * silu_c * sgt * (1.0f - sgt);
-    acc[0][k] += dyc * g.xc[k];
-    acc[1][k] += dyc;
-    acc[2][k] += dyg * g.xg[k];
-    acc[3][k] += dyg;
-    dxc[k] = dyc * gc[c];
-    dxg[k] = dyg * gg[c];
-    s1c += dxc[k];
-    s2c += dxc[k] * g.xc[k];
-    s1g += dxg[k];
-    s2g += dxg[k] * g.xg[k];
-  }
-  s1c = wsum(s1c) * (1.0f / D);
-  s2c = wsum(s2c) * (1.0f / D);
-  s1g = wsum(s1g) * (1.0f / D);
-  s2g = wsum(s2g) * (1.0f / D);
-#pragma unroll
-  for (int k = 0; k < V; ++k) {
-    const int c = lane + 64 * k;
-    dz[c] = g.rc * (dxc[k] - s1c - g.xc[k] * s2c);
-    dz[D + c] = g.rg * (dxg[k] - s1g - g.xg[k] * s2g);
+  for (int k = 0; k < 16; ++k) {
+    zc[k] *= rc;
+    zg[k] *= rg;
   }
 }
 
@@ -271,145 +257,175 @@ struct LnPtrs {
   const float *gc, *bc, *gg, *bg;
 };
 
-// Atom conv messages: msg_e = e^a_e * phi_v(z_e).
-template <int V>
-__global__ void __launch_bounds__(256) k_gate_atom_fwd(int E, const float* __restrict__ zv, const float* __restrict__ ea,
-                                                       LnPtrs ln, float* __restrict__ msg) {
-  constexpr int D = 64 * V;
-  const int row = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
-  if (row >= E) return;
-  GateRow<V> g;
-  float phi[V];
-  gate_forward<V>(zv + (int64_t)row * 2 * D, ln.gc, ln.bc, ln.gg, ln.bg, lane, g, phi);
-#pragma unroll
-  for (int k = 0; k < V; ++k) {
-    const int64_t o = (int64_t)row * D + lane + 64 * k;
-    msg[o] = ea[o] * phi[k];
-  }
-}
+// Gathered terms of the split first linear layer: z = z_pre + sum_q
+// add[q][idx_q[row]] (each a 2d-wide core | gate row).
+struct GateAdds {
+  int n;
+  const float* p[3];
+  int ld[3];
+  const int* idx[3];
+};
 
-// Bond conv messages eb_{b2} * phi_e and angle update a' = a + phi_a.
-template <int V>
-__global__ void __launch_bounds__(256) k_gate_angle_fwd(int A, const float* __restrict__ zae, int has_angle,
-                                                        const float* __restrict__ eb, const int* __restrict__ ang_b2,
-                                                        LnPtrs lne, LnPtrs lna, const float* __restrict__ a_in,
-                                                        float* __restrict__ a_out, float* __restrict__ msgb) {
-  constexpr int D = 64 * V;
-  const int row = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
-  if (row >= A) return;
-  GateRow<V> g;
-  float phi[V];
-  const float* z = zae + (int64_t)row * 4 * D;
-  gate_forward<V>(z, lne.gc, lne.bc, lne.gg, lne.bg, lane, g, phi);
-  const int64_t b2 = ang_b2[row];
+template <int D>
+__device__ __forceinline__ void load_z(const float* __restrict__ z, int ldz, const GateAdds& ad, int row, int c0,
+                                       float (&zc)[16], float (&zg)[16]) {
+  load16(z + (int64_t)row * ldz + c0, zc);
+  load16(z + (int64_t)row * ldz + D + c0, zg);
 #pragma unroll
-  for (int k = 0; k < V; ++k) msgb[(int64_t)row * D + lane + 64 * k] = eb[b2 * D + lane + 64 * k] * phi[k];
-  if (has_angle) {
-    gate_forward<V>(z + 2 * D, lna.gc, lna.bc, lna.gg, lna.bg, lane, g, phi);
+  for (int q = 0; q < 3; ++q) {
+    if (q >= ad.n) break;
+    const float* r = ad.p[q] + (int64_t)ad.idx[q][row] * ad.ld[q];
+    float uc[16], ug[16];
+    load16(r + c0, uc);
+    load16(r + D + c0, ug);
 #pragma unroll
-    for (int k = 0; k < V; ++k) {
-      const int64_t o = (int64_t)row * D + lane + 64 * k;
-      a_out[o] = a_in[o] + phi[k];
+    for (int k = 0; k < 16; ++k) {
+      zc[k] += uc[k];
+      zg[k] += ug[k];
     }
   }
 }
 
-// Backward of the atom conv gate: dphi = dm_src * e^a, d e^a += dm_src * phi.
-template <int V>
-__global__ void __launch_bounds__(1024) k_gate_atom_bwd(int E, const float* __restrict__ zv, const float* __restrict__ ea,
-                                                       const float* __restrict__ dm, const int* __restrict__ edge_src,
-                                                       LnPtrs ln, float* __restrict__ dzv, float* __restrict__ dea,
-                                                       float* __restrict__ lnpart) {
-  constexpr int D = 64 * V;
-  __shared__ float red[16][4 * D];
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  float acc[4][V];
+enum GateFwdMode { FWD_ATOM = 0, FWD_BOND = 1, FWD_ANGLE = 2 };
+
+// Forward gate. z rows at z + row*ldz (2d values).
+//   FWD_ATOM : out[row] = e^a[row] * phi            (atom conv message)
+//   FWD_BOND : out[row] = e^b[b2[row]] * phi        (bond conv message)
+//   FWD_ANGLE: out[row] = a[row] + phi              (angle update)
+template <int D, int MODE>
+__global__ void __launch_bounds__(256) k_gate_fwd(int rows, const float* __restrict__ z, int ldz, GateAdds ad,
+                                                  LnPtrs ln, const float* __restrict__ mulv,
+                                                  const int* __restrict__ mul_idx, float* __restrict__ out) {
+  constexpr int LPR = RowShape<D>::LPR, RPW = RowShape<D>::RPW;
+  const int lane = threadIdx.x & 63, slot = lane / LPR, c0 = 16 * (lane % LPR);
+  const int row = (blockIdx.x * 4 + (threadIdx.x >> 6)) * RPW + slot;
+  if (row >= rows) return;  // LN lanes of a row are adjacent: a row is all-in or all-out
+  float zc[16], zg[16], rc, rg;
+  load_z<D>(z, ldz, ad, row, c0, zc, zg);
+  ln_stats<LPR, D>(zc, zg, rc, rg);
+  float m[16], o[16];
+  const int64_t mrow = MODE == FWD_BOND ? mul_idx[row] : row;
+  load16(mulv + mrow * D + c0, m);
 #pragma unroll
-  for (int a = 0; a < 4; ++a)
-#pragma unroll
-    for (int k = 0; k < V; ++k) acc[a][k] = 0.f;
-  const int r0 = blockIdx.x * kGateRowsPerBlock;
-  for (int rr = wave; rr < kGateRowsPerBlock; rr += 16) {
-    const int row = r0 + rr;
-    if (row >= E) break;
-    GateRow<V> g;
-    float phi[V], dphi[V];
-    gate_forward<V>(zv + (int64_t)row * 2 * D, ln.gc, ln.bc, ln.gg, ln.bg, lane, g, phi);
-    const int64_t src = edge_src[row];
-#pragma unroll
-    for (int k = 0; k < V; ++k) {
-      const int c = lane + 64 * k;
-      const float dmv = dm[src * D + c];
-      const int64_t o = (int64_t)row * D + c;
-      dphi[k] = dmv * ea[o];
-      dea[o] += dmv * phi[k];
-    }
-    gate_backward<V>(g, dphi, ln.gc, ln.gg, lane, dzv + (int64_t)row * 2 * D, acc);
+  for (int k = 0; k < 16; ++k) {
+    const int c = c0 + k;
+    const float yc = ln.gc[c] * zc[k] + ln.bc[c];
+    const float yg = ln.gg[c] * zg[k] + ln.bg[c];
+    const float phi = yc * sigm(yc) * sigm(yg);
+    o[k] = MODE == FWD_ANGLE ? m[k] + phi : m[k] * phi;
   }
-#pragma unroll
-  for (int a = 0; a < 4; ++a)
-#pragma unroll
-    for (int k = 0; k < V; ++k) red[wave][a * D + lane + 64 * k] = acc[a][k];
-  __syncthreads();
-  for (int c = threadIdx.x; c < 4 * D; c += 1024) {
-    float s = 0.f;
-    for (int q = 0; q < 16; ++q) s += red[q][c];
-    lnpart[(int64_t)blockIdx.x * 4 * D + c] = s;
-  }
+  store16(out + (int64_t)row * D + c0, o);
 }
 
-// Backward of the angle gates. dphi_e = dmu_b1 * eb_b1 * eb_b2;
-// t2 = dmu_b1 * eb_b1 * phi_e (gradient of eb_b2); dphi_a = da'.
-template <int V>
-__global__ void __launch_bounds__(1024) k_gate_angle_bwd(int A, const float* __restrict__ zae, int has_angle,
-                                                        const float* __restrict__ eb, const int* __restrict__ ang_b1,
-                                                        const int* __restrict__ ang_b2, const float* __restrict__ dmu,
-                                                        const float* __restrict__ da_next, LnPtrs lne, LnPtrs lna,
-                                                        float* __restrict__ dzae, float* __restrict__ t2,
-                                                        float* __restrict__ lnpart) {
-  constexpr int D = 64 * V;
-  __shared__ float red[16][4 * D];
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  float acc_e[4][V], acc_a[4][V];
+enum GateBwdMode { BWD_ATOM = 0, BWD_BOND = 1, BWD_ANGLE = 2 };
+
+// Backward gate: dz (2d values) from dphi, plus the LayerNorm parameter
+// partial sums of the block (g_c, b_c, g_g, b_g; 4d values) into lnpart.
+//   BWD_ATOM : dphi = dm[src] * e^a[row]; d e^a[row] += dm[src] * phi
+//   BWD_BOND : w = dmu[b1] * e^b[b1]; dphi = w * e^b[b2]; t2[row] = w * phi
+//   BWD_ANGLE: dphi = da'[row]
+// Each block covers kGateRows rows.
+constexpr int kGateRows = 128;
+template <int D, int MODE>
+__global__ void __launch_bounds__(256) k_gate_bwd(int rows, const float* __restrict__ z, int ldz, GateAdds ad, LnPtrs ln,
+                                                  const float* __restrict__ up, const int* __restrict__ up_idx,
+                                                  const float* __restrict__ eb, const int* __restrict__ b2_idx,
+                                                  float* __restrict__ aux, float* __restrict__ dz, int lddz,
+                                                  float* __restrict__ lnpart) {
+  constexpr int LPR = RowShape<D>::LPR, RPW = RowShape<D>::RPW;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, slot = lane / LPR, c0 = 16 * (lane % LPR);
+  float acc[4][16];
 #pragma unroll
   for (int a = 0; a < 4; ++a)
 #pragma unroll
-    for (int k = 0; k < V; ++k) acc_e[a][k] = acc_a[a][k] = 0.f;
-  const int r0 = blockIdx.x * kGateRowsPerBlock;
-  for (int rr = wave; rr < kGateRowsPerBlock; rr += 16) {
-    const int row = r0 + rr;
-    if (row >= A) break;
-    const float* z = zae + (int64_t)row * 4 * D;
-    float* dz = dzae + (int64_t)row * 4 * D;
-    GateRow<V> g;
-    float phi[V], dphi[V];
-    gate_forward<V>(z, lne.gc, lne.bc, lne.gg, lne.bg, lane, g, phi);
-    const int64_t b1 = ang_b1[row], b2 = ang_b2[row];
+    for (int k = 0; k < 16; ++k) acc[a][k] = 0.f;
+  for (int it = 0; it < kGateRows / (4 * RPW); ++it) {
+    const int row = blockIdx.x * kGateRows + (it * 4 + wave) * RPW + slot;
+    if (row >= rows) continue;
+    float zc[16], zg[16], rc, rg;
+    load_z<D>(z, ldz, ad, row, c0, zc, zg);
+    ln_stats<LPR, D>(zc, zg, rc, rg);
+    float u[16], w[16], dphi[16];
+    if (MODE == BWD_ANGLE) {
+      load16(up + (int64_t)row * D + c0, dphi);
+    } else {
+      const int64_t ur = up_idx[row];
+      load16(up + ur * D + c0, u);
+      if (MODE == BWD_ATOM) {
+        load16(eb + (int64_t)row * D + c0, w);  // e^a of this edge
 #pragma unroll
-    for (int k = 0; k < V; ++k) {
-      const int c = lane + 64 * k;
-      const float w = dmu[b1 * D + c] * eb[b1 * D + c];
-      dphi[k] = w * eb[b2 * D + c];
-      t2[(int64_t)row * D + c] = w * phi[k];
+        for (int k = 0; k < 16; ++k) dphi[k] = u[k] * w[k];
+      } else {
+        float e1[16], e2[16];
+        load16(eb + ur * D + c0, e1);
+        load16(eb + (int64_t)b2_idx[row] * D + c0, e2);
+#pragma unroll
+        for (int k = 0; k < 16; ++k) {
+          w[k] = u[k] * e1[k];
+          dphi[k] = w[k] * e2[k];
+        }
+      }
     }
-    gate_backward<V>(g, dphi, lne.gc, lne.gg, lane, dz, acc_e);
-    if (has_angle) {
-      gate_forward<V>(z + 2 * D, lna.gc, lna.bc, lna.gg, lna.bg, lane, g, phi);
+    float dyc[16], dyg[16], side[16];
+    float s1c = 0.f, s2c = 0.f, s1g = 0.f, s2g = 0.f;
 #pragma unroll
-      for (int k = 0; k < V; ++k) dphi[k] = da_next[(int64_t)row * D + lane + 64 * k];
-      gate_backward<V>(g, dphi, lna.gc, lna.gg, lane, dz + 2 * D, acc_a);
+    for (int k = 0; k < 16; ++k) {
+      const int c = c0 + k;
+      const float yc = ln.gc[c] * zc[k] + ln.bc[c];
+      const float yg = ln.gg[c] * zg[k] + ln.bg[c];
+      const float sc = sigm(yc), sg = sigm(yg);
+      const float silu_c = yc * sc;
+      side[k] = silu_c * sg;  // phi
+      const float gy_c = dphi[k] * sg * sc * (1.0f + yc * (1.0f - sc));
+      const float gy_g = dphi[k] * silu_c * sg * (1.0f - sg);
+      acc[0][k] += gy_c * zc[k];
+      acc[1][k] += gy_c;
+      acc[2][k] += gy_g * zg[k];
+      acc[3][k] += gy_g;
+      dyc[k] = gy_c * ln.gc[c];
+      dyg[k] = gy_g * ln.gg[c];
+      s1c += dyc[k];
+      s2c += dyc[k] * zc[k];
+      s1g += dyg[k];
+      s2g += dyg[k] * zg[k];
+    }
+    s1c = rowsum<LPR>(s1c) * (1.0f / D);
+    s2c = rowsum<LPR>(s2c) * (1.0f / D);
+    s1g = rowsum<LPR>(s1g) * (1.0f / D);
+    s2g = rowsum<LPR>(s2g) * (1.0f / D);
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+      dyc[k] = rc * (dyc[k] - s1c - zc[k] * s2c);
+      dyg[k] = rg * (dyg[k] - s1g - zg[k] * s2g);
+    }
+    store16(dz + (int64_t)row * lddz + c0, dyc);
+    store16(dz + (int64_t)row * lddz + D + c0, dyg);
+    if (MODE == BWD_ATOM) {
+      float de[16];
+      load16(aux + (int64_t)row * D + c0, de);
+#pragma unroll
+      for (int k = 0; k < 16; ++k) de[k] += u[k] * side[k];
+      store16(aux + (int64_t)row * D + c0, de);
+    } else if (MODE == BWD_BOND) {
+#pragma unroll
+      for (int k = 0; k < 16; ++k) side[k] *= w[k];
+      store16(aux + (int64_t)row * D + c0, side);
     }
   }
-  for (int half = 0; half < 2; ++half) {
+  // LayerNorm partials: lanes with the same columns (same lane % LPR) over
+  // all slots and wavefronts, summed in a fixed order through LDS.
+  __shared__ float red[4][64][17];
 #pragma unroll
-    for (int a = 0; a < 4; ++a)
+  for (int a = 0; a < 4; ++a) {
 #pragma unroll
-      for (int k = 0; k < V; ++k) red[wave][a * D + lane + 64 * k] = half ? acc_a[a][k] : acc_e[a][k];
+    for (int k = 0; k < 16; ++k) red[wave][lane][k] = acc[a][k];
     __syncthreads();
-    for (int c = threadIdx.x; c < 4 * D; c += 1024) {
+    for (int c = threadIdx.x; c < D; c += 256) {
+      const int sub = c / 16, k = c % 16;
       float s = 0.f;
-      for (int q = 0; q < 16; ++q) s += red[q][c];
-      lnpart[(int64_t)blockIdx.x * 8 * D + half * 4 * D + c] = s;
+      for (int w = 0; w < 4; ++w)
+        for (int sl = 0; sl < RPW; ++sl) s += red[w][sl * LPR + sub][k];
+      lnpart[(int64_t)blockIdx.x * 4 * D + a * D + c] = s;
     }
     __syncthreads();
   }
@@ -442,10 +458,13 @@ __global__ void __launch_bounds__(256) k_segsum(int nseg, int ncb, const int* __
   if (out2) out2[(int64_t)s * ld_out2 + c] = mul[(int64_t)s * ld_mul + c] * acc;
 }
 
-// Per bond b (centre i, local index p among k bonds): DZ1 = sum over angles
-// (b, *) of dz, DZ2 = sum over angles (*, b) of dz, and
-// d eb_b += dmu_b * S_b + sum over angles (*, b) of t2.
-__global__ void __launch_bounds__(256) k_bond_bwd_reduce(int B, int D, int W4, const int* __restrict__ bond_src,
+// Per bond b (centre i, local index q among k bonds): DZ1 = sum over the
+// angles (b, *) of dz, DZ2 = sum over the angles (*, b) of dz, and
+// d eb_b += dmu_b * S_b + sum over the angles (*, b) of t2. One wavefront per
+// bond; a lane owns CPL consecutive dz columns and TPL t2 columns; two
+// independent accumulators per sum (fixed order).
+template <int CPL, int TPL>
+__global__ void __launch_bounds__(256) k_bond_bwd_reduce(int B, int D, const int* __restrict__ bond_src,
                                                          const int* __restrict__ bond_ptr, const int* __restrict__ angle_ptr,
                                                          const float* __restrict__ dzae, const float* __restrict__ t2,
                                                          const float* __restrict__ dmu, const float* __restrict__ ssum,
@@ -454,26 +473,47 @@ __global__ void __launch_bounds__(256) k_bond_bwd_reduce(int B, int D, int W4, c
   if (b >= B) return;
   const int i = bond_src[b], k0 = bond_ptr[i], k = bond_ptr[i + 1] - k0, q = b - k0;
   const int lo = angle_ptr[b], hi = angle_ptr[b + 1];
-  for (int c = lane; c < W4; c += 64) {
-    float s1 = 0.f, s2 = 0.f;
-    for (int r = lo; r < hi; ++r) s1 += dzae[(int64_t)r * 4 * D + c];
-    for (int p = 0; p < k; ++p) {
-      if (p == q) continue;
-      const int64_t al = angle_ptr[k0 + p] + (q < p ? q : q - 1);
-      s2 += dzae[al * 4 * D + c];
-    }
-    DZ12[(int64_t)b * 8 * D + c] = s1;
-    DZ12[(int64_t)b * 8 * D + 4 * D + c] = s2;
+  const int64_t ld = 4 * D;
+  const int c = lane * CPL;
+  float s1[2][CPL], s2[2][CPL];
+#pragma unroll
+  for (int u = 0; u < 2; ++u)
+#pragma unroll
+    for (int x = 0; x < CPL; ++x) s1[u][x] = s2[u][x] = 0.f;
+  int r = lo;
+  for (; r + 1 < hi; r += 2) {
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+#pragma unroll
+      for (int x = 0; x < CPL; ++x) s1[u][x] += dzae[(int64_t)(r + u) * ld + c + x];
   }
-  for (int c = lane; c < D; c += 64) {
-    float s = 0.f;
-    for (int p = 0; p < k; ++p) {
-      if (p == q) continue;
-      const int64_t al = angle_ptr[k0 + p] + (q < p ? q : q - 1);
-      s += t2[al * D + c];
-    }
-    const int64_t o = (int64_t)b * D + c;
-    deb[o] += dmu[o] * ssum[o] + s;
+  if (r < hi)
+#pragma unroll
+    for (int x = 0; x < CPL; ++x) s1[0][x] += dzae[(int64_t)r * ld + c + x];
+  // angles (p, q) for p != q: index angle_ptr[k0 + p] + (q < p ? q : q - 1)
+  float tt[2][TPL];
+#pragma unroll
+  for (int u = 0; u < 2; ++u)
+#pragma unroll
+    for (int x = 0; x < TPL; ++x) tt[u][x] = 0.f;
+  for (int p = 0; p < k; ++p) {
+    if (p == q) continue;
+    const int u = p & 1;
+    const int64_t al = angle_ptr[k0 + p] + (q < p ? q : q - 1);
+#pragma unroll
+    for (int x = 0; x < CPL; ++x) s2[u][x] += dzae[al * ld + c + x];
+#pragma unroll
+    for (int x = 0; x < TPL; ++x) tt[u][x] += t2[al * D + lane * TPL + x];
+  }
+#pragma unroll
+  for (int x = 0; x < CPL; ++x) {
+    DZ12[(int64_t)b * 8 * D + c + x] = s1[0][x] + s1[1][x];
+    DZ12[(int64_t)b * 8 * D + 4 * D + c + x] = s2[0][x] + s2[1][x];
+  }
+#pragma unroll
+  for (int x = 0; x < TPL; ++x) {
+    const int64_t o = (int64_t)b * D + lane * TPL + x;
+    deb[o] += dmu[o] * ssum[o] + (tt[0][x] + tt[1][x]);
   }
 }
 
@@ -677,12 +717,13 @@ struct Acts {
   float* e[kMaxLayers + 1];
   float* a[kMaxLayers];
   float *zv[kMaxLayers], *zae[kMaxLayers], *m[kMaxLayers], *ssum[kMaxLayers], *mu[kMaxLayers];
-  float *msg, *msgb, *Xa, *Xb;
+  float *msg, *msgb, *Xa[kMaxLayers], *Xb[kMaxLayers];
   float *hE1, *aE1, *hE2, *aE2, *hS1, *aS1, *hS2, *aS2, *hF1, *aF1, *hF2, *aF2, *oE, *oS, *oF;
   // backward
   float *dv[2], *de[2], *da[2], *dm, *dmu, *dzv, *dzae, *t2, *AT, *DZ12, *dea, *deb;
   float *doE, *doS, *dn, *doF, *dh2E, *dh2S, *dh2F, *dh1ES, *dh1F, *drbf_a, *drbf_b;
   float *lnpart, *tnpart, *fpart, *Pal;
+  double* red2;
   int64_t tnpart_cap;
   // loss
   float *dE, *dF, *dS, *out_E, *out_F, *out_S;
@@ -718,8 +759,10 @@ void carve_acts(Arena& ar, const Dims& m, Acts& a, int64_t n_params_aligned) {
   }
   a.msg = ar.take<float>(E * D);
   a.msgb = ar.take<float>(A * D);
-  a.Xa = ar.take<float>(N * 8 * D);
-  a.Xb = ar.take<float>(B * 8 * D);
+  for (int t = 0; t < m.T; ++t) {
+    a.Xa[t] = ar.take<float>(N * 8 * D);
+    a.Xb[t] = ar.take<float>(B * 8 * D);
+  }
   float** atom_heads[] = {&a.hE1, &a.aE1, &a.hE2, &a.aE2, &a.hS1, &a.aS1, &a.hS2, &a.aS2};
   for (auto p : atom_heads) *p = ar.take<float>(N * D);
   float** edge_heads[] = {&a.hF1, &a.aF1, &a.hF2, &a.aF2};
@@ -752,8 +795,9 @@ void carve_acts(Arena& ar, const Dims& m, Acts& a, int64_t n_params_aligned) {
   a.dh1F = ar.take<float>(E * D);
   a.drbf_a = ar.take<float>(E * R);
   a.drbf_b = ar.take<float>(B * R);
-  const int64_t gate_blocks = cdiv(std::max<int64_t>(std::max(E, A), 1), kGateRowsPerBlock);
-  a.lnpart = ar.take<float>(gate_blocks * 8 * D);
+  const int64_t gate_blocks = cdiv(std::max<int64_t>(std::max(E, A), 1), kGateRows);
+  a.lnpart = ar.take<float>(gate_blocks * 4 * D);
+  a.red2 = ar.take<double>(kReduceGroups * 8 * D);
   a.tnpart_cap = kTnPartFloats;
   a.tnpart = ar.take<float>(a.tnpart_cap);
   a.fpart = ar.take<float>(cdiv(std::max(E, (int64_t)1), kFreqRowsPerBlock) * R);
@@ -867,6 +911,44 @@ int pack_params(const ParamLayout& L, const ParamLayout& La, const float* P, flo
   return CHGNET_OK;
 }
 
+template <int MODE>
+int gate_fwd(int D, int64_t rows, const float* z, int ldz, const GateAdds& ad, LnPtrs ln, const float* mulv,
+             const int* idx, float* out, hipStream_t st, const char* tag) {
+  if (rows <= 0) return CHGNET_OK;
+  if (D == 64)
+    KLAUNCH(st, tag, k_gate_fwd<64, MODE><<<(unsigned)cdiv(rows, 4 * RowShape<64>::RPW), 256, 0, st>>>(
+                         (int)rows, z, ldz, ad, ln, mulv, idx, out));
+  else
+    KLAUNCH(st, tag, k_gate_fwd<128, MODE><<<(unsigned)cdiv(rows, 4 * RowShape<128>::RPW), 256, 0, st>>>(
+                         (int)rows, z, ldz, ad, ln, mulv, idx, out));
+  return CHGNET_OK;
+}
+
+template <int MODE>
+int gate_bwd(int D, int64_t rows, const float* z, int ldz, const GateAdds& ad, LnPtrs ln, const float* up,
+             const int* up_idx, const float* eb, const int* b2_idx, float* aux, float* dz, int lddz, const Acts& a,
+             float* ln_grad, hipStream_t st, const char* tag) {
+  if (rows <= 0) return CHGNET_OK;
+  const int64_t nb = cdiv(rows, kGateRows);
+  if (D == 64)
+    KLAUNCH(st, tag, k_gate_bwd<64, MODE><<<(unsigned)nb, 256, 0, st>>>((int)rows, z, ldz, ad, ln, up, up_idx, eb,
+                                                                          b2_idx, aux, dz, lddz, a.lnpart));
+  else
+    KLAUNCH(st, tag, k_gate_bwd<128, MODE><<<(unsigned)nb, 256, 0, st>>>((int)rows, z, ldz, ad, ln, up, up_idx, eb,
+                                                                           b2_idx, aux, dz, lddz, a.lnpart));
+  return reduce_rows_launch(a.lnpart, (int)nb, 4 * D, 4 * D, ln_grad, a.red2, st);
+}
+
+GateAdds adds(int n, const float* p0, int ld0, const int* i0, const float* p1, int ld1, const int* i1,
+              const float* p2 = nullptr, int ld2 = 0, const int* i2 = nullptr) {
+  GateAdds a{};
+  a.n = n;
+  a.p[0] = p0; a.ld[0] = ld0; a.idx[0] = i0;
+  a.p[1] = p1; a.ld[1] = ld1; a.idx[1] = i1;
+  a.p[2] = p2; a.ld[2] = ld2; a.idx[2] = i2;
+  return a;
+}
+
 LnPtrs ln_ptrs(const float* P, const GatedOffsets& g) { return LnPtrs{P + g.g_c, P + g.b_c, P + g.g_g, P + g.b_g}; }
 
 struct Ctx {
@@ -903,10 +985,6 @@ int make_ctx(const chgnet_hparams* hp, const chgnet_batch* batch, const chgnet_g
   if (!ws || !ar.ok()) return fail(CHGNET_EWORKSPACE, "workspace too small (query chgnet_workspace_size)");
   return CHGNET_OK;
 }
-
-#define LAUNCH_V(kern, V, grid, block, st, ...)                                                    \
-  KLAUNCH(st, #kern, if ((V) == 1) kern<1><<<(grid), (block), 0, (st)>>>(__VA_ARGS__);          \
-                     else kern<2><<<(grid), (block), 0, (st)>>>(__VA_ARGS__))
 
 // ---------------------------------------------------------------------------
 // Forward.
@@ -972,7 +1050,7 @@ int forward_impl(Ctx& c, const float* Pflat, float* energy, float* forces, float
     for (int k = 0; k < 4; ++k) {
       if (k == 3 && !ang) break;
       const float* W = k == 0 ? Wav : k == 1 ? Wav + D * 2 * D : k == 2 ? Wbe : Wan;
-      GemmProblem p = gp(N, 2 * D, a.Xa + k * 2 * D, 8 * D);
+      GemmProblem p = gp(N, 2 * D, a.Xa[t] + k * 2 * D, 8 * D);
       seg(p, a.v[t], D, 0, D, W, 2 * D, 0);
       ps.push_back(p);
     }
@@ -980,40 +1058,44 @@ int forward_impl(Ctx& c, const float* Pflat, float* energy, float* forces, float
       if ((k & 1) && !ang) continue;
       // k: 0 bond-conv role b1, 1 angle role b1, 2 bond-conv role b2, 3 angle role b2
       const float* W = (k & 1 ? Wan : Wbe) + (k < 2 ? 1 : 2) * D * 2 * D;
-      GemmProblem p = gp(B, 2 * D, a.Xb + k * 2 * D, 8 * D);
+      GemmProblem p = gp(B, 2 * D, a.Xb[t] + k * 2 * D, 8 * D);
       p.a_rows = g.bond_edge;
       seg(p, a.e[t], D, 0, D, W, 2 * D, 0);
       ps.push_back(p);
     }
     CHG_TRY(run_gemms(ps, st, "gemm_proj"));
     ps.clear();
-    // edge term + gathered atom terms -> atom conv pre-activation
+    // edge and angle terms (+ bias); the gathered atom and bond terms are
+    // added by the gate kernels, which stream each row once
     {
       GemmProblem p = gp(E, 2 * D, a.zv[t], 2 * D);
       seg(p, a.e[t], D, 0, D, Wav + 2 * D * 2 * D, 2 * D, 0);
       p.bias = P + lo.av.b;
-      addend(p, a.Xa, 8 * D, a.edge_src);
-      addend(p, a.Xa + 2 * D, 8 * D, g.edge_dst);
       ps.push_back(p);
       for (int k = 0; k < (ang ? 2 : 1); ++k) {
         const float* W = (k ? Wan : Wbe) + 3 * D * 2 * D;
         GemmProblem q = gp(A, 2 * D, a.zae[t] + k * 2 * D, 4 * D);
         seg(q, a.a[t], D, 0, D, W, 2 * D, 0);
         q.bias = P + (k ? lo.an.b : lo.be.b);
-        addend(q, a.Xa + (4 + 2 * k) * D, 8 * D, a.ang_ctr);
-        addend(q, a.Xb + k * 2 * D, 8 * D, a.ang_b1);
-        addend(q, a.Xb + (4 + 2 * k) * D, 8 * D, a.ang_b2);
         ps.push_back(q);
       }
       CHG_TRY(run_gemms(ps, st, "gemm_z"));
       ps.clear();
     }
     // gates and aggregations
-    if (E > 0) LAUNCH_V(k_gate_atom_fwd, V, (unsigned)cdiv(E, 4), 256, st, (int)E, a.zv[t], a.ea, ln_ptrs(P, lo.av), a.msg);
+    const GateAdds ad_av = adds(2, a.Xa[t], 8 * D, a.edge_src, a.Xa[t] + 2 * D, 8 * D, g.edge_dst);
+    const GateAdds ad_be = adds(3, a.Xa[t] + 4 * D, 8 * D, a.ang_ctr, a.Xb[t], 8 * D, a.ang_b1, a.Xb[t] + 4 * D, 8 * D,
+                                a.ang_b2);
+    const GateAdds ad_an = adds(3, a.Xa[t] + 6 * D, 8 * D, a.ang_ctr, a.Xb[t] + 2 * D, 8 * D, a.ang_b1,
+                                a.Xb[t] + 6 * D, 8 * D, a.ang_b2);
+    CHG_TRY(gate_fwd<FWD_ATOM>(D, E, a.zv[t], 2 * D, ad_av, ln_ptrs(P, lo.av), a.ea, nullptr, a.msg, st,
+                               "k_gate_atom_fwd"));
     CHG_TRY(segsum(N, g.edge_ptr, nullptr, a.msg, D, D, a.m[t], D, 0, nullptr, 0, nullptr, 0, st));
-    if (A > 0)
-      LAUNCH_V(k_gate_angle_fwd, V, (unsigned)cdiv(A, 4), 256, st, (int)A, a.zae[t], ang ? 1 : 0, a.eb, a.ang_b2,
-               ln_ptrs(P, lo.be), ln_ptrs(P, ang ? lo.an : lo.be), a.a[t], ang ? a.a[t + 1] : a.a[t], a.msgb);
+    CHG_TRY(gate_fwd<FWD_BOND>(D, A, a.zae[t], 4 * D, ad_be, ln_ptrs(P, lo.be), a.eb, a.ang_b2, a.msgb, st,
+                               "k_gate_bond_fwd"));
+    if (ang)
+      CHG_TRY(gate_fwd<FWD_ANGLE>(D, A, a.zae[t] + 2 * D, 4 * D, ad_an, ln_ptrs(P, lo.an), a.a[t], nullptr, a.a[t + 1],
+                                  st, "k_gate_angle_fwd"));
     CHG_TRY(segsum(B, g.angle_ptr, nullptr, a.msgb, D, D, a.ssum[t], D, 0, a.eb, D, a.mu[t], D, st));
     // updates: v' = v + m Wo + bo; e' = e (+ mu Wo + bo on bonds)
     if (E > 0) {
@@ -1200,26 +1282,33 @@ int backward_impl(Ctx& c, const float* Pflat, bool repack, const float* dE, cons
       CHG_TRY(run_tns(ts, a, st, "tn_out"));
       ts.clear();
     }
-    // angle gates
-    const int64_t ablocks = cdiv(A, kGateRowsPerBlock);
-    if (A > 0) {
-      LAUNCH_V(k_gate_angle_bwd, V, (unsigned)ablocks, 1024, st, (int)A, a.zae[t], ang ? 1 : 0, a.eb, a.ang_b1, a.ang_b2,
-               a.dmu, a.da[cur], ln_ptrs(P, lo.be), ln_ptrs(P, ang ? lo.an : lo.be), a.dzae, a.t2, a.lnpart);
-      CHG_TRY(reduce_rows_launch(a.lnpart, (int)ablocks, 8 * D, 4 * D, G + lg.be.g_c, st));
-      if (ang) CHG_TRY(reduce_rows_launch(a.lnpart + 4 * D, (int)ablocks, 8 * D, 4 * D, G + lg.an.g_c, st));
-    }
+    // angle gates (bond conv, then angle update)
+    const GateAdds ad_av = adds(2, a.Xa[t], 8 * D, a.edge_src, a.Xa[t] + 2 * D, 8 * D, g.edge_dst);
+    const GateAdds ad_be = adds(3, a.Xa[t] + 4 * D, 8 * D, a.ang_ctr, a.Xb[t], 8 * D, a.ang_b1, a.Xb[t] + 4 * D, 8 * D,
+                                a.ang_b2);
+    const GateAdds ad_an = adds(3, a.Xa[t] + 6 * D, 8 * D, a.ang_ctr, a.Xb[t] + 2 * D, 8 * D, a.ang_b1,
+                                a.Xb[t] + 6 * D, 8 * D, a.ang_b2);
+    CHG_TRY(gate_bwd<BWD_BOND>(D, A, a.zae[t], 4 * D, ad_be, ln_ptrs(P, lo.be), a.dmu, a.ang_b1, a.eb, a.ang_b2, a.t2,
+                               a.dzae, 4 * D, a, G + lg.be.g_c, st, "k_gate_bond_bwd"));
+    if (ang)
+      CHG_TRY(gate_bwd<BWD_ANGLE>(D, A, a.zae[t] + 2 * D, 4 * D, ad_an, ln_ptrs(P, lo.an), a.da[cur], nullptr, nullptr,
+                                  nullptr, nullptr, a.dzae + 2 * D, 4 * D, a, G + lg.an.g_c, st, "k_gate_angle_bwd"));
     if (B > 0) {
-      KLAUNCH(st, "k_bond_bwd_reduce", k_bond_bwd_reduce<<<(unsigned)cdiv(B, 4), 256, 0, st>>>((int)B, D, W4, a.bond_src, g.bond_ptr, g.angle_ptr, a.dzae,
-                                                              a.t2, a.dmu, a.ssum[t], a.DZ12, a.deb));
+      const unsigned nb = (unsigned)cdiv(B, 4);
+      const int cpl = W4 / 64;
+#define BOND_REDUCE(CPL, TPL)                                                                                    \
+  KLAUNCH(st, "k_bond_bwd_reduce", k_bond_bwd_reduce<CPL, TPL><<<nb, 256, 0, st>>>((int)B, D, a.bond_src, g.bond_ptr, \
+                                                       g.angle_ptr, a.dzae, a.t2, a.dmu, a.ssum[t], a.DZ12, a.deb))
+      if (cpl == 2) BOND_REDUCE(2, 1);
+      else if (cpl == 4 && D == 64) BOND_REDUCE(4, 1);
+      else if (cpl == 4) BOND_REDUCE(4, 2);
+      else BOND_REDUCE(8, 2);
+#undef BOND_REDUCE
     }
     CHG_TRY(segsum(N, g.bond_ptr, nullptr, a.DZ12, 8 * D, W4, a.AT + 4 * D, 8 * D, 0, nullptr, 0, nullptr, 0, st));
     // atom conv gate
-    const int64_t eblocks = cdiv(E, kGateRowsPerBlock);
-    if (E > 0) {
-      LAUNCH_V(k_gate_atom_bwd, V, (unsigned)eblocks, 1024, st, (int)E, a.zv[t], a.ea, a.dm, a.edge_src, ln_ptrs(P, lo.av),
-               a.dzv, a.dea, a.lnpart);
-      CHG_TRY(reduce_rows_launch(a.lnpart, (int)eblocks, 4 * D, 4 * D, G + lg.av.g_c, st));
-    }
+    CHG_TRY(gate_bwd<BWD_ATOM>(D, E, a.zv[t], 2 * D, ad_av, ln_ptrs(P, lo.av), a.dm, a.edge_src, a.ea, nullptr, a.dea,
+                               a.dzv, 2 * D, a, G + lg.av.g_c, st, "k_gate_atom_bwd"));
     CHG_TRY(segsum(N, g.edge_ptr, nullptr, a.dzv, 2 * D, 2 * D, a.AT, 8 * D, 0, nullptr, 0, nullptr, 0, st));
     CHG_TRY(segsum(N, g.edge_ptr, g.edge_rev, a.dzv, 2 * D, 2 * D, a.AT + 2 * D, 8 * D, 0, nullptr, 0, nullptr, 0, st));
     // input gradients
@@ -1306,13 +1395,13 @@ int backward_impl(Ctx& c, const float* Pflat, bool repack, const float* dE, cons
       const int64_t nb = cdiv(E, kFreqRowsPerBlock);
       KLAUNCH(st, "k_rbf_fgrad", k_rbf_fgrad<<<(unsigned)nb, 256, 0, st>>>((int)E, nullptr, a.edge_len, P + L.f_a, m.R, c.hp->r_atom,
                                                 c.hp->envelope_p, a.drbf_a, a.fpart));
-      CHG_TRY(reduce_rows_launch(a.fpart, (int)nb, m.R, m.R, G + Lg.f_a, st));
+      CHG_TRY(reduce_rows_launch(a.fpart, (int)nb, m.R, m.R, G + Lg.f_a, a.red2, st));
     }
     if (B > 0) {
       const int64_t nb = cdiv(B, kFreqRowsPerBlock);
       KLAUNCH(st, "k_rbf_fgrad", k_rbf_fgrad<<<(unsigned)nb, 256, 0, st>>>((int)B, g.bond_edge, a.edge_len, P + L.f_b, m.R, c.hp->r_bond,
                                                 c.hp->envelope_p, a.drbf_b, a.fpart));
-      CHG_TRY(reduce_rows_launch(a.fpart, (int)nb, m.R, m.R, G + Lg.f_b, st));
+      CHG_TRY(reduce_rows_launch(a.fpart, (int)nb, m.R, m.R, G + Lg.f_b, a.red2, st));
     }
   }
   return CHGNET_OK;
