@@ -85,26 +85,22 @@ __device__ __forceinline__ void gemm_fetch(const GemmProblem& P, const GemmSeg& 
   }
 }
 
-template <int BN, int NADD>
+template <int BN>
 __global__ void __launch_bounds__(256) k_gemm(GemmBatch batch) {
-  constexpr int BM = 128, KC = 32, NT = BN / 32, KP = KC + 4;
+  constexpr int BM = 128, KC = 32, NT = BN / 32, KP = KC + 4, SP = 64 + 4;
   const GemmProblem& P = batch.p[blockIdx.z];
   const int r0 = blockIdx.x * BM, c0 = blockIdx.y * BN;
   if (r0 >= P.M || c0 >= P.N) return;
-  // Tiles are stored k-contiguous: As[row][k], Bs[col][k]. In MFMA k-step i,
-  // lane half h = lane / 32 supplies k = 16 h + i, so each lane reads its 16
-  // A and B values of a chunk with four 16-byte LDS reads.
-  __shared__ __attribute__((aligned(16))) float As[BM][KP];
-  __shared__ __attribute__((aligned(16))) float Bs[BN][KP];
-  __shared__ int64_t ridx[NADD + 2][BM];  // addend rows, residual row, output row
+  // Operand tiles are stored k-contiguous: As[row][k], Bs[col][k]. In MFMA
+  // k-step i, lane half h = lane / 32 supplies k = 16 h + i, so each lane
+  // reads its 16 A and B values of a chunk with four 16-byte LDS reads.
+  // After the K loop the same LDS holds the output tile, 64 columns at a
+  // time, so the epilogue writes whole rows with 16-byte stores.
+  constexpr int kOperand = BM * KP + BN * KP, kStage = 4 * 32 * SP;
+  __shared__ __attribute__((aligned(16))) float smem[kOperand > kStage ? kOperand : kStage];
+  float (*As)[KP] = reinterpret_cast<float (*)[KP]>(smem);
+  float (*Bs)[KP] = reinterpret_cast<float (*)[KP]>(smem + BM * KP);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, h = lane >> 5;
-  if (tid < BM) {
-    const int row = min(r0 + tid, P.M - 1);
-#pragma unroll
-    for (int q = 0; q < NADD; ++q) ridx[q][tid] = (P.add_rows[q] ? P.add_rows[q][row] : row) * (int64_t)P.add_ld[q];
-    ridx[NADD][tid] = P.res ? (P.res_rows ? P.res_rows[row] : row) * (int64_t)P.res_ld : 0;
-    ridx[NADD + 1][tid] = (P.c_rows ? P.c_rows[row] : row) * (int64_t)P.ldc;
-  }
   v16f acc[NT];
 #pragma unroll
   for (int t = 0; t < NT; ++t)
@@ -169,51 +165,90 @@ __global__ void __launch_bounds__(256) k_gemm(GemmBatch batch) {
       for (int t = 0; t < NT; ++t) acc[t] = __builtin_amdgcn_mfma_f32_32x32x2f32(af[i], bf[t][i], acc[t], 0, 0, 0);
     __syncthreads();
   }
-  __syncthreads();
-  // epilogue: acc[t][j] is C(row, col) with row = 8(j/4) + 4(lane/32) + j%4
-  float bias[NT];
+  // ---- epilogue, 64 columns (two 32x32 tiles) at a time through LDS
+  float* stg = smem + wave * 32 * SP;
+  const bool cvec = (P.ldc & 3) == 0 && ((uintptr_t)P.C & 15) == 0 && (!P.res || ((P.res_ld & 3) == 0 && ((uintptr_t)P.res & 15) == 0)) &&
+                    (P.act != ACT_DSILU_MUL || ((P.mul_ld & 3) == 0 && ((uintptr_t)P.mul & 15) == 0)) &&
+                    (P.act != ACT_SILU_OUT || ((P.ldc2 & 3) == 0 && ((uintptr_t)P.C2 & 15) == 0));
 #pragma unroll
-  for (int t = 0; t < NT; ++t) {
-    const int col = c0 + 32 * t + (lane & 31);
-    bias[t] = (P.bias && col < P.N) ? P.bias[col] : 0.f;
-  }
+  for (int half = 0; half < (NT + 1) / 2; ++half) {
 #pragma unroll
-  for (int j = 0; j < 16; ++j) {
-    const int lr = 32 * wave + 8 * (j >> 2) + 4 * (lane >> 5) + (j & 3);
-    const int row = r0 + lr;
-    if (row >= P.M) continue;
-    int64_t addr[NADD > 0 ? NADD : 1];
+    for (int tt = 0; tt < 2; ++tt) {
+      if (2 * half + tt >= NT) break;
 #pragma unroll
-    for (int q = 0; q < NADD; ++q) addr[q] = ridx[q][lr];
-    const int64_t rr = ridx[NADD][lr], cr = ridx[NADD + 1][lr];
-#pragma unroll
-    for (int t = 0; t < NT; ++t) {
-      const int col = c0 + 32 * t + (lane & 31);
-      if (col >= P.N) continue;
-      float v = acc[t][j];
-      if (P.act == ACT_DSILU_MUL) {
-        const float x = P.mul[(int64_t)row * P.mul_ld + col];
-        const float sg = sigm(x);
-        v *= sg * (1.0f + x * (1.0f - sg));
-      }
-      v += bias[t];
-#pragma unroll
-      for (int q = 0; q < NADD; ++q) v += P.add[q][addr[q] + col];
-      if (P.res) v += P.res[rr + col];
-      float* dst = P.C + cr + col;
-      *dst = P.accumulate ? *dst + v : v;
-      if (P.act == ACT_SILU_OUT) P.C2[(int64_t)row * P.ldc2 + col] = v * sigm(v);
+      for (int j = 0; j < 16; ++j)
+        stg[(8 * (j >> 2) + 4 * h + (j & 3)) * SP + 32 * tt + (lane & 31)] = acc[2 * half + tt][j];
     }
+    __syncthreads();
+    // lane: rows (lane / 16) + 4 i, columns 4 (lane % 16) .. +3 of this half
+    const int cl = 4 * (lane & 15);
+    const int col = c0 + 64 * half + cl;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int lr = (lane >> 4) + 4 * i;
+      const int row = r0 + 32 * wave + lr;
+      if (row >= P.M || col >= P.N) continue;
+      float v[4];
+      const float4 sv = *reinterpret_cast<const float4*>(stg + lr * SP + cl);
+      v[0] = sv.x; v[1] = sv.y; v[2] = sv.z; v[3] = sv.w;
+      const int64_t rr = P.res ? (P.res_rows ? P.res_rows[row] : row) * (int64_t)P.res_ld : 0;
+      const int64_t cr = (P.c_rows ? P.c_rows[row] : row) * (int64_t)P.ldc;
+      if (cvec && col + 3 < P.N) {
+        if (P.act == ACT_DSILU_MUL) {
+          const float4 x4 = *reinterpret_cast<const float4*>(P.mul + (int64_t)row * P.mul_ld + col);
+          const float xs[4] = {x4.x, x4.y, x4.z, x4.w};
+#pragma unroll
+          for (int u = 0; u < 4; ++u) {
+            const float sg = sigm(xs[u]);
+            v[u] *= sg * (1.0f + xs[u] * (1.0f - sg));
+          }
+        }
+        if (P.bias)
+#pragma unroll
+          for (int u = 0; u < 4; ++u) v[u] += P.bias[col + u];
+        if (P.res) {
+          const float4 r4 = *reinterpret_cast<const float4*>(P.res + rr + col);
+          v[0] += r4.x; v[1] += r4.y; v[2] += r4.z; v[3] += r4.w;
+        }
+        float4* dst = reinterpret_cast<float4*>(P.C + cr + col);
+        if (P.accumulate) {
+          const float4 o = *dst;
+          v[0] += o.x; v[1] += o.y; v[2] += o.z; v[3] += o.w;
+        }
+        *dst = make_float4(v[0], v[1], v[2], v[3]);
+        if (P.act == ACT_SILU_OUT)
+          *reinterpret_cast<float4*>(P.C2 + (int64_t)row * P.ldc2 + col) =
+              make_float4(v[0] * sigm(v[0]), v[1] * sigm(v[1]), v[2] * sigm(v[2]), v[3] * sigm(v[3]));
+      } else {
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int cc = col + u;
+          if (cc >= P.N) break;
+          float x = v[u];
+          if (P.act == ACT_DSILU_MUL) {
+            const float m = P.mul[(int64_t)row * P.mul_ld + cc];
+            const float sg = sigm(m);
+            x *= sg * (1.0f + m * (1.0f - sg));
+          }
+          if (P.bias) x += P.bias[cc];
+          if (P.res) x += P.res[rr + cc];
+          float* dst = P.C + cr + cc;
+          *dst = P.accumulate ? *dst + x : x;
+          if (P.act == ACT_SILU_OUT) P.C2[(int64_t)row * P.ldc2 + cc] = x * sigm(x);
+        }
+      }
+    }
+    __syncthreads();
   }
 }
 
 struct TnPlan {
   TnProblem p;
-  int rpc;       // rows per chunk
+  int rpc;      // rows per chunk
   int nchunks;
-  int tiles_n;   // tiles along n
-  int tiles;     // total 64x64 tiles
-  int64_t off;   // partial offset
+  int tiles_n;  // tiles along n
+  int tiles;    // total output tiles
+  int64_t off;  // partial offset
 };
 struct TnLaunch {
   int n;
@@ -283,13 +318,19 @@ __global__ void __launch_bounds__(256) k_tn(TnLaunch L, float* __restrict__ part
     }
     __syncthreads();
     if (rb + RC < rhi) fetch(rb + RC);
+    // lane half h takes rows 16h .. 16h+15 of the chunk (k-step i -> row 16h+i)
+    float af[16], bf0[16], bf1[16];
+    const int h = lane >> 5;
 #pragma unroll
-    for (int kk = 0; kk < RC; kk += 2) {
-      const float a = Xs[kk + (lane >> 5)][wm + (lane & 31)];
-      const float b0 = Ys[kk + (lane >> 5)][wn + (lane & 31)];
-      const float b1 = Ys[kk + (lane >> 5)][wn + 32 + (lane & 31)];
-      acc[0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a, b0, acc[0], 0, 0, 0);
-      acc[1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a, b1, acc[1], 0, 0, 0);
+    for (int i = 0; i < 16; ++i) {
+      af[i] = Xs[16 * h + i][wm + (lane & 31)];
+      bf0[i] = Ys[16 * h + i][wn + (lane & 31)];
+      bf1[i] = Ys[16 * h + i][wn + 32 + (lane & 31)];
+    }
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      acc[0] = __builtin_amdgcn_mfma_f32_32x32x2f32(af[i], bf0[i], acc[0], 0, 0, 0);
+      acc[1] = __builtin_amdgcn_mfma_f32_32x32x2f32(af[i], bf1[i], acc[1], 0, 0, 0);
     }
     __syncthreads();
   }
@@ -334,7 +375,9 @@ __global__ void __launch_bounds__(1024) k_tn_reduce(TnLaunch L, const float* __r
     double s = 0.0;
     for (int q = 0; q < 16; ++q) s += red[q][lane];
     const int m = (int)(k / P.N), n = (int)(k % P.N);
-    float* o = P.out + (int64_t)m * P.ld_out + n;
+    const int q = P.owidth > 0 ? n / P.owidth : 0;
+    const int nn = P.owidth > 0 ? n - q * P.owidth : n;
+    float* o = (q == 0 ? P.out : P.outs[q]) + (int64_t)m * P.ld_out + nn;
     *o = (float)((double)*o + s);
   }
 }
@@ -365,36 +408,20 @@ __global__ void k_reduce_rows2(const double* __restrict__ part2, int groups, int
 
 }  // namespace
 
-template <int BN>
-int gemm_launch_bn(const GemmBatch& b, int nadd, dim3 grid, hipStream_t st, const char* tag) {
-  switch (nadd) {
-    case 0: KLAUNCH(st, tag, k_gemm<BN, 0><<<grid, 256, 0, st>>>(b)); break;
-    case 1: KLAUNCH(st, tag, k_gemm<BN, 1><<<grid, 256, 0, st>>>(b)); break;
-    case 2: KLAUNCH(st, tag, k_gemm<BN, 2><<<grid, 256, 0, st>>>(b)); break;
-    default: KLAUNCH(st, tag, k_gemm<BN, 3><<<grid, 256, 0, st>>>(b)); break;
-  }
-  return CHGNET_OK;
-}
-
 int gemm_launch(const GemmBatch& b, hipStream_t st, const char* tag) {
-  // problems with different addend counts go to separate launches
-  for (int nadd = 0; nadd <= 3; ++nadd) {
-    GemmBatch g{};
-    for (int i = 0; i < b.n; ++i)
-      if (b.p[i].nadd == nadd) g.p[g.n++] = b.p[i];
-    if (g.n == 0) continue;
-    int minN = 1 << 30;
-    for (int i = 0; i < g.n; ++i) minN = std::min(minN, g.p[i].N);
-    const int BN = minN >= 128 ? 128 : 64;
-    int gx = 0, gy = 0;
-    for (int i = 0; i < g.n; ++i) {
-      gx = std::max<int>(gx, (int)cdiv(g.p[i].M, 128));
-      gy = std::max<int>(gy, (int)cdiv(g.p[i].N, BN));
-    }
-    if (gx == 0 || gy == 0) continue;
-    const dim3 grid(gx, gy, g.n);
-    CHG_TRY(BN == 128 ? gemm_launch_bn<128>(g, nadd, grid, st, tag) : gemm_launch_bn<64>(g, nadd, grid, st, tag));
+  if (b.n == 0) return CHGNET_OK;
+  // 64-column tiles: the 128-column variant needs ~170 VGPRs (2 waves per
+  // SIMD) and measured slower on every shape used here
+  const int BN = 64;
+  int gx = 0, gy = 0;
+  for (int i = 0; i < b.n; ++i) {
+    gx = std::max<int>(gx, (int)cdiv(b.p[i].M, 128));
+    gy = std::max<int>(gy, (int)cdiv(b.p[i].N, BN));
   }
+  if (gx == 0 || gy == 0) return CHGNET_OK;
+  const dim3 grid(gx, gy, b.n);
+  if (BN == 128) KLAUNCH(st, tag, k_gemm<128><<<grid, 256, 0, st>>>(b));
+  else KLAUNCH(st, tag, k_gemm<64><<<grid, 256, 0, st>>>(b));
   return CHGNET_OK;
 }
 

@@ -21,7 +21,7 @@ struct GemmSeg {
 enum GemmAct { ACT_NONE = 0, ACT_SILU_OUT = 1, ACT_DSILU_MUL = 2 };
 
 // C[c_rows(r), c] (+)= sum_seg A[a_rows(r), a_col + k] B(k, c) + bias[c]
-//                      + sum_j add_j[add_rows_j(r), c] + res[res_rows(r), c]
+//                      + res[res_rows(r), c]
 // ACT_SILU_OUT: also C2[r, c] = silu(value).
 // ACT_DSILU_MUL: value *= silu'(mul[r, c]) before bias/adds (backward of an
 //                activation; use without bias/adds/res).
@@ -31,10 +31,6 @@ struct GemmProblem {
   int nseg;
   GemmSeg seg[4];
   const float* bias;
-  int nadd;
-  const float* add[3];
-  int add_ld[3];
-  const int* add_rows[3];
   const float* res;
   int res_ld;
   const int* res_rows;
@@ -70,9 +66,13 @@ struct TnProblem {
   const int* y_rows;
   float* out;  // out[m * ld_out + n] += result
   int ld_out;
+  // optional column split: columns [q*owidth, (q+1)*owidth) go to outs[q]
+  // (outs[0] unused: out), owidth = 0 means a single output
+  int owidth;
+  float* outs[4];
 };
 
-constexpr int kMaxTnProblems = 12;
+constexpr int kMaxTnProblems = 16;
 struct TnBatch {
   int n;
   TnProblem p[kMaxTnProblems];

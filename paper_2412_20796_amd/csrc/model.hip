@@ -830,12 +830,6 @@ void seg(GemmProblem& p, const float* A, int lda, int a_col, int K, const float*
   s.ldb = ldb;
   s.trans = trans;
 }
-void addend(GemmProblem& p, const float* X, int ld, const int* rows) {
-  p.add[p.nadd] = X;
-  p.add_ld[p.nadd] = ld;
-  p.add_rows[p.nadd] = rows;
-  p.nadd++;
-}
 
 int run_gemms(const std::vector<GemmProblem>& ps, hipStream_t st, const char* tag) {
   GemmBatch b{};
@@ -867,6 +861,14 @@ TnProblem tp(int64_t R, int M, int Nn, const float* X, int ldx, int x_col, const
   p.y_rows = y_rows;
   p.out = out;
   p.ld_out = ld_out;
+  return p;
+}
+
+TnProblem split_out(TnProblem p, int owidth, float* o1, float* o2 = nullptr, float* o3 = nullptr) {
+  p.owidth = owidth;
+  p.outs[1] = o1;
+  p.outs[2] = o2;
+  p.outs[3] = o3;
   return p;
 }
 
@@ -1240,15 +1242,18 @@ int backward_impl(Ctx& c, const float* Pflat, bool repack, const float* dE, cons
     std::vector<TnProblem> ts;
     for (auto& l : ls) {
       const int o = l.h->out;
-      const float* dh1_base = l.dh1base;
-      const int dh1_col = l.dh1col;
       ts.push_back(tp(l.M, D, o, l.a2, D, 0, nullptr, l.dout, o, 0, nullptr, G + l.hg->W3, o));
       ts.push_back(tp(l.M, 1, o, nullptr, 0, 0, nullptr, l.dout, o, 0, nullptr, G + l.hg->b3, o));
       ts.push_back(tp(l.M, D, D, l.a1, D, 0, nullptr, l.dh2, D, 0, nullptr, G + l.hg->W2, D));
       ts.push_back(tp(l.M, 1, D, nullptr, 0, 0, nullptr, l.dh2, D, 0, nullptr, G + l.hg->b2, D));
-      ts.push_back(tp(l.M, D, D, l.in, D, 0, nullptr, dh1_base, l.ld1, dh1_col, nullptr, G + l.hg->W1, D));
-      ts.push_back(tp(l.M, 1, D, nullptr, 0, 0, nullptr, dh1_base, l.ld1, dh1_col, nullptr, G + l.hg->b1, D));
     }
+    // first layers: energy and stress heads share the input v^T
+    ts.push_back(split_out(tp(N, D, 2 * D, a.v[m.T], D, 0, nullptr, a.dh1ES, 2 * D, 0, nullptr, G + Lg.head[0].W1, D), D,
+                           G + Lg.head[2].W1));
+    ts.push_back(split_out(tp(N, 1, 2 * D, nullptr, 0, 0, nullptr, a.dh1ES, 2 * D, 0, nullptr, G + Lg.head[0].b1, D), D,
+                           G + Lg.head[2].b1));
+    ts.push_back(tp(E, D, D, a.e[m.T], D, 0, nullptr, a.dh1F, D, 0, nullptr, G + Lg.head[1].W1, D));
+    ts.push_back(tp(E, 1, D, nullptr, 0, 0, nullptr, a.dh1F, D, 0, nullptr, G + Lg.head[1].b1, D));
     CHG_TRY(run_tns(ts, a, st, "tn_heads"));
   }
 
@@ -1353,17 +1358,25 @@ int backward_impl(Ctx& c, const float* Pflat, bool repack, const float* dE, cons
     {
       const float* vt = a.v[t];
       const float* et = a.e[t];
-      ts.push_back(tp(N, D, 2 * D, vt, D, 0, nullptr, a.AT, 8 * D, 0, nullptr, G + lg.av.W, 2 * D));
-      ts.push_back(tp(N, D, 2 * D, vt, D, 0, nullptr, a.AT, 8 * D, 2 * D, nullptr, G + lg.av.W + D * 2 * D, 2 * D));
+      // v^T [dP | dQ | DZa_bond | DZa_angle] -> atom-role blocks of the three first layers
+      ts.push_back(split_out(tp(N, D, (ang ? 8 : 6) * D, vt, D, 0, nullptr, a.AT, 8 * D, 0, nullptr, G + lg.av.W, 2 * D),
+                             2 * D, G + lg.av.W + D * 2 * D, G + lg.be.W, ang ? G + lg.an.W : nullptr));
       ts.push_back(tp(E, D, 2 * D, et, D, 0, nullptr, a.dzv, 2 * D, 0, nullptr, G + lg.av.W + 2 * D * 2 * D, 2 * D));
+      // biases: sum over atoms of dP (= sum over edges of dz) and of DZa
       ts.push_back(tp(N, 1, 2 * D, nullptr, 0, 0, nullptr, a.AT, 8 * D, 0, nullptr, G + lg.av.b, 2 * D));
-      for (int k = 0; k < (ang ? 2 : 1); ++k) {
-        const GatedOffsets& go = k ? lg.an : lg.be;
-        ts.push_back(tp(N, D, 2 * D, vt, D, 0, nullptr, a.AT, 8 * D, (4 + 2 * k) * D, nullptr, G + go.W, 2 * D));
-        ts.push_back(tp(B, D, 2 * D, et, D, 0, g.bond_edge, a.DZ12, 8 * D, 2 * k * D, nullptr, G + go.W + D * 2 * D, 2 * D));
-        ts.push_back(tp(B, D, 2 * D, et, D, 0, g.bond_edge, a.DZ12, 8 * D, (4 + 2 * k) * D, nullptr, G + go.W + 2 * D * 2 * D, 2 * D));
-        ts.push_back(tp(A, D, 2 * D, a.a[t], D, 0, nullptr, a.dzae, 4 * D, 2 * k * D, nullptr, G + go.W + 3 * D * 2 * D, 2 * D));
-        ts.push_back(tp(N, 1, 2 * D, nullptr, 0, 0, nullptr, a.AT, 8 * D, (4 + 2 * k) * D, nullptr, G + go.b, 2 * D));
+      ts.push_back(split_out(tp(N, 1, (ang ? 4 : 2) * D, nullptr, 0, 0, nullptr, a.AT, 8 * D, 4 * D, nullptr, G + lg.be.b, 2 * D),
+                             2 * D, ang ? G + lg.an.b : nullptr));
+      if (ang) {
+        // e_b^T [DZ1_bond | DZ1_angle | DZ2_bond | DZ2_angle]
+        ts.push_back(split_out(tp(B, D, 8 * D, et, D, 0, g.bond_edge, a.DZ12, 8 * D, 0, nullptr, G + lg.be.W + D * 2 * D, 2 * D),
+                               2 * D, G + lg.an.W + D * 2 * D, G + lg.be.W + 2 * D * 2 * D, G + lg.an.W + 2 * D * 2 * D));
+        // a^T [dz_bond | dz_angle]
+        ts.push_back(split_out(tp(A, D, 4 * D, a.a[t], D, 0, nullptr, a.dzae, 4 * D, 0, nullptr, G + lg.be.W + 3 * D * 2 * D, 2 * D),
+                               2 * D, G + lg.an.W + 3 * D * 2 * D));
+      } else {
+        ts.push_back(tp(B, D, 2 * D, et, D, 0, g.bond_edge, a.DZ12, 8 * D, 0, nullptr, G + lg.be.W + D * 2 * D, 2 * D));
+        ts.push_back(tp(B, D, 2 * D, et, D, 0, g.bond_edge, a.DZ12, 8 * D, 4 * D, nullptr, G + lg.be.W + 2 * D * 2 * D, 2 * D));
+        ts.push_back(tp(A, D, 2 * D, a.a[t], D, 0, nullptr, a.dzae, 4 * D, 0, nullptr, G + lg.be.W + 3 * D * 2 * D, 2 * D));
       }
       CHG_TRY(run_tns(ts, a, st, "tn_in"));
       ts.clear();
