@@ -85,6 +85,66 @@ __device__ __forceinline__ void gemm_fetch(const GemmProblem& P, const GemmSeg& 
   }
 }
 
+// Epilogue of one row and 4 consecutive columns: activation, bias,
+// residual, optional accumulation, 16-byte stores when aligned.
+__device__ __forceinline__ bool gemm_cvec(const GemmProblem& P) {
+  return (P.ldc & 3) == 0 && ((uintptr_t)P.C & 15) == 0 &&
+         (!P.res || ((P.res_ld & 3) == 0 && ((uintptr_t)P.res & 15) == 0)) &&
+         (P.act != ACT_DSILU_MUL || ((P.mul_ld & 3) == 0 && ((uintptr_t)P.mul & 15) == 0)) &&
+         (P.act != ACT_SILU_OUT || ((P.ldc2 & 3) == 0 && ((uintptr_t)P.C2 & 15) == 0));
+}
+
+__device__ __forceinline__ void gemm_store4(const GemmProblem& P, int row, int col, float4 sv, bool cvec) {
+  if (row >= P.M || col >= P.N) return;
+  float v[4] = {sv.x, sv.y, sv.z, sv.w};
+  const int64_t rr = P.res ? (P.res_rows ? P.res_rows[row] : row) * (int64_t)P.res_ld : 0;
+  const int64_t cr = (P.c_rows ? P.c_rows[row] : row) * (int64_t)P.ldc;
+  if (cvec && col + 3 < P.N) {
+    if (P.act == ACT_DSILU_MUL) {
+      const float4 x4 = *reinterpret_cast<const float4*>(P.mul + (int64_t)row * P.mul_ld + col);
+      const float xs[4] = {x4.x, x4.y, x4.z, x4.w};
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const float sg = sigm(xs[u]);
+        v[u] *= sg * (1.0f + xs[u] * (1.0f - sg));
+      }
+    }
+    if (P.bias)
+#pragma unroll
+      for (int u = 0; u < 4; ++u) v[u] += P.bias[col + u];
+    if (P.res) {
+      const float4 r4 = *reinterpret_cast<const float4*>(P.res + rr + col);
+      v[0] += r4.x; v[1] += r4.y; v[2] += r4.z; v[3] += r4.w;
+    }
+    float4* dst = reinterpret_cast<float4*>(P.C + cr + col);
+    if (P.accumulate) {
+      const float4 o = *dst;
+      v[0] += o.x; v[1] += o.y; v[2] += o.z; v[3] += o.w;
+    }
+    *dst = make_float4(v[0], v[1], v[2], v[3]);
+    if (P.act == ACT_SILU_OUT)
+      *reinterpret_cast<float4*>(P.C2 + (int64_t)row * P.ldc2 + col) =
+          make_float4(v[0] * sigm(v[0]), v[1] * sigm(v[1]), v[2] * sigm(v[2]), v[3] * sigm(v[3]));
+    return;
+  }
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const int cc = col + u;
+    if (cc >= P.N) break;
+    float x = v[u];
+    if (P.act == ACT_DSILU_MUL) {
+      const float m = P.mul[(int64_t)row * P.mul_ld + cc];
+      const float sg = sigm(m);
+      x *= sg * (1.0f + m * (1.0f - sg));
+    }
+    if (P.bias) x += P.bias[cc];
+    if (P.res) x += P.res[rr + cc];
+    float* dst = P.C + cr + cc;
+    *dst = P.accumulate ? *dst + x : x;
+    if (P.act == ACT_SILU_OUT) P.C2[(int64_t)row * P.ldc2 + cc] = x * sigm(x);
+  }
+}
+
 template <int BN>
 __global__ void __launch_bounds__(256) k_gemm(GemmBatch batch) {
   constexpr int BM = 128, KC = 32, NT = BN / 32, KP = KC + 4, SP = 64 + 4;
@@ -167,9 +227,7 @@ __global__ void __launch_bounds__(256) k_gemm(GemmBatch batch) {
   }
   // ---- epilogue, 64 columns (two 32x32 tiles) at a time through LDS
   float* stg = smem + wave * 32 * SP;
-  const bool cvec = (P.ldc & 3) == 0 && ((uintptr_t)P.C & 15) == 0 && (!P.res || ((P.res_ld & 3) == 0 && ((uintptr_t)P.res & 15) == 0)) &&
-                    (P.act != ACT_DSILU_MUL || ((P.mul_ld & 3) == 0 && ((uintptr_t)P.mul & 15) == 0)) &&
-                    (P.act != ACT_SILU_OUT || ((P.ldc2 & 3) == 0 && ((uintptr_t)P.C2 & 15) == 0));
+  const bool cvec = gemm_cvec(P);
 #pragma unroll
   for (int half = 0; half < (NT + 1) / 2; ++half) {
 #pragma unroll
@@ -186,59 +244,126 @@ __global__ void __launch_bounds__(256) k_gemm(GemmBatch batch) {
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
       const int lr = (lane >> 4) + 4 * i;
-      const int row = r0 + 32 * wave + lr;
-      if (row >= P.M || col >= P.N) continue;
-      float v[4];
       const float4 sv = *reinterpret_cast<const float4*>(stg + lr * SP + cl);
-      v[0] = sv.x; v[1] = sv.y; v[2] = sv.z; v[3] = sv.w;
-      const int64_t rr = P.res ? (P.res_rows ? P.res_rows[row] : row) * (int64_t)P.res_ld : 0;
-      const int64_t cr = (P.c_rows ? P.c_rows[row] : row) * (int64_t)P.ldc;
-      if (cvec && col + 3 < P.N) {
-        if (P.act == ACT_DSILU_MUL) {
-          const float4 x4 = *reinterpret_cast<const float4*>(P.mul + (int64_t)row * P.mul_ld + col);
-          const float xs[4] = {x4.x, x4.y, x4.z, x4.w};
+      gemm_store4(P, r0 + 32 * wave + lr, col, sv, cvec);
+    }
+    __syncthreads();
+  }
+}
+
+// Small-M variant: a 32 x 64 output tile per block; the four wavefronts take
+// every fourth K chunk (each with its own LDS tiles) and their partial tiles
+// are added in wavefront order at the end.
+__global__ void __launch_bounds__(256) k_gemm_ks(GemmBatch batch) {
+  constexpr int BM = 32, BN = 64, KC = 32, KP = KC + 4, SP = BN + 4;
+  const GemmProblem& P = batch.p[blockIdx.z];
+  const int r0 = blockIdx.x * BM, c0 = blockIdx.y * BN;
+  if (r0 >= P.M || c0 >= P.N) return;
+  constexpr int kWave = BM * KP + BN * KP;  // floats of one wavefront's tiles
+  __shared__ __attribute__((aligned(16))) float smem[4 * kWave > 4 * BM * SP ? 4 * kWave : 4 * BM * SP];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, h = lane >> 5;
+  float (*As)[KP] = reinterpret_cast<float (*)[KP]>(smem + wave * kWave);
+  float (*Bs)[KP] = reinterpret_cast<float (*)[KP]>(smem + wave * kWave + BM * KP);
+  v16f acc[2];
+#pragma unroll
+  for (int t = 0; t < 2; ++t)
+#pragma unroll
+    for (int j = 0; j < 16; ++j) acc[t][j] = 0.f;
+  // A loads: lane -> row lane / 2, 16 consecutive k at 16 (lane & 1)
+  const int arl = lane >> 1, akl = 16 * (lane & 1);
+  const int arow_i = r0 + arl;
+  const bool aval = arow_i < P.M;
+  const int64_t arow = aval ? (P.a_rows ? P.a_rows[arow_i] : arow_i) : 0;
+  int nch = 0;
+  for (int s = 0; s < P.nseg; ++s) nch += (P.seg[s].K + KC - 1) / KC;
+  const int rounds = (nch + 3) / 4;
+  int s = 0, kc = 0;  // chunk cursor: segment s, chunk kc within it (this wave's next chunk)
+  auto advance = [&](int n) {
+    while (n > 0 && s < P.nseg) {
+      const int left = (P.seg[s].K + KC - 1) / KC - kc;
+      if (n < left) { kc += n; n = 0; } else { n -= left; ++s; kc = 0; }
+    }
+  };
+  advance(wave);
+  for (int rd = 0; rd < rounds; ++rd) {
+    const bool has = s < P.nseg;
+    if (has) {
+      const GemmSeg S = P.seg[s];
+      const int k0 = kc * KC;
+      const bool avec = ((S.lda | S.a_col) & 3) == 0 && ((uintptr_t)S.A & 15) == 0;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (aval) v = load4(S.A + arow * S.lda + S.a_col + k0, akl + 4 * q, S.K - k0, avec);
+        *reinterpret_cast<float4*>(&As[arl][akl + 4 * q]) = v;
+      }
+      const int n = c0 + lane;
+      if (!S.trans) {
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+          float v[4];
 #pragma unroll
           for (int u = 0; u < 4; ++u) {
-            const float sg = sigm(xs[u]);
-            v[u] *= sg * (1.0f + xs[u] * (1.0f - sg));
+            const int k = k0 + 4 * q + u;
+            v[u] = (n < P.N && k < S.K) ? S.B[(int64_t)k * S.ldb + n] : 0.f;
           }
+          *reinterpret_cast<float4*>(&Bs[lane][4 * q]) = make_float4(v[0], v[1], v[2], v[3]);
         }
-        if (P.bias)
-#pragma unroll
-          for (int u = 0; u < 4; ++u) v[u] += P.bias[col + u];
-        if (P.res) {
-          const float4 r4 = *reinterpret_cast<const float4*>(P.res + rr + col);
-          v[0] += r4.x; v[1] += r4.y; v[2] += r4.z; v[3] += r4.w;
-        }
-        float4* dst = reinterpret_cast<float4*>(P.C + cr + col);
-        if (P.accumulate) {
-          const float4 o = *dst;
-          v[0] += o.x; v[1] += o.y; v[2] += o.z; v[3] += o.w;
-        }
-        *dst = make_float4(v[0], v[1], v[2], v[3]);
-        if (P.act == ACT_SILU_OUT)
-          *reinterpret_cast<float4*>(P.C2 + (int64_t)row * P.ldc2 + col) =
-              make_float4(v[0] * sigm(v[0]), v[1] * sigm(v[1]), v[2] * sigm(v[2]), v[3] * sigm(v[3]));
       } else {
+        const bool bvec = (S.ldb & 3) == 0 && ((uintptr_t)S.B & 15) == 0;
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const int cc = col + u;
-          if (cc >= P.N) break;
-          float x = v[u];
-          if (P.act == ACT_DSILU_MUL) {
-            const float m = P.mul[(int64_t)row * P.mul_ld + cc];
-            const float sg = sigm(m);
-            x *= sg * (1.0f + m * (1.0f - sg));
-          }
-          if (P.bias) x += P.bias[cc];
-          if (P.res) x += P.res[rr + cc];
-          float* dst = P.C + cr + cc;
-          *dst = P.accumulate ? *dst + x : x;
-          if (P.act == ACT_SILU_OUT) P.C2[(int64_t)row * P.ldc2 + cc] = x * sigm(x);
+        for (int q = 0; q < 8; ++q) {
+          float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+          if (n < P.N) v = load4(S.B + (int64_t)n * S.ldb + k0, 4 * q, S.K - k0, bvec);
+          *reinterpret_cast<float4*>(&Bs[lane][4 * q]) = v;
         }
       }
     }
     __syncthreads();
+    if (has) {
+      float af[16], bf[2][16];
+      const float* ap = &As[lane & 31][16 * h];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const float4 v = *reinterpret_cast<const float4*>(ap + 4 * q);
+        af[4 * q] = v.x; af[4 * q + 1] = v.y; af[4 * q + 2] = v.z; af[4 * q + 3] = v.w;
+      }
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        const float* bp = &Bs[32 * t + (lane & 31)][16 * h];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const float4 v = *reinterpret_cast<const float4*>(bp + 4 * q);
+          bf[t][4 * q] = v.x; bf[t][4 * q + 1] = v.y; bf[t][4 * q + 2] = v.z; bf[t][4 * q + 3] = v.w;
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < 16; ++i)
+#pragma unroll
+        for (int t = 0; t < 2; ++t) acc[t] = __builtin_amdgcn_mfma_f32_32x32x2f32(af[i], bf[t][i], acc[t], 0, 0, 0);
+      advance(4);
+    }
+    __syncthreads();
+  }
+  // partial tiles of the four wavefronts, summed in wavefront order
+  float* stg = smem + wave * BM * SP;
+#pragma unroll
+  for (int t = 0; t < 2; ++t)
+#pragma unroll
+    for (int j = 0; j < 16; ++j) stg[(8 * (j >> 2) + 4 * h + (j & 3)) * SP + 32 * t + (lane & 31)] = acc[t][j];
+  __syncthreads();
+  const bool cvec = gemm_cvec(P);
+  // 32 rows x 16 float4 columns = 512 float4; thread -> 2 of them
+#pragma unroll
+  for (int q = 0; q < 2; ++q) {
+    const int idx = tid + 256 * q, lr = idx >> 4, cl = 4 * (idx & 15);
+    float4 sum = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      const float4 v = *reinterpret_cast<const float4*>(smem + w * BM * SP + lr * SP + cl);
+      sum.x += v.x; sum.y += v.y; sum.z += v.z; sum.w += v.w;
+    }
+    gemm_store4(P, r0 + lr, c0 + cl, sum, cvec);
   }
 }
 
@@ -351,14 +476,16 @@ __global__ void __launch_bounds__(256) k_tn(TnLaunch L, float* __restrict__ part
 // sums chunks w, w+16, ... (fp64), then the 16 partial sums are added in
 // wave order. The result is independent of scheduling.
 __device__ __forceinline__ double sum_chunks(const float* __restrict__ src, int nchunks, int64_t stride, int w) {
-  double s0 = 0.0, s1 = 0.0;
+  double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
   int c = w;
-  for (; c + 16 < nchunks; c += 32) {
+  for (; c + 48 < nchunks; c += 64) {
     s0 += (double)src[(int64_t)c * stride];
     s1 += (double)src[(int64_t)(c + 16) * stride];
+    s2 += (double)src[(int64_t)(c + 32) * stride];
+    s3 += (double)src[(int64_t)(c + 48) * stride];
   }
-  if (c < nchunks) s0 += (double)src[(int64_t)c * stride];
-  return s0 + s1;
+  for (; c < nchunks; c += 16) s0 += (double)src[(int64_t)c * stride];
+  return (s0 + s1) + (s2 + s3);
 }
 
 __global__ void __launch_bounds__(1024) k_tn_reduce(TnLaunch L, const float* __restrict__ part) {
@@ -382,11 +509,16 @@ __global__ void __launch_bounds__(1024) k_tn_reduce(TnLaunch L, const float* __r
   }
 }
 
-// First level of the ordered row reduction: group g sums chunks
-// [g*per, (g+1)*per) (wave w takes every 4th), in fp64.
-__global__ void __launch_bounds__(256) k_reduce_rows1(const float* __restrict__ part, int nchunks, int per, int64_t stride,
-                                                      int count, double* __restrict__ part2) {
+// Ordered reduction of chunk partials in one launch: block (x, g) sums the
+// chunks of group g for 64 columns (4 wavefronts, fixed order, fp64) into
+// part2[g]; the last block of column block x to finish (atomic ticket) adds
+// the groups in group order and resets the ticket. The arithmetic order is
+// fixed; only which block performs the final sum depends on scheduling.
+__global__ void __launch_bounds__(256) k_reduce_rows(const float* __restrict__ part, int nchunks, int per, int64_t stride,
+                                                     int count, int groups, double* __restrict__ part2,
+                                                     unsigned* __restrict__ tickets, float* __restrict__ out) {
   __shared__ double red[4][64];
+  __shared__ bool last;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int k = blockIdx.x * 64 + lane, g = blockIdx.y;
   const int c0 = g * per, c1 = min(nchunks, c0 + per);
@@ -396,14 +528,29 @@ __global__ void __launch_bounds__(256) k_reduce_rows1(const float* __restrict__ 
   red[w][lane] = s;
   __syncthreads();
   if (w == 0 && k < count) part2[(int64_t)g * count + k] = ((red[0][lane] + red[1][lane]) + red[2][lane]) + red[3][lane];
-}
-
-__global__ void k_reduce_rows2(const double* __restrict__ part2, int groups, int count, float* __restrict__ out) {
-  const int k = blockIdx.x * blockDim.x + threadIdx.x;
-  if (k >= count) return;
-  double s = 0.0;
-  for (int g = 0; g < groups; ++g) s += part2[(int64_t)g * count + k];
-  out[k] = (float)((double)out[k] + s);
+  __threadfence();
+  __syncthreads();
+  if (threadIdx.x == 0) last = atomicAdd(&tickets[blockIdx.x], 1u) == (unsigned)(groups - 1);
+  __syncthreads();
+  if (!last) return;
+  __threadfence();
+  // wave w adds groups w, w+4, ... (loads issued before the adds), then the
+  // four wave sums are added in order
+  double v[8];
+#pragma unroll
+  for (int u = 0; u < 8; ++u) {
+    const int q = w + 4 * u;
+    v[u] = (k < count && q < groups)
+               ? __hip_atomic_load(&part2[(int64_t)q * count + k], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
+               : 0.0;
+  }
+  double t = 0.0;
+#pragma unroll
+  for (int u = 0; u < 8; ++u) t += v[u];
+  red[w][lane] = t;
+  __syncthreads();
+  if (w == 0 && k < count) out[k] = (float)((double)out[k] + (((red[0][lane] + red[1][lane]) + red[2][lane]) + red[3][lane]));
+  if (threadIdx.x == 0) tickets[blockIdx.x] = 0u;
 }
 
 }  // namespace
@@ -419,6 +566,19 @@ int gemm_launch(const GemmBatch& b, hipStream_t st, const char* tag) {
     gy = std::max<int>(gy, (int)cdiv(b.p[i].N, BN));
   }
   if (gx == 0 || gy == 0) return CHGNET_OK;
+  int maxM = 0, maxK = 0;
+  for (int i = 0; i < b.n; ++i) {
+    maxM = std::max(maxM, b.p[i].M);
+    int k = 0;
+    for (int s = 0; s < b.p[i].nseg; ++s) k += b.p[i].seg[s].K;
+    maxK = std::max(maxK, k);
+  }
+  if (maxM <= 32768 && maxK >= 128) {
+    // few row tiles and a long K: split K across the block's wavefronts
+    const dim3 grid((unsigned)cdiv(maxM, 32), gy, b.n);
+    KLAUNCH(st, tag, k_gemm_ks<<<grid, 256, 0, st>>>(b));
+    return CHGNET_OK;
+  }
   const dim3 grid(gx, gy, b.n);
   if (BN == 128) KLAUNCH(st, tag, k_gemm<128><<<grid, 256, 0, st>>>(b));
   else KLAUNCH(st, tag, k_gemm<64><<<grid, 256, 0, st>>>(b));
@@ -438,8 +598,8 @@ int tn_launch(const TnBatch& b, float* part, int64_t part_cap, hipStream_t st, c
     q.tiles_n = (int)cdiv(q.p.N, 128);
     q.tiles = tm * q.tiles_n;
     const int64_t mn = (int64_t)q.p.M * q.p.N;
-    int64_t nch = std::max<int64_t>(1, std::min<int64_t>(cdiv(q.p.R, 256), std::max(8, 512 / q.tiles)));
-    nch = std::min<int64_t>(nch, 128);
+    int64_t nch = std::max<int64_t>(1, std::min<int64_t>(cdiv(q.p.R, 128), std::max(8, 1024 / q.tiles)));
+    nch = std::min<int64_t>(nch, 512);
     nch = std::min<int64_t>(nch, std::max<int64_t>(1, budget / std::max<int64_t>(1, mn)));
     int64_t rpc = cdiv(cdiv(q.p.R, nch), 32) * 32;
     if (rpc < 32) rpc = 32;
@@ -462,13 +622,12 @@ int tn_launch(const TnBatch& b, float* part, int64_t part_cap, hipStream_t st, c
 }
 
 int reduce_rows_launch(const float* part, int nchunks, int64_t stride, int count, float* out, double* scratch,
-                       hipStream_t st) {
+                       unsigned* tickets, hipStream_t st) {
   if (count <= 0) return CHGNET_OK;
   const int groups = std::max(1, std::min(32, nchunks));
   const int per = (int)cdiv(std::max(nchunks, 1), groups);
-  KLAUNCH(st, "k_reduce_rows1", k_reduce_rows1<<<dim3((unsigned)cdiv(count, 64), groups), 256, 0, st>>>(
-                                    part, nchunks, per, stride, count, scratch));
-  KLAUNCH(st, "k_reduce_rows2", k_reduce_rows2<<<(unsigned)cdiv(count, 256), 256, 0, st>>>(scratch, groups, count, out));
+  KLAUNCH(st, "k_reduce_rows", k_reduce_rows<<<dim3((unsigned)cdiv(count, 64), groups), 256, 0, st>>>(
+                                   part, nchunks, per, stride, count, groups, scratch, tickets, out));
   return CHGNET_OK;
 }
 

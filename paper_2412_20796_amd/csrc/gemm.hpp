@@ -82,8 +82,9 @@ struct TnBatch {
 int tn_launch(const TnBatch& b, float* part, int64_t part_cap, hipStream_t st, const char* tag);
 
 // out[k] += sum_c part[c*stride + k] (k < count), in a fixed order, in fp64.
-// scratch: 32 * count doubles. count is at most 8 * 128 for the callers here.
+// scratch: 32 * count doubles; tickets: cdiv(count, 64) zero-initialised
+// counters (left at zero on return).
 int reduce_rows_launch(const float* part, int nchunks, int64_t stride, int count, float* out, double* scratch,
-                       hipStream_t st);
+                       unsigned* tickets, hipStream_t st);
 
 }  // namespace chg

@@ -33,7 +33,7 @@ namespace {
 constexpr float kLnEps = 1e-5f;
 constexpr int kFreqRowsPerBlock = 256;  // rows per block in frequency-gradient kernel
 constexpr int kReduceGroups = 32;      // first-level groups of the ordered partial-sum reduction
-constexpr int64_t kTnPartFloats = 16ll << 20;
+constexpr int64_t kTnPartFloats = 64ll << 20;
 
 __device__ __forceinline__ float sigm(float x) { return 1.0f / (1.0f + __expf(-x)); }
 
@@ -724,6 +724,7 @@ struct Acts {
   float *doE, *doS, *dn, *doF, *dh2E, *dh2S, *dh2F, *dh1ES, *dh1F, *drbf_a, *drbf_b;
   float *lnpart, *tnpart, *fpart, *Pal;
   double* red2;
+  unsigned* tickets;
   int64_t tnpart_cap;
   // loss
   float *dE, *dF, *dS, *out_E, *out_F, *out_S;
@@ -798,6 +799,7 @@ void carve_acts(Arena& ar, const Dims& m, Acts& a, int64_t n_params_aligned) {
   const int64_t gate_blocks = cdiv(std::max<int64_t>(std::max(E, A), 1), kGateRows);
   a.lnpart = ar.take<float>(gate_blocks * 4 * D);
   a.red2 = ar.take<double>(kReduceGroups * 8 * D);
+  a.tickets = ar.take<unsigned>(64);
   a.tnpart_cap = kTnPartFloats;
   a.tnpart = ar.take<float>(a.tnpart_cap);
   a.fpart = ar.take<float>(cdiv(std::max(E, (int64_t)1), kFreqRowsPerBlock) * R);
@@ -938,7 +940,7 @@ int gate_bwd(int D, int64_t rows, const float* z, int ldz, const GateAdds& ad, L
   else
     KLAUNCH(st, tag, k_gate_bwd<128, MODE><<<(unsigned)nb, 256, 0, st>>>((int)rows, z, ldz, ad, ln, up, up_idx, eb,
                                                                            b2_idx, aux, dz, lddz, a.lnpart));
-  return reduce_rows_launch(a.lnpart, (int)nb, 4 * D, 4 * D, ln_grad, a.red2, st);
+  return reduce_rows_launch(a.lnpart, (int)nb, 4 * D, 4 * D, ln_grad, a.red2, a.tickets, st);
 }
 
 GateAdds adds(int n, const float* p0, int ld0, const int* i0, const float* p1, int ld1, const int* i1,
@@ -1184,6 +1186,7 @@ int backward_impl(Ctx& c, const float* Pflat, bool repack, const float* dE, cons
   const int64_t N = m.N, E = m.E, B = m.B, A = m.A;
 
   CHG_TRY(fill(G, Lg.total, 0.f, st));
+  CHG_TRY(fill(reinterpret_cast<float*>(a.tickets), 64, 0.f, st));
   CHG_TRY(fill(a.dea, E * D, 0.f, st));
   CHG_TRY(fill(a.deb, B * D, 0.f, st));
 
@@ -1408,13 +1411,13 @@ int backward_impl(Ctx& c, const float* Pflat, bool repack, const float* dE, cons
       const int64_t nb = cdiv(E, kFreqRowsPerBlock);
       KLAUNCH(st, "k_rbf_fgrad", k_rbf_fgrad<<<(unsigned)nb, 256, 0, st>>>((int)E, nullptr, a.edge_len, P + L.f_a, m.R, c.hp->r_atom,
                                                 c.hp->envelope_p, a.drbf_a, a.fpart));
-      CHG_TRY(reduce_rows_launch(a.fpart, (int)nb, m.R, m.R, G + Lg.f_a, a.red2, st));
+      CHG_TRY(reduce_rows_launch(a.fpart, (int)nb, m.R, m.R, G + Lg.f_a, a.red2, a.tickets, st));
     }
     if (B > 0) {
       const int64_t nb = cdiv(B, kFreqRowsPerBlock);
       KLAUNCH(st, "k_rbf_fgrad", k_rbf_fgrad<<<(unsigned)nb, 256, 0, st>>>((int)B, g.bond_edge, a.edge_len, P + L.f_b, m.R, c.hp->r_bond,
                                                 c.hp->envelope_p, a.drbf_b, a.fpart));
-      CHG_TRY(reduce_rows_launch(a.fpart, (int)nb, m.R, m.R, G + Lg.f_b, a.red2, st));
+      CHG_TRY(reduce_rows_launch(a.fpart, (int)nb, m.R, m.R, G + Lg.f_b, a.red2, a.tickets, st));
     }
   }
   return CHGNET_OK;
