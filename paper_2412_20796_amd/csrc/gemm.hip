@@ -509,48 +509,50 @@ __global__ void __launch_bounds__(1024) k_tn_reduce(TnLaunch L, const float* __r
   }
 }
 
-// Ordered reduction of chunk partials in one launch: block (x, g) sums the
-// chunks of group g for 64 columns (4 wavefronts, fixed order, fp64) into
-// part2[g]; the last block of column block x to finish (atomic ticket) adds
-// the groups in group order and resets the ticket. The arithmetic order is
-// fixed; only which block performs the final sum depends on scheduling.
-__global__ void __launch_bounds__(256) k_reduce_rows(const float* __restrict__ part, int nchunks, int per, int64_t stride,
-                                                     int count, int groups, double* __restrict__ part2,
-                                                     unsigned* __restrict__ tickets, float* __restrict__ out) {
+// Ordered reduction of chunk partials, two launches. Level 1: block
+// (x, g, job) sums the chunks of group g for 64 columns (4 wavefronts, fixed
+// order, fp64) into part2[job][g]. Level 2: block (x, job) adds the groups in
+// order (4 wavefronts x 8 groups, then the 4 wave sums in order).
+__global__ void __launch_bounds__(256) k_reduce_rows1(ReduceJobs J, int groups_max, double* __restrict__ part2_all) {
   __shared__ double red[4][64];
-  __shared__ bool last;
+  const ReduceJob& R = J.j[blockIdx.z];
+  const int count = R.count, nchunks = R.nchunks;
+  const int groups = max(1, min(groups_max, nchunks));
+  const int per = (nchunks + groups - 1) / groups;
+  if ((int)blockIdx.y >= groups || (int)blockIdx.x * 64 >= count) return;
+  double* part2 = part2_all + (int64_t)blockIdx.z * groups_max * 8 * 128;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int k = blockIdx.x * 64 + lane, g = blockIdx.y;
   const int c0 = g * per, c1 = min(nchunks, c0 + per);
   double s = 0.0;
   if (k < count)
-    for (int c = c0 + w; c < c1; c += 4) s += (double)part[(int64_t)c * stride + k];
+    for (int c = c0 + w; c < c1; c += 4) s += (double)R.part[(int64_t)c * R.stride + k];
   red[w][lane] = s;
   __syncthreads();
   if (w == 0 && k < count) part2[(int64_t)g * count + k] = ((red[0][lane] + red[1][lane]) + red[2][lane]) + red[3][lane];
-  __threadfence();
-  __syncthreads();
-  if (threadIdx.x == 0) last = atomicAdd(&tickets[blockIdx.x], 1u) == (unsigned)(groups - 1);
-  __syncthreads();
-  if (!last) return;
-  __threadfence();
-  // wave w adds groups w, w+4, ... (loads issued before the adds), then the
-  // four wave sums are added in order
+}
+
+__global__ void __launch_bounds__(256) k_reduce_rows2(ReduceJobs J, int groups_max, const double* __restrict__ part2_all) {
+  __shared__ double red[4][64];
+  const ReduceJob& R = J.j[blockIdx.y];
+  const int count = R.count;
+  const int groups = max(1, min(groups_max, R.nchunks));
+  if ((int)blockIdx.x * 64 >= count) return;
+  const double* part2 = part2_all + (int64_t)blockIdx.y * groups_max * 8 * 128;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int k = blockIdx.x * 64 + lane;
   double v[8];
 #pragma unroll
   for (int u = 0; u < 8; ++u) {
     const int q = w + 4 * u;
-    v[u] = (k < count && q < groups)
-               ? __hip_atomic_load(&part2[(int64_t)q * count + k], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
-               : 0.0;
+    v[u] = (k < count && q < groups) ? part2[(int64_t)q * count + k] : 0.0;
   }
   double t = 0.0;
 #pragma unroll
   for (int u = 0; u < 8; ++u) t += v[u];
   red[w][lane] = t;
   __syncthreads();
-  if (w == 0 && k < count) out[k] = (float)((double)out[k] + (((red[0][lane] + red[1][lane]) + red[2][lane]) + red[3][lane]));
-  if (threadIdx.x == 0) tickets[blockIdx.x] = 0u;
+  if (w == 0 && k < count) R.out[k] = (float)((double)R.out[k] + (((red[0][lane] + red[1][lane]) + red[2][lane]) + red[3][lane]));
 }
 
 }  // namespace
@@ -621,14 +623,27 @@ int tn_launch(const TnBatch& b, float* part, int64_t part_cap, hipStream_t st, c
   return CHGNET_OK;
 }
 
+int reduce_rows_multi(const ReduceJobs& J, double* scratch, unsigned* tickets, hipStream_t st) {
+  if (J.n == 0) return CHGNET_OK;
+  int maxc = 0, maxg = 1;
+  for (int i = 0; i < J.n; ++i) {
+    if (J.j[i].count > 8 * 128) return fail(CHGNET_EINVAL, "reduce: count too large");
+    maxc = std::max(maxc, J.j[i].count);
+    maxg = std::max(maxg, std::min(32, J.j[i].nchunks));
+  }
+  if (maxc == 0) return CHGNET_OK;
+  (void)tickets;
+  KLAUNCH(st, "k_reduce_rows1", k_reduce_rows1<<<dim3((unsigned)cdiv(maxc, 64), maxg, J.n), 256, 0, st>>>(J, 32, scratch));
+  KLAUNCH(st, "k_reduce_rows2", k_reduce_rows2<<<dim3((unsigned)cdiv(maxc, 64), J.n), 256, 0, st>>>(J, 32, scratch));
+  return CHGNET_OK;
+}
+
 int reduce_rows_launch(const float* part, int nchunks, int64_t stride, int count, float* out, double* scratch,
                        unsigned* tickets, hipStream_t st) {
-  if (count <= 0) return CHGNET_OK;
-  const int groups = std::max(1, std::min(32, nchunks));
-  const int per = (int)cdiv(std::max(nchunks, 1), groups);
-  KLAUNCH(st, "k_reduce_rows", k_reduce_rows<<<dim3((unsigned)cdiv(count, 64), groups), 256, 0, st>>>(
-                                   part, nchunks, per, stride, count, groups, scratch, tickets, out));
-  return CHGNET_OK;
+  ReduceJobs J{};
+  J.n = 1;
+  J.j[0] = ReduceJob{part, nchunks, stride, count, out};
+  return reduce_rows_multi(J, scratch, tickets, st);
 }
 
 }  // namespace chg

@@ -81,6 +81,21 @@ struct TnBatch {
 // part: scratch of part_cap floats.
 int tn_launch(const TnBatch& b, float* part, int64_t part_cap, hipStream_t st, const char* tag);
 
+struct ReduceJob {
+  const float* part;
+  int nchunks;
+  int64_t stride;
+  int count;
+  float* out;
+};
+struct ReduceJobs {
+  int n;
+  ReduceJob j[3];
+};
+// Up to 3 independent reductions in one launch; scratch: 3 * 32 * 1024
+// doubles, tickets: 3 * 64 zero-initialised counters (left at zero).
+int reduce_rows_multi(const ReduceJobs& J, double* scratch, unsigned* tickets, hipStream_t st);
+
 // out[k] += sum_c part[c*stride + k] (k < count), in a fixed order, in fp64.
 // scratch: 32 * count doubles; tickets: cdiv(count, 64) zero-initialised
 // counters (left at zero on return).

@@ -292,29 +292,54 @@ enum GateFwdMode { FWD_ATOM = 0, FWD_BOND = 1, FWD_ANGLE = 2 };
 //   FWD_ATOM : out[row] = e^a[row] * phi            (atom conv message)
 //   FWD_BOND : out[row] = e^b[b2[row]] * phi        (bond conv message)
 //   FWD_ANGLE: out[row] = a[row] + phi              (angle update)
+struct GateFwdJob {
+  int mode, rows, ldz, block0;
+  const float* z;
+  GateAdds ad;
+  LnPtrs ln;
+  const float* mulv;
+  const int* mul_idx;
+  float* out;
+};
+struct GateFwdJobs {
+  int n;
+  GateFwdJob j[3];
+};
+
 template <int D, int MODE>
-__global__ void __launch_bounds__(256) k_gate_fwd(int rows, const float* __restrict__ z, int ldz, GateAdds ad,
-                                                  LnPtrs ln, const float* __restrict__ mulv,
-                                                  const int* __restrict__ mul_idx, float* __restrict__ out) {
+__device__ __forceinline__ void gate_fwd_rows(int blk, const GateFwdJob& J) {
   constexpr int LPR = RowShape<D>::LPR, RPW = RowShape<D>::RPW;
   const int lane = threadIdx.x & 63, slot = lane / LPR, c0 = 16 * (lane % LPR);
-  const int row = (blockIdx.x * 4 + (threadIdx.x >> 6)) * RPW + slot;
-  if (row >= rows) return;  // LN lanes of a row are adjacent: a row is all-in or all-out
+  const int row = (blk * 4 + (threadIdx.x >> 6)) * RPW + slot;
+  if (row >= J.rows) return;  // LN lanes of a row are adjacent: a row is all-in or all-out
   float zc[16], zg[16], rc, rg;
-  load_z<D>(z, ldz, ad, row, c0, zc, zg);
+  load_z<D>(J.z, J.ldz, J.ad, row, c0, zc, zg);
   ln_stats<LPR, D>(zc, zg, rc, rg);
-  float m[16], o[16];
-  const int64_t mrow = MODE == FWD_BOND ? mul_idx[row] : row;
-  load16(mulv + mrow * D + c0, m);
+  float mv[16], o[16];
+  const int64_t mrow = MODE == FWD_BOND ? J.mul_idx[row] : row;
+  load16(J.mulv + mrow * D + c0, mv);
 #pragma unroll
   for (int k = 0; k < 16; ++k) {
     const int c = c0 + k;
-    const float yc = ln.gc[c] * zc[k] + ln.bc[c];
-    const float yg = ln.gg[c] * zg[k] + ln.bg[c];
+    const float yc = J.ln.gc[c] * zc[k] + J.ln.bc[c];
+    const float yg = J.ln.gg[c] * zg[k] + J.ln.bg[c];
     const float phi = yc * sigm(yc) * sigm(yg);
-    o[k] = MODE == FWD_ANGLE ? m[k] + phi : m[k] * phi;
+    o[k] = MODE == FWD_ANGLE ? mv[k] + phi : mv[k] * phi;
   }
-  store16(out + (int64_t)row * D + c0, o);
+  store16(J.out + (int64_t)row * D + c0, o);
+}
+
+// The independent gates of a layer (atom conv, bond conv, angle update; Eq.
+// 11) in one launch: job k owns blocks [block0_k, block0_{k+1}).
+template <int D>
+__global__ void __launch_bounds__(256) k_gate_fwd(GateFwdJobs J) {
+  int k = 0;
+  while (k + 1 < J.n && (int)blockIdx.x >= J.j[k + 1].block0) ++k;
+  const GateFwdJob& jb = J.j[k];
+  const int blk = blockIdx.x - jb.block0;
+  if (jb.mode == FWD_ATOM) gate_fwd_rows<D, FWD_ATOM>(blk, jb);
+  else if (jb.mode == FWD_BOND) gate_fwd_rows<D, FWD_BOND>(blk, jb);
+  else gate_fwd_rows<D, FWD_ANGLE>(blk, jb);
 }
 
 enum GateBwdMode { BWD_ATOM = 0, BWD_BOND = 1, BWD_ANGLE = 2 };
@@ -326,12 +351,33 @@ enum GateBwdMode { BWD_ATOM = 0, BWD_BOND = 1, BWD_ANGLE = 2 };
 //   BWD_ANGLE: dphi = da'[row]
 // Each block covers kGateRows rows.
 constexpr int kGateRows = 128;
+struct GateBwdJob {
+  int mode, rows, ldz, lddz, block0;
+  const float* z;
+  GateAdds ad;
+  LnPtrs ln;
+  const float *up, *eb;
+  const int *up_idx, *b2_idx;
+  float *aux, *dz, *lnpart;
+};
+struct GateBwdJobs {
+  int n;
+  GateBwdJob j[3];
+};
+
 template <int D, int MODE>
-__global__ void __launch_bounds__(256) k_gate_bwd(int rows, const float* __restrict__ z, int ldz, GateAdds ad, LnPtrs ln,
-                                                  const float* __restrict__ up, const int* __restrict__ up_idx,
-                                                  const float* __restrict__ eb, const int* __restrict__ b2_idx,
-                                                  float* __restrict__ aux, float* __restrict__ dz, int lddz,
-                                                  float* __restrict__ lnpart) {
+__device__ __forceinline__ void gate_bwd_rows(int blk, const GateBwdJob& J, float (*red)[64][17]) {
+  const int rows = J.rows, ldz = J.ldz, lddz = J.lddz;
+  const float* __restrict__ z = J.z;
+  const GateAdds& ad = J.ad;
+  const LnPtrs& ln = J.ln;
+  const float* __restrict__ up = J.up;
+  const int* __restrict__ up_idx = J.up_idx;
+  const float* __restrict__ eb = J.eb;
+  const int* __restrict__ b2_idx = J.b2_idx;
+  float* __restrict__ aux = J.aux;
+  float* __restrict__ dz = J.dz;
+  float* __restrict__ lnpart = J.lnpart;
   constexpr int LPR = RowShape<D>::LPR, RPW = RowShape<D>::RPW;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, slot = lane / LPR, c0 = 16 * (lane % LPR);
   float acc[4][16];
@@ -340,7 +386,7 @@ __global__ void __launch_bounds__(256) k_gate_bwd(int rows, const float* __restr
 #pragma unroll
     for (int k = 0; k < 16; ++k) acc[a][k] = 0.f;
   for (int it = 0; it < kGateRows / (4 * RPW); ++it) {
-    const int row = blockIdx.x * kGateRows + (it * 4 + wave) * RPW + slot;
+    const int row = blk * kGateRows + (it * 4 + wave) * RPW + slot;
     if (row >= rows) continue;
     float zc[16], zg[16], rc, rg;
     load_z<D>(z, ldz, ad, row, c0, zc, zg);
@@ -414,7 +460,6 @@ __global__ void __launch_bounds__(256) k_gate_bwd(int rows, const float* __restr
   }
   // LayerNorm partials: lanes with the same columns (same lane % LPR) over
   // all slots and wavefronts, summed in a fixed order through LDS.
-  __shared__ float red[4][64][17];
 #pragma unroll
   for (int a = 0; a < 4; ++a) {
 #pragma unroll
@@ -425,10 +470,22 @@ __global__ void __launch_bounds__(256) k_gate_bwd(int rows, const float* __restr
       float s = 0.f;
       for (int w = 0; w < 4; ++w)
         for (int sl = 0; sl < RPW; ++sl) s += red[w][sl * LPR + sub][k];
-      lnpart[(int64_t)blockIdx.x * 4 * D + a * D + c] = s;
+      lnpart[(int64_t)blk * 4 * D + a * D + c] = s;
     }
     __syncthreads();
   }
+}
+
+template <int D>
+__global__ void __launch_bounds__(256) k_gate_bwd(GateBwdJobs J) {
+  int k = 0;
+  while (k + 1 < J.n && (int)blockIdx.x >= J.j[k + 1].block0) ++k;
+  const GateBwdJob& jb = J.j[k];
+  const int blk = blockIdx.x - jb.block0;
+  __shared__ float red[4][64][17];
+  if (jb.mode == BWD_ATOM) gate_bwd_rows<D, BWD_ATOM>(blk, jb, red);
+  else if (jb.mode == BWD_BOND) gate_bwd_rows<D, BWD_BOND>(blk, jb, red);
+  else gate_bwd_rows<D, BWD_ANGLE>(blk, jb, red);
 }
 
 // Segmented row sums: out[s] (+)= sum_{r in [ptr[s], ptr[s+1])} vals[idx(r)];
@@ -725,6 +782,7 @@ struct Acts {
   float *lnpart, *tnpart, *fpart, *Pal;
   double* red2;
   unsigned* tickets;
+  int64_t lnpart_stride;
   int64_t tnpart_cap;
   // loss
   float *dE, *dF, *dS, *out_E, *out_F, *out_S;
@@ -797,9 +855,10 @@ void carve_acts(Arena& ar, const Dims& m, Acts& a, int64_t n_params_aligned) {
   a.drbf_a = ar.take<float>(E * R);
   a.drbf_b = ar.take<float>(B * R);
   const int64_t gate_blocks = cdiv(std::max<int64_t>(std::max(E, A), 1), kGateRows);
-  a.lnpart = ar.take<float>(gate_blocks * 4 * D);
-  a.red2 = ar.take<double>(kReduceGroups * 8 * D);
-  a.tickets = ar.take<unsigned>(64);
+  a.lnpart_stride = gate_blocks * 4 * D;
+  a.lnpart = ar.take<float>(3 * a.lnpart_stride);
+  a.red2 = ar.take<double>(3 * kReduceGroups * 8 * 128);  // per reduce job: 32 groups x up to 1024 columns
+  a.tickets = ar.take<unsigned>(3 * 64);
   a.tnpart_cap = kTnPartFloats;
   a.tnpart = ar.take<float>(a.tnpart_cap);
   a.fpart = ar.take<float>(cdiv(std::max(E, (int64_t)1), kFreqRowsPerBlock) * R);
@@ -915,32 +974,80 @@ int pack_params(const ParamLayout& L, const ParamLayout& La, const float* P, flo
   return CHGNET_OK;
 }
 
-template <int MODE>
-int gate_fwd(int D, int64_t rows, const float* z, int ldz, const GateAdds& ad, LnPtrs ln, const float* mulv,
-             const int* idx, float* out, hipStream_t st, const char* tag) {
-  if (rows <= 0) return CHGNET_OK;
-  if (D == 64)
-    KLAUNCH(st, tag, k_gate_fwd<64, MODE><<<(unsigned)cdiv(rows, 4 * RowShape<64>::RPW), 256, 0, st>>>(
-                         (int)rows, z, ldz, ad, ln, mulv, idx, out));
-  else
-    KLAUNCH(st, tag, k_gate_fwd<128, MODE><<<(unsigned)cdiv(rows, 4 * RowShape<128>::RPW), 256, 0, st>>>(
-                         (int)rows, z, ldz, ad, ln, mulv, idx, out));
+// Launch the gates of one layer (forward) as one multi-job kernel.
+int gate_fwd_launch(int D, GateFwdJobs J, hipStream_t st) {
+  constexpr int RPB64 = 4 * RowShape<64>::RPW, RPB128 = 4 * RowShape<128>::RPW;
+  const int rpb = D == 64 ? RPB64 : RPB128;
+  GateFwdJobs K{};
+  int blocks = 0;
+  for (int i = 0; i < J.n; ++i) {
+    if (J.j[i].rows <= 0) continue;
+    K.j[K.n] = J.j[i];
+    K.j[K.n].block0 = blocks;
+    blocks += (int)cdiv(J.j[i].rows, rpb);
+    K.n++;
+  }
+  if (blocks == 0) return CHGNET_OK;
+  if (D == 64) KLAUNCH(st, "k_gate_fwd", k_gate_fwd<64><<<blocks, 256, 0, st>>>(K));
+  else KLAUNCH(st, "k_gate_fwd", k_gate_fwd<128><<<blocks, 256, 0, st>>>(K));
   return CHGNET_OK;
 }
 
-template <int MODE>
-int gate_bwd(int D, int64_t rows, const float* z, int ldz, const GateAdds& ad, LnPtrs ln, const float* up,
-             const int* up_idx, const float* eb, const int* b2_idx, float* aux, float* dz, int lddz, const Acts& a,
-             float* ln_grad, hipStream_t st, const char* tag) {
-  if (rows <= 0) return CHGNET_OK;
-  const int64_t nb = cdiv(rows, kGateRows);
-  if (D == 64)
-    KLAUNCH(st, tag, k_gate_bwd<64, MODE><<<(unsigned)nb, 256, 0, st>>>((int)rows, z, ldz, ad, ln, up, up_idx, eb,
-                                                                          b2_idx, aux, dz, lddz, a.lnpart));
-  else
-    KLAUNCH(st, tag, k_gate_bwd<128, MODE><<<(unsigned)nb, 256, 0, st>>>((int)rows, z, ldz, ad, ln, up, up_idx, eb,
-                                                                           b2_idx, aux, dz, lddz, a.lnpart));
-  return reduce_rows_launch(a.lnpart, (int)nb, 4 * D, 4 * D, ln_grad, a.red2, a.tickets, st);
+GateFwdJob fwd_job(int mode, int64_t rows, const float* z, int ldz, const GateAdds& ad, LnPtrs ln, const float* mulv,
+                   const int* idx, float* out) {
+  GateFwdJob j{};
+  j.mode = mode;
+  j.rows = (int)rows;
+  j.z = z;
+  j.ldz = ldz;
+  j.ad = ad;
+  j.ln = ln;
+  j.mulv = mulv;
+  j.mul_idx = idx;
+  j.out = out;
+  return j;
+}
+
+GateBwdJob bwd_job(int mode, int64_t rows, const float* z, int ldz, const GateAdds& ad, LnPtrs ln, const float* up,
+                   const int* up_idx, const float* eb, const int* b2_idx, float* aux, float* dz, int lddz) {
+  GateBwdJob j{};
+  j.mode = mode;
+  j.rows = (int)rows;
+  j.z = z;
+  j.ldz = ldz;
+  j.ad = ad;
+  j.ln = ln;
+  j.up = up;
+  j.up_idx = up_idx;
+  j.eb = eb;
+  j.b2_idx = b2_idx;
+  j.aux = aux;
+  j.dz = dz;
+  j.lddz = lddz;
+  return j;
+}
+
+// Backward gates of one layer in one launch, then one launch reducing each
+// job's LayerNorm partials into ln_grad[k].
+int gate_bwd_launch(int D, GateBwdJobs J, float* const* ln_grad, const Acts& a, hipStream_t st) {
+  GateBwdJobs K{};
+  ReduceJobs R{};
+  int blocks = 0;
+  for (int i = 0; i < J.n; ++i) {
+    if (J.j[i].rows <= 0) continue;
+    const int nb = (int)cdiv(J.j[i].rows, kGateRows);
+    K.j[K.n] = J.j[i];
+    K.j[K.n].block0 = blocks;
+    K.j[K.n].lnpart = a.lnpart + (int64_t)i * a.lnpart_stride;
+    R.j[R.n] = ReduceJob{K.j[K.n].lnpart, nb, 4 * D, 4 * D, ln_grad[i]};
+    blocks += nb;
+    K.n++;
+    R.n++;
+  }
+  if (blocks == 0) return CHGNET_OK;
+  if (D == 64) KLAUNCH(st, "k_gate_bwd", k_gate_bwd<64><<<blocks, 256, 0, st>>>(K));
+  else KLAUNCH(st, "k_gate_bwd", k_gate_bwd<128><<<blocks, 256, 0, st>>>(K));
+  return reduce_rows_multi(R, a.red2, a.tickets, st);
 }
 
 GateAdds adds(int n, const float* p0, int ld0, const int* i0, const float* p1, int ld1, const int* i1,
@@ -1092,14 +1199,14 @@ int forward_impl(Ctx& c, const float* Pflat, float* energy, float* forces, float
                                 a.ang_b2);
     const GateAdds ad_an = adds(3, a.Xa[t] + 6 * D, 8 * D, a.ang_ctr, a.Xb[t] + 2 * D, 8 * D, a.ang_b1,
                                 a.Xb[t] + 6 * D, 8 * D, a.ang_b2);
-    CHG_TRY(gate_fwd<FWD_ATOM>(D, E, a.zv[t], 2 * D, ad_av, ln_ptrs(P, lo.av), a.ea, nullptr, a.msg, st,
-                               "k_gate_atom_fwd"));
+    {
+      GateFwdJobs J{};
+      J.j[J.n++] = fwd_job(FWD_ATOM, E, a.zv[t], 2 * D, ad_av, ln_ptrs(P, lo.av), a.ea, nullptr, a.msg);
+      J.j[J.n++] = fwd_job(FWD_BOND, A, a.zae[t], 4 * D, ad_be, ln_ptrs(P, lo.be), a.eb, a.ang_b2, a.msgb);
+      if (ang) J.j[J.n++] = fwd_job(FWD_ANGLE, A, a.zae[t] + 2 * D, 4 * D, ad_an, ln_ptrs(P, lo.an), a.a[t], nullptr, a.a[t + 1]);
+      CHG_TRY(gate_fwd_launch(D, J, st));
+    }
     CHG_TRY(segsum(N, g.edge_ptr, nullptr, a.msg, D, D, a.m[t], D, 0, nullptr, 0, nullptr, 0, st));
-    CHG_TRY(gate_fwd<FWD_BOND>(D, A, a.zae[t], 4 * D, ad_be, ln_ptrs(P, lo.be), a.eb, a.ang_b2, a.msgb, st,
-                               "k_gate_bond_fwd"));
-    if (ang)
-      CHG_TRY(gate_fwd<FWD_ANGLE>(D, A, a.zae[t] + 2 * D, 4 * D, ad_an, ln_ptrs(P, lo.an), a.a[t], nullptr, a.a[t + 1],
-                                  st, "k_gate_angle_fwd"));
     CHG_TRY(segsum(B, g.angle_ptr, nullptr, a.msgb, D, D, a.ssum[t], D, 0, a.eb, D, a.mu[t], D, st));
     // updates: v' = v + m Wo + bo; e' = e (+ mu Wo + bo on bonds)
     if (E > 0) {
@@ -1186,7 +1293,7 @@ int backward_impl(Ctx& c, const float* Pflat, bool repack, const float* dE, cons
   const int64_t N = m.N, E = m.E, B = m.B, A = m.A;
 
   CHG_TRY(fill(G, Lg.total, 0.f, st));
-  CHG_TRY(fill(reinterpret_cast<float*>(a.tickets), 64, 0.f, st));
+  CHG_TRY(fill(reinterpret_cast<float*>(a.tickets), 3 * 64, 0.f, st));
   CHG_TRY(fill(a.dea, E * D, 0.f, st));
   CHG_TRY(fill(a.deb, B * D, 0.f, st));
 
@@ -1296,11 +1403,18 @@ int backward_impl(Ctx& c, const float* Pflat, bool repack, const float* dE, cons
                                 a.ang_b2);
     const GateAdds ad_an = adds(3, a.Xa[t] + 6 * D, 8 * D, a.ang_ctr, a.Xb[t] + 2 * D, 8 * D, a.ang_b1,
                                 a.Xb[t] + 6 * D, 8 * D, a.ang_b2);
-    CHG_TRY(gate_bwd<BWD_BOND>(D, A, a.zae[t], 4 * D, ad_be, ln_ptrs(P, lo.be), a.dmu, a.ang_b1, a.eb, a.ang_b2, a.t2,
-                               a.dzae, 4 * D, a, G + lg.be.g_c, st, "k_gate_bond_bwd"));
-    if (ang)
-      CHG_TRY(gate_bwd<BWD_ANGLE>(D, A, a.zae[t] + 2 * D, 4 * D, ad_an, ln_ptrs(P, lo.an), a.da[cur], nullptr, nullptr,
-                                  nullptr, nullptr, a.dzae + 2 * D, 4 * D, a, G + lg.an.g_c, st, "k_gate_angle_bwd"));
+    {
+      GateBwdJobs J{};
+      J.j[J.n++] = bwd_job(BWD_BOND, A, a.zae[t], 4 * D, ad_be, ln_ptrs(P, lo.be), a.dmu, a.ang_b1, a.eb, a.ang_b2, a.t2,
+                           a.dzae, 4 * D);
+      J.j[J.n++] = bwd_job(BWD_ATOM, E, a.zv[t], 2 * D, ad_av, ln_ptrs(P, lo.av), a.dm, a.edge_src, a.ea, nullptr, a.dea,
+                           a.dzv, 2 * D);
+      if (ang)
+        J.j[J.n++] = bwd_job(BWD_ANGLE, A, a.zae[t] + 2 * D, 4 * D, ad_an, ln_ptrs(P, lo.an), a.da[cur], nullptr, nullptr,
+                             nullptr, nullptr, a.dzae + 2 * D, 4 * D);
+      float* lg_out[3] = {G + lg.be.g_c, G + lg.av.g_c, G + lg.an.g_c};
+      CHG_TRY(gate_bwd_launch(D, J, lg_out, a, st));
+    }
     if (B > 0) {
       const unsigned nb = (unsigned)cdiv(B, 4);
       const int cpl = W4 / 64;
@@ -1314,9 +1428,6 @@ int backward_impl(Ctx& c, const float* Pflat, bool repack, const float* dE, cons
 #undef BOND_REDUCE
     }
     CHG_TRY(segsum(N, g.bond_ptr, nullptr, a.DZ12, 8 * D, W4, a.AT + 4 * D, 8 * D, 0, nullptr, 0, nullptr, 0, st));
-    // atom conv gate
-    CHG_TRY(gate_bwd<BWD_ATOM>(D, E, a.zv[t], 2 * D, ad_av, ln_ptrs(P, lo.av), a.dm, a.edge_src, a.ea, nullptr, a.dea,
-                               a.dzv, 2 * D, a, G + lg.av.g_c, st, "k_gate_atom_bwd"));
     CHG_TRY(segsum(N, g.edge_ptr, nullptr, a.dzv, 2 * D, 2 * D, a.AT, 8 * D, 0, nullptr, 0, nullptr, 0, st));
     CHG_TRY(segsum(N, g.edge_ptr, g.edge_rev, a.dzv, 2 * D, 2 * D, a.AT + 2 * D, 8 * D, 0, nullptr, 0, nullptr, 0, st));
     // input gradients
