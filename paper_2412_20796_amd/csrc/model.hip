@@ -488,31 +488,62 @@ __global__ void __launch_bounds__(256) k_gate_bwd(GateBwdJobs J) {
   else gate_bwd_rows<D, BWD_ANGLE>(blk, jb, red);
 }
 
-// Segmented row sums: out[s] (+)= sum_{r in [ptr[s], ptr[s+1])} vals[idx(r)];
-// optionally out2[s] = mul[s] * sum. One wavefront per segment.
-__global__ void __launch_bounds__(256) k_segsum(int nseg, int ncb, const int* __restrict__ ptr, const int* __restrict__ idx,
-                                                const float* __restrict__ vals, int ld_in, int width, float* __restrict__ out,
-                                                int ld_out, int accumulate, const float* __restrict__ mul, int ld_mul,
-                                                float* __restrict__ out2, int ld_out2) {
-  const int wid = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
-  const int s = wid / ncb, c = (wid % ncb) * 64 + lane;
-  if (s >= nseg || c >= width) return;
-  const int lo = ptr[s], hi = ptr[s + 1];
+// Segmented row sums, several independent jobs per launch:
+//   out[s] (+)= sum_{r in [ptr[s], ptr[s+1])} vals[idx(r)]; optionally
+//   out2[s] = mul[s] * sum. WPS wavefronts per (segment, 64 columns) split the
+// rows (wave w takes every WPS-th group of 4 rows) and their sums are added
+// in wave order: the result does not depend on scheduling.
+struct SegJob {
+  int nseg, ncb, width, ld_in, ld_out, ld_mul, ld_out2, accumulate, block0;
+  const int* ptr;
+  const int* idx;
+  const float* vals;
+  float* out;
+  const float* mul;
+  float* out2;
+};
+struct SegJobs {
+  int n;
+  SegJob j[3];
+};
+
+template <int WPS>
+__global__ void __launch_bounds__(256) k_segsum(SegJobs J) {
+  constexpr int SPB = 4 / WPS;  // (segment, column block) units per block
+  int k = 0;
+  while (k + 1 < J.n && (int)blockIdx.x >= J.j[k + 1].block0) ++k;
+  const SegJob& S = J.j[k];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int unit = (blockIdx.x - S.block0) * SPB + wave / WPS, w = wave % WPS;
+  const int s = unit / S.ncb, c = (unit % S.ncb) * 64 + lane;
+  const bool ok = s < S.nseg && c < S.width;
   float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
-  int r = lo;
-  for (; r + 3 < hi; r += 4) {
-    const int64_t i0 = idx ? idx[r] : r, i1 = idx ? idx[r + 1] : r + 1, i2 = idx ? idx[r + 2] : r + 2,
-                  i3 = idx ? idx[r + 3] : r + 3;
-    a0 += vals[i0 * ld_in + c];
-    a1 += vals[i1 * ld_in + c];
-    a2 += vals[i2 * ld_in + c];
-    a3 += vals[i3 * ld_in + c];
+  if (ok) {
+    const int lo = S.ptr[s], hi = S.ptr[s + 1];
+    int r = lo + 4 * w;
+    for (; r + 3 < hi; r += 4 * WPS) {
+      const int64_t i0 = S.idx ? S.idx[r] : r, i1 = S.idx ? S.idx[r + 1] : r + 1, i2 = S.idx ? S.idx[r + 2] : r + 2,
+                    i3 = S.idx ? S.idx[r + 3] : r + 3;
+      a0 += S.vals[i0 * S.ld_in + c];
+      a1 += S.vals[i1 * S.ld_in + c];
+      a2 += S.vals[i2 * S.ld_in + c];
+      a3 += S.vals[i3 * S.ld_in + c];
+    }
+    // r is now the start of one of this wave's groups: its partial tail
+    for (; r < hi; ++r) a0 += S.vals[(int64_t)(S.idx ? S.idx[r] : r) * S.ld_in + c];
   }
-  for (; r < hi; ++r) a0 += vals[(int64_t)(idx ? idx[r] : r) * ld_in + c];
-  const float acc = (a0 + a1) + (a2 + a3);
-  float* o = out + (int64_t)s * ld_out + c;
-  *o = accumulate ? *o + acc : acc;
-  if (out2) out2[(int64_t)s * ld_out2 + c] = mul[(int64_t)s * ld_mul + c] * acc;
+  float acc = (a0 + a1) + (a2 + a3);
+  if (WPS > 1) {
+    __shared__ float red[4][64];
+    red[wave][lane] = acc;
+    __syncthreads();
+    if (w != 0) return;
+    for (int q = 1; q < WPS; ++q) acc += red[wave + q][lane];
+  }
+  if (!ok) return;
+  float* o = S.out + (int64_t)s * S.ld_out + c;
+  *o = S.accumulate ? *o + acc : acc;
+  if (S.out2) S.out2[(int64_t)s * S.ld_out2 + c] = S.mul[(int64_t)s * S.ld_mul + c] * acc;
 }
 
 // Per bond b (centre i, local index q among k bonds): DZ1 = sum over the
@@ -713,15 +744,27 @@ __global__ void k_seed_edges2(int E, const int* __restrict__ edge_rev, const flo
   if (e < E) doF[e] = 0.5f * (dn[e] + dn[edge_rev[e]]);
 }
 
-// dW_Z[z] = sum over atoms with Z_i = z+1 of dv0_i (ordered by atom index).
-__global__ void k_embed_bwd_Z(int N, int D, const int* __restrict__ Z, const float* __restrict__ dv0, float* __restrict__ gWZ) {
-  const int z = blockIdx.x + 1;
-  for (int c = threadIdx.x; c < D; c += blockDim.x) {
-    float acc = 0.f;
-    for (int i = 0; i < N; ++i)
-      if (Z[i] == z) acc += dv0[(int64_t)i * D + c];
-    gWZ[(int64_t)(z - 1) * D + c] += acc;
+// dW_Z[z] = sum over atoms with Z_i = z+1 of dv0_i, in atom order. One
+// wavefront per element: lanes scan 64 atoms at a time, then the matching
+// rows are added in order (lanes over columns).
+__global__ void __launch_bounds__(256) k_embed_bwd_Z(int N, int D, const int* __restrict__ Z, const float* __restrict__ dv0,
+                                                     float* __restrict__ gWZ) {
+  const int z = blockIdx.x * 4 + (threadIdx.x >> 6) + 1, lane = threadIdx.x & 63;
+  if (z > 94) return;
+  float acc0 = 0.f, acc1 = 0.f;
+  for (int base = 0; base < N; base += 64) {
+    const int i = base + lane;
+    unsigned long long m = __ballot(i < N && Z[i] == z);
+    while (m) {
+      const int b = __ffsll(m) - 1;
+      m &= m - 1;
+      const int64_t row = (int64_t)(base + b) * D;
+      acc0 += dv0[row + lane];
+      if (D > 64) acc1 += dv0[row + 64 + lane];
+    }
   }
+  gWZ[(int64_t)(z - 1) * D + lane] += acc0;
+  if (D > 64) gWZ[(int64_t)(z - 1) * D + 64 + lane] += acc1;
 }
 
 // Partial sums over rows of d sRBF_n * d sRBF_n / d f_n.
@@ -952,12 +995,41 @@ int fill(float* p, int64_t n, float v, hipStream_t st) {
   return CHGNET_OK;
 }
 
-int segsum(int64_t nseg, const int* ptr, const int* idx, const float* vals, int ld_in, int width, float* out, int ld_out,
-           int accumulate, const float* mul, int ld_mul, float* out2, int ld_out2, hipStream_t st) {
-  if (nseg <= 0) return CHGNET_OK;
-  const int ncb = (int)cdiv(width, 64);
-  KLAUNCH(st, "k_segsum", k_segsum<<<(unsigned)cdiv(nseg * ncb, 4), 256, 0, st>>>((int)nseg, ncb, ptr, idx, vals, ld_in, width, out, ld_out,
-                                                          accumulate, mul, ld_mul, out2, ld_out2));
+SegJob seg_job(int64_t nseg, const int* ptr, const int* idx, const float* vals, int ld_in, int width, float* out,
+               int ld_out, const float* mul = nullptr, int ld_mul = 0, float* out2 = nullptr, int ld_out2 = 0) {
+  SegJob j{};
+  j.nseg = (int)nseg;
+  j.ncb = (int)cdiv(width, 64);
+  j.ptr = ptr;
+  j.idx = idx;
+  j.vals = vals;
+  j.ld_in = ld_in;
+  j.width = width;
+  j.out = out;
+  j.ld_out = ld_out;
+  j.mul = mul;
+  j.ld_mul = ld_mul;
+  j.out2 = out2;
+  j.ld_out2 = ld_out2;
+  return j;
+}
+
+// wps: wavefronts per segment (4 for long segments such as the edges of an
+// atom, 1 for short ones such as the angles of a bond)
+int segsum_launch(SegJobs J, int wps, hipStream_t st) {
+  SegJobs K{};
+  int blocks = 0;
+  const int spb = 4 / wps;
+  for (int i = 0; i < J.n; ++i) {
+    if (J.j[i].nseg <= 0) continue;
+    K.j[K.n] = J.j[i];
+    K.j[K.n].block0 = blocks;
+    blocks += (int)cdiv((int64_t)J.j[i].nseg * J.j[i].ncb, spb);
+    K.n++;
+  }
+  if (blocks == 0) return CHGNET_OK;
+  if (wps == 4) KLAUNCH(st, "k_segsum", k_segsum<4><<<blocks, 256, 0, st>>>(K));
+  else KLAUNCH(st, "k_segsum", k_segsum<1><<<blocks, 256, 0, st>>>(K));
   return CHGNET_OK;
 }
 
@@ -1206,8 +1278,14 @@ int forward_impl(Ctx& c, const float* Pflat, float* energy, float* forces, float
       if (ang) J.j[J.n++] = fwd_job(FWD_ANGLE, A, a.zae[t] + 2 * D, 4 * D, ad_an, ln_ptrs(P, lo.an), a.a[t], nullptr, a.a[t + 1]);
       CHG_TRY(gate_fwd_launch(D, J, st));
     }
-    CHG_TRY(segsum(N, g.edge_ptr, nullptr, a.msg, D, D, a.m[t], D, 0, nullptr, 0, nullptr, 0, st));
-    CHG_TRY(segsum(B, g.angle_ptr, nullptr, a.msgb, D, D, a.ssum[t], D, 0, a.eb, D, a.mu[t], D, st));
+    {
+      SegJobs J{};
+      J.j[J.n++] = seg_job(N, g.edge_ptr, nullptr, a.msg, D, D, a.m[t], D);
+      CHG_TRY(segsum_launch(J, 4, st));
+      J = SegJobs{};
+      J.j[J.n++] = seg_job(B, g.angle_ptr, nullptr, a.msgb, D, D, a.ssum[t], D, a.eb, D, a.mu[t], D);
+      CHG_TRY(segsum_launch(J, 1, st));
+    }
     // updates: v' = v + m Wo + bo; e' = e (+ mu Wo + bo on bonds)
     if (E > 0) {
       KLAUNCH(st, "k_copy", k_copy<<<(unsigned)cdiv(E * D, 256), 256, 0, st>>>(a.e[t + 1], a.e[t], E * D));
@@ -1427,9 +1505,13 @@ int backward_impl(Ctx& c, const float* Pflat, bool repack, const float* dE, cons
       else BOND_REDUCE(8, 2);
 #undef BOND_REDUCE
     }
-    CHG_TRY(segsum(N, g.bond_ptr, nullptr, a.DZ12, 8 * D, W4, a.AT + 4 * D, 8 * D, 0, nullptr, 0, nullptr, 0, st));
-    CHG_TRY(segsum(N, g.edge_ptr, nullptr, a.dzv, 2 * D, 2 * D, a.AT, 8 * D, 0, nullptr, 0, nullptr, 0, st));
-    CHG_TRY(segsum(N, g.edge_ptr, g.edge_rev, a.dzv, 2 * D, 2 * D, a.AT + 2 * D, 8 * D, 0, nullptr, 0, nullptr, 0, st));
+    {
+      SegJobs J{};
+      J.j[J.n++] = seg_job(N, g.edge_ptr, nullptr, a.dzv, 2 * D, 2 * D, a.AT, 8 * D);
+      J.j[J.n++] = seg_job(N, g.edge_ptr, g.edge_rev, a.dzv, 2 * D, 2 * D, a.AT + 2 * D, 8 * D);
+      J.j[J.n++] = seg_job(N, g.bond_ptr, nullptr, a.DZ12, 8 * D, W4, a.AT + 4 * D, 8 * D);
+      CHG_TRY(segsum_launch(J, 4, st));
+    }
     // input gradients
     {
       GemmProblem p = gp(N, D, a.dv[nx], D);
@@ -1499,7 +1581,7 @@ int backward_impl(Ctx& c, const float* Pflat, bool repack, const float* dE, cons
   }
 
   // embeddings
-  KLAUNCH(st, "k_embed_bwd_Z", k_embed_bwd_Z<<<94, 64, 0, st>>>((int)N, D, bt.Z, a.dv[cur], G + Lg.W_Z));
+  KLAUNCH(st, "k_embed_bwd_Z", k_embed_bwd_Z<<<24, 256, 0, st>>>((int)N, D, bt.Z, a.dv[cur], G + Lg.W_Z));
   {
     std::vector<TnProblem> ts;
     ts.push_back(tp(E, m.R, D, a.rbf_a, m.R, 0, nullptr, a.de[cur], D, 0, nullptr, G + Lg.W_e, 2 * D));
