@@ -34,6 +34,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample", type=int, default=0, help="structures in the CPU oracle sample (0 = auto)")
     ap.add_argument("--no-roofline", action="store_true")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="first run a plain 256 MiB device copy (reference for HBM traffic counters)")
     return ap.parse_args()
 
 
@@ -69,6 +71,12 @@ def main():
         step_no[0] += 1
         bd.step(hp, db, g, p, tg, ws, grad=grad, loss=loss, adam=(m, v, (lr, b1, b2, eps, float(step_no[0]))))
 
+    if args.calibrate_copy:
+        src = torch.ones(64 << 20, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     for _ in range(max(args.warmup, 1)):
         one_step()
     torch.cuda.synchronize()

@@ -9,6 +9,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <string>
 
 #include "common.hpp"
 #include "gemm.hpp"
@@ -145,109 +146,127 @@ __device__ __forceinline__ void gemm_store4(const GemmProblem& P, int row, int c
   }
 }
 
-template <int BN>
+// ROLE only names the instantiation (0 other, 1 forward pre-activations,
+// 2 input gradients) so that profilers can tell the launches apart.
+template <int BN, int ROLE>
 __global__ void __launch_bounds__(256) k_gemm(GemmBatch batch) {
   constexpr int BM = 128, KC = 32, NT = BN / 32, KP = KC + 4, SP = 64 + 4;
   const GemmProblem& P = batch.p[blockIdx.z];
-  const int r0 = blockIdx.x * BM, c0 = blockIdx.y * BN;
-  if (r0 >= P.M || c0 >= P.N) return;
+  const int c0 = blockIdx.y * BN;
+  const int ntiles = (P.M + BM - 1) / BM;
+  if ((int)blockIdx.x >= ntiles || c0 >= P.N) return;
   // Operand tiles are stored k-contiguous: As[row][k], Bs[col][k]. In MFMA
   // k-step i, lane half h = lane / 32 supplies k = 16 h + i, so each lane
   // reads its 16 A and B values of a chunk with four 16-byte LDS reads.
   // After the K loop the same LDS holds the output tile, 64 columns at a
-  // time, so the epilogue writes whole rows with 16-byte stores.
+  // time, so the epilogue writes whole rows with 16-byte stores. A block
+  // walks row tiles blockIdx.x, blockIdx.x + gridDim.x, ...; the first chunk
+  // of its next tile is fetched before the current tile's epilogue.
   constexpr int kOperand = BM * KP + BN * KP, kStage = 4 * 32 * SP;
   __shared__ __attribute__((aligned(16))) float smem[kOperand > kStage ? kOperand : kStage];
   float (*As)[KP] = reinterpret_cast<float (*)[KP]>(smem);
   float (*Bs)[KP] = reinterpret_cast<float (*)[KP]>(smem + BM * KP);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, h = lane >> 5;
-  v16f acc[NT];
-#pragma unroll
-  for (int t = 0; t < NT; ++t)
-#pragma unroll
-    for (int j = 0; j < 16; ++j) acc[t][j] = 0.f;
   const int ar = tid >> 3, ak = (tid & 7) * 4;
+  const bool cvec = gemm_cvec(P);
   int64_t arow[4];
   bool aval[4];
+  auto set_rows = [&](int r0) {
 #pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    const int r = r0 + ar + 32 * q;
-    aval[q] = r < P.M;
-    arow[q] = aval[q] ? (P.a_rows ? P.a_rows[r] : r) : 0;
-  }
+    for (int q = 0; q < 4; ++q) {
+      const int r = r0 + ar + 32 * q;
+      aval[q] = r < P.M;
+      arow[q] = aval[q] ? (P.a_rows ? P.a_rows[r] : r) : 0;
+    }
+  };
   GemmStage<BN> g;
-  int s = 0, k0 = 0;
+  int tile = blockIdx.x;
+  set_rows(tile * BM);
   if (P.nseg > 0) gemm_fetch<BN>(P, P.seg[0], 0, c0, tid, arow, aval, g);
-  while (s < P.nseg) {
-    const bool trans = P.seg[s].trans;
+  while (tile < ntiles) {
+    const int r0 = tile * BM;
+    const int next = tile + gridDim.x;
+    v16f acc[NT];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) *reinterpret_cast<float4*>(&As[ar + 32 * q][ak]) = g.a[q];
-    if (!trans) {
-      constexpr int G = 256 / BN;
+    for (int t = 0; t < NT; ++t)
 #pragma unroll
-      for (int q = 0; q < BN / 32; ++q)
-        *reinterpret_cast<float4*>(&Bs[tid % BN][4 * (tid / BN + G * q)]) = g.b[q];
-    } else {
+      for (int j = 0; j < 16; ++j) acc[t][j] = 0.f;
+    int s = 0, k0 = 0;
+    while (s < P.nseg) {
+      const bool trans = P.seg[s].trans;
 #pragma unroll
-      for (int q = 0; q < BN / 32; ++q) {
-        const int idx = tid + 256 * q, n = idx / (KC / 4), kk = (idx % (KC / 4)) * 4;
-        *reinterpret_cast<float4*>(&Bs[n][kk]) = g.b[q];
-      }
-    }
-    __syncthreads();
-    k0 += KC;
-    if (k0 >= P.seg[s].K) {
-      k0 = 0;
-      ++s;
-    }
-    if (s < P.nseg) gemm_fetch<BN>(P, P.seg[s], k0, c0, tid, arow, aval, g);
-    float af[16], bf[NT][16];
-    {
-      const float* ap = &As[32 * wave + (lane & 31)][16 * h];
+      for (int q = 0; q < 4; ++q) *reinterpret_cast<float4*>(&As[ar + 32 * q][ak]) = g.a[q];
+      if (!trans) {
+        constexpr int G = 256 / BN;
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const float4 v = *reinterpret_cast<const float4*>(ap + 4 * q);
-        af[4 * q] = v.x; af[4 * q + 1] = v.y; af[4 * q + 2] = v.z; af[4 * q + 3] = v.w;
-      }
+        for (int q = 0; q < BN / 32; ++q)
+          *reinterpret_cast<float4*>(&Bs[tid % BN][4 * (tid / BN + G * q)]) = g.b[q];
+      } else {
 #pragma unroll
-      for (int t = 0; t < NT; ++t) {
-        const float* bp = &Bs[32 * t + (lane & 31)][16 * h];
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const float4 v = *reinterpret_cast<const float4*>(bp + 4 * q);
-          bf[t][4 * q] = v.x; bf[t][4 * q + 1] = v.y; bf[t][4 * q + 2] = v.z; bf[t][4 * q + 3] = v.w;
+        for (int q = 0; q < BN / 32; ++q) {
+          const int idx = tid + 256 * q, n = idx / (KC / 4), kk = (idx % (KC / 4)) * 4;
+          *reinterpret_cast<float4*>(&Bs[n][kk]) = g.b[q];
         }
       }
+      __syncthreads();
+      k0 += KC;
+      if (k0 >= P.seg[s].K) {
+        k0 = 0;
+        ++s;
+      }
+      if (s < P.nseg) {
+        gemm_fetch<BN>(P, P.seg[s], k0, c0, tid, arow, aval, g);
+      } else if (next < ntiles) {
+        set_rows(next * BM);
+        gemm_fetch<BN>(P, P.seg[0], 0, c0, tid, arow, aval, g);
+      }
+      float af[16], bf[NT][16];
+      {
+        const float* ap = &As[32 * wave + (lane & 31)][16 * h];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const float4 v = *reinterpret_cast<const float4*>(ap + 4 * q);
+          af[4 * q] = v.x; af[4 * q + 1] = v.y; af[4 * q + 2] = v.z; af[4 * q + 3] = v.w;
+        }
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+          const float* bp = &Bs[32 * t + (lane & 31)][16 * h];
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const float4 v = *reinterpret_cast<const float4*>(bp + 4 * q);
+            bf[t][4 * q] = v.x; bf[t][4 * q + 1] = v.y; bf[t][4 * q + 2] = v.z; bf[t][4 * q + 3] = v.w;
+          }
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < 16; ++i)
+#pragma unroll
+        for (int t = 0; t < NT; ++t) acc[t] = __builtin_amdgcn_mfma_f32_32x32x2f32(af[i], bf[t][i], acc[t], 0, 0, 0);
+      __syncthreads();
     }
+    // ---- epilogue, 64 columns (two 32x32 tiles) at a time through LDS
+    float* stg = smem + wave * 32 * SP;
 #pragma unroll
-    for (int i = 0; i < 16; ++i)
+    for (int half = 0; half < (NT + 1) / 2; ++half) {
 #pragma unroll
-      for (int t = 0; t < NT; ++t) acc[t] = __builtin_amdgcn_mfma_f32_32x32x2f32(af[i], bf[t][i], acc[t], 0, 0, 0);
-    __syncthreads();
-  }
-  // ---- epilogue, 64 columns (two 32x32 tiles) at a time through LDS
-  float* stg = smem + wave * 32 * SP;
-  const bool cvec = gemm_cvec(P);
+      for (int tt = 0; tt < 2; ++tt) {
+        if (2 * half + tt >= NT) break;
 #pragma unroll
-  for (int half = 0; half < (NT + 1) / 2; ++half) {
+        for (int j = 0; j < 16; ++j)
+          stg[(8 * (j >> 2) + 4 * h + (j & 3)) * SP + 32 * tt + (lane & 31)] = acc[2 * half + tt][j];
+      }
+      __syncthreads();
+      const int cl = 4 * (lane & 15);
+      const int col = c0 + 64 * half + cl;
 #pragma unroll
-    for (int tt = 0; tt < 2; ++tt) {
-      if (2 * half + tt >= NT) break;
-#pragma unroll
-      for (int j = 0; j < 16; ++j)
-        stg[(8 * (j >> 2) + 4 * h + (j & 3)) * SP + 32 * tt + (lane & 31)] = acc[2 * half + tt][j];
+      for (int i = 0; i < 8; ++i) {
+        const int lr = (lane >> 4) + 4 * i;
+        const float4 sv = *reinterpret_cast<const float4*>(stg + lr * SP + cl);
+        gemm_store4(P, r0 + 32 * wave + lr, col, sv, cvec);
+      }
+      __syncthreads();
     }
-    __syncthreads();
-    // lane: rows (lane / 16) + 4 i, columns 4 (lane % 16) .. +3 of this half
-    const int cl = 4 * (lane & 15);
-    const int col = c0 + 64 * half + cl;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int lr = (lane >> 4) + 4 * i;
-      const float4 sv = *reinterpret_cast<const float4*>(stg + lr * SP + cl);
-      gemm_store4(P, r0 + 32 * wave + lr, col, sv, cvec);
-    }
-    __syncthreads();
+    tile = next;
   }
 }
 
@@ -382,6 +401,8 @@ struct TnLaunch {
 
 // Split-K X^T Y: a 64 x 128 output tile per block (waves in a 2 x 2 grid,
 // 32 x 64 each as two 32x32 MFMA tiles), rows streamed 32 at a time.
+// ROLE only names the instantiation (1: interaction-block weight gradients).
+template <int ROLE>
 __global__ void __launch_bounds__(256) k_tn(TnLaunch L, float* __restrict__ part) {
   constexpr int TM = 64, TN = 128, RC = 32;
   const TnPlan& Q = L.q[blockIdx.z];
@@ -581,9 +602,14 @@ int gemm_launch(const GemmBatch& b, hipStream_t st, const char* tag) {
     KLAUNCH(st, tag, k_gemm_ks<<<grid, 256, 0, st>>>(b));
     return CHGNET_OK;
   }
-  const dim3 grid(gx, gy, b.n);
-  if (BN == 128) KLAUNCH(st, tag, k_gemm<128><<<grid, 256, 0, st>>>(b));
-  else KLAUNCH(st, tag, k_gemm<64><<<grid, 256, 0, st>>>(b));
+  // persistent row tiles: about 2048 blocks over the launch
+  const int per_problem = std::max(1, 2048 / (gy * b.n));
+  const dim3 grid(std::min(gx, per_problem), gy, b.n);
+  const std::string t(tag);
+  if (BN == 128) KLAUNCH(st, tag, k_gemm<128, 0><<<grid, 256, 0, st>>>(b));
+  else if (t == "gemm_z") KLAUNCH(st, tag, k_gemm<64, 1><<<grid, 256, 0, st>>>(b));
+  else if (t == "gemm_in_bwd") KLAUNCH(st, tag, k_gemm<64, 2><<<grid, 256, 0, st>>>(b));
+  else KLAUNCH(st, tag, k_gemm<64, 0><<<grid, 256, 0, st>>>(b));
   return CHGNET_OK;
 }
 
@@ -615,7 +641,8 @@ int tn_launch(const TnBatch& b, float* part, int64_t part_cap, hipStream_t st, c
   if (off > part_cap) return fail(CHGNET_EWORKSPACE, "split-K partial buffer too small");
   if (b.n == 0) return CHGNET_OK;
   if (gx > 0) {
-    KLAUNCH(st, tag, k_tn<<<dim3(gx, gy, b.n), 256, 0, st>>>(L, part));
+    if (std::string(tag) == "tn_in") KLAUNCH(st, tag, k_tn<1><<<dim3(gx, gy, b.n), 256, 0, st>>>(L, part));
+    else KLAUNCH(st, tag, k_tn<0><<<dim3(gx, gy, b.n), 256, 0, st>>>(L, part));
   }
   int64_t maxmn = 0;
   for (int i = 0; i < b.n; ++i) maxmn = std::max<int64_t>(maxmn, (int64_t)b.p[i].M * b.p[i].N);
