@@ -36,11 +36,20 @@ def parse():
     ap.add_argument("--no-roofline", action="store_true")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="first run a plain 256 MiB device copy (reference for HBM traffic counters)")
+    ap.add_argument("--traffic-summary", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="no GPU: reduce two rocprofv3 counter CSVs (FETCH_SIZE, WRITE_SIZE) to a markdown summary")
     return ap.parse_args()
 
 
 def main():
     args = parse()
+    if args.traffic_summary:
+        cmd = ["rocprofv3 --pmc %s --output-format csv -d gpurun_out/pmc_%s -o run -- python3 bench.py "
+               "--workload %s --no-cpu-baseline --no-roofline --steps 3 --warmup 1 --calibrate-copy"
+               % (c, c.split("_")[0].lower(), args.workload) for c in ("FETCH_SIZE", "WRITE_SIZE")]
+        cmd.append("python3 bench.py --workload %s --traffic-summary %s %s" % ((args.workload,) + tuple(args.traffic_summary)))
+        print(traffic_summary(args.traffic_summary[0], args.traffic_summary[1], args.workload, cmd))
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path (run with --gpus 1)", file=sys.stderr)
         sys.exit(2)
@@ -122,7 +131,8 @@ def main():
             one_step()
         torch.cuda.synchronize()
         prof = bd.profile_stop()
-        out["roofline"], out["kernels"] = roofline(prof, args.steps, dict(N=b.n_atoms, E=E, B=B, A=A, S=S, D=d, T=T))
+        out["roofline"], out["kernels"] = roofline(prof, args.steps, dict(N=b.n_atoms, E=E, B=B, A=A, S=S, D=d, T=T,
+                                                                            workload=args.workload))
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(args.workload, args.cpu_sample)
     print(json.dumps(out), flush=True)
@@ -137,7 +147,7 @@ def algorithmic_cost(tag, z):
     the last layer (bond conv only); an edge costs 4d^2 (e W, d -> 2d). The
     backward input gradients cost the same per unit, the weight gradients the
     same again (A^T B over the rows). Bytes count each array read or written
-    once (gathered rows of small per-atom/per-bond tables excluded)."""
+    once, gathered tables (per-atom and per-bond rows) once each."""
     N, E, B, A, D, T = z["N"], z["E"], z["B"], z["A"], z["D"], z["T"]
     Tang = T - 1  # layers with an angle update
     f = 4  # bytes per fp32
@@ -152,17 +162,112 @@ def algorithmic_cost(tag, z):
         return "mfma", T * (N * 16 * D * D + B * 8 * D * D) - N * 4 * D * D - B * 4 * D * D
     if tag == "gemm_bond_bwd":
         return "mfma", Tang * B * 16 * D * D + B * 8 * D * D
-    if tag == "k_gate_angle_fwd":  # read z (4d or 2d), read a, write a', write eb-weighted message
-        return "hbm", f * (Tang * A * (4 * D + 3 * D) + A * (2 * D + D))
-    if tag == "k_gate_angle_bwd":  # read z, da'; write dz, t2
-        return "hbm", f * (Tang * A * (4 * D + D + 4 * D + D) + A * (2 * D + 2 * D + D))
-    if tag == "k_gate_atom_fwd":  # read z (2d), e^a; write message
-        return "hbm", f * T * E * (2 * D + 2 * D)
-    if tag == "k_gate_atom_bwd":  # read z, e^a, d e^a; write dz, d e^a
-        return "hbm", f * T * E * (2 * D + D + D + 2 * D + D)
+    if tag == "k_gate_fwd":
+        # per edge: z (2d) + e^a (d) in, message (d) out; per angle: bond gate
+        # z (2d) in, message (d) out; angle gate z (2d) + a (d) in, a' (d)
+        # out. Tables: per-atom terms N x 8d (6d last layer), per-bond terms
+        # B x 8d (4d), e^b B x d.
+        lay = E * 4 * D + A * 7 * D + N * 8 * D + B * 9 * D
+        last = E * 4 * D + A * 3 * D + N * 6 * D + B * 5 * D
+        return "hbm", f * (Tang * lay + last)
+    if tag == "k_gate_bwd":
+        # per edge: z (2d), e^a (d), d e^a (d) in; dz (2d), d e^a (d) out;
+        # per angle and gate: z (2d) + upstream (d) in, dz (2d) out (the bond
+        # gate's upstream is gathered, its t2 (d) written). Tables as in the
+        # forward plus dm N x d, dmu B x d.
+        lay = E * 7 * D + A * 10 * D + N * 9 * D + B * 10 * D
+        last = E * 7 * D + A * 5 * D + N * 7 * D + B * 6 * D
+        return "hbm", f * (Tang * lay + last)
     if tag == "k_bond_bwd_reduce":  # read dz twice (both roles), t2; write DZ12
         return "hbm", f * (Tang * A * (8 * D + D) + A * (4 * D + D) + T * B * 8 * D)
     return None, None
+
+
+# rocprofv3 kernel symbol of each launch tag that has an algorithmic cost
+TAG_SYMBOL = {
+    "gemm_z": "k_gemm<64, 1>",
+    "gemm_in_bwd": "k_gemm<64, 2>",
+    "tn_in": "k_tn<1>",
+    "k_gate_fwd": "k_gate_fwd<64>",
+    "k_gate_bwd": "k_gate_bwd<64>",
+}
+
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_%s.md")
+SOURCE_DIR = os.path.join(ROOT, "paper_2412_20796_amd", "csrc")
+
+
+def source_digest():
+    """sha256 over the HIP sources: traffic measured on other sources is stale."""
+    import hashlib
+
+    h = hashlib.sha256()
+    for name in sorted(os.listdir(SOURCE_DIR)):
+        if name.endswith((".hip", ".hpp")):
+            h.update(name.encode())
+            h.update(open(os.path.join(SOURCE_DIR, name), "rb").read())
+    return h.hexdigest()
+
+
+def measured_traffic(workload, tag):
+    """HBM bytes per launch of `tag` from the committed counter summary, or
+    None if there is none for this workload, the kernel, or these sources."""
+    path = TRAFFIC_FILE % workload
+    sym = TAG_SYMBOL.get(tag)
+    if sym is None or not os.path.exists(path):
+        return None
+    text = open(path).read()
+    start = text.find("```json")
+    if start < 0:
+        return None
+    data = json.loads(text[start + 7:text.index("```", start + 7)])
+    if data.get("source_sha256") != source_digest():
+        return None
+    k = data["kernels"].get(sym)
+    return None if k is None else k["fetch_bytes"] + k["write_bytes"]
+
+
+def traffic_summary(fetch_csv, write_csv, workload, command):
+    """Reduce two rocprofv3 counter runs (FETCH_SIZE, WRITE_SIZE; KiB per
+    dispatch) to bytes per dispatch for each kernel, each counter scaled by
+    what it reads for the 256 MiB plain copy that --calibrate-copy launches
+    first (the largest copy kernel in the run). Prints a markdown summary
+    with a JSON block that roofline() reads."""
+    import collections
+    import csv
+
+    def per_kernel(path, counter):
+        d = collections.defaultdict(list)
+        for r in csv.DictReader(open(path)):
+            if r["Counter_Name"] == counter:
+                d[r["Kernel_Name"].replace("chg::(anonymous namespace)::", "").split("(")[0].replace("void ", "")]\
+                    .append(float(r["Counter_Value"]))
+        return d
+
+    fk, wk = per_kernel(fetch_csv, "FETCH_SIZE"), per_kernel(write_csv, "WRITE_SIZE")
+    copies = [k for k in fk if "copy" in k.lower() and not k.startswith("k_")]
+    ck = max(copies, key=lambda k: max(fk[k]))
+    ideal_kib = 256 * 1024
+    sf, sw = ideal_kib / max(fk[ck]), ideal_kib / max(wk[ck])
+    kern = {}
+    for k in fk:
+        if k == ck or k not in wk:
+            continue
+        F = sum(fk[k]) / len(fk[k]) * sf * 1024
+        W = sum(wk[k]) / len(wk[k]) * sw * 1024
+        kern[k] = {"dispatches": len(fk[k]), "fetch_bytes": round(F), "write_bytes": round(W)}
+    data = {"workload": workload, "source_sha256": source_digest(), "calibration_kernel": ck,
+            "fetch_scale": round(sf, 4), "write_scale": round(sw, 4), "kernels": kern}
+    lines = ["# HBM traffic per dispatch, workload %s" % workload, "",
+             "Commands (repository root, one MI355X):", ""]
+    lines += ["    " + c for c in command]
+    lines += ["", "Calibration: a 256 MiB device-to-device copy (%s) reads FETCH_SIZE %.0f KiB and "
+              "WRITE_SIZE %.0f KiB; every kernel's counters are scaled by %.4f (fetch) and %.4f (write)."
+              % (ck, max(fk[ck]), max(wk[ck]), sf, sw), "",
+              "| kernel | dispatches | fetch MB/dispatch | write MB/dispatch |", "|---|---|---|---|"]
+    for k, v in sorted(kern.items(), key=lambda kv: -(kv[1]["fetch_bytes"] + kv[1]["write_bytes"]) * kv[1]["dispatches"])[:20]:
+        lines.append("| %s | %d | %.1f | %.1f |" % (k, v["dispatches"], v["fetch_bytes"] / 1e6, v["write_bytes"] / 1e6))
+    lines += ["", "```json", json.dumps(data, indent=1), "```", ""]
+    return "\n".join(lines)
 
 
 def roofline(prof, steps, z):
@@ -188,8 +293,9 @@ def roofline(prof, steps, z):
     per_launch = work / n_launch
     rl = {"kernel": dom["tag"], "bound": dom["bound"], "achieved": dom["achieved"],
           "peak": FP32_PEAK_TFLOPS if dom["bound"] == "mfma" else HBM_PEAK_GBS, "unit": dom["unit"],
-          "frac": dom["frac"], "traffic": None,
+          "frac": dom["frac"], "traffic": measured_traffic(z["workload"], dom["tag"]),
           "work_per_launch": per_launch, "work_unit": "flop" if bound == "mfma" else "byte",
+          "traffic_unit": "bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
           "avg_launch_us": dom["avg_launch_us"], "launches_per_step": n_launch,
           "timing": "HIP events around every launch of the kernel on the library's stream, %d steps" % steps}
     return rl, rows[:14]

@@ -186,9 +186,11 @@ __global__ void k_embed_v0(int N, int D, const int* __restrict__ Z, const float*
 
 // ---------------------------------------------------------------------------
 // GatedMLP rows: phi = SiLU(LN_c(z_c)) * sigmoid(LN_g(z_g)).
-// A row is held by LPR = d/16 adjacent lanes, each with 16 contiguous core
-// columns and the 16 matching gate columns; LayerNorm statistics are sums
-// over those LPR lanes by DPP permutes (no LDS traffic). A wavefront works
+// A row is held by LPR = d/CPL adjacent lanes with CPL core columns and the
+// CPL matching gate columns each. Lane j of a row owns the float4 chunks at
+// columns q*4*LPR + 4j (q < CPL/4), so one float4 load of a wavefront reads
+// 4*LPR contiguous columns of every row it touches. LayerNorm statistics are
+// sums over the LPR lanes by DPP permutes (no LDS traffic). A wavefront works
 // on 64/LPR rows at a time.
 // ---------------------------------------------------------------------------
 template <int CTRL>
@@ -198,47 +200,57 @@ __device__ __forceinline__ float dpp(float v) {
 
 template <int LPR>
 __device__ __forceinline__ float rowsum(float v) {
+  static_assert(LPR == 4 || LPR == 8 || LPR == 16, "row of 4, 8 or 16 lanes");
   v += dpp<0xB1>(v);  // quad_perm [1,0,3,2]
   v += dpp<0x4E>(v);  // quad_perm [2,3,0,1]
-  if (LPR == 8) v += dpp<0x141>(v);  // row_half_mirror: pairs the two quads
+  if (LPR >= 8) v += dpp<0x141>(v);   // row_half_mirror: pairs the two quads of 8 lanes
+  if (LPR == 16) v += dpp<0x140>(v);  // row_mirror: pairs the two halves of 16 lanes
   return v;
 }
 
-template <int D>
-struct RowShape {
-  static constexpr int LPR = D / 16;    // lanes per row
+template <int D, int CPL>
+struct Lanes {
+  static constexpr int LPR = D / CPL;   // lanes per row
   static constexpr int RPW = 64 / LPR;  // rows per wavefront pass
+  static constexpr int NQ = CPL / 4;    // float4 chunks per lane
+  static constexpr int STRIDE = 4 * LPR;
+  // column of the lane's k-th value (lane j within its row)
+  static __device__ __forceinline__ int col(int j, int k) { return (k >> 2) * STRIDE + 4 * j + (k & 3); }
 };
 
-__device__ __forceinline__ void load16(const float* __restrict__ p, float (&v)[16]) {
+template <int D, int CPL>
+__device__ __forceinline__ void load_cols(const float* __restrict__ p, int j, float (&v)[CPL]) {
 #pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    const float4 t = *reinterpret_cast<const float4*>(p + 4 * q);
+  for (int q = 0; q < CPL / 4; ++q) {
+    const float4 t = *reinterpret_cast<const float4*>(p + q * Lanes<D, CPL>::STRIDE + 4 * j);
     v[4 * q] = t.x;
     v[4 * q + 1] = t.y;
     v[4 * q + 2] = t.z;
     v[4 * q + 3] = t.w;
   }
 }
-__device__ __forceinline__ void store16(float* __restrict__ p, const float (&v)[16]) {
+template <int D, int CPL>
+__device__ __forceinline__ void store_cols(float* __restrict__ p, int j, const float (&v)[CPL]) {
 #pragma unroll
-  for (int q = 0; q < 4; ++q)
-    *reinterpret_cast<float4*>(p + 4 * q) = make_float4(v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]);
+  for (int q = 0; q < CPL / 4; ++q)
+    *reinterpret_cast<float4*>(p + q * Lanes<D, CPL>::STRIDE + 4 * j) =
+        make_float4(v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]);
 }
 
 // Normalised core/gate (xc, xg) and 1/std (rc, rg) of one row; in place.
-template <int LPR, int D>
-__device__ __forceinline__ void ln_stats(float (&zc)[16], float (&zg)[16], float& rc, float& rg) {
+template <int D, int CPL>
+__device__ __forceinline__ void ln_stats(float (&zc)[CPL], float (&zg)[CPL], float& rc, float& rg) {
+  constexpr int LPR = Lanes<D, CPL>::LPR;
   float sc = 0.f, sg = 0.f;
 #pragma unroll
-  for (int k = 0; k < 16; ++k) {
+  for (int k = 0; k < CPL; ++k) {
     sc += zc[k];
     sg += zg[k];
   }
   const float mc = rowsum<LPR>(sc) * (1.0f / D), mg = rowsum<LPR>(sg) * (1.0f / D);
   float vc = 0.f, vg = 0.f;
 #pragma unroll
-  for (int k = 0; k < 16; ++k) {
+  for (int k = 0; k < CPL; ++k) {
     zc[k] -= mc;
     zg[k] -= mg;
     vc += zc[k] * zc[k];
@@ -247,7 +259,7 @@ __device__ __forceinline__ void ln_stats(float (&zc)[16], float (&zg)[16], float
   rc = rsqrtf(rowsum<LPR>(vc) * (1.0f / D) + kLnEps);
   rg = rsqrtf(rowsum<LPR>(vg) * (1.0f / D) + kLnEps);
 #pragma unroll
-  for (int k = 0; k < 16; ++k) {
+  for (int k = 0; k < CPL; ++k) {
     zc[k] *= rc;
     zg[k] *= rg;
   }
@@ -266,25 +278,29 @@ struct GateAdds {
   const int* idx[3];
 };
 
-template <int D>
-__device__ __forceinline__ void load_z(const float* __restrict__ z, int ldz, const GateAdds& ad, int row, int c0,
-                                       float (&zc)[16], float (&zg)[16]) {
-  load16(z + (int64_t)row * ldz + c0, zc);
-  load16(z + (int64_t)row * ldz + D + c0, zg);
+template <int D, int CPL>
+__device__ __forceinline__ void load_z(const float* __restrict__ z, int ldz, const GateAdds& ad, int row, int j,
+                                       float (&zc)[CPL], float (&zg)[CPL]) {
+  load_cols<D, CPL>(z + (int64_t)row * ldz, j, zc);
+  load_cols<D, CPL>(z + (int64_t)row * ldz + D, j, zg);
 #pragma unroll
   for (int q = 0; q < 3; ++q) {
     if (q >= ad.n) break;
     const float* r = ad.p[q] + (int64_t)ad.idx[q][row] * ad.ld[q];
-    float uc[16], ug[16];
-    load16(r + c0, uc);
-    load16(r + D + c0, ug);
+    float uc[CPL], ug[CPL];
+    load_cols<D, CPL>(r, j, uc);
+    load_cols<D, CPL>(r + D, j, ug);
 #pragma unroll
-    for (int k = 0; k < 16; ++k) {
+    for (int k = 0; k < CPL; ++k) {
       zc[k] += uc[k];
       zg[k] += ug[k];
     }
   }
 }
+
+// Columns per lane of the forward and backward gates.
+constexpr int kFwdCpl = 16;
+constexpr int kBwdCpl = 8;
 
 enum GateFwdMode { FWD_ATOM = 0, FWD_BOND = 1, FWD_ANGLE = 2 };
 
@@ -308,25 +324,26 @@ struct GateFwdJobs {
 
 template <int D, int MODE>
 __device__ __forceinline__ void gate_fwd_rows(int blk, const GateFwdJob& J) {
-  constexpr int LPR = RowShape<D>::LPR, RPW = RowShape<D>::RPW;
-  const int lane = threadIdx.x & 63, slot = lane / LPR, c0 = 16 * (lane % LPR);
-  const int row = (blk * 4 + (threadIdx.x >> 6)) * RPW + slot;
+  constexpr int CPL = kFwdCpl;
+  using L = Lanes<D, CPL>;
+  const int lane = threadIdx.x & 63, slot = lane / L::LPR, j = lane % L::LPR;
+  const int row = (blk * 4 + (threadIdx.x >> 6)) * L::RPW + slot;
   if (row >= J.rows) return;  // LN lanes of a row are adjacent: a row is all-in or all-out
-  float zc[16], zg[16], rc, rg;
-  load_z<D>(J.z, J.ldz, J.ad, row, c0, zc, zg);
-  ln_stats<LPR, D>(zc, zg, rc, rg);
-  float mv[16], o[16];
+  float zc[CPL], zg[CPL], rc, rg;
+  load_z<D, CPL>(J.z, J.ldz, J.ad, row, j, zc, zg);
+  ln_stats<D, CPL>(zc, zg, rc, rg);
+  float mv[CPL], o[CPL];
   const int64_t mrow = MODE == FWD_BOND ? J.mul_idx[row] : row;
-  load16(J.mulv + mrow * D + c0, mv);
+  load_cols<D, CPL>(J.mulv + mrow * D, j, mv);
 #pragma unroll
-  for (int k = 0; k < 16; ++k) {
-    const int c = c0 + k;
+  for (int k = 0; k < CPL; ++k) {
+    const int c = L::col(j, k);
     const float yc = J.ln.gc[c] * zc[k] + J.ln.bc[c];
     const float yg = J.ln.gg[c] * zg[k] + J.ln.bg[c];
     const float phi = yc * sigm(yc) * sigm(yg);
     o[k] = MODE == FWD_ANGLE ? mv[k] + phi : mv[k] * phi;
   }
-  store16(J.out + (int64_t)row * D + c0, o);
+  store_cols<D, CPL>(J.out + (int64_t)row * D, j, o);
 }
 
 // The independent gates of a layer (atom conv, bond conv, angle update; Eq.
@@ -365,8 +382,17 @@ struct GateBwdJobs {
   GateBwdJob j[3];
 };
 
+// LDS staging of the per-lane LayerNorm partials: [4 sums][4 waves][RPW
+// slots][d columns + 4 pad].
+template <int D>
+struct GateBwdLds {
+  static constexpr int RPW = Lanes<D, kBwdCpl>::RPW;
+  static constexpr int LD = D + 4;
+  static constexpr int FLOATS = 4 * 4 * RPW * LD;
+};
+
 template <int D, int MODE>
-__device__ __forceinline__ void gate_bwd_rows(int blk, const GateBwdJob& J, float (*red)[64][17]) {
+__device__ __forceinline__ void gate_bwd_rows(int blk, const GateBwdJob& J, float* red) {
   const int rows = J.rows, ldz = J.ldz, lddz = J.lddz;
   const float* __restrict__ z = J.z;
   const GateAdds& ad = J.ad;
@@ -378,45 +404,47 @@ __device__ __forceinline__ void gate_bwd_rows(int blk, const GateBwdJob& J, floa
   float* __restrict__ aux = J.aux;
   float* __restrict__ dz = J.dz;
   float* __restrict__ lnpart = J.lnpart;
-  constexpr int LPR = RowShape<D>::LPR, RPW = RowShape<D>::RPW;
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, slot = lane / LPR, c0 = 16 * (lane % LPR);
-  float acc[4][16];
+  constexpr int CPL = kBwdCpl;
+  using L = Lanes<D, CPL>;
+  constexpr int LPR = L::LPR, RPW = L::RPW;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, slot = lane / LPR, j = lane % LPR;
+  float acc[4][CPL];
 #pragma unroll
   for (int a = 0; a < 4; ++a)
 #pragma unroll
-    for (int k = 0; k < 16; ++k) acc[a][k] = 0.f;
+    for (int k = 0; k < CPL; ++k) acc[a][k] = 0.f;
   for (int it = 0; it < kGateRows / (4 * RPW); ++it) {
     const int row = blk * kGateRows + (it * 4 + wave) * RPW + slot;
     if (row >= rows) continue;
-    float zc[16], zg[16], rc, rg;
-    load_z<D>(z, ldz, ad, row, c0, zc, zg);
-    ln_stats<LPR, D>(zc, zg, rc, rg);
-    float u[16], w[16], dphi[16];
+    float zc[CPL], zg[CPL], rc, rg;
+    load_z<D, CPL>(z, ldz, ad, row, j, zc, zg);
+    ln_stats<D, CPL>(zc, zg, rc, rg);
+    float u[CPL], w[CPL], dphi[CPL];
     if (MODE == BWD_ANGLE) {
-      load16(up + (int64_t)row * D + c0, dphi);
+      load_cols<D, CPL>(up + (int64_t)row * D, j, dphi);
     } else {
       const int64_t ur = up_idx[row];
-      load16(up + ur * D + c0, u);
+      load_cols<D, CPL>(up + ur * D, j, u);
       if (MODE == BWD_ATOM) {
-        load16(eb + (int64_t)row * D + c0, w);  // e^a of this edge
+        load_cols<D, CPL>(eb + (int64_t)row * D, j, w);  // e^a of this edge
 #pragma unroll
-        for (int k = 0; k < 16; ++k) dphi[k] = u[k] * w[k];
+        for (int k = 0; k < CPL; ++k) dphi[k] = u[k] * w[k];
       } else {
-        float e1[16], e2[16];
-        load16(eb + ur * D + c0, e1);
-        load16(eb + (int64_t)b2_idx[row] * D + c0, e2);
+        float e1[CPL], e2[CPL];
+        load_cols<D, CPL>(eb + ur * D, j, e1);
+        load_cols<D, CPL>(eb + (int64_t)b2_idx[row] * D, j, e2);
 #pragma unroll
-        for (int k = 0; k < 16; ++k) {
+        for (int k = 0; k < CPL; ++k) {
           w[k] = u[k] * e1[k];
           dphi[k] = w[k] * e2[k];
         }
       }
     }
-    float dyc[16], dyg[16], side[16];
+    float dyc[CPL], dyg[CPL], side[CPL];
     float s1c = 0.f, s2c = 0.f, s1g = 0.f, s2g = 0.f;
 #pragma unroll
-    for (int k = 0; k < 16; ++k) {
-      const int c = c0 + k;
+    for (int k = 0; k < CPL; ++k) {
+      const int c = L::col(j, k);
       const float yc = ln.gc[c] * zc[k] + ln.bc[c];
       const float yg = ln.gg[c] * zg[k] + ln.bg[c];
       const float sc = sigm(yc), sg = sigm(yg);
@@ -440,39 +468,42 @@ __device__ __forceinline__ void gate_bwd_rows(int blk, const GateBwdJob& J, floa
     s1g = rowsum<LPR>(s1g) * (1.0f / D);
     s2g = rowsum<LPR>(s2g) * (1.0f / D);
 #pragma unroll
-    for (int k = 0; k < 16; ++k) {
+    for (int k = 0; k < CPL; ++k) {
       dyc[k] = rc * (dyc[k] - s1c - zc[k] * s2c);
       dyg[k] = rg * (dyg[k] - s1g - zg[k] * s2g);
     }
-    store16(dz + (int64_t)row * lddz + c0, dyc);
-    store16(dz + (int64_t)row * lddz + D + c0, dyg);
+    store_cols<D, CPL>(dz + (int64_t)row * lddz, j, dyc);
+    store_cols<D, CPL>(dz + (int64_t)row * lddz + D, j, dyg);
     if (MODE == BWD_ATOM) {
-      float de[16];
-      load16(aux + (int64_t)row * D + c0, de);
+      float de[CPL];
+      load_cols<D, CPL>(aux + (int64_t)row * D, j, de);
 #pragma unroll
-      for (int k = 0; k < 16; ++k) de[k] += u[k] * side[k];
-      store16(aux + (int64_t)row * D + c0, de);
+      for (int k = 0; k < CPL; ++k) de[k] += u[k] * side[k];
+      store_cols<D, CPL>(aux + (int64_t)row * D, j, de);
     } else if (MODE == BWD_BOND) {
 #pragma unroll
-      for (int k = 0; k < 16; ++k) side[k] *= w[k];
-      store16(aux + (int64_t)row * D + c0, side);
+      for (int k = 0; k < CPL; ++k) side[k] *= w[k];
+      store_cols<D, CPL>(aux + (int64_t)row * D, j, side);
     }
   }
-  // LayerNorm partials: lanes with the same columns (same lane % LPR) over
-  // all slots and wavefronts, summed in a fixed order through LDS.
+  // LayerNorm partials: every lane stages its four partial rows in LDS, then
+  // each thread sums one (sum, column) pair over the waves and row slots in
+  // a fixed order.
+  using S = GateBwdLds<D>;
 #pragma unroll
-  for (int a = 0; a < 4; ++a) {
+  for (int a = 0; a < 4; ++a)
 #pragma unroll
-    for (int k = 0; k < 16; ++k) red[wave][lane][k] = acc[a][k];
-    __syncthreads();
-    for (int c = threadIdx.x; c < D; c += 256) {
-      const int sub = c / 16, k = c % 16;
-      float s = 0.f;
-      for (int w = 0; w < 4; ++w)
-        for (int sl = 0; sl < RPW; ++sl) s += red[w][sl * LPR + sub][k];
-      lnpart[(int64_t)blk * 4 * D + a * D + c] = s;
-    }
-    __syncthreads();
+    for (int q = 0; q < CPL / 4; ++q)
+      *reinterpret_cast<float4*>(red + ((a * 4 + wave) * RPW + slot) * S::LD + q * L::STRIDE + 4 * j) =
+          make_float4(acc[a][4 * q], acc[a][4 * q + 1], acc[a][4 * q + 2], acc[a][4 * q + 3]);
+  __syncthreads();
+  for (int t = threadIdx.x; t < 4 * D; t += 256) {
+    const int a = t / D, c = t % D;
+    float s = 0.f;
+    for (int w = 0; w < 4; ++w)
+#pragma unroll
+      for (int sl = 0; sl < RPW; ++sl) s += red[((a * 4 + w) * RPW + sl) * S::LD + c];
+    lnpart[(int64_t)blk * 4 * D + t] = s;
   }
 }
 
@@ -482,7 +513,7 @@ __global__ void __launch_bounds__(256) k_gate_bwd(GateBwdJobs J) {
   while (k + 1 < J.n && (int)blockIdx.x >= J.j[k + 1].block0) ++k;
   const GateBwdJob& jb = J.j[k];
   const int blk = blockIdx.x - jb.block0;
-  __shared__ float red[4][64][17];
+  __shared__ __align__(16) float red[GateBwdLds<D>::FLOATS];
   if (jb.mode == BWD_ATOM) gate_bwd_rows<D, BWD_ATOM>(blk, jb, red);
   else if (jb.mode == BWD_BOND) gate_bwd_rows<D, BWD_BOND>(blk, jb, red);
   else gate_bwd_rows<D, BWD_ANGLE>(blk, jb, red);
@@ -1048,7 +1079,7 @@ int pack_params(const ParamLayout& L, const ParamLayout& La, const float* P, flo
 
 // Launch the gates of one layer (forward) as one multi-job kernel.
 int gate_fwd_launch(int D, GateFwdJobs J, hipStream_t st) {
-  constexpr int RPB64 = 4 * RowShape<64>::RPW, RPB128 = 4 * RowShape<128>::RPW;
+  constexpr int RPB64 = 4 * Lanes<64, kFwdCpl>::RPW, RPB128 = 4 * Lanes<128, kFwdCpl>::RPW;
   const int rpb = D == 64 ? RPB64 : RPB128;
   GateFwdJobs K{};
   int blocks = 0;
