@@ -359,6 +359,163 @@ __global__ void __launch_bounds__(256) k_gate_fwd(GateFwdJobs J) {
   else gate_fwd_rows<D, FWD_ANGLE>(blk, jb);
 }
 
+// Forward gate with its own pre-activation product (d = 64): z = x W + b
+// (+ the gathered terms) is formed tile by tile in LDS and never round-trips
+// through HBM. A block walks 64-row tiles of all jobs (persistent, stride =
+// grid). Wave w keeps the fp32 MFMA B fragments of output columns
+// [32w, 32w + 32) of W (64 x 128: core | gate) in registers; the x tile is
+// staged in LDS; each wave forms its 64 x 32 slice of z with 32x32x2 MFMAs
+// (lane half h supplies k = 16h + i in step i of each 32-wide k block) and
+// writes it to the z tile; the row-layout gate then reads z from LDS.
+typedef float v16f __attribute__((ext_vector_type(16)));
+
+struct GateMmJob {
+  int mode, rows, tile0;
+  const float* x;  // [rows, 64]
+  const float* W;  // [64, 128] core | gate columns, row stride ldw
+  int ldw;
+  const float* bias;  // [128]
+  GateAdds ad;
+  LnPtrs ln;
+  const float* mulv;
+  const int* mul_idx;
+  float* out;
+  float* zsave;  // optional [rows, ldzs]: x W + b, kept for the backward pass
+  int ldzs;
+};
+struct GateMmJobs {
+  int n, ntiles;
+  GateMmJob j[3];
+};
+
+constexpr int kMmRows = 64;
+constexpr int kMmXld = 64 + 4;
+constexpr int kMmZld = 128 + 4;
+
+constexpr int kMmCpl = 8;
+
+template <int MODE>
+__device__ __forceinline__ void gate_mm_row(const GateMmJob& J, int r0, int lr, const float* Zs) {
+  constexpr int D = 64, CPL = kMmCpl;
+  using L = Lanes<D, CPL>;
+  const int j = (threadIdx.x & 63) % L::LPR;
+  const int row = r0 + lr;
+  if (row >= J.rows) return;
+  float zc[CPL], zg[CPL], rc, rg;
+  load_cols<D, CPL>(Zs + lr * kMmZld, j, zc);
+  load_cols<D, CPL>(Zs + lr * kMmZld + D, j, zg);
+  if (J.zsave) {
+    store_cols<D, CPL>(J.zsave + (int64_t)row * J.ldzs, j, zc);
+    store_cols<D, CPL>(J.zsave + (int64_t)row * J.ldzs + D, j, zg);
+  }
+#pragma unroll
+  for (int q = 0; q < 3; ++q) {
+    if (q >= J.ad.n) break;
+    const float* r = J.ad.p[q] + (int64_t)J.ad.idx[q][row] * J.ad.ld[q];
+    float uc[CPL], ug[CPL];
+    load_cols<D, CPL>(r, j, uc);
+    load_cols<D, CPL>(r + D, j, ug);
+#pragma unroll
+    for (int k = 0; k < CPL; ++k) {
+      zc[k] += uc[k];
+      zg[k] += ug[k];
+    }
+  }
+  ln_stats<D, CPL>(zc, zg, rc, rg);
+  float mv[CPL], o[CPL];
+  const int64_t mrow = MODE == FWD_BOND ? J.mul_idx[row] : row;
+  load_cols<D, CPL>(J.mulv + mrow * D, j, mv);
+#pragma unroll
+  for (int k = 0; k < CPL; ++k) {
+    const int c = L::col(j, k);
+    const float yc = J.ln.gc[c] * zc[k] + J.ln.bc[c];
+    const float yg = J.ln.gg[c] * zg[k] + J.ln.bg[c];
+    const float phi = yc * sigm(yc) * sigm(yg);
+    o[k] = MODE == FWD_ANGLE ? mv[k] + phi : mv[k] * phi;
+  }
+  store_cols<D, CPL>(J.out + (int64_t)row * D, j, o);
+}
+
+__global__ void __launch_bounds__(256, 3) k_gate_fwd_mm(GateMmJobs J) {
+  __shared__ __attribute__((aligned(16))) float Xs[kMmRows * kMmXld];
+  __shared__ __attribute__((aligned(16))) float Zs[kMmRows * kMmZld];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, h = lane >> 5, l32 = lane & 31;
+  // x tile loads: thread -> row tid / 4, 16 columns at 16 (tid % 4)
+  const int xr = tid >> 2, xc = 16 * (tid & 3);
+  auto job_of = [&](int tile) {
+    int k = 0;
+    while (k + 1 < J.n && tile >= J.j[k + 1].tile0) ++k;
+    return k;
+  };
+  auto fetch_x = [&](int tile, float4 (&v)[4]) {
+    const GateMmJob& jb = J.j[job_of(tile)];
+    const int row = (tile - jb.tile0) * kMmRows + xr;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) v[q] = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (row < jb.rows) {
+      const float* p = jb.x + (int64_t)row * 64 + xc;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) v[q] = *reinterpret_cast<const float4*>(p + 4 * q);
+    }
+  };
+  int tile = blockIdx.x;
+  if (tile >= J.ntiles) return;
+  float4 xv[4];
+  fetch_x(tile, xv);
+  int cur = -1;
+  float bfr[2][16], bias = 0.f;
+  while (tile < J.ntiles) {
+    const int k = job_of(tile);
+    const GateMmJob& jb = J.j[k];
+    if (k != cur) {
+      cur = k;
+      const int col = 32 * wave + l32;
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) bfr[kb][i] = jb.W[(int64_t)(32 * kb + 16 * h + i) * jb.ldw + col];
+      bias = jb.bias[col];
+    }
+#pragma unroll
+    for (int q = 0; q < 4; ++q) *reinterpret_cast<float4*>(&Xs[xr * kMmXld + xc + 4 * q]) = xv[q];
+    __syncthreads();
+    const int next = tile + gridDim.x;
+    if (next < J.ntiles) fetch_x(next, xv);
+#pragma unroll
+    for (int s = 0; s < kMmRows / 32; ++s) {
+      v16f acc;
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[e] = 0.f;
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) {
+        float af[16];
+        const float* ap = &Xs[(32 * s + l32) * kMmXld + 32 * kb + 16 * h];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const float4 v = *reinterpret_cast<const float4*>(ap + 4 * q);
+          af[4 * q] = v.x; af[4 * q + 1] = v.y; af[4 * q + 2] = v.z; af[4 * q + 3] = v.w;
+        }
+#pragma unroll
+        for (int i = 0; i < 16; ++i) acc = __builtin_amdgcn_mfma_f32_32x32x2f32(af[i], bfr[kb][i], acc, 0, 0, 0);
+      }
+#pragma unroll
+      for (int e = 0; e < 16; ++e)
+        Zs[(32 * s + 8 * (e >> 2) + 4 * h + (e & 3)) * kMmZld + 32 * wave + l32] = acc[e] + bias;
+    }
+    __syncthreads();
+    const int r0 = (tile - jb.tile0) * kMmRows;
+    using GL = Lanes<64, kMmCpl>;
+#pragma unroll 1
+    for (int pass = 0; pass < kMmRows / (4 * GL::RPW); ++pass) {
+      const int lr = (pass * 4 + wave) * GL::RPW + lane / GL::LPR;
+      if (jb.mode == FWD_ATOM) gate_mm_row<FWD_ATOM>(jb, r0, lr, Zs);
+      else if (jb.mode == FWD_BOND) gate_mm_row<FWD_BOND>(jb, r0, lr, Zs);
+      else gate_mm_row<FWD_ANGLE>(jb, r0, lr, Zs);
+    }
+    tile = next;
+  }
+}
+
 enum GateBwdMode { BWD_ATOM = 0, BWD_BOND = 1, BWD_ANGLE = 2 };
 
 // Backward gate: dz (2d values) from dphi, plus the LayerNorm parameter
@@ -1096,6 +1253,46 @@ int gate_fwd_launch(int D, GateFwdJobs J, hipStream_t st) {
   return CHGNET_OK;
 }
 
+// Launch the fused (d = 64) forward gates of one layer: a persistent grid of
+// at most three blocks per compute unit, tiles spread evenly over blocks.
+int gate_fwd_mm_launch(GateMmJobs J, hipStream_t st) {
+  GateMmJobs K{};
+  int tiles = 0;
+  for (int i = 0; i < J.n; ++i) {
+    if (J.j[i].rows <= 0) continue;
+    K.j[K.n] = J.j[i];
+    K.j[K.n].tile0 = tiles;
+    tiles += (int)cdiv(J.j[i].rows, kMmRows);
+    K.n++;
+  }
+  K.ntiles = tiles;
+  if (tiles == 0) return CHGNET_OK;
+  constexpr int kMaxBlocks = 3 * 256;
+  const int per = (int)cdiv(tiles, kMaxBlocks);
+  const int grid = (int)cdiv(tiles, per);
+  KLAUNCH(st, "k_gate_fwd", k_gate_fwd_mm<<<grid, 256, 0, st>>>(K));
+  return CHGNET_OK;
+}
+
+GateMmJob mm_job(int mode, int64_t rows, const float* x, const float* W, const float* bias, const GateAdds& ad,
+                 LnPtrs ln, const float* mulv, const int* idx, float* out, float* zsave, int ldzs) {
+  GateMmJob j{};
+  j.mode = mode;
+  j.rows = (int)rows;
+  j.x = x;
+  j.W = W;
+  j.ldw = 128;
+  j.bias = bias;
+  j.ad = ad;
+  j.ln = ln;
+  j.mulv = mulv;
+  j.mul_idx = idx;
+  j.out = out;
+  j.zsave = zsave;
+  j.ldzs = ldzs;
+  return j;
+}
+
 GateFwdJob fwd_job(int mode, int64_t rows, const float* z, int ldz, const GateAdds& ad, LnPtrs ln, const float* mulv,
                    const int* idx, float* out) {
   GateFwdJob j{};
@@ -1279,30 +1476,40 @@ int forward_impl(Ctx& c, const float* Pflat, float* energy, float* forces, float
     }
     CHG_TRY(run_gemms(ps, st, "gemm_proj"));
     ps.clear();
-    // edge and angle terms (+ bias); the gathered atom and bond terms are
-    // added by the gate kernels, which stream each row once
-    {
-      GemmProblem p = gp(E, 2 * D, a.zv[t], 2 * D);
-      seg(p, a.e[t], D, 0, D, Wav + 2 * D * 2 * D, 2 * D, 0);
-      p.bias = P + lo.av.b;
-      ps.push_back(p);
-      for (int k = 0; k < (ang ? 2 : 1); ++k) {
-        const float* W = (k ? Wan : Wbe) + 3 * D * 2 * D;
-        GemmProblem q = gp(A, 2 * D, a.zae[t] + k * 2 * D, 4 * D);
-        seg(q, a.a[t], D, 0, D, W, 2 * D, 0);
-        q.bias = P + (k ? lo.an.b : lo.be.b);
-        ps.push_back(q);
-      }
-      CHG_TRY(run_gemms(ps, st, "gemm_z"));
-      ps.clear();
-    }
-    // gates and aggregations
     const GateAdds ad_av = adds(2, a.Xa[t], 8 * D, a.edge_src, a.Xa[t] + 2 * D, 8 * D, g.edge_dst);
     const GateAdds ad_be = adds(3, a.Xa[t] + 4 * D, 8 * D, a.ang_ctr, a.Xb[t], 8 * D, a.ang_b1, a.Xb[t] + 4 * D, 8 * D,
                                 a.ang_b2);
     const GateAdds ad_an = adds(3, a.Xa[t] + 6 * D, 8 * D, a.ang_ctr, a.Xb[t] + 2 * D, 8 * D, a.ang_b1,
                                 a.Xb[t] + 6 * D, 8 * D, a.ang_b2);
-    {
+    const float* Wx_av = Wav + 2 * D * 2 * D;  // rows of e_ij
+    const float* Wx_be = Wbe + 3 * D * 2 * D;  // rows of a_ijk
+    const float* Wx_an = Wan + 3 * D * 2 * D;
+    if (D == 64) {
+      // pre-activations formed inside the gate kernel; z kept for the backward
+      GateMmJobs J{};
+      J.j[J.n++] = mm_job(FWD_ATOM, E, a.e[t], Wx_av, P + lo.av.b, ad_av, ln_ptrs(P, lo.av), a.ea, nullptr, a.msg,
+                          a.zv[t], 2 * D);
+      J.j[J.n++] = mm_job(FWD_BOND, A, a.a[t], Wx_be, P + lo.be.b, ad_be, ln_ptrs(P, lo.be), a.eb, a.ang_b2, a.msgb,
+                          a.zae[t], 4 * D);
+      if (ang)
+        J.j[J.n++] = mm_job(FWD_ANGLE, A, a.a[t], Wx_an, P + lo.an.b, ad_an, ln_ptrs(P, lo.an), a.a[t], nullptr,
+                            a.a[t + 1], a.zae[t] + 2 * D, 4 * D);
+      CHG_TRY(gate_fwd_mm_launch(J, st));
+    } else {
+      // edge and angle terms (+ bias) by the GEMM; the gathered atom and bond
+      // terms are added by the gate kernels, which stream each row once
+      GemmProblem p = gp(E, 2 * D, a.zv[t], 2 * D);
+      seg(p, a.e[t], D, 0, D, Wx_av, 2 * D, 0);
+      p.bias = P + lo.av.b;
+      ps.push_back(p);
+      for (int k = 0; k < (ang ? 2 : 1); ++k) {
+        GemmProblem q = gp(A, 2 * D, a.zae[t] + k * 2 * D, 4 * D);
+        seg(q, a.a[t], D, 0, D, k ? Wx_an : Wx_be, 2 * D, 0);
+        q.bias = P + (k ? lo.an.b : lo.be.b);
+        ps.push_back(q);
+      }
+      CHG_TRY(run_gemms(ps, st, "gemm_z"));
+      ps.clear();
       GateFwdJobs J{};
       J.j[J.n++] = fwd_job(FWD_ATOM, E, a.zv[t], 2 * D, ad_av, ln_ptrs(P, lo.av), a.ea, nullptr, a.msg);
       J.j[J.n++] = fwd_job(FWD_BOND, A, a.zae[t], 4 * D, ad_be, ln_ptrs(P, lo.be), a.eb, a.ang_b2, a.msgb);
