@@ -388,108 +388,230 @@ __global__ void __launch_bounds__(256) k_gemm_ks(GemmBatch batch) {
 
 struct TnPlan {
   TnProblem p;
-  int rpc;      // rows per chunk
+  int vx, vy;            // fragment widths: a wave tile is 32 vx x 32 vy
+  int tiles_m, tiles_n;  // wave tiles per chunk (tiles_m = 0: column sums only)
+  int rpc;               // rows per chunk (a multiple of 64: four wave ranges of 16-row groups)
   int nchunks;
-  int tiles_n;  // tiles along n
-  int tiles;    // total output tiles
-  int64_t off;  // partial offset
+  int block0;            // first block of this problem in the launch
+  int has_bias;          // partials carry one more row: the column sums of Y
+  float* bout;           // destination of the column sums (split like out)
+  int bowidth;
+  float* bouts[4];
+  int64_t off;  // partial offset; a chunk's partial is (M + has_bias) x N
 };
 struct TnLaunch {
   int n;
   TnPlan q[kMaxTnProblems];
 };
 
-// Split-K X^T Y: a 64 x 128 output tile per block (waves in a 2 x 2 grid,
-// 32 x 64 each as two 32x32 MFMA tiles), rows streamed 32 at a time.
+// Split-K X^T Y without LDS tiles: each wavefront streams its own row range
+// and loads its MFMA fragments straight from global memory. In MFMA k-step i
+// of a group of 2 KS rows, lane half h supplies row KS h + i; lane c = lane % 32
+// holds columns vx c + v (v < vx) of the X row and vy c + u of the Y row, so
+// wave tile v of X and u of Y are column-interleaved and the fragment loads
+// are 4- or 8-byte vectors. The next group's fragments are loaded while the
+// current group's MFMAs run. The four wavefronts of a block take consecutive
+// quarters of the block's rows; their tiles are added in wave order in LDS.
+// A problem with a bias row also sums the Y columns (the bias gradient of a
+// layer whose weight gradient is X^T Y).
 // ROLE only names the instantiation (1: interaction-block weight gradients).
-template <int ROLE>
-__global__ void __launch_bounds__(256) k_tn(TnLaunch L, float* __restrict__ part) {
-  constexpr int TM = 64, TN = 128, RC = 32;
-  const TnPlan& Q = L.q[blockIdx.z];
+constexpr int kTnRed = 2 * 64 * 64 + 4 * 64;
+
+template <int VX, int VY, bool XFULL, bool YFULL, bool HASX = true>
+__device__ __forceinline__ void tn_wave(const TnPlan& Q, int chunk, int m0, int n0, bool colsum, float* red,
+                                        float* __restrict__ part) {
+  // MFMA k-steps (row pairs) per register buffer: 2, or 1 where two-column
+  // fragments are loaded one element at a time (partial or unaligned tiles,
+  // not on the common shapes)
+  constexpr int KS = ((VX == 2 && HASX && !XFULL) || (VY == 2 && !YFULL)) ? 1 : 2;
   const TnProblem& P = Q.p;
-  const int chunk = blockIdx.x;
-  if (chunk >= Q.nchunks || (int)blockIdx.y >= Q.tiles) return;
-  const int m0 = (blockIdx.y / Q.tiles_n) * TM, n0 = (blockIdx.y % Q.tiles_n) * TN;
-  const int rlo = chunk * Q.rpc;
-  const int rhi = min(P.R, rlo + Q.rpc);
-  __shared__ float Xs[RC][TM + 4];
-  __shared__ float Ys[RC][TN + 4];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = (wave >> 1) * 32, wn = (wave & 1) * 64;
-  v16f acc[2];
+  const int lane = threadIdx.x & 63, c = lane & 31, h = lane >> 5;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // uniform: scalar row range
+  const int wr = Q.rpc / 4;
+  const int rlo = chunk * Q.rpc + wave * wr;
+  const int rhi = min(P.R, rlo + wr);
+  const int xm = m0 + VX * c, yn = n0 + VY * c;
+  v16f acc[VX][VY];
 #pragma unroll
-  for (int t = 0; t < 2; ++t)
+  for (int v = 0; v < VX; ++v)
 #pragma unroll
-    for (int j = 0; j < 16; ++j) acc[t][j] = 0.f;
-  const bool xvec = P.X && ((P.ldx | P.x_col) & 3) == 0 && ((uintptr_t)P.X & 15) == 0;
-  const bool yvec = ((P.ldy | P.y_col) & 3) == 0 && ((uintptr_t)P.Y & 15) == 0;
-  float4 xs[2], ys[4];
-  auto fetch = [&](int rb) {
+    for (int u = 0; u < VY; ++u)
 #pragma unroll
-    for (int q = 0; q < 2; ++q) {
-      const int idx = tid + 256 * q, lr = idx >> 4, cc = (idx & 15) * 4, r = rb + lr;
-      float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-      if (r < rhi) {
-        if (P.X) {
-          const int64_t xr = P.x_rows ? P.x_rows[r] : r;
-          v = load4(P.X + xr * P.ldx + P.x_col + m0, cc, P.M - m0, xvec);
-        } else if (m0 == 0 && cc == 0) {
-          v.x = 1.0f;
+      for (int j = 0; j < 16; ++j) acc[v][u][j] = 0.f;
+  float ysum[VY];
+#pragma unroll
+  for (int u = 0; u < VY; ++u) ysum[u] = 0.f;
+  float xf[2][KS][VX], yf[2][KS][VY];
+  // Branch-free loads: rows and columns are clamped into the matrix. Columns
+  // past M or N only reach outputs that are not stored; rows past the wave's
+  // range are cancelled by a 0/1 mask on the Y values, applied when the
+  // group is consumed, so that every load of a group is in flight at once.
+  float rmask[2][KS];
+  auto fetch = [&](int g, int b) {
+    int xr[KS], yr[KS];
+#pragma unroll
+    for (int i = 0; i < KS; ++i) {
+      xr[i] = yr[i] = min(g + KS * h + i, rhi - 1);
+      rmask[b][i] = g + KS * h + i < rhi ? 1.f : 0.f;
+    }
+    if (P.x_rows)
+#pragma unroll
+      for (int i = 0; i < KS; ++i) xr[i] = P.x_rows[xr[i]];
+    if (P.y_rows)
+#pragma unroll
+      for (int i = 0; i < KS; ++i) yr[i] = P.y_rows[yr[i]];
+#pragma unroll
+    for (int i = 0; i < KS; ++i) {
+      if (HASX) {
+        const float* xp = P.X + (int64_t)xr[i] * P.ldx + P.x_col;
+        if (XFULL) {
+          const float2 t = *reinterpret_cast<const float2*>(xp + xm);
+          xf[b][i][0] = t.x;
+          xf[b][i][VX - 1] = t.y;
+        } else {
+#pragma unroll
+          for (int v = 0; v < VX; ++v) xf[b][i][v] = xp[min(xm + v, P.M - 1)];
         }
       }
-      xs[q] = v;
-    }
+      const float* yp = P.Y + (int64_t)yr[i] * P.ldy + P.y_col;
+      if (YFULL) {
+        const float2 t = *reinterpret_cast<const float2*>(yp + yn);
+        yf[b][i][0] = t.x;
+        yf[b][i][VY - 1] = t.y;
+      } else {
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int idx = tid + 256 * q, lr = idx >> 5, cc = (idx & 31) * 4, r = rb + lr;
-      float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-      if (r < rhi) {
-        const int64_t yr = P.y_rows ? P.y_rows[r] : r;
-        v = load4(P.Y + yr * P.ldy + P.y_col + n0, cc, P.N - n0, yvec);
+        for (int u = 0; u < VY; ++u) yf[b][i][u] = yp[min(yn + u, P.N - 1)];
       }
-      ys[q] = v;
     }
   };
-  if (rlo < rhi) fetch(rlo);
-  for (int rb = rlo; rb < rhi; rb += RC) {
+  auto compute = [&](int b) {
 #pragma unroll
-    for (int q = 0; q < 2; ++q) {
-      const int idx = tid + 256 * q;
-      *reinterpret_cast<float4*>(&Xs[idx >> 4][(idx & 15) * 4]) = xs[q];
-    }
+    for (int i = 0; i < KS; ++i) {
+      float y[VY];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int idx = tid + 256 * q;
-      *reinterpret_cast<float4*>(&Ys[idx >> 5][(idx & 31) * 4]) = ys[q];
-    }
-    __syncthreads();
-    if (rb + RC < rhi) fetch(rb + RC);
-    // lane half h takes rows 16h .. 16h+15 of the chunk (k-step i -> row 16h+i)
-    float af[16], bf0[16], bf1[16];
-    const int h = lane >> 5;
+      for (int u = 0; u < VY; ++u) y[u] = yf[b][i][u] * rmask[b][i];
+      if (HASX) {
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      af[i] = Xs[16 * h + i][wm + (lane & 31)];
-      bf0[i] = Ys[16 * h + i][wn + (lane & 31)];
-      bf1[i] = Ys[16 * h + i][wn + 32 + (lane & 31)];
-    }
+        for (int v = 0; v < VX; ++v)
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      acc[0] = __builtin_amdgcn_mfma_f32_32x32x2f32(af[i], bf0[i], acc[0], 0, 0, 0);
-      acc[1] = __builtin_amdgcn_mfma_f32_32x32x2f32(af[i], bf1[i], acc[1], 0, 0, 0);
+          for (int u = 0; u < VY; ++u)
+            acc[v][u] = __builtin_amdgcn_mfma_f32_32x32x2f32(xf[b][i][v], y[u], acc[v][u], 0, 0, 0);
+      }
+      if (colsum) {
+#pragma unroll
+        for (int u = 0; u < VY; ++u) ysum[u] += y[u];
+      }
     }
-    __syncthreads();
+  };
+  // two register buffers, alternating with a constant index
+  constexpr int GR = 2 * KS;  // rows per group
+  if (rlo < rhi) fetch(rlo, 0);
+  for (int g = rlo; g < rhi; g += 2 * GR) {
+    if (g + GR < rhi) fetch(g + GR, 1);
+    compute(0);
+    if (g + GR >= rhi) break;
+    if (g + 2 * GR < rhi) fetch(g + 2 * GR, 0);
+    compute(1);
   }
-  float* out = part + Q.off + (int64_t)chunk * P.M * P.N;
+  // column sums: the two lane halves hold different rows of the same column
+  if (colsum) {
 #pragma unroll
-  for (int j = 0; j < 16; ++j) {
-    const int m = m0 + wm + 8 * (j >> 2) + 4 * (lane >> 5) + (j & 3);
-    if (m >= P.M) continue;
+    for (int u = 0; u < VY; ++u) ysum[u] += __shfl_xor(ysum[u], 32);
+    if (h == 0) {
 #pragma unroll
-    for (int t = 0; t < 2; ++t) {
-      const int n = n0 + wn + 32 * t + (lane & 31);
-      if (n < P.N) out[(int64_t)m * P.N + n] = acc[t][j];
+      for (int u = 0; u < VY; ++u) red[2 * 64 * 64 + wave * 64 + u * 32 + c] = ysum[u];
     }
+  }
+  // wave tiles added in the order (w0 + w1) + (w2 + w3)
+  auto put = [&](float* dst) {
+#pragma unroll
+    for (int v = 0; v < VX; ++v)
+#pragma unroll
+      for (int u = 0; u < VY; ++u)
+#pragma unroll
+        for (int j = 0; j < 16; ++j) dst[((v * VY + u) * 16 + j) * 64 + lane] = acc[v][u][j];
+  };
+  auto add = [&](const float* src) {
+#pragma unroll
+    for (int v = 0; v < VX; ++v)
+#pragma unroll
+      for (int u = 0; u < VY; ++u)
+#pragma unroll
+        for (int j = 0; j < 16; ++j) acc[v][u][j] += src[((v * VY + u) * 16 + j) * 64 + lane];
+  };
+  if (wave == 1) put(red);
+  if (wave == 3) put(red + 64 * 64);
+  __syncthreads();
+  if (wave == 0) add(red);
+  if (wave == 2) add(red + 64 * 64);
+  __syncthreads();
+  if (wave == 2) put(red);
+  __syncthreads();
+  if (wave != 0) return;
+  add(red);
+  const int rows_out = P.M + Q.has_bias;
+  float* out = part + Q.off + (int64_t)chunk * rows_out * P.N;
+  if (HASX) {
+#pragma unroll
+    for (int v = 0; v < VX; ++v)
+#pragma unroll
+      for (int j = 0; j < 16; ++j) {
+        const int m = m0 + VX * (8 * (j >> 2) + 4 * h + (j & 3)) + v;
+        if (m >= P.M) continue;
+#pragma unroll
+        for (int u = 0; u < VY; ++u) {
+          const int n = yn + u;
+          if (n < P.N) out[(int64_t)m * P.N + n] = acc[v][u][j];
+        }
+      }
+  }
+  if (colsum && h == 0) {
+    const float* ys = red + 2 * 64 * 64;
+#pragma unroll
+    for (int u = 0; u < VY; ++u) {
+      const int k = u * 32 + c;
+      const float s = (ys[k] + ys[64 + k]) + (ys[128 + k] + ys[192 + k]);
+      const int n = yn + u;
+      if (n < P.N) out[(int64_t)P.M * P.N + n] = s;
+    }
+  }
+}
+
+template <int ROLE>
+__global__ void __launch_bounds__(256, 3) k_tn(TnLaunch L, float* __restrict__ part) {
+  __shared__ float red[kTnRed];
+  int k = 0;
+  while (k + 1 < L.n && (int)blockIdx.x >= L.q[k + 1].block0) ++k;
+  const TnPlan& Q = L.q[k];
+  const int lb = blockIdx.x - Q.block0;
+  const int tiles = max(Q.tiles_m, 1) * Q.tiles_n;
+  const int chunk = lb / tiles, tile = lb % tiles;
+  const int tm = tile / Q.tiles_n, tn = tile % Q.tiles_n;
+  const int m0 = tm * 32 * Q.vx, n0 = tn * 32 * Q.vy;
+  const bool colsum = Q.has_bias && tm == 0;
+  // 8-byte fragment loads where the wave tile lies inside the matrix and
+  // the rows are 8-byte aligned
+  const TnProblem& P = Q.p;
+  const bool xf = Q.vx == 2 && P.X && ((P.ldx | P.x_col) & 1) == 0 && ((uintptr_t)P.X & 7) == 0 && m0 + 64 <= P.M;
+  const bool yf = Q.vy == 2 && ((P.ldy | P.y_col) & 1) == 0 && ((uintptr_t)P.Y & 7) == 0 && n0 + 64 <= P.N;
+  if (Q.tiles_m == 0) {
+    // column sums only
+    if (yf) tn_wave<1, 2, false, true, false>(Q, chunk, m0, n0, colsum, red, part);
+    else if (Q.vy == 2) tn_wave<1, 2, false, false, false>(Q, chunk, m0, n0, colsum, red, part);
+    else tn_wave<1, 1, false, false, false>(Q, chunk, m0, n0, colsum, red, part);
+  } else if (Q.vx == 2 && Q.vy == 2) {
+    if (xf && yf) tn_wave<2, 2, true, true>(Q, chunk, m0, n0, colsum, red, part);
+    else if (xf) tn_wave<2, 2, true, false>(Q, chunk, m0, n0, colsum, red, part);
+    else if (yf) tn_wave<2, 2, false, true>(Q, chunk, m0, n0, colsum, red, part);
+    else tn_wave<2, 2, false, false>(Q, chunk, m0, n0, colsum, red, part);
+  } else if (Q.vx == 2) {
+    if (xf) tn_wave<2, 1, true, false>(Q, chunk, m0, n0, colsum, red, part);
+    else tn_wave<2, 1, false, false>(Q, chunk, m0, n0, colsum, red, part);
+  } else if (Q.vy == 2) {
+    if (yf) tn_wave<1, 2, false, true>(Q, chunk, m0, n0, colsum, red, part);
+    else tn_wave<1, 2, false, false>(Q, chunk, m0, n0, colsum, red, part);
+  } else {
+    tn_wave<1, 1, false, false>(Q, chunk, m0, n0, colsum, red, part);
   }
 }
 
@@ -513,7 +635,7 @@ __global__ void __launch_bounds__(1024) k_tn_reduce(TnLaunch L, const float* __r
   __shared__ double red[16][64];
   const TnPlan& Q = L.q[blockIdx.y];
   const TnProblem& P = Q.p;
-  const int64_t mn = (int64_t)P.M * P.N;
+  const int64_t mn = (int64_t)(P.M + Q.has_bias) * P.N;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int64_t k = (int64_t)blockIdx.x * 64 + lane;
   if ((int64_t)blockIdx.x * 64 >= mn) return;
@@ -523,9 +645,16 @@ __global__ void __launch_bounds__(1024) k_tn_reduce(TnLaunch L, const float* __r
     double s = 0.0;
     for (int q = 0; q < 16; ++q) s += red[q][lane];
     const int m = (int)(k / P.N), n = (int)(k % P.N);
-    const int q = P.owidth > 0 ? n / P.owidth : 0;
-    const int nn = P.owidth > 0 ? n - q * P.owidth : n;
-    float* o = (q == 0 ? P.out : P.outs[q]) + (int64_t)m * P.ld_out + nn;
+    float* o;
+    if (m < P.M) {
+      const int q = P.owidth > 0 ? n / P.owidth : 0;
+      const int nn = P.owidth > 0 ? n - q * P.owidth : n;
+      o = (q == 0 ? P.out : P.outs[q]) + (int64_t)m * P.ld_out + nn;
+    } else {
+      const int q = Q.bowidth > 0 ? n / Q.bowidth : 0;
+      const int nn = Q.bowidth > 0 ? n - q * Q.bowidth : n;
+      o = (q == 0 ? Q.bout : Q.bouts[q]) + nn;
+    }
     *o = (float)((double)*o + s);
   }
 }
@@ -614,39 +743,71 @@ int gemm_launch(const GemmBatch& b, hipStream_t st, const char* tag) {
 }
 
 int tn_launch(const TnBatch& b, float* part, int64_t part_cap, hipStream_t st, const char* tag) {
-  TnLaunch L;
-  L.n = b.n;
-  int64_t off = 0;
-  int gx = 0, gy = 0;
-  const int64_t budget = part_cap / std::max(1, b.n);
+  if (b.n == 0) return CHGNET_OK;
+  // A bias problem (X = ones, M = 1) becomes the column-sum row of a weight
+  // problem over the same Y rows and columns, so Y is streamed once.
+  TnLaunch L{};
   for (int i = 0; i < b.n; ++i) {
+    const TnProblem& p = b.p[i];
+    if (p.X == nullptr) continue;
+    if (p.M <= 0 || p.N <= 0) return fail(CHGNET_EINVAL, "tn: empty output");
+    TnPlan& q = L.q[L.n++];
+    q = TnPlan{};
+    q.p = p;
+  }
+  for (int i = 0; i < b.n; ++i) {
+    const TnProblem& p = b.p[i];
+    if (p.X != nullptr) continue;
+    if (p.M != 1 || p.N <= 0) return fail(CHGNET_EINVAL, "tn: a problem without X must have one output row");
+    TnPlan* host = nullptr;
+    for (int j = 0; j < L.n && !host; ++j) {
+      const TnProblem& w = L.q[j].p;
+      if (!L.q[j].has_bias && w.X && w.R == p.R && w.N == p.N && w.Y == p.Y && w.ldy == p.ldy && w.y_col == p.y_col &&
+          w.y_rows == p.y_rows)
+        host = &L.q[j];
+    }
+    if (!host) {
+      host = &L.q[L.n++];
+      *host = TnPlan{};
+      host->p = p;
+      host->p.M = 0;
+    }
+    host->has_bias = 1;
+    host->bout = p.out;
+    host->bowidth = p.owidth;
+    for (int q = 1; q < 4; ++q) host->bouts[q] = p.outs[q];
+  }
+  int64_t units = 0;
+  for (int i = 0; i < L.n; ++i) {
     TnPlan& q = L.q[i];
-    q.p = b.p[i];
-    const int tm = (int)cdiv(q.p.M, 64);
-    q.tiles_n = (int)cdiv(q.p.N, 128);
-    q.tiles = tm * q.tiles_n;
-    const int64_t mn = (int64_t)q.p.M * q.p.N;
-    int64_t nch = std::max<int64_t>(1, std::min<int64_t>(cdiv(q.p.R, 128), std::max(8, 1024 / q.tiles)));
-    nch = std::min<int64_t>(nch, 512);
-    nch = std::min<int64_t>(nch, std::max<int64_t>(1, budget / std::max<int64_t>(1, mn)));
-    int64_t rpc = cdiv(cdiv(q.p.R, nch), 32) * 32;
-    if (rpc < 32) rpc = 32;
-    q.rpc = (int)rpc;
+    q.vx = q.p.M <= 32 ? 1 : 2;
+    q.vy = q.p.N <= 32 ? 1 : 2;
+    q.tiles_m = q.p.X ? (int)cdiv(q.p.M, 32 * q.vx) : 0;
+    q.tiles_n = (int)cdiv(q.p.N, 32 * q.vy);
+    units += cdiv(std::max(q.p.R, 0), 64) * std::max(q.tiles_m, 1) * q.tiles_n;
+  }
+  // about a thousand blocks over the launch, every problem with the same chunk length
+  const int64_t per = std::max<int64_t>(1, cdiv(units, 1024));
+  const int rpc = (int)std::min<int64_t>(64 * per, 1 << 24);
+  int64_t off = 0, blocks = 0, maxmn = 0;
+  for (int i = 0; i < L.n; ++i) {
+    TnPlan& q = L.q[i];
+    q.rpc = rpc;
     q.nchunks = q.p.R > 0 ? (int)cdiv(q.p.R, rpc) : 0;
+    q.block0 = (int)blocks;
     q.off = off;
+    const int64_t mn = (int64_t)(q.p.M + q.has_bias) * q.p.N;
     off += (int64_t)q.nchunks * mn;
-    gx = std::max(gx, q.nchunks);
-    gy = std::max(gy, q.tiles);
+    blocks += (int64_t)q.nchunks * std::max(q.tiles_m, 1) * q.tiles_n;
+    maxmn = std::max(maxmn, mn);
   }
   if (off > part_cap) return fail(CHGNET_EWORKSPACE, "split-K partial buffer too small");
-  if (b.n == 0) return CHGNET_OK;
-  if (gx > 0) {
-    if (std::string(tag) == "tn_in") KLAUNCH(st, tag, k_tn<1><<<dim3(gx, gy, b.n), 256, 0, st>>>(L, part));
-    else KLAUNCH(st, tag, k_tn<0><<<dim3(gx, gy, b.n), 256, 0, st>>>(L, part));
+  if (blocks > 0x7fffffff) return fail(CHGNET_EINVAL, "tn: too many blocks");
+  if (blocks > 0) {
+    if (std::string(tag) == "tn_in") KLAUNCH(st, tag, k_tn<1><<<(unsigned)blocks, 256, 0, st>>>(L, part));
+    else KLAUNCH(st, tag, k_tn<0><<<(unsigned)blocks, 256, 0, st>>>(L, part));
+    KLAUNCH(st, "k_tn_reduce", k_tn_reduce<<<dim3((unsigned)cdiv(maxmn, 64), L.n), 1024, 0, st>>>(L, part));
   }
-  int64_t maxmn = 0;
-  for (int i = 0; i < b.n; ++i) maxmn = std::max<int64_t>(maxmn, (int64_t)b.p[i].M * b.p[i].N);
-  KLAUNCH(st, "k_tn_reduce", k_tn_reduce<<<dim3((unsigned)cdiv(maxmn, 64), b.n), 1024, 0, st>>>(L, part));
   return CHGNET_OK;
 }
 
