@@ -503,14 +503,16 @@ __device__ __forceinline__ void tn_wave(const TnPlan& Q, int chunk, int m0, int 
       }
     }
   };
-  // two register buffers, alternating with a constant index
+  // two register buffers, alternating with a constant index; a fixed trip
+  // count (rows past the range are masked) keeps the accumulators in place
   constexpr int GR = 2 * KS;  // rows per group
-  if (rlo < rhi) fetch(rlo, 0);
-  for (int g = rlo; g < rhi; g += 2 * GR) {
-    if (g + GR < rhi) fetch(g + GR, 1);
+  const int iters = rhi > rlo ? (rhi - rlo + 2 * GR - 1) / (2 * GR) : 0;
+  if (iters > 0) fetch(rlo, 0);
+  for (int it = 0; it < iters; ++it) {
+    const int g = rlo + it * 2 * GR;
+    fetch(g + GR, 1);
     compute(0);
-    if (g + GR >= rhi) break;
-    if (g + 2 * GR < rhi) fetch(g + 2 * GR, 0);
+    if (it + 1 < iters) fetch(g + 2 * GR, 0);
     compute(1);
   }
   // column sums: the two lane halves hold different rows of the same column
@@ -786,8 +788,9 @@ int tn_launch(const TnBatch& b, float* part, int64_t part_cap, hipStream_t st, c
     q.tiles_n = (int)cdiv(q.p.N, 32 * q.vy);
     units += cdiv(std::max(q.p.R, 0), 64) * std::max(q.tiles_m, 1) * q.tiles_n;
   }
-  // about a thousand blocks over the launch, every problem with the same chunk length
-  const int64_t per = std::max<int64_t>(1, cdiv(units, 1024));
+  // about one block per resident slot (three 4-wave blocks per compute
+  // unit): fewer, longer blocks measured faster than several rounds
+  const int64_t per = std::max<int64_t>(1, cdiv(units, 3 * 256));
   const int rpc = (int)std::min<int64_t>(64 * per, 1 << 24);
   int64_t off = 0, blocks = 0, maxmn = 0;
   for (int i = 0; i < L.n; ++i) {
