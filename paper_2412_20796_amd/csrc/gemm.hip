@@ -270,119 +270,140 @@ __global__ void __launch_bounds__(256) k_gemm(GemmBatch batch) {
   }
 }
 
-// Small-M variant: a 32 x 64 output tile per block; the four wavefronts take
-// every fourth K chunk (each with its own LDS tiles) and their partial tiles
-// are added in wavefront order at the end.
-__global__ void __launch_bounds__(256) k_gemm_ks(GemmBatch batch) {
-  constexpr int BM = 32, BN = 64, KC = 32, KP = KC + 4, SP = BN + 4;
+// Direct-load GEMM for short or few row tiles: each wavefront owns a 32 x 64
+// tile of C and streams its fragments straight from global memory (no LDS
+// staging), k in groups of 8: in MFMA k-step i of a group, lane half h
+// supplies k = 4h + i; lane c = lane % 32 holds output columns 2c + u of the
+// tile (u < 2: two 32x32 tiles with interleaved columns), so B fragments are
+// 8-byte row pieces (or 16-byte k runs when B is stored transposed). The
+// WK wavefronts of a tile split its k groups into contiguous runs and their
+// partial tiles are added in wave order in LDS before the shared epilogue.
+// Rows, columns and k beyond the matrices are clamped into them and
+// cancelled through a 0/1 mask on the B fragment (a clamped A entry is a
+// finite operand entry times zero).
+constexpr int kGwWaves = 8;
+constexpr int kGwLd = 64 + 4;
+
+template <int WK>
+__global__ void __launch_bounds__(512, 2) k_gemm_w(GemmBatch batch) {
+  __shared__ __attribute__((aligned(16))) float slot[kGwWaves * 32 * kGwLd];
   const GemmProblem& P = batch.p[blockIdx.z];
-  const int r0 = blockIdx.x * BM, c0 = blockIdx.y * BN;
-  if (r0 >= P.M || c0 >= P.N) return;
-  constexpr int kWave = BM * KP + BN * KP;  // floats of one wavefront's tiles
-  __shared__ __attribute__((aligned(16))) float smem[4 * kWave > 4 * BM * SP ? 4 * kWave : 4 * BM * SP];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, h = lane >> 5;
-  float (*As)[KP] = reinterpret_cast<float (*)[KP]>(smem + wave * kWave);
-  float (*Bs)[KP] = reinterpret_cast<float (*)[KP]>(smem + wave * kWave + BM * KP);
+  constexpr int TPB = kGwWaves / WK;  // row tiles per block
+  const int tid = threadIdx.x, lane = tid & 63, c = lane & 31, h = lane >> 5;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int tl = wave / WK, kp = wave % WK;
+  const int r0 = (blockIdx.x * TPB + tl) * 32, n0 = blockIdx.y * 64;
+  if (blockIdx.x * TPB * 32 >= P.M || n0 >= P.N) return;  // uniform over the block
+  int groups = 0;
+  for (int s = 0; s < P.nseg; ++s) groups += (P.seg[s].K + 7) / 8;
+  const int g_lo = kp * groups / WK, g_hi = (kp + 1) * groups / WK;
+  // this lane's A row (clamped) and B columns (clamped)
+  const int arow_i = min(r0 + c, P.M - 1);
+  const int64_t arow = P.a_rows ? P.a_rows[arow_i] : arow_i;
+  const int ncol0 = n0 + 2 * c;
+  const int nc0 = min(ncol0, P.N - 1), nc1 = min(ncol0 + 1, P.N - 1);
+  const float nm0 = ncol0 < P.N ? 1.f : 0.f, nm1 = ncol0 + 1 < P.N ? 1.f : 0.f;
   v16f acc[2];
 #pragma unroll
-  for (int t = 0; t < 2; ++t)
+  for (int u = 0; u < 2; ++u)
 #pragma unroll
-    for (int j = 0; j < 16; ++j) acc[t][j] = 0.f;
-  // A loads: lane -> row lane / 2, 16 consecutive k at 16 (lane & 1)
-  const int arl = lane >> 1, akl = 16 * (lane & 1);
-  const int arow_i = r0 + arl;
-  const bool aval = arow_i < P.M;
-  const int64_t arow = aval ? (P.a_rows ? P.a_rows[arow_i] : arow_i) : 0;
-  int nch = 0;
-  for (int s = 0; s < P.nseg; ++s) nch += (P.seg[s].K + KC - 1) / KC;
-  const int rounds = (nch + 3) / 4;
-  int s = 0, kc = 0;  // chunk cursor: segment s, chunk kc within it (this wave's next chunk)
-  auto advance = [&](int n) {
-    while (n > 0 && s < P.nseg) {
-      const int left = (P.seg[s].K + KC - 1) / KC - kc;
-      if (n < left) { kc += n; n = 0; } else { n -= left; ++s; kc = 0; }
+    for (int j = 0; j < 16; ++j) acc[u][j] = 0.f;
+  constexpr int NB = 4;  // register buffers: NB - 1 groups in flight ahead of the MFMAs
+  float af[NB][4], bf[NB][4][2];
+  // group g -> (segment, k0)
+  auto locate = [&](int g, int& s, int& k0) {
+    s = 0;
+    int left = g;
+    while (s + 1 < P.nseg && left >= (P.seg[s].K + 7) / 8) {
+      left -= (P.seg[s].K + 7) / 8;
+      ++s;
+    }
+    k0 = 8 * left;
+  };
+  auto fetch = [&](int g, int b) {
+    int s, k0;
+    locate(g, s, k0);
+    const GemmSeg& S = P.seg[s];
+    const int kb = k0 + 4 * h;
+    const float* ap = S.A + arow * S.lda + S.a_col;
+    // vector paths only where every lane's piece is inside (uniform tests)
+    if (((S.lda | S.a_col | S.K) & 3) == 0 && ((uintptr_t)S.A & 15) == 0 && (S.K & 7) == 0) {
+      const float4 t = *reinterpret_cast<const float4*>(ap + kb);
+      af[b][0] = t.x; af[b][1] = t.y; af[b][2] = t.z; af[b][3] = t.w;
+    } else {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) af[b][i] = ap[min(kb + i, S.K - 1)];
+    }
+    float km[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) km[i] = kb + i < S.K ? 1.f : 0.f;
+    if (!S.trans) {
+      const bool bvec = (S.ldb & 1) == 0 && ((uintptr_t)S.B & 7) == 0 && n0 + 64 <= P.N;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float* bp = S.B + (int64_t)min(kb + i, S.K - 1) * S.ldb;
+        if (bvec) {
+          const float2 t = *reinterpret_cast<const float2*>(bp + ncol0);
+          bf[b][i][0] = t.x * km[i];
+          bf[b][i][1] = t.y * km[i];
+        } else {
+          bf[b][i][0] = bp[nc0] * (km[i] * nm0);
+          bf[b][i][1] = bp[nc1] * (km[i] * nm1);
+        }
+      }
+    } else {
+      const bool bvec = (S.ldb & 3) == 0 && ((uintptr_t)S.B & 15) == 0 && (S.K & 7) == 0;
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        const float* bp = S.B + (int64_t)(u ? nc1 : nc0) * S.ldb;
+        const float m = u ? nm1 : nm0;
+        if (bvec) {
+          const float4 t = *reinterpret_cast<const float4*>(bp + kb);
+          bf[b][0][u] = t.x * m; bf[b][1][u] = t.y * m; bf[b][2][u] = t.z * m; bf[b][3][u] = t.w * m;
+        } else {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) bf[b][i][u] = bp[min(kb + i, S.K - 1)] * (km[i] * m);
+        }
+      }
     }
   };
-  advance(wave);
-  for (int rd = 0; rd < rounds; ++rd) {
-    const bool has = s < P.nseg;
-    if (has) {
-      const GemmSeg S = P.seg[s];
-      const int k0 = kc * KC;
-      const bool avec = ((S.lda | S.a_col) & 3) == 0 && ((uintptr_t)S.A & 15) == 0;
+  auto compute = [&](int b) {
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (aval) v = load4(S.A + arow * S.lda + S.a_col + k0, akl + 4 * q, S.K - k0, avec);
-        *reinterpret_cast<float4*>(&As[arl][akl + 4 * q]) = v;
-      }
-      const int n = c0 + lane;
-      if (!S.trans) {
+    for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int q = 0; q < 8; ++q) {
-          float v[4];
+      for (int u = 0; u < 2; ++u) acc[u] = __builtin_amdgcn_mfma_f32_32x32x2f32(af[b][i], bf[b][i][u], acc[u], 0, 0, 0);
+  };
+  const int n = g_hi - g_lo;
 #pragma unroll
-          for (int u = 0; u < 4; ++u) {
-            const int k = k0 + 4 * q + u;
-            v[u] = (n < P.N && k < S.K) ? S.B[(int64_t)k * S.ldb + n] : 0.f;
-          }
-          *reinterpret_cast<float4*>(&Bs[lane][4 * q]) = make_float4(v[0], v[1], v[2], v[3]);
-        }
-      } else {
-        const bool bvec = (S.ldb & 3) == 0 && ((uintptr_t)S.B & 15) == 0;
+  for (int j = 0; j < NB - 1; ++j)
+    if (j < n) fetch(g_lo + j, j);
+  for (int it = 0; it < n; it += NB) {
 #pragma unroll
-        for (int q = 0; q < 8; ++q) {
-          float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-          if (n < P.N) v = load4(S.B + (int64_t)n * S.ldb + k0, 4 * q, S.K - k0, bvec);
-          *reinterpret_cast<float4*>(&Bs[lane][4 * q]) = v;
-        }
-      }
+    for (int j = 0; j < NB; ++j) {
+      if (it + j + NB - 1 < n) fetch(g_lo + it + j + NB - 1, (j + NB - 1) % NB);
+      if (it + j < n) compute(j);
     }
-    __syncthreads();
-    if (has) {
-      float af[16], bf[2][16];
-      const float* ap = &As[lane & 31][16 * h];
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const float4 v = *reinterpret_cast<const float4*>(ap + 4 * q);
-        af[4 * q] = v.x; af[4 * q + 1] = v.y; af[4 * q + 2] = v.z; af[4 * q + 3] = v.w;
-      }
-#pragma unroll
-      for (int t = 0; t < 2; ++t) {
-        const float* bp = &Bs[32 * t + (lane & 31)][16 * h];
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const float4 v = *reinterpret_cast<const float4*>(bp + 4 * q);
-          bf[t][4 * q] = v.x; bf[t][4 * q + 1] = v.y; bf[t][4 * q + 2] = v.z; bf[t][4 * q + 3] = v.w;
-        }
-      }
-#pragma unroll
-      for (int i = 0; i < 16; ++i)
-#pragma unroll
-        for (int t = 0; t < 2; ++t) acc[t] = __builtin_amdgcn_mfma_f32_32x32x2f32(af[i], bf[t][i], acc[t], 0, 0, 0);
-      advance(4);
-    }
-    __syncthreads();
   }
-  // partial tiles of the four wavefronts, summed in wavefront order
-  float* stg = smem + wave * BM * SP;
+  // partial tiles -> LDS, rows 8(j/4) + 4h + j%4, columns 2c + u
+  float* my = slot + wave * 32 * kGwLd;
 #pragma unroll
-  for (int t = 0; t < 2; ++t)
+  for (int u = 0; u < 2; ++u)
 #pragma unroll
-    for (int j = 0; j < 16; ++j) stg[(8 * (j >> 2) + 4 * h + (j & 3)) * SP + 32 * t + (lane & 31)] = acc[t][j];
+    for (int j = 0; j < 16; ++j) my[(8 * (j >> 2) + 4 * h + (j & 3)) * kGwLd + 2 * c + u] = acc[u][j];
   __syncthreads();
+  // wave-ordered sum of each tile's WK partials, epilogue with row-contiguous
+  // 4-column pieces: 32 rows x 16 pieces per tile
   const bool cvec = gemm_cvec(P);
-  // 32 rows x 16 float4 columns = 512 float4; thread -> 2 of them
+  for (int q = tid; q < TPB * 32 * 16; q += 512) {
+    const int t = q / (32 * 16), rr = (q / 16) % 32, cl = 4 * (q % 16);
+    const float* base = slot + (t * WK) * 32 * kGwLd + rr * kGwLd + cl;
+    float4 sum = *reinterpret_cast<const float4*>(base);
 #pragma unroll
-  for (int q = 0; q < 2; ++q) {
-    const int idx = tid + 256 * q, lr = idx >> 4, cl = 4 * (idx & 15);
-    float4 sum = make_float4(0.f, 0.f, 0.f, 0.f);
-#pragma unroll
-    for (int w = 0; w < 4; ++w) {
-      const float4 v = *reinterpret_cast<const float4*>(smem + w * BM * SP + lr * SP + cl);
+    for (int p = 1; p < WK; ++p) {
+      const float4 v = *reinterpret_cast<const float4*>(base + p * 32 * kGwLd);
       sum.x += v.x; sum.y += v.y; sum.z += v.z; sum.w += v.w;
     }
-    gemm_store4(P, r0 + lr, c0 + cl, sum, cvec);
+    gemm_store4(P, (blockIdx.x * TPB + t) * 32 + rr, n0 + cl, sum, cvec);
   }
 }
 
@@ -720,17 +741,31 @@ int gemm_launch(const GemmBatch& b, hipStream_t st, const char* tag) {
     gy = std::max<int>(gy, (int)cdiv(b.p[i].N, BN));
   }
   if (gx == 0 || gy == 0) return CHGNET_OK;
-  int maxM = 0, maxK = 0;
+  int maxM = 0, maxN = 0;
   for (int i = 0; i < b.n; ++i) {
     maxM = std::max(maxM, b.p[i].M);
-    int k = 0;
-    for (int s = 0; s < b.p[i].nseg; ++s) k += b.p[i].seg[s].K;
-    maxK = std::max(maxK, k);
+    maxN = std::max(maxN, b.p[i].N);
   }
-  if (maxM <= 32768 && maxK >= 128) {
-    // few row tiles and a long K: split K across the block's wavefronts
-    const dim3 grid((unsigned)cdiv(maxM, 32), gy, b.n);
-    KLAUNCH(st, tag, k_gemm_ks<<<grid, 256, 0, st>>>(b));
+  if (maxM <= 32768) {
+    // few row tiles: direct-load wave tiles, k split over 1-8 wavefronts so
+    // that the launch has about 2048 of them
+    int64_t tiles = 0;
+    int maxg = 0;
+    for (int i = 0; i < b.n; ++i) {
+      tiles += cdiv(b.p[i].M, 32) * cdiv(b.p[i].N, 64);
+      int g = 0;
+      for (int s = 0; s < b.p[i].nseg; ++s) g += (int)cdiv(b.p[i].seg[s].K, 8);
+      maxg = std::max(maxg, g);
+    }
+    int wk = 1;
+    while (wk < kGwWaves && tiles * wk < 2048 && 2 * wk * 2 <= maxg) wk *= 2;
+    const unsigned gyw = (unsigned)cdiv(maxN, 64);
+    const unsigned gxw = (unsigned)cdiv(maxM, 32 * (kGwWaves / wk));
+    const dim3 grid(gxw, gyw, b.n);
+    if (wk == 1) KLAUNCH(st, tag, k_gemm_w<1><<<grid, 512, 0, st>>>(b));
+    else if (wk == 2) KLAUNCH(st, tag, k_gemm_w<2><<<grid, 512, 0, st>>>(b));
+    else if (wk == 4) KLAUNCH(st, tag, k_gemm_w<4><<<grid, 512, 0, st>>>(b));
+    else KLAUNCH(st, tag, k_gemm_w<8><<<grid, 512, 0, st>>>(b));
     return CHGNET_OK;
   }
   // persistent row tiles: about 2048 blocks over the launch

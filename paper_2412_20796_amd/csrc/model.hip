@@ -361,12 +361,12 @@ __global__ void __launch_bounds__(256) k_gate_fwd(GateFwdJobs J) {
 
 // Forward gate with its own pre-activation product (d = 64): z = x W + b
 // (+ the gathered terms) is formed tile by tile in LDS and never round-trips
-// through HBM. A block walks 64-row tiles of all jobs (persistent, stride =
-// grid). Wave w keeps the fp32 MFMA B fragments of output columns
-// [32w, 32w + 32) of W (64 x 128: core | gate) in registers; the x tile is
-// staged in LDS; each wave forms its 64 x 32 slice of z with 32x32x2 MFMAs
-// (lane half h supplies k = 16h + i in step i of each 32-wide k block) and
-// writes it to the z tile; the row-layout gate then reads z from LDS.
+// through HBM. Producer wave w keeps the fp32 MFMA B fragments of output
+// columns [32w, 32w + 32) of W (64 x 128: core | gate) in registers; the x
+// tile is staged in LDS; each producer forms its 64 x 32 slice of z with
+// 32x32x2 MFMAs (lane half h supplies k = 16h + i in step i of each 32-wide
+// k block) and writes it to the z tile; the consumers' row-layout gate then
+// reads z from LDS.
 typedef float v16f __attribute__((ext_vector_type(16)));
 
 struct GateMmJob {
@@ -394,12 +394,38 @@ constexpr int kMmZld = 128 + 4;
 
 constexpr int kMmCpl = 8;
 
+// Gathered operands of one gate row (the atom/bond terms of the split first
+// layer and the multiplier row), loaded one tile ahead of their use; the
+// row indices are loaded one tile ahead of that.
+struct GateRowIn {
+  float ac[3][kMmCpl], ag[3][kMmCpl], mv[kMmCpl];
+};
+
+__device__ __forceinline__ void gate_mm_index(const GateMmJob& J, int row, int (&ix)[4]) {
+  const int r = min(row, J.rows - 1);
+#pragma unroll
+  for (int q = 0; q < 3; ++q) ix[q] = q < J.ad.n ? J.ad.idx[q][r] : 0;
+  ix[3] = J.mode == FWD_BOND ? J.mul_idx[r] : r;
+}
+
+__device__ __forceinline__ void gate_mm_gather(const GateMmJob& J, const int (&ix)[4], GateRowIn& in) {
+  constexpr int D = 64, CPL = kMmCpl;
+  const int j = (threadIdx.x & 63) % Lanes<D, CPL>::LPR;
+#pragma unroll
+  for (int q = 0; q < 3; ++q) {
+    if (q >= J.ad.n) break;
+    const float* r = J.ad.p[q] + (int64_t)ix[q] * J.ad.ld[q];
+    load_cols<D, CPL>(r, j, in.ac[q]);
+    load_cols<D, CPL>(r + D, j, in.ag[q]);
+  }
+  load_cols<D, CPL>(J.mulv + (int64_t)ix[3] * D, j, in.mv);
+}
+
 template <int MODE>
-__device__ __forceinline__ void gate_mm_row(const GateMmJob& J, int r0, int lr, const float* Zs) {
+__device__ __forceinline__ void gate_mm_row(const GateMmJob& J, int row, int lr, const float* Zs, const GateRowIn& in) {
   constexpr int D = 64, CPL = kMmCpl;
   using L = Lanes<D, CPL>;
   const int j = (threadIdx.x & 63) % L::LPR;
-  const int row = r0 + lr;
   if (row >= J.rows) return;
   float zc[CPL], zg[CPL], rc, rg;
   load_cols<D, CPL>(Zs + lr * kMmZld, j, zc);
@@ -411,42 +437,49 @@ __device__ __forceinline__ void gate_mm_row(const GateMmJob& J, int r0, int lr, 
 #pragma unroll
   for (int q = 0; q < 3; ++q) {
     if (q >= J.ad.n) break;
-    const float* r = J.ad.p[q] + (int64_t)J.ad.idx[q][row] * J.ad.ld[q];
-    float uc[CPL], ug[CPL];
-    load_cols<D, CPL>(r, j, uc);
-    load_cols<D, CPL>(r + D, j, ug);
 #pragma unroll
     for (int k = 0; k < CPL; ++k) {
-      zc[k] += uc[k];
-      zg[k] += ug[k];
+      zc[k] += in.ac[q][k];
+      zg[k] += in.ag[q][k];
     }
   }
   ln_stats<D, CPL>(zc, zg, rc, rg);
-  float mv[CPL], o[CPL];
-  const int64_t mrow = MODE == FWD_BOND ? J.mul_idx[row] : row;
-  load_cols<D, CPL>(J.mulv + mrow * D, j, mv);
+  float o[CPL];
 #pragma unroll
   for (int k = 0; k < CPL; ++k) {
     const int c = L::col(j, k);
     const float yc = J.ln.gc[c] * zc[k] + J.ln.bc[c];
     const float yg = J.ln.gg[c] * zg[k] + J.ln.bg[c];
     const float phi = yc * sigm(yc) * sigm(yg);
-    o[k] = MODE == FWD_ANGLE ? mv[k] + phi : mv[k] * phi;
+    o[k] = MODE == FWD_ANGLE ? in.mv[k] + phi : in.mv[k] * phi;
   }
   store_cols<D, CPL>(J.out + (int64_t)row * D, j, o);
 }
 
-__global__ void __launch_bounds__(256, 3) k_gate_fwd_mm(GateMmJobs J) {
-  __shared__ __attribute__((aligned(16))) float Xs[kMmRows * kMmXld];
-  __shared__ __attribute__((aligned(16))) float Zs[kMmRows * kMmZld];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, h = lane >> 5, l32 = lane & 31;
-  // x tile loads: thread -> row tid / 4, 16 columns at 16 (tid % 4)
-  const int xr = tid >> 2, xc = 16 * (tid & 3);
+// Producer and consumer wavefronts: waves 0-3 form z of tile i (x tile and
+// z tile double-buffered in LDS) while waves 4-11 run the gate rows of tile
+// i-1 and gather the operands of tile i; one block barrier per tile hands
+// the buffers over. One block per
+// compute unit, walking tiles blockIdx.x, blockIdx.x + gridDim.x, ...
+constexpr int kMmProducers = 4, kMmConsumers = 8;
+constexpr int kMmThreads = 64 * (kMmProducers + kMmConsumers);
+
+__global__ void __launch_bounds__(kMmThreads, 1) k_gate_fwd_mm(GateMmJobs J) {
+  __shared__ __attribute__((aligned(16))) float Xs[2][kMmRows * kMmXld];
+  __shared__ __attribute__((aligned(16))) float Zs[2][kMmRows * kMmZld];
+  const int tid = threadIdx.x, lane = tid & 63, h = lane >> 5, l32 = lane & 31;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const bool producer = wave < kMmProducers;
   auto job_of = [&](int tile) {
     int k = 0;
     while (k + 1 < J.n && tile >= J.j[k + 1].tile0) ++k;
     return k;
   };
+  const int nt = (int)blockIdx.x < J.ntiles ? (J.ntiles - 1 - (int)blockIdx.x) / (int)gridDim.x + 1 : 0;
+  if (nt == 0) return;
+  auto tile_of = [&](int i) { return (int)blockIdx.x + i * (int)gridDim.x; };
+  // producers: x tile loads, thread -> row tid / 4, 16 columns at 16 (tid % 4)
+  const int xr = tid >> 2, xc = 16 * (tid & 3);
   auto fetch_x = [&](int tile, float4 (&v)[4]) {
     const GateMmJob& jb = J.j[job_of(tile)];
     const int row = (tile - jb.tile0) * kMmRows + xr;
@@ -458,61 +491,109 @@ __global__ void __launch_bounds__(256, 3) k_gate_fwd_mm(GateMmJobs J) {
       for (int q = 0; q < 4; ++q) v[q] = *reinterpret_cast<const float4*>(p + 4 * q);
     }
   };
-  int tile = blockIdx.x;
-  if (tile >= J.ntiles) return;
-  float4 xv[4];
-  fetch_x(tile, xv);
-  int cur = -1;
-  float bfr[2][16], bias = 0.f;
-  while (tile < J.ntiles) {
-    const int k = job_of(tile);
-    const GateMmJob& jb = J.j[k];
-    if (k != cur) {
-      cur = k;
-      const int col = 32 * wave + l32;
+  auto store_x = [&](float* X, const float4 (&v)[4]) {
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) bfr[kb][i] = jb.W[(int64_t)(32 * kb + 16 * h + i) * jb.ldw + col];
-      bias = jb.bias[col];
-    }
-#pragma unroll
-    for (int q = 0; q < 4; ++q) *reinterpret_cast<float4*>(&Xs[xr * kMmXld + xc + 4 * q]) = xv[q];
+    for (int q = 0; q < 4; ++q) *reinterpret_cast<float4*>(&X[xr * kMmXld + xc + 4 * q]) = v[q];
+  };
+  // Producers and consumers run separate loops with the same number of block
+  // barriers (nt + 1 after the prologue), so each keeps only its own state.
+  if (producer) {
+    float4 xv[4];
+    int cur = -1;
+    float bfr[2][16], bias = 0.f;
+    fetch_x(tile_of(0), xv);
+    store_x(Xs[0], xv);
+    if (nt > 1) fetch_x(tile_of(1), xv);
     __syncthreads();
-    const int next = tile + gridDim.x;
-    if (next < J.ntiles) fetch_x(next, xv);
+    for (int i = 0; i <= nt; ++i) {
+      if (i < nt) {
+        const int tile = tile_of(i);
+        const int k = job_of(tile);
+        const GateMmJob& jb = J.j[k];
+        if (k != cur) {
+          cur = k;
+          const int col = 32 * wave + l32;
 #pragma unroll
-    for (int s = 0; s < kMmRows / 32; ++s) {
-      v16f acc;
+          for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) acc[e] = 0.f;
+            for (int e = 0; e < 16; ++e) bfr[kb][e] = jb.W[(int64_t)(32 * kb + 16 * h + e) * jb.ldw + col];
+          bias = jb.bias[col];
+        }
+        if (i + 1 < nt) {
+          store_x(Xs[(i + 1) & 1], xv);
+          if (i + 2 < nt) fetch_x(tile_of(i + 2), xv);
+        }
+        const float* X = Xs[i & 1];
+        float* Z = Zs[i & 1];
+        // the two 32-row subtiles are independent accumulation chains
+        v16f acc[kMmRows / 32];
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
-        float af[16];
-        const float* ap = &Xs[(32 * s + l32) * kMmXld + 32 * kb + 16 * h];
+        for (int s = 0; s < kMmRows / 32; ++s)
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const float4 v = *reinterpret_cast<const float4*>(ap + 4 * q);
-          af[4 * q] = v.x; af[4 * q + 1] = v.y; af[4 * q + 2] = v.z; af[4 * q + 3] = v.w;
+          for (int e = 0; e < 16; ++e) acc[s][e] = 0.f;
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb) {
+          float af[kMmRows / 32][16];
+#pragma unroll
+          for (int s = 0; s < kMmRows / 32; ++s) {
+            const float* ap = &X[(32 * s + l32) * kMmXld + 32 * kb + 16 * h];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+              const float4 v = *reinterpret_cast<const float4*>(ap + 4 * q);
+              af[s][4 * q] = v.x; af[s][4 * q + 1] = v.y; af[s][4 * q + 2] = v.z; af[s][4 * q + 3] = v.w;
+            }
+          }
+#pragma unroll
+          for (int e = 0; e < 16; ++e)
+#pragma unroll
+            for (int s = 0; s < kMmRows / 32; ++s)
+              acc[s] = __builtin_amdgcn_mfma_f32_32x32x2f32(af[s][e], bfr[kb][e], acc[s], 0, 0, 0);
         }
 #pragma unroll
-        for (int i = 0; i < 16; ++i) acc = __builtin_amdgcn_mfma_f32_32x32x2f32(af[i], bfr[kb][i], acc, 0, 0, 0);
-      }
+        for (int s = 0; s < kMmRows / 32; ++s)
 #pragma unroll
-      for (int e = 0; e < 16; ++e)
-        Zs[(32 * s + 8 * (e >> 2) + 4 * h + (e & 3)) * kMmZld + 32 * wave + l32] = acc[e] + bias;
+          for (int e = 0; e < 16; ++e)
+            Z[(32 * s + 8 * (e >> 2) + 4 * h + (e & 3)) * kMmZld + 32 * wave + l32] = acc[s][e] + bias;
+      }
+      __syncthreads();
+    }
+  } else {
+    // lane row within the tile; gathered operands of the next tile and row
+    // indices of the one after
+    using GL = Lanes<64, kMmCpl>;
+    static_assert(kMmConsumers * GL::RPW == kMmRows, "one consumer pass per tile");
+    const int lr = (wave - kMmProducers) * GL::RPW + lane / GL::LPR;
+    auto row_of = [&](int tile, const GateMmJob& jb) { return (tile - jb.tile0) * kMmRows + lr; };
+    GateRowIn in;
+    int ix[4];
+    const GateMmJob& j0 = J.j[job_of(tile_of(0))];
+    gate_mm_index(j0, row_of(tile_of(0), j0), ix);
+    gate_mm_gather(j0, ix, in);
+    if (nt > 1) {
+      const GateMmJob& j1 = J.j[job_of(tile_of(1))];
+      gate_mm_index(j1, row_of(tile_of(1), j1), ix);
     }
     __syncthreads();
-    const int r0 = (tile - jb.tile0) * kMmRows;
-    using GL = Lanes<64, kMmCpl>;
-#pragma unroll 1
-    for (int pass = 0; pass < kMmRows / (4 * GL::RPW); ++pass) {
-      const int lr = (pass * 4 + wave) * GL::RPW + lane / GL::LPR;
-      if (jb.mode == FWD_ATOM) gate_mm_row<FWD_ATOM>(jb, r0, lr, Zs);
-      else if (jb.mode == FWD_BOND) gate_mm_row<FWD_BOND>(jb, r0, lr, Zs);
-      else gate_mm_row<FWD_ANGLE>(jb, r0, lr, Zs);
+    for (int i = 0; i <= nt; ++i) {
+      if (i > 0) {
+        const int tile = tile_of(i - 1);
+        const GateMmJob& jb = J.j[job_of(tile)];
+        const int row = row_of(tile, jb);
+        const float* Z = Zs[(i - 1) & 1];
+        if (jb.mode == FWD_ATOM) gate_mm_row<FWD_ATOM>(jb, row, lr, Z, in);
+        else if (jb.mode == FWD_BOND) gate_mm_row<FWD_BOND>(jb, row, lr, Z, in);
+        else gate_mm_row<FWD_ANGLE>(jb, row, lr, Z, in);
+        if (i < nt) {
+          const GateMmJob& jn = J.j[job_of(tile_of(i))];
+          gate_mm_gather(jn, ix, in);
+          if (i + 1 < nt) {
+            const GateMmJob& jm = J.j[job_of(tile_of(i + 1))];
+            gate_mm_index(jm, row_of(tile_of(i + 1), jm), ix);
+          }
+        }
+      }
+      __syncthreads();
     }
-    tile = next;
   }
 }
 
@@ -1254,7 +1335,7 @@ int gate_fwd_launch(int D, GateFwdJobs J, hipStream_t st) {
 }
 
 // Launch the fused (d = 64) forward gates of one layer: a persistent grid of
-// at most three blocks per compute unit, tiles spread evenly over blocks.
+// one block per compute unit.
 int gate_fwd_mm_launch(GateMmJobs J, hipStream_t st) {
   GateMmJobs K{};
   int tiles = 0;
@@ -1267,10 +1348,8 @@ int gate_fwd_mm_launch(GateMmJobs J, hipStream_t st) {
   }
   K.ntiles = tiles;
   if (tiles == 0) return CHGNET_OK;
-  constexpr int kMaxBlocks = 3 * 256;
-  const int per = (int)cdiv(tiles, kMaxBlocks);
-  const int grid = (int)cdiv(tiles, per);
-  KLAUNCH(st, "k_gate_fwd", k_gate_fwd_mm<<<grid, 256, 0, st>>>(K));
+  const int grid = std::min(tiles, 256);
+  KLAUNCH(st, "k_gate_fwd", k_gate_fwd_mm<<<grid, kMmThreads, 0, st>>>(K));
   return CHGNET_OK;
 }
 
