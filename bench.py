@@ -162,11 +162,19 @@ def algorithmic_cost(tag, z):
         return "mfma", T * (N * 16 * D * D + B * 8 * D * D) - N * 4 * D * D - B * 4 * D * D
     if tag == "gemm_bond_bwd":
         return "mfma", Tang * B * 16 * D * D + B * 8 * D * D
+    if tag == "k_gate_fwd" and D == 64:
+        # pre-activations formed in the kernel (d = 64): per edge x (d) and
+        # e^a (d) in, z kept for the backward (2d) and message (d) out; per
+        # angle and gate x (d) in, z (2d) and output (d) out, the angle gate
+        # also reads a (d). Tables: per-atom terms N x 8d (6d last layer),
+        # per-bond terms B x 8d (4d), e^b B x d.
+        lay = E * 5 * D + A * 9 * D + N * 8 * D + B * 9 * D
+        last = E * 5 * D + A * 4 * D + N * 6 * D + B * 5 * D
+        return "hbm", f * (Tang * lay + last)
     if tag == "k_gate_fwd":
-        # per edge: z (2d) + e^a (d) in, message (d) out; per angle: bond gate
-        # z (2d) in, message (d) out; angle gate z (2d) + a (d) in, a' (d)
-        # out. Tables: per-atom terms N x 8d (6d last layer), per-bond terms
-        # B x 8d (4d), e^b B x d.
+        # z from the product kernel: per edge z (2d) + e^a (d) in, message (d)
+        # out; per angle: bond gate z (2d) in, message (d) out; angle gate z
+        # (2d) + a (d) in, a' (d) out. Tables as above.
         lay = E * 4 * D + A * 7 * D + N * 8 * D + B * 9 * D
         last = E * 4 * D + A * 3 * D + N * 6 * D + B * 5 * D
         return "hbm", f * (Tang * lay + last)
@@ -188,7 +196,7 @@ TAG_SYMBOL = {
     "gemm_z": "k_gemm<64, 1>",
     "gemm_in_bwd": "k_gemm<64, 2>",
     "tn_in": "k_tn<1>",
-    "k_gate_fwd": "k_gate_fwd<64>",
+    "k_gate_fwd": "k_gate_fwd_mm",
     "k_gate_bwd": "k_gate_bwd<64>",
 }
 

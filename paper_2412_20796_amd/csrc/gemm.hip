@@ -741,14 +741,18 @@ int gemm_launch(const GemmBatch& b, hipStream_t st, const char* tag) {
     gy = std::max<int>(gy, (int)cdiv(b.p[i].N, BN));
   }
   if (gx == 0 || gy == 0) return CHGNET_OK;
-  int maxM = 0, maxN = 0;
+  int maxM = 0, maxN = 0, maxK = 0;
   for (int i = 0; i < b.n; ++i) {
     maxM = std::max(maxM, b.p[i].M);
     maxN = std::max(maxN, b.p[i].N);
+    int k = 0;
+    for (int s = 0; s < b.p[i].nseg; ++s) k += b.p[i].seg[s].K;
+    maxK = std::max(maxK, k);
   }
-  if (maxM <= 32768) {
-    // few row tiles: direct-load wave tiles, k split over 1-8 wavefronts so
-    // that the launch has about 2048 of them
+  if (maxM <= 32768 && (maxK >= 128 || maxM <= 4096)) {
+    // few row tiles and a long k, or very few rows: direct-load wave tiles,
+    // k split over 1-8 wavefronts so that the launch has about 2048 of them
+    // (with k = 64 and ~10^4 rows the LDS-staged tiles below measured faster)
     int64_t tiles = 0;
     int maxg = 0;
     for (int i = 0; i < b.n; ++i) {

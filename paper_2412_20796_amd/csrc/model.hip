@@ -270,12 +270,15 @@ struct LnPtrs {
 };
 
 // Gathered terms of the split first linear layer: z = z_pre + sum_q
-// add[q][idx_q[row]] (each a 2d-wide core | gate row).
+// add[q][idx_q[row]] (each a 2d-wide core | gate row), at most two (atom
+// conv: source and destination atom; angle gates: first bond with its centre
+// atom folded in, and second bond).
+constexpr int kMaxAdds = 2;
 struct GateAdds {
   int n;
-  const float* p[3];
-  int ld[3];
-  const int* idx[3];
+  const float* p[kMaxAdds];
+  int ld[kMaxAdds];
+  const int* idx[kMaxAdds];
 };
 
 template <int D, int CPL>
@@ -284,7 +287,7 @@ __device__ __forceinline__ void load_z(const float* __restrict__ z, int ldz, con
   load_cols<D, CPL>(z + (int64_t)row * ldz, j, zc);
   load_cols<D, CPL>(z + (int64_t)row * ldz + D, j, zg);
 #pragma unroll
-  for (int q = 0; q < 3; ++q) {
+  for (int q = 0; q < kMaxAdds; ++q) {
     if (q >= ad.n) break;
     const float* r = ad.p[q] + (int64_t)ad.idx[q][row] * ad.ld[q];
     float uc[CPL], ug[CPL];
@@ -398,27 +401,27 @@ constexpr int kMmCpl = 8;
 // layer and the multiplier row), loaded one tile ahead of their use; the
 // row indices are loaded one tile ahead of that.
 struct GateRowIn {
-  float ac[3][kMmCpl], ag[3][kMmCpl], mv[kMmCpl];
+  float ac[kMaxAdds][kMmCpl], ag[kMaxAdds][kMmCpl], mv[kMmCpl];
 };
 
-__device__ __forceinline__ void gate_mm_index(const GateMmJob& J, int row, int (&ix)[4]) {
+__device__ __forceinline__ void gate_mm_index(const GateMmJob& J, int row, int (&ix)[kMaxAdds + 1]) {
   const int r = min(row, J.rows - 1);
 #pragma unroll
-  for (int q = 0; q < 3; ++q) ix[q] = q < J.ad.n ? J.ad.idx[q][r] : 0;
-  ix[3] = J.mode == FWD_BOND ? J.mul_idx[r] : r;
+  for (int q = 0; q < kMaxAdds; ++q) ix[q] = q < J.ad.n ? J.ad.idx[q][r] : 0;
+  ix[kMaxAdds] = J.mode == FWD_BOND ? J.mul_idx[r] : r;
 }
 
-__device__ __forceinline__ void gate_mm_gather(const GateMmJob& J, const int (&ix)[4], GateRowIn& in) {
+__device__ __forceinline__ void gate_mm_gather(const GateMmJob& J, const int (&ix)[kMaxAdds + 1], GateRowIn& in) {
   constexpr int D = 64, CPL = kMmCpl;
   const int j = (threadIdx.x & 63) % Lanes<D, CPL>::LPR;
 #pragma unroll
-  for (int q = 0; q < 3; ++q) {
+  for (int q = 0; q < kMaxAdds; ++q) {
     if (q >= J.ad.n) break;
     const float* r = J.ad.p[q] + (int64_t)ix[q] * J.ad.ld[q];
     load_cols<D, CPL>(r, j, in.ac[q]);
     load_cols<D, CPL>(r + D, j, in.ag[q]);
   }
-  load_cols<D, CPL>(J.mulv + (int64_t)ix[3] * D, j, in.mv);
+  load_cols<D, CPL>(J.mulv + (int64_t)ix[kMaxAdds] * D, j, in.mv);
 }
 
 template <int MODE>
@@ -435,7 +438,7 @@ __device__ __forceinline__ void gate_mm_row(const GateMmJob& J, int row, int lr,
     store_cols<D, CPL>(J.zsave + (int64_t)row * J.ldzs + D, j, zg);
   }
 #pragma unroll
-  for (int q = 0; q < 3; ++q) {
+  for (int q = 0; q < kMaxAdds; ++q) {
     if (q >= J.ad.n) break;
 #pragma unroll
     for (int k = 0; k < CPL; ++k) {
@@ -459,17 +462,79 @@ __device__ __forceinline__ void gate_mm_row(const GateMmJob& J, int row, int lr,
 // Producer and consumer wavefronts: waves 0-3 form z of tile i (x tile and
 // z tile double-buffered in LDS) while waves 4-11 run the gate rows of tile
 // i-1 and gather the operands of tile i; one block barrier per tile hands
-// the buffers over. One block per
-// compute unit, walking tiles blockIdx.x, blockIdx.x + gridDim.x, ...
+// the buffers over. Producers and consumers run separate loops with the same
+// number of block barriers, so each keeps only its own state.
 constexpr int kMmProducers = 4, kMmConsumers = 8;
 constexpr int kMmThreads = 64 * (kMmProducers + kMmConsumers);
 
+// Producer pieces (threads 0-255). x tile loads: thread -> row tid / 4, 16
+// columns at 16 (tid % 4); rows past `rows` read as zero.
+__device__ __forceinline__ void mm_fetch_x(const float* __restrict__ x, int rows, int row0, float4 (&v)[4]) {
+  const int tid = threadIdx.x, row = row0 + (tid >> 2), xc = 16 * (tid & 3);
+#pragma unroll
+  for (int q = 0; q < 4; ++q) v[q] = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (row < rows) {
+    const float* p = x + (int64_t)row * 64 + xc;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) v[q] = *reinterpret_cast<const float4*>(p + 4 * q);
+  }
+}
+__device__ __forceinline__ void mm_store_x(float* X, const float4 (&v)[4]) {
+  const int tid = threadIdx.x, xr = tid >> 2, xc = 16 * (tid & 3);
+#pragma unroll
+  for (int q = 0; q < 4; ++q) *reinterpret_cast<float4*>(&X[xr * kMmXld + xc + 4 * q]) = v[q];
+}
+// B fragments of W columns [32 wave, 32 wave + 32) and their bias
+__device__ __forceinline__ void mm_load_w(const float* __restrict__ W, int ldw, const float* __restrict__ b, int wave,
+                                          float (&bfr)[2][16], float& bias) {
+  const int lane = threadIdx.x & 63, h = lane >> 5, col = 32 * wave + (lane & 31);
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) bfr[kb][e] = W[(int64_t)(32 * kb + 16 * h + e) * ldw + col];
+  bias = b[col];
+}
+// z slice (64 rows x 32 columns) of one producer wave, X -> Z
+__device__ __forceinline__ void mm_tile(const float* X, float* Z, const float (&bfr)[2][16], float bias, int wave) {
+  const int lane = threadIdx.x & 63, h = lane >> 5, l32 = lane & 31;
+  // the two 32-row subtiles are independent accumulation chains
+  v16f acc[kMmRows / 32];
+#pragma unroll
+  for (int s = 0; s < kMmRows / 32; ++s)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) acc[s][e] = 0.f;
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb) {
+    float af[kMmRows / 32][16];
+#pragma unroll
+    for (int s = 0; s < kMmRows / 32; ++s) {
+      const float* ap = &X[(32 * s + l32) * kMmXld + 32 * kb + 16 * h];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const float4 v = *reinterpret_cast<const float4*>(ap + 4 * q);
+        af[s][4 * q] = v.x; af[s][4 * q + 1] = v.y; af[s][4 * q + 2] = v.z; af[s][4 * q + 3] = v.w;
+      }
+    }
+#pragma unroll
+    for (int e = 0; e < 16; ++e)
+#pragma unroll
+      for (int s = 0; s < kMmRows / 32; ++s)
+        acc[s] = __builtin_amdgcn_mfma_f32_32x32x2f32(af[s][e], bfr[kb][e], acc[s], 0, 0, 0);
+  }
+#pragma unroll
+  for (int s = 0; s < kMmRows / 32; ++s)
+#pragma unroll
+    for (int e = 0; e < 16; ++e)
+      Z[(32 * s + 8 * (e >> 2) + 4 * h + (e & 3)) * kMmZld + 32 * wave + l32] = acc[s][e] + bias;
+}
+
+// One block per compute unit, walking tiles blockIdx.x, blockIdx.x +
+// gridDim.x, ... of the concatenated jobs.
 __global__ void __launch_bounds__(kMmThreads, 1) k_gate_fwd_mm(GateMmJobs J) {
   __shared__ __attribute__((aligned(16))) float Xs[2][kMmRows * kMmXld];
   __shared__ __attribute__((aligned(16))) float Zs[2][kMmRows * kMmZld];
-  const int tid = threadIdx.x, lane = tid & 63, h = lane >> 5, l32 = lane & 31;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const bool producer = wave < kMmProducers;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   auto job_of = [&](int tile) {
     int k = 0;
     while (k + 1 < J.n && tile >= J.j[k + 1].tile0) ++k;
@@ -478,82 +543,30 @@ __global__ void __launch_bounds__(kMmThreads, 1) k_gate_fwd_mm(GateMmJobs J) {
   const int nt = (int)blockIdx.x < J.ntiles ? (J.ntiles - 1 - (int)blockIdx.x) / (int)gridDim.x + 1 : 0;
   if (nt == 0) return;
   auto tile_of = [&](int i) { return (int)blockIdx.x + i * (int)gridDim.x; };
-  // producers: x tile loads, thread -> row tid / 4, 16 columns at 16 (tid % 4)
-  const int xr = tid >> 2, xc = 16 * (tid & 3);
   auto fetch_x = [&](int tile, float4 (&v)[4]) {
     const GateMmJob& jb = J.j[job_of(tile)];
-    const int row = (tile - jb.tile0) * kMmRows + xr;
-#pragma unroll
-    for (int q = 0; q < 4; ++q) v[q] = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (row < jb.rows) {
-      const float* p = jb.x + (int64_t)row * 64 + xc;
-#pragma unroll
-      for (int q = 0; q < 4; ++q) v[q] = *reinterpret_cast<const float4*>(p + 4 * q);
-    }
+    mm_fetch_x(jb.x, jb.rows, (tile - jb.tile0) * kMmRows, v);
   };
-  auto store_x = [&](float* X, const float4 (&v)[4]) {
-#pragma unroll
-    for (int q = 0; q < 4; ++q) *reinterpret_cast<float4*>(&X[xr * kMmXld + xc + 4 * q]) = v[q];
-  };
-  // Producers and consumers run separate loops with the same number of block
-  // barriers (nt + 1 after the prologue), so each keeps only its own state.
-  if (producer) {
+  if (wave < kMmProducers) {
     float4 xv[4];
     int cur = -1;
     float bfr[2][16], bias = 0.f;
     fetch_x(tile_of(0), xv);
-    store_x(Xs[0], xv);
+    mm_store_x(Xs[0], xv);
     if (nt > 1) fetch_x(tile_of(1), xv);
     __syncthreads();
     for (int i = 0; i <= nt; ++i) {
       if (i < nt) {
-        const int tile = tile_of(i);
-        const int k = job_of(tile);
-        const GateMmJob& jb = J.j[k];
+        const int k = job_of(tile_of(i));
         if (k != cur) {
           cur = k;
-          const int col = 32 * wave + l32;
-#pragma unroll
-          for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-            for (int e = 0; e < 16; ++e) bfr[kb][e] = jb.W[(int64_t)(32 * kb + 16 * h + e) * jb.ldw + col];
-          bias = jb.bias[col];
+          mm_load_w(J.j[k].W, J.j[k].ldw, J.j[k].bias, wave, bfr, bias);
         }
         if (i + 1 < nt) {
-          store_x(Xs[(i + 1) & 1], xv);
+          mm_store_x(Xs[(i + 1) & 1], xv);
           if (i + 2 < nt) fetch_x(tile_of(i + 2), xv);
         }
-        const float* X = Xs[i & 1];
-        float* Z = Zs[i & 1];
-        // the two 32-row subtiles are independent accumulation chains
-        v16f acc[kMmRows / 32];
-#pragma unroll
-        for (int s = 0; s < kMmRows / 32; ++s)
-#pragma unroll
-          for (int e = 0; e < 16; ++e) acc[s][e] = 0.f;
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb) {
-          float af[kMmRows / 32][16];
-#pragma unroll
-          for (int s = 0; s < kMmRows / 32; ++s) {
-            const float* ap = &X[(32 * s + l32) * kMmXld + 32 * kb + 16 * h];
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-              const float4 v = *reinterpret_cast<const float4*>(ap + 4 * q);
-              af[s][4 * q] = v.x; af[s][4 * q + 1] = v.y; af[s][4 * q + 2] = v.z; af[s][4 * q + 3] = v.w;
-            }
-          }
-#pragma unroll
-          for (int e = 0; e < 16; ++e)
-#pragma unroll
-            for (int s = 0; s < kMmRows / 32; ++s)
-              acc[s] = __builtin_amdgcn_mfma_f32_32x32x2f32(af[s][e], bfr[kb][e], acc[s], 0, 0, 0);
-        }
-#pragma unroll
-        for (int s = 0; s < kMmRows / 32; ++s)
-#pragma unroll
-          for (int e = 0; e < 16; ++e)
-            Z[(32 * s + 8 * (e >> 2) + 4 * h + (e & 3)) * kMmZld + 32 * wave + l32] = acc[s][e] + bias;
+        mm_tile(Xs[i & 1], Zs[i & 1], bfr, bias, wave);
       }
       __syncthreads();
     }
@@ -565,7 +578,7 @@ __global__ void __launch_bounds__(kMmThreads, 1) k_gate_fwd_mm(GateMmJobs J) {
     const int lr = (wave - kMmProducers) * GL::RPW + lane / GL::LPR;
     auto row_of = [&](int tile, const GateMmJob& jb) { return (tile - jb.tile0) * kMmRows + lr; };
     GateRowIn in;
-    int ix[4];
+    int ix[kMaxAdds + 1];
     const GateMmJob& j0 = J.j[job_of(tile_of(0))];
     gate_mm_index(j0, row_of(tile_of(0), j0), ix);
     gate_mm_gather(j0, ix, in);
@@ -1429,13 +1442,11 @@ int gate_bwd_launch(int D, GateBwdJobs J, float* const* ln_grad, const Acts& a, 
   return reduce_rows_multi(R, a.red2, a.tickets, st);
 }
 
-GateAdds adds(int n, const float* p0, int ld0, const int* i0, const float* p1, int ld1, const int* i1,
-              const float* p2 = nullptr, int ld2 = 0, const int* i2 = nullptr) {
+GateAdds adds(int n, const float* p0, int ld0, const int* i0, const float* p1, int ld1, const int* i1) {
   GateAdds a{};
   a.n = n;
   a.p[0] = p0; a.ld[0] = ld0; a.idx[0] = i0;
   a.p[1] = p1; a.ld[1] = ld1; a.idx[1] = i1;
-  a.p[2] = p2; a.ld[2] = ld2; a.idx[2] = i2;
   return a;
 }
 
@@ -1544,6 +1555,8 @@ int forward_impl(Ctx& c, const float* Pflat, float* energy, float* forces, float
       seg(p, a.v[t], D, 0, D, W, 2 * D, 0);
       ps.push_back(p);
     }
+    CHG_TRY(run_gemms(ps, st, "gemm_proj"));
+    ps.clear();
     for (int k = 0; k < 4; ++k) {
       if ((k & 1) && !ang) continue;
       // k: 0 bond-conv role b1, 1 angle role b1, 2 bond-conv role b2, 3 angle role b2
@@ -1551,15 +1564,20 @@ int forward_impl(Ctx& c, const float* Pflat, float* energy, float* forces, float
       GemmProblem p = gp(B, 2 * D, a.Xb[t] + k * 2 * D, 8 * D);
       p.a_rows = g.bond_edge;
       seg(p, a.e[t], D, 0, D, W, 2 * D, 0);
+      if (k < 2) {
+        // the centre atom of an angle is the source atom of its first bond:
+        // its term is folded into the first-bond row
+        p.res = a.Xa[t] + (4 + 2 * k) * D;
+        p.res_ld = 8 * D;
+        p.res_rows = a.bond_src;
+      }
       ps.push_back(p);
     }
     CHG_TRY(run_gemms(ps, st, "gemm_proj"));
     ps.clear();
     const GateAdds ad_av = adds(2, a.Xa[t], 8 * D, a.edge_src, a.Xa[t] + 2 * D, 8 * D, g.edge_dst);
-    const GateAdds ad_be = adds(3, a.Xa[t] + 4 * D, 8 * D, a.ang_ctr, a.Xb[t], 8 * D, a.ang_b1, a.Xb[t] + 4 * D, 8 * D,
-                                a.ang_b2);
-    const GateAdds ad_an = adds(3, a.Xa[t] + 6 * D, 8 * D, a.ang_ctr, a.Xb[t] + 2 * D, 8 * D, a.ang_b1,
-                                a.Xb[t] + 6 * D, 8 * D, a.ang_b2);
+    const GateAdds ad_be = adds(2, a.Xb[t], 8 * D, a.ang_b1, a.Xb[t] + 4 * D, 8 * D, a.ang_b2);
+    const GateAdds ad_an = adds(2, a.Xb[t] + 2 * D, 8 * D, a.ang_b1, a.Xb[t] + 6 * D, 8 * D, a.ang_b2);
     const float* Wx_av = Wav + 2 * D * 2 * D;  // rows of e_ij
     const float* Wx_be = Wbe + 3 * D * 2 * D;  // rows of a_ijk
     const float* Wx_an = Wan + 3 * D * 2 * D;
@@ -1794,10 +1812,8 @@ int backward_impl(Ctx& c, const float* Pflat, bool repack, const float* dE, cons
     }
     // angle gates (bond conv, then angle update)
     const GateAdds ad_av = adds(2, a.Xa[t], 8 * D, a.edge_src, a.Xa[t] + 2 * D, 8 * D, g.edge_dst);
-    const GateAdds ad_be = adds(3, a.Xa[t] + 4 * D, 8 * D, a.ang_ctr, a.Xb[t], 8 * D, a.ang_b1, a.Xb[t] + 4 * D, 8 * D,
-                                a.ang_b2);
-    const GateAdds ad_an = adds(3, a.Xa[t] + 6 * D, 8 * D, a.ang_ctr, a.Xb[t] + 2 * D, 8 * D, a.ang_b1,
-                                a.Xb[t] + 6 * D, 8 * D, a.ang_b2);
+    const GateAdds ad_be = adds(2, a.Xb[t], 8 * D, a.ang_b1, a.Xb[t] + 4 * D, 8 * D, a.ang_b2);
+    const GateAdds ad_an = adds(2, a.Xb[t] + 2 * D, 8 * D, a.ang_b1, a.Xb[t] + 6 * D, 8 * D, a.ang_b2);
     {
       GateBwdJobs J{};
       J.j[J.n++] = bwd_job(BWD_BOND, A, a.zae[t], 4 * D, ad_be, ln_ptrs(P, lo.be), a.dmu, a.ang_b1, a.eb, a.ang_b2, a.t2,
