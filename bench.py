@@ -91,17 +91,17 @@ def main():
     torch.cuda.synchronize()
     E, B, A = g.n_edges, g.n_bonds, g.n_angles
 
-    t0 = torch.cuda.Event(enable_timing=True)
-    t1 = torch.cuda.Event(enable_timing=True)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     torch.cuda.synchronize()
     wall0 = time.perf_counter()
-    t0.record()
-    for _ in range(args.steps):
+    ev[0].record()
+    for k in range(args.steps):
         one_step()
-    t1.record()
+        ev[k + 1].record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
-    ms = t0.elapsed_time(t1) / args.steps
+    ms = ev[0].elapsed_time(ev[-1]) / args.steps
+    per_step = np.array([ev[k].elapsed_time(ev[k + 1]) for k in range(args.steps)])
     S = b.n_struct
     value = S / (ms * 1e-3)
 
@@ -122,6 +122,9 @@ def main():
                    "angles": A, "d": d, "layers": T, "parallelism": "single GPU"},
         "edges_per_s": round(E / (ms * 1e-3), 1),
         "angles_per_s": round(A / (ms * 1e-3), 1),
+        "ms_per_step_median": round(float(np.median(per_step)), 4),
+        "ms_per_step_p10_p90": [round(float(np.percentile(per_step, 10)), 4),
+                                round(float(np.percentile(per_step, 90)), 4)],
         "wall_s_timed": round(wall, 3),
         "final_loss": float(loss.cpu()[0]),
     }
@@ -331,8 +334,10 @@ def cpu_baseline(workload, sample, min_seconds=10.0):
     hp = om.HParams(d=d, n_layers=T)
     reps = 0
     t = time.perf_counter()
+    n_edges = 0
     while True:
-        om.step(hp, sb, params.astype(np.float64), tgt)
+        _, _, _, graph = om.step(hp, sb, params.astype(np.float64), tgt)
+        n_edges = len(graph["edge_dst"])
         reps += 1
         dt = time.perf_counter() - t
         if dt >= min_seconds or reps >= 20:
@@ -344,6 +349,7 @@ def cpu_baseline(workload, sample, min_seconds=10.0):
     except Exception:  # pragma: no cover - threadpoolctl is optional
         threads = 1
     return {"value": round(reps * sample / dt, 4), "unit": "structures/s", "cores": threads, "kind": "oracle",
+            "host_cpus": len(os.sched_getaffinity(0)), "edges_per_s": round(reps * n_edges / dt, 1),
             "sample": "%d of the %d structures (%d atoms), %d full step(s) (graph, forward, loss, backward) in %.1f s"
                       % (sample, b.n_struct, n, reps, dt)}
 
