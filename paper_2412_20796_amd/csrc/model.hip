@@ -31,7 +31,7 @@ int validate_batch(const chgnet_batch* b);
 namespace {
 
 constexpr float kLnEps = 1e-5f;
-constexpr int kFreqRowsPerBlock = 256;  // rows per block in frequency-gradient kernel
+constexpr int kFreqRowsPerBlock = 64;  // rows per block in frequency-gradient kernel
 constexpr int kReduceGroups = 32;      // first-level groups of the ordered partial-sum reduction
 constexpr int64_t kTnPartFloats = 64ll << 20;
 
@@ -59,21 +59,33 @@ __global__ void k_fill(float* __restrict__ p, int64_t n, float v) {
   if (i < n) p[i] = v;
 }
 
+constexpr int kPackTensors = 128, kPackChunk = 2048;
 struct PackTable {
   int n;
-  int src[96], dst[96], len[96];
+  int src[kPackTensors], dst[kPackTensors], len[kPackTensors];
+  int chunk0[kPackTensors + 1];  // first chunk of each tensor; chunk0[n] = total
 };
 
-// Copy of the flat parameters with every tensor on a 16-byte boundary.
-__global__ void k_pack_params(PackTable t, const float* __restrict__ src, float* __restrict__ dst) {
-  if ((int)blockIdx.x >= t.n) return;
-  const int s = t.src[blockIdx.x], d = t.dst[blockIdx.x], n = t.len[blockIdx.x];
-  for (int i = threadIdx.x; i < n; i += blockDim.x) dst[d + i] = src[s + i];
+// Copy of the flat parameters with every tensor on a 16-byte boundary; one
+// block per chunk of kPackChunk values of one tensor.
+__global__ void __launch_bounds__(256) k_pack_params(PackTable t, const float* __restrict__ src, float* __restrict__ dst) {
+  const int b = blockIdx.x;
+  int lo = 0, hi = t.n;  // tensor k with chunk0[k] <= b < chunk0[k + 1]
+  while (hi - lo > 1) {
+    const int mid = (lo + hi) / 2;
+    if (t.chunk0[mid] <= b) lo = mid;
+    else hi = mid;
+  }
+  const int base = (b - t.chunk0[lo]) * kPackChunk;
+  const int n = min(kPackChunk, t.len[lo] - base);
+  const float* s = src + t.src[lo] + base;
+  float* d = dst + t.dst[lo] + base;
+  for (int i = threadIdx.x; i < n; i += 256) d[i] = s[i];
 }
 
-__global__ void k_copy(float* __restrict__ dst, const float* __restrict__ src, int64_t n) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < n) dst[i] = src[i];
+// dst = src, n4 float4 values (16-byte aligned arrays), grid-stride
+__global__ void __launch_bounds__(256) k_copy4(float4* __restrict__ dst, const float4* __restrict__ src, int64_t n4) {
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n4; i += (int64_t)gridDim.x * 256) dst[i] = src[i];
 }
 
 // ---------------------------------------------------------------------------
@@ -1050,25 +1062,32 @@ __global__ void __launch_bounds__(256) k_embed_bwd_Z(int N, int D, const int* __
 }
 
 // Partial sums over rows of d sRBF_n * d sRBF_n / d f_n.
+// d(loss)/d f_n of the radial basis: sum over rows of drbf[row, n] times
+// d rbf_n / d f_n. A wavefront pass covers 64 / NP rows x NP basis slots
+// (NP = 32 or 64 >= R); 64 rows per block; per-block sums into part[block].
 __global__ void __launch_bounds__(256) k_rbf_fgrad(int rows, const int* __restrict__ idx, const float* __restrict__ len,
                                                    const float* __restrict__ freq, int R, float cutoff, int p,
                                                    const float* __restrict__ drbf, float* __restrict__ part) {
   __shared__ float red[4][64];
-  const int n = threadIdx.x & 63, sub = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int np = R <= 32 ? 32 : 64, rpp = 64 / np;  // basis slots and rows per pass
+  const int n = lane % np, rs = lane / np;
   float acc = 0.f;
   if (n < R) {
     const float inv_c = 1.0f / cutoff, pre = sqrtf(2.0f * inv_c) * inv_c, f = freq[n];
-    const int r0 = blockIdx.x * kFreqRowsPerBlock;
-    for (int rr = sub; rr < kFreqRowsPerBlock; rr += 4) {
+    const int r0 = blockIdx.x * kFreqRowsPerBlock + wave * (kFreqRowsPerBlock / 4);
+    for (int rr = rs; rr < kFreqRowsPerBlock / 4; rr += rpp) {
       const int row = r0 + rr;
       if (row >= rows) break;
       const float d = len[idx ? idx[row] : row];
       acc += drbf[(int64_t)row * R + n] * pre * cosf(f * d * inv_c) * envelope(d * inv_c, p);
     }
   }
-  red[sub][n] = acc;
+  // the rpp row slots of a wave hold the same n: fold them, then the waves
+  if (np == 32) acc += __shfl_xor(acc, 32);
+  if (lane < np) red[wave][lane] = acc;
   __syncthreads();
-  if (threadIdx.x < 64 && (int)threadIdx.x < R)
+  if (threadIdx.x < R)
     part[(int64_t)blockIdx.x * R + threadIdx.x] = ((red[0][threadIdx.x] + red[1][threadIdx.x]) + red[2][threadIdx.x]) + red[3][threadIdx.x];
 }
 
@@ -1316,14 +1335,18 @@ int segsum_launch(SegJobs J, int wps, hipStream_t st) {
 }
 
 int pack_params(const ParamLayout& L, const ParamLayout& La, const float* P, float* Pal, hipStream_t st) {
-  for (int k0 = 0; k0 < L.ntensors; k0 += 96) {
+  for (int k0 = 0; k0 < L.ntensors; k0 += kPackTensors) {
     PackTable t{};
-    for (int k = k0; k < L.ntensors && t.n < 96; ++k, ++t.n) {
+    int chunks = 0;
+    for (int k = k0; k < L.ntensors && t.n < kPackTensors; ++k, ++t.n) {
       t.src[t.n] = (int)L.toff[k];
       t.dst[t.n] = (int)La.toff[k];
       t.len[t.n] = (int)L.tlen[k];
+      t.chunk0[t.n] = chunks;
+      chunks += (int)cdiv(std::max<int64_t>(L.tlen[k], 1), kPackChunk);
     }
-    KLAUNCH(st, "k_pack_params", k_pack_params<<<t.n, 256, 0, st>>>(t, P, Pal));
+    t.chunk0[t.n] = chunks;
+    KLAUNCH(st, "k_pack_params", k_pack_params<<<chunks, 256, 0, st>>>(t, P, Pal));
   }
   return CHGNET_OK;
 }
@@ -1623,7 +1646,9 @@ int forward_impl(Ctx& c, const float* Pflat, float* energy, float* forces, float
     }
     // updates: v' = v + m Wo + bo; e' = e (+ mu Wo + bo on bonds)
     if (E > 0) {
-      KLAUNCH(st, "k_copy", k_copy<<<(unsigned)cdiv(E * D, 256), 256, 0, st>>>(a.e[t + 1], a.e[t], E * D));
+      const int64_t n4 = E * D / 4;  // d is a multiple of 4 and the arena aligns to 256 B
+      KLAUNCH(st, "k_copy", k_copy4<<<(unsigned)std::min<int64_t>(cdiv(n4, 256), 4096), 256, 0, st>>>(
+                                reinterpret_cast<float4*>(a.e[t + 1]), reinterpret_cast<const float4*>(a.e[t]), n4));
     }
     {
       GemmProblem p = gp(N, D, a.v[t + 1], D);
