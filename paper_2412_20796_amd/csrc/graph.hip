@@ -4,7 +4,7 @@
 // axis, each at least r + margin thick (so the neighbours of an atom lie in
 // the slabs within K_a = floor((r + margin) n_a / h_a) + 1 of its own, with
 // periodic images handled by "virtual" slab indices), atoms are binned by
-// their wrapped fractional coordinates, and one wavefront per atom tests all
+// their wrapped fractional coordinates, and one block per atom tests all
 // candidates with the exact fp32 inclusion expression. The accepted (j, n)
 // keys of an atom are then sorted in LDS into the canonical (j, n1, n2, n3)
 // order, so the output does not depend on the order in which atoms landed in
@@ -222,11 +222,24 @@ struct SearchArgs {
   const int* bin_atoms;
 };
 
-// Visit every candidate (j, n) of atom i; calls f(j, n1, n2, n3, d2) on the
-// lanes of one wavefront for the candidates that pass the atom cutoff.
+// One 256-thread block per atom. The candidates of atom i are the atoms of
+// its (2K+1)^3 virtual slabs; the block takes the virtual slabs 256 at a
+// time, scans their atom counts, and then spreads the flattened candidate
+// list over all threads (a thread finds its slab by binary search over the
+// scanned counts), so small slabs do not leave lanes idle.
+constexpr int kSearchThreads = 256;
+struct SearchShared {
+  int pre[kSearchThreads];  // exclusive prefix of the slabs' atom counts
+  int lo[kSearchThreads];   // first bin_atoms slot of each slab
+  int m[kSearchThreads][3];  // lattice translation of each virtual slab
+  int wsum[kSearchThreads / 64];
+};
+
+// Calls f(j, n1, n2, n3, d2) on the thread that holds candidate (j, n) of
+// atom i, for every candidate that passes the atom cutoff.
 template <class F>
-__device__ __forceinline__ void for_each_neighbour(const SearchArgs& A, int i, F&& f) {
-  const int lane = threadIdx.x & 63;
+__device__ __forceinline__ void block_search(const SearchArgs& A, int i, SearchShared& sh, F&& f) {
+  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
   const int s = A.atom_struct[i];
   const StructInfo& si = A.info[s];
   float L[9];
@@ -234,52 +247,82 @@ __device__ __forceinline__ void for_each_neighbour(const SearchArgs& A, int i, F
   const float ri[3] = {A.pos[i * 3 + 0], A.pos[i * 3 + 1], A.pos[i * 3 + 2]};
   const int ci[3] = {A.atom_cell[i * 3 + 0], A.atom_cell[i * 3 + 1], A.atom_cell[i * 3 + 2]};
   const int wi[3] = {A.atom_wrap[i * 3 + 0], A.atom_wrap[i * 3 + 1], A.atom_wrap[i * 3 + 2]};
-  for (int d0 = -si.K[0]; d0 <= si.K[0]; ++d0) {
-    const int v0 = ci[0] + d0, b0 = floor_mod(v0, si.nb[0]), m0 = (v0 - b0) / si.nb[0];
-    for (int d1 = -si.K[1]; d1 <= si.K[1]; ++d1) {
-      const int v1 = ci[1] + d1, b1 = floor_mod(v1, si.nb[1]), m1 = (v1 - b1) / si.nb[1];
-      for (int d2 = -si.K[2]; d2 <= si.K[2]; ++d2) {
-        const int v2 = ci[2] + d2, b2 = floor_mod(v2, si.nb[2]), m2 = (v2 - b2) / si.nb[2];
-        const int bin = si.bin_base + (b0 * si.nb[1] + b1) * si.nb[2] + b2;
-        const int lo = A.bin_start[bin], hi = A.bin_start[bin + 1];
-        for (int base = lo; base < hi; base += 64) {
-          const int idx = base + lane;
-          bool pass = false;
-          int j = 0, n1 = 0, n2 = 0, n3 = 0;
-          float dd = 0.f;
-          if (idx < hi) {
-            j = A.bin_atoms[idx];
-            n1 = m0 - A.atom_wrap[j * 3 + 0] + wi[0];
-            n2 = m1 - A.atom_wrap[j * 3 + 1] + wi[1];
-            n3 = m2 - A.atom_wrap[j * 3 + 2] + wi[2];
-            const float rj[3] = {A.pos[j * 3 + 0], A.pos[j * 3 + 1], A.pos[j * 3 + 2]};
-            dd = pair_d2(ri, rj, n1, n2, n3, L);
-            pass = dd < A.rc2_atom && !(j == i && n1 == 0 && n2 == 0 && n3 == 0);
-          }
-          f(pass, j, n1, n2, n3, dd);
-        }
-      }
+  const int w0 = 2 * si.K[0] + 1, w1 = 2 * si.K[1] + 1, w2 = 2 * si.K[2] + 1;
+  const int nv = w0 * w1 * w2;
+  for (int v0 = 0; v0 < nv; v0 += kSearchThreads) {
+    const int v = v0 + t;
+    int cnt = 0;
+    if (v < nv) {
+      const int d2 = v % w2 - si.K[2], d1 = (v / w2) % w1 - si.K[1], d0 = v / (w2 * w1) - si.K[0];
+      const int x0 = ci[0] + d0, b0 = floor_mod(x0, si.nb[0]);
+      const int x1 = ci[1] + d1, b1 = floor_mod(x1, si.nb[1]);
+      const int x2 = ci[2] + d2, b2 = floor_mod(x2, si.nb[2]);
+      const int bin = si.bin_base + (b0 * si.nb[1] + b1) * si.nb[2] + b2;
+      const int lo = A.bin_start[bin];
+      cnt = A.bin_start[bin + 1] - lo;
+      sh.lo[t] = lo;
+      sh.m[t][0] = (x0 - b0) / si.nb[0];
+      sh.m[t][1] = (x1 - b1) / si.nb[1];
+      sh.m[t][2] = (x2 - b2) / si.nb[2];
     }
+    // block exclusive scan of the counts
+    int incl = cnt;
+    for (int off = 1; off < 64; off <<= 1) {
+      const int y = __shfl_up(incl, off, 64);
+      if (lane >= off) incl += y;
+    }
+    if (lane == 63) sh.wsum[w] = incl;
+    __syncthreads();
+    int base = 0, total = 0;
+    for (int k = 0; k < kSearchThreads / 64; ++k) {
+      base += k < w ? sh.wsum[k] : 0;
+      total += sh.wsum[k];
+    }
+    sh.pre[t] = base + incl - cnt;
+    __syncthreads();
+    for (int c = t; c < total; c += kSearchThreads) {
+      int lo = 0, hi = kSearchThreads - 1;  // last slab u with pre[u] <= c
+      while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (sh.pre[mid] <= c) lo = mid;
+        else hi = mid - 1;
+      }
+      const int j = A.bin_atoms[sh.lo[lo] + (c - sh.pre[lo])];
+      const int n1 = sh.m[lo][0] - A.atom_wrap[j * 3 + 0] + wi[0];
+      const int n2 = sh.m[lo][1] - A.atom_wrap[j * 3 + 1] + wi[1];
+      const int n3 = sh.m[lo][2] - A.atom_wrap[j * 3 + 2] + wi[2];
+      const float rj[3] = {A.pos[j * 3 + 0], A.pos[j * 3 + 1], A.pos[j * 3 + 2]};
+      const float dd = pair_d2(ri, rj, n1, n2, n3, L);
+      if (dd < A.rc2_atom && !(j == i && n1 == 0 && n2 == 0 && n3 == 0)) f(j, n1, n2, n3, dd);
+    }
+    __syncthreads();
   }
 }
 
-__device__ __forceinline__ int wave_sum(int v) {
+// Block-wide sum of one int per thread (256 threads); every thread gets it.
+__device__ __forceinline__ int block_sum(int v, int* wsum) {
   for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
-  return v;
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) wsum[threadIdx.x >> 6] = v;
+  __syncthreads();
+  int t = 0;
+  for (int k = 0; k < kSearchThreads / 64; ++k) t += wsum[k];
+  return t;
 }
 
-// One wavefront per atom: count edges and bonds.
-__global__ void __launch_bounds__(256) k_count(SearchArgs A, int* __restrict__ edge_count, int* __restrict__ bond_count) {
-  const int i = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (i >= A.N) return;
+// Count edges and bonds of atom blockIdx.x.
+__global__ void __launch_bounds__(kSearchThreads) k_count(SearchArgs A, int* __restrict__ edge_count,
+                                                          int* __restrict__ bond_count) {
+  __shared__ SearchShared sh;
+  const int i = blockIdx.x;
   int ne = 0, nb = 0;
-  for_each_neighbour(A, i, [&](bool pass, int, int, int, int, float dd) {
-    ne += pass ? 1 : 0;
-    nb += (pass && dd < A.rc2_bond) ? 1 : 0;
+  block_search(A, i, sh, [&](int, int, int, int, float dd) {
+    ++ne;
+    nb += dd < A.rc2_bond ? 1 : 0;
   });
-  ne = wave_sum(ne);
-  nb = wave_sum(nb);
-  if ((threadIdx.x & 63) == 0) {
+  ne = block_sum(ne, sh.wsum);
+  nb = block_sum(nb, sh.wsum);
+  if (threadIdx.x == 0) {
     edge_count[i] = ne;
     bond_count[i] = nb;
   }
@@ -346,31 +389,30 @@ __device__ __forceinline__ unsigned long long make_key(int j, int n1, int n2, in
          (bond ? 1ull : 0ull);
 }
 
-// One 64-thread block per atom: gather accepted keys into LDS, bitonic sort,
-// write edges in canonical order and the atom's bond list.
-__global__ void __launch_bounds__(64) k_fill(SearchArgs A, int sort_size, const int* __restrict__ edge_ptr,
-                                             const int* __restrict__ bond_ptr, int* __restrict__ edge_dst,
-                                             int* __restrict__ edge_img, int* __restrict__ bond_edge) {
+// One block per atom: gather the accepted keys into LDS (slots taken with an
+// LDS counter; the order is fixed by the sort that follows), bitonic sort,
+// write the edges in canonical order and the atom's bond list.
+__global__ void __launch_bounds__(kSearchThreads) k_fill(SearchArgs A, int sort_size, const int* __restrict__ edge_ptr,
+                                                         const int* __restrict__ bond_ptr, int* __restrict__ edge_dst,
+                                                         int* __restrict__ edge_img, int* __restrict__ bond_edge) {
   extern __shared__ unsigned long long keys[];
-  const int i = blockIdx.x;
-  const int lane = threadIdx.x;
-  int count = 0;
-  for_each_neighbour(A, i, [&](bool pass, int j, int n1, int n2, int n3, float dd) {
-    const unsigned long long m = __ballot(pass);
-    if (pass) {
-      const int rank = __popcll(m & ((1ull << lane) - 1ull));
-      const int slot = count + rank;
-      if (slot < sort_size) keys[slot] = make_key(j, n1, n2, n3, dd < A.rc2_bond);
-    }
-    count += __popcll(m);
+  __shared__ SearchShared sh;
+  __shared__ int nkeys;
+  const int i = blockIdx.x, t = threadIdx.x, lane = t & 63, w = t >> 6;
+  if (t == 0) nkeys = 0;
+  __syncthreads();
+  block_search(A, i, sh, [&](int j, int n1, int n2, int n3, float dd) {
+    const int slot = atomicAdd(&nkeys, 1);
+    if (slot < sort_size) keys[slot] = make_key(j, n1, n2, n3, dd < A.rc2_bond);
   });
-  for (int k = count + lane; k < sort_size; k += 64) keys[k] = ~0ull;
+  const int count = min(nkeys, sort_size);
+  for (int k = count + t; k < sort_size; k += kSearchThreads) keys[k] = ~0ull;
   __syncthreads();
   // bitonic sort of sort_size (power of two) keys
   for (int size = 2; size <= sort_size; size <<= 1) {
     for (int stride = size >> 1; stride > 0; stride >>= 1) {
-      for (int t = lane; t < sort_size / 2; t += 64) {
-        const int lo = 2 * t - (t & (stride - 1));
+      for (int u = t; u < sort_size / 2; u += kSearchThreads) {
+        const int lo = 2 * u - (u & (stride - 1));
         const int hi = lo + stride;
         const bool up = (lo & size) == 0;
         const unsigned long long a = keys[lo], b = keys[hi];
@@ -381,22 +423,26 @@ __global__ void __launch_bounds__(64) k_fill(SearchArgs A, int sort_size, const 
   }
   const int e0 = edge_ptr[i];
   const int b0 = bond_ptr[i];
-  int nb = 0;
-  for (int base = 0; base < count; base += 64) {
-    const int k = base + lane;
+  int nb = 0;  // bonds written before this round of kSearchThreads keys
+  for (int base = 0; base < count; base += kSearchThreads) {
+    const int k = base + t;
     bool bond = false;
     if (k < count) {
       const unsigned long long key = keys[k];
-      const int j = (int)(key >> 31);
-      edge_dst[e0 + k] = j;
+      edge_dst[e0 + k] = (int)(key >> 31);
       edge_img[(e0 + k) * 3 + 0] = (int)((key >> 21) & 1023) - kImgBias;
       edge_img[(e0 + k) * 3 + 1] = (int)((key >> 11) & 1023) - kImgBias;
       edge_img[(e0 + k) * 3 + 2] = (int)((key >> 1) & 1023) - kImgBias;
       bond = (key & 1ull) != 0;
     }
     const unsigned long long m = __ballot(bond);
-    if (bond) bond_edge[b0 + nb + __popcll(m & ((1ull << lane) - 1ull))] = e0 + k;
-    nb += __popcll(m);
+    if (lane == 0) sh.wsum[w] = __popcll(m);
+    __syncthreads();
+    int before = nb;
+    for (int q = 0; q < w; ++q) before += sh.wsum[q];
+    if (bond) bond_edge[b0 + before + __popcll(m & ((1ull << lane) - 1ull))] = e0 + k;
+    for (int q = 0; q < kSearchThreads / 64; ++q) nb += sh.wsum[q];
+    __syncthreads();
   }
 }
 
@@ -514,7 +560,7 @@ int build_graph(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_grap
   A.atom_wrap = g.atom_wrap;
   A.bin_start = g.bin_start;
   A.bin_atoms = g.bin_atoms;
-  KLAUNCH(st, "k_count", k_count<<<cdiv(N, 4), 256, 0, st>>>(A, g.edge_count, g.bond_count));
+  KLAUNCH(st, "k_count", k_count<<<N, kSearchThreads, 0, st>>>(A, g.edge_count, g.bond_count));
   KLAUNCH(st, "k_scan_counts", k_scan_counts<<<1, 1024, 0, st>>>(N, g.edge_count, g.bond_count, graph->edge_ptr, graph->bond_ptr, g.angle_base,
                                     g.ginfo));
 
@@ -546,7 +592,7 @@ int build_graph(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_grap
 
   int sort_size = 64;
   while (sort_size < hinfo.max_count) sort_size <<= 1;
-  KLAUNCH(st, "k_fill", k_fill<<<N, 64, sizeof(unsigned long long) * sort_size, st>>>(A, sort_size, graph->edge_ptr, graph->bond_ptr,
+  KLAUNCH(st, "k_fill", k_fill<<<N, kSearchThreads, sizeof(unsigned long long) * sort_size, st>>>(A, sort_size, graph->edge_ptr, graph->bond_ptr,
                                                                 graph->edge_dst, graph->edge_img, graph->bond_edge));
   KLAUNCH(st, "k_rev", k_rev<<<cdiv(N, 4), 256, 0, st>>>(N, graph->edge_ptr, graph->edge_dst, graph->edge_img, graph->edge_rev, g.ginfo));
   KLAUNCH(st, "k_angles", k_angles<<<cdiv(N, 256), 256, 0, st>>>(N, graph->bond_ptr, g.angle_base, graph->angle_ptr, graph->angle_b2));
