@@ -74,71 +74,91 @@ __device__ __forceinline__ int find_struct(const int* atom_ptr, int S, int i) {
 }
 
 // Per-structure setup: inverse lattice, slab counts and reach. One block.
-__global__ void k_struct_setup(int S, const int* __restrict__ atom_ptr, const float* __restrict__ lattice, float r,
-                               StructInfo* __restrict__ info, int* __restrict__ total_bins, GraphInfo* ginfo) {
-  for (int s = threadIdx.x; s < S; s += blockDim.x) {
-    StructInfo si;
-    double L[9];
-    for (int k = 0; k < 9; ++k) {
-      si.L[k] = lattice[s * 9 + k];
-      L[k] = (double)si.L[k];
-    }
-    // rows a0, a1, a2; cofactor rows give the reciprocal basis
-    double c0[3] = {L[4] * L[8] - L[5] * L[7], L[5] * L[6] - L[3] * L[8], L[3] * L[7] - L[4] * L[6]};
-    double c1[3] = {L[7] * L[2] - L[8] * L[1], L[8] * L[0] - L[6] * L[2], L[6] * L[1] - L[7] * L[0]};
-    double c2[3] = {L[1] * L[5] - L[2] * L[4], L[2] * L[3] - L[0] * L[5], L[0] * L[4] - L[1] * L[3]};
-    double det = L[0] * c0[0] + L[1] * c0[1] + L[2] * c0[2];
-    int n_s = atom_ptr[s + 1] - atom_ptr[s];
-    if (!(fabs(det) >= 1e-6) || n_s < 0) {
-      atomicOr(&ginfo->err, n_s < 0 ? ERR_PTR : ERR_DET);
-      for (int k = 0; k < 9; ++k) si.Linv[k] = 0.0;
-      si.nb[0] = si.nb[1] = si.nb[2] = 1;
-      si.K[0] = si.K[1] = si.K[2] = 0;
+// Inverse lattice, slab counts and reach of structure s (flags bad input).
+__device__ StructInfo struct_info(int s, const int* __restrict__ atom_ptr, const float* __restrict__ lattice, float r,
+                                  GraphInfo* ginfo) {
+  StructInfo si{};
+  double L[9];
+  for (int k = 0; k < 9; ++k) {
+    si.L[k] = lattice[s * 9 + k];
+    L[k] = (double)si.L[k];
+  }
+  // rows a0, a1, a2; cofactor rows give the reciprocal basis
+  double c0[3] = {L[4] * L[8] - L[5] * L[7], L[5] * L[6] - L[3] * L[8], L[3] * L[7] - L[4] * L[6]};
+  double c1[3] = {L[7] * L[2] - L[8] * L[1], L[8] * L[0] - L[6] * L[2], L[6] * L[1] - L[7] * L[0]};
+  double c2[3] = {L[1] * L[5] - L[2] * L[4], L[2] * L[3] - L[0] * L[5], L[0] * L[4] - L[1] * L[3]};
+  double det = L[0] * c0[0] + L[1] * c0[1] + L[2] * c0[2];
+  int n_s = atom_ptr[s + 1] - atom_ptr[s];
+  if (!(fabs(det) >= 1e-6) || n_s < 0) {
+    atomicOr(&ginfo->err, n_s < 0 ? ERR_PTR : ERR_DET);
+    for (int k = 0; k < 9; ++k) si.Linv[k] = 0.0;
+    si.nb[0] = si.nb[1] = si.nb[2] = 1;
+    si.K[0] = si.K[1] = si.K[2] = 0;
+    return si;
+  }
+  // frac = cart @ Linv, Linv = L^{-1}; column a of Linv = c_a / det
+  for (int row = 0; row < 3; ++row) {
+    si.Linv[row * 3 + 0] = c0[row] / det;
+    si.Linv[row * 3 + 1] = c1[row] / det;
+    si.Linv[row * 3 + 2] = c2[row] / det;
+  }
+  double vol = fabs(det);
+  double h[3];
+  const double* cs[3] = {c0, c1, c2};
+  for (int a = 0; a < 3; ++a) h[a] = vol / sqrt(cs[a][0] * cs[a][0] + cs[a][1] * cs[a][1] + cs[a][2] * cs[a][2]);
+  const double rr = (double)r + kMargin;
+  long long nb[3];
+  for (int a = 0; a < 3; ++a) {
+    double q = floor(h[a] / rr);
+    nb[a] = q < 1.0 ? 1 : (q > 1024.0 ? 1024 : (long long)q);
+  }
+  long long cap = n_s > 1 ? n_s : 1;
+  while (nb[0] * nb[1] * nb[2] > cap) {
+    int a = 0;
+    if (nb[1] > nb[a]) a = 1;
+    if (nb[2] > nb[a]) a = 2;
+    nb[a] -= 1;
+  }
+  bool thin = false;
+  for (int a = 0; a < 3; ++a) {
+    si.nb[a] = (int)nb[a];
+    double kk = floor(rr * (double)nb[a] / h[a]) + 1.0;
+    if (kk > kMaxK) { thin = true; kk = 0; }
+    si.K[a] = (int)kk;
+  }
+  if (thin) atomicOr(&ginfo->err, ERR_THIN);
+  si.bin_base = 0;
+  return si;
+}
+
+__global__ void __launch_bounds__(1024) k_struct_setup(int S, const int* __restrict__ atom_ptr,
+                                                       const float* __restrict__ lattice, float r,
+                                                       StructInfo* __restrict__ info, int* __restrict__ total_bins,
+                                                       GraphInfo* ginfo) {
+  __shared__ int scan[1024];
+  int carry = 0;  // bins of the structures of earlier rounds
+  for (int s0 = 0; s0 < S; s0 += 1024) {
+    const int s = s0 + (int)threadIdx.x;
+    int bins = 0;
+    if (s < S) {
+      const StructInfo si = struct_info(s, atom_ptr, lattice, r, ginfo);
       info[s] = si;
-      continue;
+      bins = si.nb[0] * si.nb[1] * si.nb[2];
     }
-    // frac = cart @ Linv, Linv = L^{-1}; column a of Linv = c_a / det
-    for (int row = 0; row < 3; ++row) {
-      si.Linv[row * 3 + 0] = c0[row] / det;
-      si.Linv[row * 3 + 1] = c1[row] / det;
-      si.Linv[row * 3 + 2] = c2[row] / det;
+    // exclusive scan of the bin counts over the round (Hillis-Steele in LDS)
+    scan[threadIdx.x] = bins;
+    __syncthreads();
+    for (int off = 1; off < 1024; off <<= 1) {
+      const int y = threadIdx.x >= (unsigned)off ? scan[threadIdx.x - off] : 0;
+      __syncthreads();
+      scan[threadIdx.x] += y;
+      __syncthreads();
     }
-    double vol = fabs(det);
-    double h[3];
-    const double* cs[3] = {c0, c1, c2};
-    for (int a = 0; a < 3; ++a) h[a] = vol / sqrt(cs[a][0] * cs[a][0] + cs[a][1] * cs[a][1] + cs[a][2] * cs[a][2]);
-    const double rr = (double)r + kMargin;
-    long long nb[3];
-    for (int a = 0; a < 3; ++a) {
-      double q = floor(h[a] / rr);
-      nb[a] = q < 1.0 ? 1 : (q > 1024.0 ? 1024 : (long long)q);
-    }
-    long long cap = n_s > 1 ? n_s : 1;
-    while (nb[0] * nb[1] * nb[2] > cap) {
-      int a = 0;
-      if (nb[1] > nb[a]) a = 1;
-      if (nb[2] > nb[a]) a = 2;
-      nb[a] -= 1;
-    }
-    bool thin = false;
-    for (int a = 0; a < 3; ++a) {
-      si.nb[a] = (int)nb[a];
-      double kk = floor(rr * (double)nb[a] / h[a]) + 1.0;
-      if (kk > kMaxK) { thin = true; kk = 0; }
-      si.K[a] = (int)kk;
-    }
-    if (thin) atomicOr(&ginfo->err, ERR_THIN);
-    info[s] = si;
+    if (s < S) info[s].bin_base = carry + scan[threadIdx.x] - bins;
+    carry += scan[1023];
+    __syncthreads();
   }
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    int acc = 0;
-    for (int s = 0; s < S; ++s) {
-      info[s].bin_base = acc;
-      acc += info[s].nb[0] * info[s].nb[1] * info[s].nb[2];
-    }
-    *total_bins = acc;
-  }
+  if (threadIdx.x == 0) *total_bins = carry;
 }
 
 __global__ void k_atom_bin(int N, int S, const int* __restrict__ atom_ptr, const float* __restrict__ pos,
@@ -469,18 +489,23 @@ __global__ void k_rev(int N, const int* __restrict__ edge_ptr, const int* __rest
   }
 }
 
-__global__ void k_angles(int N, const int* __restrict__ bond_ptr, const long long* __restrict__ angle_base,
-                         int* __restrict__ angle_ptr, int* __restrict__ angle_b2) {
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+// Angle list of atom i (one wavefront per atom): angle_ptr of its bonds and,
+// if requested, the second bond of each of its k(k-1) angles.
+__global__ void __launch_bounds__(256) k_angles(int N, const int* __restrict__ bond_ptr,
+                                                const long long* __restrict__ angle_base, int* __restrict__ angle_ptr,
+                                                int* __restrict__ angle_b2) {
+  const int i = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
   if (i >= N) return;
   const int b0 = bond_ptr[i], k = bond_ptr[i + 1] - b0;
   const long long a0 = angle_base[i];
-  for (int p = 0; p < k; ++p) angle_ptr[b0 + p] = (int)(a0 + (long long)p * (k - 1));
-  if (i == N - 1) angle_ptr[bond_ptr[N]] = (int)angle_base[N];
-  if (angle_b2) {
-    for (int p = 0; p < k; ++p)
-      for (int q = 0; q < k; ++q)
-        if (q != p) angle_b2[a0 + (long long)p * (k - 1) + (q < p ? q : q - 1)] = b0 + q;
+  for (int p = lane; p < k; p += 64) angle_ptr[b0 + p] = (int)(a0 + (long long)p * (k - 1));
+  if (i == N - 1 && lane == 0) angle_ptr[bond_ptr[N]] = (int)angle_base[N];
+  if (angle_b2 && k > 1) {
+    const int na = k * (k - 1);
+    for (int x = lane; x < na; x += 64) {
+      const int p = x / (k - 1), qq = x - p * (k - 1);
+      angle_b2[a0 + x] = b0 + (qq < p ? qq : qq + 1);
+    }
   }
 }
 
@@ -542,7 +567,7 @@ int build_graph(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_grap
   CHG_HIP(hipMemsetAsync(g.ginfo, 0, sizeof(GraphInfo), st));
   CHG_HIP(hipMemsetAsync(g.bin_count, 0, sizeof(int) * (nbins_cap + 1), st));
   CHG_HIP(hipMemsetAsync(g.bin_cursor, 0, sizeof(int) * (nbins_cap + 1), st));
-  KLAUNCH(st, "k_struct_setup", k_struct_setup<<<1, 256, 0, st>>>(S, batch->atom_ptr, batch->lattice, hp->r_atom, g.info, g.total_bins, g.ginfo));
+  KLAUNCH(st, "k_struct_setup", k_struct_setup<<<1, 1024, 0, st>>>(S, batch->atom_ptr, batch->lattice, hp->r_atom, g.info, g.total_bins, g.ginfo));
   KLAUNCH(st, "k_atom_bin", k_atom_bin<<<cdiv(N, 256), 256, 0, st>>>(N, S, batch->atom_ptr, batch->pos, batch->Z, g.info, g.atom_struct, g.atom_bin,
                                            g.atom_cell, g.atom_wrap, g.bin_count, g.ginfo));
   // total bins <= N + S (each crystal has at most max(1, n_s) bins)
@@ -595,7 +620,7 @@ int build_graph(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_grap
   KLAUNCH(st, "k_fill", k_fill<<<N, kSearchThreads, sizeof(unsigned long long) * sort_size, st>>>(A, sort_size, graph->edge_ptr, graph->bond_ptr,
                                                                 graph->edge_dst, graph->edge_img, graph->bond_edge));
   KLAUNCH(st, "k_rev", k_rev<<<cdiv(N, 4), 256, 0, st>>>(N, graph->edge_ptr, graph->edge_dst, graph->edge_img, graph->edge_rev, g.ginfo));
-  KLAUNCH(st, "k_angles", k_angles<<<cdiv(N, 256), 256, 0, st>>>(N, graph->bond_ptr, g.angle_base, graph->angle_ptr, graph->angle_b2));
+  KLAUNCH(st, "k_angles", k_angles<<<cdiv(N, 4), 256, 0, st>>>(N, graph->bond_ptr, g.angle_base, graph->angle_ptr, graph->angle_b2));
   return CHGNET_OK;
 }
 
