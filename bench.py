@@ -158,8 +158,8 @@ def algorithmic_cost(tag, z):
         return "mfma", T * E * 4 * D * D + Tang * A * 8 * D * D + A * 4 * D * D
     if tag == "gemm_in_bwd":
         return "mfma", T * (E * 4 * D * D + N * 16 * D * D) - N * 4 * D * D + Tang * A * 8 * D * D + A * 4 * D * D
-    if tag == "tn_in":
-        return "mfma", (T * (E * 4 * D * D + N * 16 * D * D + B * 8 * D * D) - N * 4 * D * D
+    if tag == "tn_in":  # first-layer and output-layer weight gradients of every block
+        return "mfma", (T * (E * 4 * D * D + N * 16 * D * D + B * 8 * D * D + (N + B) * 2 * D * D) - N * 4 * D * D
                         + Tang * (A * 8 * D * D + B * 8 * D * D) + A * 4 * D * D)
     if tag == "gemm_proj":
         return "mfma", T * (N * 16 * D * D + B * 8 * D * D) - N * 4 * D * D - B * 4 * D * D

@@ -853,7 +853,7 @@ int tn_launch(const TnBatch& b, float* part, int64_t part_cap, hipStream_t st, c
   return CHGNET_OK;
 }
 
-int reduce_rows_multi(const ReduceJobs& J, double* scratch, unsigned* tickets, hipStream_t st) {
+int reduce_rows_multi(const ReduceJobs& J, double* scratch, hipStream_t st) {
   if (J.n == 0) return CHGNET_OK;
   int maxc = 0, maxg = 1;
   for (int i = 0; i < J.n; ++i) {
@@ -862,18 +862,17 @@ int reduce_rows_multi(const ReduceJobs& J, double* scratch, unsigned* tickets, h
     maxg = std::max(maxg, std::min(32, J.j[i].nchunks));
   }
   if (maxc == 0) return CHGNET_OK;
-  (void)tickets;
   KLAUNCH(st, "k_reduce_rows1", k_reduce_rows1<<<dim3((unsigned)cdiv(maxc, 64), maxg, J.n), 256, 0, st>>>(J, 32, scratch));
   KLAUNCH(st, "k_reduce_rows2", k_reduce_rows2<<<dim3((unsigned)cdiv(maxc, 64), J.n), 256, 0, st>>>(J, 32, scratch));
   return CHGNET_OK;
 }
 
 int reduce_rows_launch(const float* part, int nchunks, int64_t stride, int count, float* out, double* scratch,
-                       unsigned* tickets, hipStream_t st) {
+                       hipStream_t st) {
   ReduceJobs J{};
   J.n = 1;
   J.j[0] = ReduceJob{part, nchunks, stride, count, out};
-  return reduce_rows_multi(J, scratch, tickets, st);
+  return reduce_rows_multi(J, scratch, st);
 }
 
 }  // namespace chg

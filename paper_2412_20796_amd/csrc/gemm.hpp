@@ -92,14 +92,13 @@ struct ReduceJobs {
   int n;
   ReduceJob j[3];
 };
-// Up to 3 independent reductions in one launch; scratch: 3 * 32 * 1024
-// doubles, tickets: 3 * 64 zero-initialised counters (left at zero).
-int reduce_rows_multi(const ReduceJobs& J, double* scratch, unsigned* tickets, hipStream_t st);
+// Up to 3 independent reductions in two launches (32 ordered group sums,
+// then their ordered sum); scratch: 3 * 32 * 1024 doubles.
+int reduce_rows_multi(const ReduceJobs& J, double* scratch, hipStream_t st);
 
 // out[k] += sum_c part[c*stride + k] (k < count), in a fixed order, in fp64.
-// scratch: 32 * count doubles; tickets: cdiv(count, 64) zero-initialised
-// counters (left at zero on return).
+// scratch: 32 * count doubles.
 int reduce_rows_launch(const float* part, int nchunks, int64_t stride, int count, float* out, double* scratch,
-                       unsigned* tickets, hipStream_t st);
+                       hipStream_t st);
 
 }  // namespace chg

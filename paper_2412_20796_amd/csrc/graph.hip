@@ -509,6 +509,17 @@ __global__ void __launch_bounds__(256) k_angles(int N, const int* __restrict__ b
   }
 }
 
+// Clears the graph info record and the bin counters (n each).
+__global__ void k_zero_scratch(GraphInfo* __restrict__ ginfo, int* __restrict__ bin_count, int* __restrict__ bin_cursor,
+                               int n) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i == 0) *ginfo = GraphInfo{};
+  if (i < n) {
+    bin_count[i] = 0;
+    bin_cursor[i] = 0;
+  }
+}
+
 struct GraphScratch {
   StructInfo* info;
   GraphInfo* ginfo;
@@ -564,9 +575,10 @@ int build_graph(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_grap
   if (!ws || !ar.ok()) return fail(CHGNET_EWORKSPACE, "workspace too small for the graph build");
   const int64_t nbins_cap = (int64_t)N + S + 1;
 
-  CHG_HIP(hipMemsetAsync(g.ginfo, 0, sizeof(GraphInfo), st));
-  CHG_HIP(hipMemsetAsync(g.bin_count, 0, sizeof(int) * (nbins_cap + 1), st));
-  CHG_HIP(hipMemsetAsync(g.bin_cursor, 0, sizeof(int) * (nbins_cap + 1), st));
+  {
+    const int n = (int)(nbins_cap + 1);
+    KLAUNCH(st, "k_zero_scratch", k_zero_scratch<<<(unsigned)cdiv(n, 256), 256, 0, st>>>(g.ginfo, g.bin_count, g.bin_cursor, n));
+  }
   KLAUNCH(st, "k_struct_setup", k_struct_setup<<<1, 1024, 0, st>>>(S, batch->atom_ptr, batch->lattice, hp->r_atom, g.info, g.total_bins, g.ginfo));
   KLAUNCH(st, "k_atom_bin", k_atom_bin<<<cdiv(N, 256), 256, 0, st>>>(N, S, batch->atom_ptr, batch->pos, batch->Z, g.info, g.atom_struct, g.atom_bin,
                                            g.atom_cell, g.atom_wrap, g.bin_count, g.ginfo));

@@ -639,6 +639,7 @@ struct GateBwdJob {
   const float *up, *eb;
   const int *up_idx, *b2_idx;
   float *aux, *dz, *lnpart;
+  int aux_acc;  // BWD_ATOM: add to aux (0: the first layer of the backward overwrites it)
 };
 struct GateBwdJobs {
   int n;
@@ -739,9 +740,14 @@ __device__ __forceinline__ void gate_bwd_rows(int blk, const GateBwdJob& J, floa
     store_cols<D, CPL>(dz + (int64_t)row * lddz + D, j, dyg);
     if (MODE == BWD_ATOM) {
       float de[CPL];
-      load_cols<D, CPL>(aux + (int64_t)row * D, j, de);
+      if (J.aux_acc) {
+        load_cols<D, CPL>(aux + (int64_t)row * D, j, de);
 #pragma unroll
-      for (int k = 0; k < CPL; ++k) de[k] += u[k] * side[k];
+        for (int k = 0; k < CPL; ++k) de[k] += u[k] * side[k];
+      } else {
+#pragma unroll
+        for (int k = 0; k < CPL; ++k) de[k] = u[k] * side[k];
+      }
       store_cols<D, CPL>(aux + (int64_t)row * D, j, de);
     } else if (MODE == BWD_BOND) {
 #pragma unroll
@@ -850,7 +856,7 @@ __global__ void __launch_bounds__(256) k_bond_bwd_reduce(int B, int D, const int
                                                          const int* __restrict__ bond_ptr, const int* __restrict__ angle_ptr,
                                                          const float* __restrict__ dzae, const float* __restrict__ t2,
                                                          const float* __restrict__ dmu, const float* __restrict__ ssum,
-                                                         float* __restrict__ DZ12, float* __restrict__ deb) {
+                                                         float* __restrict__ DZ12, float* __restrict__ deb, int deb_acc) {
   const int b = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
   if (b >= B) return;
   const int i = bond_src[b], k0 = bond_ptr[i], k = bond_ptr[i + 1] - k0, q = b - k0;
@@ -895,7 +901,8 @@ __global__ void __launch_bounds__(256) k_bond_bwd_reduce(int B, int D, const int
 #pragma unroll
   for (int x = 0; x < TPL; ++x) {
     const int64_t o = (int64_t)b * D + lane * TPL + x;
-    deb[o] += dmu[o] * ssum[o] + (tt[0][x] + tt[1][x]);
+    const float v = dmu[o] * ssum[o] + (tt[0][x] + tt[1][x]);
+    deb[o] = deb_acc ? deb[o] + v : v;
   }
 }
 
@@ -1125,7 +1132,6 @@ struct Acts {
   float *doE, *doS, *dn, *doF, *dh2E, *dh2S, *dh2F, *dh1ES, *dh1F, *drbf_a, *drbf_b;
   float *lnpart, *tnpart, *fpart, *Pal;
   double* red2;
-  unsigned* tickets;
   int64_t lnpart_stride;
   int64_t tnpart_cap;
   // loss
@@ -1202,7 +1208,6 @@ void carve_acts(Arena& ar, const Dims& m, Acts& a, int64_t n_params_aligned) {
   a.lnpart_stride = gate_blocks * 4 * D;
   a.lnpart = ar.take<float>(3 * a.lnpart_stride);
   a.red2 = ar.take<double>(3 * kReduceGroups * 8 * 128);  // per reduce job: 32 groups x up to 1024 columns
-  a.tickets = ar.take<unsigned>(3 * 64);
   a.tnpart_cap = kTnPartFloats;
   a.tnpart = ar.take<float>(a.tnpart_cap);
   a.fpart = ar.take<float>(cdiv(std::max(E, (int64_t)1), kFreqRowsPerBlock) * R);
@@ -1462,7 +1467,7 @@ int gate_bwd_launch(int D, GateBwdJobs J, float* const* ln_grad, const Acts& a, 
   if (blocks == 0) return CHGNET_OK;
   if (D == 64) KLAUNCH(st, "k_gate_bwd", k_gate_bwd<64><<<blocks, 256, 0, st>>>(K));
   else KLAUNCH(st, "k_gate_bwd", k_gate_bwd<128><<<blocks, 256, 0, st>>>(K));
-  return reduce_rows_multi(R, a.red2, a.tickets, st);
+  return reduce_rows_multi(R, a.red2, st);
 }
 
 GateAdds adds(int n, const float* p0, int ld0, const int* i0, const float* p1, int ld1, const int* i1) {
@@ -1731,9 +1736,6 @@ int backward_impl(Ctx& c, const float* Pflat, bool repack, const float* dE, cons
   const int64_t N = m.N, E = m.E, B = m.B, A = m.A;
 
   CHG_TRY(fill(G, Lg.total, 0.f, st));
-  CHG_TRY(fill(reinterpret_cast<float*>(a.tickets), 3 * 64, 0.f, st));
-  CHG_TRY(fill(a.dea, E * D, 0.f, st));
-  CHG_TRY(fill(a.deb, B * D, 0.f, st));
 
   // heads
   KLAUNCH(st, "k_seed_atoms", k_seed_atoms<<<(unsigned)cdiv(N, 256), 256, 0, st>>>((int)N, a.atom_struct, bt.lattice, dE, dS, a.doE, a.doS));
@@ -1832,8 +1834,7 @@ int backward_impl(Ctx& c, const float* Pflat, bool repack, const float* dE, cons
       ts.push_back(tp(N, 1, D, nullptr, 0, 0, nullptr, a.dv[cur], D, 0, nullptr, G + lg.av_bo, D));
       ts.push_back(tp(B, D, D, a.mu[t], D, 0, nullptr, a.de[cur], D, 0, g.bond_edge, G + lg.be_Wo, D));
       ts.push_back(tp(B, 1, D, nullptr, 0, 0, nullptr, a.de[cur], D, 0, g.bond_edge, G + lg.be_bo, D));
-      CHG_TRY(run_tns(ts, a, st, "tn_out"));
-      ts.clear();
+      // launched with the first-layer weight gradients below (inputs unchanged)
     }
     // angle gates (bond conv, then angle update)
     const GateAdds ad_av = adds(2, a.Xa[t], 8 * D, a.edge_src, a.Xa[t] + 2 * D, 8 * D, g.edge_dst);
@@ -1845,6 +1846,7 @@ int backward_impl(Ctx& c, const float* Pflat, bool repack, const float* dE, cons
                            a.dzae, 4 * D);
       J.j[J.n++] = bwd_job(BWD_ATOM, E, a.zv[t], 2 * D, ad_av, ln_ptrs(P, lo.av), a.dm, a.edge_src, a.ea, nullptr, a.dea,
                            a.dzv, 2 * D);
+      J.j[J.n - 1].aux_acc = t < m.T - 1;  // the first layer of the backward starts d e^a
       if (ang)
         J.j[J.n++] = bwd_job(BWD_ANGLE, A, a.zae[t] + 2 * D, 4 * D, ad_an, ln_ptrs(P, lo.an), a.da[cur], nullptr, nullptr,
                              nullptr, nullptr, a.dzae + 2 * D, 4 * D);
@@ -1856,7 +1858,8 @@ int backward_impl(Ctx& c, const float* Pflat, bool repack, const float* dE, cons
       const int cpl = W4 / 64;
 #define BOND_REDUCE(CPL, TPL)                                                                                    \
   KLAUNCH(st, "k_bond_bwd_reduce", k_bond_bwd_reduce<CPL, TPL><<<nb, 256, 0, st>>>((int)B, D, a.bond_src, g.bond_ptr, \
-                                                       g.angle_ptr, a.dzae, a.t2, a.dmu, a.ssum[t], a.DZ12, a.deb))
+                                                       g.angle_ptr, a.dzae, a.t2, a.dmu, a.ssum[t], a.DZ12, a.deb, \
+                                                       t < m.T - 1))
       if (cpl == 2) BOND_REDUCE(2, 1);
       else if (cpl == 4 && D == 64) BOND_REDUCE(4, 1);
       else if (cpl == 4) BOND_REDUCE(4, 2);
@@ -1962,13 +1965,13 @@ int backward_impl(Ctx& c, const float* Pflat, bool repack, const float* dE, cons
       const int64_t nb = cdiv(E, kFreqRowsPerBlock);
       KLAUNCH(st, "k_rbf_fgrad", k_rbf_fgrad<<<(unsigned)nb, 256, 0, st>>>((int)E, nullptr, a.edge_len, P + L.f_a, m.R, c.hp->r_atom,
                                                 c.hp->envelope_p, a.drbf_a, a.fpart));
-      CHG_TRY(reduce_rows_launch(a.fpart, (int)nb, m.R, m.R, G + Lg.f_a, a.red2, a.tickets, st));
+      CHG_TRY(reduce_rows_launch(a.fpart, (int)nb, m.R, m.R, G + Lg.f_a, a.red2, st));
     }
     if (B > 0) {
       const int64_t nb = cdiv(B, kFreqRowsPerBlock);
       KLAUNCH(st, "k_rbf_fgrad", k_rbf_fgrad<<<(unsigned)nb, 256, 0, st>>>((int)B, g.bond_edge, a.edge_len, P + L.f_b, m.R, c.hp->r_bond,
                                                 c.hp->envelope_p, a.drbf_b, a.fpart));
-      CHG_TRY(reduce_rows_launch(a.fpart, (int)nb, m.R, m.R, G + Lg.f_b, a.red2, a.tickets, st));
+      CHG_TRY(reduce_rows_launch(a.fpart, (int)nb, m.R, m.R, G + Lg.f_b, a.red2, st));
     }
   }
   return CHGNET_OK;
