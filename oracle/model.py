@@ -32,7 +32,17 @@ library alike):
 * Stress head: sigma_s = (1/V_s) sum_i sum_ab c_i,ab u_a u_b^T, u_a the unit
   lattice vectors, c_i the 9 outputs of the stress MLP.
 * Loss: prefactor-weighted mean squared errors of per-atom energy, force
-  components and stress components (magnetic moments are not modelled).
+  components and stress components; optionally the Huber loss of Sec. IV
+  (h(r) = r^2/2 for |r| <= delta, delta (|r| - delta/2) beyond), whose delta
+  the paper does not state (a caller's choice).
+* Magnetic-moment head (Sec. II-B; Sec. IV lists magmom among the
+  predictions but gives no formula): m_i = |v^T_i w_m + b_m|, a linear map of
+  the final atom features whose absolute value is the moment's magnitude;
+  d|x|/dx at 0 is taken as 0. Its loss term averages over the N atoms.
+* Interaction-block order: the default is Eq. (11) (all three modules read
+  layer-t features). HParams.sequential selects the reference block of
+  Eq. (10): the bond conv reads v^{t+1}, the angle update reads v^{t+1} and
+  the updated bond features e^{t+1} (Eq. (5), (6)).
 """
 from __future__ import annotations
 
@@ -54,6 +64,8 @@ class HParams:
     envelope_p: int = 8
     r_atom: float = 6.0
     r_bond: float = 3.0
+    magmom: bool = False      # magnetic-moment head
+    sequential: bool = False  # Eq. (10) block instead of Eq. (11)
 
 
 # ---------------------------------------------------------------------------
@@ -77,6 +89,8 @@ def layout(hp: HParams):
     for h, o in (("E", 1), ("F", 1), ("S", 9)):
         ent += [(h + "_W1", (d, d)), (h + "_b1", (d,)), (h + "_W2", (d, d)), (h + "_b2", (d,)),
                 (h + "_W3", (d, o)), (h + "_b3", (o,))]
+    if hp.magmom:
+        ent += [("M_W", (d, 1)), ("M_b", (1,))]
     out, off = {}, 0
     for name, shape in ent:
         n = int(np.prod(shape))
@@ -240,7 +254,8 @@ def derived(batch, graph):
 # ---------------------------------------------------------------------------
 
 def forward(hp: HParams, batch, graph, params):
-    """Returns (energy [S], forces [N,3], stress [S,3,3], cache)."""
+    """Returns (energy [S], forces [N,3], stress [S,3,3], cache); with the
+    magnetic-moment head, cache["magmom"] holds the moments [N]."""
     P = unpack(hp, np.asarray(params, dtype=np.float64))
     g = derived(batch, graph)
     d, T = hp.d, hp.n_layers
@@ -267,19 +282,25 @@ def forward(hp: HParams, batch, graph, params):
         phiv, zv = gated_mlp(fv, P, pre + "av_", d)
         m = seg_sum(ea * phiv, src, N)
         v_new = v + m @ P[pre + "av_Wo"] + P[pre + "av_bo"]
-        # Eq. (5), (6) with the Eq. (11) inputs (all layer-t features)
-        fa = np.concatenate([v[ctr], e[be[b1]], e[be[b2]], a], axis=1)
+        # Eq. (5): bond conv on [v_i, e_ij, e_ik, a_ijk], v = v^t under
+        # Eq. (11), v^{t+1} under Eq. (10)
+        vb = v_new if hp.sequential else v
+        fa = np.concatenate([vb[ctr], e[be[b1]], e[be[b2]], a], axis=1)
         phie, ze = gated_mlp(fa, P, pre + "be_", d)
         ssum = seg_sum(eb[b2] * phie, b1, g["B"])
         mu = eb * ssum
         e_new = e.copy()
         e_new[be] += mu @ P[pre + "be_Wo"] + P[pre + "be_bo"]
-        za, a_new = None, a
+        # Eq. (6): angle update; Eq. (11) reuses the bond-conv input, Eq. (10)
+        # reads v^{t+1} and e^{t+1}
+        za, a_new, fan = None, a, fa
         if t < T - 1:
-            phia, za = gated_mlp(fa, P, pre + "an_", d)
+            if hp.sequential:
+                fan = np.concatenate([v_new[ctr], e_new[be[b1]], e_new[be[b2]], a], axis=1)
+            phia, za = gated_mlp(fan, P, pre + "an_", d)
             a_new = a + phia
         layers.append(dict(v=v, e=e, a=a, fv=fv, zv=zv, phiv=phiv, m=m, fa=fa, ze=ze, phie=phie,
-                           ssum=ssum, mu=mu, za=za))
+                           ssum=ssum, mu=mu, za=za, fan=fan))
         v, e, a = v_new, e_new, a_new
 
     # Energy output (Sec. II-B (4)): sum over atoms of an MLP of v^T
@@ -297,8 +318,14 @@ def forward(hp: HParams, batch, graph, params):
     vol = np.abs(np.linalg.det(g["L"]))
     stress = np.einsum("sab,sax,sby->sxy", Csum, U, U) / vol[:, None, None]
 
+    # Magnetic moments: |v^T w_m + b_m| per atom
+    oM = magmom = None
+    if hp.magmom:
+        oM = (v @ P["M_W"] + P["M_b"])[:, 0]
+        magmom = np.abs(oM)
+
     cache = dict(P=P, g=g, Zidx=Z - 1, rbf_a=rbf_a, rbf_b=rbf_b, ft=ft, ea=ea, eb=eb, layers=layers, vT=v, eT=e,
-                 cE=cE, cF=cF, cSc=cSc, xhat=xhat, U=U, vol=vol)
+                 cE=cE, cF=cF, cSc=cSc, xhat=xhat, U=U, vol=vol, oM=oM, magmom=magmom)
     return energy, forces, stress, cache
 
 
@@ -306,26 +333,51 @@ def forward(hp: HParams, batch, graph, params):
 # Loss.
 # ---------------------------------------------------------------------------
 
-def loss_and_grads(energy, forces, stress, n_per, E_t, F_t, S_t, w=(2.0, 1.5, 0.1)):
-    """Weighted MSE of per-atom energy, forces and stress, and its gradient."""
+def huber(r, delta):
+    """Huber's loss of residuals r: r^2/2 inside [-delta, delta], linear with
+    slope delta outside; and its derivative clip(r, -delta, delta)."""
+    r = np.asarray(r, dtype=np.float64)
+    inside = np.abs(r) <= delta
+    return (np.where(inside, 0.5 * r * r, delta * (np.abs(r) - 0.5 * delta)),
+            np.where(inside, r, delta * np.sign(r)))
+
+
+def _pointwise(r, delta):
+    """(loss, derivative) per residual: squared error, or Huber if delta."""
+    r = np.asarray(r, dtype=np.float64)
+    if delta is None:
+        return r * r, 2.0 * r
+    return huber(r, delta)
+
+
+def loss_and_grads(energy, forces, stress, n_per, E_t, F_t, S_t, w=(2.0, 1.5, 0.1), delta=None):
+    """Weighted mean of per-atom energy, force-component and stress-component
+    errors (squared, or Huber with threshold delta) and its gradient."""
     S = energy.shape[0]
     N = forces.shape[0]
-    re = energy / n_per - E_t
-    rf = forces - F_t
-    rs = stress - S_t
-    loss = w[0] * np.mean(re ** 2) + w[1] * np.mean(rf ** 2) + w[2] * np.mean(rs ** 2)
-    dE = w[0] * 2.0 * re / n_per / S
-    dF = w[1] * 2.0 * rf / (3 * N)
-    dS = w[2] * 2.0 * rs / (9 * S)
+    le, ge = _pointwise(energy / n_per - E_t, delta)
+    lf, gf = _pointwise(forces - F_t, delta)
+    ls, gs = _pointwise(stress - S_t, delta)
+    loss = w[0] * np.mean(le) + w[1] * np.mean(lf) + w[2] * np.mean(ls)
+    dE = w[0] * ge / n_per / S
+    dF = w[1] * gf / (3 * N)
+    dS = w[2] * gs / (9 * S)
     return loss, dE, dF, dS
+
+
+def magmom_loss(magmom, M_t, w=0.1, delta=None):
+    """Weighted mean over atoms of the magnetic-moment error and its gradient."""
+    lm, gm = _pointwise(np.asarray(magmom, dtype=np.float64) - M_t, delta)
+    return w * np.mean(lm), w * gm / magmom.shape[0]
 
 
 # ---------------------------------------------------------------------------
 # Backward (first order, weights only).
 # ---------------------------------------------------------------------------
 
-def backward(hp: HParams, cache, dE, dF, dS):
-    """Gradient of <dE,E> + <dF,F> + <dS,sigma> w.r.t. every parameter (flat)."""
+def backward(hp: HParams, cache, dE, dF, dS, dM=None):
+    """Gradient of <dE,E> + <dF,F> + <dS,sigma> (+ <dM,magmom>) w.r.t. every
+    parameter (flat)."""
     P, g = cache["P"], cache["g"]
     d, T = hp.d, hp.n_layers
     N, S, B = g["N"], g["S"], g["B"]
@@ -339,6 +391,11 @@ def backward(hp: HParams, cache, dE, dF, dS):
     dv = mlp3_backward(dE[g["struct"]][:, None], cache["vT"], cache["cE"], P, "E", G)
     dC = np.einsum("sxy,sax,sby->sab", dS, cache["U"], cache["U"]) / cache["vol"][:, None, None]
     dv += mlp3_backward(dC.reshape(S, 9)[g["struct"]], cache["vT"], cache["cSc"], P, "S", G)
+    if hp.magmom and dM is not None:
+        gm = np.asarray(dM, dtype=np.float64) * np.sign(cache["oM"])
+        G["M_W"] += cache["vT"].T @ gm[:, None]
+        G["M_b"] += gm.sum()
+        dv += gm[:, None] * P["M_W"][:, 0][None, :]
     dn = (dF[src] * cache["xhat"]).sum(axis=1)
     dm = 0.5 * (dn + dn[g["rev"]])
     de = mlp3_backward(dm[:, None], cache["eT"], cache["cF"], P, "F", G)
@@ -347,17 +404,19 @@ def backward(hp: HParams, cache, dE, dF, dS):
     deb = np.zeros_like(cache["eb"])
     da = None
     ea, eb = cache["ea"], cache["eb"]
+    seq = hp.sequential
     for t in reversed(range(T)):
         pre = "L%d_" % t
         Ls = cache["layers"][t]
-        # residual paths
-        dv_in = dv.copy()
-        de_in = de.copy()
+        # dv, de, da: gradients with respect to v^{t+1}, e^{t+1}, a^{t+1}
         da_in = np.zeros_like(Ls["a"]) if da is None else da.copy()
-        # v' = v + m Wo + bo
-        dmsg = dv @ P[pre + "av_Wo"].T
-        G[pre + "av_Wo"] += Ls["m"].T @ dv
-        G[pre + "av_bo"] += dv.sum(axis=0)
+        if seq and t < T - 1:
+            # Eq. (10): the angle update read v^{t+1} and e^{t+1}
+            dfan = gated_mlp_backward(da, Ls["fan"], Ls["za"], P, pre + "an_", d, G)
+            dv = dv + seg_sum(dfan[:, :d], ctr, N)
+            de = de + seg_sum(dfan[:, d:2 * d], be[b1], g["E"]) + seg_sum(dfan[:, 2 * d:3 * d], be[b2], g["E"])
+            da_in += dfan[:, 3 * d:]
+        de_in = de.copy()
         # e'_b = e_b + mu Wo + bo (bonds only)
         deb_rows = de[be]
         dmu = deb_rows @ P[pre + "be_Wo"].T
@@ -368,12 +427,19 @@ def backward(hp: HParams, cache, dE, dF, dS):
         dphie = dmu[b1] * eb[b1] * eb[b2]
         deb += seg_sum(dmu[b1] * eb[b1] * Ls["phie"], b2, B)
         dfa = gated_mlp_backward(dphie, Ls["fa"], Ls["ze"], P, pre + "be_", d, G)
-        if t < T - 1:
+        if not seq and t < T - 1:
             dfa = dfa + gated_mlp_backward(da, Ls["fa"], Ls["za"], P, pre + "an_", d, G)
-        dv_in += seg_sum(dfa[:, :d], ctr, N)
+        dv_ctr = seg_sum(dfa[:, :d], ctr, N)
+        if seq:
+            dv = dv + dv_ctr  # the bond conv read v^{t+1}
         de_in += seg_sum(dfa[:, d:2 * d], be[b1], g["E"])
         de_in += seg_sum(dfa[:, 2 * d:3 * d], be[b2], g["E"])
         da_in += dfa[:, 3 * d:]
+        # v' = v + m Wo + bo
+        dv_in = dv.copy() if seq else dv + dv_ctr
+        dmsg = dv @ P[pre + "av_Wo"].T
+        G[pre + "av_Wo"] += Ls["m"].T @ dv
+        G[pre + "av_bo"] += dv.sum(axis=0)
         # m_i = sum_e ea_e * phi_v
         dphiv = dmsg[src] * ea
         dea += dmsg[src] * Ls["phiv"]
@@ -412,13 +478,21 @@ def adam(params, grad, m, v, lr, b1, b2, eps, t):
     return params - lr * mhat / (np.sqrt(vhat) + eps), m, v
 
 
-def step(hp: HParams, batch, params, targets, w=(2.0, 1.5, 0.1), graph=None):
-    """Graph build, forward, loss, backward: (loss, grad, outputs)."""
+def step(hp: HParams, batch, params, targets, w=(2.0, 1.5, 0.1), graph=None, delta=None, w_m=0.1):
+    """Graph build, forward, loss, backward: (loss, grad, outputs). targets are
+    (E, F, S) per-atom energy, forces, stress, plus magnetic moments M [N]
+    when the head is on; delta selects the Huber loss; w_m weighs the moments."""
     from . import graph as graph_mod
 
     if graph is None:
         graph = graph_mod.build_graph(batch.atom_ptr, batch.pos, batch.lattice, hp.r_atom, hp.r_bond)
     energy, forces, stress, cache = forward(hp, batch, graph, params)
-    loss, dE, dF, dS = loss_and_grads(energy, forces, stress, cache["g"]["n_per"], *targets, w=w)
-    grad = backward(hp, cache, dE, dF, dS)
-    return loss, grad, (energy, forces, stress), graph
+    loss, dE, dF, dS = loss_and_grads(energy, forces, stress, cache["g"]["n_per"], *targets[:3], w=w, delta=delta)
+    dM = None
+    outputs = (energy, forces, stress)
+    if hp.magmom:
+        lm, dM = magmom_loss(cache["magmom"], targets[3], w_m, delta)
+        loss += lm
+        outputs = outputs + (cache["magmom"],)
+    grad = backward(hp, cache, dE, dF, dS, dM)
+    return loss, grad, outputs, graph

@@ -219,7 +219,7 @@ def random_crystals(seed: int, n_struct: int, n_lo: int, n_hi: int, rho=(0.07, 0
 # this listing is used only to pick each tensor's initial distribution.
 # --------------------------------------------------------------------------
 
-def _param_listing(d: int, T: int, R: int = 31, K: int = 31):
+def _param_listing(d: int, T: int, R: int = 31, K: int = 31, magmom: bool = False):
     out = [("W_Z", (N_ELEMENTS, d), "normal"), ("f_a", (R,), "freq"), ("f_b", (R,), "freq"),
            ("W_e", (R, 2 * d), "fan"), ("b_e0", (d,), "fan:%d" % R), ("W_eb", (R, d), "fan"),
            ("W_th", (K, d), "fan"), ("b_th", (d,), "fan:%d" % K)]
@@ -238,15 +238,17 @@ def _param_listing(d: int, T: int, R: int = 31, K: int = 31):
         out += [(h + "_W1", (d, d), "fan"), (h + "_b1", (d,), "fan:%d" % d),
                 (h + "_W2", (d, d), "fan"), (h + "_b2", (d,), "fan:%d" % d),
                 (h + "_W3", (d, o), "fan"), (h + "_b3", (o,), "fan:%d" % d)]
+    if magmom:
+        out += [("M_W", (d, 1), "fan"), ("M_b", (1,), "fan:%d" % d)]
     return out
 
 
-def make_params(d: int, T: int, seed=(0, 1, 0)) -> np.ndarray:
+def make_params(d: int, T: int, seed=(0, 1, 0), magmom: bool = False) -> np.ndarray:
     """Flat fp32 parameter vector: U(+-1/sqrt(fan_in)) for weights and biases,
     LayerNorm scale 1 and shift 0, element table N(0,1), frequencies n*pi."""
     rng = np.random.default_rng(list(seed))
     chunks = []
-    for _, shape, kind in _param_listing(d, T):
+    for _, shape, kind in _param_listing(d, T, magmom=magmom):
         n = int(np.prod(shape))
         if kind == "normal":
             x = rng.standard_normal(n)
@@ -264,22 +266,25 @@ def make_params(d: int, T: int, seed=(0, 1, 0)) -> np.ndarray:
     return np.concatenate(chunks).astype(np.float32)
 
 
-def make_targets(batch: Batch, seed=(0, 2, 0)):
+def make_targets(batch: Batch, seed=(0, 2, 0), magmom: bool = False):
     """Random targets: per-atom energy N(0,1) per structure, force components
-    N(0,1), stress (M + M^T)/2 with M ~ N(0,1)."""
+    N(0,1), stress (M + M^T)/2 with M ~ N(0,1); with magmom, also magnetic
+    moments |N(0,1)| per atom (drawn after the others)."""
     rng = np.random.default_rng(list(seed))
     S, N = batch.n_struct, batch.n_atoms
     e = rng.standard_normal(S).astype(np.float32)
     f = rng.standard_normal((N, 3)).astype(np.float32)
     m = rng.standard_normal((S, 3, 3))
     s = (0.5 * (m + m.transpose(0, 2, 1))).astype(np.float32)
-    return e, f, s
+    if not magmom:
+        return e, f, s
+    return e, f, s, np.abs(rng.standard_normal(N)).astype(np.float32)
 
 
-def workload_inputs(name: str, rep: int = 0):
+def workload_inputs(name: str, rep: int = 0, magmom: bool = False):
     """(batch, params, targets, d, T) of a named workload."""
     cfg, d, T = WORKLOADS[name]
     batch = make_batch(name, rep)
-    params = make_params(d, T, seed=(cfg, 1, rep))
-    targets = make_targets(batch, seed=(cfg, 2, rep))
+    params = make_params(d, T, seed=(cfg, 1, rep), magmom=magmom)
+    targets = make_targets(batch, seed=(cfg, 2, rep), magmom=magmom)
     return batch, params, targets, d, T
