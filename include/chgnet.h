@@ -28,7 +28,7 @@
  * 31 radial and 31 angular basis functions, envelope exponent p = 8, atom
  * graph cutoff 6 A, bond graph cutoff 3 A. Supported: d in {64, 128},
  * 1 <= T <= 16, 1 <= n_rbf <= 64, n_fourier odd in [1, 63], p in [2, 16],
- * 0 < r_bond <= r_atom <= 20.
+ * 0 < r_bond <= r_atom <= 20, magmom and sequential in {0, 1}.
  */
 #ifndef CHGNET_H
 #define CHGNET_H
@@ -54,7 +54,23 @@ typedef struct {
   int32_t envelope_p; /* polynomial envelope exponent p (8)                 */
   float r_atom;       /* atom-graph cutoff, Angstrom (6)                    */
   float r_bond;       /* bond-graph cutoff, Angstrom (3)                    */
+  int32_t magmom;     /* 1: magnetic-moment head m_i = |v^T_i w_m + b_m|    */
+  int32_t sequential; /* 0: FastCHGNet block, Eq. 11 (bond conv and angle
+                         update read layer-t features); 1: the reference
+                         block of Eq. 10 (bond conv reads v^{t+1}, angle
+                         update reads v^{t+1} and e^{t+1})                  */
 } chgnet_hparams;
+
+/* Loss of chgnet_step (Sec. IV, "Parameters Setting"), host memory. Each term
+ * is a mean over its elements of rho(prediction - target): per-atom energy
+ * E_s/n_s over S crystals, force components over 3N, stress components over
+ * 9S, magnetic moments over N. rho(r) = r^2 if huber_delta <= 0, else Huber's
+ * loss: r^2/2 for |r| <= delta, delta (|r| - delta/2) beyond. The paper's
+ * prefactors are 2, 1.5, 0.1, 0.1 with Huber's loss; its delta is not stated. */
+typedef struct {
+  float w_energy, w_force, w_stress, w_magmom;
+  float huber_delta;
+} chgnet_loss;
 
 /* A batch of S crystals with N atoms in total (Alg. 2: all structures
  * concatenated). Atoms of structure s are atom_ptr[s] .. atom_ptr[s+1]-1. */
@@ -103,8 +119,10 @@ typedef struct {
  *                 g_c, b_c, g_g, b_g [d], Wo [d,d], bo [d]
  *     angle upd.: only if t < T-1: W [4d,2d], b [2d], g_c, b_c, g_g, b_g [d]
  *   heads E, F, S (energy, force, stress), each:
- *     W1 [d,d], b1 [d], W2 [d,d], b2 [d], W3 [d,o], b3 [o], o = 1, 1, 9.
- * d = 64, T = 4, R = K = 31 gives 405,001; d = 128, T = 5 gives 1,975,753. */
+ *     W1 [d,d], b1 [d], W2 [d,d], b2 [d], W3 [d,o], b3 [o], o = 1, 1, 9;
+ *   only if magmom: w_m [d,1], b_m [1].
+ * d = 64, T = 4, R = K = 31 gives 405,001 (405,066 with magmom); d = 128,
+ * T = 5 gives 1,975,753. The layout does not depend on `sequential`. */
 int chgnet_param_count(const chgnet_hparams* hp, int64_t* n);
 
 /* Workspace bytes for a batch of S structures, N atoms and at most E edges,
@@ -124,35 +142,39 @@ int chgnet_workspace_size(const chgnet_hparams* hp, int64_t N, int64_t E, int64_
 int chgnet_build_graph(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_graph* graph, void* ws,
                        size_t ws_bytes, void* stream);
 
-/* Forward pass (Eq. 2-9 with the Eq. 11 inputs): energy [S] (total energy of
- * each crystal), forces [N,3], stress [S,3,3]. `graph` must hold a graph of
- * `batch` (n_edges/n_bonds/n_angles set; angle_b2 may be NULL). If
- * save_for_backward != 0 the activations stay in `ws` for chgnet_backward. */
+/* Forward pass (Eq. 2-9; interaction blocks of Eq. 11, or Eq. 10 if
+ * hp->sequential): energy [S] (total energy of each crystal), forces [N,3],
+ * stress [S,3,3] and, if hp->magmom, magnetic moments magmom [N] (may be NULL
+ * when not wanted; must be NULL without the head). `graph` must hold a graph
+ * of `batch` (n_edges/n_bonds/n_angles set; angle_b2 may be NULL). The
+ * activations always stay in `ws` for chgnet_backward (save_for_backward is
+ * accepted for compatibility and ignored). */
 int chgnet_forward(const chgnet_hparams* hp, const chgnet_batch* batch, const chgnet_graph* graph,
-                   const float* params, float* energy, float* forces, float* stress, int save_for_backward,
-                   void* ws, size_t ws_bytes, void* stream);
+                   const float* params, float* energy, float* forces, float* stress, float* magmom,
+                   int save_for_backward, void* ws, size_t ws_bytes, void* stream);
 
 /* Backward pass for the weights: grad [P] (overwritten) = d/dparams of
- * sum(dE*energy) + sum(dF*forces) + sum(dS*stress), using the activations of
- * the preceding chgnet_forward(save_for_backward=1) on the same ws, batch,
- * graph and params. Positions and lattices are not differentiated. */
+ * sum(dE*energy) + sum(dF*forces) + sum(dS*stress) (+ sum(dM*magmom) with
+ * the head; dM [N] may be NULL, meaning zero; it must be NULL without the
+ * head), using the activations of the preceding chgnet_forward on the same ws,
+ * batch, graph and params. Positions and lattices are not differentiated.
+ * d|x|/dx is taken as 0 at x = 0. */
 int chgnet_backward(const chgnet_hparams* hp, const chgnet_batch* batch, const chgnet_graph* graph,
-                    const float* params, const float* dE, const float* dF, const float* dS, float* grad, void* ws,
-                    size_t ws_bytes, void* stream);
+                    const float* params, const float* dE, const float* dF, const float* dS, const float* dM,
+                    float* grad, void* ws, size_t ws_bytes, void* stream);
 
-/* One training step: build graph, forward, loss, backward, optional Adam.
- * Loss = w0 * mean_s (E_s/n_s - E_target_s)^2 + w1 * mean (F - F_target)^2
- *      + w2 * mean (stress - S_target)^2, loss_w = {w0, w1, w2} on the HOST
- * (the paper's prefactors are 2, 1.5, 0.1). E_target [S] is per atom.
- * loss [1] is a device scalar. If adam_hp (HOST array {lr, beta1, beta2, eps,
- * t}, t >= 1 the step number) is non-NULL, params, adam_m and adam_v [P] are
- * updated in place by bias-corrected Adam; otherwise params are unchanged and
- * adam_m / adam_v may be NULL. energy/forces/stress outputs are not returned
- * (use chgnet_forward). Errors as for chgnet_build_graph. */
+/* One training step: build graph, forward, loss (chgnet_loss, HOST), backward,
+ * optional Adam. E_target [S] is per atom, F_target [N,3], S_target [S,3,3],
+ * M_target [N] magnetic moments (required with the head, must be NULL
+ * without it). loss [1] is a device scalar. If adam_hp (HOST array {lr,
+ * beta1, beta2, eps, t}, t >= 1 the step number) is non-NULL, params, adam_m
+ * and adam_v [P] are updated in place by bias-corrected Adam; otherwise
+ * params are unchanged and adam_m / adam_v may be NULL. The predictions are
+ * not returned (use chgnet_forward). Errors as for chgnet_build_graph. */
 int chgnet_step(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_graph* graph, float* params,
-                const float* E_target, const float* F_target, const float* S_target, const float* loss_w,
-                float* loss, float* grad, float* adam_m, float* adam_v, const float* adam_hp, void* ws,
-                size_t ws_bytes, void* stream);
+                const float* E_target, const float* F_target, const float* S_target, const float* M_target,
+                const chgnet_loss* loss_cfg, float* loss, float* grad, float* adam_m, float* adam_v,
+                const float* adam_hp, void* ws, size_t ws_bytes, void* stream);
 
 /* Text of the last error on the calling thread ("" if none). */
 const char* chgnet_last_error_string(void);

@@ -31,7 +31,12 @@ class ChgnetError(RuntimeError):
 class HParams(ctypes.Structure):
     _fields_ = [("d", ctypes.c_int32), ("n_layers", ctypes.c_int32), ("n_rbf", ctypes.c_int32),
                 ("n_fourier", ctypes.c_int32), ("envelope_p", ctypes.c_int32), ("r_atom", ctypes.c_float),
-                ("r_bond", ctypes.c_float)]
+                ("r_bond", ctypes.c_float), ("magmom", ctypes.c_int32), ("sequential", ctypes.c_int32)]
+
+
+class LossCfg(ctypes.Structure):
+    _fields_ = [("w_energy", ctypes.c_float), ("w_force", ctypes.c_float), ("w_stress", ctypes.c_float),
+                ("w_magmom", ctypes.c_float), ("huber_delta", ctypes.c_float)]
 
 
 class CBatch(ctypes.Structure):
@@ -60,11 +65,11 @@ def lib():
         L.chgnet_build_graph.argtypes = [ctypes.POINTER(HParams), ctypes.POINTER(CBatch), ctypes.POINTER(CGraph), vp,
                                          ctypes.c_size_t, vp]
         L.chgnet_forward.argtypes = [ctypes.POINTER(HParams), ctypes.POINTER(CBatch), ctypes.POINTER(CGraph), vp, vp,
-                                     vp, vp, ctypes.c_int, vp, ctypes.c_size_t, vp]
+                                     vp, vp, vp, ctypes.c_int, vp, ctypes.c_size_t, vp]
         L.chgnet_backward.argtypes = [ctypes.POINTER(HParams), ctypes.POINTER(CBatch), ctypes.POINTER(CGraph), vp, vp,
-                                      vp, vp, vp, vp, ctypes.c_size_t, vp]
+                                      vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
         L.chgnet_step.argtypes = [ctypes.POINTER(HParams), ctypes.POINTER(CBatch), ctypes.POINTER(CGraph), vp, vp, vp,
-                                  vp, ctypes.POINTER(ctypes.c_float), vp, vp, vp, vp, ctypes.POINTER(ctypes.c_float),
+                                  vp, vp, ctypes.POINTER(LossCfg), vp, vp, vp, vp, ctypes.POINTER(ctypes.c_float),
                                   vp, ctypes.c_size_t, vp]
         L.chgnet_last_error_string.restype = ctypes.c_char_p
         L.chgnet_profile_start.argtypes = [ctypes.c_int]
@@ -81,8 +86,9 @@ def _check(code):
         raise ChgnetError(code, lib().chgnet_last_error_string().decode())
 
 
-def hparams(d=64, n_layers=4, n_rbf=31, n_fourier=31, envelope_p=8, r_atom=6.0, r_bond=3.0) -> HParams:
-    return HParams(d, n_layers, n_rbf, n_fourier, envelope_p, r_atom, r_bond)
+def hparams(d=64, n_layers=4, n_rbf=31, n_fourier=31, envelope_p=8, r_atom=6.0, r_bond=3.0, magmom=False,
+            sequential=False) -> HParams:
+    return HParams(d, n_layers, n_rbf, n_fourier, envelope_p, r_atom, r_bond, int(magmom), int(sequential))
 
 
 def param_count(hp: HParams) -> int:
@@ -242,39 +248,49 @@ def ensure_ws(hp, batch, graph, ws):
 
 
 def forward(hp, batch, graph, params, ws, save_for_backward=True):
+    """(energy, forces, stress), plus magnetic moments with the head."""
     ensure_ws(hp, batch, graph, ws)
     dev = batch.pos.device
     S, N = batch.n_struct, batch.n_atoms
     energy = torch.empty(S, dtype=torch.float32, device=dev)
     forces = torch.empty(N, 3, dtype=torch.float32, device=dev)
     stress = torch.empty(S, 3, 3, dtype=torch.float32, device=dev)
+    magmom = torch.empty(N, dtype=torch.float32, device=dev) if hp.magmom else None
     cb, cg = batch.c(), graph.c()
     _check(lib().chgnet_forward(ctypes.byref(hp), ctypes.byref(cb), ctypes.byref(cg), _ptr(params), _ptr(energy),
-                                _ptr(forces), _ptr(stress), int(save_for_backward), ws.ptr, ws.nbytes, _stream(dev)))
+                                _ptr(forces), _ptr(stress), _ptr(magmom), int(save_for_backward), ws.ptr, ws.nbytes,
+                                _stream(dev)))
+    if hp.magmom:
+        return energy, forces, stress, magmom
     return energy, forces, stress
 
 
-def backward(hp, batch, graph, params, dE, dF, dS, ws, grad=None):
+def backward(hp, batch, graph, params, dE, dF, dS, ws, grad=None, dM=None):
     dev = batch.pos.device
     if grad is None:
         grad = torch.empty_like(params)
     cb, cg = batch.c(), graph.c()
     _check(lib().chgnet_backward(ctypes.byref(hp), ctypes.byref(cb), ctypes.byref(cg), _ptr(params),
-                                 _ptr(dE.contiguous()), _ptr(dF.contiguous()), _ptr(dS.contiguous()), _ptr(grad),
-                                 ws.ptr, ws.nbytes, _stream(dev)))
+                                 _ptr(dE.contiguous()), _ptr(dF.contiguous()), _ptr(dS.contiguous()),
+                                 _ptr(None if dM is None else dM.contiguous()), _ptr(grad), ws.ptr, ws.nbytes,
+                                 _stream(dev)))
     return grad
 
 
-def step(hp, batch, graph, params, targets, ws, loss_w=(2.0, 1.5, 0.1), grad=None, loss=None, adam=None):
-    """One training step. targets = (E_target [S], F_target [N,3], S_target [S,3,3]) device tensors.
-    adam = (m, v, (lr, b1, b2, eps, t)) or None. Returns (loss, grad)."""
+def step(hp, batch, graph, params, targets, ws, loss_w=(2.0, 1.5, 0.1, 0.1), huber_delta=0.0, grad=None, loss=None,
+         adam=None):
+    """One training step. targets = (E_target [S], F_target [N,3], S_target [S,3,3]) device tensors, plus
+    M_target [N] with the magnetic-moment head. loss_w = energy, force, stress (, magmom) prefactors;
+    huber_delta > 0 selects Huber's loss. adam = (m, v, (lr, b1, b2, eps, t)) or None. Returns (loss, grad)."""
     dev = batch.pos.device
     ensure_ws(hp, batch, graph, ws)
     if grad is None:
         grad = torch.empty_like(params)
     if loss is None:
         loss = torch.empty(1, dtype=torch.float32, device=dev)
-    lw = (ctypes.c_float * 3)(*loss_w)
+    w = tuple(loss_w) + (0.0,) * (4 - len(loss_w))
+    lw = LossCfg(w[0], w[1], w[2], w[3], huber_delta)
+    mt = targets[3] if hp.magmom else None
     m = v = None
     ahp = None
     if adam is not None:
@@ -284,8 +300,8 @@ def step(hp, batch, graph, params, targets, ws, loss_w=(2.0, 1.5, 0.1), grad=Non
     for _ in range(2):
         cg = graph.c()
         code = lib().chgnet_step(ctypes.byref(hp), ctypes.byref(cb), ctypes.byref(cg), _ptr(params),
-                                 _ptr(targets[0]), _ptr(targets[1]), _ptr(targets[2]), lw, _ptr(loss), _ptr(grad),
-                                 _ptr(m), _ptr(v), ahp, ws.ptr, ws.nbytes, _stream(dev))
+                                 _ptr(targets[0]), _ptr(targets[1]), _ptr(targets[2]), _ptr(mt), ctypes.byref(lw),
+                                 _ptr(loss), _ptr(grad), _ptr(m), _ptr(v), ahp, ws.ptr, ws.nbytes, _stream(dev))
         graph.take_counts(cg)
         if code == CHGNET_ECAPACITY:
             graph.resize(int(cg.n_edges * 1.25) + 64, int(cg.n_bonds * 1.25) + 64, int(cg.n_angles * 1.25) + 64, dev)

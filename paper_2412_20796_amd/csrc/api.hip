@@ -15,13 +15,15 @@ size_t acts_bytes(const chgnet_hparams& hp, int64_t N, int64_t E, int64_t B, int
 int build_graph(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_graph* graph, void* ws, size_t ws_bytes,
                 hipStream_t st);
 int forward_entry(const chgnet_hparams* hp, const chgnet_batch* batch, const chgnet_graph* graph, const float* params,
-                  float* energy, float* forces, float* stress, void* ws, size_t ws_bytes, hipStream_t st);
+                  float* energy, float* forces, float* stress, float* magmom, void* ws, size_t ws_bytes,
+                  hipStream_t st);
 int backward_entry(const chgnet_hparams* hp, const chgnet_batch* batch, const chgnet_graph* graph, const float* params,
-                   const float* dE, const float* dF, const float* dS, float* grad, void* ws, size_t ws_bytes,
-                   hipStream_t st);
+                   const float* dE, const float* dF, const float* dS, const float* dM, float* grad, void* ws,
+                   size_t ws_bytes, hipStream_t st);
 int step_entry(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_graph* graph, float* params,
-               const float* E_t, const float* F_t, const float* S_t, const float* loss_w, float* loss, float* grad,
-               float* adam_m, float* adam_v, const float* adam_hp, void* ws, size_t ws_bytes, hipStream_t st);
+               const float* E_t, const float* F_t, const float* S_t, const float* M_t, const chgnet_loss* loss_cfg,
+               float* loss, float* grad, float* adam_m, float* adam_v, const float* adam_hp, void* ws,
+               size_t ws_bytes, hipStream_t st);
 
 namespace {
 thread_local std::string g_last_error;
@@ -47,7 +49,7 @@ int prof_mark(hipStream_t st) {
 
 void prof_close(hipStream_t st, int first, const char* tag) {
   if (first < 0) return;
-  hipEventRecord(g_prof.ev[first + 1], st);
+  (void)hipEventRecord(g_prof.ev[first + 1], st);
   g_prof.recs.push_back({tag, first, first + 1});
 }
 
@@ -67,6 +69,8 @@ int validate_hparams(const chgnet_hparams* hp) {
   if (hp->envelope_p < 2 || hp->envelope_p > 16) return fail(CHGNET_EINVAL, "envelope_p must be in 2..16");
   if (!(hp->r_bond > 0.f) || !(hp->r_bond <= hp->r_atom) || !(hp->r_atom <= 20.f))
     return fail(CHGNET_EINVAL, "cutoffs must satisfy 0 < r_bond <= r_atom <= 20");
+  if ((hp->magmom != 0 && hp->magmom != 1) || (hp->sequential != 0 && hp->sequential != 1))
+    return fail(CHGNET_EINVAL, "magmom and sequential must be 0 or 1");
   return CHGNET_OK;
 }
 
@@ -124,6 +128,11 @@ ParamLayout make_layout(const chgnet_hparams& hp, int align) {
     ho.W3 = take(d * ho.out);
     ho.b3 = take(ho.out);
   }
+  L.M_W = L.M_b = -1;
+  if (hp.magmom) {
+    L.M_W = take(d);
+    L.M_b = take(1);
+  }
   L.total = off;
   return L;
 }
@@ -153,25 +162,26 @@ int chgnet_build_graph(const chgnet_hparams* hp, const chgnet_batch* batch, chgn
 }
 
 int chgnet_forward(const chgnet_hparams* hp, const chgnet_batch* batch, const chgnet_graph* graph, const float* params,
-                   float* energy, float* forces, float* stress, int save_for_backward, void* ws, size_t ws_bytes,
-                   void* stream) {
+                   float* energy, float* forces, float* stress, float* magmom, int save_for_backward, void* ws,
+                   size_t ws_bytes, void* stream) {
   (void)save_for_backward;  // activations are always kept in ws
-  return chg::forward_entry(hp, batch, graph, params, energy, forces, stress, ws, ws_bytes,
+  return chg::forward_entry(hp, batch, graph, params, energy, forces, stress, magmom, ws, ws_bytes,
                             static_cast<hipStream_t>(stream));
 }
 
 int chgnet_backward(const chgnet_hparams* hp, const chgnet_batch* batch, const chgnet_graph* graph, const float* params,
-                    const float* dE, const float* dF, const float* dS, float* grad, void* ws, size_t ws_bytes,
-                    void* stream) {
-  return chg::backward_entry(hp, batch, graph, params, dE, dF, dS, grad, ws, ws_bytes, static_cast<hipStream_t>(stream));
+                    const float* dE, const float* dF, const float* dS, const float* dM, float* grad, void* ws,
+                    size_t ws_bytes, void* stream) {
+  return chg::backward_entry(hp, batch, graph, params, dE, dF, dS, dM, grad, ws, ws_bytes,
+                             static_cast<hipStream_t>(stream));
 }
 
 int chgnet_step(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_graph* graph, float* params,
-                const float* E_target, const float* F_target, const float* S_target, const float* loss_w, float* loss,
-                float* grad, float* adam_m, float* adam_v, const float* adam_hp, void* ws, size_t ws_bytes,
-                void* stream) {
-  return chg::step_entry(hp, batch, graph, params, E_target, F_target, S_target, loss_w, loss, grad, adam_m, adam_v,
-                         adam_hp, ws, ws_bytes, static_cast<hipStream_t>(stream));
+                const float* E_target, const float* F_target, const float* S_target, const float* M_target,
+                const chgnet_loss* loss_cfg, float* loss, float* grad, float* adam_m, float* adam_v,
+                const float* adam_hp, void* ws, size_t ws_bytes, void* stream) {
+  return chg::step_entry(hp, batch, graph, params, E_target, F_target, S_target, M_target, loss_cfg, loss, grad,
+                         adam_m, adam_v, adam_hp, ws, ws_bytes, static_cast<hipStream_t>(stream));
 }
 
 const char* chgnet_last_error_string(void) { return chg::g_last_error.c_str(); }

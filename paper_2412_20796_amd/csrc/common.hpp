@@ -96,6 +96,7 @@ struct ParamLayout {
   int64_t W_Z, f_a, f_b, W_e, b_e0, W_eb, W_th, b_th;
   LayerOffsets layer[kMaxLayers];
   HeadOffsets head[3];  // E, F, S
+  int64_t M_W, M_b;     // magnetic-moment head (-1 without it)
   int64_t total;
   int ntensors;                 // every tensor in layout order
   int64_t toff[kMaxTensors], tlen[kMaxTensors];

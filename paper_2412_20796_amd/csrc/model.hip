@@ -847,11 +847,12 @@ __global__ void __launch_bounds__(256) k_segsum(SegJobs J) {
 }
 
 // Per bond b (centre i, local index q among k bonds): DZ1 = sum over the
-// angles (b, *) of dz, DZ2 = sum over the angles (*, b) of dz, and
-// d eb_b += dmu_b * S_b + sum over the angles (*, b) of t2. One wavefront per
-// bond; a lane owns CPL consecutive dz columns and TPL t2 columns; two
-// independent accumulators per sum (fixed order).
-template <int CPL, int TPL>
+// angles (b, *) of dz, DZ2 = sum over the angles (*, b) of dz, and, if DEB,
+// d eb_b += dmu_b * S_b + sum over the angles (*, b) of t2. One
+// wavefront per bond; a lane owns CPL consecutive dz columns (dz rows have
+// 4d floats, DZ12 rows 8d: DZ1 at column c, DZ2 at 4d + c) and TPL t2
+// columns; two independent accumulators per sum (fixed order).
+template <int CPL, int TPL, bool DEB>
 __global__ void __launch_bounds__(256) k_bond_bwd_reduce(int B, int D, const int* __restrict__ bond_src,
                                                          const int* __restrict__ bond_ptr, const int* __restrict__ angle_ptr,
                                                          const float* __restrict__ dzae, const float* __restrict__ t2,
@@ -890,14 +891,16 @@ __global__ void __launch_bounds__(256) k_bond_bwd_reduce(int B, int D, const int
     const int64_t al = angle_ptr[k0 + p] + (q < p ? q : q - 1);
 #pragma unroll
     for (int x = 0; x < CPL; ++x) s2[u][x] += dzae[al * ld + c + x];
+    if (DEB)
 #pragma unroll
-    for (int x = 0; x < TPL; ++x) tt[u][x] += t2[al * D + lane * TPL + x];
+      for (int x = 0; x < TPL; ++x) tt[u][x] += t2[al * D + lane * TPL + x];
   }
 #pragma unroll
   for (int x = 0; x < CPL; ++x) {
     DZ12[(int64_t)b * 8 * D + c + x] = s1[0][x] + s1[1][x];
     DZ12[(int64_t)b * 8 * D + 4 * D + c + x] = s2[0][x] + s2[1][x];
   }
+  if (!DEB) return;
 #pragma unroll
   for (int x = 0; x < TPL; ++x) {
     const int64_t o = (int64_t)b * D + lane * TPL + x;
@@ -975,42 +978,96 @@ __global__ void __launch_bounds__(256) k_forces(int N, const int* __restrict__ e
   }
 }
 
-// Loss (weighted MSE, per-atom energy) and its gradient; one block.
+// Magnetic moments: o_i = v_i . w_m + b_m, m_i = |o_i| (mag may be NULL); one
+// wavefront per atom, fixed-order wave reduction. o is kept for the loss and
+// the backward.
+__global__ void __launch_bounds__(256) k_magmom(int N, int D, const float* __restrict__ v, const float* __restrict__ w,
+                                                const float* __restrict__ b, float* __restrict__ om,
+                                                float* __restrict__ mag) {
+  const int i = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (i >= N) return;
+  float s = 0.f;
+  for (int c = lane; c < D; c += 64) s += v[(int64_t)i * D + c] * w[c];
+  s = wsum(s);
+  if (lane == 0) {
+    const float o = s + b[0];
+    om[i] = o;
+    if (mag) mag[i] = fabsf(o);
+  }
+}
+
+// g_i = dM_i sign(o_i) (sign(0) = 0); dv_i += g_i w_m.
+__global__ void __launch_bounds__(256) k_magmom_bwd(int N, int D, const float* __restrict__ dM, const float* __restrict__ om,
+                                                    const float* __restrict__ w, float* __restrict__ g,
+                                                    float* __restrict__ dv) {
+  const int i = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (i >= N) return;
+  const float o = om[i];
+  const float gi = o > 0.f ? dM[i] : o < 0.f ? -dM[i] : 0.f;
+  if (lane == 0) g[i] = gi;
+  for (int c = lane; c < D; c += 64) dv[(int64_t)i * D + c] += gi * w[c];
+}
+
+// Per-residual loss and derivative: squared error, or Huber's loss with
+// threshold delta > 0 (r^2/2 inside [-delta, delta], linear beyond).
+__device__ __forceinline__ double rho(double r, double delta, double& g) {
+  if (delta <= 0.0) {
+    g = 2.0 * r;
+    return r * r;
+  }
+  if (fabs(r) <= delta) {
+    g = r;
+    return 0.5 * r * r;
+  }
+  g = r > 0.0 ? delta : -delta;
+  return delta * (fabs(r) - 0.5 * delta);
+}
+
+// Loss (weighted mean errors, per-atom energy) and its gradient; one block,
+// fp64 accumulation in a fixed order.
 __global__ void __launch_bounds__(256) k_loss(int S, int N, const int* __restrict__ atom_ptr, const float* __restrict__ energy,
                                               const float* __restrict__ forces, const float* __restrict__ stress,
-                                              const float* __restrict__ Et, const float* __restrict__ Ft,
-                                              const float* __restrict__ St, float w0, float w1, float w2,
-                                              float* __restrict__ loss, float* __restrict__ dE, float* __restrict__ dF,
-                                              float* __restrict__ dS) {
-  __shared__ double red[3][256];
-  double le = 0.0, lf = 0.0, ls = 0.0;
+                                              const float* __restrict__ om, const float* __restrict__ Et,
+                                              const float* __restrict__ Ft, const float* __restrict__ St,
+                                              const float* __restrict__ Mt, chgnet_loss lw, float* __restrict__ loss,
+                                              float* __restrict__ dE, float* __restrict__ dF, float* __restrict__ dS,
+                                              float* __restrict__ dM) {
+  __shared__ double red[4][256];
+  const double delta = lw.huber_delta;
+  double le = 0.0, lf = 0.0, ls = 0.0, lm = 0.0, g;
   for (int s = threadIdx.x; s < S; s += 256) {
     const double n = (double)(atom_ptr[s + 1] - atom_ptr[s]);
-    const double r = (double)energy[s] / n - (double)Et[s];
-    le += r * r;
-    dE[s] = (float)(w0 * 2.0 * r / n / S);
+    le += rho((double)energy[s] / n - (double)Et[s], delta, g);
+    dE[s] = (float)(lw.w_energy * g / n / S);
   }
   for (int k = threadIdx.x; k < 3 * N; k += 256) {
-    const double r = (double)forces[k] - (double)Ft[k];
-    lf += r * r;
-    dF[k] = (float)(w1 * 2.0 * r / (3.0 * N));
+    lf += rho((double)forces[k] - (double)Ft[k], delta, g);
+    dF[k] = (float)(lw.w_force * g / (3.0 * N));
   }
   for (int k = threadIdx.x; k < 9 * S; k += 256) {
-    const double r = (double)stress[k] - (double)St[k];
-    ls += r * r;
-    dS[k] = (float)(w2 * 2.0 * r / (9.0 * S));
+    ls += rho((double)stress[k] - (double)St[k], delta, g);
+    dS[k] = (float)(lw.w_stress * g / (9.0 * S));
   }
+  if (om)
+    for (int k = threadIdx.x; k < N; k += 256) {
+      lm += rho(fabs((double)om[k]) - (double)Mt[k], delta, g);
+      dM[k] = (float)(lw.w_magmom * g / N);
+    }
   red[0][threadIdx.x] = le;
   red[1][threadIdx.x] = lf;
   red[2][threadIdx.x] = ls;
+  red[3][threadIdx.x] = lm;
   __syncthreads();
   for (int off = 128; off > 0; off >>= 1) {
     if ((int)threadIdx.x < off)
-      for (int k = 0; k < 3; ++k) red[k][threadIdx.x] += red[k][threadIdx.x + off];
+      for (int k = 0; k < 4; ++k) red[k][threadIdx.x] += red[k][threadIdx.x + off];
     __syncthreads();
   }
-  if (threadIdx.x == 0)
-    loss[0] = (float)(w0 * red[0][0] / S + w1 * red[1][0] / (3.0 * N) + w2 * red[2][0] / (9.0 * S));
+  if (threadIdx.x == 0) {
+    double l = lw.w_energy * red[0][0] / S + lw.w_force * red[1][0] / (3.0 * N) + lw.w_stress * red[2][0] / (9.0 * S);
+    if (om) l += lw.w_magmom * red[3][0] / N;
+    loss[0] = (float)l;
+  }
 }
 
 // Upstream gradients of the head outputs.
@@ -1126,7 +1183,8 @@ struct Acts {
   float* a[kMaxLayers];
   float *zv[kMaxLayers], *zae[kMaxLayers], *m[kMaxLayers], *ssum[kMaxLayers], *mu[kMaxLayers];
   float *msg, *msgb, *Xa[kMaxLayers], *Xb[kMaxLayers];
-  float *hE1, *aE1, *hE2, *aE2, *hS1, *aS1, *hS2, *aS2, *hF1, *aF1, *hF2, *aF2, *oE, *oS, *oF;
+  float *hE1, *aE1, *hE2, *aE2, *hS1, *aS1, *hS2, *aS2, *hF1, *aF1, *hF2, *aF2, *oE, *oS, *oF, *oM, *gM;
+  float* dvf;  // gradient of v^{t+1} including the sequential block's bond and angle inputs
   // backward
   float *dv[2], *de[2], *da[2], *dm, *dmu, *dzv, *dzae, *t2, *AT, *DZ12, *dea, *deb;
   float *doE, *doS, *dn, *doF, *dh2E, *dh2S, *dh2F, *dh1ES, *dh1F, *drbf_a, *drbf_b;
@@ -1135,7 +1193,7 @@ struct Acts {
   int64_t lnpart_stride;
   int64_t tnpart_cap;
   // loss
-  float *dE, *dF, *dS, *out_E, *out_F, *out_S;
+  float *dE, *dF, *dS, *dM, *out_E, *out_F, *out_S, *out_M;
 };
 
 void carve_acts(Arena& ar, const Dims& m, Acts& a, int64_t n_params_aligned) {
@@ -1179,6 +1237,9 @@ void carve_acts(Arena& ar, const Dims& m, Acts& a, int64_t n_params_aligned) {
   a.oE = ar.take<float>(N);
   a.oS = ar.take<float>(N * 9);
   a.oF = ar.take<float>(E);
+  a.oM = ar.take<float>(N);
+  a.gM = ar.take<float>(N);
+  a.dvf = ar.take<float>(N * D);
   for (int k = 0; k < 2; ++k) {
     a.dv[k] = ar.take<float>(N * D);
     a.de[k] = ar.take<float>(E * D);
@@ -1214,9 +1275,11 @@ void carve_acts(Arena& ar, const Dims& m, Acts& a, int64_t n_params_aligned) {
   a.dE = ar.take<float>(S);
   a.dF = ar.take<float>(3 * N);
   a.dS = ar.take<float>(9 * S);
+  a.dM = ar.take<float>(N);
   a.out_E = ar.take<float>(S);
   a.out_F = ar.take<float>(3 * N);
   a.out_S = ar.take<float>(9 * S);
+  a.out_M = ar.take<float>(N);
 }
 
 // ---------------------------------------------------------------------------
@@ -1518,7 +1581,8 @@ int make_ctx(const chgnet_hparams* hp, const chgnet_batch* batch, const chgnet_g
 // ---------------------------------------------------------------------------
 // Forward.
 // ---------------------------------------------------------------------------
-int forward_impl(Ctx& c, const float* Pflat, float* energy, float* forces, float* stress, hipStream_t st) {
+int forward_impl(Ctx& c, const float* Pflat, float* energy, float* forces, float* stress, float* magmom,
+                 hipStream_t st) {
   const Dims& m = c.dm;
   Acts& a = c.a;
   const ParamLayout& L = c.La;
@@ -1568,109 +1632,162 @@ int forward_impl(Ctx& c, const float* Pflat, float* energy, float* forces, float
     CHG_TRY(run_gemms(ps, st, "gemm_embed"));
   }
 
+  const bool seq = c.hp->sequential != 0;
   for (int t = 0; t < m.T; ++t) {
     const LayerOffsets& lo = L.layer[t];
     const bool ang = lo.has_angle;
     const float* Wav = P + lo.av.W;
     const float* Wbe = P + lo.be.W;
     const float* Wan = P + lo.an.W;
-    // atom and bond terms of the split first linear layers
-    std::vector<GemmProblem> ps;
-    for (int k = 0; k < 4; ++k) {
-      if (k == 3 && !ang) break;
-      const float* W = k == 0 ? Wav : k == 1 ? Wav + D * 2 * D : k == 2 ? Wbe : Wan;
-      GemmProblem p = gp(N, 2 * D, a.Xa[t] + k * 2 * D, 8 * D);
-      seg(p, a.v[t], D, 0, D, W, 2 * D, 0);
-      ps.push_back(p);
-    }
-    CHG_TRY(run_gemms(ps, st, "gemm_proj"));
-    ps.clear();
-    for (int k = 0; k < 4; ++k) {
-      if ((k & 1) && !ang) continue;
-      // k: 0 bond-conv role b1, 1 angle role b1, 2 bond-conv role b2, 3 angle role b2
-      const float* W = (k & 1 ? Wan : Wbe) + (k < 2 ? 1 : 2) * D * 2 * D;
-      GemmProblem p = gp(B, 2 * D, a.Xb[t] + k * 2 * D, 8 * D);
-      p.a_rows = g.bond_edge;
-      seg(p, a.e[t], D, 0, D, W, 2 * D, 0);
-      if (k < 2) {
-        // the centre atom of an angle is the source atom of its first bond:
-        // its term is folded into the first-bond row
-        p.res = a.Xa[t] + (4 + 2 * k) * D;
-        p.res_ld = 8 * D;
-        p.res_rows = a.bond_src;
+    // Atom terms of the split first linear layers, Xa blocks k0..k1-1:
+    // 0 atom conv v_i, 1 atom conv v_j, 2 bond conv centre, 3 angle centre.
+    auto proj_atoms = [&](int k0, int k1, const float* vin) -> int {
+      std::vector<GemmProblem> ps;
+      for (int k = k0; k < k1; ++k) {
+        if (k == 3 && !ang) break;
+        const float* W = k == 0 ? Wav : k == 1 ? Wav + D * 2 * D : k == 2 ? Wbe : Wan;
+        GemmProblem p = gp(N, 2 * D, a.Xa[t] + k * 2 * D, 8 * D);
+        seg(p, vin, D, 0, D, W, 2 * D, 0);
+        ps.push_back(p);
       }
-      ps.push_back(p);
-    }
-    CHG_TRY(run_gemms(ps, st, "gemm_proj"));
-    ps.clear();
+      return run_gemms(ps, st, "gemm_proj");
+    };
+    // Bond terms, Xb blocks in `mask`: 0 bond-conv role b1, 1 angle role b1,
+    // 2 bond-conv role b2, 3 angle role b2.
+    auto proj_bonds = [&](int mask, const float* ein) -> int {
+      std::vector<GemmProblem> ps;
+      for (int k = 0; k < 4; ++k) {
+        if (!((mask >> k) & 1) || ((k & 1) && !ang)) continue;
+        const float* W = (k & 1 ? Wan : Wbe) + (k < 2 ? 1 : 2) * D * 2 * D;
+        GemmProblem p = gp(B, 2 * D, a.Xb[t] + k * 2 * D, 8 * D);
+        p.a_rows = g.bond_edge;
+        seg(p, ein, D, 0, D, W, 2 * D, 0);
+        if (k < 2) {
+          // the centre atom of an angle is the source atom of its first bond:
+          // its term is folded into the first-bond row
+          p.res = a.Xa[t] + (4 + 2 * k) * D;
+          p.res_ld = 8 * D;
+          p.res_rows = a.bond_src;
+        }
+        ps.push_back(p);
+      }
+      return run_gemms(ps, st, "gemm_proj");
+    };
     const GateAdds ad_av = adds(2, a.Xa[t], 8 * D, a.edge_src, a.Xa[t] + 2 * D, 8 * D, g.edge_dst);
     const GateAdds ad_be = adds(2, a.Xb[t], 8 * D, a.ang_b1, a.Xb[t] + 4 * D, 8 * D, a.ang_b2);
     const GateAdds ad_an = adds(2, a.Xb[t] + 2 * D, 8 * D, a.ang_b1, a.Xb[t] + 6 * D, 8 * D, a.ang_b2);
     const float* Wx_av = Wav + 2 * D * 2 * D;  // rows of e_ij
     const float* Wx_be = Wbe + 3 * D * 2 * D;  // rows of a_ijk
     const float* Wx_an = Wan + 3 * D * 2 * D;
-    if (D == 64) {
-      // pre-activations formed inside the gate kernel; z kept for the backward
-      GateMmJobs J{};
-      J.j[J.n++] = mm_job(FWD_ATOM, E, a.e[t], Wx_av, P + lo.av.b, ad_av, ln_ptrs(P, lo.av), a.ea, nullptr, a.msg,
-                          a.zv[t], 2 * D);
-      J.j[J.n++] = mm_job(FWD_BOND, A, a.a[t], Wx_be, P + lo.be.b, ad_be, ln_ptrs(P, lo.be), a.eb, a.ang_b2, a.msgb,
-                          a.zae[t], 4 * D);
-      if (ang)
-        J.j[J.n++] = mm_job(FWD_ANGLE, A, a.a[t], Wx_an, P + lo.an.b, ad_an, ln_ptrs(P, lo.an), a.a[t], nullptr,
-                            a.a[t + 1], a.zae[t] + 2 * D, 4 * D);
-      CHG_TRY(gate_fwd_mm_launch(J, st));
-    } else {
+    // GatedMLPs: bit 0 atom conv, bit 1 bond conv, bit 2 angle update
+    auto gates = [&](int which) -> int {
+      if (!ang) which &= 3;
+      if (D == 64) {
+        // pre-activations formed inside the gate kernel; z kept for the backward
+        GateMmJobs J{};
+        if (which & 1)
+          J.j[J.n++] = mm_job(FWD_ATOM, E, a.e[t], Wx_av, P + lo.av.b, ad_av, ln_ptrs(P, lo.av), a.ea, nullptr, a.msg,
+                              a.zv[t], 2 * D);
+        if (which & 2)
+          J.j[J.n++] = mm_job(FWD_BOND, A, a.a[t], Wx_be, P + lo.be.b, ad_be, ln_ptrs(P, lo.be), a.eb, a.ang_b2,
+                              a.msgb, a.zae[t], 4 * D);
+        if (which & 4)
+          J.j[J.n++] = mm_job(FWD_ANGLE, A, a.a[t], Wx_an, P + lo.an.b, ad_an, ln_ptrs(P, lo.an), a.a[t], nullptr,
+                              a.a[t + 1], a.zae[t] + 2 * D, 4 * D);
+        return gate_fwd_mm_launch(J, st);
+      }
       // edge and angle terms (+ bias) by the GEMM; the gathered atom and bond
       // terms are added by the gate kernels, which stream each row once
-      GemmProblem p = gp(E, 2 * D, a.zv[t], 2 * D);
-      seg(p, a.e[t], D, 0, D, Wx_av, 2 * D, 0);
-      p.bias = P + lo.av.b;
-      ps.push_back(p);
-      for (int k = 0; k < (ang ? 2 : 1); ++k) {
+      std::vector<GemmProblem> ps;
+      if (which & 1) {
+        GemmProblem p = gp(E, 2 * D, a.zv[t], 2 * D);
+        seg(p, a.e[t], D, 0, D, Wx_av, 2 * D, 0);
+        p.bias = P + lo.av.b;
+        ps.push_back(p);
+      }
+      for (int k = 0; k < 2; ++k) {
+        if (!(which & (2 << k))) continue;
         GemmProblem q = gp(A, 2 * D, a.zae[t] + k * 2 * D, 4 * D);
         seg(q, a.a[t], D, 0, D, k ? Wx_an : Wx_be, 2 * D, 0);
         q.bias = P + (k ? lo.an.b : lo.be.b);
         ps.push_back(q);
       }
       CHG_TRY(run_gemms(ps, st, "gemm_z"));
-      ps.clear();
       GateFwdJobs J{};
-      J.j[J.n++] = fwd_job(FWD_ATOM, E, a.zv[t], 2 * D, ad_av, ln_ptrs(P, lo.av), a.ea, nullptr, a.msg);
-      J.j[J.n++] = fwd_job(FWD_BOND, A, a.zae[t], 4 * D, ad_be, ln_ptrs(P, lo.be), a.eb, a.ang_b2, a.msgb);
-      if (ang) J.j[J.n++] = fwd_job(FWD_ANGLE, A, a.zae[t] + 2 * D, 4 * D, ad_an, ln_ptrs(P, lo.an), a.a[t], nullptr, a.a[t + 1]);
-      CHG_TRY(gate_fwd_launch(D, J, st));
-    }
-    {
+      if (which & 1) J.j[J.n++] = fwd_job(FWD_ATOM, E, a.zv[t], 2 * D, ad_av, ln_ptrs(P, lo.av), a.ea, nullptr, a.msg);
+      if (which & 2)
+        J.j[J.n++] = fwd_job(FWD_BOND, A, a.zae[t], 4 * D, ad_be, ln_ptrs(P, lo.be), a.eb, a.ang_b2, a.msgb);
+      if (which & 4)
+        J.j[J.n++] = fwd_job(FWD_ANGLE, A, a.zae[t] + 2 * D, 4 * D, ad_an, ln_ptrs(P, lo.an), a.a[t], nullptr,
+                             a.a[t + 1]);
+      return gate_fwd_launch(D, J, st);
+    };
+    // messages: m_i = sum over out-edges of e^a * phi_v; mu_b = eb_b * sum over
+    // angles (b, b2) of eb_b2 * phi_e
+    auto messages = [&](int which) -> int {
       SegJobs J{};
-      J.j[J.n++] = seg_job(N, g.edge_ptr, nullptr, a.msg, D, D, a.m[t], D);
-      CHG_TRY(segsum_launch(J, 4, st));
-      J = SegJobs{};
-      J.j[J.n++] = seg_job(B, g.angle_ptr, nullptr, a.msgb, D, D, a.ssum[t], D, a.eb, D, a.mu[t], D);
-      CHG_TRY(segsum_launch(J, 1, st));
-    }
+      if (which & 1) {
+        J.j[J.n++] = seg_job(N, g.edge_ptr, nullptr, a.msg, D, D, a.m[t], D);
+        CHG_TRY(segsum_launch(J, 4, st));
+      }
+      if (which & 2) {
+        J = SegJobs{};
+        J.j[J.n++] = seg_job(B, g.angle_ptr, nullptr, a.msgb, D, D, a.ssum[t], D, a.eb, D, a.mu[t], D);
+        CHG_TRY(segsum_launch(J, 1, st));
+      }
+      return CHGNET_OK;
+    };
     // updates: v' = v + m Wo + bo; e' = e (+ mu Wo + bo on bonds)
-    if (E > 0) {
-      const int64_t n4 = E * D / 4;  // d is a multiple of 4 and the arena aligns to 256 B
-      KLAUNCH(st, "k_copy", k_copy4<<<(unsigned)std::min<int64_t>(cdiv(n4, 256), 4096), 256, 0, st>>>(
-                                reinterpret_cast<float4*>(a.e[t + 1]), reinterpret_cast<const float4*>(a.e[t]), n4));
-    }
-    {
-      GemmProblem p = gp(N, D, a.v[t + 1], D);
-      seg(p, a.m[t], D, 0, D, P + lo.av_Wo, D, 0);
-      p.bias = P + lo.av_bo;
-      p.res = a.v[t];
-      p.res_ld = D;
-      ps.push_back(p);
-      p = gp(B, D, a.e[t + 1], D);
-      seg(p, a.mu[t], D, 0, D, P + lo.be_Wo, D, 0);
-      p.bias = P + lo.be_bo;
-      p.res = a.e[t];
-      p.res_ld = D;
-      p.res_rows = g.bond_edge;
-      p.c_rows = g.bond_edge;
-      ps.push_back(p);
-      CHG_TRY(run_gemms(ps, st, "gemm_update"));
+    auto updates = [&](int which) -> int {
+      std::vector<GemmProblem> ps;
+      if (which & 1) {
+        GemmProblem p = gp(N, D, a.v[t + 1], D);
+        seg(p, a.m[t], D, 0, D, P + lo.av_Wo, D, 0);
+        p.bias = P + lo.av_bo;
+        p.res = a.v[t];
+        p.res_ld = D;
+        ps.push_back(p);
+      }
+      if (which & 2) {
+        if (E > 0) {
+          const int64_t n4 = E * D / 4;  // d is a multiple of 4 and the arena aligns to 256 B
+          KLAUNCH(st, "k_copy", k_copy4<<<(unsigned)std::min<int64_t>(cdiv(n4, 256), 4096), 256, 0, st>>>(
+                                    reinterpret_cast<float4*>(a.e[t + 1]), reinterpret_cast<const float4*>(a.e[t]), n4));
+        }
+        GemmProblem p = gp(B, D, a.e[t + 1], D);
+        seg(p, a.mu[t], D, 0, D, P + lo.be_Wo, D, 0);
+        p.bias = P + lo.be_bo;
+        p.res = a.e[t];
+        p.res_ld = D;
+        p.res_rows = g.bond_edge;
+        p.c_rows = g.bond_edge;
+        ps.push_back(p);
+      }
+      return run_gemms(ps, st, "gemm_update");
+    };
+    if (!seq) {
+      // Eq. (11): the three modules read layer-t features and run together
+      CHG_TRY(proj_atoms(0, 4, a.v[t]));
+      CHG_TRY(proj_bonds(15, a.e[t]));
+      CHG_TRY(gates(7));
+      CHG_TRY(messages(3));
+      CHG_TRY(updates(3));
+    } else {
+      // Eq. (10): atom conv, then bond conv on v^{t+1}, then the angle update
+      // on v^{t+1} and e^{t+1}
+      CHG_TRY(proj_atoms(0, 2, a.v[t]));
+      CHG_TRY(gates(1));
+      CHG_TRY(messages(1));
+      CHG_TRY(updates(1));
+      CHG_TRY(proj_atoms(2, 4, a.v[t + 1]));
+      CHG_TRY(proj_bonds(5, a.e[t]));
+      CHG_TRY(gates(2));
+      CHG_TRY(messages(2));
+      CHG_TRY(updates(2));
+      if (ang) {
+        CHG_TRY(proj_bonds(10, a.e[t + 1]));
+        CHG_TRY(gates(4));
+      }
     }
   }
 
@@ -1716,14 +1833,17 @@ int forward_impl(Ctx& c, const float* Pflat, float* energy, float* forces, float
   }
   KLAUNCH(st, "k_struct_heads", k_struct_heads<<<(unsigned)S, 256, 0, st>>>((int)S, bt.atom_ptr, bt.lattice, a.oE, a.oS, energy, stress));
   KLAUNCH(st, "k_forces", k_forces<<<(unsigned)cdiv(N, 4), 256, 0, st>>>((int)N, g.edge_ptr, g.edge_rev, a.oF, a.edge_xhat, forces));
+  if (c.hp->magmom)
+    KLAUNCH(st, "k_magmom", k_magmom<<<(unsigned)cdiv(N, 4), 256, 0, st>>>((int)N, D, a.v[m.T], P + L.M_W, P + L.M_b,
+                                                                            a.oM, magmom));
   return CHGNET_OK;
 }
 
 // ---------------------------------------------------------------------------
 // Backward (weights only).
 // ---------------------------------------------------------------------------
-int backward_impl(Ctx& c, const float* Pflat, bool repack, const float* dE, const float* dF, const float* dS, float* G,
-                  hipStream_t st) {
+int backward_impl(Ctx& c, const float* Pflat, bool repack, const float* dE, const float* dF, const float* dS,
+                  const float* dM, float* G, hipStream_t st) {
   const Dims& m = c.dm;
   Acts& a = c.a;
   const ParamLayout& L = c.La;   // reads from the aligned weight copy
@@ -1789,6 +1909,10 @@ int backward_impl(Ctx& c, const float* Pflat, bool repack, const float* dE, cons
       ps.push_back(p);
       CHG_TRY(run_gemms(ps, st, "gemm_head_bwd0"));
     }
+    const bool mag = c.hp->magmom && dM;
+    if (mag)
+      KLAUNCH(st, "k_magmom_bwd", k_magmom_bwd<<<(unsigned)cdiv(N, 4), 256, 0, st>>>((int)N, D, dM, a.oM, P + L.M_W, a.gM,
+                                                                                      a.dv[cur]));
     std::vector<TnProblem> ts;
     for (auto& l : ls) {
       const int o = l.h->out;
@@ -1804,10 +1928,15 @@ int backward_impl(Ctx& c, const float* Pflat, bool repack, const float* dE, cons
                            G + Lg.head[2].b1));
     ts.push_back(tp(E, D, D, a.e[m.T], D, 0, nullptr, a.dh1F, D, 0, nullptr, G + Lg.head[1].W1, D));
     ts.push_back(tp(E, 1, D, nullptr, 0, 0, nullptr, a.dh1F, D, 0, nullptr, G + Lg.head[1].b1, D));
+    if (mag) {
+      ts.push_back(tp(N, D, 1, a.v[m.T], D, 0, nullptr, a.gM, 1, 0, nullptr, G + Lg.M_W, 1));
+      ts.push_back(tp(N, 1, 1, nullptr, 0, 0, nullptr, a.gM, 1, 0, nullptr, G + Lg.M_b, 1));
+    }
     CHG_TRY(run_tns(ts, a, st, "tn_heads"));
   }
 
   // interaction blocks in reverse
+  const bool seq = c.hp->sequential != 0;
   for (int t = m.T - 1; t >= 0; --t) {
     const LayerOffsets& lo = L.layer[t];
     const LayerOffsets& lg = Lg.layer[t];
@@ -1819,68 +1948,134 @@ int backward_impl(Ctx& c, const float* Pflat, bool repack, const float* dE, cons
     const int nx = 1 - cur;
     std::vector<GemmProblem> ps;
     std::vector<TnProblem> ts;
-    // output linears of the atom and bond updates
-    {
-      GemmProblem p = gp(N, D, a.dm, D);
-      seg(p, a.dv[cur], D, 0, D, P + lo.av_Wo, D, 1);
-      ps.push_back(p);
-      p = gp(B, D, a.dmu, D);
-      p.a_rows = g.bond_edge;
-      seg(p, a.de[cur], D, 0, D, P + lo.be_Wo, D, 1);
-      ps.push_back(p);
-      CHG_TRY(run_gemms(ps, st, "gemm_out_bwd"));
-      ps.clear();
-      ts.push_back(tp(N, D, D, a.m[t], D, 0, nullptr, a.dv[cur], D, 0, nullptr, G + lg.av_Wo, D));
-      ts.push_back(tp(N, 1, D, nullptr, 0, 0, nullptr, a.dv[cur], D, 0, nullptr, G + lg.av_bo, D));
-      ts.push_back(tp(B, D, D, a.mu[t], D, 0, nullptr, a.de[cur], D, 0, g.bond_edge, G + lg.be_Wo, D));
-      ts.push_back(tp(B, 1, D, nullptr, 0, 0, nullptr, a.de[cur], D, 0, g.bond_edge, G + lg.be_bo, D));
-      // launched with the first-layer weight gradients below (inputs unchanged)
-    }
-    // angle gates (bond conv, then angle update)
     const GateAdds ad_av = adds(2, a.Xa[t], 8 * D, a.edge_src, a.Xa[t] + 2 * D, 8 * D, g.edge_dst);
     const GateAdds ad_be = adds(2, a.Xb[t], 8 * D, a.ang_b1, a.Xb[t] + 4 * D, 8 * D, a.ang_b2);
     const GateAdds ad_an = adds(2, a.Xb[t] + 2 * D, 8 * D, a.ang_b1, a.Xb[t] + 6 * D, 8 * D, a.ang_b2);
-    {
+    // GatedMLP backward: bit 0 atom conv, bit 1 bond conv, bit 2 angle update
+    auto gates = [&](int which) -> int {
+      if (!ang) which &= 3;
       GateBwdJobs J{};
-      J.j[J.n++] = bwd_job(BWD_BOND, A, a.zae[t], 4 * D, ad_be, ln_ptrs(P, lo.be), a.dmu, a.ang_b1, a.eb, a.ang_b2, a.t2,
-                           a.dzae, 4 * D);
-      J.j[J.n++] = bwd_job(BWD_ATOM, E, a.zv[t], 2 * D, ad_av, ln_ptrs(P, lo.av), a.dm, a.edge_src, a.ea, nullptr, a.dea,
-                           a.dzv, 2 * D);
-      J.j[J.n - 1].aux_acc = t < m.T - 1;  // the first layer of the backward starts d e^a
-      if (ang)
-        J.j[J.n++] = bwd_job(BWD_ANGLE, A, a.zae[t] + 2 * D, 4 * D, ad_an, ln_ptrs(P, lo.an), a.da[cur], nullptr, nullptr,
-                             nullptr, nullptr, a.dzae + 2 * D, 4 * D);
-      float* lg_out[3] = {G + lg.be.g_c, G + lg.av.g_c, G + lg.an.g_c};
-      CHG_TRY(gate_bwd_launch(D, J, lg_out, a, st));
-    }
-    if (B > 0) {
+      float* lg_out[3];
+      if (which & 2) {
+        lg_out[J.n] = G + lg.be.g_c;
+        J.j[J.n++] = bwd_job(BWD_BOND, A, a.zae[t], 4 * D, ad_be, ln_ptrs(P, lo.be), a.dmu, a.ang_b1, a.eb, a.ang_b2,
+                             a.t2, a.dzae, 4 * D);
+      }
+      if (which & 1) {
+        lg_out[J.n] = G + lg.av.g_c;
+        J.j[J.n++] = bwd_job(BWD_ATOM, E, a.zv[t], 2 * D, ad_av, ln_ptrs(P, lo.av), a.dm, a.edge_src, a.ea, nullptr,
+                             a.dea, a.dzv, 2 * D);
+        J.j[J.n - 1].aux_acc = t < m.T - 1;  // the first layer of the backward starts d e^a
+      }
+      if (which & 4) {
+        lg_out[J.n] = G + lg.an.g_c;
+        J.j[J.n++] = bwd_job(BWD_ANGLE, A, a.zae[t] + 2 * D, 4 * D, ad_an, ln_ptrs(P, lo.an), a.da[cur], nullptr,
+                             nullptr, nullptr, nullptr, a.dzae + 2 * D, 4 * D);
+      }
+      return gate_bwd_launch(D, J, lg_out, a, st);
+    };
+    // per-bond sums of dz over the bond's two angle roles (DZ12) from `ncols`
+    // columns of dzae starting at col0; with_deb also forms d e^b
+    auto bond_reduce = [&](int col0, int ncols, bool with_deb) -> int {
+      if (B <= 0) return CHGNET_OK;
       const unsigned nb = (unsigned)cdiv(B, 4);
-      const int cpl = W4 / 64;
-#define BOND_REDUCE(CPL, TPL)                                                                                    \
-  KLAUNCH(st, "k_bond_bwd_reduce", k_bond_bwd_reduce<CPL, TPL><<<nb, 256, 0, st>>>((int)B, D, a.bond_src, g.bond_ptr, \
-                                                       g.angle_ptr, a.dzae, a.t2, a.dmu, a.ssum[t], a.DZ12, a.deb, \
-                                                       t < m.T - 1))
-      if (cpl == 2) BOND_REDUCE(2, 1);
-      else if (cpl == 4 && D == 64) BOND_REDUCE(4, 1);
-      else if (cpl == 4) BOND_REDUCE(4, 2);
-      else BOND_REDUCE(8, 2);
+      const int cpl = ncols / 64;
+      const float* dz = a.dzae + col0;
+      float* dz12 = a.DZ12 + col0;
+      const int acc = t < m.T - 1;
+#define BOND_REDUCE(CPL, TPL, DEB)                                                                                \
+  KLAUNCH(st, "k_bond_bwd_reduce", k_bond_bwd_reduce<CPL, TPL, DEB><<<nb, 256, 0, st>>>((int)B, D, a.bond_src,      \
+                                     g.bond_ptr, g.angle_ptr, dz, a.t2, a.dmu, a.ssum[t], dz12, a.deb, acc))
+      if (with_deb) {
+        if (cpl == 2) BOND_REDUCE(2, 1, true);
+        else if (cpl == 4 && D == 64) BOND_REDUCE(4, 1, true);
+        else if (cpl == 4) BOND_REDUCE(4, 2, true);
+        else BOND_REDUCE(8, 2, true);
+      } else {
+        if (cpl == 2) BOND_REDUCE(2, 1, false);
+        else BOND_REDUCE(4, 2, false);
+      }
 #undef BOND_REDUCE
+      return CHGNET_OK;
+    };
+    // output linears of the atom and bond updates: dm = dv' Wo^T, dmu = de'_b Wo^T
+    auto out_bwd = [&](const float* dvo, bool atoms, bool bonds) -> int {
+      std::vector<GemmProblem> q;
+      if (atoms) {
+        GemmProblem p = gp(N, D, a.dm, D);
+        seg(p, dvo, D, 0, D, P + lo.av_Wo, D, 1);
+        q.push_back(p);
+      }
+      if (bonds) {
+        GemmProblem p = gp(B, D, a.dmu, D);
+        p.a_rows = g.bond_edge;
+        seg(p, a.de[cur], D, 0, D, P + lo.be_Wo, D, 1);
+        q.push_back(p);
+      }
+      return run_gemms(q, st, "gemm_out_bwd");
+    };
+    SegJobs sj{};
+    if (!seq) {
+      CHG_TRY(out_bwd(a.dv[cur], true, true));
+      CHG_TRY(gates(7));
+      CHG_TRY(bond_reduce(0, W4, true));
+      sj.j[sj.n++] = seg_job(N, g.edge_ptr, nullptr, a.dzv, 2 * D, 2 * D, a.AT, 8 * D);
+      sj.j[sj.n++] = seg_job(N, g.edge_ptr, g.edge_rev, a.dzv, 2 * D, 2 * D, a.AT + 2 * D, 8 * D);
+      sj.j[sj.n++] = seg_job(N, g.bond_ptr, nullptr, a.DZ12, 8 * D, W4, a.AT + 4 * D, 8 * D);
+      CHG_TRY(segsum_launch(sj, 4, st));
+    } else {
+      // Eq. (10), in reverse: the angle update read e^{t+1} (its bond terms
+      // join de', the gradient of e^{t+1}) and v^{t+1}; the bond conv read
+      // v^{t+1}; both centre terms join dvf, the gradient of v^{t+1}, before
+      // the atom conv.
+      if (ang) {
+        CHG_TRY(gates(4));
+        CHG_TRY(bond_reduce(2 * D, 2 * D, false));
+        GemmProblem p = gp(B, D, a.de[cur], D);
+        p.c_rows = g.bond_edge;
+        p.accumulate = 1;
+        seg(p, a.DZ12, 8 * D, 2 * D, 2 * D, Wan + D * 2 * D, 2 * D, 1);
+        seg(p, a.DZ12, 8 * D, 6 * D, 2 * D, Wan + 2 * D * 2 * D, 2 * D, 1);
+        ps.push_back(p);
+        CHG_TRY(run_gemms(ps, st, "gemm_bond_bwd"));
+        ps.clear();
+      }
+      CHG_TRY(out_bwd(nullptr, false, true));
+      CHG_TRY(gates(2));
+      CHG_TRY(bond_reduce(0, 2 * D, true));
+      sj.j[sj.n++] = seg_job(N, g.bond_ptr, nullptr, a.DZ12, 8 * D, W4, a.AT + 4 * D, 8 * D);
+      CHG_TRY(segsum_launch(sj, 4, st));
+      GemmProblem p = gp(N, D, a.dvf, D);
+      seg(p, a.AT, 8 * D, 4 * D, 2 * D, Wbe, 2 * D, 1);
+      if (ang) seg(p, a.AT, 8 * D, 6 * D, 2 * D, Wan, 2 * D, 1);
+      p.res = a.dv[cur];
+      p.res_ld = D;
+      ps.push_back(p);
+      CHG_TRY(run_gemms(ps, st, "gemm_in_bwd"));
+      ps.clear();
+      CHG_TRY(out_bwd(a.dvf, true, false));
+      CHG_TRY(gates(1));
+      sj = SegJobs{};
+      sj.j[sj.n++] = seg_job(N, g.edge_ptr, nullptr, a.dzv, 2 * D, 2 * D, a.AT, 8 * D);
+      sj.j[sj.n++] = seg_job(N, g.edge_ptr, g.edge_rev, a.dzv, 2 * D, 2 * D, a.AT + 2 * D, 8 * D);
+      CHG_TRY(segsum_launch(sj, 4, st));
     }
-    {
-      SegJobs J{};
-      J.j[J.n++] = seg_job(N, g.edge_ptr, nullptr, a.dzv, 2 * D, 2 * D, a.AT, 8 * D);
-      J.j[J.n++] = seg_job(N, g.edge_ptr, g.edge_rev, a.dzv, 2 * D, 2 * D, a.AT + 2 * D, 8 * D);
-      J.j[J.n++] = seg_job(N, g.bond_ptr, nullptr, a.DZ12, 8 * D, W4, a.AT + 4 * D, 8 * D);
-      CHG_TRY(segsum_launch(J, 4, st));
-    }
+    // gradient of v^{t+1} as seen by the atom update
+    const float* dvo = seq ? a.dvf : a.dv[cur];
+    ts.push_back(tp(N, D, D, a.m[t], D, 0, nullptr, dvo, D, 0, nullptr, G + lg.av_Wo, D));
+    ts.push_back(tp(N, 1, D, nullptr, 0, 0, nullptr, dvo, D, 0, nullptr, G + lg.av_bo, D));
+    ts.push_back(tp(B, D, D, a.mu[t], D, 0, nullptr, a.de[cur], D, 0, g.bond_edge, G + lg.be_Wo, D));
+    ts.push_back(tp(B, 1, D, nullptr, 0, 0, nullptr, a.de[cur], D, 0, g.bond_edge, G + lg.be_bo, D));
     // input gradients
     {
       GemmProblem p = gp(N, D, a.dv[nx], D);
       seg(p, a.AT, 8 * D, 0, 2 * D, Wav, 2 * D, 1);
       seg(p, a.AT, 8 * D, 2 * D, 2 * D, Wav + D * 2 * D, 2 * D, 1);
-      seg(p, a.AT, 8 * D, 4 * D, 2 * D, Wbe, 2 * D, 1);
-      if (ang) seg(p, a.AT, 8 * D, 6 * D, 2 * D, Wan, 2 * D, 1);
-      p.res = a.dv[cur];
+      if (!seq) {
+        seg(p, a.AT, 8 * D, 4 * D, 2 * D, Wbe, 2 * D, 1);
+        if (ang) seg(p, a.AT, 8 * D, 6 * D, 2 * D, Wan, 2 * D, 1);
+      }
+      p.res = dvo;
       p.res_ld = D;
       ps.push_back(p);
       p = gp(E, D, a.de[nx], D);
@@ -1903,7 +2098,7 @@ int backward_impl(Ctx& c, const float* Pflat, bool repack, const float* dE, cons
       p.accumulate = 1;
       seg(p, a.DZ12, 8 * D, 0, 2 * D, Wbe + D * 2 * D, 2 * D, 1);
       seg(p, a.DZ12, 8 * D, 4 * D, 2 * D, Wbe + 2 * D * 2 * D, 2 * D, 1);
-      if (ang) {
+      if (ang && !seq) {
         seg(p, a.DZ12, 8 * D, 2 * D, 2 * D, Wan + D * 2 * D, 2 * D, 1);
         seg(p, a.DZ12, 8 * D, 6 * D, 2 * D, Wan + 2 * D * 2 * D, 2 * D, 1);
       }
@@ -1915,24 +2110,43 @@ int backward_impl(Ctx& c, const float* Pflat, bool repack, const float* dE, cons
     {
       const float* vt = a.v[t];
       const float* et = a.e[t];
-      // v^T [dP | dQ | DZa_bond | DZa_angle] -> atom-role blocks of the three first layers
-      ts.push_back(split_out(tp(N, D, (ang ? 8 : 6) * D, vt, D, 0, nullptr, a.AT, 8 * D, 0, nullptr, G + lg.av.W, 2 * D),
-                             2 * D, G + lg.av.W + D * 2 * D, G + lg.be.W, ang ? G + lg.an.W : nullptr));
+      if (!seq) {
+        // v^T [dP | dQ | DZa_bond | DZa_angle] -> atom-role blocks of the three first layers
+        ts.push_back(split_out(tp(N, D, (ang ? 8 : 6) * D, vt, D, 0, nullptr, a.AT, 8 * D, 0, nullptr, G + lg.av.W, 2 * D),
+                               2 * D, G + lg.av.W + D * 2 * D, G + lg.be.W, ang ? G + lg.an.W : nullptr));
+      } else {
+        // the atom conv read v^t; the bond conv and angle update read v^{t+1}
+        ts.push_back(split_out(tp(N, D, 4 * D, vt, D, 0, nullptr, a.AT, 8 * D, 0, nullptr, G + lg.av.W, 2 * D), 2 * D,
+                               G + lg.av.W + D * 2 * D));
+        ts.push_back(split_out(tp(N, D, (ang ? 4 : 2) * D, a.v[t + 1], D, 0, nullptr, a.AT, 8 * D, 4 * D, nullptr,
+                                  G + lg.be.W, 2 * D),
+                               2 * D, ang ? G + lg.an.W : nullptr));
+      }
       ts.push_back(tp(E, D, 2 * D, et, D, 0, nullptr, a.dzv, 2 * D, 0, nullptr, G + lg.av.W + 2 * D * 2 * D, 2 * D));
       // biases: sum over atoms of dP (= sum over edges of dz) and of DZa
       ts.push_back(tp(N, 1, 2 * D, nullptr, 0, 0, nullptr, a.AT, 8 * D, 0, nullptr, G + lg.av.b, 2 * D));
       ts.push_back(split_out(tp(N, 1, (ang ? 4 : 2) * D, nullptr, 0, 0, nullptr, a.AT, 8 * D, 4 * D, nullptr, G + lg.be.b, 2 * D),
                              2 * D, ang ? G + lg.an.b : nullptr));
-      if (ang) {
+      if (ang && !seq) {
         // e_b^T [DZ1_bond | DZ1_angle | DZ2_bond | DZ2_angle]
         ts.push_back(split_out(tp(B, D, 8 * D, et, D, 0, g.bond_edge, a.DZ12, 8 * D, 0, nullptr, G + lg.be.W + D * 2 * D, 2 * D),
                                2 * D, G + lg.an.W + D * 2 * D, G + lg.be.W + 2 * D * 2 * D, G + lg.an.W + 2 * D * 2 * D));
+      } else {
+        ts.push_back(tp(B, D, 2 * D, et, D, 0, g.bond_edge, a.DZ12, 8 * D, 0, nullptr, G + lg.be.W + D * 2 * D, 2 * D));
+        ts.push_back(tp(B, D, 2 * D, et, D, 0, g.bond_edge, a.DZ12, 8 * D, 4 * D, nullptr, G + lg.be.W + 2 * D * 2 * D, 2 * D));
+        if (ang) {
+          // the angle update of Eq. (10) read e^{t+1}
+          const float* et1 = a.e[t + 1];
+          ts.push_back(tp(B, D, 2 * D, et1, D, 0, g.bond_edge, a.DZ12, 8 * D, 2 * D, nullptr, G + lg.an.W + D * 2 * D, 2 * D));
+          ts.push_back(tp(B, D, 2 * D, et1, D, 0, g.bond_edge, a.DZ12, 8 * D, 6 * D, nullptr, G + lg.an.W + 2 * D * 2 * D,
+                          2 * D));
+        }
+      }
+      if (ang) {
         // a^T [dz_bond | dz_angle]
         ts.push_back(split_out(tp(A, D, 4 * D, a.a[t], D, 0, nullptr, a.dzae, 4 * D, 0, nullptr, G + lg.be.W + 3 * D * 2 * D, 2 * D),
                                2 * D, G + lg.an.W + 3 * D * 2 * D));
       } else {
-        ts.push_back(tp(B, D, 2 * D, et, D, 0, g.bond_edge, a.DZ12, 8 * D, 0, nullptr, G + lg.be.W + D * 2 * D, 2 * D));
-        ts.push_back(tp(B, D, 2 * D, et, D, 0, g.bond_edge, a.DZ12, 8 * D, 4 * D, nullptr, G + lg.be.W + 2 * D * 2 * D, 2 * D));
         ts.push_back(tp(A, D, 2 * D, a.a[t], D, 0, nullptr, a.dzae, 4 * D, 0, nullptr, G + lg.be.W + 3 * D * 2 * D, 2 * D));
       }
       CHG_TRY(run_tns(ts, a, st, "tn_in"));
@@ -1988,26 +2202,34 @@ size_t acts_bytes(const chgnet_hparams& hp, int64_t N, int64_t E, int64_t B, int
 }
 
 int forward_entry(const chgnet_hparams* hp, const chgnet_batch* batch, const chgnet_graph* graph, const float* params,
-                  float* energy, float* forces, float* stress, void* ws, size_t ws_bytes, hipStream_t st) {
+                  float* energy, float* forces, float* stress, float* magmom, void* ws, size_t ws_bytes,
+                  hipStream_t st) {
   Ctx c;
   CHG_TRY(make_ctx(hp, batch, graph, ws, ws_bytes, c));
   if (!params || !energy || !forces || !stress) return fail(CHGNET_EINVAL, "forward: null output or params");
-  return forward_impl(c, params, energy, forces, stress, st);
+  if (magmom && !hp->magmom) return fail(CHGNET_EINVAL, "forward: magmom output without the magnetic-moment head");
+  return forward_impl(c, params, energy, forces, stress, magmom, st);
 }
 
 int backward_entry(const chgnet_hparams* hp, const chgnet_batch* batch, const chgnet_graph* graph, const float* params,
-                   const float* dE, const float* dF, const float* dS, float* grad, void* ws, size_t ws_bytes,
-                   hipStream_t st) {
+                   const float* dE, const float* dF, const float* dS, const float* dM, float* grad, void* ws,
+                   size_t ws_bytes, hipStream_t st) {
   Ctx c;
   CHG_TRY(make_ctx(hp, batch, graph, ws, ws_bytes, c));
   if (!params || !dE || !dF || !dS || !grad) return fail(CHGNET_EINVAL, "backward: null argument");
-  return backward_impl(c, params, true, dE, dF, dS, grad, st);
+  if (dM && !hp->magmom) return fail(CHGNET_EINVAL, "backward: dM without the magnetic-moment head");
+  return backward_impl(c, params, true, dE, dF, dS, dM, grad, st);
 }
 
 int step_entry(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_graph* graph, float* params,
-               const float* E_t, const float* F_t, const float* S_t, const float* loss_w, float* loss, float* grad,
-               float* adam_m, float* adam_v, const float* adam_hp, void* ws, size_t ws_bytes, hipStream_t st) {
-  if (!params || !E_t || !F_t || !S_t || !loss_w || !loss || !grad) return fail(CHGNET_EINVAL, "step: null argument");
+               const float* E_t, const float* F_t, const float* S_t, const float* M_t, const chgnet_loss* loss_cfg,
+               float* loss, float* grad, float* adam_m, float* adam_v, const float* adam_hp, void* ws,
+               size_t ws_bytes, hipStream_t st) {
+  if (!params || !E_t || !F_t || !S_t || !loss_cfg || !loss || !grad) return fail(CHGNET_EINVAL, "step: null argument");
+  CHG_TRY(validate_hparams(hp));
+  if ((M_t != nullptr) != (hp->magmom != 0))
+    return fail(CHGNET_EINVAL, "step: M_target is required with the magnetic-moment head and only with it");
+  if (!std::isfinite(loss_cfg->huber_delta)) return fail(CHGNET_EINVAL, "step: huber_delta is not finite");
   if (adam_hp && (!adam_m || !adam_v || !(adam_hp[4] >= 1.0f)))
     return fail(CHGNET_EINVAL, "step: Adam needs m, v and a step number t >= 1");
   CHG_TRY(build_graph(hp, batch, graph, ws, ws_bytes, st));
@@ -2016,10 +2238,12 @@ int step_entry(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_graph
   float* e_out = c.a.out_E;
   float* f_out = c.a.out_F;
   float* s_out = c.a.out_S;
-  CHG_TRY(forward_impl(c, params, e_out, f_out, s_out, st));
-  KLAUNCH(st, "k_loss", k_loss<<<1, 256, 0, st>>>((int)c.dm.S, (int)c.dm.N, batch->atom_ptr, e_out, f_out, s_out, E_t, F_t, S_t, loss_w[0],
-                            loss_w[1], loss_w[2], loss, c.a.dE, c.a.dF, c.a.dS));
-  CHG_TRY(backward_impl(c, params, false, c.a.dE, c.a.dF, c.a.dS, grad, st));
+  CHG_TRY(forward_impl(c, params, e_out, f_out, s_out, nullptr, st));
+  const bool mag = hp->magmom != 0;
+  KLAUNCH(st, "k_loss", k_loss<<<1, 256, 0, st>>>((int)c.dm.S, (int)c.dm.N, batch->atom_ptr, e_out, f_out, s_out,
+                                                   mag ? c.a.oM : nullptr, E_t, F_t, S_t, M_t, *loss_cfg, loss, c.a.dE,
+                                                   c.a.dF, c.a.dS, c.a.dM));
+  CHG_TRY(backward_impl(c, params, false, c.a.dE, c.a.dF, c.a.dS, mag ? c.a.dM : nullptr, grad, st));
   if (adam_hp) {
     const float lr = adam_hp[0], b1 = adam_hp[1], b2 = adam_hp[2], eps = adam_hp[3], t = adam_hp[4];
     const float c1 = 1.0f - powf(b1, t), c2 = 1.0f - powf(b2, t);

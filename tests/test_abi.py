@@ -38,6 +38,10 @@ def test_param_count_matches_oracle_layout(L):
     for d, T in ((64, 4), (128, 5), (64, 1), (128, 2)):
         assert L.param_count(L.hparams(d=d, n_layers=T)) == om.param_count(om.HParams(d=d, n_layers=T))
     assert L.param_count(L.hparams(d=64, n_layers=4)) == 405_001
+    for d, T in ((64, 4), (128, 3)):
+        ohp = om.HParams(d=d, n_layers=T, magmom=True)
+        assert L.param_count(L.hparams(d=d, n_layers=T, magmom=True)) == om.param_count(ohp)
+        assert L.param_count(L.hparams(d=d, n_layers=T, sequential=True)) == om.param_count(om.HParams(d=d, n_layers=T))
 
 
 def test_workspace_size_monotone(L):
@@ -50,7 +54,7 @@ def test_workspace_size_monotone(L):
 
 @pytest.mark.parametrize("kw", [dict(d=32), dict(d=96), dict(n_layers=0), dict(n_layers=17), dict(n_fourier=30),
                                 dict(n_rbf=0), dict(n_rbf=65), dict(r_bond=7.0), dict(r_atom=25.0, r_bond=3.0),
-                                dict(envelope_p=1)])
+                                dict(envelope_p=1), dict(magmom=2), dict(sequential=-1)])
 def test_bad_hparams_rejected(L, kw):
     with pytest.raises(L.ChgnetError) as e:
         L.param_count(L.hparams(**kw))
