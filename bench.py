@@ -31,6 +31,9 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="triclinic40")
+    ap.add_argument("--magmom", action="store_true", help="model variant: magnetic-moment head and its loss term")
+    ap.add_argument("--huber", type=float, default=0.0, help="model variant: Huber loss with this delta (0 = MSE)")
+    ap.add_argument("--sequential", action="store_true", help="model variant: the Eq. (10) interaction block")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample", type=int, default=0, help="structures in the CPU oracle sample (0 = auto)")
     ap.add_argument("--no-roofline", action="store_true")
@@ -61,8 +64,8 @@ def main():
 
     dev = "cuda:0"
     torch.cuda.set_device(0)
-    b, params, targets, d, T = synth.workload_inputs(args.workload)
-    hp = bd.hparams(d=d, n_layers=T)
+    b, params, targets, d, T = synth.workload_inputs(args.workload, magmom=args.magmom)
+    hp = bd.hparams(d=d, n_layers=T, magmom=args.magmom, sequential=args.sequential)
     db = bd.DeviceBatch.from_host(b, dev)
     g = bd.DeviceGraph(b.n_atoms, 1024, 256, 1024, dev)
     ws = bd.Workspace(dev)
@@ -78,7 +81,8 @@ def main():
 
     def one_step():
         step_no[0] += 1
-        bd.step(hp, db, g, p, tg, ws, grad=grad, loss=loss, adam=(m, v, (lr, b1, b2, eps, float(step_no[0]))))
+        bd.step(hp, db, g, p, tg, ws, loss_w=(2.0, 1.5, 0.1, 0.1), huber_delta=args.huber, grad=grad, loss=loss,
+                adam=(m, v, (lr, b1, b2, eps, float(step_no[0]))))
 
     if args.calibrate_copy:
         src = torch.ones(64 << 20, dtype=torch.float32, device=dev)
@@ -119,7 +123,10 @@ def main():
         "dtype": "fp32",
         "data": "synthetic (seeded crystals shaped like the paper's training set; random-init weights)",
         "config": {"workload": args.workload, "structures": S, "atoms": b.n_atoms, "edges": E, "bonds": B,
-                   "angles": A, "d": d, "layers": T, "parallelism": "single GPU"},
+                   "angles": A, "d": d, "layers": T, "parallelism": "single GPU",
+                   "block": "Eq. 10 (sequential)" if args.sequential else "Eq. 11",
+                   "loss": "Huber delta=%g" % args.huber if args.huber > 0 else "MSE",
+                   "heads": "E, F, S, magmom" if args.magmom else "E, F, S"},
         "edges_per_s": round(E / (ms * 1e-3), 1),
         "angles_per_s": round(A / (ms * 1e-3), 1),
         "ms_per_step_median": round(float(np.median(per_step)), 4),
@@ -137,7 +144,7 @@ def main():
         out["roofline"], out["kernels"] = roofline(prof, args.steps, dict(N=b.n_atoms, E=E, B=B, A=A, S=S, D=d, T=T,
                                                                             workload=args.workload))
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(args.workload, args.cpu_sample)
+        out["cpu_baseline"] = cpu_baseline(args.workload, args.cpu_sample, variant=args)
     print(json.dumps(out), flush=True)
 
 
@@ -312,7 +319,7 @@ def roofline(prof, steps, z):
     return rl, rows[:14]
 
 
-def cpu_baseline(workload, sample, min_seconds=10.0):
+def cpu_baseline(workload, sample, min_seconds=10.0, variant=None):
     """The CPU oracle (fp64 NumPy, untuned) on a bounded sample of the same
     workload: graph build, forward, loss and backward of the first `sample`
     structures (default: the whole batch), repeated until min_seconds of CPU
@@ -322,7 +329,8 @@ def cpu_baseline(workload, sample, min_seconds=10.0):
     from oracle import model as om
     from paper_2412_20796_amd import synth
 
-    b, params, targets, d, T = synth.workload_inputs(workload)
+    mag = bool(variant and variant.magmom)
+    b, params, targets, d, T = synth.workload_inputs(workload, magmom=mag)
     if sample <= 0:
         sample = b.n_struct
     ptr = [0]
@@ -330,13 +338,14 @@ def cpu_baseline(workload, sample, min_seconds=10.0):
         ptr.append(ptr[-1] + int(b.atom_ptr[s + 1] - b.atom_ptr[s]))
     n = ptr[-1]
     sb = synth.Batch(np.asarray(ptr, np.int32), b.pos[:n], b.lattice[:sample], b.Z[:n])
-    tgt = (targets[0][:sample], targets[1][:n], targets[2][:sample])
-    hp = om.HParams(d=d, n_layers=T)
+    tgt = (targets[0][:sample], targets[1][:n], targets[2][:sample]) + ((targets[3][:n],) if mag else ())
+    hp = om.HParams(d=d, n_layers=T, magmom=mag, sequential=bool(variant and variant.sequential))
+    delta = variant.huber if variant and variant.huber > 0 else None
     reps = 0
     t = time.perf_counter()
     n_edges = 0
     while True:
-        _, _, _, graph = om.step(hp, sb, params.astype(np.float64), tgt)
+        _, _, _, graph = om.step(hp, sb, params.astype(np.float64), tgt, delta=delta)
         n_edges = len(graph["edge_dst"])
         reps += 1
         dt = time.perf_counter() - t
