@@ -176,6 +176,32 @@ int chgnet_step(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_grap
                 const chgnet_loss* loss_cfg, float* loss, float* grad, float* adam_m, float* adam_v,
                 const float* adam_hp, void* ws, size_t ws_bytes, void* stream);
 
+/* Molecular-dynamics state of a batch (device arrays; Sec. V, Table 2). */
+typedef struct {
+  float* pos;            /* [N,3] positions, A (the batch's pos array); updated   */
+  float* vel;            /* [N,3] velocities, A/fs; updated                       */
+  const float* inv_mass; /* [N] inverse masses, 1/u                               */
+  float* forces;         /* [N,3] forces at pos, eV/A: read if forces_valid,
+                            written at the end                                    */
+  float* energy;         /* [S] energies at the final positions, eV (or NULL)     */
+  float* stress;         /* [S,3,3] stresses at the final positions (or NULL)     */
+} chgnet_md_state;
+
+/* n_steps of NVE velocity-Verlet molecular dynamics with the model's direct
+ * force head, lattices fixed: per step v += dt/2 a; x += dt v; graph and
+ * forward at the new x; v += dt/2 a, with a = F / m * 0.0096485332157 A/fs^2
+ * per eV/(A u) (dt in fs). batch->pos must equal state->pos. If forces_valid
+ * is 0 the forces at the initial positions are computed first. Every step
+ * rebuilds the graph (one wait for its sizes, as chgnet_build_graph);
+ * positions are not wrapped into the cell. *steps_done (host) receives the
+ * number of completed steps: on CHGNET_ECAPACITY the state is that of the
+ * last completed step with valid forces; grow the graph and call again for
+ * the remaining steps with forces_valid = 1. The model variant of hp applies
+ * (magmom is not returned). Errors as for chgnet_build_graph. */
+int chgnet_md(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_graph* graph, const float* params,
+              const chgnet_md_state* state, float dt, int n_steps, int forces_valid, int* steps_done, void* ws,
+              size_t ws_bytes, void* stream);
+
 /* Text of the last error on the calling thread ("" if none). */
 const char* chgnet_last_error_string(void);
 

@@ -18,7 +18,7 @@ _lib = None
 
 CHGNET_OK, CHGNET_EINVAL, CHGNET_ECAPACITY, CHGNET_EWORKSPACE, CHGNET_EHIP = 0, -1, -2, -3, -4
 EXPORTED = ("chgnet_param_count", "chgnet_workspace_size", "chgnet_build_graph", "chgnet_forward",
-            "chgnet_backward", "chgnet_step", "chgnet_last_error_string", "chgnet_profile_start",
+            "chgnet_backward", "chgnet_step", "chgnet_md", "chgnet_last_error_string", "chgnet_profile_start",
             "chgnet_profile_stop")
 
 
@@ -37,6 +37,11 @@ class HParams(ctypes.Structure):
 class LossCfg(ctypes.Structure):
     _fields_ = [("w_energy", ctypes.c_float), ("w_force", ctypes.c_float), ("w_stress", ctypes.c_float),
                 ("w_magmom", ctypes.c_float), ("huber_delta", ctypes.c_float)]
+
+
+class MdState(ctypes.Structure):
+    _fields_ = [("pos", ctypes.c_void_p), ("vel", ctypes.c_void_p), ("inv_mass", ctypes.c_void_p),
+                ("forces", ctypes.c_void_p), ("energy", ctypes.c_void_p), ("stress", ctypes.c_void_p)]
 
 
 class CBatch(ctypes.Structure):
@@ -71,6 +76,9 @@ def lib():
         L.chgnet_step.argtypes = [ctypes.POINTER(HParams), ctypes.POINTER(CBatch), ctypes.POINTER(CGraph), vp, vp, vp,
                                   vp, vp, ctypes.POINTER(LossCfg), vp, vp, vp, vp, ctypes.POINTER(ctypes.c_float),
                                   vp, ctypes.c_size_t, vp]
+        L.chgnet_md.argtypes = [ctypes.POINTER(HParams), ctypes.POINTER(CBatch), ctypes.POINTER(CGraph), vp,
+                                ctypes.POINTER(MdState), ctypes.c_float, ctypes.c_int, ctypes.c_int,
+                                ctypes.POINTER(ctypes.c_int), vp, ctypes.c_size_t, vp]
         L.chgnet_last_error_string.restype = ctypes.c_char_p
         L.chgnet_profile_start.argtypes = [ctypes.c_int]
         L.chgnet_profile_stop.argtypes = [ctypes.c_char_p, ctypes.c_size_t]
@@ -309,4 +317,38 @@ def step(hp, batch, graph, params, targets, ws, loss_w=(2.0, 1.5, 0.1, 0.1), hub
             continue
         _check(code)
         return loss, grad
+    raise ChgnetError(CHGNET_ECAPACITY, "graph capacity retry failed")
+
+
+def md(hp, batch, graph, params, vel, inv_mass, dt, n_steps, ws, forces=None, energy=None, stress=None):
+    """n_steps of velocity-Verlet MD (chgnet_md) on batch.pos and vel in place, growing the graph when
+    its capacity runs out. forces: [N,3] forces at batch.pos (computed first if None). Returns
+    (forces, energy, stress) at the final positions."""
+    dev = batch.pos.device
+    S, N = batch.n_struct, batch.n_atoms
+    valid = forces is not None
+    if forces is None:
+        forces = torch.empty(N, 3, dtype=torch.float32, device=dev)
+    if energy is None:
+        energy = torch.empty(S, dtype=torch.float32, device=dev)
+    if stress is None:
+        stress = torch.empty(S, 3, 3, dtype=torch.float32, device=dev)
+    st = MdState(_ptr(batch.pos).value, _ptr(vel).value, _ptr(inv_mass).value, _ptr(forces).value,
+                 _ptr(energy).value, _ptr(stress).value)
+    cb = batch.c()
+    left = n_steps
+    for _ in range(8):
+        ensure_ws(hp, batch, graph, ws)
+        cg = graph.c()
+        done = ctypes.c_int(0)
+        code = lib().chgnet_md(ctypes.byref(hp), ctypes.byref(cb), ctypes.byref(cg), _ptr(params), ctypes.byref(st),
+                               dt, left, int(valid), ctypes.byref(done), ws.ptr, ws.nbytes, _stream(dev))
+        graph.take_counts(cg)
+        left -= done.value
+        valid = valid or done.value > 0
+        if code == CHGNET_ECAPACITY:
+            graph.resize(int(cg.n_edges * 1.25) + 64, int(cg.n_bonds * 1.25) + 64, int(cg.n_angles * 1.25) + 64, dev)
+            continue
+        _check(code)
+        return forces, energy, stress
     raise ChgnetError(CHGNET_ECAPACITY, "graph capacity retry failed")

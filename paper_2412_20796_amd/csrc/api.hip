@@ -24,6 +24,9 @@ int step_entry(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_graph
                const float* E_t, const float* F_t, const float* S_t, const float* M_t, const chgnet_loss* loss_cfg,
                float* loss, float* grad, float* adam_m, float* adam_v, const float* adam_hp, void* ws,
                size_t ws_bytes, hipStream_t st);
+int md_entry(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_graph* graph, const float* params,
+             const chgnet_md_state* s, float dt, int n_steps, int forces_valid, int* steps_done, void* ws,
+             size_t ws_bytes, hipStream_t st);
 
 namespace {
 thread_local std::string g_last_error;
@@ -182,6 +185,13 @@ int chgnet_step(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_grap
                 const float* adam_hp, void* ws, size_t ws_bytes, void* stream) {
   return chg::step_entry(hp, batch, graph, params, E_target, F_target, S_target, M_target, loss_cfg, loss, grad,
                          adam_m, adam_v, adam_hp, ws, ws_bytes, static_cast<hipStream_t>(stream));
+}
+
+int chgnet_md(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_graph* graph, const float* params,
+              const chgnet_md_state* state, float dt, int n_steps, int forces_valid, int* steps_done, void* ws,
+              size_t ws_bytes, void* stream) {
+  return chg::md_entry(hp, batch, graph, params, state, dt, n_steps, forces_valid, steps_done, ws, ws_bytes,
+                       static_cast<hipStream_t>(stream));
 }
 
 const char* chgnet_last_error_string(void) { return chg::g_last_error.c_str(); }

@@ -1168,6 +1168,31 @@ __global__ void k_adam(int64_t P, float* __restrict__ params, const float* __res
 }
 
 // ---------------------------------------------------------------------------
+// Velocity Verlet (NVE, fixed lattices). h = dt/2 times the acceleration of
+// 1 eV/A on 1 u in A/fs^2.
+// ---------------------------------------------------------------------------
+// first half kick and drift into the trial state: v' = v + h F / m, x' = x + dt v'
+__global__ void k_md_kick_drift(int n3, const float* __restrict__ pos, const float* __restrict__ vel,
+                                const float* __restrict__ F, const float* __restrict__ inv_mass, float h, float dt,
+                                float* __restrict__ pos2, float* __restrict__ vel2) {
+  const int k = blockIdx.x * blockDim.x + threadIdx.x;
+  if (k >= n3) return;
+  const float v = vel[k] + h * inv_mass[k / 3] * F[k];
+  vel2[k] = v;
+  pos2[k] = pos[k] + dt * v;
+}
+
+// second half kick with the new forces, and commit of the trial positions
+__global__ void k_md_kick_commit(int n3, const float* __restrict__ pos2, const float* __restrict__ vel2,
+                                 const float* __restrict__ F, const float* __restrict__ inv_mass, float h,
+                                 float* __restrict__ pos, float* __restrict__ vel) {
+  const int k = blockIdx.x * blockDim.x + threadIdx.x;
+  if (k >= n3) return;
+  vel[k] = vel2[k] + h * inv_mass[k / 3] * F[k];
+  pos[k] = pos2[k];
+}
+
+// ---------------------------------------------------------------------------
 // Workspace carving.
 // ---------------------------------------------------------------------------
 struct Dims {
@@ -1194,11 +1219,17 @@ struct Acts {
   int64_t tnpart_cap;
   // loss
   float *dE, *dF, *dS, *dM, *out_E, *out_F, *out_S, *out_M;
+  // molecular dynamics: trial positions and velocities
+  float *md_pos, *md_vel;
 };
 
 void carve_acts(Arena& ar, const Dims& m, Acts& a, int64_t n_params_aligned) {
   const int64_t N = m.N, S = m.S, E = m.E, B = m.B, A = m.A, D = m.D, R = m.R, K = m.K;
   a.Pal = ar.take<float>(n_params_aligned);
+  // carved before anything that depends on the graph sizes: the same address
+  // for every graph of the batch
+  a.md_pos = ar.take<float>(3 * N);
+  a.md_vel = ar.take<float>(3 * N);
   a.atom_struct = ar.take<int>(N);
   a.edge_src = ar.take<int>(E);
   a.bond_src = ar.take<int>(B);
@@ -1582,11 +1613,11 @@ int make_ctx(const chgnet_hparams* hp, const chgnet_batch* batch, const chgnet_g
 // Forward.
 // ---------------------------------------------------------------------------
 int forward_impl(Ctx& c, const float* Pflat, float* energy, float* forces, float* stress, float* magmom,
-                 hipStream_t st) {
+                 hipStream_t st, bool pack = true) {
   const Dims& m = c.dm;
   Acts& a = c.a;
   const ParamLayout& L = c.La;
-  CHG_TRY(pack_params(c.L, c.La, Pflat, a.Pal, st));
+  if (pack) CHG_TRY(pack_params(c.L, c.La, Pflat, a.Pal, st));
   const float* P = a.Pal;
   const chgnet_graph& g = *c.graph;
   const chgnet_batch& bt = *c.batch;
@@ -2248,6 +2279,57 @@ int step_entry(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_graph
     const float lr = adam_hp[0], b1 = adam_hp[1], b2 = adam_hp[2], eps = adam_hp[3], t = adam_hp[4];
     const float c1 = 1.0f - powf(b1, t), c2 = 1.0f - powf(b2, t);
     KLAUNCH(st, "k_adam", k_adam<<<(unsigned)cdiv(c.L.total, 256), 256, 0, st>>>(c.L.total, params, grad, adam_m, adam_v, lr, b1, b2, eps, c1, c2));
+  }
+  return CHGNET_OK;
+}
+
+int md_entry(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_graph* graph, const float* params,
+             const chgnet_md_state* s, float dt, int n_steps, int forces_valid, int* steps_done, void* ws,
+             size_t ws_bytes, hipStream_t st) {
+  if (steps_done) *steps_done = 0;
+  CHG_TRY(validate_hparams(hp));
+  if (!batch || !s || !params || !steps_done) return fail(CHGNET_EINVAL, "md: null argument");
+  if (!s->pos || !s->vel || !s->inv_mass || !s->forces || s->pos != batch->pos)
+    return fail(CHGNET_EINVAL, "md: state arrays missing or state->pos != batch->pos");
+  if (!(dt > 0.f) || !std::isfinite(dt) || n_steps < 0) return fail(CHGNET_EINVAL, "md: need dt > 0 and n_steps >= 0");
+  // 1 eV / (A u) in A / fs^2: e / u * 1e10 m/s^2 = e / u * 1e-10 A/fs^2 (CODATA 2018 e and u)
+  constexpr double kAccel = 1.602176634e-19 / 1.66053906660e-27 * 1e-10;
+  const float h = (float)(0.5 * (double)dt * kAccel);
+  const int n3 = 3 * batch->n_atoms;
+  const unsigned nb = (unsigned)cdiv(n3, 256);
+  chgnet_batch trial = *batch;
+  bool packed = false;
+  auto forces_at = [&](const chgnet_batch* b) -> int {
+    CHG_TRY(build_graph(hp, b, graph, ws, ws_bytes, st));
+    Ctx c;
+    CHG_TRY(make_ctx(hp, b, graph, ws, ws_bytes, c));
+    CHG_TRY(forward_impl(c, params, s->energy ? s->energy : c.a.out_E, s->forces, s->stress ? s->stress : c.a.out_S,
+                         nullptr, st, !packed));
+    packed = true;
+    return CHGNET_OK;
+  };
+  if (!forces_valid) CHG_TRY(forces_at(batch));
+  // trial positions and velocities sit in the workspace at an address that
+  // does not depend on the graph sizes; a step that runs out of graph
+  // capacity leaves the caller's state at the last completed step
+  float *pos2, *vel2;
+  {
+    CHG_TRY(validate_batch(batch));
+    Arena ar{static_cast<char*>(ws), ws_bytes, 0};
+    ar.used = graph_scratch_bytes(batch->n_atoms, batch->n_struct);
+    Acts a;
+    Dims d0{batch->n_atoms, batch->n_struct, 0, 0, 0, hp->d, hp->n_layers, hp->n_rbf, hp->n_fourier};
+    carve_acts(ar, d0, a, make_layout(*hp, 4).total);
+    if (!ws || !ar.ok()) return fail(CHGNET_EWORKSPACE, "workspace too small (query chgnet_workspace_size)");
+    pos2 = a.md_pos;
+    vel2 = a.md_vel;
+  }
+  for (int k = 0; k < n_steps; ++k) {
+    KLAUNCH(st, "k_md", k_md_kick_drift<<<nb, 256, 0, st>>>(n3, s->pos, s->vel, s->forces, s->inv_mass, h, dt, pos2, vel2));
+    trial.pos = pos2;
+    CHG_TRY(forces_at(&trial));
+    KLAUNCH(st, "k_md", k_md_kick_commit<<<nb, 256, 0, st>>>(n3, pos2, vel2, s->forces, s->inv_mass, h, s->pos, s->vel));
+    *steps_done = k + 1;
   }
   return CHGNET_OK;
 }

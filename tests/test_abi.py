@@ -27,7 +27,7 @@ def L():
 
 def test_exports_every_declared_symbol(L):
     names = _declared()
-    assert len(names) == 9
+    assert len(names) == 10
     lib = ctypes.CDLL(L._LIB_PATH)
     for n in names:
         assert hasattr(lib, n), n
@@ -67,3 +67,7 @@ def test_null_arguments_rejected(L):
     assert lib.chgnet_param_count(ctypes.byref(hp), None) == L.CHGNET_EINVAL
     assert lib.chgnet_build_graph(ctypes.byref(hp), None, None, None, 0, None) == L.CHGNET_EINVAL
     assert b"batch" in lib.chgnet_last_error_string()
+    done = ctypes.c_int(7)
+    assert lib.chgnet_md(ctypes.byref(hp), None, None, None, None, 1.0, 1, 0, ctypes.byref(done), None, 0,
+                         None) == L.CHGNET_EINVAL
+    assert done.value == 0
