@@ -43,6 +43,15 @@ library alike):
   layer-t features). HParams.sequential selects the reference block of
   Eq. (10): the bond conv reads v^{t+1}, the angle update reads v^{t+1} and
   the updated bond features e^{t+1} (Eq. (5), (6)).
+* Conservative readout (HParams.conservative; the reference CHGNet output
+  layer, Sec. II-B (4)): F_i = -dE/dr_i and sigma = (1/V) dE/d(eps) for the
+  homogeneous strain r -> (I + eps) r of positions and lattice, replacing the
+  force and stress heads (whose weights are then unused). E depends on the
+  positions only through the edge vectors r_e = r_j + n L - r_i (lengths in
+  the radial bases, bond-pair angles in the Fourier basis), so with
+  g_e = dE/dr_e: F_i = sum over edges leaving i of g_e minus the sum over
+  edges entering i, and sigma = (1/V) sum_e g_e r_e^T. d(theta)/dr is
+  undefined for collinear bond pairs (|r1 x r2| = 0); it is taken as 0 there.
 """
 from __future__ import annotations
 
@@ -64,8 +73,9 @@ class HParams:
     envelope_p: int = 8
     r_atom: float = 6.0
     r_bond: float = 3.0
-    magmom: bool = False      # magnetic-moment head
-    sequential: bool = False  # Eq. (10) block instead of Eq. (11)
+    magmom: bool = False        # magnetic-moment head
+    sequential: bool = False    # Eq. (10) block instead of Eq. (11)
+    conservative: bool = False  # F and sigma as derivatives of E
 
 
 # ---------------------------------------------------------------------------
@@ -143,6 +153,31 @@ def srbf_dfreq(r, freq, cutoff, p):
     """d sRBF_n / d f_n (elementwise), [n_edges, n_rbf]."""
     r = np.asarray(r, dtype=np.float64)[:, None]
     return math.sqrt(2.0 / cutoff) * np.cos(freq[None, :] * r / cutoff) / cutoff * envelope(r / cutoff, p)
+
+
+def envelope_dx(x, p):
+    """u'(x) from differentiating each term of the polynomial."""
+    return (-(p + 1) * (p + 2) / 2.0 * p * x ** (p - 1) + p * (p + 2) * (p + 1) * x ** p
+            - p * (p + 1) / 2.0 * (p + 2) * x ** (p + 1))
+
+
+def srbf_dr(r, freq, cutoff, p):
+    """d sRBF_n / d r (product rule on sin(f r / c) * (1/r) * u(r/c)), [n_edges, n_rbf]."""
+    r = np.asarray(r, dtype=np.float64)[:, None]
+    a = freq[None, :] * r / cutoff
+    x = r / cutoff
+    return math.sqrt(2.0 / cutoff) * (np.cos(a) * freq[None, :] / cutoff / r * envelope(x, p)
+                                      - np.sin(a) / (r * r) * envelope(x, p)
+                                      + np.sin(a) / r * envelope_dx(x, p) / cutoff)
+
+
+def fourier_dtheta(theta, n_fourier):
+    """d FT / d theta, [n_angles, n_fourier]."""
+    m = (n_fourier - 1) // 2
+    ks = np.arange(1, m + 1)[None, :]
+    th = np.asarray(theta, dtype=np.float64)[:, None]
+    return np.concatenate([np.zeros((th.shape[0], 1)), -ks * np.sin(ks * th) / math.sqrt(math.pi),
+                           ks * np.cos(ks * th) / math.sqrt(math.pi)], axis=1)
 
 
 def fourier(theta, n_fourier):
@@ -326,7 +361,39 @@ def forward(hp: HParams, batch, graph, params):
 
     cache = dict(P=P, g=g, Zidx=Z - 1, rbf_a=rbf_a, rbf_b=rbf_b, ft=ft, ea=ea, eb=eb, layers=layers, vT=v, eT=e,
                  cE=cE, cF=cF, cSc=cSc, xhat=xhat, U=U, vol=vol, oM=oM, magmom=magmom)
+    if hp.conservative:
+        forces, stress = conservative_readout(hp, cache)
     return energy, forces, stress, cache
+
+
+def conservative_readout(hp, cache):
+    """F = -dE/dr and sigma = (1/V) dE/d(eps) through the backward of E."""
+    P, g = cache["P"], cache["g"]
+    N, S = g["N"], g["S"]
+    _, gi = backward(hp, cache, np.ones(S), np.zeros((N, 3)), np.zeros((S, 3, 3)), inputs=True)
+    be, b1, b2, rvec, dist = g["bond_edge"], g["b1"], g["b2"], g["rvec"], g["dist"]
+    xhat = rvec / dist[:, None]
+    # radial bases: dE/d|r_e| along r_e / |r_e|
+    gd = (gi["drbf_a"] * srbf_dr(dist, P["f_a"], hp.r_atom, hp.envelope_p)).sum(axis=1)
+    gvec = gd[:, None] * xhat
+    gdb = (gi["drbf_b"] * srbf_dr(dist[be], P["f_b"], hp.r_bond, hp.envelope_p)).sum(axis=1)
+    np.add.at(gvec, be, gdb[:, None] * xhat[be])
+    # angular basis: theta = atan2(|r1 x r2|, r1 . r2);
+    # d theta / d r1 = (c r1 / |r1|^2 - r2) / s, and symmetrically for r2
+    gth = (gi["dft"] * fourier_dtheta(g["theta"], hp.n_fourier)).sum(axis=1)
+    r1, r2 = rvec[be[b1]], rvec[be[b2]]
+    c = (r1 * r2).sum(axis=1)
+    sn = np.linalg.norm(np.cross(r1, r2), axis=1)
+    ok = sn > 0
+    inv = np.where(ok, 1.0 / np.where(ok, sn, 1.0), 0.0)[:, None]
+    d1 = (c[:, None] * r1 / (r1 * r1).sum(axis=1, keepdims=True) - r2) * inv
+    d2 = (c[:, None] * r2 / (r2 * r2).sum(axis=1, keepdims=True) - r1) * inv
+    np.add.at(gvec, be[b1], gth[:, None] * d1)
+    np.add.at(gvec, be[b2], gth[:, None] * d2)
+    # r_e = r_dst + n L - r_src
+    forces = seg_sum(gvec, g["src"], N) - seg_sum(gvec, g["dst"], N)
+    sig = seg_sum(np.einsum("ea,eb->eab", gvec, rvec), g["struct"][g["src"]], S)
+    return forces, sig / cache["vol"][:, None, None]
 
 
 # ---------------------------------------------------------------------------
@@ -375,9 +442,11 @@ def magmom_loss(magmom, M_t, w=0.1, delta=None):
 # Backward (first order, weights only).
 # ---------------------------------------------------------------------------
 
-def backward(hp: HParams, cache, dE, dF, dS, dM=None):
+def backward(hp: HParams, cache, dE, dF, dS, dM=None, inputs=False):
     """Gradient of <dE,E> + <dF,F> + <dS,sigma> (+ <dM,magmom>) w.r.t. every
-    parameter (flat)."""
+    parameter (flat), with the direct force and stress heads. With inputs,
+    also the gradients with respect to the two radial bases and the angular
+    basis: (flat, dict(drbf_a, drbf_b, dft))."""
     P, g = cache["P"], cache["g"]
     d, T = hp.d, hp.n_layers
     N, S, B = g["N"], g["S"], g["B"]
@@ -466,6 +535,8 @@ def backward(hp: HParams, cache, dE, dF, dS, dM=None):
     flat = np.zeros(total)
     for k, (o, s) in lay.items():
         flat[o:o + int(np.prod(s))] = G[k].reshape(-1)
+    if inputs:
+        return flat, dict(drbf_a=drbf_a, drbf_b=drbf_b, dft=da @ P["W_th"].T)
     return flat
 
 
@@ -484,6 +555,8 @@ def step(hp: HParams, batch, params, targets, w=(2.0, 1.5, 0.1), graph=None, del
     when the head is on; delta selects the Huber loss; w_m weighs the moments."""
     from . import graph as graph_mod
 
+    if hp.conservative:
+        raise NotImplementedError("training through the conservative readout needs second derivatives")
     if graph is None:
         graph = graph_mod.build_graph(batch.atom_ptr, batch.pos, batch.lattice, hp.r_atom, hp.r_bond)
     energy, forces, stress, cache = forward(hp, batch, graph, params)
