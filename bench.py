@@ -34,6 +34,8 @@ def parse():
     ap.add_argument("--magmom", action="store_true", help="model variant: magnetic-moment head and its loss term")
     ap.add_argument("--huber", type=float, default=0.0, help="model variant: Huber loss with this delta (0 = MSE)")
     ap.add_argument("--sequential", action="store_true", help="model variant: the Eq. (10) interaction block")
+    ap.add_argument("--conservative", action="store_true",
+                    help="with --md: forces and stress as derivatives of the energy (no training through it)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample", type=int, default=0, help="structures in the CPU oracle sample (0 = auto)")
     ap.add_argument("--no-roofline", action="store_true")
@@ -70,6 +72,9 @@ def main():
     if args.md:
         print(json.dumps(md_bench(args, bd, synth, dev)), flush=True)
         return
+    if args.conservative:
+        print("bench.py: training through the conservative readout is not supported (use --md)", file=sys.stderr)
+        sys.exit(2)
     b, params, targets, d, T = synth.workload_inputs(args.workload, magmom=args.magmom)
     hp = bd.hparams(d=d, n_layers=T, magmom=args.magmom, sequential=args.sequential)
     db = bd.DeviceBatch.from_host(b, dev)
@@ -173,7 +178,7 @@ def md_bench(args, bd, synth, dev):
     else:
         b = b0
     rng = np.random.default_rng(17)
-    hp = bd.hparams(d=d, n_layers=T, sequential=args.sequential)
+    hp = bd.hparams(d=d, n_layers=T, sequential=args.sequential, conservative=args.conservative)
     db = bd.DeviceBatch.from_host(b, dev)
     g = bd.DeviceGraph(b.n_atoms, 1024, 256, 1024, dev)
     ws = bd.Workspace(dev)
@@ -199,7 +204,8 @@ def md_bench(args, bd, synth, dev):
         "config": {"workload": "md-" + workload, "structures": b.n_struct, "atoms": b.n_atoms,
                    "replicas": R, "edges": g.n_edges, "bonds": g.n_bonds, "angles": g.n_angles, "d": d,
                    "layers": T, "integrator": "velocity Verlet, dt %.1f fs" % dt,
-                   "block": "Eq. 10 (sequential)" if args.sequential else "Eq. 11"},
+                   "block": "Eq. 10 (sequential)" if args.sequential else "Eq. 11",
+                   "readout": "conservative (F = -dE/dr)" if args.conservative else "direct force/stress heads"},
         "atom_steps_per_s": round(b.n_atoms * 1e3 / ms, 1),
         "wall_ms_per_step": round(1e3 * wall / args.steps, 4),
         "paper_context": "one-step MD of an 8-atom LiMnO2 cell: 0.0077 s (FastCHGNet), 0.022 s (CHGNet), "

@@ -28,7 +28,7 @@
  * 31 radial and 31 angular basis functions, envelope exponent p = 8, atom
  * graph cutoff 6 A, bond graph cutoff 3 A. Supported: d in {64, 128},
  * 1 <= T <= 16, 1 <= n_rbf <= 64, n_fourier odd in [1, 63], p in [2, 16],
- * 0 < r_bond <= r_atom <= 20, magmom and sequential in {0, 1}.
+ * 0 < r_bond <= r_atom <= 20, magmom, sequential and conservative in {0, 1}.
  */
 #ifndef CHGNET_H
 #define CHGNET_H
@@ -59,6 +59,14 @@ typedef struct {
                          update read layer-t features); 1: the reference
                          block of Eq. 10 (bond conv reads v^{t+1}, angle
                          update reads v^{t+1} and e^{t+1})                  */
+  int32_t conservative; /* 1: forces and stress as derivatives of the energy,
+                         F_i = -dE/dr_i, sigma = (1/V) dE/d(eps) for the
+                         strain r -> (I + eps) r of positions and lattice
+                         (the reference output layer, Sec. II-B (4)); the
+                         force and stress head weights are then unused.
+                         Forward and MD only: training through it needs
+                         second derivatives, which this library does not
+                         compute (chgnet_backward/chgnet_step: EINVAL).    */
 } chgnet_hparams;
 
 /* Loss of chgnet_step (Sec. IV, "Parameters Setting"), host memory. Each term
@@ -197,7 +205,7 @@ typedef struct {
  * number of completed steps: on CHGNET_ECAPACITY the state is that of the
  * last completed step with valid forces; grow the graph and call again for
  * the remaining steps with forces_valid = 1. The model variant of hp applies
- * (magmom is not returned). Errors as for chgnet_build_graph. */
+ * (conservative forces included; magmom is not returned). Errors as for chgnet_build_graph. */
 int chgnet_md(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_graph* graph, const float* params,
               const chgnet_md_state* state, float dt, int n_steps, int forces_valid, int* steps_done, void* ws,
               size_t ws_bytes, void* stream);

@@ -31,7 +31,8 @@ class ChgnetError(RuntimeError):
 class HParams(ctypes.Structure):
     _fields_ = [("d", ctypes.c_int32), ("n_layers", ctypes.c_int32), ("n_rbf", ctypes.c_int32),
                 ("n_fourier", ctypes.c_int32), ("envelope_p", ctypes.c_int32), ("r_atom", ctypes.c_float),
-                ("r_bond", ctypes.c_float), ("magmom", ctypes.c_int32), ("sequential", ctypes.c_int32)]
+                ("r_bond", ctypes.c_float), ("magmom", ctypes.c_int32), ("sequential", ctypes.c_int32),
+                ("conservative", ctypes.c_int32)]
 
 
 class LossCfg(ctypes.Structure):
@@ -95,8 +96,9 @@ def _check(code):
 
 
 def hparams(d=64, n_layers=4, n_rbf=31, n_fourier=31, envelope_p=8, r_atom=6.0, r_bond=3.0, magmom=False,
-            sequential=False) -> HParams:
-    return HParams(d, n_layers, n_rbf, n_fourier, envelope_p, r_atom, r_bond, int(magmom), int(sequential))
+            sequential=False, conservative=False) -> HParams:
+    return HParams(d, n_layers, n_rbf, n_fourier, envelope_p, r_atom, r_bond, int(magmom), int(sequential),
+                   int(conservative))
 
 
 def param_count(hp: HParams) -> int:

@@ -72,8 +72,9 @@ int validate_hparams(const chgnet_hparams* hp) {
   if (hp->envelope_p < 2 || hp->envelope_p > 16) return fail(CHGNET_EINVAL, "envelope_p must be in 2..16");
   if (!(hp->r_bond > 0.f) || !(hp->r_bond <= hp->r_atom) || !(hp->r_atom <= 20.f))
     return fail(CHGNET_EINVAL, "cutoffs must satisfy 0 < r_bond <= r_atom <= 20");
-  if ((hp->magmom != 0 && hp->magmom != 1) || (hp->sequential != 0 && hp->sequential != 1))
-    return fail(CHGNET_EINVAL, "magmom and sequential must be 0 or 1");
+  if ((hp->magmom != 0 && hp->magmom != 1) || (hp->sequential != 0 && hp->sequential != 1) ||
+      (hp->conservative != 0 && hp->conservative != 1))
+    return fail(CHGNET_EINVAL, "magmom, sequential and conservative must be 0 or 1");
   return CHGNET_OK;
 }
 

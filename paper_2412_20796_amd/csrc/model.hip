@@ -1168,6 +1168,155 @@ __global__ void k_adam(int64_t P, float* __restrict__ params, const float* __res
 }
 
 // ---------------------------------------------------------------------------
+// Conservative readout: F = -dE/dr, sigma = (1/V) dE/d(eps), from the
+// gradients of E with respect to the radial bases (drbf) and the angular
+// basis (dft). g_e = dE/dr_e is formed per edge; fp64 arithmetic.
+// ---------------------------------------------------------------------------
+// sum_n drbf_n d sRBF_n / dr at r (product rule on sin(f r/c) (1/r) u(r/c))
+__device__ double drbf_dr(const float* __restrict__ drbf, const float* __restrict__ freq, int R, double r, double c,
+                          int p) {
+  const double x = r / c;
+  double xp1 = 1.0;  // x^(p-1)
+  for (int k = 0; k < p - 1; ++k) xp1 *= x;
+  const double u = 1.0 + xp1 * x * (-0.5 * (p + 1) * (p + 2) + x * ((double)p * (p + 2) - x * 0.5 * p * (p + 1)));
+  const double du = -0.5 * p * (p + 1) * (p + 2) * xp1 * (1.0 - x) * (1.0 - x);
+  const double pre = sqrt(2.0 / c);
+  double acc = 0.0;
+  for (int n = 0; n < R; ++n) {
+    const double f = freq[n];
+    double sa, ca;
+    sincos(f * x, &sa, &ca);
+    acc += (double)drbf[n] * pre * (ca * f / c / r * u - sa / (r * r) * u + sa / r * du / c);
+  }
+  return acc;
+}
+
+// g_e = (sum_n drbf_a d sRBF_n(6 A) / dr) r_e / |r_e|
+__global__ void k_cons_edges(int E, const float* __restrict__ len, const float* __restrict__ xhat,
+                             const float* __restrict__ drbf_a, const float* __restrict__ freq, int R, float cutoff,
+                             int p, float* __restrict__ gvec) {
+  const int e = blockIdx.x * blockDim.x + threadIdx.x;
+  if (e >= E) return;
+  const double gd = drbf_dr(drbf_a + (int64_t)e * R, freq, R, len[e], cutoff, p);
+  for (int c = 0; c < 3; ++c) gvec[3 * e + c] = (float)(gd * xhat[3 * e + c]);
+}
+
+// Per angle: g_theta = sum_k dft_k d FT_k / d theta; p1 = g_theta d theta / d r1,
+// p2 = g_theta d theta / d r2 with d theta / d r1 = (c r1 / |r1|^2 - r2) / s
+// (c = r1.r2, s = |r1 x r2|; zero when s = 0).
+__global__ void k_cons_angles(int A, const int* __restrict__ ang_b1, const int* __restrict__ ang_b2,
+                              const int* __restrict__ bond_edge, const int* __restrict__ ang_ctr,
+                              const int* __restrict__ edge_dst, const int* __restrict__ edge_img,
+                              const int* __restrict__ atom_struct, const float* __restrict__ pos,
+                              const float* __restrict__ lattice, const float* __restrict__ dft, int K,
+                              float* __restrict__ pang) {
+  const int al = blockIdx.x * blockDim.x + threadIdx.x;
+  if (al >= A) return;
+  const int i = ang_ctr[al];
+  const float* L = lattice + 9 * atom_struct[i];
+  double r[2][3];
+  const int es[2] = {bond_edge[ang_b1[al]], bond_edge[ang_b2[al]]};
+  for (int q = 0; q < 2; ++q) {
+    const int e = es[q], j = edge_dst[e];
+    const double n0 = edge_img[3 * e], n1 = edge_img[3 * e + 1], n2 = edge_img[3 * e + 2];
+    for (int c = 0; c < 3; ++c)
+      r[q][c] = (double)pos[3 * j + c] + (n0 * (double)L[c] + n1 * (double)L[3 + c] + n2 * (double)L[6 + c]) - (double)pos[3 * i + c];
+  }
+  const double dot = r[0][0] * r[1][0] + r[0][1] * r[1][1] + r[0][2] * r[1][2];
+  const double cx = r[0][1] * r[1][2] - r[0][2] * r[1][1];
+  const double cy = r[0][2] * r[1][0] - r[0][0] * r[1][2];
+  const double cz = r[0][0] * r[1][1] - r[0][1] * r[1][0];
+  const double sn = sqrt(cx * cx + cy * cy + cz * cz);
+  const double h = sqrt(dot * dot + sn * sn);
+  const double c1 = dot / h, s1 = sn / h;
+  const int M = (K - 1) / 2;
+  const float* d = dft + (int64_t)al * K;
+  const double inv_sqrt_pi = 0.56418958354775628695;
+  double gth = 0.0, cm = 1.0, sm = 0.0;
+  for (int m = 1; m <= M; ++m) {
+    const double cn = cm * c1 - sm * s1, snn = sm * c1 + cm * s1;
+    cm = cn;
+    sm = snn;
+    gth += m * inv_sqrt_pi * (-(double)d[m] * sm + (double)d[M + m] * cm);
+  }
+  const double inv_s = sn > 0.0 ? 1.0 / sn : 0.0;
+  const double n1 = r[0][0] * r[0][0] + r[0][1] * r[0][1] + r[0][2] * r[0][2];
+  const double n2 = r[1][0] * r[1][0] + r[1][1] * r[1][1] + r[1][2] * r[1][2];
+  for (int c = 0; c < 3; ++c) {
+    pang[6 * (int64_t)al + c] = (float)(gth * (dot * r[0][c] / n1 - r[1][c]) * inv_s);
+    pang[6 * (int64_t)al + 3 + c] = (float)(gth * (dot * r[1][c] / n2 - r[0][c]) * inv_s);
+  }
+}
+
+// Per bond b (edge e): g_e += (sum_n drbf_b d sRBF_n(3 A) / dr) r_e / |r_e|
+// + sum over angles (b, *) of p1 + sum over angles (*, b) of p2 (fixed order).
+__global__ void k_cons_bonds(int B, const int* __restrict__ bond_edge, const int* __restrict__ bond_src,
+                             const int* __restrict__ bond_ptr, const int* __restrict__ angle_ptr,
+                             const float* __restrict__ len, const float* __restrict__ xhat,
+                             const float* __restrict__ drbf_b, const float* __restrict__ freq, int R, float cutoff,
+                             int p, const float* __restrict__ pang, float* __restrict__ gvec) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= B) return;
+  const int e = bond_edge[b];
+  const double gd = drbf_dr(drbf_b + (int64_t)b * R, freq, R, len[e], cutoff, p);
+  double g[3];
+  for (int c = 0; c < 3; ++c) g[c] = gd * xhat[3 * e + c];
+  for (int al = angle_ptr[b]; al < angle_ptr[b + 1]; ++al)
+    for (int c = 0; c < 3; ++c) g[c] += pang[6 * (int64_t)al + c];
+  const int i = bond_src[b], k0 = bond_ptr[i], k = bond_ptr[i + 1] - k0, q = b - k0;
+  for (int pp = 0; pp < k; ++pp) {
+    if (pp == q) continue;
+    const int64_t al = angle_ptr[k0 + pp] + (q < pp ? q : q - 1);
+    for (int c = 0; c < 3; ++c) g[c] += pang[6 * al + 3 + c];
+  }
+  for (int c = 0; c < 3; ++c) gvec[3 * e + c] += (float)g[c];
+}
+
+// F_i = sum over edges e leaving i of (g_e - g_rev(e)); one wavefront per atom.
+__global__ void __launch_bounds__(256) k_cons_forces(int N, const int* __restrict__ edge_ptr,
+                                                     const int* __restrict__ edge_rev, const float* __restrict__ gvec,
+                                                     float* __restrict__ forces) {
+  const int i = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (i >= N) return;
+  float f[3] = {0.f, 0.f, 0.f};
+  for (int e = edge_ptr[i] + lane; e < edge_ptr[i + 1]; e += 64) {
+    const int r = edge_rev[e];
+    for (int c = 0; c < 3; ++c) f[c] += gvec[3 * e + c] - gvec[3 * r + c];
+  }
+  for (int c = 0; c < 3; ++c) f[c] = wsum(f[c]);
+  if (lane == 0)
+    for (int c = 0; c < 3; ++c) forces[3 * i + c] = f[c];
+}
+
+// sigma_s = (1/V_s) sum over the edges of crystal s of g_e r_e^T; one block per crystal.
+__global__ void __launch_bounds__(256) k_cons_stress(int S, const int* __restrict__ atom_ptr,
+                                                     const int* __restrict__ edge_ptr, const float* __restrict__ len,
+                                                     const float* __restrict__ xhat, const float* __restrict__ gvec,
+                                                     const float* __restrict__ lattice, float* __restrict__ stress) {
+  const int s = blockIdx.x;
+  __shared__ double red[9][256];
+  double acc[9];
+  for (int k = 0; k < 9; ++k) acc[k] = 0.0;
+  for (int e = edge_ptr[atom_ptr[s]] + threadIdx.x; e < edge_ptr[atom_ptr[s + 1]]; e += 256) {
+    const double l = len[e];
+    for (int a = 0; a < 3; ++a)
+      for (int b = 0; b < 3; ++b) acc[3 * a + b] += (double)gvec[3 * e + a] * l * (double)xhat[3 * e + b];
+  }
+  for (int k = 0; k < 9; ++k) red[k][threadIdx.x] = acc[k];
+  __syncthreads();
+  for (int off = 128; off > 0; off >>= 1) {
+    if ((int)threadIdx.x < off)
+      for (int k = 0; k < 9; ++k) red[k][threadIdx.x] += red[k][threadIdx.x + off];
+    __syncthreads();
+  }
+  if (threadIdx.x < 9) {
+    double U[9], vol;
+    lattice_units(lattice + 9 * s, U, vol);
+    stress[9 * s + threadIdx.x] = (float)(red[threadIdx.x][0] / vol);
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Velocity Verlet (NVE, fixed lattices). h = dt/2 times the acceleration of
 // 1 eV/A on 1 u in A/fs^2.
 // ---------------------------------------------------------------------------
@@ -1221,6 +1370,8 @@ struct Acts {
   float *dE, *dF, *dS, *dM, *out_E, *out_F, *out_S, *out_M;
   // molecular dynamics: trial positions and velocities
   float *md_pos, *md_vel;
+  // conservative readout: dE/d FT [A,K], dE/dr_e [E,3], per-angle d theta terms [A,6]
+  float *dft, *gvec, *pang;
 };
 
 void carve_acts(Arena& ar, const Dims& m, Acts& a, int64_t n_params_aligned) {
@@ -1311,6 +1462,9 @@ void carve_acts(Arena& ar, const Dims& m, Acts& a, int64_t n_params_aligned) {
   a.out_F = ar.take<float>(3 * N);
   a.out_S = ar.take<float>(9 * S);
   a.out_M = ar.take<float>(N);
+  a.dft = ar.take<float>(A * K);
+  a.gvec = ar.take<float>(3 * E);
+  a.pang = ar.take<float>(6 * A);
 }
 
 // ---------------------------------------------------------------------------
@@ -1553,7 +1707,7 @@ int gate_bwd_launch(int D, GateBwdJobs J, float* const* ln_grad, const Acts& a, 
     K.j[K.n] = J.j[i];
     K.j[K.n].block0 = blocks;
     K.j[K.n].lnpart = a.lnpart + (int64_t)i * a.lnpart_stride;
-    R.j[R.n] = ReduceJob{K.j[K.n].lnpart, nb, 4 * D, 4 * D, ln_grad[i]};
+    R.j[R.n] = ReduceJob{K.j[K.n].lnpart, nb, 4 * D, 4 * D, ln_grad ? ln_grad[i] : nullptr};
     blocks += nb;
     K.n++;
     R.n++;
@@ -1561,7 +1715,7 @@ int gate_bwd_launch(int D, GateBwdJobs J, float* const* ln_grad, const Acts& a, 
   if (blocks == 0) return CHGNET_OK;
   if (D == 64) KLAUNCH(st, "k_gate_bwd", k_gate_bwd<64><<<blocks, 256, 0, st>>>(K));
   else KLAUNCH(st, "k_gate_bwd", k_gate_bwd<128><<<blocks, 256, 0, st>>>(K));
-  return reduce_rows_multi(R, a.red2, st);
+  return ln_grad ? reduce_rows_multi(R, a.red2, st) : CHGNET_OK;
 }
 
 GateAdds adds(int n, const float* p0, int ld0, const int* i0, const float* p1, int ld1, const int* i1) {
@@ -1873,8 +2027,10 @@ int forward_impl(Ctx& c, const float* Pflat, float* energy, float* forces, float
 // ---------------------------------------------------------------------------
 // Backward (weights only).
 // ---------------------------------------------------------------------------
+// G == nullptr: input gradients only (no weight gradients); dft_out != nullptr:
+// also dE/d FT = da^0 W_th^T [A,K] for the conservative readout.
 int backward_impl(Ctx& c, const float* Pflat, bool repack, const float* dE, const float* dF, const float* dS,
-                  const float* dM, float* G, hipStream_t st) {
+                  const float* dM, float* G, hipStream_t st, float* dft_out = nullptr) {
   const Dims& m = c.dm;
   Acts& a = c.a;
   const ParamLayout& L = c.La;   // reads from the aligned weight copy
@@ -1886,7 +2042,8 @@ int backward_impl(Ctx& c, const float* Pflat, bool repack, const float* dE, cons
   const int D = m.D, V = D / 64;
   const int64_t N = m.N, E = m.E, B = m.B, A = m.A;
 
-  CHG_TRY(fill(G, Lg.total, 0.f, st));
+  const bool wg = G != nullptr;
+  if (wg) CHG_TRY(fill(G, Lg.total, 0.f, st));
 
   // heads
   KLAUNCH(st, "k_seed_atoms", k_seed_atoms<<<(unsigned)cdiv(N, 256), 256, 0, st>>>((int)N, a.atom_struct, bt.lattice, dE, dS, a.doE, a.doS));
@@ -1963,7 +2120,7 @@ int backward_impl(Ctx& c, const float* Pflat, bool repack, const float* dE, cons
       ts.push_back(tp(N, D, 1, a.v[m.T], D, 0, nullptr, a.gM, 1, 0, nullptr, G + Lg.M_W, 1));
       ts.push_back(tp(N, 1, 1, nullptr, 0, 0, nullptr, a.gM, 1, 0, nullptr, G + Lg.M_b, 1));
     }
-    CHG_TRY(run_tns(ts, a, st, "tn_heads"));
+    if (wg) CHG_TRY(run_tns(ts, a, st, "tn_heads"));
   }
 
   // interaction blocks in reverse
@@ -2003,7 +2160,7 @@ int backward_impl(Ctx& c, const float* Pflat, bool repack, const float* dE, cons
         J.j[J.n++] = bwd_job(BWD_ANGLE, A, a.zae[t] + 2 * D, 4 * D, ad_an, ln_ptrs(P, lo.an), a.da[cur], nullptr,
                              nullptr, nullptr, nullptr, a.dzae + 2 * D, 4 * D);
       }
-      return gate_bwd_launch(D, J, lg_out, a, st);
+      return gate_bwd_launch(D, J, wg ? lg_out : nullptr, a, st);
     };
     // per-bond sums of dz over the bond's two angle roles (DZ12) from `ncols`
     // columns of dzae starting at col0; with_deb also forms d e^b
@@ -2180,14 +2337,14 @@ int backward_impl(Ctx& c, const float* Pflat, bool repack, const float* dE, cons
       } else {
         ts.push_back(tp(A, D, 2 * D, a.a[t], D, 0, nullptr, a.dzae, 4 * D, 0, nullptr, G + lg.be.W + 3 * D * 2 * D, 2 * D));
       }
-      CHG_TRY(run_tns(ts, a, st, "tn_in"));
+      if (wg) CHG_TRY(run_tns(ts, a, st, "tn_in"));
       ts.clear();
     }
     cur = nx;
   }
 
   // embeddings
-  KLAUNCH(st, "k_embed_bwd_Z", k_embed_bwd_Z<<<24, 256, 0, st>>>((int)N, D, bt.Z, a.dv[cur], G + Lg.W_Z));
+  if (wg) KLAUNCH(st, "k_embed_bwd_Z", k_embed_bwd_Z<<<24, 256, 0, st>>>((int)N, D, bt.Z, a.dv[cur], G + Lg.W_Z));
   {
     std::vector<TnProblem> ts;
     ts.push_back(tp(E, m.R, D, a.rbf_a, m.R, 0, nullptr, a.de[cur], D, 0, nullptr, G + Lg.W_e, 2 * D));
@@ -2196,7 +2353,7 @@ int backward_impl(Ctx& c, const float* Pflat, bool repack, const float* dE, cons
     ts.push_back(tp(B, m.R, D, a.rbf_b, m.R, 0, nullptr, a.deb, D, 0, nullptr, G + Lg.W_eb, D));
     ts.push_back(tp(A, m.K, D, a.ft, m.K, 0, nullptr, a.da[cur], D, 0, nullptr, G + Lg.W_th, D));
     ts.push_back(tp(A, 1, D, nullptr, 0, 0, nullptr, a.da[cur], D, 0, nullptr, G + Lg.b_th, D));
-    CHG_TRY(run_tns(ts, a, st, "tn_embed"));
+    if (wg) CHG_TRY(run_tns(ts, a, st, "tn_embed"));
     std::vector<GemmProblem> ps;
     GemmProblem p = gp(E, m.R, a.drbf_a, m.R);
     seg(p, a.de[cur], D, 0, D, P + L.W_e, 2 * D, 1);
@@ -2205,7 +2362,13 @@ int backward_impl(Ctx& c, const float* Pflat, bool repack, const float* dE, cons
     p = gp(B, m.R, a.drbf_b, m.R);
     seg(p, a.deb, D, 0, D, P + L.W_eb, D, 1);
     ps.push_back(p);
+    if (dft_out) {
+      p = gp(A, m.K, dft_out, m.K);
+      seg(p, a.da[cur], D, 0, D, P + L.W_th, D, 1);
+      ps.push_back(p);
+    }
     CHG_TRY(run_gemms(ps, st, "gemm_embed_bwd"));
+    if (!wg) return CHGNET_OK;
     if (E > 0) {
       const int64_t nb = cdiv(E, kFreqRowsPerBlock);
       KLAUNCH(st, "k_rbf_fgrad", k_rbf_fgrad<<<(unsigned)nb, 256, 0, st>>>((int)E, nullptr, a.edge_len, P + L.f_a, m.R, c.hp->r_atom,
@@ -2224,6 +2387,49 @@ int backward_impl(Ctx& c, const float* Pflat, bool repack, const float* dE, cons
 
 }  // namespace
 
+// Conservative readout after a forward pass: the backward of E with respect
+// to the inputs of the bases (no weight gradients), then dE/dr_e per edge,
+// forces and stresses.
+int conservative_impl(Ctx& c, float* forces, float* stress, hipStream_t st) {
+  Acts& a = c.a;
+  const Dims& m = c.dm;
+  const ParamLayout& L = c.La;
+  const float* P = a.Pal;
+  const chgnet_graph& g = *c.graph;
+  const chgnet_batch& bt = *c.batch;
+  const int64_t N = m.N, S = m.S, E = m.E, B = m.B, A = m.A;
+  CHG_TRY(fill(a.dE, S, 1.f, st));
+  CHG_TRY(fill(a.dF, 3 * N, 0.f, st));
+  CHG_TRY(fill(a.dS, 9 * S, 0.f, st));
+  CHG_TRY(backward_impl(c, nullptr, false, a.dE, a.dF, a.dS, nullptr, nullptr, st, a.dft));
+  const int p = c.hp->envelope_p;
+  if (E > 0)
+    KLAUNCH(st, "k_cons", k_cons_edges<<<(unsigned)cdiv(E, 256), 256, 0, st>>>((int)E, a.edge_len, a.edge_xhat, a.drbf_a,
+                                                                              P + L.f_a, m.R, c.hp->r_atom, p, a.gvec));
+  if (A > 0)
+    KLAUNCH(st, "k_cons", k_cons_angles<<<(unsigned)cdiv(A, 256), 256, 0, st>>>((int)A, a.ang_b1, a.ang_b2, g.bond_edge,
+                                                                               a.ang_ctr, g.edge_dst, g.edge_img,
+                                                                               a.atom_struct, bt.pos, bt.lattice, a.dft,
+                                                                               m.K, a.pang));
+  if (B > 0)
+    KLAUNCH(st, "k_cons", k_cons_bonds<<<(unsigned)cdiv(B, 256), 256, 0, st>>>((int)B, g.bond_edge, a.bond_src, g.bond_ptr,
+                                                                              g.angle_ptr, a.edge_len, a.edge_xhat,
+                                                                              a.drbf_b, P + L.f_b, m.R, c.hp->r_bond, p,
+                                                                              a.pang, a.gvec));
+  KLAUNCH(st, "k_cons", k_cons_forces<<<(unsigned)cdiv(N, 4), 256, 0, st>>>((int)N, g.edge_ptr, g.edge_rev, a.gvec, forces));
+  KLAUNCH(st, "k_cons", k_cons_stress<<<(unsigned)S, 256, 0, st>>>((int)S, bt.atom_ptr, g.edge_ptr, a.edge_len,
+                                                                      a.edge_xhat, a.gvec, bt.lattice, stress));
+  return CHGNET_OK;
+}
+
+// Forward pass with the readout the hyperparameters select.
+int forward_full(Ctx& c, const float* Pflat, float* energy, float* forces, float* stress, float* magmom,
+                 hipStream_t st, bool pack = true) {
+  CHG_TRY(forward_impl(c, Pflat, energy, forces, stress, magmom, st, pack));
+  if (c.hp->conservative) CHG_TRY(conservative_impl(c, forces, stress, st));
+  return CHGNET_OK;
+}
+
 size_t acts_bytes(const chgnet_hparams& hp, int64_t N, int64_t E, int64_t B, int64_t A, int64_t S) {
   Arena ar;
   Acts a;
@@ -2239,7 +2445,7 @@ int forward_entry(const chgnet_hparams* hp, const chgnet_batch* batch, const chg
   CHG_TRY(make_ctx(hp, batch, graph, ws, ws_bytes, c));
   if (!params || !energy || !forces || !stress) return fail(CHGNET_EINVAL, "forward: null output or params");
   if (magmom && !hp->magmom) return fail(CHGNET_EINVAL, "forward: magmom output without the magnetic-moment head");
-  return forward_impl(c, params, energy, forces, stress, magmom, st);
+  return forward_full(c, params, energy, forces, stress, magmom, st);
 }
 
 int backward_entry(const chgnet_hparams* hp, const chgnet_batch* batch, const chgnet_graph* graph, const float* params,
@@ -2249,6 +2455,8 @@ int backward_entry(const chgnet_hparams* hp, const chgnet_batch* batch, const ch
   CHG_TRY(make_ctx(hp, batch, graph, ws, ws_bytes, c));
   if (!params || !dE || !dF || !dS || !grad) return fail(CHGNET_EINVAL, "backward: null argument");
   if (dM && !hp->magmom) return fail(CHGNET_EINVAL, "backward: dM without the magnetic-moment head");
+  if (hp->conservative)
+    return fail(CHGNET_EINVAL, "backward: the conservative readout needs second derivatives (not supported)");
   return backward_impl(c, params, true, dE, dF, dS, dM, grad, st);
 }
 
@@ -2258,6 +2466,8 @@ int step_entry(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_graph
                size_t ws_bytes, hipStream_t st) {
   if (!params || !E_t || !F_t || !S_t || !loss_cfg || !loss || !grad) return fail(CHGNET_EINVAL, "step: null argument");
   CHG_TRY(validate_hparams(hp));
+  if (hp->conservative)
+    return fail(CHGNET_EINVAL, "step: training through the conservative readout needs second derivatives (not supported)");
   if ((M_t != nullptr) != (hp->magmom != 0))
     return fail(CHGNET_EINVAL, "step: M_target is required with the magnetic-moment head and only with it");
   if (!std::isfinite(loss_cfg->huber_delta)) return fail(CHGNET_EINVAL, "step: huber_delta is not finite");
@@ -2303,7 +2513,7 @@ int md_entry(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_graph* 
     CHG_TRY(build_graph(hp, b, graph, ws, ws_bytes, st));
     Ctx c;
     CHG_TRY(make_ctx(hp, b, graph, ws, ws_bytes, c));
-    CHG_TRY(forward_impl(c, params, s->energy ? s->energy : c.a.out_E, s->forces, s->stress ? s->stress : c.a.out_S,
+    CHG_TRY(forward_full(c, params, s->energy ? s->energy : c.a.out_E, s->forces, s->stress ? s->stress : c.a.out_S,
                          nullptr, st, !packed));
     packed = true;
     return CHGNET_OK;

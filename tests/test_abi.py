@@ -54,7 +54,8 @@ def test_workspace_size_monotone(L):
 
 @pytest.mark.parametrize("kw", [dict(d=32), dict(d=96), dict(n_layers=0), dict(n_layers=17), dict(n_fourier=30),
                                 dict(n_rbf=0), dict(n_rbf=65), dict(r_bond=7.0), dict(r_atom=25.0, r_bond=3.0),
-                                dict(envelope_p=1), dict(magmom=2), dict(sequential=-1)])
+                                dict(envelope_p=1), dict(magmom=2), dict(sequential=-1),
+                                dict(conservative=3)])
 def test_bad_hparams_rejected(L, kw):
     with pytest.raises(L.ChgnetError) as e:
         L.param_count(L.hparams(**kw))
