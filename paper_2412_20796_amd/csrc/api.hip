@@ -50,6 +50,8 @@ int prof_mark(hipStream_t st) {
   return i;
 }
 
+bool prof_active() { return g_prof.on; }
+
 void prof_close(hipStream_t st, int first, const char* tag) {
   if (first < 0) return;
   (void)hipEventRecord(g_prof.ev[first + 1], st);

@@ -40,6 +40,7 @@ int fail(int code, const std::string& msg);
 // Optional per-launch timing (measurement only; off unless enabled through
 // chgnet_profile_start). Events bracket each launch on its own stream.
 int prof_mark(hipStream_t st);                       // returns event index or -1
+bool prof_active();
 void prof_close(hipStream_t st, int first, const char* tag);
 
 #define KLAUNCH(st, tag, ...)                                                                 \

@@ -35,7 +35,8 @@ constexpr int kFreqRowsPerBlock = 64;  // rows per block in frequency-gradient k
 constexpr int kReduceGroups = 32;      // first-level groups of the ordered partial-sum reduction
 constexpr int64_t kTnPartFloats = 64ll << 20;
 
-__device__ __forceinline__ float sigm(float x) { return 1.0f / (1.0f + __expf(-x)); }
+// logistic sigmoid; the hardware reciprocal (about 1 ulp) instead of an IEEE division
+__device__ __forceinline__ float sigm(float x) { return __builtin_amdgcn_rcpf(1.0f + __expf(-x)); }
 
 __device__ __forceinline__ float wsum(float v) {
 #pragma unroll
@@ -268,8 +269,10 @@ __device__ __forceinline__ void ln_stats(float (&zc)[CPL], float (&zg)[CPL], flo
     vc += zc[k] * zc[k];
     vg += zg[k] * zg[k];
   }
-  rc = rsqrtf(rowsum<LPR>(vc) * (1.0f / D) + kLnEps);
-  rg = rsqrtf(rowsum<LPR>(vg) * (1.0f / D) + kLnEps);
+  // the argument is at least the LayerNorm epsilon: the hardware reciprocal
+  // square root needs no denormal scaling
+  rc = __builtin_amdgcn_rsqf(rowsum<LPR>(vc) * (1.0f / D) + kLnEps);
+  rg = __builtin_amdgcn_rsqf(rowsum<LPR>(vg) * (1.0f / D) + kLnEps);
 #pragma unroll
   for (int k = 0; k < CPL; ++k) {
     zc[k] *= rc;
@@ -436,8 +439,14 @@ __device__ __forceinline__ void gate_mm_gather(const GateMmJob& J, const int (&i
   load_cols<D, CPL>(J.mulv + (int64_t)ix[kMaxAdds] * D, j, in.mv);
 }
 
+// LayerNorm scale and shift (core and gate) of this lane's columns
+struct GateLnRegs {
+  float gc[kMmCpl], bc[kMmCpl], gg[kMmCpl], bg[kMmCpl];
+};
+
 template <int MODE>
-__device__ __forceinline__ void gate_mm_row(const GateMmJob& J, int row, int lr, const float* Zs, const GateRowIn& in) {
+__device__ __forceinline__ void gate_mm_row(const GateMmJob& J, int row, int lr, const float* Zs, const GateRowIn& in,
+                                            const GateLnRegs& ln) {
   constexpr int D = 64, CPL = kMmCpl;
   using L = Lanes<D, CPL>;
   const int j = (threadIdx.x & 63) % L::LPR;
@@ -462,9 +471,8 @@ __device__ __forceinline__ void gate_mm_row(const GateMmJob& J, int row, int lr,
   float o[CPL];
 #pragma unroll
   for (int k = 0; k < CPL; ++k) {
-    const int c = L::col(j, k);
-    const float yc = J.ln.gc[c] * zc[k] + J.ln.bc[c];
-    const float yg = J.ln.gg[c] * zg[k] + J.ln.bg[c];
+    const float yc = ln.gc[k] * zc[k] + ln.bc[k];
+    const float yg = ln.gg[k] * zg[k] + ln.bg[k];
     const float phi = yc * sigm(yc) * sigm(yg);
     o[k] = MODE == FWD_ANGLE ? in.mv[k] + phi : in.mv[k] * phi;
   }
@@ -545,8 +553,18 @@ __device__ __forceinline__ void mm_tile(const float* X, float* Z, const float (&
 __global__ void __launch_bounds__(kMmThreads, 1) k_gate_fwd_mm(GateMmJobs J) {
   __shared__ __attribute__((aligned(16))) float Xs[2][kMmRows * kMmXld];
   __shared__ __attribute__((aligned(16))) float Zs[2][kMmRows * kMmZld];
+  // LayerNorm parameters of every job: [job][gc, bc, gg, bg][64]
+  __shared__ __attribute__((aligned(16))) float LnS[3][4][64];
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  {
+    static_assert(kMmThreads == 3 * 4 * 64, "one LayerNorm value per thread");
+    const int t = threadIdx.x, jb = t / 256, q = (t / 64) % 4, c = t % 64;
+    if (jb < J.n) {
+      const LnPtrs& ln = J.j[jb].ln;
+      LnS[jb][q][c] = (q == 0 ? ln.gc : q == 1 ? ln.bc : q == 2 ? ln.gg : ln.bg)[c];
+    }
+  }
   auto job_of = [&](int tile) {
     int k = 0;
     while (k + 1 < J.n && tile >= J.j[k + 1].tile0) ++k;
@@ -590,6 +608,8 @@ __global__ void __launch_bounds__(kMmThreads, 1) k_gate_fwd_mm(GateMmJobs J) {
     const int lr = (wave - kMmProducers) * GL::RPW + lane / GL::LPR;
     auto row_of = [&](int tile, const GateMmJob& jb) { return (tile - jb.tile0) * kMmRows + lr; };
     GateRowIn in;
+    GateLnRegs lnr;
+    int lnjob = -1;
     int ix[kMaxAdds + 1];
     const GateMmJob& j0 = J.j[job_of(tile_of(0))];
     gate_mm_index(j0, row_of(tile_of(0), j0), ix);
@@ -602,12 +622,21 @@ __global__ void __launch_bounds__(kMmThreads, 1) k_gate_fwd_mm(GateMmJobs J) {
     for (int i = 0; i <= nt; ++i) {
       if (i > 0) {
         const int tile = tile_of(i - 1);
-        const GateMmJob& jb = J.j[job_of(tile)];
+        const int k = job_of(tile);
+        const GateMmJob& jb = J.j[k];
+        if (k != lnjob) {
+          lnjob = k;
+          const int jl = lane % GL::LPR;
+          load_cols<64, kMmCpl>(LnS[k][0], jl, lnr.gc);
+          load_cols<64, kMmCpl>(LnS[k][1], jl, lnr.bc);
+          load_cols<64, kMmCpl>(LnS[k][2], jl, lnr.gg);
+          load_cols<64, kMmCpl>(LnS[k][3], jl, lnr.bg);
+        }
         const int row = row_of(tile, jb);
         const float* Z = Zs[(i - 1) & 1];
-        if (jb.mode == FWD_ATOM) gate_mm_row<FWD_ATOM>(jb, row, lr, Z, in);
-        else if (jb.mode == FWD_BOND) gate_mm_row<FWD_BOND>(jb, row, lr, Z, in);
-        else gate_mm_row<FWD_ANGLE>(jb, row, lr, Z, in);
+        if (jb.mode == FWD_ATOM) gate_mm_row<FWD_ATOM>(jb, row, lr, Z, in, lnr);
+        else if (jb.mode == FWD_BOND) gate_mm_row<FWD_BOND>(jb, row, lr, Z, in, lnr);
+        else gate_mm_row<FWD_ANGLE>(jb, row, lr, Z, in, lnr);
         if (i < nt) {
           const GateMmJob& jn = J.j[job_of(tile_of(i))];
           gate_mm_gather(jn, ix, in);
@@ -1359,6 +1388,9 @@ struct Acts {
   float *msg, *msgb, *Xa[kMaxLayers], *Xb[kMaxLayers];
   float *hE1, *aE1, *hE2, *aE2, *hS1, *aS1, *hS2, *aS2, *hF1, *aF1, *hF2, *aF2, *oE, *oS, *oF, *oM, *gM;
   float* dvf;  // gradient of v^{t+1} including the sequential block's bond and angle inputs
+  // two copies of the per-layer backward intermediates, alternating by layer,
+  // so a layer's weight gradients can run while the next layer is formed
+  float *dzv_pp[2], *dzae_pp[2], *AT_pp[2], *DZ12_pp[2], *dvf_pp[2];
   // backward
   float *dv[2], *de[2], *da[2], *dm, *dmu, *dzv, *dzae, *t2, *AT, *DZ12, *dea, *deb;
   float *doE, *doS, *dn, *doF, *dh2E, *dh2S, *dh2F, *dh1ES, *dh1F, *drbf_a, *drbf_b;
@@ -1421,7 +1453,8 @@ void carve_acts(Arena& ar, const Dims& m, Acts& a, int64_t n_params_aligned) {
   a.oF = ar.take<float>(E);
   a.oM = ar.take<float>(N);
   a.gM = ar.take<float>(N);
-  a.dvf = ar.take<float>(N * D);
+  for (int k = 0; k < 2; ++k) a.dvf_pp[k] = ar.take<float>(N * D);
+  a.dvf = a.dvf_pp[0];
   for (int k = 0; k < 2; ++k) {
     a.dv[k] = ar.take<float>(N * D);
     a.de[k] = ar.take<float>(E * D);
@@ -1429,11 +1462,17 @@ void carve_acts(Arena& ar, const Dims& m, Acts& a, int64_t n_params_aligned) {
   }
   a.dm = ar.take<float>(N * D);
   a.dmu = ar.take<float>(B * D);
-  a.dzv = ar.take<float>(E * 2 * D);
-  a.dzae = ar.take<float>(A * 4 * D);
+  for (int k = 0; k < 2; ++k) {
+    a.dzv_pp[k] = ar.take<float>(E * 2 * D);
+    a.dzae_pp[k] = ar.take<float>(A * 4 * D);
+    a.AT_pp[k] = ar.take<float>(N * 8 * D);
+    a.DZ12_pp[k] = ar.take<float>(B * 8 * D);
+  }
+  a.dzv = a.dzv_pp[0];
+  a.dzae = a.dzae_pp[0];
+  a.AT = a.AT_pp[0];
+  a.DZ12 = a.DZ12_pp[0];
   a.t2 = ar.take<float>(A * D);
-  a.AT = ar.take<float>(N * 8 * D);
-  a.DZ12 = ar.take<float>(B * 8 * D);
   a.dea = ar.take<float>(E * D);
   a.deb = ar.take<float>(B * D);
   a.doE = ar.take<float>(N);
@@ -2027,6 +2066,43 @@ int forward_impl(Ctx& c, const float* Pflat, float* energy, float* forces, float
 // ---------------------------------------------------------------------------
 // Backward (weights only).
 // ---------------------------------------------------------------------------
+// Weight gradients run on a second stream of the device (default priority),
+// forked from and joined back into the caller's stream by events; one set
+// per host thread and device, created on first use.
+struct SideStream {
+  hipStream_t side = nullptr;
+  hipEvent_t ready[kMaxLayers], done[kMaxLayers], heads, embed, fin;
+};
+
+int side_stream(SideStream*& out) {
+  constexpr int kMaxDevices = 64;
+  thread_local SideStream cache[kMaxDevices];
+  int dev = 0;
+  CHG_HIP(hipGetDevice(&dev));
+  if (dev < 0 || dev >= kMaxDevices) return fail(CHGNET_EHIP, "device index out of range");
+  SideStream& ss = cache[dev];
+  if (!ss.side) {
+    CHG_HIP(hipStreamCreateWithFlags(&ss.side, hipStreamNonBlocking));
+    auto mk = [](hipEvent_t& e) { return hipEventCreateWithFlags(&e, hipEventDisableTiming); };
+    for (int t = 0; t < kMaxLayers; ++t) {
+      CHG_HIP(mk(ss.ready[t]));
+      CHG_HIP(mk(ss.done[t]));
+    }
+    CHG_HIP(mk(ss.heads));
+    CHG_HIP(mk(ss.embed));
+    CHG_HIP(mk(ss.fin));
+  }
+  out = &ss;
+  return CHGNET_OK;
+}
+
+// the side stream waits for everything enqueued on st so far
+int side_fork(SideStream& ss, hipStream_t st, hipEvent_t e) {
+  CHG_HIP(hipEventRecord(e, st));
+  CHG_HIP(hipStreamWaitEvent(ss.side, e, 0));
+  return CHGNET_OK;
+}
+
 // G == nullptr: input gradients only (no weight gradients); dft_out != nullptr:
 // also dE/d FT = da^0 W_th^T [A,K] for the conservative readout.
 int backward_impl(Ctx& c, const float* Pflat, bool repack, const float* dE, const float* dF, const float* dS,
@@ -2043,7 +2119,20 @@ int backward_impl(Ctx& c, const float* Pflat, bool repack, const float* dE, cons
   const int64_t N = m.N, E = m.E, B = m.B, A = m.A;
 
   const bool wg = G != nullptr;
-  if (wg) CHG_TRY(fill(G, Lg.total, 0.f, st));
+  SideStream* ssp = nullptr;
+  if (wg) {
+    CHG_TRY(fill(G, Lg.total, 0.f, st));
+    CHG_TRY(side_stream(ssp));
+  }
+  SideStream no_side;
+  if (wg && prof_active()) {
+    // per-launch timing: everything on the caller's stream, so each
+    // launch's duration is its own
+    no_side = *ssp;
+    no_side.side = st;
+    ssp = &no_side;
+  }
+  SideStream& ss = wg ? *ssp : no_side;
 
   // heads
   KLAUNCH(st, "k_seed_atoms", k_seed_atoms<<<(unsigned)cdiv(N, 256), 256, 0, st>>>((int)N, a.atom_struct, bt.lattice, dE, dS, a.doE, a.doS));
@@ -2120,7 +2209,10 @@ int backward_impl(Ctx& c, const float* Pflat, bool repack, const float* dE, cons
       ts.push_back(tp(N, D, 1, a.v[m.T], D, 0, nullptr, a.gM, 1, 0, nullptr, G + Lg.M_W, 1));
       ts.push_back(tp(N, 1, 1, nullptr, 0, 0, nullptr, a.gM, 1, 0, nullptr, G + Lg.M_b, 1));
     }
-    if (wg) CHG_TRY(run_tns(ts, a, st, "tn_heads"));
+    if (wg) {
+      CHG_TRY(side_fork(ss, st, ss.heads));
+      CHG_TRY(run_tns(ts, a, ss.side, "tn_heads"));
+    }
   }
 
   // interaction blocks in reverse
@@ -2130,6 +2222,11 @@ int backward_impl(Ctx& c, const float* Pflat, bool repack, const float* dE, cons
     const LayerOffsets& lg = Lg.layer[t];
     const bool ang = lo.has_angle;
     const int W4 = ang ? 4 * D : 2 * D;
+    a.dzv = a.dzv_pp[t & 1];
+    a.dzae = a.dzae_pp[t & 1];
+    a.AT = a.AT_pp[t & 1];
+    a.DZ12 = a.DZ12_pp[t & 1];
+    a.dvf = a.dvf_pp[t & 1];
     const float* Wav = P + lo.av.W;
     const float* Wbe = P + lo.be.W;
     const float* Wan = P + lo.an.W;
@@ -2254,46 +2351,6 @@ int backward_impl(Ctx& c, const float* Pflat, bool repack, const float* dE, cons
     ts.push_back(tp(N, 1, D, nullptr, 0, 0, nullptr, dvo, D, 0, nullptr, G + lg.av_bo, D));
     ts.push_back(tp(B, D, D, a.mu[t], D, 0, nullptr, a.de[cur], D, 0, g.bond_edge, G + lg.be_Wo, D));
     ts.push_back(tp(B, 1, D, nullptr, 0, 0, nullptr, a.de[cur], D, 0, g.bond_edge, G + lg.be_bo, D));
-    // input gradients
-    {
-      GemmProblem p = gp(N, D, a.dv[nx], D);
-      seg(p, a.AT, 8 * D, 0, 2 * D, Wav, 2 * D, 1);
-      seg(p, a.AT, 8 * D, 2 * D, 2 * D, Wav + D * 2 * D, 2 * D, 1);
-      if (!seq) {
-        seg(p, a.AT, 8 * D, 4 * D, 2 * D, Wbe, 2 * D, 1);
-        if (ang) seg(p, a.AT, 8 * D, 6 * D, 2 * D, Wan, 2 * D, 1);
-      }
-      p.res = dvo;
-      p.res_ld = D;
-      ps.push_back(p);
-      p = gp(E, D, a.de[nx], D);
-      seg(p, a.dzv, 2 * D, 0, 2 * D, Wav + 2 * D * 2 * D, 2 * D, 1);
-      p.res = a.de[cur];
-      p.res_ld = D;
-      ps.push_back(p);
-      p = gp(A, D, a.da[nx], D);
-      seg(p, a.dzae, 4 * D, 0, 2 * D, Wbe + 3 * D * 2 * D, 2 * D, 1);
-      if (ang) {
-        seg(p, a.dzae, 4 * D, 2 * D, 2 * D, Wan + 3 * D * 2 * D, 2 * D, 1);
-        p.res = a.da[cur];
-        p.res_ld = D;
-      }
-      ps.push_back(p);
-      CHG_TRY(run_gemms(ps, st, "gemm_in_bwd"));
-      ps.clear();
-      p = gp(B, D, a.de[nx], D);
-      p.c_rows = g.bond_edge;
-      p.accumulate = 1;
-      seg(p, a.DZ12, 8 * D, 0, 2 * D, Wbe + D * 2 * D, 2 * D, 1);
-      seg(p, a.DZ12, 8 * D, 4 * D, 2 * D, Wbe + 2 * D * 2 * D, 2 * D, 1);
-      if (ang && !seq) {
-        seg(p, a.DZ12, 8 * D, 2 * D, 2 * D, Wan + D * 2 * D, 2 * D, 1);
-        seg(p, a.DZ12, 8 * D, 6 * D, 2 * D, Wan + 2 * D * 2 * D, 2 * D, 1);
-      }
-      ps.push_back(p);
-      CHG_TRY(run_gemms(ps, st, "gemm_bond_bwd"));
-      ps.clear();
-    }
     // weight gradients of the first linear layers
     {
       const float* vt = a.v[t];
@@ -2337,9 +2394,59 @@ int backward_impl(Ctx& c, const float* Pflat, bool repack, const float* dE, cons
       } else {
         ts.push_back(tp(A, D, 2 * D, a.a[t], D, 0, nullptr, a.dzae, 4 * D, 0, nullptr, G + lg.be.W + 3 * D * 2 * D, 2 * D));
       }
-      if (wg) CHG_TRY(run_tns(ts, a, st, "tn_in"));
-      ts.clear();
     }
+    // input gradients (they overwrite dv and de of the layer above, which its
+    // weight gradients read)
+    if (wg && t + 1 < m.T) CHG_HIP(hipStreamWaitEvent(st, ss.done[t + 1], 0));
+    {
+      GemmProblem p = gp(N, D, a.dv[nx], D);
+      seg(p, a.AT, 8 * D, 0, 2 * D, Wav, 2 * D, 1);
+      seg(p, a.AT, 8 * D, 2 * D, 2 * D, Wav + D * 2 * D, 2 * D, 1);
+      if (!seq) {
+        seg(p, a.AT, 8 * D, 4 * D, 2 * D, Wbe, 2 * D, 1);
+        if (ang) seg(p, a.AT, 8 * D, 6 * D, 2 * D, Wan, 2 * D, 1);
+      }
+      p.res = dvo;
+      p.res_ld = D;
+      ps.push_back(p);
+      p = gp(E, D, a.de[nx], D);
+      seg(p, a.dzv, 2 * D, 0, 2 * D, Wav + 2 * D * 2 * D, 2 * D, 1);
+      p.res = a.de[cur];
+      p.res_ld = D;
+      ps.push_back(p);
+      p = gp(A, D, a.da[nx], D);
+      seg(p, a.dzae, 4 * D, 0, 2 * D, Wbe + 3 * D * 2 * D, 2 * D, 1);
+      if (ang) {
+        seg(p, a.dzae, 4 * D, 2 * D, 2 * D, Wan + 3 * D * 2 * D, 2 * D, 1);
+        p.res = a.da[cur];
+        p.res_ld = D;
+      }
+      ps.push_back(p);
+      CHG_TRY(run_gemms(ps, st, "gemm_in_bwd"));
+      ps.clear();
+      p = gp(B, D, a.de[nx], D);
+      p.c_rows = g.bond_edge;
+      p.accumulate = 1;
+      seg(p, a.DZ12, 8 * D, 0, 2 * D, Wbe + D * 2 * D, 2 * D, 1);
+      seg(p, a.DZ12, 8 * D, 4 * D, 2 * D, Wbe + 2 * D * 2 * D, 2 * D, 1);
+      if (ang && !seq) {
+        seg(p, a.DZ12, 8 * D, 2 * D, 2 * D, Wan + D * 2 * D, 2 * D, 1);
+        seg(p, a.DZ12, 8 * D, 6 * D, 2 * D, Wan + 2 * D * 2 * D, 2 * D, 1);
+      }
+      ps.push_back(p);
+      CHG_TRY(run_gemms(ps, st, "gemm_bond_bwd"));
+      ps.clear();
+    }
+    // the weight gradients of this layer run on the side stream, overlapping
+    // the gate backward of the next layer; the buffers they read are not
+    // written again before the wait on done(t) in the next layer (the
+    // intermediates alternate between two copies by layer)
+    if (wg) {
+      CHG_TRY(side_fork(ss, st, ss.ready[t]));
+      CHG_TRY(run_tns(ts, a, ss.side, "tn_in"));
+      CHG_HIP(hipEventRecord(ss.done[t], ss.side));
+    }
+    ts.clear();
     cur = nx;
   }
 
@@ -2353,7 +2460,10 @@ int backward_impl(Ctx& c, const float* Pflat, bool repack, const float* dE, cons
     ts.push_back(tp(B, m.R, D, a.rbf_b, m.R, 0, nullptr, a.deb, D, 0, nullptr, G + Lg.W_eb, D));
     ts.push_back(tp(A, m.K, D, a.ft, m.K, 0, nullptr, a.da[cur], D, 0, nullptr, G + Lg.W_th, D));
     ts.push_back(tp(A, 1, D, nullptr, 0, 0, nullptr, a.da[cur], D, 0, nullptr, G + Lg.b_th, D));
-    if (wg) CHG_TRY(run_tns(ts, a, st, "tn_embed"));
+    if (wg) {
+      CHG_TRY(side_fork(ss, st, ss.embed));
+      CHG_TRY(run_tns(ts, a, ss.side, "tn_embed"));
+    }
     std::vector<GemmProblem> ps;
     GemmProblem p = gp(E, m.R, a.drbf_a, m.R);
     seg(p, a.de[cur], D, 0, D, P + L.W_e, 2 * D, 1);
@@ -2382,6 +2492,9 @@ int backward_impl(Ctx& c, const float* Pflat, bool repack, const float* dE, cons
       CHG_TRY(reduce_rows_launch(a.fpart, (int)nb, m.R, m.R, G + Lg.f_b, a.red2, st));
     }
   }
+  // join: later work on the caller's stream sees every weight gradient
+  CHG_HIP(hipEventRecord(ss.fin, ss.side));
+  CHG_HIP(hipStreamWaitEvent(st, ss.fin, 0));
   return CHGNET_OK;
 }
 
