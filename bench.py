@@ -35,7 +35,9 @@ def parse():
     ap.add_argument("--huber", type=float, default=0.0, help="model variant: Huber loss with this delta (0 = MSE)")
     ap.add_argument("--sequential", action="store_true", help="model variant: the Eq. (10) interaction block")
     ap.add_argument("--conservative", action="store_true",
-                    help="with --md: forces and stress as derivatives of the energy (no training through it)")
+                    help="with --md or --forward-only: forces and stress as derivatives of the energy")
+    ap.add_argument("--forward-only", action="store_true",
+                    help="time inference (graph build + forward with the readout) instead of training steps")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample", type=int, default=0, help="structures in the CPU oracle sample (0 = auto)")
     ap.add_argument("--no-roofline", action="store_true")
@@ -72,11 +74,12 @@ def main():
     if args.md:
         print(json.dumps(md_bench(args, bd, synth, dev)), flush=True)
         return
-    if args.conservative:
-        print("bench.py: training through the conservative readout is not supported (use --md)", file=sys.stderr)
+    if args.conservative and not args.forward_only:
+        print("bench.py: training through the conservative readout is not supported (use --md or --forward-only)",
+              file=sys.stderr)
         sys.exit(2)
     b, params, targets, d, T = synth.workload_inputs(args.workload, magmom=args.magmom)
-    hp = bd.hparams(d=d, n_layers=T, magmom=args.magmom, sequential=args.sequential)
+    hp = bd.hparams(d=d, n_layers=T, magmom=args.magmom, sequential=args.sequential, conservative=args.conservative)
     db = bd.DeviceBatch.from_host(b, dev)
     g = bd.DeviceGraph(b.n_atoms, 1024, 256, 1024, dev)
     ws = bd.Workspace(dev)
@@ -92,6 +95,10 @@ def main():
 
     def one_step():
         step_no[0] += 1
+        if args.forward_only:
+            bd.build_graph(hp, db, g, ws)
+            bd.forward(hp, db, g, p, ws)
+            return
         bd.step(hp, db, g, p, tg, ws, loss_w=(2.0, 1.5, 0.1, 0.1), huber_delta=args.huber, grad=grad, loss=loss,
                 adam=(m, v, (lr, b1, b2, eps, float(step_no[0]))))
 
@@ -121,7 +128,8 @@ def main():
     value = S / (ms * 1e-3)
 
     out = {
-        "metric": "training structures/sec (fwd+bwd) on 1 MI355X",
+        "metric": ("inference structures/sec (graph + forward) on 1 MI355X" if args.forward_only
+                   else "training structures/sec (fwd+bwd) on 1 MI355X"),
         "value": round(value, 2),
         "unit": "structures/s",
         "n_gpus": 1,
@@ -137,7 +145,9 @@ def main():
                    "angles": A, "d": d, "layers": T, "parallelism": "single GPU",
                    "block": "Eq. 10 (sequential)" if args.sequential else "Eq. 11",
                    "loss": "Huber delta=%g" % args.huber if args.huber > 0 else "MSE",
-                   "heads": "E, F, S, magmom" if args.magmom else "E, F, S"},
+                   "heads": "E, F, S, magmom" if args.magmom else "E, F, S",
+                   "readout": "conservative (F = -dE/dr)" if args.conservative else "direct force/stress heads",
+                   "step": "graph + forward" if args.forward_only else "graph + forward + loss + backward + Adam"},
         "edges_per_s": round(E / (ms * 1e-3), 1),
         "angles_per_s": round(A / (ms * 1e-3), 1),
         "ms_per_step_median": round(float(np.median(per_step)), 4),
@@ -404,13 +414,21 @@ def cpu_baseline(workload, sample, min_seconds=10.0, variant=None):
     n = ptr[-1]
     sb = synth.Batch(np.asarray(ptr, np.int32), b.pos[:n], b.lattice[:sample], b.Z[:n])
     tgt = (targets[0][:sample], targets[1][:n], targets[2][:sample]) + ((targets[3][:n],) if mag else ())
-    hp = om.HParams(d=d, n_layers=T, magmom=mag, sequential=bool(variant and variant.sequential))
+    fwd = bool(variant and variant.forward_only)
+    hp = om.HParams(d=d, n_layers=T, magmom=mag, sequential=bool(variant and variant.sequential),
+                    conservative=bool(variant and variant.conservative))
     delta = variant.huber if variant and variant.huber > 0 else None
     reps = 0
     t = time.perf_counter()
     n_edges = 0
     while True:
-        _, _, _, graph = om.step(hp, sb, params.astype(np.float64), tgt, delta=delta)
+        if fwd:
+            from oracle import graph as og
+
+            graph = og.build_graph(sb.atom_ptr, sb.pos, sb.lattice, hp.r_atom, hp.r_bond)
+            om.forward(hp, sb, graph, params.astype(np.float64))
+        else:
+            _, _, _, graph = om.step(hp, sb, params.astype(np.float64), tgt, delta=delta)
         n_edges = len(graph["edge_dst"])
         reps += 1
         dt = time.perf_counter() - t
@@ -424,8 +442,9 @@ def cpu_baseline(workload, sample, min_seconds=10.0, variant=None):
         threads = 1
     return {"value": round(reps * sample / dt, 4), "unit": "structures/s", "cores": threads, "kind": "oracle",
             "host_cpus": len(os.sched_getaffinity(0)), "edges_per_s": round(reps * n_edges / dt, 1),
-            "sample": "%d of the %d structures (%d atoms), %d full step(s) (graph, forward, loss, backward) in %.1f s"
-                      % (sample, b.n_struct, n, reps, dt)}
+            "sample": "%d of the %d structures (%d atoms), %d %s in %.1f s"
+                      % (sample, b.n_struct, n, reps, "inference(s) (graph, forward)" if fwd
+                         else "full step(s) (graph, forward, loss, backward)", dt)}
 
 
 if __name__ == "__main__":
