@@ -152,15 +152,24 @@ template <int BN, int ROLE>
 __global__ void __launch_bounds__(256) k_gemm(GemmBatch batch) {
   constexpr int BM = 128, KC = 32, NT = BN / 32, KP = KC + 4, SP = 64 + 4;
   const GemmProblem& P = batch.p[blockIdx.z];
-  const int c0 = blockIdx.y * BN;
+  // Workgroups are dealt to the 8 XCDs round-robin by linear id (gridDim.x
+  // is a multiple of 8). Renumber so that the column tiles of one row worker
+  // share an XCD, and its A rows are fetched into one L2.
+  int bx, by;
+  {
+    const int p = blockIdx.x + gridDim.x * blockIdx.y, j = p >> 3;
+    by = j % gridDim.y;
+    bx = 8 * (j / gridDim.y) + (p & 7);
+  }
+  const int c0 = by * BN;
   const int ntiles = (P.M + BM - 1) / BM;
-  if ((int)blockIdx.x >= ntiles || c0 >= P.N) return;
+  if (bx >= ntiles || c0 >= P.N) return;
   // Operand tiles are stored k-contiguous: As[row][k], Bs[col][k]. In MFMA
   // k-step i, lane half h = lane / 32 supplies k = 16 h + i, so each lane
   // reads its 16 A and B values of a chunk with four 16-byte LDS reads.
   // After the K loop the same LDS holds the output tile, 64 columns at a
   // time, so the epilogue writes whole rows with 16-byte stores. A block
-  // walks row tiles blockIdx.x, blockIdx.x + gridDim.x, ...; the first chunk
+  // walks row tiles bx, bx + gridDim.x, ...; the first chunk
   // of its next tile is fetched before the current tile's epilogue.
   constexpr int kOperand = BM * KP + BN * KP, kStage = 4 * 32 * SP;
   __shared__ __attribute__((aligned(16))) float smem[kOperand > kStage ? kOperand : kStage];
@@ -180,7 +189,7 @@ __global__ void __launch_bounds__(256) k_gemm(GemmBatch batch) {
     }
   };
   GemmStage<BN> g;
-  int tile = blockIdx.x;
+  int tile = bx;
   set_rows(tile * BM);
   if (P.nseg > 0) gemm_fetch<BN>(P, P.seg[0], 0, c0, tid, arow, aval, g);
   while (tile < ntiles) {
@@ -772,9 +781,10 @@ int gemm_launch(const GemmBatch& b, hipStream_t st, const char* tag) {
     else KLAUNCH(st, tag, k_gemm_w<8><<<grid, 512, 0, st>>>(b));
     return CHGNET_OK;
   }
-  // persistent row tiles: about 2048 blocks over the launch
+  // persistent row tiles: about 2048 blocks over the launch; row workers in
+  // multiples of 8 (one per XCD, see k_gemm)
   const int per_problem = std::max(1, 2048 / (gy * b.n));
-  const dim3 grid(std::min(gx, per_problem), gy, b.n);
+  const dim3 grid((unsigned)(cdiv(std::min(gx, per_problem), 8) * 8), gy, b.n);
   const std::string t(tag);
   if (BN == 128) KLAUNCH(st, tag, k_gemm<128, 0><<<grid, 256, 0, st>>>(b));
   else if (t == "gemm_z") KLAUNCH(st, tag, k_gemm<64, 1><<<grid, 256, 0, st>>>(b));
