@@ -18,9 +18,13 @@
  *  - Floating-point data are IEEE fp32; integer data are int32 unless noted.
  *  - All matrices are row-major. A lattice is 3x3 with ROWS = lattice vectors,
  *    so Cartesian = fractional @ lattice.
- *  - No global state: calls are re-entrant as long as concurrent calls use
- *    different workspaces. Results are bitwise reproducible run to run (no
- *    floating-point atomics).
+ *  - No global data: calls are re-entrant as long as concurrent calls use
+ *    different workspaces. The backward pass overlaps its weight-gradient
+ *    products with the next layer on a second HIP stream (default priority)
+ *    that the library creates, with a few events, once per host thread and
+ *    device; it forks from and joins back into `stream`, so the call still
+ *    behaves as work enqueued on `stream`. Results are bitwise reproducible
+ *    run to run (no floating-point atomics).
  *  - Return value: CHGNET_OK (0) or a negative error code below; the text of
  *    the last error of the calling thread is chgnet_last_error_string().
  *
