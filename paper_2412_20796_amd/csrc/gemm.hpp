@@ -88,12 +88,13 @@ struct ReduceJob {
   int count;
   float* out;
 };
+constexpr int kMaxReduceJobs = 20;
 struct ReduceJobs {
   int n;
-  ReduceJob j[3];
+  ReduceJob j[kMaxReduceJobs];
 };
-// Up to 3 independent reductions in two launches (32 ordered group sums,
-// then their ordered sum); scratch: 3 * 32 * 1024 doubles.
+// Up to kMaxReduceJobs independent reductions in two launches (32 ordered
+// group sums, then their ordered sum); scratch: n * 32 * 1024 doubles.
 int reduce_rows_multi(const ReduceJobs& J, double* scratch, hipStream_t st);
 
 // out[k] += sum_c part[c*stride + k] (k < count), in a fixed order, in fp64.

@@ -601,9 +601,13 @@ int build_graph(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_grap
   KLAUNCH(st, "k_scan_counts", k_scan_counts<<<1, 1024, 0, st>>>(N, g.edge_count, g.bond_count, graph->edge_ptr, graph->bond_ptr, g.angle_base,
                                     g.ginfo));
 
-  GraphInfo hinfo;
-  CHG_HIP(hipMemcpyAsync(&hinfo, g.ginfo, sizeof(GraphInfo), hipMemcpyDeviceToHost, st));
+  // the sizes come back through a small pinned buffer (one per host thread,
+  // allocated on first use): a direct DMA instead of a staged pageable copy
+  thread_local GraphInfo* pinned = nullptr;
+  if (!pinned) CHG_HIP(hipHostMalloc(reinterpret_cast<void**>(&pinned), sizeof(GraphInfo), hipHostMallocDefault));
+  CHG_HIP(hipMemcpyAsync(pinned, g.ginfo, sizeof(GraphInfo), hipMemcpyDeviceToHost, st));
   CHG_HIP(hipStreamSynchronize(st));
+  const GraphInfo hinfo = *pinned;
   if (hinfo.err) {
     std::string m = "build_graph: invalid input:";
     if (hinfo.err & ERR_Z) m += " Z outside 1..94;";

@@ -1488,11 +1488,13 @@ void carve_acts(Arena& ar, const Dims& m, Acts& a, int64_t n_params_aligned) {
   a.drbf_b = ar.take<float>(B * R);
   const int64_t gate_blocks = cdiv(std::max<int64_t>(std::max(E, A), 1), kGateRows);
   a.lnpart_stride = gate_blocks * 4 * D;
-  a.lnpart = ar.take<float>(3 * a.lnpart_stride);
-  a.red2 = ar.take<double>(3 * kReduceGroups * 8 * 128);  // per reduce job: 32 groups x up to 1024 columns
+  // LayerNorm parameter partials of every gate of every layer (reduced
+  // together at the end of the backward)
+  a.lnpart = ar.take<float>(3 * m.T * a.lnpart_stride);
+  a.red2 = ar.take<double>((int64_t)kMaxReduceJobs * kReduceGroups * 8 * 128);  // per job: 32 groups x <= 1024 columns
   a.tnpart_cap = kTnPartFloats;
   a.tnpart = ar.take<float>(a.tnpart_cap);
-  a.fpart = ar.take<float>(cdiv(std::max(E, (int64_t)1), kFreqRowsPerBlock) * R);
+  a.fpart = ar.take<float>(2 * cdiv(std::max(E, (int64_t)1), kFreqRowsPerBlock) * R);
   a.dE = ar.take<float>(S);
   a.dF = ar.take<float>(3 * N);
   a.dS = ar.take<float>(9 * S);
@@ -1736,25 +1738,27 @@ GateBwdJob bwd_job(int mode, int64_t rows, const float* z, int ldz, const GateAd
 
 // Backward gates of one layer in one launch, then one launch reducing each
 // job's LayerNorm partials into ln_grad[k].
-int gate_bwd_launch(int D, GateBwdJobs J, float* const* ln_grad, const Acts& a, hipStream_t st) {
+// Job i writes its LayerNorm parameter partials to slot[i] (lnpart slots of
+// 3 x T); with ln_grad their reductions into ln_grad[i] are appended to
+// `defer`, to run after the whole backward.
+int gate_bwd_launch(int D, GateBwdJobs J, float* const* ln_grad, const int* slot, const Acts& a,
+                    std::vector<ReduceJob>& defer, hipStream_t st) {
   GateBwdJobs K{};
-  ReduceJobs R{};
   int blocks = 0;
   for (int i = 0; i < J.n; ++i) {
     if (J.j[i].rows <= 0) continue;
     const int nb = (int)cdiv(J.j[i].rows, kGateRows);
     K.j[K.n] = J.j[i];
     K.j[K.n].block0 = blocks;
-    K.j[K.n].lnpart = a.lnpart + (int64_t)i * a.lnpart_stride;
-    R.j[R.n] = ReduceJob{K.j[K.n].lnpart, nb, 4 * D, 4 * D, ln_grad ? ln_grad[i] : nullptr};
+    K.j[K.n].lnpart = a.lnpart + (int64_t)slot[i] * a.lnpart_stride;
+    if (ln_grad) defer.push_back(ReduceJob{K.j[K.n].lnpart, nb, 4 * D, 4 * D, ln_grad[i]});
     blocks += nb;
     K.n++;
-    R.n++;
   }
   if (blocks == 0) return CHGNET_OK;
   if (D == 64) KLAUNCH(st, "k_gate_bwd", k_gate_bwd<64><<<blocks, 256, 0, st>>>(K));
   else KLAUNCH(st, "k_gate_bwd", k_gate_bwd<128><<<blocks, 256, 0, st>>>(K));
-  return ln_grad ? reduce_rows_multi(R, a.red2, st) : CHGNET_OK;
+  return CHGNET_OK;
 }
 
 GateAdds adds(int n, const float* p0, int ld0, const int* i0, const float* p1, int ld1, const int* i1) {
@@ -2124,6 +2128,7 @@ int backward_impl(Ctx& c, const float* Pflat, bool repack, const float* dE, cons
     CHG_TRY(fill(G, Lg.total, 0.f, st));
     CHG_TRY(side_stream(ssp));
   }
+  std::vector<ReduceJob> reduce_jobs;  // ordered partial sums, run at the end
   SideStream no_side;
   if (wg && prof_active()) {
     // per-launch timing: everything on the caller's stream, so each
@@ -2241,23 +2246,27 @@ int backward_impl(Ctx& c, const float* Pflat, bool repack, const float* dE, cons
       if (!ang) which &= 3;
       GateBwdJobs J{};
       float* lg_out[3];
+      int slot[3];
       if (which & 2) {
+        slot[J.n] = 3 * t;
         lg_out[J.n] = G + lg.be.g_c;
         J.j[J.n++] = bwd_job(BWD_BOND, A, a.zae[t], 4 * D, ad_be, ln_ptrs(P, lo.be), a.dmu, a.ang_b1, a.eb, a.ang_b2,
                              a.t2, a.dzae, 4 * D);
       }
       if (which & 1) {
+        slot[J.n] = 3 * t + 1;
         lg_out[J.n] = G + lg.av.g_c;
         J.j[J.n++] = bwd_job(BWD_ATOM, E, a.zv[t], 2 * D, ad_av, ln_ptrs(P, lo.av), a.dm, a.edge_src, a.ea, nullptr,
                              a.dea, a.dzv, 2 * D);
         J.j[J.n - 1].aux_acc = t < m.T - 1;  // the first layer of the backward starts d e^a
       }
       if (which & 4) {
+        slot[J.n] = 3 * t + 2;
         lg_out[J.n] = G + lg.an.g_c;
         J.j[J.n++] = bwd_job(BWD_ANGLE, A, a.zae[t] + 2 * D, 4 * D, ad_an, ln_ptrs(P, lo.an), a.da[cur], nullptr,
                              nullptr, nullptr, nullptr, a.dzae + 2 * D, 4 * D);
       }
-      return gate_bwd_launch(D, J, wg ? lg_out : nullptr, a, st);
+      return gate_bwd_launch(D, J, wg ? lg_out : nullptr, slot, a, reduce_jobs, st);
     };
     // per-bond sums of dz over the bond's two angle roles (DZ12) from `ncols`
     // columns of dzae starting at col0; with_deb also forms d e^b
@@ -2479,17 +2488,24 @@ int backward_impl(Ctx& c, const float* Pflat, bool repack, const float* dE, cons
     }
     CHG_TRY(run_gemms(ps, st, "gemm_embed_bwd"));
     if (!wg) return CHGNET_OK;
+    float* fpart_b = a.fpart + cdiv(std::max(E, (int64_t)1), kFreqRowsPerBlock) * m.R;
     if (E > 0) {
       const int64_t nb = cdiv(E, kFreqRowsPerBlock);
       KLAUNCH(st, "k_rbf_fgrad", k_rbf_fgrad<<<(unsigned)nb, 256, 0, st>>>((int)E, nullptr, a.edge_len, P + L.f_a, m.R, c.hp->r_atom,
                                                 c.hp->envelope_p, a.drbf_a, a.fpart));
-      CHG_TRY(reduce_rows_launch(a.fpart, (int)nb, m.R, m.R, G + Lg.f_a, a.red2, st));
+      reduce_jobs.push_back(ReduceJob{a.fpart, (int)nb, m.R, m.R, G + Lg.f_a});
     }
     if (B > 0) {
       const int64_t nb = cdiv(B, kFreqRowsPerBlock);
       KLAUNCH(st, "k_rbf_fgrad", k_rbf_fgrad<<<(unsigned)nb, 256, 0, st>>>((int)B, g.bond_edge, a.edge_len, P + L.f_b, m.R, c.hp->r_bond,
-                                                c.hp->envelope_p, a.drbf_b, a.fpart));
-      CHG_TRY(reduce_rows_launch(a.fpart, (int)nb, m.R, m.R, G + Lg.f_b, a.red2, st));
+                                                c.hp->envelope_p, a.drbf_b, fpart_b));
+      reduce_jobs.push_back(ReduceJob{fpart_b, (int)nb, m.R, m.R, G + Lg.f_b});
+    }
+    // every LayerNorm and frequency gradient: ordered sums of the partials
+    for (size_t i0 = 0; i0 < reduce_jobs.size(); i0 += kMaxReduceJobs) {
+      ReduceJobs R{};
+      for (size_t i = i0; i < reduce_jobs.size() && R.n < kMaxReduceJobs; ++i) R.j[R.n++] = reduce_jobs[i];
+      CHG_TRY(reduce_rows_multi(R, a.red2, st));
     }
   }
   // join: later work on the caller's stream sees every weight gradient
@@ -2586,13 +2602,27 @@ int step_entry(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_graph
   if (!std::isfinite(loss_cfg->huber_delta)) return fail(CHGNET_EINVAL, "step: huber_delta is not finite");
   if (adam_hp && (!adam_m || !adam_v || !(adam_hp[4] >= 1.0f)))
     return fail(CHGNET_EINVAL, "step: Adam needs m, v and a step number t >= 1");
+  {
+    // the weight copy sits at the start of the activations, at an address
+    // that does not depend on the graph: pack it before the graph build so
+    // the device has work while the host waits for the graph sizes
+    CHG_TRY(validate_batch(batch));
+    Arena ar{static_cast<char*>(ws), ws_bytes, 0};
+    ar.used = graph_scratch_bytes(batch->n_atoms, batch->n_struct);
+    Acts a0;
+    Dims d0{batch->n_atoms, batch->n_struct, 0, 0, 0, hp->d, hp->n_layers, hp->n_rbf, hp->n_fourier};
+    const ParamLayout L1 = make_layout(*hp, 1), L4 = make_layout(*hp, 4);
+    carve_acts(ar, d0, a0, L4.total);
+    if (!ws || !ar.ok()) return fail(CHGNET_EWORKSPACE, "workspace too small (query chgnet_workspace_size)");
+    CHG_TRY(pack_params(L1, L4, params, a0.Pal, st));
+  }
   CHG_TRY(build_graph(hp, batch, graph, ws, ws_bytes, st));
   Ctx c;
   CHG_TRY(make_ctx(hp, batch, graph, ws, ws_bytes, c));
   float* e_out = c.a.out_E;
   float* f_out = c.a.out_F;
   float* s_out = c.a.out_S;
-  CHG_TRY(forward_impl(c, params, e_out, f_out, s_out, nullptr, st));
+  CHG_TRY(forward_impl(c, params, e_out, f_out, s_out, nullptr, st, false));
   const bool mag = hp->magmom != 0;
   KLAUNCH(st, "k_loss", k_loss<<<1, 256, 0, st>>>((int)c.dm.S, (int)c.dm.N, batch->atom_ptr, e_out, f_out, s_out,
                                                    mag ? c.a.oM : nullptr, E_t, F_t, S_t, M_t, *loss_cfg, loss, c.a.dE,
