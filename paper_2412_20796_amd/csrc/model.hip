@@ -824,6 +824,7 @@ __global__ void __launch_bounds__(256) k_gate_bwd(GateBwdJobs J) {
 // in wave order: the result does not depend on scheduling.
 struct SegJob {
   int nseg, ncb, width, ld_in, ld_out, ld_mul, ld_out2, accumulate, block0;
+  int wps;  // wavefronts per (segment, column block): 4 for long segments, 1 for short
   const int* ptr;
   const int* idx;
   const float* vals;
@@ -837,11 +838,8 @@ struct SegJobs {
 };
 
 template <int WPS>
-__global__ void __launch_bounds__(256) k_segsum(SegJobs J) {
+__device__ __forceinline__ void segsum_block(const SegJob& S) {
   constexpr int SPB = 4 / WPS;  // (segment, column block) units per block
-  int k = 0;
-  while (k + 1 < J.n && (int)blockIdx.x >= J.j[k + 1].block0) ++k;
-  const SegJob& S = J.j[k];
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int unit = (blockIdx.x - S.block0) * SPB + wave / WPS, w = wave % WPS;
   const int s = unit / S.ncb, c = (unit % S.ncb) * 64 + lane;
@@ -873,6 +871,15 @@ __global__ void __launch_bounds__(256) k_segsum(SegJobs J) {
   float* o = S.out + (int64_t)s * S.ld_out + c;
   *o = S.accumulate ? *o + acc : acc;
   if (S.out2) S.out2[(int64_t)s * S.ld_out2 + c] = S.mul[(int64_t)s * S.ld_mul + c] * acc;
+}
+
+// Jobs of either segment length in one launch; each block runs its job's
+// variant (the choice is uniform over the block).
+__global__ void __launch_bounds__(256) k_segsum(SegJobs J) {
+  int k = 0;
+  while (k + 1 < J.n && (int)blockIdx.x >= J.j[k + 1].block0) ++k;
+  if (J.j[k].wps == 4) segsum_block<4>(J.j[k]);
+  else segsum_block<1>(J.j[k]);
 }
 
 // Per bond b (centre i, local index q among k bonds): DZ1 = sum over the
@@ -1611,20 +1618,22 @@ SegJob seg_job(int64_t nseg, const int* ptr, const int* idx, const float* vals, 
 
 // wps: wavefronts per segment (4 for long segments such as the edges of an
 // atom, 1 for short ones such as the angles of a bond)
+// wps: wavefronts per (segment, column block) for jobs that do not set
+// their own (4 for long segments such as the edges of an atom, 1 for short
+// ones such as the angles of a bond)
 int segsum_launch(SegJobs J, int wps, hipStream_t st) {
   SegJobs K{};
   int blocks = 0;
-  const int spb = 4 / wps;
   for (int i = 0; i < J.n; ++i) {
     if (J.j[i].nseg <= 0) continue;
     K.j[K.n] = J.j[i];
     K.j[K.n].block0 = blocks;
-    blocks += (int)cdiv((int64_t)J.j[i].nseg * J.j[i].ncb, spb);
+    if (K.j[K.n].wps != 1 && K.j[K.n].wps != 4) K.j[K.n].wps = wps;
+    blocks += (int)cdiv((int64_t)J.j[i].nseg * J.j[i].ncb, 4 / K.j[K.n].wps);
     K.n++;
   }
   if (blocks == 0) return CHGNET_OK;
-  if (wps == 4) KLAUNCH(st, "k_segsum", k_segsum<4><<<blocks, 256, 0, st>>>(K));
-  else KLAUNCH(st, "k_segsum", k_segsum<1><<<blocks, 256, 0, st>>>(K));
+  KLAUNCH(st, "k_segsum", k_segsum<<<blocks, 256, 0, st>>>(K));
   return CHGNET_OK;
 }
 
@@ -1955,15 +1964,14 @@ int forward_impl(Ctx& c, const float* Pflat, float* energy, float* forces, float
     auto messages = [&](int which) -> int {
       SegJobs J{};
       if (which & 1) {
-        J.j[J.n++] = seg_job(N, g.edge_ptr, nullptr, a.msg, D, D, a.m[t], D);
-        CHG_TRY(segsum_launch(J, 4, st));
+        J.j[J.n] = seg_job(N, g.edge_ptr, nullptr, a.msg, D, D, a.m[t], D);
+        J.j[J.n++].wps = 4;
       }
       if (which & 2) {
-        J = SegJobs{};
-        J.j[J.n++] = seg_job(B, g.angle_ptr, nullptr, a.msgb, D, D, a.ssum[t], D, a.eb, D, a.mu[t], D);
-        CHG_TRY(segsum_launch(J, 1, st));
+        J.j[J.n] = seg_job(B, g.angle_ptr, nullptr, a.msgb, D, D, a.ssum[t], D, a.eb, D, a.mu[t], D);
+        J.j[J.n++].wps = 1;
       }
-      return CHGNET_OK;
+      return segsum_launch(J, 4, st);
     };
     // updates: v' = v + m Wo + bo; e' = e (+ mu Wo + bo on bonds)
     auto updates = [&](int which) -> int {
