@@ -249,12 +249,12 @@ def algorithmic_cost(tag, z):
         return "mfma", Tang * B * 16 * D * D + B * 8 * D * D
     if tag == "k_gate_fwd" and D == 64:
         # pre-activations formed in the kernel (d = 64): per edge x (d) and
-        # e^a (d) in, z kept for the backward (2d) and message (d) out; per
-        # angle and gate x (d) in, z (2d) and output (d) out, the angle gate
-        # also reads a (d). Tables: per-atom terms N x 8d (6d last layer),
-        # per-bond terms B x 8d (4d), e^b B x d.
-        lay = E * 5 * D + A * 9 * D + N * 8 * D + B * 9 * D
-        last = E * 5 * D + A * 4 * D + N * 6 * D + B * 5 * D
+        # e^a (d) in, z kept for the backward (2d), message (d) and the copy
+        # of x into e^{t+1} (d) out; per angle and gate x (d) in, z (2d) and
+        # output (d) out, the angle gate also reads a (d). Tables: per-atom
+        # terms N x 8d (6d last layer), per-bond terms B x 8d (4d), e^b B x d.
+        lay = E * 6 * D + A * 9 * D + N * 8 * D + B * 9 * D
+        last = E * 6 * D + A * 4 * D + N * 6 * D + B * 5 * D
         return "hbm", f * (Tang * lay + last)
     if tag == "k_gate_fwd":
         # z from the product kernel: per edge z (2d) + e^a (d) in, message (d)

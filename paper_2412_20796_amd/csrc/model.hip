@@ -400,6 +400,7 @@ struct GateMmJob {
   float* out;
   float* zsave;  // optional [rows, ldzs]: x W + b, kept for the backward pass
   int ldzs;
+  float* xcopy;  // optional [rows, 64]: a copy of x (the residual part of e^{t+1})
 };
 struct GateMmJobs {
   int n, ntiles;
@@ -504,6 +505,15 @@ __device__ __forceinline__ void mm_store_x(float* X, const float4 (&v)[4]) {
 #pragma unroll
   for (int q = 0; q < 4; ++q) *reinterpret_cast<float4*>(&X[xr * kMmXld + xc + 4 * q]) = v[q];
 }
+// the same x tile piece to global memory (rows past `rows` are skipped)
+__device__ __forceinline__ void mm_copy_x(float* __restrict__ dst, int rows, int row0, const float4 (&v)[4]) {
+  const int tid = threadIdx.x, row = row0 + (tid >> 2), xc = 16 * (tid & 3);
+  if (row < rows) {
+    float* p = dst + (int64_t)row * 64 + xc;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) *reinterpret_cast<float4*>(p + 4 * q) = v[q];
+  }
+}
 // B fragments of W columns [32 wave, 32 wave + 32) and their bias
 __device__ __forceinline__ void mm_load_w(const float* __restrict__ W, int ldw, const float* __restrict__ b, int wave,
                                           float (&bfr)[2][16], float& bias) {
@@ -577,12 +587,17 @@ __global__ void __launch_bounds__(kMmThreads, 1) k_gate_fwd_mm(GateMmJobs J) {
     const GateMmJob& jb = J.j[job_of(tile)];
     mm_fetch_x(jb.x, jb.rows, (tile - jb.tile0) * kMmRows, v);
   };
+  auto copy_x = [&](int tile, const float4 (&v)[4]) {
+    const GateMmJob& jb = J.j[job_of(tile)];
+    if (jb.xcopy) mm_copy_x(jb.xcopy, jb.rows, (tile - jb.tile0) * kMmRows, v);
+  };
   if (wave < kMmProducers) {
     float4 xv[4];
     int cur = -1;
     float bfr[2][16], bias = 0.f;
     fetch_x(tile_of(0), xv);
     mm_store_x(Xs[0], xv);
+    copy_x(tile_of(0), xv);
     if (nt > 1) fetch_x(tile_of(1), xv);
     __syncthreads();
     for (int i = 0; i <= nt; ++i) {
@@ -594,6 +609,7 @@ __global__ void __launch_bounds__(kMmThreads, 1) k_gate_fwd_mm(GateMmJobs J) {
         }
         if (i + 1 < nt) {
           mm_store_x(Xs[(i + 1) & 1], xv);
+          copy_x(tile_of(i + 1), xv);
           if (i + 2 < nt) fetch_x(tile_of(i + 2), xv);
         }
         mm_tile(Xs[i & 1], Zs[i & 1], bfr, bias, wave);
@@ -1922,9 +1938,11 @@ int forward_impl(Ctx& c, const float* Pflat, float* energy, float* forces, float
       if (D == 64) {
         // pre-activations formed inside the gate kernel; z kept for the backward
         GateMmJobs J{};
-        if (which & 1)
-          J.j[J.n++] = mm_job(FWD_ATOM, E, a.e[t], Wx_av, P + lo.av.b, ad_av, ln_ptrs(P, lo.av), a.ea, nullptr, a.msg,
-                              a.zv[t], 2 * D);
+        if (which & 1) {
+          J.j[J.n] = mm_job(FWD_ATOM, E, a.e[t], Wx_av, P + lo.av.b, ad_av, ln_ptrs(P, lo.av), a.ea, nullptr, a.msg,
+                            a.zv[t], 2 * D);
+          J.j[J.n++].xcopy = a.e[t + 1];  // e^{t+1} = e^t outside G^b (the bond rows are updated after)
+        }
         if (which & 2)
           J.j[J.n++] = mm_job(FWD_BOND, A, a.a[t], Wx_be, P + lo.be.b, ad_be, ln_ptrs(P, lo.be), a.eb, a.ang_b2,
                               a.msgb, a.zae[t], 4 * D);
@@ -1985,7 +2003,7 @@ int forward_impl(Ctx& c, const float* Pflat, float* energy, float* forces, float
         ps.push_back(p);
       }
       if (which & 2) {
-        if (E > 0) {
+        if (E > 0 && D != 64) {  // at d = 64 the atom-conv gate launch wrote the copy
           const int64_t n4 = E * D / 4;  // d is a multiple of 4 and the arena aligns to 256 B
           KLAUNCH(st, "k_copy", k_copy4<<<(unsigned)std::min<int64_t>(cdiv(n4, 256), 4096), 256, 0, st>>>(
                                     reinterpret_cast<float4*>(a.e[t + 1]), reinterpret_cast<const float4*>(a.e[t]), n4));
