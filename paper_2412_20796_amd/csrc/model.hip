@@ -841,6 +841,14 @@ __global__ void __launch_bounds__(256) k_gate_bwd(GateBwdJobs J) {
 struct SegJob {
   int nseg, ncb, width, ld_in, ld_out, ld_mul, ld_out2, accumulate, block0;
   int wps;  // wavefronts per (segment, column block): 4 for long segments, 1 for short
+  // optional output linear of the update (64-wide rows only): with y the
+  // segment's result (out2 if set, else out), upd[urow(s)] = res[urow(s)]
+  // + y Wo + bo, urow = upd_rows ? upd_rows[s] : s
+  const float* Wo;
+  const float* bo;
+  const float* res;
+  float* upd;
+  const int* upd_rows;
   const int* ptr;
   const int* idx;
   const float* vals;
@@ -886,7 +894,26 @@ __device__ __forceinline__ void segsum_block(const SegJob& S) {
   if (!ok) return;
   float* o = S.out + (int64_t)s * S.ld_out + c;
   *o = S.accumulate ? *o + acc : acc;
-  if (S.out2) S.out2[(int64_t)s * S.ld_out2 + c] = S.mul[(int64_t)s * S.ld_mul + c] * acc;
+  float y = acc;
+  if (S.out2) {
+    y = S.mul[(int64_t)s * S.ld_mul + c] * acc;
+    S.out2[(int64_t)s * S.ld_out2 + c] = y;
+  }
+  if (S.Wo) {
+    // the wavefront holds the whole 64-wide row, lane c column c: out
+    // column c = sum_k y_k Wo[k][c], y_k broadcast from lane k (fixed order,
+    // two interleaved partial sums)
+    const int64_t ur = S.upd_rows ? S.upd_rows[s] : s;
+    float u0 = 0.f, u1 = 0.f;
+#pragma unroll 8
+    for (int k = 0; k < 64; k += 2) {
+      const float y0 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(y), k));
+      const float y1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(y), k + 1));
+      u0 += y0 * S.Wo[k * 64 + c];
+      u1 += y1 * S.Wo[(k + 1) * 64 + c];
+    }
+    S.upd[ur * 64 + c] = (S.res[ur * 64 + c] + (u0 + u1)) + S.bo[c];
+  }
 }
 
 // Jobs of either segment length in one launch; each block runs its job's
@@ -1645,6 +1672,8 @@ int segsum_launch(SegJobs J, int wps, hipStream_t st) {
     K.j[K.n] = J.j[i];
     K.j[K.n].block0 = blocks;
     if (K.j[K.n].wps != 1 && K.j[K.n].wps != 4) K.j[K.n].wps = wps;
+    if (K.j[K.n].Wo && (K.j[K.n].width != 64 || K.j[K.n].ncb != 1))
+      return fail(CHGNET_EINVAL, "segsum: the fused output linear needs 64-wide rows");
     blocks += (int)cdiv((int64_t)J.j[i].nseg * J.j[i].ncb, 4 / K.j[K.n].wps);
     K.n++;
   }
@@ -1979,20 +2008,39 @@ int forward_impl(Ctx& c, const float* Pflat, float* energy, float* forces, float
     };
     // messages: m_i = sum over out-edges of e^a * phi_v; mu_b = eb_b * sum over
     // angles (b, b2) of eb_b2 * phi_e
+    // at d = 64 the same launch applies the output linears of the updates
+    // (v' = v + m Wo + bo; e'_b = e_b + mu Wo + bo): a wavefront holds a row
+    const bool fuse_upd = D == 64;
     auto messages = [&](int which) -> int {
       SegJobs J{};
       if (which & 1) {
-        J.j[J.n] = seg_job(N, g.edge_ptr, nullptr, a.msg, D, D, a.m[t], D);
-        J.j[J.n++].wps = 4;
+        SegJob& q = J.j[J.n++];
+        q = seg_job(N, g.edge_ptr, nullptr, a.msg, D, D, a.m[t], D);
+        q.wps = 4;
+        if (fuse_upd) {
+          q.Wo = P + lo.av_Wo;
+          q.bo = P + lo.av_bo;
+          q.res = a.v[t];
+          q.upd = a.v[t + 1];
+        }
       }
       if (which & 2) {
-        J.j[J.n] = seg_job(B, g.angle_ptr, nullptr, a.msgb, D, D, a.ssum[t], D, a.eb, D, a.mu[t], D);
-        J.j[J.n++].wps = 1;
+        SegJob& q = J.j[J.n++];
+        q = seg_job(B, g.angle_ptr, nullptr, a.msgb, D, D, a.ssum[t], D, a.eb, D, a.mu[t], D);
+        q.wps = 1;
+        if (fuse_upd) {
+          q.Wo = P + lo.be_Wo;
+          q.bo = P + lo.be_bo;
+          q.res = a.e[t];
+          q.upd = a.e[t + 1];
+          q.upd_rows = g.bond_edge;
+        }
       }
       return segsum_launch(J, 4, st);
     };
     // updates: v' = v + m Wo + bo; e' = e (+ mu Wo + bo on bonds)
     auto updates = [&](int which) -> int {
+      if (fuse_upd) return CHGNET_OK;  // done by the message launch (and the copy by the atom-conv gate)
       std::vector<GemmProblem> ps;
       if (which & 1) {
         GemmProblem p = gp(N, D, a.v[t + 1], D);
