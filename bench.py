@@ -54,9 +54,11 @@ def parse():
 def main():
     args = parse()
     if args.traffic_summary:
-        cmd = ["rocprofv3 --pmc %s --output-format csv -d gpurun_out/pmc_%s -o run -- python3 bench.py "
+        # the counter runs wrote their CSVs into <dir>/run_counter_collection.csv
+        cmd = ["rocprofv3 --pmc %s --output-format csv -d %s -o run -- python3 bench.py "
                "--workload %s --no-cpu-baseline --no-roofline --steps 3 --warmup 1 --calibrate-copy"
-               % (c, c.split("_")[0].lower(), args.workload) for c in ("FETCH_SIZE", "WRITE_SIZE")]
+               % (c, os.path.dirname(path) or ".", args.workload)
+               for c, path in zip(("FETCH_SIZE", "WRITE_SIZE"), args.traffic_summary)]
         cmd.append("python3 bench.py --workload %s --traffic-summary %s %s" % ((args.workload,) + tuple(args.traffic_summary)))
         print(traffic_summary(args.traffic_summary[0], args.traffic_summary[1], args.workload, cmd))
         return
