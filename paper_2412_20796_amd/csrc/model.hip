@@ -250,6 +250,30 @@ __device__ __forceinline__ void store_cols(float* __restrict__ p, int j, const f
         make_float4(v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]);
 }
 
+// Streaming variants for data touched once here and not again soon (the
+// pre-activations saved for the backward pass, the copy into e^{t+1}):
+// nontemporal accesses keep them from displacing cached table rows.
+typedef float v4f __attribute__((ext_vector_type(4)));
+template <int D, int CPL>
+__device__ __forceinline__ void load_cols_nt(const float* __restrict__ p, int j, float (&v)[CPL]) {
+#pragma unroll
+  for (int q = 0; q < CPL / 4; ++q) {
+    const v4f t = __builtin_nontemporal_load(reinterpret_cast<const v4f*>(p + q * Lanes<D, CPL>::STRIDE + 4 * j));
+    v[4 * q] = t.x;
+    v[4 * q + 1] = t.y;
+    v[4 * q + 2] = t.z;
+    v[4 * q + 3] = t.w;
+  }
+}
+template <int D, int CPL>
+__device__ __forceinline__ void store_cols_nt(float* __restrict__ p, int j, const float (&v)[CPL]) {
+#pragma unroll
+  for (int q = 0; q < CPL / 4; ++q) {
+    const v4f t = {v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]};
+    __builtin_nontemporal_store(t, reinterpret_cast<v4f*>(p + q * Lanes<D, CPL>::STRIDE + 4 * j));
+  }
+}
+
 // Normalised core/gate (xc, xg) and 1/std (rc, rg) of one row; in place.
 template <int D, int CPL>
 __device__ __forceinline__ void ln_stats(float (&zc)[CPL], float (&zg)[CPL], float& rc, float& rg) {
@@ -299,8 +323,8 @@ struct GateAdds {
 template <int D, int CPL>
 __device__ __forceinline__ void load_z(const float* __restrict__ z, int ldz, const GateAdds& ad, int row, int j,
                                        float (&zc)[CPL], float (&zg)[CPL]) {
-  load_cols<D, CPL>(z + (int64_t)row * ldz, j, zc);
-  load_cols<D, CPL>(z + (int64_t)row * ldz + D, j, zg);
+  load_cols_nt<D, CPL>(z + (int64_t)row * ldz, j, zc);
+  load_cols_nt<D, CPL>(z + (int64_t)row * ldz + D, j, zg);
 #pragma unroll
   for (int q = 0; q < kMaxAdds; ++q) {
     if (q >= ad.n) break;
@@ -456,8 +480,8 @@ __device__ __forceinline__ void gate_mm_row(const GateMmJob& J, int row, int lr,
   load_cols<D, CPL>(Zs + lr * kMmZld, j, zc);
   load_cols<D, CPL>(Zs + lr * kMmZld + D, j, zg);
   if (J.zsave) {
-    store_cols<D, CPL>(J.zsave + (int64_t)row * J.ldzs, j, zc);
-    store_cols<D, CPL>(J.zsave + (int64_t)row * J.ldzs + D, j, zg);
+    store_cols_nt<D, CPL>(J.zsave + (int64_t)row * J.ldzs, j, zc);
+    store_cols_nt<D, CPL>(J.zsave + (int64_t)row * J.ldzs + D, j, zg);
   }
 #pragma unroll
   for (int q = 0; q < kMaxAdds; ++q) {
@@ -511,7 +535,10 @@ __device__ __forceinline__ void mm_copy_x(float* __restrict__ dst, int rows, int
   if (row < rows) {
     float* p = dst + (int64_t)row * 64 + xc;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) *reinterpret_cast<float4*>(p + 4 * q) = v[q];
+    for (int q = 0; q < 4; ++q) {
+      const v4f t = {v[q].x, v[q].y, v[q].z, v[q].w};
+      __builtin_nontemporal_store(t, reinterpret_cast<v4f*>(p + 4 * q));
+    }
   }
 }
 // B fragments of W columns [32 wave, 32 wave + 32) and their bias
