@@ -165,6 +165,7 @@ def main():
         torch.cuda.synchronize()
         prof = bd.profile_stop()
         out["roofline"], out["kernels"] = roofline(prof, args.steps, dict(N=b.n_atoms, E=E, B=B, A=A, S=S, D=d, T=T,
+                                                                            fused_bwd=d == 64 and not args.sequential,
                                                                             workload=args.workload))
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(args.workload, args.cpu_sample, variant=args)
@@ -240,6 +241,10 @@ def algorithmic_cost(tag, z):
     f = 4  # bytes per fp32
     if tag == "gemm_z":
         return "mfma", T * E * 4 * D * D + Tang * A * 8 * D * D + A * 4 * D * D
+    if tag == "gemm_in_bwd" and z.get("fused_bwd"):
+        # the edge and angle rows are formed by the fused gate backward; this
+        # launch holds the atom rows and the bond rows (k = 8d, 6d last layer)
+        return "mfma", T * N * 16 * D * D - N * 4 * D * D + Tang * B * 16 * D * D + B * 8 * D * D
     if tag == "gemm_in_bwd":
         return "mfma", T * (E * 4 * D * D + N * 16 * D * D) - N * 4 * D * D + Tang * A * 8 * D * D + A * 4 * D * D
     if tag == "tn_in":  # first-layer and output-layer weight gradients of every block
@@ -265,6 +270,13 @@ def algorithmic_cost(tag, z):
         lay = E * 4 * D + A * 7 * D + N * 8 * D + B * 9 * D
         last = E * 4 * D + A * 3 * D + N * 6 * D + B * 5 * D
         return "hbm", f * (Tang * lay + last)
+    if tag == "k_gate_bwd" and z.get("fused_bwd"):
+        # as below, plus the input gradients the kernel forms: per edge the
+        # residual (d) in and de (d) out; per angle da (d) out and, in layers
+        # with an angle update, the residual (d) in
+        lay = E * 9 * D + A * 12 * D + N * 9 * D + B * 10 * D
+        last = E * 9 * D + A * 6 * D + N * 7 * D + B * 6 * D
+        return "hbm", f * (Tang * lay + last)
     if tag == "k_gate_bwd":
         # per edge: z (2d), e^a (d), d e^a (d) in; dz (2d), d e^a (d) out;
         # per angle and gate: z (2d) + upstream (d) in, dz (2d) out (the bond
@@ -284,7 +296,7 @@ TAG_SYMBOL = {
     "gemm_in_bwd": "k_gemm<64, 2>",
     "tn_in": "k_tn<1>",
     "k_gate_fwd": "k_gate_fwd_mm",
-    "k_gate_bwd": "k_gate_bwd<64>",
+    "k_gate_bwd": "k_gate_bwd_mm",
 }
 
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_%s.md")

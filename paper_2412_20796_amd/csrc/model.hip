@@ -860,6 +860,348 @@ __global__ void __launch_bounds__(256) k_gate_bwd(GateBwdJobs J) {
   else gate_bwd_rows<D, BWD_ANGLE>(blk, jb, red);
 }
 
+// ---------------------------------------------------------------------------
+// Fused backward gates and input-gradient product (d = 64). A tile is 64
+// rows: edges of the atom conv (one gate), or angles (the bond-conv gate and,
+// in layers with an angle update, the angle-update gate of the same angles).
+// Consumer wavefronts form dz of the tile's gates as k_gate_bwd does (stored
+// to global memory for the weight gradients and the segment sums, and to an
+// LDS tile); producer wavefronts then form the gradient of the rows' own
+// input block, dX = sum over the gates of dz W_g^T (+ residual), with 16x16x4
+// fp32 MFMAs. Producer p owns output columns [16p, 16p + 16) of all 64 rows;
+// in step s of a 128-wide k block lane group q = lane / 16 supplies
+// k = 32q + s for both operands, so a lane's B fragment of a gate is 32
+// consecutive entries of one weight row, held in registers.
+// LayerNorm parameter partials accumulate in a consumer's registers while
+// its wavefront stays on one gate; when it changes gate (and at the end)
+// they are summed over the wavefront's row slots and staged in LDS, and the
+// block adds its wavefronts in a fixed order.
+// ---------------------------------------------------------------------------
+struct GateBwdMmJob {
+  int rows, tile0, ngates;
+  int gid[2];  // LayerNorm partial slot of each gate: 0 atom conv, 1 bond conv, 2 angle update
+  GateBwdJob g[2];
+  const float* W[2];  // rows of each gate's first-layer weight for this input block: [64][128]
+  const float* res;   // [rows, 64] added to dX, or nullptr
+  float* dx;          // [rows, 64]
+};
+struct GateBwdMmJobs {
+  int n, ntiles;
+  GateBwdMmJob j[2];
+  float* lnpart[3];  // by slot: [gridDim.x][4 * 64], or nullptr
+};
+constexpr int kBmLd = 256 + 4;
+
+// Row indices of a consumer row: the gathered terms' rows, the upstream row
+// and (bond gate) the second bond.
+struct BwdMmIdx {
+  int a0, a1, up, b2;
+};
+__device__ __forceinline__ void bwd_mm_index(const GateBwdJob& J, int row, BwdMmIdx& x) {
+  x.a0 = J.ad.n > 0 ? J.ad.idx[0][row] : 0;
+  x.a1 = J.ad.n > 1 ? J.ad.idx[1][row] : 0;
+  x.up = J.mode == BWD_ANGLE ? row : J.up_idx[row];
+  x.b2 = J.mode == BWD_BOND ? J.b2_idx[row] : 0;
+}
+
+template <int MODE>
+__device__ __forceinline__ void gate_bwd_mm_row(const GateBwdJob& J, int row, const BwdMmIdx& x, int j,
+                                                const float* lnS, float (&acc)[4][kMmCpl], float* zrow) {
+  constexpr int D = 64, CPL = kMmCpl;
+  constexpr int LPR = Lanes<D, CPL>::LPR;
+  float zc[CPL], zg[CPL], rc, rg;
+  load_cols_nt<D, CPL>(J.z + (int64_t)row * J.ldz, j, zc);
+  load_cols_nt<D, CPL>(J.z + (int64_t)row * J.ldz + D, j, zg);
+  static_assert(kMaxAdds == 2, "two gathered terms");
+  if (J.ad.n > 0) {
+    float uc[CPL], ug[CPL];
+    const float* r = J.ad.p[0] + (int64_t)x.a0 * J.ad.ld[0];
+    load_cols<D, CPL>(r, j, uc);
+    load_cols<D, CPL>(r + D, j, ug);
+#pragma unroll
+    for (int k = 0; k < CPL; ++k) {
+      zc[k] += uc[k];
+      zg[k] += ug[k];
+    }
+  }
+  if (J.ad.n > 1) {
+    float uc[CPL], ug[CPL];
+    const float* r = J.ad.p[1] + (int64_t)x.a1 * J.ad.ld[1];
+    load_cols<D, CPL>(r, j, uc);
+    load_cols<D, CPL>(r + D, j, ug);
+#pragma unroll
+    for (int k = 0; k < CPL; ++k) {
+      zc[k] += uc[k];
+      zg[k] += ug[k];
+    }
+  }
+  float u[CPL], w[CPL], dphi[CPL];
+  if (MODE == BWD_ANGLE) {
+    load_cols<D, CPL>(J.up + (int64_t)row * D, j, dphi);
+  } else {
+    const int64_t ur = x.up;
+    load_cols<D, CPL>(J.up + ur * D, j, u);
+    if (MODE == BWD_ATOM) {
+      load_cols<D, CPL>(J.eb + (int64_t)row * D, j, w);  // e^a of this edge
+#pragma unroll
+      for (int k = 0; k < CPL; ++k) dphi[k] = u[k] * w[k];
+    } else {
+      float e1[CPL], e2[CPL];
+      load_cols<D, CPL>(J.eb + ur * D, j, e1);
+      load_cols<D, CPL>(J.eb + (int64_t)x.b2 * D, j, e2);
+#pragma unroll
+      for (int k = 0; k < CPL; ++k) {
+        w[k] = u[k] * e1[k];
+        dphi[k] = w[k] * e2[k];
+      }
+    }
+  }
+  ln_stats<D, CPL>(zc, zg, rc, rg);
+  float gc[CPL], bc[CPL], gg[CPL], bg[CPL];
+  load_cols<D, CPL>(lnS, j, gc);
+  load_cols<D, CPL>(lnS + 64, j, bc);
+  load_cols<D, CPL>(lnS + 128, j, gg);
+  load_cols<D, CPL>(lnS + 192, j, bg);
+  float dyc[CPL], dyg[CPL], side[CPL];
+  float s1c = 0.f, s2c = 0.f, s1g = 0.f, s2g = 0.f;
+#pragma unroll
+  for (int k = 0; k < CPL; ++k) {
+    const float yc = gc[k] * zc[k] + bc[k];
+    const float yg = gg[k] * zg[k] + bg[k];
+    const float sc = sigm(yc), sg = sigm(yg);
+    const float silu_c = yc * sc;
+    side[k] = silu_c * sg;  // phi
+    const float gy_c = dphi[k] * sg * sc * (1.0f + yc * (1.0f - sc));
+    const float gy_g = dphi[k] * silu_c * sg * (1.0f - sg);
+    acc[0][k] += gy_c * zc[k];
+    acc[1][k] += gy_c;
+    acc[2][k] += gy_g * zg[k];
+    acc[3][k] += gy_g;
+    dyc[k] = gy_c * gc[k];
+    dyg[k] = gy_g * gg[k];
+    s1c += dyc[k];
+    s2c += dyc[k] * zc[k];
+    s1g += dyg[k];
+    s2g += dyg[k] * zg[k];
+  }
+  s1c = rowsum<LPR>(s1c) * (1.0f / D);
+  s2c = rowsum<LPR>(s2c) * (1.0f / D);
+  s1g = rowsum<LPR>(s1g) * (1.0f / D);
+  s2g = rowsum<LPR>(s2g) * (1.0f / D);
+#pragma unroll
+  for (int k = 0; k < CPL; ++k) {
+    dyc[k] = rc * (dyc[k] - s1c - zc[k] * s2c);
+    dyg[k] = rg * (dyg[k] - s1g - zg[k] * s2g);
+  }
+  store_cols<D, CPL>(J.dz + (int64_t)row * J.lddz, j, dyc);
+  store_cols<D, CPL>(J.dz + (int64_t)row * J.lddz + D, j, dyg);
+  store_cols<D, CPL>(zrow, j, dyc);
+  store_cols<D, CPL>(zrow + D, j, dyg);
+  if (MODE == BWD_ATOM) {
+    float de[CPL];
+    if (J.aux_acc) {
+      load_cols<D, CPL>(J.aux + (int64_t)row * D, j, de);
+#pragma unroll
+      for (int k = 0; k < CPL; ++k) de[k] += u[k] * side[k];
+    } else {
+#pragma unroll
+      for (int k = 0; k < CPL; ++k) de[k] = u[k] * side[k];
+    }
+    store_cols<D, CPL>(J.aux + (int64_t)row * D, j, de);
+  } else if (MODE == BWD_BOND) {
+#pragma unroll
+    for (int k = 0; k < CPL; ++k) side[k] *= w[k];
+    store_cols<D, CPL>(J.aux + (int64_t)row * D, j, side);
+  }
+}
+
+// Sum a consumer's LayerNorm partials over the wavefront's 8 row slots
+// (lanes j + 8 s) in a fixed order, store them to wsum[4][64] and clear them.
+__device__ __forceinline__ void bwd_mm_flush(float (&acc)[4][kMmCpl], float* wsum) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int a = 0; a < 4; ++a)
+#pragma unroll
+    for (int k = 0; k < kMmCpl; ++k) {
+      float v = acc[a][k];
+      v += __shfl_xor(v, 8);
+      v += __shfl_xor(v, 16);
+      v += __shfl_xor(v, 32);
+      acc[a][k] = v;
+    }
+  if (lane < Lanes<64, kMmCpl>::LPR)
+#pragma unroll
+    for (int a = 0; a < 4; ++a) store_cols<64, kMmCpl>(wsum + a * 64, lane, acc[a]);
+#pragma unroll
+  for (int a = 0; a < 4; ++a)
+#pragma unroll
+    for (int k = 0; k < kMmCpl; ++k) acc[a][k] = 0.f;
+}
+
+// One block per compute unit, walking tiles blockIdx.x, blockIdx.x +
+// gridDim.x, ... of the concatenated jobs; consumers fill the dz tile of
+// tile i while producers multiply tile i - 1 (one block barrier per tile).
+__global__ void __launch_bounds__(kMmThreads, 1) k_gate_bwd_mm(GateBwdMmJobs J) {
+  __shared__ __attribute__((aligned(16))) float Zs[2][kMmRows * kBmLd];
+  __shared__ __attribute__((aligned(16))) float LnS[2][2][4][64];
+  __shared__ __attribute__((aligned(16))) float Wsum[3][kMmConsumers][4 * 64];
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  for (int t = threadIdx.x; t < 2 * 2 * 4 * 64; t += kMmThreads) {
+    const int jb = t / 512, g = (t / 256) % 2, q = (t / 64) % 4, c = t % 64;
+    float v = 0.f;
+    if (jb < J.n && g < J.j[jb].ngates) {
+      const LnPtrs& ln = J.j[jb].g[g].ln;
+      v = (q == 0 ? ln.gc : q == 1 ? ln.bc : q == 2 ? ln.gg : ln.bg)[c];
+    }
+    LnS[jb][g][q][c] = v;
+  }
+  for (int t = threadIdx.x; t < 3 * kMmConsumers * 4 * 64; t += kMmThreads) (&Wsum[0][0][0])[t] = 0.f;
+  auto job_of = [&](int tile) {
+    int k = 0;
+    while (k + 1 < J.n && tile >= J.j[k + 1].tile0) ++k;
+    return k;
+  };
+  // the grid never exceeds the tile count: every block has a tile
+  const int nt = (J.ntiles - 1 - (int)blockIdx.x) / (int)gridDim.x + 1;
+  auto tile_of = [&](int i) { return (int)blockIdx.x + i * (int)gridDim.x; };
+  __syncthreads();
+  if (wave < kMmProducers) {
+    const int n = lane & 15, q4 = lane >> 4, col = 16 * wave + n;
+    float bf[2][32];
+    int cur = -1;
+    // residual of output element (row 16 rt + 4 q4 + v, column col) of tile
+    // ii, loaded one tile ahead
+    float rv[4][4], rvn[4][4];
+    auto load_res = [&](int ii) {
+      if (ii >= nt) return;
+      const int tile = tile_of(ii);
+      const GateBwdMmJob& jb = J.j[job_of(tile)];
+      const int row0 = (tile - jb.tile0) * kMmRows;
+#pragma unroll
+      for (int rt = 0; rt < 4; ++rt)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const int row = row0 + 16 * rt + 4 * q4 + v;
+          rvn[rt][v] = (jb.res && row < jb.rows) ? jb.res[(int64_t)row * 64 + col] : 0.f;
+        }
+    };
+    load_res(0);
+    for (int i = 0; i <= nt; ++i) {
+      if (i > 0) {
+        const int tile = tile_of(i - 1);
+        const int k = job_of(tile);
+        const GateBwdMmJob& jb = J.j[k];
+        const int ng = jb.ngates;
+        if (k != cur) {
+          cur = k;
+#pragma unroll
+          for (int g = 0; g < 2; ++g) {
+            if (g < ng) {
+              const float* wr = jb.W[g] + (int64_t)col * 128 + 32 * q4;
+#pragma unroll
+              for (int s4 = 0; s4 < 8; ++s4) {
+                const float4 v = *reinterpret_cast<const float4*>(wr + 4 * s4);
+                bf[g][4 * s4] = v.x; bf[g][4 * s4 + 1] = v.y; bf[g][4 * s4 + 2] = v.z; bf[g][4 * s4 + 3] = v.w;
+              }
+            }
+          }
+        }
+        const int row0 = (tile - jb.tile0) * kMmRows;
+#pragma unroll
+        for (int rt = 0; rt < 4; ++rt)
+#pragma unroll
+          for (int v = 0; v < 4; ++v) rv[rt][v] = rvn[rt][v];
+        load_res(i);
+        v4f acc[4];
+#pragma unroll
+        for (int rt = 0; rt < 4; ++rt) acc[rt] = v4f{0.f, 0.f, 0.f, 0.f};
+        const float* Z = Zs[(i - 1) & 1];
+#pragma unroll
+        for (int g = 0; g < 2; ++g) {
+          if (g < ng) {
+#pragma unroll
+            for (int s4 = 0; s4 < 8; ++s4) {
+              float4 a4[4];
+#pragma unroll
+              for (int rt = 0; rt < 4; ++rt)
+                a4[rt] = *reinterpret_cast<const float4*>(Z + (16 * rt + n) * kBmLd + 128 * g + 32 * q4 + 4 * s4);
+#pragma unroll
+              for (int rt = 0; rt < 4; ++rt) acc[rt] = __builtin_amdgcn_mfma_f32_16x16x4f32(a4[rt].x, bf[g][4 * s4], acc[rt], 0, 0, 0);
+#pragma unroll
+              for (int rt = 0; rt < 4; ++rt) acc[rt] = __builtin_amdgcn_mfma_f32_16x16x4f32(a4[rt].y, bf[g][4 * s4 + 1], acc[rt], 0, 0, 0);
+#pragma unroll
+              for (int rt = 0; rt < 4; ++rt) acc[rt] = __builtin_amdgcn_mfma_f32_16x16x4f32(a4[rt].z, bf[g][4 * s4 + 2], acc[rt], 0, 0, 0);
+#pragma unroll
+              for (int rt = 0; rt < 4; ++rt) acc[rt] = __builtin_amdgcn_mfma_f32_16x16x4f32(a4[rt].w, bf[g][4 * s4 + 3], acc[rt], 0, 0, 0);
+            }
+          }
+        }
+#pragma unroll
+        for (int rt = 0; rt < 4; ++rt)
+#pragma unroll
+          for (int v = 0; v < 4; ++v) {
+            const int row = row0 + 16 * rt + 4 * q4 + v;
+            if (row < jb.rows) jb.dx[(int64_t)row * 64 + col] = acc[rt][v] + rv[rt][v];
+          }
+      }
+      __syncthreads();
+    }
+  } else {
+    using GL = Lanes<64, kMmCpl>;
+    const int cw = wave - kMmProducers, j = lane % GL::LPR, slot = lane / GL::LPR;
+    float acc[4][kMmCpl];
+#pragma unroll
+    for (int a = 0; a < 4; ++a)
+#pragma unroll
+      for (int k = 0; k < kMmCpl; ++k) acc[a][k] = 0.f;
+    int gid_cur = -1;
+    for (int i = 0; i <= nt; ++i) {
+      if (i < nt) {
+        const int tile = tile_of(i);
+        const int k = __builtin_amdgcn_readfirstlane(job_of(tile));
+        const GateBwdMmJob& jb = J.j[k];
+        // the wavefronts are split evenly over the tile's gates; a wavefront
+        // covers 8 ng consecutive rows of its gate, 8 rows per pass
+        const int wpg = kMmConsumers / jb.ngates;
+        const int g = __builtin_amdgcn_readfirstlane(cw / wpg);
+        const int gid = jb.gid[g];
+        if (gid != gid_cur) {
+          if (gid_cur >= 0) bwd_mm_flush(acc, Wsum[gid_cur][cw]);
+          gid_cur = gid;
+        }
+        const GateBwdJob& gj = jb.g[g];
+        const float* lnS = &LnS[k][g][0][0];
+        const int row0 = (tile - jb.tile0) * kMmRows;
+#pragma unroll
+        for (int sub = 0; sub < 2; ++sub) {
+          if (sub >= jb.ngates) break;
+          const int lr = (cw % wpg) * 8 * jb.ngates + 8 * sub + slot;
+          const int row = row0 + lr;
+          if (row < jb.rows) {
+            BwdMmIdx x;
+            bwd_mm_index(gj, row, x);
+            float* zrow = Zs[i & 1] + lr * kBmLd + 128 * g;
+            if (gj.mode == BWD_ATOM) gate_bwd_mm_row<BWD_ATOM>(gj, row, x, j, lnS, acc, zrow);
+            else if (gj.mode == BWD_BOND) gate_bwd_mm_row<BWD_BOND>(gj, row, x, j, lnS, acc, zrow);
+            else gate_bwd_mm_row<BWD_ANGLE>(gj, row, x, j, lnS, acc, zrow);
+          }
+        }
+      }
+      __syncthreads();
+    }
+    if (gid_cur >= 0) bwd_mm_flush(acc, Wsum[gid_cur][cw]);
+  }
+  __syncthreads();
+  for (int t = threadIdx.x; t < 3 * 4 * 64; t += kMmThreads) {
+    const int gid = t / 256, c = t % 256;
+    if (!J.lnpart[gid]) continue;
+    float s = 0.f;
+    for (int w = 0; w < kMmConsumers; ++w) s += Wsum[gid][w][c];
+    J.lnpart[gid][(int64_t)blockIdx.x * 256 + c] = s;
+  }
+}
+
 // Segmented row sums, several independent jobs per launch:
 //   out[s] (+)= sum_{r in [ptr[s], ptr[s+1])} vals[idx(r)]; optionally
 //   out2[s] = mul[s] * sum. WPS wavefronts per (segment, 64 columns) split the
@@ -1469,7 +1811,10 @@ struct Acts {
   // so a layer's weight gradients can run while the next layer is formed
   float *dzv_pp[2], *dzae_pp[2], *AT_pp[2], *DZ12_pp[2], *dvf_pp[2];
   // backward
-  float *dv[2], *de[2], *da[2], *dm, *dmu, *dzv, *dzae, *t2, *AT, *DZ12, *dea, *deb;
+  // the gradient of e^t rotates through three copies: the fused backward
+  // gate of layer t writes it while the weight gradients of layer t + 1 may
+  // still read the copy of e^{t+2}
+  float *dv[2], *de[3], *da[2], *dm, *dmu, *dzv, *dzae, *t2, *AT, *DZ12, *dea, *deb;
   float *doE, *doS, *dn, *doF, *dh2E, *dh2S, *dh2F, *dh1ES, *dh1F, *drbf_a, *drbf_b;
   float *lnpart, *tnpart, *fpart, *Pal;
   double* red2;
@@ -1534,9 +1879,9 @@ void carve_acts(Arena& ar, const Dims& m, Acts& a, int64_t n_params_aligned) {
   a.dvf = a.dvf_pp[0];
   for (int k = 0; k < 2; ++k) {
     a.dv[k] = ar.take<float>(N * D);
-    a.de[k] = ar.take<float>(E * D);
     a.da[k] = ar.take<float>(A * D);
   }
+  for (int k = 0; k < 3; ++k) a.de[k] = ar.take<float>(E * D);
   a.dm = ar.take<float>(N * D);
   a.dmu = ar.take<float>(B * D);
   for (int k = 0; k < 2; ++k) {
@@ -1563,7 +1908,7 @@ void carve_acts(Arena& ar, const Dims& m, Acts& a, int64_t n_params_aligned) {
   a.dh1F = ar.take<float>(E * D);
   a.drbf_a = ar.take<float>(E * R);
   a.drbf_b = ar.take<float>(B * R);
-  const int64_t gate_blocks = cdiv(std::max<int64_t>(std::max(E, A), 1), kGateRows);
+  const int64_t gate_blocks = std::max<int64_t>(cdiv(std::max<int64_t>(std::max(E, A), 1), kGateRows), 256);
   a.lnpart_stride = gate_blocks * 4 * D;
   // LayerNorm parameter partials of every gate of every layer (reduced
   // together at the end of the backward)
@@ -1839,6 +2184,38 @@ int gate_bwd_launch(int D, GateBwdJobs J, float* const* ln_grad, const int* slot
   if (blocks == 0) return CHGNET_OK;
   if (D == 64) KLAUNCH(st, "k_gate_bwd", k_gate_bwd<64><<<blocks, 256, 0, st>>>(K));
   else KLAUNCH(st, "k_gate_bwd", k_gate_bwd<128><<<blocks, 256, 0, st>>>(K));
+  return CHGNET_OK;
+}
+
+// Launch the fused (d = 64) backward gates and their input-gradient products
+// of one layer: a persistent grid of at most one block per compute unit.
+// slot[gid] is the lnpart slot of gate id gid (0 atom conv, 1 bond conv, 2
+// angle update); with ln_grad, each used slot's reduction into ln_grad[gid]
+// is appended to `defer`.
+int gate_bwd_mm_launch(GateBwdMmJobs J, float* const* ln_grad, const int* slot, const Acts& a,
+                       std::vector<ReduceJob>& defer, hipStream_t st) {
+  GateBwdMmJobs K{};
+  int tiles = 0;
+  bool used[3] = {false, false, false};
+  for (int i = 0; i < J.n; ++i) {
+    if (J.j[i].rows <= 0) continue;
+    K.j[K.n] = J.j[i];
+    K.j[K.n].tile0 = tiles;
+    tiles += (int)cdiv(J.j[i].rows, kMmRows);
+    for (int g = 0; g < J.j[i].ngates; ++g) used[J.j[i].gid[g]] = true;
+    K.n++;
+  }
+  K.ntiles = tiles;
+  if (tiles == 0) return CHGNET_OK;
+  const int grid = std::min(tiles, 256);
+  if ((int64_t)grid * 4 * 64 > a.lnpart_stride) return fail(CHGNET_EINVAL, "gate_bwd_mm: LayerNorm partial slots too small");
+  for (int gid = 0; gid < 3; ++gid) {
+    K.lnpart[gid] = nullptr;
+    if (!used[gid] || !ln_grad) continue;
+    K.lnpart[gid] = a.lnpart + (int64_t)slot[gid] * a.lnpart_stride;
+    defer.push_back(ReduceJob{K.lnpart[gid], grid, 4 * 64, 4 * 64, ln_grad[gid]});
+  }
+  KLAUNCH(st, "k_gate_bwd", k_gate_bwd_mm<<<grid, kMmThreads, 0, st>>>(K));
   return CHGNET_OK;
 }
 
@@ -2246,7 +2623,7 @@ int backward_impl(Ctx& c, const float* Pflat, bool repack, const float* dE, cons
     KLAUNCH(st, "k_seed_edges", k_seed_edges<<<(unsigned)cdiv(E, 256), 256, 0, st>>>((int)E, a.edge_src, dF, a.edge_xhat, a.dn));
     KLAUNCH(st, "k_seed_edges2", k_seed_edges2<<<(unsigned)cdiv(E, 256), 256, 0, st>>>((int)E, g.edge_rev, a.dn, a.doF));
   }
-  int cur = 0;
+  int cur = 0, ecur = 0;  // dv and da alternate between two copies, de rotates through three
   {
     const HeadOffsets &hE = L.head[0], &hF = L.head[1], &hS = L.head[2];
     struct Lay {
@@ -2287,7 +2664,7 @@ int backward_impl(Ctx& c, const float* Pflat, bool repack, const float* dE, cons
       seg(p, a.dh1ES, 2 * D, 0, D, P + hE.W1, D, 1);
       seg(p, a.dh1ES, 2 * D, D, D, P + hS.W1, D, 1);
       ps.push_back(p);
-      p = gp(E, D, a.de[cur], D);
+      p = gp(E, D, a.de[ecur], D);
       seg(p, a.dh1F, D, 0, D, P + hF.W1, D, 1);
       ps.push_back(p);
       CHG_TRY(run_gemms(ps, st, "gemm_head_bwd0"));
@@ -2323,6 +2700,9 @@ int backward_impl(Ctx& c, const float* Pflat, bool repack, const float* dE, cons
 
   // interaction blocks in reverse
   const bool seq = c.hp->sequential != 0;
+  // at d = 64 (Eq. 11 block) the gate backward also forms the input gradients
+  // of the edge and angle rows (k_gate_bwd_mm)
+  const bool fused = D == 64 && !seq;
   for (int t = m.T - 1; t >= 0; --t) {
     const LayerOffsets& lo = L.layer[t];
     const LayerOffsets& lg = Lg.layer[t];
@@ -2336,7 +2716,7 @@ int backward_impl(Ctx& c, const float* Pflat, bool repack, const float* dE, cons
     const float* Wav = P + lo.av.W;
     const float* Wbe = P + lo.be.W;
     const float* Wan = P + lo.an.W;
-    const int nx = 1 - cur;
+    const int nx = 1 - cur, enx = (ecur + 1) % 3;
     std::vector<GemmProblem> ps;
     std::vector<TnProblem> ts;
     const GateAdds ad_av = adds(2, a.Xa[t], 8 * D, a.edge_src, a.Xa[t] + 2 * D, 8 * D, g.edge_dst);
@@ -2368,6 +2748,45 @@ int backward_impl(Ctx& c, const float* Pflat, bool repack, const float* dE, cons
                              nullptr, nullptr, nullptr, a.dzae + 2 * D, 4 * D);
       }
       return gate_bwd_launch(D, J, wg ? lg_out : nullptr, slot, a, reduce_jobs, st);
+    };
+    // fused gate backward and edge/angle input gradients (d = 64): edges
+    // de(e^t) = de(e^{t+1}) + dz_v W_av,e^T; angles da(a^t) = da(a^{t+1}) +
+    // dz_b W_be,a^T + dz_a W_an,a^T (no angle update in the last layer)
+    auto gates_mm = [&]() -> int {
+      GateBwdMmJobs J{};
+      {
+        GateBwdMmJob& q = J.j[J.n++];
+        q.rows = (int)E;
+        q.ngates = 1;
+        q.gid[0] = 0;
+        q.g[0] = bwd_job(BWD_ATOM, E, a.zv[t], 2 * D, ad_av, ln_ptrs(P, lo.av), a.dm, a.edge_src, a.ea, nullptr, a.dea,
+                         a.dzv, 2 * D);
+        q.g[0].aux_acc = t < m.T - 1;  // the first layer of the backward starts d e^a
+        q.W[0] = Wav + 2 * D * 2 * D;
+        q.res = a.de[ecur];
+        q.dx = a.de[enx];
+      }
+      {
+        GateBwdMmJob& q = J.j[J.n++];
+        q.rows = (int)A;
+        q.ngates = ang ? 2 : 1;
+        q.gid[0] = 1;
+        q.g[0] = bwd_job(BWD_BOND, A, a.zae[t], 4 * D, ad_be, ln_ptrs(P, lo.be), a.dmu, a.ang_b1, a.eb, a.ang_b2, a.t2,
+                         a.dzae, 4 * D);
+        q.W[0] = Wbe + 3 * D * 2 * D;
+        if (ang) {
+          q.gid[1] = 2;
+          q.g[1] = bwd_job(BWD_ANGLE, A, a.zae[t] + 2 * D, 4 * D, ad_an, ln_ptrs(P, lo.an), a.da[cur], nullptr, nullptr,
+                           nullptr, nullptr, a.dzae + 2 * D, 4 * D);
+          q.W[1] = Wan + 3 * D * 2 * D;
+          q.res = a.da[cur];
+        }
+        q.dx = a.da[nx];
+      }
+      const int slot[3] = {3 * t + 1, 3 * t, 3 * t + 2};
+      if (!wg) return gate_bwd_mm_launch(J, nullptr, slot, a, reduce_jobs, st);
+      float* lg_out[3] = {G + lg.av.g_c, G + lg.be.g_c, G + lg.an.g_c};
+      return gate_bwd_mm_launch(J, lg_out, slot, a, reduce_jobs, st);
     };
     // per-bond sums of dz over the bond's two angle roles (DZ12) from `ncols`
     // columns of dzae starting at col0; with_deb also forms d e^b
@@ -2404,7 +2823,7 @@ int backward_impl(Ctx& c, const float* Pflat, bool repack, const float* dE, cons
       if (bonds) {
         GemmProblem p = gp(B, D, a.dmu, D);
         p.a_rows = g.bond_edge;
-        seg(p, a.de[cur], D, 0, D, P + lo.be_Wo, D, 1);
+        seg(p, a.de[ecur], D, 0, D, P + lo.be_Wo, D, 1);
         q.push_back(p);
       }
       return run_gemms(q, st, "gemm_out_bwd");
@@ -2412,7 +2831,7 @@ int backward_impl(Ctx& c, const float* Pflat, bool repack, const float* dE, cons
     SegJobs sj{};
     if (!seq) {
       CHG_TRY(out_bwd(a.dv[cur], true, true));
-      CHG_TRY(gates(7));
+      CHG_TRY(fused ? gates_mm() : gates(7));
       CHG_TRY(bond_reduce(0, W4, true));
       sj.j[sj.n++] = seg_job(N, g.edge_ptr, nullptr, a.dzv, 2 * D, 2 * D, a.AT, 8 * D);
       sj.j[sj.n++] = seg_job(N, g.edge_ptr, g.edge_rev, a.dzv, 2 * D, 2 * D, a.AT + 2 * D, 8 * D);
@@ -2426,7 +2845,7 @@ int backward_impl(Ctx& c, const float* Pflat, bool repack, const float* dE, cons
       if (ang) {
         CHG_TRY(gates(4));
         CHG_TRY(bond_reduce(2 * D, 2 * D, false));
-        GemmProblem p = gp(B, D, a.de[cur], D);
+        GemmProblem p = gp(B, D, a.de[ecur], D);
         p.c_rows = g.bond_edge;
         p.accumulate = 1;
         seg(p, a.DZ12, 8 * D, 2 * D, 2 * D, Wan + D * 2 * D, 2 * D, 1);
@@ -2459,8 +2878,8 @@ int backward_impl(Ctx& c, const float* Pflat, bool repack, const float* dE, cons
     const float* dvo = seq ? a.dvf : a.dv[cur];
     ts.push_back(tp(N, D, D, a.m[t], D, 0, nullptr, dvo, D, 0, nullptr, G + lg.av_Wo, D));
     ts.push_back(tp(N, 1, D, nullptr, 0, 0, nullptr, dvo, D, 0, nullptr, G + lg.av_bo, D));
-    ts.push_back(tp(B, D, D, a.mu[t], D, 0, nullptr, a.de[cur], D, 0, g.bond_edge, G + lg.be_Wo, D));
-    ts.push_back(tp(B, 1, D, nullptr, 0, 0, nullptr, a.de[cur], D, 0, g.bond_edge, G + lg.be_bo, D));
+    ts.push_back(tp(B, D, D, a.mu[t], D, 0, nullptr, a.de[ecur], D, 0, g.bond_edge, G + lg.be_Wo, D));
+    ts.push_back(tp(B, 1, D, nullptr, 0, 0, nullptr, a.de[ecur], D, 0, g.bond_edge, G + lg.be_bo, D));
     // weight gradients of the first linear layers
     {
       const float* vt = a.v[t];
@@ -2505,8 +2924,8 @@ int backward_impl(Ctx& c, const float* Pflat, bool repack, const float* dE, cons
         ts.push_back(tp(A, D, 2 * D, a.a[t], D, 0, nullptr, a.dzae, 4 * D, 0, nullptr, G + lg.be.W + 3 * D * 2 * D, 2 * D));
       }
     }
-    // input gradients (they overwrite dv and de of the layer above, which its
-    // weight gradients read)
+    // input gradients (they overwrite dv of the layer above, which its weight
+    // gradients read; the three copies of de leave the one they read alone)
     if (wg && t + 1 < m.T) CHG_HIP(hipStreamWaitEvent(st, ss.done[t + 1], 0));
     {
       GemmProblem p = gp(N, D, a.dv[nx], D);
@@ -2519,9 +2938,11 @@ int backward_impl(Ctx& c, const float* Pflat, bool repack, const float* dE, cons
       p.res = dvo;
       p.res_ld = D;
       ps.push_back(p);
-      p = gp(E, D, a.de[nx], D);
+    }
+    if (!fused) {
+      GemmProblem p = gp(E, D, a.de[enx], D);
       seg(p, a.dzv, 2 * D, 0, 2 * D, Wav + 2 * D * 2 * D, 2 * D, 1);
-      p.res = a.de[cur];
+      p.res = a.de[ecur];
       p.res_ld = D;
       ps.push_back(p);
       p = gp(A, D, a.da[nx], D);
@@ -2532,9 +2953,15 @@ int backward_impl(Ctx& c, const float* Pflat, bool repack, const float* dE, cons
         p.res_ld = D;
       }
       ps.push_back(p);
-      CHG_TRY(run_gemms(ps, st, "gemm_in_bwd"));
-      ps.clear();
-      p = gp(B, D, a.de[nx], D);
+    }
+    {
+      // fused: the atom rows' product shares the launch of the bond rows'
+      // (both direct-load, k = 8d)
+      if (!fused) {
+        CHG_TRY(run_gemms(ps, st, "gemm_in_bwd"));
+        ps.clear();
+      }
+      GemmProblem p = gp(B, D, a.de[enx], D);
       p.c_rows = g.bond_edge;
       p.accumulate = 1;
       seg(p, a.DZ12, 8 * D, 0, 2 * D, Wbe + D * 2 * D, 2 * D, 1);
@@ -2544,7 +2971,7 @@ int backward_impl(Ctx& c, const float* Pflat, bool repack, const float* dE, cons
         seg(p, a.DZ12, 8 * D, 6 * D, 2 * D, Wan + 2 * D * 2 * D, 2 * D, 1);
       }
       ps.push_back(p);
-      CHG_TRY(run_gemms(ps, st, "gemm_bond_bwd"));
+      CHG_TRY(run_gemms(ps, st, fused ? "gemm_in_bwd" : "gemm_bond_bwd"));
       ps.clear();
     }
     // the weight gradients of this layer run on the side stream, overlapping
@@ -2558,15 +2985,16 @@ int backward_impl(Ctx& c, const float* Pflat, bool repack, const float* dE, cons
     }
     ts.clear();
     cur = nx;
+    ecur = enx;
   }
 
   // embeddings
   if (wg) KLAUNCH(st, "k_embed_bwd_Z", k_embed_bwd_Z<<<24, 256, 0, st>>>((int)N, D, bt.Z, a.dv[cur], G + Lg.W_Z));
   {
     std::vector<TnProblem> ts;
-    ts.push_back(tp(E, m.R, D, a.rbf_a, m.R, 0, nullptr, a.de[cur], D, 0, nullptr, G + Lg.W_e, 2 * D));
+    ts.push_back(tp(E, m.R, D, a.rbf_a, m.R, 0, nullptr, a.de[ecur], D, 0, nullptr, G + Lg.W_e, 2 * D));
     ts.push_back(tp(E, m.R, D, a.rbf_a, m.R, 0, nullptr, a.dea, D, 0, nullptr, G + Lg.W_e + D, 2 * D));
-    ts.push_back(tp(E, 1, D, nullptr, 0, 0, nullptr, a.de[cur], D, 0, nullptr, G + Lg.b_e0, D));
+    ts.push_back(tp(E, 1, D, nullptr, 0, 0, nullptr, a.de[ecur], D, 0, nullptr, G + Lg.b_e0, D));
     ts.push_back(tp(B, m.R, D, a.rbf_b, m.R, 0, nullptr, a.deb, D, 0, nullptr, G + Lg.W_eb, D));
     ts.push_back(tp(A, m.K, D, a.ft, m.K, 0, nullptr, a.da[cur], D, 0, nullptr, G + Lg.W_th, D));
     ts.push_back(tp(A, 1, D, nullptr, 0, 0, nullptr, a.da[cur], D, 0, nullptr, G + Lg.b_th, D));
@@ -2576,7 +3004,7 @@ int backward_impl(Ctx& c, const float* Pflat, bool repack, const float* dE, cons
     }
     std::vector<GemmProblem> ps;
     GemmProblem p = gp(E, m.R, a.drbf_a, m.R);
-    seg(p, a.de[cur], D, 0, D, P + L.W_e, 2 * D, 1);
+    seg(p, a.de[ecur], D, 0, D, P + L.W_e, 2 * D, 1);
     seg(p, a.dea, D, 0, D, P + L.W_e + D, 2 * D, 1);
     ps.push_back(p);
     p = gp(B, m.R, a.drbf_b, m.R);
