@@ -904,9 +904,42 @@ __device__ __forceinline__ void bwd_mm_index(const GateBwdJob& J, int row, BwdMm
   x.b2 = J.mode == BWD_BOND ? J.b2_idx[row] : 0;
 }
 
+// LayerNorm parameter partials of one pass (4 sums x 8 columns per lane,
+// rows in the wavefront's 8 row slots, lane bits 3-5) summed over the slots
+// and added to this wavefront's LDS slot wsum[4][64]. Reduce-scatter: each
+// step pairs the values of two lanes differing in one slot bit, keeping one
+// of two values' sums per lane (the lane-half swaps of gfx950, then a DPP
+// rotate by 8 within a row of 16); afterwards lane (j, b3, b4, b5) holds sum
+// a of column 32 b3 + 4 j + 2 b4 + b5 for a = 0..3, and is that slot's only
+// writer (fixed order, no atomics race).
+__device__ __forceinline__ float pl_sum32(float a, float b) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(a), __float_as_uint(b), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+__device__ __forceinline__ float pl_sum16(float a, float b) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(a), __float_as_uint(b), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+__device__ __forceinline__ void bwd_mm_ln_add(const float (&p)[32], float* wsum) {
+  const int lane = threadIdx.x & 63;
+  float w[16], x[8];
+#pragma unroll
+  for (int m = 0; m < 16; ++m) w[m] = pl_sum32(p[2 * m], p[2 * m + 1]);
+#pragma unroll
+  for (int m = 0; m < 8; ++m) x[m] = pl_sum16(w[2 * m], w[2 * m + 1]);
+  const bool hi = (lane & 8) != 0;
+#pragma unroll
+  for (int m = 0; m < 4; ++m) {
+    const float keep = hi ? x[2 * m + 1] : x[2 * m], send = hi ? x[2 * m] : x[2 * m + 1];
+    const float y = keep + dpp<0x128>(send);  // row_ror:8
+    const int col = 32 * ((lane >> 3) & 1) + 4 * (lane & 7) + 2 * ((lane >> 4) & 1) + ((lane >> 5) & 1);
+    wsum[m * 64 + col] += y;
+  }
+}
+
 template <int MODE>
 __device__ __forceinline__ void gate_bwd_mm_row(const GateBwdJob& J, int row, const BwdMmIdx& x, int j,
-                                                const float* lnS, float (&acc)[4][kMmCpl], float* zrow) {
+                                                const float* lnS, float (&lp)[4 * kMmCpl], float* zrow) {
   constexpr int D = 64, CPL = kMmCpl;
   constexpr int LPR = Lanes<D, CPL>::LPR;
   float zc[CPL], zg[CPL], rc, rg;
@@ -973,10 +1006,10 @@ __device__ __forceinline__ void gate_bwd_mm_row(const GateBwdJob& J, int row, co
     side[k] = silu_c * sg;  // phi
     const float gy_c = dphi[k] * sg * sc * (1.0f + yc * (1.0f - sc));
     const float gy_g = dphi[k] * silu_c * sg * (1.0f - sg);
-    acc[0][k] += gy_c * zc[k];
-    acc[1][k] += gy_c;
-    acc[2][k] += gy_g * zg[k];
-    acc[3][k] += gy_g;
+    lp[k] = gy_c * zc[k];
+    lp[8 + k] = gy_c;
+    lp[16 + k] = gy_g * zg[k];
+    lp[24 + k] = gy_g;
     dyc[k] = gy_c * gc[k];
     dyg[k] = gy_g * gg[k];
     s1c += dyc[k];
@@ -1013,29 +1046,6 @@ __device__ __forceinline__ void gate_bwd_mm_row(const GateBwdJob& J, int row, co
     for (int k = 0; k < CPL; ++k) side[k] *= w[k];
     store_cols<D, CPL>(J.aux + (int64_t)row * D, j, side);
   }
-}
-
-// Sum a consumer's LayerNorm partials over the wavefront's 8 row slots
-// (lanes j + 8 s) in a fixed order, store them to wsum[4][64] and clear them.
-__device__ __forceinline__ void bwd_mm_flush(float (&acc)[4][kMmCpl], float* wsum) {
-  const int lane = threadIdx.x & 63;
-#pragma unroll
-  for (int a = 0; a < 4; ++a)
-#pragma unroll
-    for (int k = 0; k < kMmCpl; ++k) {
-      float v = acc[a][k];
-      v += __shfl_xor(v, 8);
-      v += __shfl_xor(v, 16);
-      v += __shfl_xor(v, 32);
-      acc[a][k] = v;
-    }
-  if (lane < Lanes<64, kMmCpl>::LPR)
-#pragma unroll
-    for (int a = 0; a < 4; ++a) store_cols<64, kMmCpl>(wsum + a * 64, lane, acc[a]);
-#pragma unroll
-  for (int a = 0; a < 4; ++a)
-#pragma unroll
-    for (int k = 0; k < kMmCpl; ++k) acc[a][k] = 0.f;
 }
 
 // One block per compute unit, walking tiles blockIdx.x, blockIdx.x +
@@ -1150,47 +1160,49 @@ __global__ void __launch_bounds__(kMmThreads, 1) k_gate_bwd_mm(GateBwdMmJobs J) 
   } else {
     using GL = Lanes<64, kMmCpl>;
     const int cw = wave - kMmProducers, j = lane % GL::LPR, slot = lane / GL::LPR;
-    float acc[4][kMmCpl];
-#pragma unroll
-    for (int a = 0; a < 4; ++a)
-#pragma unroll
-      for (int k = 0; k < kMmCpl; ++k) acc[a][k] = 0.f;
-    int gid_cur = -1;
+    // Every wavefront covers the same 8 rows of each of the tile's gates
+    // (rows 8 cw + slot), one pass per gate; the row indices of a tile are
+    // loaded one tile ahead.
+    auto tile_job = [&](int ii) { return __builtin_amdgcn_readfirstlane(job_of(tile_of(ii))); };
+    auto load_idx = [&](int ii, BwdMmIdx (&x)[2]) {
+      if (ii >= nt) return;
+      const int tile = tile_of(ii), k = tile_job(ii);
+      const GateBwdMmJob& jb = J.j[k];
+      const int row = (tile - jb.tile0) * kMmRows + 8 * cw + slot;
+      if (row >= jb.rows) return;
+      bwd_mm_index(jb.g[0], row, x[0]);
+      if (jb.ngates > 1) bwd_mm_index(jb.g[1], row, x[1]);
+    };
+    BwdMmIdx xi[2] = {}, xn[2] = {};
+    load_idx(0, xi);
     for (int i = 0; i <= nt; ++i) {
       if (i < nt) {
-        const int tile = tile_of(i);
-        const int k = __builtin_amdgcn_readfirstlane(job_of(tile));
+        load_idx(i + 1, xn);
+        const int tile = tile_of(i), k = tile_job(i);
         const GateBwdMmJob& jb = J.j[k];
-        // the wavefronts are split evenly over the tile's gates; a wavefront
-        // covers 8 ng consecutive rows of its gate, 8 rows per pass
-        const int wpg = kMmConsumers / jb.ngates;
-        const int g = __builtin_amdgcn_readfirstlane(cw / wpg);
-        const int gid = jb.gid[g];
-        if (gid != gid_cur) {
-          if (gid_cur >= 0) bwd_mm_flush(acc, Wsum[gid_cur][cw]);
-          gid_cur = gid;
-        }
-        const GateBwdJob& gj = jb.g[g];
-        const float* lnS = &LnS[k][g][0][0];
-        const int row0 = (tile - jb.tile0) * kMmRows;
+        const int lr = 8 * cw + slot;
+        const int row = (tile - jb.tile0) * kMmRows + lr;
 #pragma unroll
-        for (int sub = 0; sub < 2; ++sub) {
-          if (sub >= jb.ngates) break;
-          const int lr = (cw % wpg) * 8 * jb.ngates + 8 * sub + slot;
-          const int row = row0 + lr;
+        for (int g = 0; g < 2; ++g) {
+          if (g >= jb.ngates) break;
+          const GateBwdJob& gj = jb.g[g];
+          float lp[4 * kMmCpl];
+#pragma unroll
+          for (int q = 0; q < 4 * kMmCpl; ++q) lp[q] = 0.f;
           if (row < jb.rows) {
-            BwdMmIdx x;
-            bwd_mm_index(gj, row, x);
+            const float* lnS = &LnS[k][g][0][0];
             float* zrow = Zs[i & 1] + lr * kBmLd + 128 * g;
-            if (gj.mode == BWD_ATOM) gate_bwd_mm_row<BWD_ATOM>(gj, row, x, j, lnS, acc, zrow);
-            else if (gj.mode == BWD_BOND) gate_bwd_mm_row<BWD_BOND>(gj, row, x, j, lnS, acc, zrow);
-            else gate_bwd_mm_row<BWD_ANGLE>(gj, row, x, j, lnS, acc, zrow);
+            if (gj.mode == BWD_ATOM) gate_bwd_mm_row<BWD_ATOM>(gj, row, xi[g], j, lnS, lp, zrow);
+            else if (gj.mode == BWD_BOND) gate_bwd_mm_row<BWD_BOND>(gj, row, xi[g], j, lnS, lp, zrow);
+            else gate_bwd_mm_row<BWD_ANGLE>(gj, row, xi[g], j, lnS, lp, zrow);
           }
+          bwd_mm_ln_add(lp, Wsum[jb.gid[g]][cw]);
         }
+#pragma unroll
+        for (int g = 0; g < 2; ++g) xi[g] = xn[g];
       }
       __syncthreads();
     }
-    if (gid_cur >= 0) bwd_mm_flush(acc, Wsum[gid_cur][cw]);
   }
   __syncthreads();
   for (int t = threadIdx.x; t < 3 * 4 * 64; t += kMmThreads) {
