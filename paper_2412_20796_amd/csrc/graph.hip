@@ -467,9 +467,9 @@ __global__ void __launch_bounds__(kSearchThreads) k_fill(SearchArgs A, int sort_
 }
 
 // Reverse map: binary search of (i, -n) in the sorted edge list of j.
-__global__ void k_rev(int N, const int* __restrict__ edge_ptr, const int* __restrict__ edge_dst,
-                      const int* __restrict__ edge_img, int* __restrict__ edge_rev, GraphInfo* ginfo) {
-  const int i = blockIdx.x * 4 + (threadIdx.x >> 6);
+__device__ __forceinline__ void rev_atoms(int blk, int N, const int* __restrict__ edge_ptr, const int* __restrict__ edge_dst,
+                                          const int* __restrict__ edge_img, int* __restrict__ edge_rev, GraphInfo* ginfo) {
+  const int i = blk * 4 + (threadIdx.x >> 6);
   if (i >= N) return;
   const int lane = threadIdx.x & 63;
   for (int e = edge_ptr[i] + lane; e < edge_ptr[i + 1]; e += 64) {
@@ -491,10 +491,10 @@ __global__ void k_rev(int N, const int* __restrict__ edge_ptr, const int* __rest
 
 // Angle list of atom i (one wavefront per atom): angle_ptr of its bonds and,
 // if requested, the second bond of each of its k(k-1) angles.
-__global__ void __launch_bounds__(256) k_angles(int N, const int* __restrict__ bond_ptr,
-                                                const long long* __restrict__ angle_base, int* __restrict__ angle_ptr,
-                                                int* __restrict__ angle_b2) {
-  const int i = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+__device__ __forceinline__ void angle_atoms(int blk, int N, const int* __restrict__ bond_ptr,
+                                            const long long* __restrict__ angle_base, int* __restrict__ angle_ptr,
+                                            int* __restrict__ angle_b2) {
+  const int i = blk * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
   if (i >= N) return;
   const int b0 = bond_ptr[i], k = bond_ptr[i + 1] - b0;
   const long long a0 = angle_base[i];
@@ -507,6 +507,19 @@ __global__ void __launch_bounds__(256) k_angles(int N, const int* __restrict__ b
       angle_b2[a0 + x] = b0 + (qq < p ? qq : qq + 1);
     }
   }
+}
+
+// Reverse-edge map and angle lists in one launch: blocks [0, nb) take the
+// reverse edges of atoms 4 b .. 4 b + 3, blocks [nb, 2 nb) their angle lists.
+__global__ void __launch_bounds__(256) k_rev_angles(int N, const int* __restrict__ edge_ptr,
+                                                    const int* __restrict__ edge_dst, const int* __restrict__ edge_img,
+                                                    int* __restrict__ edge_rev, GraphInfo* ginfo,
+                                                    const int* __restrict__ bond_ptr,
+                                                    const long long* __restrict__ angle_base, int* __restrict__ angle_ptr,
+                                                    int* __restrict__ angle_b2) {
+  const int nb = (N + 3) / 4;
+  if ((int)blockIdx.x < nb) rev_atoms(blockIdx.x, N, edge_ptr, edge_dst, edge_img, edge_rev, ginfo);
+  else angle_atoms(blockIdx.x - nb, N, bond_ptr, angle_base, angle_ptr, angle_b2);
 }
 
 // Clears the graph info record and the bin counters (n each).
@@ -635,8 +648,9 @@ int build_graph(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_grap
   while (sort_size < hinfo.max_count) sort_size <<= 1;
   KLAUNCH(st, "k_fill", k_fill<<<N, kSearchThreads, sizeof(unsigned long long) * sort_size, st>>>(A, sort_size, graph->edge_ptr, graph->bond_ptr,
                                                                 graph->edge_dst, graph->edge_img, graph->bond_edge));
-  KLAUNCH(st, "k_rev", k_rev<<<cdiv(N, 4), 256, 0, st>>>(N, graph->edge_ptr, graph->edge_dst, graph->edge_img, graph->edge_rev, g.ginfo));
-  KLAUNCH(st, "k_angles", k_angles<<<cdiv(N, 4), 256, 0, st>>>(N, graph->bond_ptr, g.angle_base, graph->angle_ptr, graph->angle_b2));
+  KLAUNCH(st, "k_rev_angles", k_rev_angles<<<2 * cdiv(N, 4), 256, 0, st>>>(N, graph->edge_ptr, graph->edge_dst, graph->edge_img,
+                                                                       graph->edge_rev, g.ginfo, graph->bond_ptr, g.angle_base,
+                                                                       graph->angle_ptr, graph->angle_b2));
   return CHGNET_OK;
 }
 

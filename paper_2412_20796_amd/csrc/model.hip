@@ -92,36 +92,6 @@ __global__ void __launch_bounds__(256) k_copy4(float4* __restrict__ dst, const f
 // ---------------------------------------------------------------------------
 // Geometry (fp64) and basis expansions (Eq. 2, Alg. 2: whole batch at once).
 // ---------------------------------------------------------------------------
-__global__ void k_atom_struct(int N, int S, const int* __restrict__ atom_ptr, int* __restrict__ atom_struct) {
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < N) atom_struct[i] = upper_bound_idx(atom_ptr, S + 1, i);
-}
-
-__global__ void k_prep_edges(int E, int N, const int* __restrict__ edge_ptr, const int* __restrict__ edge_dst,
-                             const int* __restrict__ edge_img, const int* __restrict__ atom_struct,
-                             const float* __restrict__ pos, const float* __restrict__ lattice, int* __restrict__ edge_src,
-                             float* __restrict__ edge_len, float* __restrict__ edge_xhat) {
-  const int e = blockIdx.x * blockDim.x + threadIdx.x;
-  if (e >= E) return;
-  const int i = upper_bound_idx(edge_ptr, N + 1, e);
-  const int j = edge_dst[e];
-  const float* L = lattice + 9 * atom_struct[i];
-  const double n0 = edge_img[3 * e], n1 = edge_img[3 * e + 1], n2 = edge_img[3 * e + 2];
-  double r[3];
-  for (int c = 0; c < 3; ++c)
-    r[c] = (double)pos[3 * j + c] + (n0 * (double)L[c] + n1 * (double)L[3 + c] + n2 * (double)L[6 + c]) - (double)pos[3 * i + c];
-  const double d = sqrt(r[0] * r[0] + r[1] * r[1] + r[2] * r[2]);
-  edge_src[e] = i;
-  edge_len[e] = (float)d;
-  for (int c = 0; c < 3; ++c) edge_xhat[3 * e + c] = (float)(r[c] / d);
-}
-
-__global__ void k_prep_bonds(int B, const int* __restrict__ bond_edge, const int* __restrict__ edge_src,
-                             int* __restrict__ bond_src) {
-  const int b = blockIdx.x * blockDim.x + threadIdx.x;
-  if (b < B) bond_src[b] = edge_src[bond_edge[b]];
-}
-
 // sRBF_n(r) = sqrt(2/c) sin(f_n r / c) / r * u(r / c), u the polynomial envelope.
 __device__ __forceinline__ float envelope(float x, int p) {
   const float a = -0.5f * (p + 1) * (p + 2), b = (float)(p * (p + 2)), c = -0.5f * p * (p + 1);
@@ -129,46 +99,83 @@ __device__ __forceinline__ float envelope(float x, int p) {
   for (int k = 0; k < p; ++k) xp *= x;
   return 1.0f + xp * (a + x * (b + x * c));
 }
-
-__global__ void k_rbf(int rows, const int* __restrict__ idx, const float* __restrict__ len, const float* __restrict__ freq,
-                      int R, float cutoff, int p, float* __restrict__ out) {
-  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (t >= (int64_t)rows * R) return;
-  const int row = (int)(t / R), n = (int)(t % R);
-  const float d = len[idx ? idx[row] : row];
-  const float inv_c = 1.0f / cutoff;
-  out[t] = sqrtf(2.0f * inv_c) * sinf(freq[n] * d * inv_c) / d * envelope(d * inv_c, p);
+__device__ __forceinline__ float srbf(float f, float d, float inv_c, int p) {
+  return sqrtf(2.0f * inv_c) * sinf(f * d * inv_c) / d * envelope(d * inv_c, p);
 }
 
-// Angles: first bond b1 (run of angle_ptr), second bond b2, centre atom;
-// cos/sin of theta from (dot, |cross|) in fp64 and the Fourier basis by the
-// complex-power recurrence (cos m t + i sin m t) = (cos t + i sin t)^m.
-__global__ void k_prep_angles(int A, int B, const int* __restrict__ angle_ptr, const int* __restrict__ bond_ptr,
-                              const int* __restrict__ bond_edge, const int* __restrict__ bond_src,
-                              const int* __restrict__ edge_dst, const int* __restrict__ edge_img,
-                              const int* __restrict__ atom_struct, const float* __restrict__ pos,
-                              const float* __restrict__ lattice, int K, int* __restrict__ ang_b1, int* __restrict__ ang_b2,
-                              int* __restrict__ ang_ctr, float* __restrict__ ft) {
-  const int al = blockIdx.x * blockDim.x + threadIdx.x;
-  if (al >= A) return;
-  const int b1 = upper_bound_idx(angle_ptr, B + 1, al);
-  const int i = bond_src[b1];
-  const int k0 = bond_ptr[i];
-  const int p = b1 - k0;
-  const int q0 = al - angle_ptr[b1];
-  const int b2 = k0 + (q0 < p ? q0 : q0 + 1);
-  ang_b1[al] = b1;
-  ang_b2[al] = b2;
-  ang_ctr[al] = i;
-  const float* L = lattice + 9 * atom_struct[i];
-  double r[2][3];
-  const int es[2] = {bond_edge[b1], bond_edge[b2]};
-  for (int s = 0; s < 2; ++s) {
-    const int e = es[s], j = edge_dst[e];
-    const double n0 = edge_img[3 * e], n1 = edge_img[3 * e + 1], n2 = edge_img[3 * e + 2];
-    for (int c = 0; c < 3; ++c)
-      r[s][c] = (double)pos[3 * j + c] + (n0 * (double)L[c] + n1 * (double)L[3 + c] + n2 * (double)L[6 + c]) - (double)pos[3 * i + c];
+// Cartesian vector from atom i to the image n of atom j (fp64).
+__device__ __forceinline__ void edge_vector(int i, int j, const int* __restrict__ img, const float* __restrict__ L,
+                                            const float* __restrict__ pos, double (&r)[3]) {
+  const double n0 = img[0], n1 = img[1], n2 = img[2];
+  for (int c = 0; c < 3; ++c)
+    r[c] = (double)pos[3 * j + c] + (n0 * (double)L[c] + n1 * (double)L[3 + c] + n2 * (double)L[6 + c]) - (double)pos[3 * i + c];
+}
+
+// Geometry, bases and the atom embedding of a batch in one launch, by block
+// range: atoms (structure index, v0 = W_Z[Z - 1]); edges, 256 a block
+// (source atom, length, unit vector, then the block's sRBF rows at the atom
+// cutoff); angles (first and second bond, centre atom; cos/sin of theta from
+// (dot, |cross|) in fp64 and the Fourier basis by the complex-power
+// recurrence (cos m t + i sin m t) = (cos t + i sin t)^m).
+struct GeomArgs {
+  int N, S, E, B, A, D, R, K, p, nb_atoms, nb_edges;
+  float inv_ca;
+  const int *atom_ptr, *Z, *edge_ptr, *edge_dst, *edge_img, *bond_ptr, *bond_edge, *angle_ptr;
+  const float *pos, *lattice, *WZ, *freq_a;
+  int *atom_struct, *edge_src, *ang_b1, *ang_b2, *ang_ctr;
+  float *v0, *edge_len, *edge_xhat, *rbf_a, *ft;
+};
+
+__global__ void __launch_bounds__(256) k_geom(GeomArgs g) {
+  __shared__ float dl[256];
+  int blk = blockIdx.x;
+  const int tid = threadIdx.x;
+  if (blk < g.nb_atoms) {
+    const int64_t t = (int64_t)blk * 256 + tid;
+    if (t >= (int64_t)g.N * g.D) return;
+    const int i = (int)(t / g.D), c = (int)(t % g.D);
+    g.v0[t] = g.WZ[(int64_t)(g.Z[i] - 1) * g.D + c];
+    if (c == 0) g.atom_struct[i] = upper_bound_idx(g.atom_ptr, g.S + 1, i);
+    return;
   }
+  blk -= g.nb_atoms;
+  if (blk < g.nb_edges) {
+    const int e0 = blk * 256, e = e0 + tid;
+    float d = 1.0f;
+    if (e < g.E) {
+      const int i = upper_bound_idx(g.edge_ptr, g.N + 1, e);
+      const int j = g.edge_dst[e];
+      double r[3];
+      edge_vector(i, j, g.edge_img + 3 * e, g.lattice + 9 * upper_bound_idx(g.atom_ptr, g.S + 1, i), g.pos, r);
+      const double dd = sqrt(r[0] * r[0] + r[1] * r[1] + r[2] * r[2]);
+      g.edge_src[e] = i;
+      d = (float)dd;
+      g.edge_len[e] = d;
+      for (int c = 0; c < 3; ++c) g.edge_xhat[3 * e + c] = (float)(r[c] / dd);
+    }
+    dl[tid] = d;
+    __syncthreads();
+    const int ne = min(256, g.E - e0);
+    float* out = g.rbf_a + (int64_t)e0 * g.R;
+    for (int t = tid; t < ne * g.R; t += 256) out[t] = srbf(g.freq_a[t % g.R], dl[t / g.R], g.inv_ca, g.p);
+    return;
+  }
+  blk -= g.nb_edges;
+  const int al = blk * 256 + tid;
+  if (al >= g.A) return;
+  const int b1 = upper_bound_idx(g.angle_ptr, g.B + 1, al);
+  const int i = upper_bound_idx(g.bond_ptr, g.N + 1, b1);
+  const int k0 = g.bond_ptr[i];
+  const int p = b1 - k0;
+  const int q0 = al - g.angle_ptr[b1];
+  const int b2 = k0 + (q0 < p ? q0 : q0 + 1);
+  g.ang_b1[al] = b1;
+  g.ang_b2[al] = b2;
+  g.ang_ctr[al] = i;
+  const float* L = g.lattice + 9 * upper_bound_idx(g.atom_ptr, g.S + 1, i);
+  double r[2][3];
+  const int es[2] = {g.bond_edge[b1], g.bond_edge[b2]};
+  for (int s = 0; s < 2; ++s) edge_vector(i, g.edge_dst[es[s]], g.edge_img + 3 * es[s], L, g.pos, r[s]);
   const double dot = r[0][0] * r[1][0] + r[0][1] * r[1][1] + r[0][2] * r[1][2];
   const double cx = r[0][1] * r[1][2] - r[0][2] * r[1][1];
   const double cy = r[0][2] * r[1][0] - r[0][0] * r[1][2];
@@ -176,8 +183,8 @@ __global__ void k_prep_angles(int A, int B, const int* __restrict__ angle_ptr, c
   const double cr = sqrt(cx * cx + cy * cy + cz * cz);
   const double h = sqrt(dot * dot + cr * cr);
   const double c1 = dot / h, s1 = cr / h;
-  const int M = (K - 1) / 2;
-  float* o = ft + (int64_t)al * K;
+  const int M = (g.K - 1) / 2;
+  float* o = g.ft + (int64_t)al * g.K;
   const double inv_sqrt_pi = 0.56418958354775628695;
   o[0] = (float)(inv_sqrt_pi * 0.70710678118654752440);
   double cm = 1.0, sm = 0.0;
@@ -190,11 +197,25 @@ __global__ void k_prep_angles(int A, int B, const int* __restrict__ angle_ptr, c
   }
 }
 
-__global__ void k_embed_v0(int N, int D, const int* __restrict__ Z, const float* __restrict__ WZ, float* __restrict__ v0) {
-  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (t >= (int64_t)N * D) return;
-  const int i = (int)(t / D), c = (int)(t % D);
-  v0[t] = WZ[(int64_t)(Z[i] - 1) * D + c];
+// Per bond (256 a block): source atom and the block's sRBF rows at the bond
+// cutoff (from the edge lengths).
+__global__ void __launch_bounds__(256) k_bond_geom(int B, int R, int p, float inv_c, const int* __restrict__ bond_edge,
+                                                   const int* __restrict__ edge_src, const float* __restrict__ edge_len,
+                                                   const float* __restrict__ freq, int* __restrict__ bond_src,
+                                                   float* __restrict__ rbf_b) {
+  __shared__ float dl[256];
+  const int b0 = blockIdx.x * 256, b = b0 + threadIdx.x;
+  float d = 1.0f;
+  if (b < B) {
+    const int e = bond_edge[b];
+    bond_src[b] = edge_src[e];
+    d = edge_len[e];
+  }
+  dl[threadIdx.x] = d;
+  __syncthreads();
+  const int nbk = min(256, B - b0);
+  float* out = rbf_b + (int64_t)b0 * R;
+  for (int t = threadIdx.x; t < nbk * R; t += 256) out[t] = srbf(freq[t % R], dl[t / R], inv_c, p);
 }
 
 // ---------------------------------------------------------------------------
@@ -2291,26 +2312,26 @@ int forward_impl(Ctx& c, const float* Pflat, float* energy, float* forces, float
   const int D = m.D, V = D / 64;
   const int64_t N = m.N, S = m.S, E = m.E, B = m.B, A = m.A;
 
-  // geometry and bases
-  KLAUNCH(st, "k_atom_struct", k_atom_struct<<<(unsigned)cdiv(N, 256), 256, 0, st>>>((int)N, (int)S, bt.atom_ptr, a.atom_struct));
-  if (E > 0) {
-    KLAUNCH(st, "k_prep_edges", k_prep_edges<<<(unsigned)cdiv(E, 256), 256, 0, st>>>((int)E, (int)N, g.edge_ptr, g.edge_dst, g.edge_img, a.atom_struct,
-                                                         bt.pos, bt.lattice, a.edge_src, a.edge_len, a.edge_xhat));
-    KLAUNCH(st, "k_rbf", k_rbf<<<(unsigned)cdiv(E * m.R, 256), 256, 0, st>>>((int)E, nullptr, a.edge_len, P + L.f_a, m.R, c.hp->r_atom,
-                                                        c.hp->envelope_p, a.rbf_a));
+  // geometry, bases and v0 (Eq. 2)
+  {
+    GeomArgs ga{};
+    ga.N = (int)N; ga.S = (int)S; ga.E = (int)E; ga.B = (int)B; ga.A = (int)A; ga.D = D; ga.R = m.R; ga.K = m.K;
+    ga.p = c.hp->envelope_p;
+    ga.inv_ca = 1.0f / c.hp->r_atom;
+    ga.nb_atoms = (int)cdiv(N * D, 256);
+    ga.nb_edges = (int)cdiv(E, 256);
+    ga.atom_ptr = bt.atom_ptr; ga.Z = bt.Z; ga.edge_ptr = g.edge_ptr; ga.edge_dst = g.edge_dst; ga.edge_img = g.edge_img;
+    ga.bond_ptr = g.bond_ptr; ga.bond_edge = g.bond_edge; ga.angle_ptr = g.angle_ptr;
+    ga.pos = bt.pos; ga.lattice = bt.lattice; ga.WZ = P + L.W_Z; ga.freq_a = P + L.f_a;
+    ga.atom_struct = a.atom_struct; ga.edge_src = a.edge_src; ga.ang_b1 = a.ang_b1; ga.ang_b2 = a.ang_b2; ga.ang_ctr = a.ang_ctr;
+    ga.v0 = a.v[0]; ga.edge_len = a.edge_len; ga.edge_xhat = a.edge_xhat; ga.rbf_a = a.rbf_a; ga.ft = a.ft;
+    const int64_t blocks = ga.nb_atoms + ga.nb_edges + cdiv(A, 256);
+    KLAUNCH(st, "k_geom", k_geom<<<(unsigned)blocks, 256, 0, st>>>(ga));
   }
-  if (B > 0) {
-    KLAUNCH(st, "k_prep_bonds", k_prep_bonds<<<(unsigned)cdiv(B, 256), 256, 0, st>>>((int)B, g.bond_edge, a.edge_src, a.bond_src));
-    KLAUNCH(st, "k_rbf", k_rbf<<<(unsigned)cdiv(B * m.R, 256), 256, 0, st>>>((int)B, g.bond_edge, a.edge_len, P + L.f_b, m.R, c.hp->r_bond,
-                                                        c.hp->envelope_p, a.rbf_b));
-  }
-  if (A > 0) {
-    KLAUNCH(st, "k_prep_angles", k_prep_angles<<<(unsigned)cdiv(A, 256), 256, 0, st>>>((int)A, (int)B, g.angle_ptr, g.bond_ptr, g.bond_edge, a.bond_src,
-                                                          g.edge_dst, g.edge_img, a.atom_struct, bt.pos, bt.lattice, m.K,
-                                                          a.ang_b1, a.ang_b2, a.ang_ctr, a.ft));
-  }
-  // embeddings (Eq. 2)
-  KLAUNCH(st, "k_embed_v0", k_embed_v0<<<(unsigned)cdiv(N * D, 256), 256, 0, st>>>((int)N, D, bt.Z, P + L.W_Z, a.v[0]));
+  if (B > 0)
+    KLAUNCH(st, "k_bond_geom", k_bond_geom<<<(unsigned)cdiv(B, 256), 256, 0, st>>>((int)B, m.R, c.hp->envelope_p,
+                                                                              1.0f / c.hp->r_bond, g.bond_edge, a.edge_src,
+                                                                              a.edge_len, P + L.f_b, a.bond_src, a.rbf_b));
   {
     std::vector<GemmProblem> ps;
     GemmProblem p = gp(E, D, a.e[0], D);
