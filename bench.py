@@ -41,6 +41,9 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample", type=int, default=0, help="structures in the CPU oracle sample (0 = auto)")
     ap.add_argument("--no-roofline", action="store_true")
+    ap.add_argument("--launch-timing-only", action="store_true",
+                    help="warm-up and timed steps all with per-launch timing (the library's side stream then runs "
+                         "serialized, as in the roofline pass); prints the per-kernel figures only, for profiling runs")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="first run a plain 256 MiB device copy (reference for HBM traffic counters)")
     ap.add_argument("--md", action="store_true",
@@ -110,6 +113,18 @@ def main():
         dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
+    if args.launch_timing_only:
+        n = max(args.warmup, 1) + args.steps
+        bd.profile_start(400 * n + 1000)
+        for _ in range(n):
+            one_step()
+        torch.cuda.synchronize()
+        prof = bd.profile_stop()
+        E, B, A = g.n_edges, g.n_bonds, g.n_angles
+        rl, rows = roofline(prof, n, dict(N=b.n_atoms, E=E, B=B, A=A, S=b.n_struct, D=d, T=T,
+                                          fused_bwd=d == 64 and not args.sequential, workload=args.workload))
+        print(json.dumps({"launch_timing_steps": n, "roofline": rl, "kernels": rows}), flush=True)
+        return
     for _ in range(max(args.warmup, 1)):
         one_step()
     torch.cuda.synchronize()
