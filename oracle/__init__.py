@@ -15,5 +15,10 @@ Modules:
     model  - parameter layout, basis expansions, embeddings, interaction
              blocks in the dependency-free form, Force/Stress/Energy heads,
              loss, backward for every parameter, Adam.
+    md     - velocity-Verlet molecular dynamics with the model's forces.
+    autodiff - an independent PyTorch fp64 transcription of the forward,
+             differentiated by autograd: a witness of the hand-written
+             backward and the training gradient through the conservative
+             readout (second derivatives).
 """
 from . import graph, model  # noqa: F401
