@@ -1235,6 +1235,133 @@ __global__ void __launch_bounds__(kMmThreads, 1) k_gate_bwd_mm(GateBwdMmJobs J) 
   }
 }
 
+// ---------------------------------------------------------------------------
+// Readout MLPs (d = 64): the three layers of a head in one pass over its
+// rows, h1 = x W1 + b1, a1 = SiLU(h1), h2 = a1 W2 + b2, a2 = SiLU(h2),
+// o = a2 W3 + b3 (h1, a1, h2, a2 kept for the backward pass). A wavefront
+// takes 32 rows at a time: fp32 MFMA 32x32x2 with each layer's weights
+// loaded as B fragments just before it (cache-resident; lane half h supplies
+// k = 32 kb + 16 h + e in step e of 32-wide k block kb), the activations passed between layers through a
+// per-wavefront LDS tile, and the output layer as per-row dot products (each
+// lane half sums its 32 k in order, then the halves are added).
+// ---------------------------------------------------------------------------
+struct HeadJob {
+  int rows, tile0, out;
+  const float *x, *W1, *b1, *W2, *b2, *W3, *b3;
+  float *h1, *a1, *h2, *a2, *o;
+};
+struct HeadJobs {
+  int n, ntiles;
+  HeadJob j[3];
+};
+constexpr int kHdRows = 32, kHdLd = 64 + 4;
+
+__device__ __forceinline__ void hd_bfrag(const float* __restrict__ W, int lane, float (&b)[2][2][16]) {
+  const int l32 = lane & 31, h = lane >> 5;
+#pragma unroll
+  for (int ct = 0; ct < 2; ++ct)
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) b[ct][kb][e] = W[(32 * kb + 16 * h + e) * 64 + 32 * ct + l32];
+}
+
+// one dense layer of a 32-row tile: acc[ct] = A W (A fragments af)
+__device__ __forceinline__ void hd_layer(const float (&af)[2][16], const float (&b)[2][2][16], v16f (&acc)[2]) {
+#pragma unroll
+  for (int ct = 0; ct < 2; ++ct)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) acc[ct][e] = 0.f;
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+    for (int e = 0; e < 16; ++e)
+#pragma unroll
+      for (int ct = 0; ct < 2; ++ct) acc[ct] = __builtin_amdgcn_mfma_f32_32x32x2f32(af[kb][e], b[ct][kb][e], acc[ct], 0, 0, 0);
+}
+
+// bias and SiLU of a layer's tile: h and a to global memory (rows below
+// `rows`), a to the wavefront's LDS tile
+__device__ __forceinline__ void hd_epilogue(const v16f (&acc)[2], const float* __restrict__ bias, int rows, int row0,
+                                            float* __restrict__ hout, float* __restrict__ aout, float* Tw, int lane) {
+  const int l32 = lane & 31, h = lane >> 5;
+#pragma unroll
+  for (int ct = 0; ct < 2; ++ct) {
+    const int c = 32 * ct + l32;
+    const float bc = bias[c];
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      const int r = 8 * (j >> 2) + 4 * h + (j & 3);
+      const float hv = acc[ct][j] + bc;
+      const float av = hv * sigm(hv);
+      if (row0 + r < rows) {
+        hout[(int64_t)(row0 + r) * 64 + c] = hv;
+        aout[(int64_t)(row0 + r) * 64 + c] = av;
+      }
+      Tw[r * kHdLd + c] = av;
+    }
+  }
+}
+
+// the wavefront's LDS writes are visible to all its lanes
+__device__ __forceinline__ void hd_wave_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+__global__ void __launch_bounds__(256, 2) k_head_mlp(HeadJobs J) {
+  __shared__ __attribute__((aligned(16))) float T[4][kHdRows * kHdLd];
+  const int lane = threadIdx.x & 63, l32 = lane & 31, h = lane >> 5;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  float* Tw = T[wave];
+  float bf[2][2][16];
+  const int nw = (int)gridDim.x * 4;
+  for (int tile = (int)blockIdx.x * 4 + wave; tile < J.ntiles; tile += nw) {
+    int k = 0;
+    while (k + 1 < J.n && tile >= J.j[k + 1].tile0) ++k;
+    k = __builtin_amdgcn_readfirstlane(k);
+    const HeadJob& jb = J.j[k];
+    hd_bfrag(jb.W1, lane, bf);
+    const int row0 = (tile - jb.tile0) * kHdRows, row = row0 + l32;
+    const bool valid = row < jb.rows;
+    float af[2][16];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (valid) v = *reinterpret_cast<const float4*>(jb.x + (int64_t)row * 64 + 32 * kb + 16 * h + 4 * q);
+        af[kb][4 * q] = v.x; af[kb][4 * q + 1] = v.y; af[kb][4 * q + 2] = v.z; af[kb][4 * q + 3] = v.w;
+      }
+    v16f acc[2];
+    hd_layer(af, bf, acc);
+    hd_epilogue(acc, jb.b1, jb.rows, row0, jb.h1, jb.a1, Tw, lane);
+    hd_wave_sync();
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const float4 v = *reinterpret_cast<const float4*>(Tw + l32 * kHdLd + 32 * kb + 16 * h + 4 * q);
+        af[kb][4 * q] = v.x; af[kb][4 * q + 1] = v.y; af[kb][4 * q + 2] = v.z; af[kb][4 * q + 3] = v.w;
+      }
+    hd_bfrag(jb.W2, lane, bf);
+    hd_wave_sync();
+    hd_layer(af, bf, acc);
+    hd_epilogue(acc, jb.b2, jb.rows, row0, jb.h2, jb.a2, Tw, lane);
+    hd_wave_sync();
+    // output layer: lane (row l32, half h) sums k in [32 h, 32 h + 32)
+    for (int c = 0; c < jb.out; ++c) {
+      float s = 0.f;
+#pragma unroll 8
+      for (int kk = 0; kk < 32; ++kk) s += Tw[l32 * kHdLd + 32 * h + kk] * jb.W3[(32 * h + kk) * jb.out + c];
+      s += __shfl_xor(s, 32);
+      if (h == 0 && valid) jb.o[(int64_t)row * jb.out + c] = s + jb.b3[c];
+    }
+    hd_wave_sync();
+  }
+}
+
 // Segmented row sums, several independent jobs per launch:
 //   out[s] (+)= sum_{r in [ptr[s], ptr[s+1])} vals[idx(r)]; optionally
 //   out2[s] = mul[s] * sum. WPS wavefronts per (segment, 64 columns) split the
@@ -2530,8 +2657,8 @@ int forward_impl(Ctx& c, const float* Pflat, float* energy, float* forces, float
     }
   }
 
-  // heads: MLP d -> d -> d -> out with SiLU
-  {
+  // heads: MLP d -> d -> d -> out with SiLU (d = 128: three GEMM launches)
+  if (D != 64) {
     const HeadOffsets &hE = L.head[0], &hF = L.head[1], &hS = L.head[2];
     const float* vT = a.v[m.T];
     const float* eT = a.e[m.T];
@@ -2569,6 +2696,24 @@ int forward_impl(Ctx& c, const float* Pflat, float* energy, float* forces, float
       ps.push_back(p);
     }
     CHG_TRY(run_gemms(ps, st, "gemm_head3"));
+  }
+  if (D == 64) {
+    // heads: MLP d -> d -> d -> out with SiLU, the three layers in one launch
+    const HeadOffsets &hE = L.head[0], &hF = L.head[1], &hS = L.head[2];
+    HeadJobs J{};
+    int tiles = 0;
+    auto add = [&](const float* x, int64_t rows, const HeadOffsets& h, float* h1, float* a1, float* h2, float* a2, float* o) {
+      if (rows <= 0) return;
+      HeadJob& q = J.j[J.n++];
+      q = HeadJob{(int)rows, tiles, h.out, x, P + h.W1, P + h.b1, P + h.W2, P + h.b2, P + h.W3, P + h.b3, h1, a1, h2, a2, o};
+      tiles += (int)cdiv(rows, kHdRows);
+    };
+    add(a.e[m.T], E, hF, a.hF1, a.aF1, a.hF2, a.aF2, a.oF);
+    add(a.v[m.T], N, hE, a.hE1, a.aE1, a.hE2, a.aE2, a.oE);
+    add(a.v[m.T], N, hS, a.hS1, a.aS1, a.hS2, a.aS2, a.oS);
+    J.ntiles = tiles;
+    const int blocks = (int)std::min<int64_t>(cdiv(tiles, 4), 512);
+    KLAUNCH(st, "k_head_mlp", k_head_mlp<<<blocks, 256, 0, st>>>(J));
   }
   KLAUNCH(st, "k_struct_heads", k_struct_heads<<<(unsigned)S, 256, 0, st>>>((int)S, bt.atom_ptr, bt.lattice, a.oE, a.oS, energy, stress));
   KLAUNCH(st, "k_forces", k_forces<<<(unsigned)cdiv(N, 4), 256, 0, st>>>((int)N, g.edge_ptr, g.edge_rev, a.oF, a.edge_xhat, forces));
