@@ -471,12 +471,13 @@ __device__ __forceinline__ void tn_wave(const TnPlan& Q, int chunk, int m0, int 
   float ysum[VY];
 #pragma unroll
   for (int u = 0; u < VY; ++u) ysum[u] = 0.f;
-  float xf[2][KS][VX], yf[2][KS][VY];
+  constexpr int NB = 4;  // register buffers: NB - 1 groups in flight ahead of the MFMAs
+  float xf[NB][KS][VX], yf[NB][KS][VY];
   // Branch-free loads: rows and columns are clamped into the matrix. Columns
   // past M or N only reach outputs that are not stored; rows past the wave's
   // range are cancelled by a 0/1 mask on the Y values, applied when the
   // group is consumed, so that every load of a group is in flight at once.
-  float rmask[2][KS];
+  float rmask[NB][KS];
   auto fetch = [&](int g, int b) {
     int xr[KS], yr[KS];
 #pragma unroll
@@ -533,17 +534,25 @@ __device__ __forceinline__ void tn_wave(const TnPlan& Q, int chunk, int m0, int 
       }
     }
   };
-  // two register buffers, alternating with a constant index; a fixed trip
-  // count (rows past the range are masked) keeps the accumulators in place
-  constexpr int GR = 2 * KS;  // rows per group
-  const int iters = rhi > rlo ? (rhi - rlo + 2 * GR - 1) / (2 * GR) : 0;
-  if (iters > 0) fetch(rlo, 0);
+  // a ring of NB register buffers with constant indices (NB groups per
+  // iteration); a fixed trip count (rows past the range are masked) keeps
+  // the accumulators in place
+  constexpr int GRW = 2 * KS;  // rows per group (KS per lane half)
+  const int iters = rhi > rlo ? (rhi - rlo + NB * GRW - 1) / (NB * GRW) : 0;
+  if (iters > 0) {
+#pragma unroll
+    for (int b = 0; b < NB - 1; ++b) fetch(rlo + b * GRW, b);
+  }
   for (int it = 0; it < iters; ++it) {
-    const int g = rlo + it * 2 * GR;
-    fetch(g + GR, 1);
+    const int g = rlo + it * NB * GRW;
+    const bool more = it + 1 < iters;
+    fetch(g + (NB - 1) * GRW, NB - 1);
     compute(0);
-    if (it + 1 < iters) fetch(g + 2 * GR, 0);
-    compute(1);
+#pragma unroll
+    for (int b = 1; b < NB; ++b) {
+      if (more) fetch(g + (NB - 1 + b) * GRW, b - 1);
+      compute(b);
+    }
   }
   // column sums: the two lane halves hold different rows of the same column
   if (colsum) {
