@@ -989,6 +989,10 @@ __device__ __forceinline__ void gate_bwd_mm_row(const GateBwdJob& J, int row, co
       zg[k] += ug[k];
     }
   }
+  // the running sum d e^a of this edge, loaded with the row's other inputs
+  // (after the dz stores the load could not be moved ahead of them)
+  float de[CPL];
+  if (MODE == BWD_ATOM && J.aux_acc) load_cols<D, CPL>(J.aux + (int64_t)row * D, j, de);
   float u[CPL], w[CPL], dphi[CPL];
   if (MODE == BWD_ANGLE) {
     load_cols<D, CPL>(J.up + (int64_t)row * D, j, dphi);
@@ -1052,9 +1056,7 @@ __device__ __forceinline__ void gate_bwd_mm_row(const GateBwdJob& J, int row, co
   store_cols<D, CPL>(zrow, j, dyc);
   store_cols<D, CPL>(zrow + D, j, dyg);
   if (MODE == BWD_ATOM) {
-    float de[CPL];
     if (J.aux_acc) {
-      load_cols<D, CPL>(J.aux + (int64_t)row * D, j, de);
 #pragma unroll
       for (int k = 0; k < CPL; ++k) de[k] += u[k] * side[k];
     } else {
