@@ -498,8 +498,21 @@ __device__ __forceinline__ void gate_mm_row(const GateMmJob& J, int row, int lr,
   const int j = (threadIdx.x & 63) % L::LPR;
   if (row >= J.rows) return;
   float zc[CPL], zg[CPL], rc, rg;
-  load_cols<D, CPL>(Zs + lr * kMmZld, j, zc);
-  load_cols<D, CPL>(Zs + lr * kMmZld + D, j, zg);
+  {
+    // odd rows of the z tile hold the two 32-column halves of each 64-column
+    // block swapped (written so by the producers): the two rows of a read
+    // phase fall in different banks
+    const float* zr = Zs + lr * kMmZld;
+    const int sw = (lr & 1) * 32;
+#pragma unroll
+    for (int q = 0; q < CPL / 4; ++q) {
+      const int cc = (q * L::STRIDE + 4 * j) ^ sw;
+      const float4 a = *reinterpret_cast<const float4*>(zr + cc);
+      const float4 b = *reinterpret_cast<const float4*>(zr + D + cc);
+      zc[4 * q] = a.x; zc[4 * q + 1] = a.y; zc[4 * q + 2] = a.z; zc[4 * q + 3] = a.w;
+      zg[4 * q] = b.x; zg[4 * q + 1] = b.y; zg[4 * q + 2] = b.z; zg[4 * q + 3] = b.w;
+    }
+  }
   if (J.zsave) {
     store_cols_nt<D, CPL>(J.zsave + (int64_t)row * J.ldzs, j, zc);
     store_cols_nt<D, CPL>(J.zsave + (int64_t)row * J.ldzs + D, j, zg);
@@ -603,7 +616,7 @@ __device__ __forceinline__ void mm_tile(const float* X, float* Z, const float (&
   for (int s = 0; s < kMmRows / 32; ++s)
 #pragma unroll
     for (int e = 0; e < 16; ++e)
-      Z[(32 * s + 8 * (e >> 2) + 4 * h + (e & 3)) * kMmZld + 32 * wave + l32] = acc[s][e] + bias;
+      Z[(32 * s + 8 * (e >> 2) + 4 * h + (e & 3)) * kMmZld + ((32 * wave + l32) ^ ((e & 1) * 32))] = acc[s][e] + bias;
 }
 
 // One block per compute unit, walking tiles blockIdx.x, blockIdx.x +
@@ -1053,8 +1066,18 @@ __device__ __forceinline__ void gate_bwd_mm_row(const GateBwdJob& J, int row, co
   }
   store_cols<D, CPL>(J.dz + (int64_t)row * J.lddz, j, dyc);
   store_cols<D, CPL>(J.dz + (int64_t)row * J.lddz + D, j, dyg);
-  store_cols<D, CPL>(zrow, j, dyc);
-  store_cols<D, CPL>(zrow + D, j, dyg);
+  // LDS tile: odd rows hold their two 32-column halves of each 64-column
+  // block swapped (logical column c at c ^ 32), so that the two rows of a
+  // write phase fall in different banks; the producers read with the same map
+  {
+    const int sw = (row & 1) * 32;
+#pragma unroll
+    for (int q = 0; q < CPL / 4; ++q) {
+      const int cc = (q * Lanes<D, CPL>::STRIDE + 4 * j) ^ sw;
+      *reinterpret_cast<float4*>(zrow + cc) = make_float4(dyc[4 * q], dyc[4 * q + 1], dyc[4 * q + 2], dyc[4 * q + 3]);
+      *reinterpret_cast<float4*>(zrow + D + cc) = make_float4(dyg[4 * q], dyg[4 * q + 1], dyg[4 * q + 2], dyg[4 * q + 3]);
+    }
+  }
   if (MODE == BWD_ATOM) {
     if (J.aux_acc) {
 #pragma unroll
@@ -1158,7 +1181,8 @@ __global__ void __launch_bounds__(kMmThreads, 1) k_gate_bwd_mm(GateBwdMmJobs J) 
               float4 a4[4];
 #pragma unroll
               for (int rt = 0; rt < 4; ++rt)
-                a4[rt] = *reinterpret_cast<const float4*>(Z + (16 * rt + n) * kBmLd + 128 * g + 32 * q4 + 4 * s4);
+                a4[rt] = *reinterpret_cast<const float4*>(Z + (16 * rt + n) * kBmLd + 128 * g +
+                                                          ((32 * q4 + 4 * s4) ^ ((n & 1) * 32)));
 #pragma unroll
               for (int rt = 0; rt < 4; ++rt) acc[rt] = __builtin_amdgcn_mfma_f32_16x16x4f32(a4[rt].x, bf[g][4 * s4], acc[rt], 0, 0, 0);
 #pragma unroll
