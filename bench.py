@@ -35,7 +35,7 @@ def parse():
     ap.add_argument("--huber", type=float, default=0.0, help="model variant: Huber loss with this delta (0 = MSE)")
     ap.add_argument("--sequential", action="store_true", help="model variant: the Eq. (10) interaction block")
     ap.add_argument("--conservative", action="store_true",
-                    help="with --md or --forward-only: forces and stress as derivatives of the energy")
+                    help="forces and stress as derivatives of the energy (training: second derivatives)")
     ap.add_argument("--forward-only", action="store_true",
                     help="time inference (graph build + forward with the readout) instead of training steps")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -79,10 +79,6 @@ def main():
     if args.md:
         print(json.dumps(md_bench(args, bd, synth, dev)), flush=True)
         return
-    if args.conservative and not args.forward_only:
-        print("bench.py: training through the conservative readout is not supported (use --md or --forward-only)",
-              file=sys.stderr)
-        sys.exit(2)
     b, params, targets, d, T = synth.workload_inputs(args.workload, magmom=args.magmom)
     hp = bd.hparams(d=d, n_layers=T, magmom=args.magmom, sequential=args.sequential, conservative=args.conservative)
     db = bd.DeviceBatch.from_host(b, dev)
@@ -456,6 +452,13 @@ def cpu_baseline(workload, sample, min_seconds=10.0, variant=None):
 
             graph = og.build_graph(sb.atom_ptr, sb.pos, sb.lattice, hp.r_atom, hp.r_bond)
             om.forward(hp, sb, graph, params.astype(np.float64))
+        elif hp.conservative:
+            # the loss gradient through F = -dE/dr: second derivatives by autograd
+            from oracle import autodiff
+            from oracle import graph as og
+
+            graph = og.build_graph(sb.atom_ptr, sb.pos, sb.lattice, hp.r_atom, hp.r_bond)
+            autodiff.loss_and_grad(hp, sb, graph, params.astype(np.float64), tgt, delta=delta)
         else:
             _, _, _, graph = om.step(hp, sb, params.astype(np.float64), tgt, delta=delta)
         n_edges = len(graph["edge_dst"])

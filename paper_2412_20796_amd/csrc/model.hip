@@ -2423,6 +2423,8 @@ struct Ctx {
   ParamLayout L;   // public layout (gradients)
   ParamLayout La;  // aligned layout of the internal weight copy (reads)
   Acts a;
+  char* ws;        // workspace, and the bytes the activations use of it
+  size_t ws_bytes, ws_used;
 };
 
 int make_ctx(const chgnet_hparams* hp, const chgnet_batch* batch, const chgnet_graph* graph, void* ws, size_t ws_bytes,
@@ -2447,6 +2449,9 @@ int make_ctx(const chgnet_hparams* hp, const chgnet_batch* batch, const chgnet_g
   ar.used = graph_scratch_bytes(c.dm.N, c.dm.S);
   carve_acts(ar, c.dm, c.a, c.La.total);
   if (!ws || !ar.ok()) return fail(CHGNET_EWORKSPACE, "workspace too small (query chgnet_workspace_size)");
+  c.ws = static_cast<char*>(ws);
+  c.ws_bytes = ws_bytes;
+  c.ws_used = ar.used;
   return CHGNET_OK;
 }
 
@@ -3247,6 +3252,8 @@ int backward_impl(Ctx& c, const float* Pflat, bool repack, const float* dE, cons
   return CHGNET_OK;
 }
 
+#include "dual.hpp"
+
 }  // namespace
 
 // Conservative readout after a forward pass: the backward of E with respect
@@ -3297,6 +3304,11 @@ size_t acts_bytes(const chgnet_hparams& hp, int64_t N, int64_t E, int64_t B, int
   Acts a;
   Dims m{N, S, E, B, A, hp.d, hp.n_layers, hp.n_rbf, hp.n_fourier};
   carve_acts(ar, m, a, make_layout(hp, 4).total);
+  if (hp.conservative) {
+    // dual-number buffers of the weight gradient through the conservative readout
+    DualBufs d;
+    carve_dual(ar, m, make_layout(hp, 1).total, d);
+  }
   return align_up(ar.used, 256);
 }
 
@@ -3317,8 +3329,11 @@ int backward_entry(const chgnet_hparams* hp, const chgnet_batch* batch, const ch
   CHG_TRY(make_ctx(hp, batch, graph, ws, ws_bytes, c));
   if (!params || !dE || !dF || !dS || !grad) return fail(CHGNET_EINVAL, "backward: null argument");
   if (dM && !hp->magmom) return fail(CHGNET_EINVAL, "backward: dM without the magnetic-moment head");
-  if (hp->conservative)
-    return fail(CHGNET_EINVAL, "backward: the conservative readout needs second derivatives (not supported)");
+  if (hp->conservative) {
+    if (dM) return fail(CHGNET_EINVAL, "backward: the conservative readout is trained without the magnetic-moment head");
+    CHG_TRY(pack_params(c.L, c.La, params, c.a.Pal, st));
+    return cons_grad_impl(c, dE, dF, dS, grad, st);
+  }
   return backward_impl(c, params, true, dE, dF, dS, dM, grad, st);
 }
 
@@ -3328,8 +3343,8 @@ int step_entry(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_graph
                size_t ws_bytes, hipStream_t st) {
   if (!params || !E_t || !F_t || !S_t || !loss_cfg || !loss || !grad) return fail(CHGNET_EINVAL, "step: null argument");
   CHG_TRY(validate_hparams(hp));
-  if (hp->conservative)
-    return fail(CHGNET_EINVAL, "step: training through the conservative readout needs second derivatives (not supported)");
+  if (hp->conservative && (hp->sequential || hp->magmom))
+    return fail(CHGNET_EINVAL, "step: the conservative readout is trained with the Eq. (11) block and without the magnetic-moment head");
   if ((M_t != nullptr) != (hp->magmom != 0))
     return fail(CHGNET_EINVAL, "step: M_target is required with the magnetic-moment head and only with it");
   if (!std::isfinite(loss_cfg->huber_delta)) return fail(CHGNET_EINVAL, "step: huber_delta is not finite");
@@ -3356,11 +3371,13 @@ int step_entry(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_graph
   float* f_out = c.a.out_F;
   float* s_out = c.a.out_S;
   CHG_TRY(forward_impl(c, params, e_out, f_out, s_out, nullptr, st, false));
+  if (hp->conservative) CHG_TRY(conservative_impl(c, f_out, s_out, st));
   const bool mag = hp->magmom != 0;
   KLAUNCH(st, "k_loss", k_loss<<<1, 256, 0, st>>>((int)c.dm.S, (int)c.dm.N, batch->atom_ptr, e_out, f_out, s_out,
                                                    mag ? c.a.oM : nullptr, E_t, F_t, S_t, M_t, *loss_cfg, loss, c.a.dE,
                                                    c.a.dF, c.a.dS, c.a.dM));
-  CHG_TRY(backward_impl(c, params, false, c.a.dE, c.a.dF, c.a.dS, mag ? c.a.dM : nullptr, grad, st));
+  if (hp->conservative) CHG_TRY(cons_grad_impl(c, c.a.dE, c.a.dF, c.a.dS, grad, st));
+  else CHG_TRY(backward_impl(c, params, false, c.a.dE, c.a.dF, c.a.dS, mag ? c.a.dM : nullptr, grad, st));
   if (adam_hp) {
     const float lr = adam_hp[0], b1 = adam_hp[1], b2 = adam_hp[2], eps = adam_hp[3], t = adam_hp[4];
     const float c1 = 1.0f - powf(b1, t), c2 = 1.0f - powf(b2, t);

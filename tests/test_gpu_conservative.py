@@ -1,8 +1,8 @@
 """GPU conservative readout (F = -dE/dr, sigma = (1/V) dE/d(eps)) against the
 fp64 oracle: energies, forces and stresses within |gpu - oracle| <= 1e-5 +
 1e-4 |oracle| on the workload shapes, d = 128, the Eq. (10) block and cells
-without bonds or edges; molecular dynamics with conservative forces; the
-training entry points refuse the readout (it would need second derivatives)."""
+without bonds or edges; molecular dynamics with conservative forces. Training through
+the readout is covered by test_gpu_conservative_train.py."""
 import numpy as np
 import pytest
 
@@ -67,23 +67,6 @@ def test_conservative_variants_and_small_cells(bd):
     _check(bd, nb, synth.make_params(64, 2, seed=(8, 1, 0)), 64, 2, "no-bonds conservative")
     ne = synth.make_custom_batch([np.eye(3) * 13.0], [np.zeros((1, 3))], [np.array([26])])
     _check(bd, ne, synth.make_params(64, 2, seed=(8, 1, 0)), 64, 2, "no-edges conservative")
-
-
-def test_conservative_training_refused(bd):
-    b, params, targets, d, T = synth.workload_inputs("cubic8")
-    hp = bd.hparams(conservative=True)
-    db = bd.DeviceBatch.from_host(b)
-    ws = bd.Workspace()
-    g = bd.DeviceGraph(b.n_atoms, 64, 16, 64)
-    bd.build_graph(hp, db, g, ws)
-    p = _dev(params)
-    E, F, S = bd.forward(hp, db, g, p, ws)
-    with pytest.raises(bd.ChgnetError) as e:
-        bd.step(hp, db, g, p, [_dev(x) for x in targets], ws)
-    assert e.value.code == bd.CHGNET_EINVAL
-    with pytest.raises(bd.ChgnetError) as e:
-        bd.backward(hp, db, g, p, E, F, S, ws)
-    assert e.value.code == bd.CHGNET_EINVAL
 
 
 def test_conservative_md(bd):

@@ -1,0 +1,181 @@
+"""GPU weight gradient through the conservative readout (F = -dE/dr, sigma =
+(1/V) dE/d(eps); the library runs the forward pass and the weight backward in
+dual numbers) against the fp64 autodiff oracle, which differentiates the loss
+through autograd's own dE/dr and dE/d(eps) (second derivatives by
+create_graph): the training step's loss and gradient (squared and Huber
+errors) and chgnet_backward with random output gradients, on the cubic8
+workload and random small batches; at the full triclinic40 size, output
+gradients on a sample of structures against the oracle on those structures
+alone (crystals of a batch are independent and the gradient is linear in
+the output gradients). The Eq. (10) block and the
+magnetic-moment head are refused with CHGNET_EINVAL.
+
+Tolerance per parameter tensor: |gpu - ref| <= 5e-5 m + 1e-3 |ref|, with m
+the larger of the tensor's max|ref| and 1e-2 of the whole gradient's (a
+tensor whose exact gradient vanishes, such as the energy bias when the
+energy errors of a batch cancel, is held to rounding of the whole sum).
+The fp32 path forms each gradient term as a product of a first derivative
+(as accurate as the direct-head gradients, about 1e-5 relative) with
+tangents that pass through the same chain once more, and sums terms of both
+signs over every edge and angle; the bound allows about twenty times the
+first-order tests' relative error against the tensor's scale."""
+import numpy as np
+import pytest
+
+from oracle import autodiff
+from oracle import graph as og
+from oracle import model as om
+from paper_2412_20796_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+ATOL_REL, RTOL = 5e-5, 1e-3
+
+
+@pytest.fixture(scope="module")
+def bd():
+    import torch
+
+    from paper_2412_20796_amd import binding
+
+    assert torch.cuda.is_available()
+    binding.lib()
+    return binding
+
+
+def _dev(x):
+    import torch
+
+    return torch.as_tensor(np.ascontiguousarray(x)).to("cuda")
+
+
+def _assert_grad(got, ref, ohp, what):
+    lay, _ = om.layout(ohp)
+    gscale = np.abs(ref).max()
+    worst = []
+    for name, (o, s) in lay.items():
+        n = int(np.prod(s))
+        g, r = got[o:o + n].astype(np.float64), ref[o:o + n]
+        scale = max(np.abs(r).max(), 1e-2 * gscale)
+        err = np.abs(g - r)
+        bad = err > ATOL_REL * scale + RTOL * np.abs(r)
+        worst.append((float(err.max() / max(scale, 1e-30)), name))
+        if bad.any():
+            k = int(np.argmax(err - ATOL_REL * scale - RTOL * np.abs(r)))
+            raise AssertionError("%s grad %s: %d/%d outside tolerance; worst at %d: gpu %.9g ref %.9g (max|ref| %.3g)"
+                                 % (what, name, int(bad.sum()), n, k, g[k], r[k], scale))
+    worst.sort(reverse=True)
+    print(what, "largest error / max|ref|:", ", ".join("%s %.2e" % (nm, e) for e, nm in worst[:3]), flush=True)
+
+
+def _setup(bd, b, d, T, **kw):
+    hp = bd.hparams(d=d, n_layers=T, conservative=True, **kw)
+    db = bd.DeviceBatch.from_host(b)
+    ws = bd.Workspace()
+    g = bd.DeviceGraph(b.n_atoms, 64, 16, 64)
+    bd.build_graph(hp, db, g, ws)
+    return hp, db, g, ws
+
+
+def _check_step(bd, b, params, targets, d, T, name, delta=None):
+    ohp = om.HParams(d=d, n_layers=T, conservative=True)
+    graph = og.build_graph(b.atom_ptr, b.pos, b.lattice)
+    rl, rg = autodiff.loss_and_grad(ohp, b, graph, params.astype(np.float64), targets, delta=delta)
+    hp, db, g, ws = _setup(bd, b, d, T)
+    loss, grad = bd.step(hp, db, g, _dev(params), [_dev(x) for x in targets], ws, huber_delta=delta or 0.0)
+    lv = float(loss.cpu().numpy()[0])
+    assert abs(lv - rl) <= 1e-5 + 1e-4 * abs(rl), (name, lv, rl)
+    _assert_grad(grad.cpu().numpy(), rg, ohp, name)
+
+
+def test_step_cubic8(bd):
+    b, params, targets, d, T = synth.workload_inputs("cubic8")
+    _check_step(bd, b, params, targets, d, T, "cubic8 conservative step")
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_step_random_batches(bd, seed):
+    b = synth.random_crystals(seed=500 + seed, n_struct=1 + seed, n_lo=2, n_hi=12, rho=(0.06, 0.12))
+    params = synth.make_params(64, 3, seed=(12, 1, seed))
+    targets = synth.make_targets(b, seed=(12, 2, seed))
+    _check_step(bd, b, params, targets, 64, 3, "random%d conservative step" % seed, delta=0.1 if seed == 1 else None)
+
+
+def test_step_d128_single_layer(bd):
+    b = synth.random_crystals(seed=11, n_struct=2, n_lo=4, n_hi=10)
+    _check_step(bd, b, synth.make_params(128, 2, seed=(7, 1, 1)), synth.make_targets(b, seed=(7, 2, 1)), 128, 2,
+                "d128 conservative step")
+    _check_step(bd, b, synth.make_params(64, 1, seed=(7, 1, 3)), synth.make_targets(b, seed=(7, 2, 3)), 64, 1,
+                "T1 conservative step")
+
+
+def test_backward_random_output_gradients(bd):
+    """chgnet_backward after chgnet_forward: the gradient of sum(dE E) +
+    sum(dF F) + sum(dS sigma) for random dE, dF, dS."""
+    import torch
+
+    b, params, _, d, T = synth.workload_inputs("cubic8")
+    rng = np.random.default_rng(5)
+    dE = rng.standard_normal(b.n_struct)
+    dF = rng.standard_normal((b.n_atoms, 3))
+    dS = rng.standard_normal((b.n_struct, 3, 3))
+    ohp = om.HParams(d=d, n_layers=T, conservative=True)
+    graph = og.build_graph(b.atom_ptr, b.pos, b.lattice)
+    p64 = torch.tensor(params.astype(np.float64), requires_grad=True)
+    E, F, S, _, _ = autodiff.outputs(ohp, b, graph, p64, create_graph=True)
+    tot = (E * torch.tensor(dE)).sum() + (F * torch.tensor(dF)).sum() + (S * torch.tensor(dS)).sum()
+    (rg,) = torch.autograd.grad(tot, p64)
+    hp, db, g, ws = _setup(bd, b, d, T)
+    p = _dev(params)
+    bd.forward(hp, db, g, p, ws)
+    f32 = lambda x: _dev(x.astype(np.float32))
+    grad = bd.backward(hp, db, g, p, f32(dE), f32(dF), f32(dS), ws)
+    _assert_grad(grad.cpu().numpy(), rg.numpy(), ohp, "cubic8 conservative backward")
+
+
+def test_triclinic40_sampled_structures(bd):
+    import torch
+
+    from gpu_helpers import subset_batch
+
+    b, params, _, d, T = synth.workload_inputs("triclinic40")
+    sample = [3, 22]
+    rng = np.random.default_rng(9)
+    dE = np.zeros(b.n_struct)
+    dF = np.zeros((b.n_atoms, 3))
+    dS = np.zeros((b.n_struct, 3, 3))
+    sb = subset_batch(b, sample)
+    sE = rng.standard_normal(len(sample))
+    sF = rng.standard_normal((sb.n_atoms, 3))
+    sS = rng.standard_normal((len(sample), 3, 3))
+    o = 0
+    for k, s in enumerate(sample):
+        a0, a1 = b.atom_ptr[s], b.atom_ptr[s + 1]
+        dE[s], dS[s] = sE[k], sS[k]
+        dF[a0:a1] = sF[o:o + a1 - a0]
+        o += a1 - a0
+    ohp = om.HParams(d=d, n_layers=T, conservative=True)
+    graph = og.build_graph(sb.atom_ptr, sb.pos, sb.lattice)
+    p64 = torch.tensor(params.astype(np.float64), requires_grad=True)
+    E, F, S, _, _ = autodiff.outputs(ohp, sb, graph, p64, create_graph=True)
+    tot = (E * torch.tensor(sE)).sum() + (F * torch.tensor(sF)).sum() + (S * torch.tensor(sS)).sum()
+    (rg,) = torch.autograd.grad(tot, p64)
+    hp, db, g, ws = _setup(bd, b, d, T)
+    p = _dev(params)
+    bd.forward(hp, db, g, p, ws)
+    f32 = lambda x: _dev(x.astype(np.float32))
+    grad = bd.backward(hp, db, g, p, f32(dE), f32(dF), f32(dS), ws)
+    _assert_grad(grad.cpu().numpy(), rg.numpy(), ohp, "triclinic40 sampled conservative backward")
+
+
+def test_unsupported_variants_refused(bd):
+    b, params, targets, d, T = synth.workload_inputs("cubic8")
+    for kw in ({"sequential": True}, {"magmom": True}):
+        hp, db, g, ws = _setup(bd, b, d, T, **kw)
+        tg = [_dev(x) for x in targets]
+        if kw.get("magmom"):
+            tg.append(_dev(np.zeros(b.n_atoms, dtype=np.float32)))
+        p = _dev(synth.make_params(d, T, seed=(7, 1, 0), magmom=bool(kw.get("magmom"))))
+        with pytest.raises(bd.ChgnetError) as e:
+            bd.step(hp, db, g, p, tg, ws)
+        assert e.value.code == bd.CHGNET_EINVAL
