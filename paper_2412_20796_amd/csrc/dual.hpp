@@ -151,50 +151,115 @@ __global__ void __launch_bounds__(256) kd_angles(int A, int K, const int* __rest
 }
 
 // ---------------------------------------------------------------------------
-// Gathers and scatters of the gated-MLP inputs [v_i | e_ij | ...] (both parts).
+// Gathered blocks of the gated-MLP inputs [v_i | v_j | e_ij] and [v_i | e_ij |
+// e_ik | a_ijk]. The first linear layer of a gate is split by input block:
+// atom and bond blocks are multiplied once per atom or bond (projections,
+// rows of 8d: four blocks of 2d) and their rows are gathered into the
+// pre-activation by the gate kernel; in the backward pass the
+// pre-activation gradients are first summed per atom (S) and per bond (T),
+// in the graph's CSR orders, and multiplied there.
 // ---------------------------------------------------------------------------
-struct DnSeg {
-  float *v, *t;                // rows of D columns
-  const int *idx, *idx2;       // row = idx2[idx[r]] (each optional)
-  int col;                     // scatter: first column of the segment in the input rows
-};
-struct DnRowsJob {
-  int64_t rows;
-  int nseg;
-  DnSeg s[4];
-  float *xv, *xt;  // [rows, nseg * D]
-};
-
-__device__ __forceinline__ int64_t dn_row(const DnSeg& s, int64_t r) {
-  int64_t row = s.idx ? s.idx[r] : r;
-  if (s.idx2) row = s.idx2[row];
-  return row;
+// A block per atom i and block q of S (both parts): S[i] = [sum over the
+// out-edges e of dz_av[e] | of dz_av[rev e] (the edges that end at i) | sum
+// over the angles centred on i of dz_be | of dz_an]; the four wavefronts
+// take every fourth row and their sums are added in a fixed order.
+constexpr int kDzMaxCols = 4;  // 2d / 64 columns a lane
+__global__ void __launch_bounds__(256) kd_dz_atoms(int N, int D, int nblk, const int* __restrict__ ep,
+                                                   const int* __restrict__ rev, const int* __restrict__ bp,
+                                                   const int* __restrict__ ap, const float* __restrict__ zav,
+                                                   const float* __restrict__ zat, const float* __restrict__ zbv,
+                                                   const float* __restrict__ zbt, const float* __restrict__ znv,
+                                                   const float* __restrict__ znt, float* __restrict__ sv,
+                                                   float* __restrict__ st) {
+  __shared__ float red[4][2][kDzMaxCols * 64];
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int64_t i = blockIdx.x / nblk;
+  const int q = blockIdx.x % nblk;
+  const int W2 = 2 * D, nc = W2 / 64;
+  int64_t r0, r1;
+  const float *xv, *xt;
+  if (q < 2) {
+    r0 = ep[i];
+    r1 = ep[i + 1];
+    xv = zav;
+    xt = zat;
+  } else {
+    r0 = ap[bp[i]];
+    r1 = ap[bp[i + 1]];
+    xv = q == 2 ? zbv : znv;
+    xt = q == 2 ? zbt : znt;
+  }
+  float av[kDzMaxCols] = {}, at[kDzMaxCols] = {};
+  for (int64_t r = r0 + wv; r < r1; r += 4) {
+    const int64_t o = (q == 1 ? (int64_t)rev[r] : r) * W2 + lane;
+#pragma unroll
+    for (int k = 0; k < kDzMaxCols; ++k)
+      if (k < nc) {
+        av[k] += xv[o + 64 * k];
+        at[k] += xt[o + 64 * k];
+      }
+  }
+#pragma unroll
+  for (int k = 0; k < kDzMaxCols; ++k)
+    if (k < nc) {
+      red[wv][0][lane + 64 * k] = av[k];
+      red[wv][1][lane + 64 * k] = at[k];
+    }
+  __syncthreads();
+  for (int c = threadIdx.x; c < 2 * W2; c += 256) {
+    const int pl = c / W2, cc = c % W2;
+    const float v = ((red[0][pl][cc] + red[1][pl][cc]) + red[2][pl][cc]) + red[3][pl][cc];
+    (pl ? st : sv)[i * 4 * W2 + q * W2 + cc] = v;
+  }
 }
 
-// x[r, k D + c] = segment k's row (gathered) column c
-__global__ void __launch_bounds__(256) kd_gather(DnRowsJob J, int D) {
-  const int64_t w = (int64_t)J.nseg * D;
-  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (i >= J.rows * w) return;
-  const int64_t r = i / w;
-  const int k = (int)((i % w) / D), c = (int)(i % D);
-  const DnSeg& s = J.s[k];
-  const int64_t o = dn_row(s, r) * D + c;
-  J.xv[i] = s.v[o];
-  J.xt[i] = s.t[o];
+// a wavefront per bond b (both parts): T[b] = [sum over the angles whose
+// first bond is b of dz_be | 0 | of dz_an | 0]; the zero blocks take the
+// second-bond roles (kd_dz_b2)
+__global__ void __launch_bounds__(256) kd_dz_bonds(int B, int D, int ang, const int* __restrict__ ap,
+                                                   const float* __restrict__ zbv, const float* __restrict__ zbt,
+                                                   const float* __restrict__ znv, const float* __restrict__ znt,
+                                                   float* __restrict__ tv, float* __restrict__ tt) {
+  const int lane = threadIdx.x & 63;
+  const int64_t w = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (w >= B) return;
+  const int W2 = 2 * D;
+  for (int c = lane; c < W2; c += 64) {
+    float bv = 0.f, bt = 0.f, nv = 0.f, nt = 0.f;
+    for (int64_t a = ap[w]; a < ap[w + 1]; ++a) {
+      const int64_t o = a * W2 + c;
+      bv += zbv[o];
+      bt += zbt[o];
+      if (ang) {
+        nv += znv[o];
+        nt += znt[o];
+      }
+    }
+    const int64_t o = w * 4 * W2 + c;
+    tv[o] = bv;
+    tt[o] = bt;
+    tv[o + W2] = tt[o + W2] = 0.f;
+    tv[o + 2 * W2] = nv;
+    tt[o + 2 * W2] = nt;
+    tv[o + 3 * W2] = tt[o + 3 * W2] = 0.f;
+  }
 }
 
-// segment k's row (scattered) column c += x[r, k D + c]
-__global__ void __launch_bounds__(256) kd_scatter(DnRowsJob J, int D) {
-  const int64_t w = (int64_t)J.nseg * D;
+// per angle and column: T[b2] second-bond blocks += dz_be (and dz_an) rows
+__global__ void __launch_bounds__(256) kd_dz_b2(int64_t n, int D, int ang, const int* __restrict__ b2,
+                                                const float* __restrict__ zbv, const float* __restrict__ zbt,
+                                                const float* __restrict__ znv, const float* __restrict__ znt,
+                                                float* __restrict__ tv, float* __restrict__ tt) {
   const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (i >= J.rows * w) return;
-  const int64_t r = i / w;
-  const int k = (int)((i % w) / D), c = (int)(i % D);
-  const DnSeg& s = J.s[k];
-  const int64_t o = dn_row(s, r) * D + c;
-  atomicAdd(s.v + o, J.xv[i]);
-  atomicAdd(s.t + o, J.xt[i]);
+  if (i >= n) return;
+  const int W2 = 2 * D;
+  const int64_t o = (int64_t)b2[i / W2] * 4 * W2 + W2 + i % W2;
+  atomicAdd(tv + o, zbv[i]);
+  atomicAdd(tt + o, zbt[i]);
+  if (ang) {
+    atomicAdd(tv + o + 2 * W2, znv[i]);
+    atomicAdd(tt + o + 2 * W2, znt[i]);
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -205,7 +270,13 @@ constexpr int kDnMaxV = 2;  // d <= 128
 
 struct DnGate {
   int64_t rows;
-  const float *zv, *zt;  // [rows, 2d] pre-activations
+  // [rows, 2d] pre-activations; the forward adds the rows idx[k][r] of the
+  // projections add[k] (rows of 8d) to the edge or angle block's product and
+  // stores the sum
+  float *zv, *zt;
+  int nadd;
+  const float *addv[3], *addt[3];
+  const int* idx[3];
   const float *gc, *bc, *gg, *bg;
   // forward: phi -> (pv, pt), or with res_t: pt = res_t + phi tangent (a + phi)
   float *pv, *pt;
@@ -264,7 +335,32 @@ __global__ void __launch_bounds__(256) kd_gate_fwd(DnGates J, int D) {
   const int64_t r = w - J.start[k];
   const int V = D / 64;
   Dn zc[kDnMaxV], zg[kDnMaxV], xc[kDnMaxV], xg[kDnMaxV], rc, rg;
+  int64_t ro[3];
+#pragma unroll
+  for (int k = 0; k < 3; ++k) ro[k] = k < q.nadd ? (int64_t)q.idx[k][r] * 8 * D : 0;
   dn_load_z(q, r, D, lane, zc, zg);
+#pragma unroll
+  for (int k = 0; k < 3; ++k) {
+    if (k >= q.nadd) break;
+#pragma unroll
+    for (int i = 0; i < kDnMaxV; ++i) {
+      if (i >= V) break;
+      const int64_t c = ro[k] + lane + 64 * i;
+      zc[i] = zc[i] + Dn{q.addv[k][c], q.addt[k][c]};
+      zg[i] = zg[i] + Dn{q.addv[k][c + D], q.addt[k][c + D]};
+    }
+  }
+  if (q.nadd > 0) {
+#pragma unroll
+    for (int i = 0; i < kDnMaxV; ++i) {
+      if (i >= V) break;
+      const int64_t o = r * 2 * D + lane + 64 * i;
+      q.zv[o] = zc[i].v;
+      q.zt[o] = zc[i].t;
+      q.zv[o + D] = zg[i].v;
+      q.zt[o + D] = zg[i].t;
+    }
+  }
   dn_ln(zc, V, D, xc, rc);
   dn_ln(zg, V, D, xg, rg);
 #pragma unroll
@@ -518,14 +614,17 @@ struct DualBufs {
   // forward tangents
   float *rdot, *ddot, *rbfa_t, *rbfb_t, *ft_t, *ea_t, *eb_t;
   float *v_t[kMaxLayers + 1], *e_t[kMaxLayers + 1], *a_t[kMaxLayers + 1];
-  // per layer, [0] value and [1] tangent: gathered inputs, pre-activations,
-  // gate outputs and messages
-  float *xv[kMaxLayers][2], *xb[kMaxLayers][2], *zav[kMaxLayers][2], *zbe[kMaxLayers][2], *zan[kMaxLayers][2];
+  // per layer, [0] value and [1] tangent: pre-activations, gate outputs and
+  // messages
+  float *zav[kMaxLayers][2], *zbe[kMaxLayers][2], *zan[kMaxLayers][2];
   float *pav[kMaxLayers][2], *pbe[kMaxLayers][2], *m[kMaxLayers][2], *ss[kMaxLayers][2], *mu[kMaxLayers][2];
   float *h1_t, *a1_t, *h2_t, *a2_t;
   // backward, [0] value and [1] tangent
   float *dov[2], *dh2[2], *dh1[2], *dv[2], *de[2], *da[2], *dea[2], *deb[2], *dm[2], *dmu[2], *dss[2];
-  float *dpav[2], *dpbe[2], *dzav[2], *dzbe[2], *dzan[2], *dxv[2], *dxb[2], *drbfa[2], *drbfb[2];
+  float *dpav[2], *dpbe[2], *dzav[2], *dzbe[2], *dzan[2], *drbfa[2], *drbfb[2];
+  // projections of the atom and bond blocks (forward) and the per-atom and
+  // per-bond sums of the pre-activation gradients (backward), rows of 8d
+  float *PA[2], *PB[2], *S[2], *T[2];
   float *lnav, *lnbe, *lnan, *fpa, *fpb, *gB;
 };
 
@@ -546,8 +645,6 @@ void carve_dual(Arena& ar, const Dims& m, int64_t n_params, DualBufs& d) {
   }
   for (int t = 0; t < m.T; ++t)
     for (int k = 0; k < 2; ++k) {
-      d.xv[t][k] = f(E * 3 * D);
-      d.xb[t][k] = f(A * 4 * D);
       d.zav[t][k] = f(E * 2 * D);
       d.zbe[t][k] = f(A * 2 * D);
       d.zan[t][k] = f(A * 2 * D);
@@ -578,8 +675,10 @@ void carve_dual(Arena& ar, const Dims& m, int64_t n_params, DualBufs& d) {
     d.dzav[k] = f(E * 2 * D);
     d.dzbe[k] = f(A * 2 * D);
     d.dzan[k] = f(A * 2 * D);
-    d.dxv[k] = f(E * 3 * D);
-    d.dxb[k] = f(A * 4 * D);
+    d.PA[k] = f(N * 8 * D);
+    d.PB[k] = f(B * 8 * D);
+    d.S[k] = f(N * 8 * D);
+    d.T[k] = f(B * 8 * D);
     d.drbfa[k] = f(E * R);
     d.drbfb[k] = f(B * R);
   }
@@ -669,61 +768,47 @@ int cons_grad_impl(Ctx& c, const float* dE, const float* dF, const float* dS, fl
     else KLAUNCH(st, "kd_gate", kd_gate_bwd<<<(unsigned)cdiv(J.start[J.n], 4), 256, 0, st>>>(J, D));
     return CHGNET_OK;
   };
-  auto rows_job = [&](DnRowsJob J, bool gather) -> int {
-    if (J.rows <= 0) return CHGNET_OK;
-    const int64_t n = J.rows * J.nseg * D;
-    if (gather) KLAUNCH(st, "kd_rows", kd_gather<<<dn_blocks(n), 256, 0, st>>>(J, D));
-    else KLAUNCH(st, "kd_rows", kd_scatter<<<dn_blocks(n), 256, 0, st>>>(J, D));
-    return CHGNET_OK;
-  };
-  // the gated-MLP inputs: atom conv [v_i | v_j | e_ij] per edge; bond conv
-  // and angle update [v_i | e_ij | e_ik | a_ijk] per angle
-  auto xv_job = [&](float* v0, float* t0, float* e0, float* et0, float* ov, float* ot) {
-    DnRowsJob J{};
-    J.rows = E;
-    J.nseg = 3;
-    J.s[0] = DnSeg{v0, t0, a.edge_src, nullptr, 0};
-    J.s[1] = DnSeg{v0, t0, g.edge_dst, nullptr, D};
-    J.s[2] = DnSeg{e0, et0, nullptr, nullptr, 2 * D};
-    J.xv = ov;
-    J.xt = ot;
-    return J;
-  };
-  auto xb_job = [&](float* v0, float* t0, float* e0, float* et0, float* a0, float* at0, float* ov, float* ot) {
-    DnRowsJob J{};
-    J.rows = A;
-    J.nseg = 4;
-    J.s[0] = DnSeg{v0, t0, a.ang_ctr, nullptr, 0};
-    J.s[1] = DnSeg{e0, et0, a.ang_b1, g.bond_edge, D};
-    J.s[2] = DnSeg{e0, et0, a.ang_b2, g.bond_edge, 2 * D};
-    J.s[3] = DnSeg{a0, at0, nullptr, nullptr, 3 * D};
-    J.xv = ov;
-    J.xt = ot;
-    return J;
-  };
+  const int64_t WB = (int64_t)D * 2 * D;  // one d-row input block of a gate's first layer
   for (int t = 0; t < m.T; ++t) {
     const LayerOffsets& lo = L.layer[t];
     const bool ang = lo.has_angle;
-    CHG_TRY(rows_job(xv_job(a.v[t], d.v_t[t], a.e[t], d.e_t[t], d.xv[t][0], d.xv[t][1]), true));
-    CHG_TRY(rows_job(xb_job(a.v[t], d.v_t[t], a.e[t], d.e_t[t], a.a[t], d.a_t[t], d.xb[t][0], d.xb[t][1]), true));
+    const float *Wav = P + lo.av.W, *Wbe = P + lo.be.W, *Wan = P + lo.an.W;
+    // projections of the atom blocks (v W_av0 | v W_av1 | v W_be0 | v W_an0)
+    // and bond blocks (e_b W_be1 | e_b W_be2 | e_b W_an1 | e_b W_an2); the
+    // edge and angle blocks with the bias into z
     {
       std::vector<GemmProblem> ps;
+      const float* Wa[4] = {Wav, Wav + WB, Wbe, Wan};
+      for (int k = 0; k < (ang ? 4 : 3); ++k) {
+        GemmProblem p = gp(N, 2 * D, d.PA[0] + k * 2 * D, 8 * D);
+        seg(p, a.v[t], D, 0, D, Wa[k], 2 * D, 0);
+        ps.push_back(p);
+        ps.push_back(tangent_of(p, {d.v_t[t]}, d.PA[1] + k * 2 * D, nullptr));
+      }
+      const float* Wb[4] = {Wbe + WB, Wbe + 2 * WB, Wan + WB, Wan + 2 * WB};
+      for (int k = 0; k < (ang ? 4 : 2); ++k) {
+        GemmProblem p = gp(B, 2 * D, d.PB[0] + k * 2 * D, 8 * D);
+        p.a_rows = g.bond_edge;
+        seg(p, a.e[t], D, 0, D, Wb[k], 2 * D, 0);
+        ps.push_back(p);
+        ps.push_back(tangent_of(p, {d.e_t[t]}, d.PB[1] + k * 2 * D, nullptr));
+      }
       GemmProblem p = gp(E, 2 * D, d.zav[t][0], 2 * D);
-      seg(p, d.xv[t][0], 3 * D, 0, 3 * D, P + lo.av.W, 2 * D, 0);
+      seg(p, a.e[t], D, 0, D, Wav + 2 * WB, 2 * D, 0);
       p.bias = P + lo.av.b;
       ps.push_back(p);
-      ps.push_back(tangent_of(p, {d.xv[t][1]}, d.zav[t][1], nullptr));
+      ps.push_back(tangent_of(p, {d.e_t[t]}, d.zav[t][1], nullptr));
       p = gp(A, 2 * D, d.zbe[t][0], 2 * D);
-      seg(p, d.xb[t][0], 4 * D, 0, 4 * D, P + lo.be.W, 2 * D, 0);
+      seg(p, a.a[t], D, 0, D, Wbe + 3 * WB, 2 * D, 0);
       p.bias = P + lo.be.b;
       ps.push_back(p);
-      ps.push_back(tangent_of(p, {d.xb[t][1]}, d.zbe[t][1], nullptr));
+      ps.push_back(tangent_of(p, {d.a_t[t]}, d.zbe[t][1], nullptr));
       if (ang) {
         p = gp(A, 2 * D, d.zan[t][0], 2 * D);
-        seg(p, d.xb[t][0], 4 * D, 0, 4 * D, P + lo.an.W, 2 * D, 0);
+        seg(p, a.a[t], D, 0, D, Wan + 3 * WB, 2 * D, 0);
         p.bias = P + lo.an.b;
         ps.push_back(p);
-        ps.push_back(tangent_of(p, {d.xb[t][1]}, d.zan[t][1], nullptr));
+        ps.push_back(tangent_of(p, {d.a_t[t]}, d.zan[t][1], nullptr));
       }
       CHG_TRY(run_gemms(ps, st, "kd_gemm"));
     }
@@ -740,6 +825,18 @@ int cons_grad_impl(Ctx& c, const float* dE, const float* dF, const float* dS, fl
         q.bc = P + go[k]->b_c;
         q.gg = P + go[k]->g_g;
         q.bg = P + go[k]->b_g;
+        // gathered projections: atom conv v_i, v_j; bond conv and angle
+        // update the centre atom, first and second bond
+        const int pa = k == 0 ? 0 : k == 1 ? 4 * D : 6 * D, pb = k == 1 ? 0 : 4 * D;
+        const int* ix[3] = {k == 0 ? a.edge_src : a.ang_ctr, k == 0 ? g.edge_dst : a.ang_b1, a.ang_b2};
+        q.nadd = k == 0 ? 2 : 3;
+        for (int u = 0; u < q.nadd; ++u) {
+          const bool atom = u == 0 || k == 0;
+          const int col = k == 0 ? 2 * D * u : atom ? pa : pb + 2 * D * (u - 1);
+          q.addv[u] = (atom ? d.PA[0] : d.PB[0]) + col;
+          q.addt[u] = (atom ? d.PA[1] : d.PB[1]) + col;
+          q.idx[u] = ix[u];
+        }
         if (k == 0) {
           q.pv = d.pav[t][0];
           q.pt = d.pav[t][1];
@@ -803,11 +900,15 @@ int cons_grad_impl(Ctx& c, const float* dE, const float* dF, const float* dS, fl
 
   // backward in dual numbers; weight terms: X_t^T Y_v into G, X_v^T Y_t into gB
   std::vector<TnProblem> ts;
+  auto crossc = [&](int64_t Rr, int M, int Nn, const float* xv, const float* xt, int ldx, const int* xr,
+                    const float* const* y, int ldy, int ycol, const int* yr, int64_t off, int ld_out) {
+    if (Rr <= 0) return;
+    ts.push_back(tp(Rr, M, Nn, xt, ldx, 0, xr, y[0], ldy, ycol, yr, G + off, ld_out));
+    ts.push_back(tp(Rr, M, Nn, xv, ldx, 0, xr, y[1], ldy, ycol, yr, gB + off, ld_out));
+  };
   auto cross = [&](int64_t Rr, int M, int Nn, const float* xv, const float* xt, int ldx, const int* xr, const float* const* y,
                    int ldy, const int* yr, int64_t off, int ld_out) {
-    if (Rr <= 0) return;
-    ts.push_back(tp(Rr, M, Nn, xt, ldx, 0, xr, y[0], ldy, 0, yr, G + off, ld_out));
-    ts.push_back(tp(Rr, M, Nn, xv, ldx, 0, xr, y[1], ldy, 0, yr, gB + off, ld_out));
+    crossc(Rr, M, Nn, xv, xt, ldx, xr, y, ldy, 0, yr, off, ld_out);
   };
   auto colsum = [&](int64_t Rr, int Nn, const float* yt, int ldy, const int* yr, int64_t off) {
     if (Rr <= 0) return;
@@ -900,55 +1001,85 @@ int cons_grad_impl(Ctx& c, const float* dE, const float* dF, const float* dS, fl
       }
       CHG_TRY(gates(J, false));
     }
-    // gated-MLP input gradients and weight terms
+    // pre-activation gradients summed per atom (S) and per bond (T)
+    if (N > 0)
+      KLAUNCH(st, "kd_dz_sum", kd_dz_atoms<<<(unsigned)(N * (ang ? 4 : 3)), 256, 0, st>>>((int)N, D, ang ? 4 : 3, g.edge_ptr, g.edge_rev,
+                                                                                g.bond_ptr, g.angle_ptr, d.dzav[0], d.dzav[1],
+                                                                                d.dzbe[0], d.dzbe[1], d.dzan[0], d.dzan[1],
+                                                                                d.S[0], d.S[1]));
+    if (B > 0) {
+      KLAUNCH(st, "kd_dz_sum", kd_dz_bonds<<<(unsigned)cdiv(B, 4), 256, 0, st>>>((int)B, D, ang, g.angle_ptr, d.dzbe[0],
+                                                                                d.dzbe[1], d.dzan[0], d.dzan[1], d.T[0],
+                                                                                d.T[1]));
+      if (A > 0)
+        KLAUNCH(st, "kd_dz_sum", kd_dz_b2<<<dn_blocks(A * 2 * D), 256, 0, st>>>(A * 2 * D, D, ang, a.ang_b2, d.dzbe[0],
+                                                                                d.dzbe[1], d.dzan[0], d.dzan[1], d.T[0],
+                                                                                d.T[1]));
+    }
+    // input gradients of v^t, e^t and a^t (accumulated): atoms from S, edges
+    // from dz_av, angles from dz_be, dz_an; then the bond rows of e from T
     {
+      const float *Wav = P + lo.av.W, *Wbe = P + lo.be.W, *Wan = P + lo.an.W;
       std::vector<GemmProblem> ps;
-      GemmProblem p = gp(E, 3 * D, d.dxv[0], 3 * D);
-      seg(p, d.dzav[0], 2 * D, 0, 2 * D, P + lo.av.W, 2 * D, 1);
+      GemmProblem p = gp(N, D, d.dv[0], D);
+      p.accumulate = 1;
+      seg(p, d.S[0], 8 * D, 0, 2 * D, Wav, 2 * D, 1);
+      seg(p, d.S[0], 8 * D, 2 * D, 2 * D, Wav + WB, 2 * D, 1);
+      seg(p, d.S[0], 8 * D, 4 * D, 2 * D, Wbe, 2 * D, 1);
+      if (ang) seg(p, d.S[0], 8 * D, 6 * D, 2 * D, Wan, 2 * D, 1);
       ps.push_back(p);
-      ps.push_back(tangent_of(p, {d.dzav[1]}, d.dxv[1], nullptr));
-      p = gp(A, 4 * D, d.dxb[0], 4 * D);
-      seg(p, d.dzbe[0], 2 * D, 0, 2 * D, P + lo.be.W, 2 * D, 1);
-      if (ang) seg(p, d.dzan[0], 2 * D, 0, 2 * D, P + lo.an.W, 2 * D, 1);
+      ps.push_back(tangent_of(p, {d.S[1], d.S[1], d.S[1], d.S[1]}, d.dv[1], nullptr));
+      p = gp(E, D, d.de[0], D);
+      p.accumulate = 1;
+      seg(p, d.dzav[0], 2 * D, 0, 2 * D, Wav + 2 * WB, 2 * D, 1);
       ps.push_back(p);
-      if (ang) ps.push_back(tangent_of(p, {d.dzbe[1], d.dzan[1]}, d.dxb[1], nullptr));
-      else ps.push_back(tangent_of(p, {d.dzbe[1]}, d.dxb[1], nullptr));
+      ps.push_back(tangent_of(p, {d.dzav[1]}, d.de[1], nullptr));
+      p = gp(A, D, d.da[0], D);
+      p.accumulate = 1;
+      seg(p, d.dzbe[0], 2 * D, 0, 2 * D, Wbe + 3 * WB, 2 * D, 1);
+      if (ang) seg(p, d.dzan[0], 2 * D, 0, 2 * D, Wan + 3 * WB, 2 * D, 1);
+      ps.push_back(p);
+      ps.push_back(tangent_of(p, {d.dzbe[1], d.dzan[1]}, d.da[1], nullptr));
+      CHG_TRY(run_gemms(ps, st, "kd_gemm"));
+      ps.clear();
+      p = gp(B, D, d.de[0], D);
+      p.accumulate = 1;
+      p.c_rows = g.bond_edge;
+      seg(p, d.T[0], 8 * D, 0, 2 * D, Wbe + WB, 2 * D, 1);
+      seg(p, d.T[0], 8 * D, 2 * D, 2 * D, Wbe + 2 * WB, 2 * D, 1);
+      if (ang) {
+        seg(p, d.T[0], 8 * D, 4 * D, 2 * D, Wan + WB, 2 * D, 1);
+        seg(p, d.T[0], 8 * D, 6 * D, 2 * D, Wan + 2 * WB, 2 * D, 1);
+      }
+      ps.push_back(p);
+      ps.push_back(tangent_of(p, {d.T[1], d.T[1], d.T[1], d.T[1]}, d.de[1], nullptr));
       CHG_TRY(run_gemms(ps, st, "kd_gemm"));
     }
-    auto gate_terms = [&](int64_t rows, const float* const* x, int ldx, const float* const* dz, const float* lnp,
-                          const GatedOffsets& og) {
-      cross(rows, ldx, 2 * D, x[0], x[1], ldx, nullptr, dz, 2 * D, nullptr, og.W, 2 * D);
+    // weight terms of the gates, block by block: atom blocks over atoms
+    // against S, bond blocks over bonds against T, edge and angle blocks over
+    // their rows against dz
+    auto gate_terms = [&](int gi, const float* const* dz, const float* lnp, const GatedOffsets& og) {
+      const int64_t rows = gi == 0 ? E : A;
+      if (gi == 0) {
+        crossc(N, D, 2 * D, a.v[t], d.v_t[t], D, nullptr, d.S, 8 * D, 0, nullptr, og.W, 2 * D);
+        crossc(N, D, 2 * D, a.v[t], d.v_t[t], D, nullptr, d.S, 8 * D, 2 * D, nullptr, og.W + WB, 2 * D);
+        crossc(E, D, 2 * D, a.e[t], d.e_t[t], D, nullptr, dz, 2 * D, 0, nullptr, og.W + 2 * WB, 2 * D);
+      } else {
+        const int sc = gi == 1 ? 4 * D : 6 * D, tc = gi == 1 ? 0 : 4 * D;
+        crossc(N, D, 2 * D, a.v[t], d.v_t[t], D, nullptr, d.S, 8 * D, sc, nullptr, og.W, 2 * D);
+        crossc(B, D, 2 * D, a.e[t], d.e_t[t], D, g.bond_edge, d.T, 8 * D, tc, nullptr, og.W + WB, 2 * D);
+        crossc(B, D, 2 * D, a.e[t], d.e_t[t], D, g.bond_edge, d.T, 8 * D, tc + 2 * D, nullptr, og.W + 2 * WB, 2 * D);
+        crossc(A, D, 2 * D, a.a[t], d.a_t[t], D, nullptr, dz, 2 * D, 0, nullptr, og.W + 3 * WB, 2 * D);
+      }
       colsum(rows, 2 * D, dz[1], 2 * D, nullptr, og.b);
       if (rows > 0)
         ts.push_back(split_out(tp(rows, 1, 4 * D, nullptr, 0, 0, nullptr, lnp, 4 * D, 0, nullptr, gB + og.g_c, D), D,
                                gB + og.b_c, gB + og.g_g, gB + og.b_g));
     };
-    gate_terms(E, d.xv[t], 3 * D, d.dzav, d.lnav, lg.av);
-    gate_terms(A, d.xb[t], 4 * D, d.dzbe, d.lnbe, lg.be);
-    if (ang) gate_terms(A, d.xb[t], 4 * D, d.dzan, d.lnan, lg.an);
+    gate_terms(0, d.dzav, d.lnav, lg.av);
+    gate_terms(1, d.dzbe, d.lnbe, lg.be);
+    if (ang) gate_terms(2, d.dzan, d.lnan, lg.an);
     CHG_TRY(flush());
-    // scatter the input gradients to v^t, e^t and a^t
-    {
-      DnRowsJob J{};
-      J.rows = E;
-      J.nseg = 3;
-      J.s[0] = DnSeg{d.dv[0], d.dv[1], a.edge_src, nullptr, 0};
-      J.s[1] = DnSeg{d.dv[0], d.dv[1], g.edge_dst, nullptr, D};
-      J.s[2] = DnSeg{d.de[0], d.de[1], nullptr, nullptr, 2 * D};
-      J.xv = d.dxv[0];
-      J.xt = d.dxv[1];
-      CHG_TRY(rows_job(J, false));
-      J = DnRowsJob{};
-      J.rows = A;
-      J.nseg = 4;
-      J.s[0] = DnSeg{d.dv[0], d.dv[1], a.ang_ctr, nullptr, 0};
-      J.s[1] = DnSeg{d.de[0], d.de[1], a.ang_b1, g.bond_edge, D};
-      J.s[2] = DnSeg{d.de[0], d.de[1], a.ang_b2, g.bond_edge, 2 * D};
-      J.s[3] = DnSeg{d.da[0], d.da[1], nullptr, nullptr, 3 * D};
-      J.xv = d.dxb[0];
-      J.xt = d.dxb[1];
-      CHG_TRY(rows_job(J, false));
-    }
   }
 
   // embedding (Eq. 2) and sRBF frequencies
