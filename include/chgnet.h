@@ -67,10 +67,15 @@ typedef struct {
                          F_i = -dE/dr_i, sigma = (1/V) dE/d(eps) for the
                          strain r -> (I + eps) r of positions and lattice
                          (the reference output layer, Sec. II-B (4)); the
-                         force and stress head weights are then unused.
-                         Forward and MD only: training through it needs
-                         second derivatives, which this library does not
-                         compute (chgnet_backward/chgnet_step: EINVAL).    */
+                         force and stress head weights are then unused
+                         (zero gradient). Training through it (chgnet_step,
+                         chgnet_backward) takes second derivatives, as the
+                         tangent of the weight gradient along the
+                         displacement -dL/dF and the strain rate
+                         (dL/dsigma)/V (forward-over-reverse in dual
+                         numbers); with sequential = 1 both return EINVAL.
+                         The workspace then holds the dual-number buffers
+                         as well (chgnet_workspace_size includes them).     */
 } chgnet_hparams;
 
 /* Loss of chgnet_step (Sec. IV, "Parameters Setting"), host memory. Each term
@@ -170,7 +175,9 @@ int chgnet_forward(const chgnet_hparams* hp, const chgnet_batch* batch, const ch
  * the head; dM [N] may be NULL, meaning zero; it must be NULL without the
  * head), using the activations of the preceding chgnet_forward on the same ws,
  * batch, graph and params. Positions and lattices are not differentiated.
- * d|x|/dx is taken as 0 at x = 0. */
+ * d|x|/dx is taken as 0 at x = 0. With hp->conservative the forces and
+ * stresses are the derivatives of the energy, and their terms differentiate
+ * those derivatives (second derivatives; the Eq. (10) block: EINVAL). */
 int chgnet_backward(const chgnet_hparams* hp, const chgnet_batch* batch, const chgnet_graph* graph,
                     const float* params, const float* dE, const float* dF, const float* dS, const float* dM,
                     float* grad, void* ws, size_t ws_bytes, void* stream);

@@ -20,7 +20,9 @@
 // maps (embedding, gated-MLP inputs, output linears, heads) run on the GEMM
 // and weight-gradient kernels, once per part; the gates, messages and the
 // scatter of input gradients have their own kernels here. Eq. (11) blocks
-// (sequential = 0) without the magnetic-moment head.
+// (sequential = 0). The magnetic-moment loss term is first order: its output
+// takes the seed (0, l_M,i), which adds its ordinary backward to the tangent
+// part.
 
 struct Dn {
   float v, t;
@@ -704,12 +706,12 @@ GemmProblem tangent_of(GemmProblem p, std::initializer_list<const float*> at, fl
 unsigned dn_blocks(int64_t n) { return (unsigned)cdiv(std::max<int64_t>(n, 1), 256); }
 
 // G (public layout, overwritten) = tangent of the weight gradient described
-// at the top of this file, for the loss gradients dE [S], dF [N,3], dS [S,9].
-// Needs the activations of forward_impl with the same weights (a.Pal) and
-// positions.
-int cons_grad_impl(Ctx& c, const float* dE, const float* dF, const float* dS, float* G, hipStream_t st) {
+// at the top of this file, for the loss gradients dE [S], dF [N,3], dS [S,9]
+// and, with the moment head, dM [N] (may be null: zero). Needs the
+// activations of forward_impl with the same weights (a.Pal) and positions.
+int cons_grad_impl(Ctx& c, const float* dE, const float* dF, const float* dS, const float* dM, float* G,
+                   hipStream_t st) {
   if (c.hp->sequential) return fail(CHGNET_EINVAL, "conservative readout: weight gradients need the Eq. (11) block");
-  if (c.hp->magmom) return fail(CHGNET_EINVAL, "conservative readout: weight gradients without the magnetic-moment head");
   const Dims& m = c.dm;
   Acts& a = c.a;
   const ParamLayout& L = c.La;
@@ -942,6 +944,14 @@ int cons_grad_impl(Ctx& c, const float* dE, const float* dF, const float* dS, fl
   CHG_TRY(gemm2(N, D, d.dv, D, d.dh1, D, D, P + hE.W1, D, 1, nullptr));
   cross(N, D, D, a.v[m.T], d.v_t[m.T], D, nullptr, d.dh1, D, nullptr, hEg.W1, D);
   colsum(N, D, d.dh1[1], D, nullptr, hEg.b1);
+  if (c.hp->magmom && dM) {
+    // m_i = |v_i w_m + b_m| with the seed (0, l_M,i): its first-order
+    // backward, in the tangent part only
+    KLAUNCH(st, "kd_head", k_magmom_bwd<<<(unsigned)cdiv(N, 4), 256, 0, st>>>((int)N, D, dM, a.oM, P + L.M_W, a.gM,
+                                                                            d.dv[1]));
+    ts.push_back(tp(N, D, 1, a.v[m.T], D, 0, nullptr, a.gM, 1, 0, nullptr, gB + Lg.M_W, 1));
+    ts.push_back(tp(N, 1, 1, nullptr, 0, 0, nullptr, a.gM, 1, 0, nullptr, gB + Lg.M_b, 1));
+  }
   CHG_TRY(flush());
   for (int k = 0; k < 2; ++k) {
     CHG_TRY(fill(d.de[k], E * D, 0.f, st));

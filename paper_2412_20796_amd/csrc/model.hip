@@ -3330,9 +3330,8 @@ int backward_entry(const chgnet_hparams* hp, const chgnet_batch* batch, const ch
   if (!params || !dE || !dF || !dS || !grad) return fail(CHGNET_EINVAL, "backward: null argument");
   if (dM && !hp->magmom) return fail(CHGNET_EINVAL, "backward: dM without the magnetic-moment head");
   if (hp->conservative) {
-    if (dM) return fail(CHGNET_EINVAL, "backward: the conservative readout is trained without the magnetic-moment head");
     CHG_TRY(pack_params(c.L, c.La, params, c.a.Pal, st));
-    return cons_grad_impl(c, dE, dF, dS, grad, st);
+    return cons_grad_impl(c, dE, dF, dS, dM, grad, st);
   }
   return backward_impl(c, params, true, dE, dF, dS, dM, grad, st);
 }
@@ -3343,8 +3342,8 @@ int step_entry(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_graph
                size_t ws_bytes, hipStream_t st) {
   if (!params || !E_t || !F_t || !S_t || !loss_cfg || !loss || !grad) return fail(CHGNET_EINVAL, "step: null argument");
   CHG_TRY(validate_hparams(hp));
-  if (hp->conservative && (hp->sequential || hp->magmom))
-    return fail(CHGNET_EINVAL, "step: the conservative readout is trained with the Eq. (11) block and without the magnetic-moment head");
+  if (hp->conservative && hp->sequential)
+    return fail(CHGNET_EINVAL, "step: the conservative readout is trained with the Eq. (11) block");
   if ((M_t != nullptr) != (hp->magmom != 0))
     return fail(CHGNET_EINVAL, "step: M_target is required with the magnetic-moment head and only with it");
   if (!std::isfinite(loss_cfg->huber_delta)) return fail(CHGNET_EINVAL, "step: huber_delta is not finite");
@@ -3376,7 +3375,7 @@ int step_entry(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_graph
   KLAUNCH(st, "k_loss", k_loss<<<1, 256, 0, st>>>((int)c.dm.S, (int)c.dm.N, batch->atom_ptr, e_out, f_out, s_out,
                                                    mag ? c.a.oM : nullptr, E_t, F_t, S_t, M_t, *loss_cfg, loss, c.a.dE,
                                                    c.a.dF, c.a.dS, c.a.dM));
-  if (hp->conservative) CHG_TRY(cons_grad_impl(c, c.a.dE, c.a.dF, c.a.dS, grad, st));
+  if (hp->conservative) CHG_TRY(cons_grad_impl(c, c.a.dE, c.a.dF, c.a.dS, mag ? c.a.dM : nullptr, grad, st));
   else CHG_TRY(backward_impl(c, params, false, c.a.dE, c.a.dF, c.a.dS, mag ? c.a.dM : nullptr, grad, st));
   if (adam_hp) {
     const float lr = adam_hp[0], b1 = adam_hp[1], b2 = adam_hp[2], eps = adam_hp[3], t = adam_hp[4];

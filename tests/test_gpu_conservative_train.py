@@ -4,11 +4,11 @@ dual numbers) against the fp64 autodiff oracle, which differentiates the loss
 through autograd's own dE/dr and dE/d(eps) (second derivatives by
 create_graph): the training step's loss and gradient (squared and Huber
 errors) and chgnet_backward with random output gradients, on the cubic8
-workload and random small batches; at the full triclinic40 size, output
+workload, random small batches and the magnetic-moment head (its loss
+term is first order); at the full triclinic40 size, output
 gradients on a sample of structures against the oracle on those structures
 alone (crystals of a batch are independent and the gradient is linear in
-the output gradients). The Eq. (10) block and the
-magnetic-moment head are refused with CHGNET_EINVAL.
+the output gradients). The Eq. (10) block is refused with CHGNET_EINVAL.
 
 Tolerance per parameter tensor: |gpu - ref| <= 5e-5 m + 1e-3 |ref|, with m
 the larger of the tensor's max|ref| and 1e-2 of the whole gradient's (a
@@ -77,11 +77,11 @@ def _setup(bd, b, d, T, **kw):
     return hp, db, g, ws
 
 
-def _check_step(bd, b, params, targets, d, T, name, delta=None):
-    ohp = om.HParams(d=d, n_layers=T, conservative=True)
+def _check_step(bd, b, params, targets, d, T, name, delta=None, magmom=False):
+    ohp = om.HParams(d=d, n_layers=T, conservative=True, magmom=magmom)
     graph = og.build_graph(b.atom_ptr, b.pos, b.lattice)
     rl, rg = autodiff.loss_and_grad(ohp, b, graph, params.astype(np.float64), targets, delta=delta)
-    hp, db, g, ws = _setup(bd, b, d, T)
+    hp, db, g, ws = _setup(bd, b, d, T, magmom=magmom)
     loss, grad = bd.step(hp, db, g, _dev(params), [_dev(x) for x in targets], ws, huber_delta=delta or 0.0)
     lv = float(loss.cpu().numpy()[0])
     assert abs(lv - rl) <= 1e-5 + 1e-4 * abs(rl), (name, lv, rl)
@@ -99,6 +99,14 @@ def test_step_random_batches(bd, seed):
     params = synth.make_params(64, 3, seed=(12, 1, seed))
     targets = synth.make_targets(b, seed=(12, 2, seed))
     _check_step(bd, b, params, targets, 64, 3, "random%d conservative step" % seed, delta=0.1 if seed == 1 else None)
+
+
+def test_step_magmom_head(bd):
+    b = synth.random_crystals(seed=21, n_struct=2, n_lo=3, n_hi=10)
+    params = synth.make_params(64, 3, seed=(12, 1, 7), magmom=True)
+    targets = synth.make_targets(b, seed=(12, 2, 7), magmom=True)
+    _check_step(bd, b, params, targets, 64, 3, "magmom conservative step", magmom=True)
+    _check_step(bd, b, params, targets, 64, 3, "magmom huber conservative step", delta=0.2, magmom=True)
 
 
 def test_step_d128_single_layer(bd):
@@ -168,14 +176,9 @@ def test_triclinic40_sampled_structures(bd):
     _assert_grad(grad.cpu().numpy(), rg.numpy(), ohp, "triclinic40 sampled conservative backward")
 
 
-def test_unsupported_variants_refused(bd):
+def test_eq10_block_refused(bd):
     b, params, targets, d, T = synth.workload_inputs("cubic8")
-    for kw in ({"sequential": True}, {"magmom": True}):
-        hp, db, g, ws = _setup(bd, b, d, T, **kw)
-        tg = [_dev(x) for x in targets]
-        if kw.get("magmom"):
-            tg.append(_dev(np.zeros(b.n_atoms, dtype=np.float32)))
-        p = _dev(synth.make_params(d, T, seed=(7, 1, 0), magmom=bool(kw.get("magmom"))))
-        with pytest.raises(bd.ChgnetError) as e:
-            bd.step(hp, db, g, p, tg, ws)
-        assert e.value.code == bd.CHGNET_EINVAL
+    hp, db, g, ws = _setup(bd, b, d, T, sequential=True)
+    with pytest.raises(bd.ChgnetError) as e:
+        bd.step(hp, db, g, _dev(params), [_dev(x) for x in targets], ws)
+    assert e.value.code == bd.CHGNET_EINVAL
