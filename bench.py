@@ -118,7 +118,8 @@ def main():
         prof = bd.profile_stop()
         E, B, A = g.n_edges, g.n_bonds, g.n_angles
         rl, rows = roofline(prof, n, dict(N=b.n_atoms, E=E, B=B, A=A, S=b.n_struct, D=d, T=T,
-                                          fused_bwd=d == 64 and not args.sequential, workload=args.workload))
+                                          fused_bwd=d == 64 and not args.sequential, workload=args.workload,
+                                          R=hp.n_rbf, K=hp.n_fourier))
         print(json.dumps({"launch_timing_steps": n, "roofline": rl, "kernels": rows}), flush=True)
         return
     for _ in range(max(args.warmup, 1)):
@@ -177,7 +178,8 @@ def main():
         prof = bd.profile_stop()
         out["roofline"], out["kernels"] = roofline(prof, args.steps, dict(N=b.n_atoms, E=E, B=B, A=A, S=S, D=d, T=T,
                                                                             fused_bwd=d == 64 and not args.sequential,
-                                                                            workload=args.workload))
+                                                                            workload=args.workload, R=hp.n_rbf,
+                                                                            K=hp.n_fourier))
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(args.workload, args.cpu_sample, variant=args)
     print(json.dumps(out), flush=True)
@@ -298,6 +300,42 @@ def algorithmic_cost(tag, z):
         return "hbm", f * (Tang * lay + last)
     if tag == "k_bond_bwd_reduce":  # read dz twice (both roles), t2; write DZ12
         return "hbm", f * (Tang * A * (8 * D + D) + A * (4 * D + D) + T * B * 8 * D)
+    # training through the conservative readout: the dual-number pass (value
+    # and tangent parts; a linear map costs twice its flops, the tangent-only
+    # maps once)
+    R, K = z.get("R", 31), z.get("K", 31)
+    if tag == "kd_gemm":
+        emb = 2 * (2 * E * R * D + B * R * D + A * K * D) + 8 * E * D * R + 4 * B * D * R
+        heads = 4 * N * D * D + 8 * N * D * D
+        # per layer: projections (atom blocks 4 or 3, bond blocks 4 or 2), the
+        # edge and angle blocks, tangent updates; backward dm, dmu, the input
+        # gradients of atoms (S, 4 or 3 blocks of 2d), edges, angles and bonds (T)
+        lay = lambda ang: (8 * N * D * D * (4 if ang else 3) + 8 * B * D * D * (4 if ang else 2) + 8 * E * D * D
+                           + 8 * A * D * D * (2 if ang else 1) + 2 * N * D * D + 2 * B * D * D
+                           + 4 * N * D * D + 4 * B * D * D + 8 * N * D * D * (4 if ang else 3) + 8 * E * D * D
+                           + 8 * A * D * D * (2 if ang else 1) + 8 * B * D * D * (4 if ang else 2))
+        return "mfma", emb + heads + Tang * lay(True) + lay(False)
+    if tag == "kd_tn":
+        # X_t^T Y_v + X_v^T Y_t of every weight: heads, output linears, the
+        # gate blocks (atom blocks over atoms, bond blocks over bonds, edge
+        # and angle blocks over their rows), the embedding
+        emb = 8 * E * R * D + 4 * B * R * D + 4 * A * K * D
+        heads = 8 * N * D * D + 4 * N * D
+        lay = lambda ang: (4 * N * D * D + 4 * B * D * D + 16 * N * D * D + 8 * E * D * D
+                           + (8 * N * D * D + 16 * B * D * D + 8 * A * D * D) * (2 if ang else 1))
+        return "mfma", emb + heads + Tang * lay(True) + lay(False)
+    if tag == "kd_gate_fwd":
+        # per row and gate: z (2d, both parts) in and out, phi (d, both
+        # parts) out (the angle update: a tangent in, a' tangent out);
+        # projection tables N x 8d and B x 8d, both parts, once
+        lay = lambda ang: (E * 10 * D + A * 10 * D + (A * 10 * D if ang else 0) + N * 16 * D
+                           + B * 16 * D * (1 if ang else 0.5))
+        return "hbm", f * (Tang * lay(True) + lay(False))
+    if tag == "kd_gate_bwd":
+        # per row and gate: z (2d) and d phi (d) in, dz (2d) out, both parts;
+        # the LayerNorm parameter terms (4d, tangent) out
+        lay = lambda ang: (E + A * (2 if ang else 1)) * 14 * D
+        return "hbm", f * (Tang * lay(True) + lay(False))
     return None, None
 
 

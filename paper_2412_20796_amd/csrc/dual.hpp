@@ -766,8 +766,8 @@ int cons_grad_impl(Ctx& c, const float* dE, const float* dF, const float* dS, co
     J.start[0] = 0;
     for (int k = 0; k < J.n; ++k) J.start[k + 1] = J.start[k] + J.j[k].rows;
     if (J.start[J.n] == 0) return CHGNET_OK;
-    if (fwd) KLAUNCH(st, "kd_gate", kd_gate_fwd<<<(unsigned)cdiv(J.start[J.n], 4), 256, 0, st>>>(J, D));
-    else KLAUNCH(st, "kd_gate", kd_gate_bwd<<<(unsigned)cdiv(J.start[J.n], 4), 256, 0, st>>>(J, D));
+    if (fwd) KLAUNCH(st, "kd_gate_fwd", kd_gate_fwd<<<(unsigned)cdiv(J.start[J.n], 4), 256, 0, st>>>(J, D));
+    else KLAUNCH(st, "kd_gate_bwd", kd_gate_bwd<<<(unsigned)cdiv(J.start[J.n], 4), 256, 0, st>>>(J, D));
     return CHGNET_OK;
   };
   const int64_t WB = (int64_t)D * 2 * D;  // one d-row input block of a gate's first layer
