@@ -52,6 +52,17 @@ def test_workspace_size_monotone(L):
     assert 0 < g < a < b
 
 
+def test_workspace_holds_the_dual_number_buffers(L):
+    """With the conservative readout the workspace also holds the buffers of
+    the dual-number weight gradient: at least the value and tangent
+    pre-activations of every gate of every layer, T x 2 x (E + 2A) x 2d
+    floats, beyond the direct-head size."""
+    N, E, B, A, S = 100, 1000, 100, 1000, 2
+    base = L.workspace_size(L.hparams(), N, E, B, A, S)
+    cons = L.workspace_size(L.hparams(conservative=True), N, E, B, A, S)
+    assert cons - base >= 4 * 2 * (E + 2 * A) * 128 * 4
+
+
 @pytest.mark.parametrize("kw", [dict(d=32), dict(d=96), dict(n_layers=0), dict(n_layers=17), dict(n_fourier=30),
                                 dict(n_rbf=0), dict(n_rbf=65), dict(r_bond=7.0), dict(r_atom=25.0, r_bond=3.0),
                                 dict(envelope_p=1), dict(magmom=2), dict(sequential=-1),
