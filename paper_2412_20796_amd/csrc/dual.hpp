@@ -159,7 +159,7 @@ __global__ void __launch_bounds__(256) kd_angles(int A, int K, const int* __rest
 // rows of 8d: four blocks of 2d) and their rows are gathered into the
 // pre-activation by the gate kernel; in the backward pass the
 // pre-activation gradients are first summed per atom (S) and per bond (T),
-// in the graph's CSR orders, and multiplied there.
+// in the graph's CSR orders (no atomics), and multiplied there.
 // ---------------------------------------------------------------------------
 // A block per atom i and block q of S (both parts): S[i] = [sum over the
 // out-edges e of dz_av[e] | of dz_av[rev e] (the edges that end at i) | sum
@@ -216,51 +216,44 @@ __global__ void __launch_bounds__(256) kd_dz_atoms(int N, int D, int nblk, const
 }
 
 // a wavefront per bond b (both parts): T[b] = [sum over the angles whose
-// first bond is b of dz_be | 0 | of dz_an | 0]; the zero blocks take the
-// second-bond roles (kd_dz_b2)
+// first bond is b of dz_be | over the angles whose second bond is b | the
+// same two of dz_an]. At a centre atom with bonds b0 .. b0 + k - 1 the block
+// of bond p lists the other k - 1 bonds in increasing order, so the angle
+// (p, q) is the reverse of (q, p) and sits at position q - b0 (minus one if q
+// > p) of p's block: the second-bond sums read the reverses of b's own angles.
 __global__ void __launch_bounds__(256) kd_dz_bonds(int B, int D, int ang, const int* __restrict__ ap,
-                                                   const float* __restrict__ zbv, const float* __restrict__ zbt,
-                                                   const float* __restrict__ znv, const float* __restrict__ znt,
-                                                   float* __restrict__ tv, float* __restrict__ tt) {
+                                                   const int* __restrict__ bsrc, const int* __restrict__ bp,
+                                                   const int* __restrict__ b2, const float* __restrict__ zbv,
+                                                   const float* __restrict__ zbt, const float* __restrict__ znv,
+                                                   const float* __restrict__ znt, float* __restrict__ tv,
+                                                   float* __restrict__ tt) {
   const int lane = threadIdx.x & 63;
   const int64_t w = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   if (w >= B) return;
   const int W2 = 2 * D;
+  const int64_t b0 = bp[bsrc[w]], qq = w - b0;
   for (int c = lane; c < W2; c += 64) {
-    float bv = 0.f, bt = 0.f, nv = 0.f, nt = 0.f;
+    float s[8] = {};
     for (int64_t a = ap[w]; a < ap[w + 1]; ++a) {
-      const int64_t o = a * W2 + c;
-      bv += zbv[o];
-      bt += zbt[o];
+      const int64_t p = b2[a], pp = p - b0;
+      const int64_t o = a * W2 + c, o2 = (ap[p] + (qq < pp ? qq : qq - 1)) * W2 + c;
+      s[0] += zbv[o];
+      s[1] += zbt[o];
+      s[2] += zbv[o2];
+      s[3] += zbt[o2];
       if (ang) {
-        nv += znv[o];
-        nt += znt[o];
+        s[4] += znv[o];
+        s[5] += znt[o];
+        s[6] += znv[o2];
+        s[7] += znt[o2];
       }
     }
     const int64_t o = w * 4 * W2 + c;
-    tv[o] = bv;
-    tt[o] = bt;
-    tv[o + W2] = tt[o + W2] = 0.f;
-    tv[o + 2 * W2] = nv;
-    tt[o + 2 * W2] = nt;
-    tv[o + 3 * W2] = tt[o + 3 * W2] = 0.f;
-  }
-}
-
-// per angle and column: T[b2] second-bond blocks += dz_be (and dz_an) rows
-__global__ void __launch_bounds__(256) kd_dz_b2(int64_t n, int D, int ang, const int* __restrict__ b2,
-                                                const float* __restrict__ zbv, const float* __restrict__ zbt,
-                                                const float* __restrict__ znv, const float* __restrict__ znt,
-                                                float* __restrict__ tv, float* __restrict__ tt) {
-  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (i >= n) return;
-  const int W2 = 2 * D;
-  const int64_t o = (int64_t)b2[i / W2] * 4 * W2 + W2 + i % W2;
-  atomicAdd(tv + o, zbv[i]);
-  atomicAdd(tt + o, zbt[i]);
-  if (ang) {
-    atomicAdd(tv + o + 2 * W2, znv[i]);
-    atomicAdd(tt + o + 2 * W2, znt[i]);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      tv[o + k * W2] = s[2 * k];
+      tt[o + k * W2] = s[2 * k + 1];
+    }
   }
 }
 
@@ -1017,15 +1010,10 @@ int cons_grad_impl(Ctx& c, const float* dE, const float* dF, const float* dS, co
                                                                                 g.bond_ptr, g.angle_ptr, d.dzav[0], d.dzav[1],
                                                                                 d.dzbe[0], d.dzbe[1], d.dzan[0], d.dzan[1],
                                                                                 d.S[0], d.S[1]));
-    if (B > 0) {
-      KLAUNCH(st, "kd_dz_sum", kd_dz_bonds<<<(unsigned)cdiv(B, 4), 256, 0, st>>>((int)B, D, ang, g.angle_ptr, d.dzbe[0],
-                                                                                d.dzbe[1], d.dzan[0], d.dzan[1], d.T[0],
-                                                                                d.T[1]));
-      if (A > 0)
-        KLAUNCH(st, "kd_dz_sum", kd_dz_b2<<<dn_blocks(A * 2 * D), 256, 0, st>>>(A * 2 * D, D, ang, a.ang_b2, d.dzbe[0],
-                                                                                d.dzbe[1], d.dzan[0], d.dzan[1], d.T[0],
-                                                                                d.T[1]));
-    }
+    if (B > 0)
+      KLAUNCH(st, "kd_dz_sum", kd_dz_bonds<<<(unsigned)cdiv(B, 4), 256, 0, st>>>((int)B, D, ang, g.angle_ptr, a.bond_src,
+                                                                                g.bond_ptr, a.ang_b2, d.dzbe[0], d.dzbe[1],
+                                                                                d.dzan[0], d.dzan[1], d.T[0], d.T[1]));
     // input gradients of v^t, e^t and a^t (accumulated): atoms from S, edges
     // from dz_av, angles from dz_be, dz_an; then the bond rows of e from T
     {
