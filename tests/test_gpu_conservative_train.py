@@ -4,8 +4,9 @@ dual numbers) against the fp64 autodiff oracle, which differentiates the loss
 through autograd's own dE/dr and dE/d(eps) (second derivatives by
 create_graph): the training step's loss and gradient (squared and Huber
 errors) and chgnet_backward with random output gradients, on the cubic8
-workload, random small batches and the magnetic-moment head (its loss
-term is first order); at the full triclinic40 size, output
+workload, random small batches, the magnetic-moment head (its loss term
+is first order) and sparse cells (no bonds, no angles, no edges); at the
+full triclinic40 size, output
 gradients on a sample of structures against the oracle on those structures
 alone (crystals of a batch are independent and the gradient is linear in
 the output gradients). The Eq. (10) block is refused with CHGNET_EINVAL.
@@ -107,6 +108,22 @@ def test_step_magmom_head(bd):
     targets = synth.make_targets(b, seed=(12, 2, 7), magmom=True)
     _check_step(bd, b, params, targets, 64, 3, "magmom conservative step", magmom=True)
     _check_step(bd, b, params, targets, 64, 3, "magmom huber conservative step", delta=0.2, magmom=True)
+
+
+def test_step_sparse_cells(bd):
+    """Edges but no bonds (one atom in a 5 A cube: B = A = 0), bonds but no
+    angles (a dimer: one bond per atom), and an isolated atom (E = 0)."""
+    params = synth.make_params(64, 2, seed=(8, 1, 0))
+    cells = [
+        ("edges only", synth.make_custom_batch([np.eye(3) * 5.0], [np.zeros((1, 3))], [np.array([14])])),
+        ("dimer", synth.make_custom_batch([np.eye(3) * 10.0], [np.array([[0.0, 0.0, 0.0], [0.15, 0.0, 0.0]])],
+                                          [np.array([8, 8])])),
+        ("no edges", synth.make_custom_batch([np.eye(3) * 13.0], [np.zeros((1, 3))], [np.array([26])])),
+    ]
+    for k, (name, b) in enumerate(cells):
+        g = og.build_graph(b.atom_ptr, b.pos, b.lattice)
+        print(name, "E B A =", len(g["edge_dst"]), len(g["bond_edge"]), len(g["angle_b2"]), flush=True)
+        _check_step(bd, b, params, synth.make_targets(b, seed=(8, 2, k)), 64, 2, name + " conservative step")
 
 
 def test_step_d128_single_layer(bd):
