@@ -332,9 +332,9 @@ def algorithmic_cost(tag, z):
                            + B * 16 * D * (1 if ang else 0.5))
         return "hbm", f * (Tang * lay(True) + lay(False))
     if tag == "kd_gate_bwd":
-        # per row and gate: z (2d) and d phi (d) in, dz (2d) out, both parts;
-        # the LayerNorm parameter terms (4d, tangent) out
-        lay = lambda ang: (E + A * (2 if ang else 1)) * 14 * D
+        # per row and gate: z (2d) and d phi (d) in, dz (2d) out, both parts
+        # (the LayerNorm parameter terms stay in registers)
+        lay = lambda ang: (E + A * (2 if ang else 1)) * 10 * D
         return "hbm", f * (Tang * lay(True) + lay(False))
     return None, None
 

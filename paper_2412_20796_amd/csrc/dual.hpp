@@ -262,6 +262,7 @@ __global__ void __launch_bounds__(256) kd_dz_bonds(int B, int D, int ang, const 
 // wavefront a row, d / 64 columns a lane.
 // ---------------------------------------------------------------------------
 constexpr int kDnMaxV = 2;  // d <= 128
+constexpr int kDnGateWaves = 8192;  // wavefronts of the gate backward (8 a SIMD)
 
 struct DnGate {
   int64_t rows;
@@ -277,7 +278,7 @@ struct DnGate {
   float *pv, *pt;
   const float* res_t;
   // backward: d phi in (dpv, dpt) -> dz (dzv, dzt) and the tangents of the
-  // LayerNorm parameter terms per row, lnp [rows, 4d]: dy_c xhat_c | dy_c | dy_g xhat_g | dy_g
+  // LayerNorm parameter terms summed per wavefront, lnp [waves, 4d]
   const float *dpv, *dpt;
   float *dzv, *dzt, *lnp;
 };
@@ -375,13 +376,11 @@ __global__ void __launch_bounds__(256) kd_gate_fwd(DnGates J, int D) {
   }
 }
 
-__global__ void __launch_bounds__(256) kd_gate_bwd(DnGates J, int D) {
-  const int lane = threadIdx.x & 63;
-  const int64_t w = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (w >= J.start[J.n]) return;
-  const int k = dn_job(J, w);
-  const DnGate& q = J.j[k];
-  const int64_t r = w - J.start[k];
+// Backward of the gates: every wavefront walks the rows w, w + W, ... of each
+// job (W wavefronts in the grid) and keeps the tangents of its rows'
+// LayerNorm parameter terms in registers; it writes them once per job, as
+// row w of lnp [W, 4d]: dy_c xhat_c | dy_c | dy_g xhat_g | dy_g.
+__device__ __forceinline__ void dn_gate_bwd_row(const DnGate& q, int64_t r, int D, int lane, float (&acc)[4][kDnMaxV]) {
   const int V = D / 64;
   Dn zc[kDnMaxV], zg[kDnMaxV], xc[kDnMaxV], xg[kDnMaxV], rc, rg;
   dn_load_z(q, r, D, lane, zc, zg);
@@ -401,11 +400,10 @@ __global__ void __launch_bounds__(256) kd_gate_bwd(DnGates J, int D) {
     const Dn sc = dn_sigm(yc), sg = dn_sigm(yg);
     const Dn dyc = dp * sg * (sc * (1.0f + yc * (1.0f - sc)));
     const Dn dyg = dp * (yc * sc) * sg * (1.0f - sg);
-    float* lp = q.lnp + r * 4 * D + c;
-    lp[0] = (dyc * xc[i]).t;
-    lp[D] = dyc.t;
-    lp[2 * D] = (dyg * xg[i]).t;
-    lp[3 * D] = dyg.t;
+    acc[0][i] += (dyc * xc[i]).t;
+    acc[1][i] += dyc.t;
+    acc[2][i] += (dyg * xg[i]).t;
+    acc[3][i] += dyg.t;
     gc[i] = q.gc[c] * dyc;
     gg[i] = q.gg[c] * dyg;
     s1c = s1c + gc[i];
@@ -428,6 +426,22 @@ __global__ void __launch_bounds__(256) kd_gate_bwd(DnGates J, int D) {
     q.dzt[o] = dc.t;
     q.dzv[o + D] = dg.v;
     q.dzt[o + D] = dg.t;
+  }
+}
+
+__global__ void __launch_bounds__(256) kd_gate_bwd(DnGates J, int D) {
+  const int lane = threadIdx.x & 63;
+  const int64_t w = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6), W = (int64_t)gridDim.x * 4;
+  for (int k = 0; k < J.n; ++k) {
+    const DnGate& q = J.j[k];
+    float acc[4][kDnMaxV] = {};
+    for (int64_t r = w; r < q.rows; r += W) dn_gate_bwd_row(q, r, D, lane, acc);
+#pragma unroll
+    for (int i = 0; i < kDnMaxV; ++i) {
+      if (i >= D / 64) break;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) q.lnp[w * 4 * D + u * D + lane + 64 * i] = acc[u][i];
+    }
   }
 }
 
@@ -677,9 +691,9 @@ void carve_dual(Arena& ar, const Dims& m, int64_t n_params, DualBufs& d) {
     d.drbfa[k] = f(E * R);
     d.drbfb[k] = f(B * R);
   }
-  d.lnav = f(E * 4 * D);
-  d.lnbe = f(A * 4 * D);
-  d.lnan = f(A * 4 * D);
+  d.lnav = f(kDnGateWaves * 4 * D);
+  d.lnbe = f(kDnGateWaves * 4 * D);
+  d.lnan = f(kDnGateWaves * 4 * D);
   d.fpa = f(E * R);
   d.fpb = f(B * R);
   d.gB = f(n_params);
@@ -758,9 +772,13 @@ int cons_grad_impl(Ctx& c, const float* dE, const float* dF, const float* dS, co
   auto gates = [&](DnGates& J, bool fwd) -> int {
     J.start[0] = 0;
     for (int k = 0; k < J.n; ++k) J.start[k + 1] = J.start[k] + J.j[k].rows;
-    if (J.start[J.n] == 0) return CHGNET_OK;
-    if (fwd) KLAUNCH(st, "kd_gate_fwd", kd_gate_fwd<<<(unsigned)cdiv(J.start[J.n], 4), 256, 0, st>>>(J, D));
-    else KLAUNCH(st, "kd_gate_bwd", kd_gate_bwd<<<(unsigned)cdiv(J.start[J.n], 4), 256, 0, st>>>(J, D));
+    if (fwd) {
+      if (J.start[J.n] > 0)
+        KLAUNCH(st, "kd_gate_fwd", kd_gate_fwd<<<(unsigned)cdiv(J.start[J.n], 4), 256, 0, st>>>(J, D));
+    } else {
+      // every wavefront writes its LayerNorm terms, also for jobs without rows
+      KLAUNCH(st, "kd_gate_bwd", kd_gate_bwd<<<(unsigned)(kDnGateWaves / 4), 256, 0, st>>>(J, D));
+    }
     return CHGNET_OK;
   };
   const int64_t WB = (int64_t)D * 2 * D;  // one d-row input block of a gate's first layer
@@ -1070,9 +1088,9 @@ int cons_grad_impl(Ctx& c, const float* dE, const float* dF, const float* dS, co
         crossc(A, D, 2 * D, a.a[t], d.a_t[t], D, nullptr, dz, 2 * D, 0, nullptr, og.W + 3 * WB, 2 * D);
       }
       colsum(rows, 2 * D, dz[1], 2 * D, nullptr, og.b);
-      if (rows > 0)
-        ts.push_back(split_out(tp(rows, 1, 4 * D, nullptr, 0, 0, nullptr, lnp, 4 * D, 0, nullptr, gB + og.g_c, D), D,
-                               gB + og.b_c, gB + og.g_g, gB + og.b_g));
+      // LayerNorm scales and shifts: the column sums of the per-wavefront terms
+      ts.push_back(split_out(tp(kDnGateWaves, 1, 4 * D, nullptr, 0, 0, nullptr, lnp, 4 * D, 0, nullptr, gB + og.g_c, D), D,
+                             gB + og.b_c, gB + og.g_g, gB + og.b_g));
     };
     gate_terms(0, d.dzav, d.lnav, lg.av);
     gate_terms(1, d.dzbe, d.lnbe, lg.be);
