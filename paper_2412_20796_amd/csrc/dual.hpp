@@ -262,7 +262,7 @@ __global__ void __launch_bounds__(256) kd_dz_bonds(int B, int D, int ang, const 
 // wavefront a row, d / 64 columns a lane.
 // ---------------------------------------------------------------------------
 constexpr int kDnMaxV = 2;  // d <= 128
-constexpr int kDnGateWaves = 8192;  // wavefronts of the gate backward (8 a SIMD)
+constexpr int kDnGateWaves = 4096;  // wavefronts of the gate kernels: one resident round, 4 a SIMD
 
 struct DnGate {
   int64_t rows;
@@ -284,117 +284,167 @@ struct DnGate {
 };
 struct DnGates {
   int n;
-  int64_t start[4];  // first wavefront of each job; start[n] = total
+  int64_t start[4];  // prefix sums of the jobs' rows; start[n] = total
   DnGate j[3];
 };
 
-__device__ __forceinline__ void dn_ln(const Dn (&z)[kDnMaxV], int V, int D, Dn (&xh)[kDnMaxV], Dn& rstd) {
+template <int MV>
+__device__ __forceinline__ void dn_ln(const Dn (&z)[MV], int V, int D, Dn (&xh)[MV], Dn& rstd) {
   Dn s{0.f, 0.f};
 #pragma unroll
-  for (int i = 0; i < kDnMaxV; ++i)
+  for (int i = 0; i < MV; ++i)
     if (i < V) s = s + z[i];
   const Dn mu = (1.0f / D) * dn_wsum(s);
   Dn q{0.f, 0.f};
 #pragma unroll
-  for (int i = 0; i < kDnMaxV; ++i)
+  for (int i = 0; i < MV; ++i)
     if (i < V) q = q + (z[i] - mu) * (z[i] - mu);
   rstd = dn_recip(dn_sqrt((1.0f / D) * dn_wsum(q) + kLnEps));
 #pragma unroll
-  for (int i = 0; i < kDnMaxV; ++i) xh[i] = (z[i] - mu) * rstd;
+  for (int i = 0; i < MV; ++i) xh[i] = (z[i] - mu) * rstd;
 }
 
-__device__ __forceinline__ int dn_job(const DnGates& J, int64_t w) {
-  int k = 0;
-  while (k + 1 < J.n && w >= J.start[k + 1]) ++k;
-  return k;
-}
-
-__device__ __forceinline__ void dn_load_z(const DnGate& q, int64_t r, int D, int lane, Dn (&zc)[kDnMaxV],
-                                          Dn (&zg)[kDnMaxV]) {
+// Raw inputs of one forward row (lane's columns): z core/gate value and
+// tangent, and the gathered projection rows, summed only when the row is
+// computed, so that the loads of the next row are in flight meanwhile.
+template <int V>
+struct DnFwdRaw {
+  float z[4][V];
+  float a[3][4][V];
+};
+template <int V>
+__device__ __forceinline__ void dn_fwd_load(const DnGate& q, int64_t r, const int64_t (&ro)[3], int D, int lane,
+                                            DnFwdRaw<V>& x) {
 #pragma unroll
-  for (int i = 0; i < kDnMaxV; ++i) {
-    zc[i] = zg[i] = Dn{0.f, 0.f};
-    if (i < D / 64) {
-      const int64_t o = r * 2 * D + lane + 64 * i;
-      zc[i] = Dn{q.zv[o], q.zt[o]};
-      zg[i] = Dn{q.zv[o + D], q.zt[o + D]};
+  for (int i = 0; i < V; ++i) {
+    const int64_t o = r * 2 * D + lane + 64 * i;
+    x.z[0][i] = q.zv[o];
+    x.z[1][i] = q.zt[o];
+    x.z[2][i] = q.zv[o + D];
+    x.z[3][i] = q.zt[o + D];
+#pragma unroll
+    for (int k = 0; k < 3; ++k) {
+      if (k >= q.nadd) break;
+      const int64_t c = ro[k] + lane + 64 * i;
+      x.a[k][0][i] = q.addv[k][c];
+      x.a[k][1][i] = q.addt[k][c];
+      x.a[k][2][i] = q.addv[k][c + D];
+      x.a[k][3][i] = q.addt[k][c + D];
     }
   }
 }
-
-__global__ void __launch_bounds__(256) kd_gate_fwd(DnGates J, int D) {
-  const int lane = threadIdx.x & 63;
-  const int64_t w = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (w >= J.start[J.n]) return;
-  const int k = dn_job(J, w);
-  const DnGate& q = J.j[k];
-  const int64_t r = w - J.start[k];
-  const int V = D / 64;
-  Dn zc[kDnMaxV], zg[kDnMaxV], xc[kDnMaxV], xg[kDnMaxV], rc, rg;
-  int64_t ro[3];
+__device__ __forceinline__ void dn_fwd_index(const DnGate& q, int64_t r, int D, int64_t (&ro)[3]) {
 #pragma unroll
   for (int k = 0; k < 3; ++k) ro[k] = k < q.nadd ? (int64_t)q.idx[k][r] * 8 * D : 0;
-  dn_load_z(q, r, D, lane, zc, zg);
+}
+
+// Forward of the gates: every wavefront walks the rows w, w + W, ... of each
+// job, loading row r + W (and the gather indices of r + 2W) before it
+// computes row r.
+template <int V>
+__global__ void __launch_bounds__(256) kd_gate_fwd(DnGates J) {
+  constexpr int D = 64 * V;
+  const int lane = threadIdx.x & 63;
+  const int64_t w = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6), W = (int64_t)gridDim.x * 4;
+  for (int job = 0; job < J.n; ++job) {
+    const DnGate& q = J.j[job];
+    if (w >= q.rows) continue;
+    int64_t ro[3], ron[3];
+    DnFwdRaw<V> cur, nxt;
+    dn_fwd_index(q, w, D, ro);
+    if (w + W < q.rows) dn_fwd_index(q, w + W, D, ron);
+    dn_fwd_load(q, w, ro, D, lane, cur);
+    for (int64_t r = w; r < q.rows; r += W) {
+      if (r + W < q.rows) {
+        dn_fwd_load(q, r + W, ron, D, lane, nxt);
+        if (r + 2 * W < q.rows) dn_fwd_index(q, r + 2 * W, D, ron);
+      }
+      Dn zc[V], zg[V], xc[V], xg[V], rc, rg;
 #pragma unroll
-  for (int k = 0; k < 3; ++k) {
-    if (k >= q.nadd) break;
+      for (int i = 0; i < V; ++i) {
+        zc[i] = Dn{cur.z[0][i], cur.z[1][i]};
+        zg[i] = Dn{cur.z[2][i], cur.z[3][i]};
 #pragma unroll
-    for (int i = 0; i < kDnMaxV; ++i) {
-      if (i >= V) break;
-      const int64_t c = ro[k] + lane + 64 * i;
-      zc[i] = zc[i] + Dn{q.addv[k][c], q.addt[k][c]};
-      zg[i] = zg[i] + Dn{q.addv[k][c + D], q.addt[k][c + D]};
-    }
-  }
-  if (q.nadd > 0) {
+        for (int k = 0; k < 3; ++k) {
+          if (k >= q.nadd) break;
+          zc[i] = zc[i] + Dn{cur.a[k][0][i], cur.a[k][1][i]};
+          zg[i] = zg[i] + Dn{cur.a[k][2][i], cur.a[k][3][i]};
+        }
+      }
+      if (q.nadd > 0) {
 #pragma unroll
-    for (int i = 0; i < kDnMaxV; ++i) {
-      if (i >= V) break;
-      const int64_t o = r * 2 * D + lane + 64 * i;
-      q.zv[o] = zc[i].v;
-      q.zt[o] = zc[i].t;
-      q.zv[o + D] = zg[i].v;
-      q.zt[o + D] = zg[i].t;
-    }
-  }
-  dn_ln(zc, V, D, xc, rc);
-  dn_ln(zg, V, D, xg, rg);
+        for (int i = 0; i < V; ++i) {
+          const int64_t o = r * 2 * D + lane + 64 * i;
+          q.zv[o] = zc[i].v;
+          q.zt[o] = zc[i].t;
+          q.zv[o + D] = zg[i].v;
+          q.zt[o + D] = zg[i].t;
+        }
+      }
+      dn_ln(zc, V, D, xc, rc);
+      dn_ln(zg, V, D, xg, rg);
 #pragma unroll
-  for (int i = 0; i < kDnMaxV; ++i) {
-    if (i >= V) break;
-    const int c = lane + 64 * i;
-    const Dn yc = q.gc[c] * xc[i] + q.bc[c];
-    const Dn yg = q.gg[c] * xg[i] + q.bg[c];
-    const Dn ph = yc * dn_sigm(yc) * dn_sigm(yg);
-    const int64_t o = r * D + c;
-    if (q.res_t) {
-      q.pt[o] = q.res_t[o] + ph.t;
-    } else {
-      q.pv[o] = ph.v;
-      q.pt[o] = ph.t;
+      for (int i = 0; i < V; ++i) {
+        const int c = lane + 64 * i;
+        const Dn yc = q.gc[c] * xc[i] + q.bc[c];
+        const Dn yg = q.gg[c] * xg[i] + q.bg[c];
+        const Dn ph = yc * dn_sigm(yc) * dn_sigm(yg);
+        const int64_t o = r * D + c;
+        if (q.res_t) {
+          q.pt[o] = q.res_t[o] + ph.t;
+        } else {
+          q.pv[o] = ph.v;
+          q.pt[o] = ph.t;
+        }
+      }
+      cur = nxt;
     }
   }
 }
 
 // Backward of the gates: every wavefront walks the rows w, w + W, ... of each
-// job (W wavefronts in the grid) and keeps the tangents of its rows'
-// LayerNorm parameter terms in registers; it writes them once per job, as
-// row w of lnp [W, 4d]: dy_c xhat_c | dy_c | dy_g xhat_g | dy_g.
-__device__ __forceinline__ void dn_gate_bwd_row(const DnGate& q, int64_t r, int D, int lane, float (&acc)[4][kDnMaxV]) {
-  const int V = D / 64;
-  Dn zc[kDnMaxV], zg[kDnMaxV], xc[kDnMaxV], xg[kDnMaxV], rc, rg;
-  dn_load_z(q, r, D, lane, zc, zg);
+// job (W wavefronts in the grid), loading row r + W before it computes row
+// r, and keeps the tangents of its rows' LayerNorm parameter terms in
+// registers; it writes them once per job, as row w of lnp [W, 4d]:
+// dy_c xhat_c | dy_c | dy_g xhat_g | dy_g.
+template <int V>
+struct DnBwdRaw {
+  float z[4][V];
+  float dp[2][V];
+};
+template <int V>
+__device__ __forceinline__ void dn_bwd_load(const DnGate& q, int64_t r, int lane, DnBwdRaw<V>& x) {
+  constexpr int D = 64 * V;
+#pragma unroll
+  for (int i = 0; i < V; ++i) {
+    const int64_t o = r * 2 * D + lane + 64 * i, op = r * D + lane + 64 * i;
+    x.z[0][i] = q.zv[o];
+    x.z[1][i] = q.zt[o];
+    x.z[2][i] = q.zv[o + D];
+    x.z[3][i] = q.zt[o + D];
+    x.dp[0][i] = q.dpv[op];
+    x.dp[1][i] = q.dpt[op];
+  }
+}
+
+template <int V>
+__device__ __forceinline__ void dn_gate_bwd_row(const DnGate& q, int64_t r, int lane, const DnBwdRaw<V>& x,
+                                                float (&acc)[4][V]) {
+  constexpr int D = 64 * V;
+  Dn zc[V], zg[V], xc[V], xg[V], rc, rg;
+#pragma unroll
+  for (int i = 0; i < V; ++i) {
+    zc[i] = Dn{x.z[0][i], x.z[1][i]};
+    zg[i] = Dn{x.z[2][i], x.z[3][i]};
+  }
   dn_ln(zc, V, D, xc, rc);
   dn_ln(zg, V, D, xg, rg);
-  Dn gc[kDnMaxV], gg[kDnMaxV];
+  Dn gc[V], gg[V];
   Dn s1c{0.f, 0.f}, s2c{0.f, 0.f}, s1g{0.f, 0.f}, s2g{0.f, 0.f};
 #pragma unroll
-  for (int i = 0; i < kDnMaxV; ++i) {
-    gc[i] = gg[i] = Dn{0.f, 0.f};
-    if (i >= V) continue;
+  for (int i = 0; i < V; ++i) {
     const int c = lane + 64 * i;
-    const int64_t o = r * D + c;
-    const Dn dp{q.dpv[o], q.dpt[o]};
+    const Dn dp{x.dp[0][i], x.dp[1][i]};
     const Dn yc = q.gc[c] * xc[i] + q.bc[c];
     const Dn yg = q.gg[c] * xg[i] + q.bg[c];
     const Dn sc = dn_sigm(yc), sg = dn_sigm(yg);
@@ -417,8 +467,7 @@ __device__ __forceinline__ void dn_gate_bwd_row(const DnGate& q, int64_t r, int 
   s1g = inv * dn_wsum(s1g);
   s2g = inv * dn_wsum(s2g);
 #pragma unroll
-  for (int i = 0; i < kDnMaxV; ++i) {
-    if (i >= V) break;
+  for (int i = 0; i < V; ++i) {
     const int64_t o = r * 2 * D + lane + 64 * i;
     const Dn dc = rc * (gc[i] - s1c - xc[i] * s2c);
     const Dn dg = rg * (gg[i] - s1g - xg[i] * s2g);
@@ -429,19 +478,25 @@ __device__ __forceinline__ void dn_gate_bwd_row(const DnGate& q, int64_t r, int 
   }
 }
 
-__global__ void __launch_bounds__(256) kd_gate_bwd(DnGates J, int D) {
+template <int V>
+__global__ void __launch_bounds__(256) kd_gate_bwd(DnGates J) {
+  constexpr int D = 64 * V;
   const int lane = threadIdx.x & 63;
   const int64_t w = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6), W = (int64_t)gridDim.x * 4;
   for (int k = 0; k < J.n; ++k) {
     const DnGate& q = J.j[k];
-    float acc[4][kDnMaxV] = {};
-    for (int64_t r = w; r < q.rows; r += W) dn_gate_bwd_row(q, r, D, lane, acc);
+    float acc[4][V] = {};
+    DnBwdRaw<V> cur, nxt;
+    if (w < q.rows) dn_bwd_load(q, w, lane, cur);
+    for (int64_t r = w; r < q.rows; r += W) {
+      if (r + W < q.rows) dn_bwd_load(q, r + W, lane, nxt);
+      dn_gate_bwd_row(q, r, lane, cur, acc);
+      cur = nxt;
+    }
 #pragma unroll
-    for (int i = 0; i < kDnMaxV; ++i) {
-      if (i >= D / 64) break;
+    for (int i = 0; i < V; ++i)
 #pragma unroll
       for (int u = 0; u < 4; ++u) q.lnp[w * 4 * D + u * D + lane + 64 * i] = acc[u][i];
-    }
   }
 }
 
@@ -774,10 +829,14 @@ int cons_grad_impl(Ctx& c, const float* dE, const float* dF, const float* dS, co
     for (int k = 0; k < J.n; ++k) J.start[k + 1] = J.start[k] + J.j[k].rows;
     if (fwd) {
       if (J.start[J.n] > 0)
-        KLAUNCH(st, "kd_gate_fwd", kd_gate_fwd<<<(unsigned)cdiv(J.start[J.n], 4), 256, 0, st>>>(J, D));
+      {
+        if (D == 64) KLAUNCH(st, "kd_gate_fwd", kd_gate_fwd<1><<<(unsigned)(kDnGateWaves / 4), 256, 0, st>>>(J));
+        else KLAUNCH(st, "kd_gate_fwd", kd_gate_fwd<2><<<(unsigned)(kDnGateWaves / 4), 256, 0, st>>>(J));
+      }
     } else {
       // every wavefront writes its LayerNorm terms, also for jobs without rows
-      KLAUNCH(st, "kd_gate_bwd", kd_gate_bwd<<<(unsigned)(kDnGateWaves / 4), 256, 0, st>>>(J, D));
+      if (D == 64) KLAUNCH(st, "kd_gate_bwd", kd_gate_bwd<1><<<(unsigned)(kDnGateWaves / 4), 256, 0, st>>>(J));
+      else KLAUNCH(st, "kd_gate_bwd", kd_gate_bwd<2><<<(unsigned)(kDnGateWaves / 4), 256, 0, st>>>(J));
     }
     return CHGNET_OK;
   };
