@@ -503,22 +503,37 @@ __global__ void __launch_bounds__(256) kd_gate_bwd(DnGates J) {
 // ---------------------------------------------------------------------------
 // Messages (Eq. 4, 5) and their backward.
 // ---------------------------------------------------------------------------
-// m_i = sum over the edges e of atom i (CSR by source) of e^a_e * phi_e
+// m_i = sum over the edges e of atom i (CSR by source) of e^a_e * phi_e: a
+// block per atom, its four wavefronts take every fourth edge and their sums
+// are added in a fixed order
 __global__ void __launch_bounds__(256) kd_msg_atoms(int N, int D, const int* __restrict__ ep,
                                                     const float* __restrict__ eav, const float* __restrict__ eat,
                                                     const float* __restrict__ pv, const float* __restrict__ pt,
                                                     float* __restrict__ mv, float* __restrict__ mt) {
-  const int lane = threadIdx.x & 63;
-  const int64_t w = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (w >= N) return;
-  for (int c = lane; c < D; c += 64) {
-    Dn s{0.f, 0.f};
-    for (int64_t e = ep[w]; e < ep[w + 1]; ++e) {
-      const int64_t o = e * D + c;
-      s = s + Dn{eav[o], eat[o]} * Dn{pv[o], pt[o]};
+  __shared__ float red[4][2][kDnMaxV * 64];
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int64_t i = blockIdx.x;
+  float sv[kDnMaxV] = {}, st[kDnMaxV] = {};
+  for (int64_t e = ep[i] + wv; e < ep[i + 1]; e += 4) {
+#pragma unroll
+    for (int k = 0; k < kDnMaxV; ++k) {
+      if (k >= D / 64) break;
+      const int64_t o = e * D + lane + 64 * k;
+      const Dn x = Dn{eav[o], eat[o]} * Dn{pv[o], pt[o]};
+      sv[k] += x.v;
+      st[k] += x.t;
     }
-    mv[w * D + c] = s.v;
-    mt[w * D + c] = s.t;
+  }
+#pragma unroll
+  for (int k = 0; k < kDnMaxV; ++k) {
+    red[wv][0][lane + 64 * k] = sv[k];
+    red[wv][1][lane + 64 * k] = st[k];
+  }
+  __syncthreads();
+  for (int c = threadIdx.x; c < 2 * D; c += 256) {
+    const int pl = c / D, cc = c % D;
+    const float v = ((red[0][pl][cc] + red[1][pl][cc]) + red[2][pl][cc]) + red[3][pl][cc];
+    (pl ? mt : mv)[i * D + cc] = v;
   }
 }
 
@@ -923,7 +938,7 @@ int cons_grad_impl(Ctx& c, const float* dE, const float* dF, const float* dS, co
       CHG_TRY(gates(J, true));
     }
     if (N > 0)
-      KLAUNCH(st, "kd_msg", kd_msg_atoms<<<(unsigned)cdiv(N, 4), 256, 0, st>>>((int)N, D, g.edge_ptr, a.ea, d.ea_t,
+      KLAUNCH(st, "kd_msg", kd_msg_atoms<<<(unsigned)N, 256, 0, st>>>((int)N, D, g.edge_ptr, a.ea, d.ea_t,
                                                                               d.pav[t][0], d.pav[t][1], d.m[t][0], d.m[t][1]));
     if (B > 0)
       KLAUNCH(st, "kd_msg", kd_msg_bonds<<<(unsigned)cdiv(B, 4), 256, 0, st>>>((int)B, D, g.angle_ptr, a.ang_b2, a.eb, d.eb_t,
