@@ -6,7 +6,7 @@ create_graph): the training step's loss and gradient (squared and Huber
 errors) and chgnet_backward with random output gradients, on the cubic8
 workload, random small batches, the magnetic-moment head (its loss term
 is first order) and sparse cells (no bonds, no angles, no edges); at the
-full triclinic40 size, output
+full triclinic40 (d = 64, T = 4) and wide128 (d = 128, T = 5) sizes, output
 gradients on a sample of structures against the oracle on those structures
 alone (crystals of a batch are independent and the gradient is linear in
 the output gradients). The Eq. (10) block is refused with CHGNET_EINVAL.
@@ -158,13 +158,13 @@ def test_backward_random_output_gradients(bd):
     _assert_grad(grad.cpu().numpy(), rg.numpy(), ohp, "cubic8 conservative backward")
 
 
-def test_triclinic40_sampled_structures(bd):
+@pytest.mark.parametrize("workload,sample", [("triclinic40", [3, 22]), ("wide128", [5, 77])])
+def test_full_size_sampled_structures(bd, workload, sample):
     import torch
 
     from gpu_helpers import subset_batch
 
-    b, params, _, d, T = synth.workload_inputs("triclinic40")
-    sample = [3, 22]
+    b, params, _, d, T = synth.workload_inputs(workload)
     rng = np.random.default_rng(9)
     dE = np.zeros(b.n_struct)
     dF = np.zeros((b.n_atoms, 3))
@@ -190,7 +190,7 @@ def test_triclinic40_sampled_structures(bd):
     bd.forward(hp, db, g, p, ws)
     f32 = lambda x: _dev(x.astype(np.float32))
     grad = bd.backward(hp, db, g, p, f32(dE), f32(dF), f32(dS), ws)
-    _assert_grad(grad.cpu().numpy(), rg.numpy(), ohp, "triclinic40 sampled conservative backward")
+    _assert_grad(grad.cpu().numpy(), rg.numpy(), ohp, workload + " sampled conservative backward")
 
 
 def test_eq10_block_refused(bd):
