@@ -18,8 +18,9 @@
 // own; tangents, and both parts of every backward quantity, are kept in
 // separate arrays of the same shape (value array, tangent array). The linear
 // maps (embedding, gated-MLP inputs, output linears, heads) run on the GEMM
-// and weight-gradient kernels, once per part; the gates, messages and the
-// scatter of input gradients have their own kernels here. Eq. (11) blocks
+// and weight-gradient kernels, once per part; the gates, the messages and
+// the per-atom and per-bond sums of the pre-activation gradients have their
+// own kernels here. Eq. (11) blocks
 // (sequential = 0). The magnetic-moment loss term is first order: its output
 // takes the seed (0, l_M,i), which adds its ordinary backward to the tangent
 // part.
