@@ -118,3 +118,39 @@ def test_conservative_gradient_differs_from_direct_heads(case):
             assert np.all(tg[o:o + n] == 0.0), name
     o, s = lay["L0_av_W"]
     assert np.abs(tg[o:o + int(np.prod(s))]).max() > 0
+
+
+@pytest.mark.parametrize("delta", [None, 0.4])
+def test_loss_gradient_is_the_tangent_of_the_weight_gradient(case, delta):
+    """The identity behind the forward-over-reverse GPU path: with the loss
+    gradients l_E, l_F, l_sigma of the outputs, the loss gradient through the
+    conservative readout equals d/dh at h = 0 of the first-order weight
+    gradient of sum_s (1 + h l_E,s) E_s at positions r - h l_F and strain
+    h l_sigma / V (central differences in h, fp64)."""
+    import torch
+
+    b, g, seed = case
+    hp = _hp(conservative=True)
+    p = _small_params(hp, seed)
+    targets = synth.make_targets(b, seed=(7, 2, 80 + seed))
+    _, tg = autodiff.loss_and_grad(hp, b, g, p, targets, delta=delta)
+    ix = autodiff._indices(b, g)
+    E, F, S, _, _ = autodiff.outputs(hp, b, g, p, create_graph=False, ix=ix)
+    E, F, S = (x.detach().requires_grad_(True) for x in (E, F, S))
+    Et, Ft, St = (torch.as_tensor(x, dtype=torch.float64) for x in targets[:3])
+    n = torch.as_tensor(ix["n_per"])
+    pw = lambda r: r * r if delta is None else torch.where(r.abs() <= delta, 0.5 * r * r, delta * (r.abs() - 0.5 * delta))
+    loss = 2.0 * pw(E / n - Et).mean() + 1.5 * pw(F - Ft).mean() + 0.1 * pw(S - St).mean()
+    lE, lF, lS = torch.autograd.grad(loss, (E, F, S))
+    vol = torch.abs(torch.linalg.det(torch.as_tensor(b.lattice, dtype=torch.float64)))
+    pos0 = torch.as_tensor(b.pos, dtype=torch.float64)
+
+    def weight_grad(h):
+        pt = torch.tensor(p, dtype=torch.float64, requires_grad=True)
+        En, _, _, _ = autodiff.forward(hp, b, g, pt, pos=pos0 - h * lF, strain=h * lS / vol[:, None, None], ix=ix)
+        (gr,) = torch.autograd.grad(((1.0 + h * lE) * En).sum(), pt)
+        return gr.numpy()
+
+    h = 1e-5
+    tangent = (weight_grad(h) - weight_grad(-h)) / (2 * h)
+    np.testing.assert_allclose(tangent, tg, rtol=1e-5, atol=1e-7 * np.abs(tg).max())
