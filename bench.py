@@ -514,7 +514,8 @@ def cpu_baseline(workload, sample, min_seconds=10.0, variant=None):
             "host_cpus": len(os.sched_getaffinity(0)), "edges_per_s": round(reps * n_edges / dt, 1),
             "sample": "%d of the %d structures (%d atoms), %d %s in %.1f s"
                       % (sample, b.n_struct, n, reps, "inference(s) (graph, forward)" if fwd
-                         else "full step(s) (graph, forward, loss, backward)", dt)}
+                         else "full step(s) (graph, forward, loss, backward through F = -dE/dr by autograd)"
+                         if hp.conservative else "full step(s) (graph, forward, loss, backward)", dt)}
 
 
 if __name__ == "__main__":
