@@ -626,7 +626,19 @@ __global__ void __launch_bounds__(256, 3) k_tn(TnLaunch L, float* __restrict__ p
   const TnPlan& Q = L.q[k];
   const int lb = blockIdx.x - Q.block0;
   const int tiles = max(Q.tiles_m, 1) * Q.tiles_n;
-  const int chunk = lb / tiles, tile = lb % tiles;
+  // The tiles of a row chunk sit 8 block indices apart, so that they run on
+  // one XCD (blocks are dealt to the 8 XCDs in turn) and share its L2 for the
+  // chunk's rows; chunks after the last full group of 8 keep consecutive tiles.
+  const int grouped = (Q.nchunks / 8) * 8 * tiles;
+  int chunk, tile;
+  if (lb < grouped) {
+    const int g = lb / (8 * tiles), rem = lb % (8 * tiles);
+    tile = rem / 8;
+    chunk = g * 8 + rem % 8;
+  } else {
+    chunk = (Q.nchunks / 8) * 8 + (lb - grouped) / tiles;
+    tile = (lb - grouped) % tiles;
+  }
   const int tm = tile / Q.tiles_n, tn = tile % Q.tiles_n;
   const int m0 = tm * 32 * Q.vx, n0 = tn * 32 * Q.vy;
   const bool colsum = Q.has_bias && tm == 0;
