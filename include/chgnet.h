@@ -102,10 +102,14 @@ typedef struct {
 
 /* Atom graph G^a, bond graph G^b and angle list (Sec. II-B (1)).
  *  Edges: all directed (i, j, n) with i, j in one crystal, n in Z^3,
- *   (i,j,n) != (i,i,0) and D2 < r_atom^2, where D2 is the fp32 expression
- *      s_c = ((n1*L1c) + (n2*L2c)) + (n3*L3c);  dl_c = (r_jc + s_c) - r_ic;
+ *   (i,j,n) != (i,i,0) and D2 < r_atom^2. D2 is evaluated in the canonical
+ *   orientation (p, q, m) of the pair {(i, j, n), (j, i, -n)}: p < q, or
+ *   p = q with m lexicographically positive (first non-zero component > 0).
+ *   It is the fp32 expression
+ *      s_c = ((m1*L1c) + (m2*L2c)) + (m3*L3c);  dl_c = (r_qc + s_c) - r_pc;
  *      D2  = ((dl_x*dl_x) + (dl_y*dl_y)) + (dl_z*dl_z)
- *   evaluated with one round-to-nearest per operation (no fused multiply-add).
+ *   with one round-to-nearest per operation (no fused multiply-add), so both
+ *   directions of a pair get the same D2 and every edge has its reverse.
  *   Every translation is kept (no truncation). Order: CSR by i, then by j,
  *   then (n1, n2, n3) lexicographically.
  *  Bonds: the edges with D2 < r_bond^2, in edge order.

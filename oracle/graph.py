@@ -10,16 +10,24 @@ Definitions (Sec. II-B (1) of the paper; cutoffs from Sec. IV, "Dataset"):
   centre atom.
 
 Reading (the paper does not say how the cutoff test is rounded): the test is
-the fp32 expression
+an fp32 expression evaluated in one fixed orientation of each pair. The two
+directions (i, j, n) and (j, i, -n) of a pair describe one separation; the
+canonical one is (i, j, n) with i < j, or, for i = j, with n
+lexicographically positive (first non-zero component > 0). With (p, q, m)
+the canonical orientation of the edge being tested,
 
-    s_c  = ((n1*L1c) + (n2*L2c)) + (n3*L3c)
-    dl_c = (r_jc + s_c) - r_ic
+    s_c  = ((m1*L1c) + (m2*L2c)) + (m3*L3c)
+    dl_c = (r_qc + s_c) - r_pc
     D2   = ((dl_x*dl_x) + (dl_y*dl_y)) + (dl_z*dl_z)
 
 with one IEEE round-to-nearest per operation and no fused multiply-add, and
-an edge exists iff D2 < rc*rc (strict). This makes the edge set exactly
-reproducible. Every translation satisfying the test is kept (no truncation of
-the image range); the per-pair enumeration range below is generous.
+an edge exists iff D2 < rc*rc (strict). Both directions therefore get the
+same D2, so an edge's reverse always exists (the plain expression
+(r_j + s) - r_i rounds differently from (r_i - s) - r_j, and near the
+cutoff one direction can pass while the other fails). This makes the edge
+set exactly reproducible. Every translation satisfying the test is kept (no
+truncation of the image range); the per-pair enumeration range below is
+generous.
 
 Canonical order: edges grouped by source atom i (CSR), then by j, then by
 (n1, n2, n3) lexicographically. rev(i, j, n) = (j, i, -n). Bonds keep G^a
@@ -39,20 +47,46 @@ def interplanar_spacings(L):
 
 
 def fp32_d2(ri, rj, n, L):
-    """The fp32 cutoff expression, vectorised over leading axes of rj and n.
+    """The fp32 expression ((r_j + s) - r_i)^2 summed over x, y, z, with
+    s = n L, vectorised over leading axes of rj and n (one orientation).
 
-    ri: float32 [3]; rj: float32 [..., 3]; n: int [..., 3]; L: float32 [3, 3].
-    Every operation is a separate float32 ufunc, so each rounds once."""
+    ri: float32 [..., 3] or [3]; rj: float32 [..., 3]; n: int [..., 3];
+    L: float32 [3, 3]. Every operation is a separate float32 ufunc, so each
+    rounds once."""
     nf = n.astype(np.float32)
     L = L.astype(np.float32)
-    d2 = None
+    ri = np.asarray(ri, np.float32)
     dl = []
     for c in range(3):
         s = (nf[..., 0] * L[0, c] + nf[..., 1] * L[1, c]) + nf[..., 2] * L[2, c]
-        dl.append((rj[..., c] + s) - ri[c])
+        dl.append((rj[..., c] + s) - ri[..., c])
     d2 = (dl[0] * dl[0] + dl[1] * dl[1]) + dl[2] * dl[2]
     assert d2.dtype == np.float32
     return d2
+
+
+def is_canonical(i, j, n):
+    """True where (i, j, n) is the canonical orientation of its pair: i < j,
+    or i = j and n lexicographically positive. Vectorised over i, j, n[..., 3]."""
+    n = np.asarray(n)
+    lexpos = (n[..., 0] > 0) | ((n[..., 0] == 0) & ((n[..., 1] > 0) | ((n[..., 1] == 0) & (n[..., 2] > 0))))
+    i = np.asarray(i)
+    j = np.asarray(j)
+    return (i < j) | ((i == j) & lexpos)
+
+
+def pair_d2(i, j, n, pos32, L):
+    """The cutoff test's D2 of edges (i, j, n): the fp32 expression evaluated
+    in the canonical orientation of each pair, so that D2(i, j, n) equals
+    D2(j, i, -n) bit for bit. i, j int [...]; n int [..., 3]."""
+    i = np.asarray(i)
+    j = np.asarray(j)
+    n = np.asarray(n)
+    canon = is_canonical(i, j, n)
+    p = np.where(canon, i, j)
+    q = np.where(canon, j, i)
+    m = np.where(canon[..., None], n, -n)
+    return fp32_d2(pos32[p], pos32[q], m, L)
 
 
 def _edges_of_atom(i, a0, a1, pos32, L32, frac, h, rc):
@@ -74,7 +108,7 @@ def _edges_of_atom(i, a0, a1, pos32, L32, frac, h, rc):
     valid = (grid[None, :, :] < cnt[:, None, :]).all(axis=2)
     J = np.broadcast_to(js[:, None], valid.shape)[valid]
     Nimg = Nimg[valid]
-    d2 = fp32_d2(pos32[i], pos32[J], Nimg, L32)
+    d2 = pair_d2(np.full(J.shape, i), J, Nimg, pos32, L32)
     keep = d2 < rc2
     keep &= ~((J == i) & (Nimg == 0).all(axis=1))
     J, Nimg, d2 = J[keep], Nimg[keep], d2[keep]

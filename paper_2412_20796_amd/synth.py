@@ -214,6 +214,42 @@ def random_crystals(seed: int, n_struct: int, n_lo: int, n_hi: int, rho=(0.07, 0
     return _assemble(structs, Zs)
 
 
+def boundary_batch(kind: str) -> Batch:
+    """Crystals with one pair placed within a few fp32 ulps of a cutoff, in
+    fp32 Cartesian coordinates (no rounding through fractional coordinates).
+
+    * ``"atom"``: cubic a = 4.3, atoms at (x0, 1, 1) and (x1, 1, 1) with x1
+      stepped by single ulps around x0 + 1.7, so the pair through the
+      translation (1, 0, 0) is 6 A long (direct distance 1.7 A).
+    * ``"bond"``: cubic a = 4.6, x1 around x0 - 1.6, so the pair through
+      (1, 0, 0) is 3 A long (direct distance 1.6 A).
+    * ``"self"``: one atom at (x0, 1, 1) in a cubic cell whose edge is
+      stepped by ulps around 6 A (the atom's own images at the cutoff)."""
+    f32 = np.float32
+    lat, pos, ptr = [], [], [0]
+    for x0 in (0.3, 1.1, 2.189443, 3.0):
+        x0 = f32(x0)
+        for k in range(-6, 7):
+            if kind == "self":
+                a = f32(6.0)
+                for _ in range(abs(k)):
+                    a = np.nextafter(a, f32(np.sign(k) * 10.0))
+                lat.append(np.eye(3, dtype=np.float32) * a)
+                pos.append(np.array([[x0, 1.0, 1.0]], np.float32))
+            else:
+                a, off = (f32(4.3), f32(1.7)) if kind == "atom" else (f32(4.6), f32(-1.6))
+                x1 = f32(x0 + off)
+                for _ in range(abs(k)):
+                    x1 = np.nextafter(x1, f32(np.sign(k) * 100.0))
+                lat.append(np.eye(3, dtype=np.float32) * a)
+                pos.append(np.array([[x0, 1.0, 1.0], [x1, 1.0, 1.0]], np.float32))
+            ptr.append(ptr[-1] + len(pos[-1]))
+    rng = np.random.default_rng([98, 0, len(kind)])
+    P = np.concatenate(pos)
+    return Batch(np.asarray(ptr, np.int32), P, np.stack(lat).astype(np.float32),
+                 rng.integers(1, N_ELEMENTS + 1, size=len(P)).astype(np.int32))
+
+
 # --------------------------------------------------------------------------
 # Initial weights. The flat layout is the one documented in include/chgnet.h;
 # this listing is used only to pick each tensor's initial distribution.

@@ -81,7 +81,10 @@ def test_lattice_point_counts(kind, a):
 
 
 def _scalar_bruteforce(atom_ptr, pos, lat, rc, reach=6):
-    """Pure-Python enumeration over a very wide image box, scalar fp32."""
+    """Pure-Python enumeration over a very wide image box, scalar fp32, each
+    pair's separation taken in its canonical orientation (lower atom index
+    first; for an atom's own images, the translation whose first non-zero
+    component is positive)."""
     out = []
     f32 = np.float32
     for s in range(len(atom_ptr) - 1):
@@ -91,10 +94,15 @@ def _scalar_bruteforce(atom_ptr, pos, lat, rc, reach=6):
                 for n in itertools.product(range(-reach, reach + 1), repeat=3):
                     if i == j and n == (0, 0, 0):
                         continue
+                    first = next(x for x in n if x != 0) if any(n) else 0
+                    if i < j or (i == j and first > 0):
+                        p, q, m = i, j, n
+                    else:
+                        p, q, m = j, i, tuple(-x for x in n)
                     dl = []
                     for c in range(3):
-                        sc = f32(f32(f32(n[0]) * L[0, c]) + f32(f32(n[1]) * L[1, c])) + f32(f32(n[2]) * L[2, c])
-                        dl.append(f32(f32(pos[j, c] + f32(sc)) - pos[i, c]))
+                        sc = f32(f32(f32(m[0]) * L[0, c]) + f32(f32(m[1]) * L[1, c])) + f32(f32(m[2]) * L[2, c])
+                        dl.append(f32(f32(pos[q, c] + f32(sc)) - pos[p, c]))
                     d2 = f32(f32(dl[0] * dl[0]) + f32(dl[1] * dl[1])) + f32(dl[2] * dl[2])
                     if d2 < f32(rc * rc):
                         out.append((i, j) + tuple(n))
@@ -168,3 +176,86 @@ def test_sampled_rows_match_full_build():
         lo, hi = g["edge_ptr"][i], g["edge_ptr"][i + 1]
         np.testing.assert_array_equal(dst, g["edge_dst"][lo:hi])
         np.testing.assert_array_equal(img, g["edge_img"][lo:hi])
+
+
+def _edge_tuples(g):
+    src = np.repeat(np.arange(len(g["edge_ptr"]) - 1), np.diff(g["edge_ptr"]))
+    return [(int(src[e]), int(g["edge_dst"][e])) + tuple(int(x) for x in g["edge_img"][e]) for e in range(len(src))]
+
+
+def _assert_reverse_total(g):
+    """Every edge (i, j, n) has its reverse (j, i, -n), and edge_rev names it."""
+    src = np.repeat(np.arange(len(g["edge_ptr"]) - 1), np.diff(g["edge_ptr"]))
+    rev = g["edge_rev"]
+    assert (rev[rev] == np.arange(len(rev))).all()
+    assert (g["edge_dst"][rev] == src).all() and (src[rev] == g["edge_dst"]).all()
+    np.testing.assert_array_equal(g["edge_img"][rev], -g["edge_img"])
+    ed = set(_edge_tuples(g))
+    assert all((t[1], t[0], -t[2], -t[3], -t[4]) in ed for t in ed)
+    # bond graph closed under reversal, D2 equal in both directions
+    be = set(g["bond_edge"].tolist())
+    assert all(int(rev[b]) in be for b in be)
+    np.testing.assert_array_equal(g["edge_d2"][rev], g["edge_d2"])
+
+
+def test_golden_reverse_pair_cell():
+    """A pair 1 fp32 ulp inside the cutoff in one orientation and exactly on it
+    in the other (golden fixture): both directions are edges."""
+    from fractions import Fraction
+
+    with open(os.path.join(GOLDEN, "reverse_pair_cell.json")) as f:
+        c = json.load(f)
+    a = np.float32(c["lattice_a"])
+    pos = np.asarray(c["pos"], np.float32)
+    g = graph.build_graph(np.array([0, 2]), pos, (np.eye(3, dtype=np.float32) * a)[None])
+    _assert_reverse_total(g)
+    got = set(_edge_tuples(g))
+    for t in c["boundary_edges"]:
+        assert tuple(t) in got, t
+    assert len(got) == c["edges"]
+    # away from the boundary, membership follows exact rational arithmetic
+    A = Fraction(float(a))
+    P = [[Fraction(float(x)) for x in r] for r in pos]
+    away = 0
+    for i in range(2):
+        for j in range(2):
+            for n in itertools.product(range(-3, 4), repeat=3):
+                if i == j and n == (0, 0, 0):
+                    continue
+                d2 = sum((P[j][k] + n[k] * A - P[i][k]) ** 2 for k in range(3))
+                if abs(d2 - 36) > Fraction(1, 1000):
+                    assert ((i, j) + n in got) == (d2 < 36), (i, j, n)
+                    away += d2 < 36
+    assert away == c["edges_away_from_boundary"]
+
+
+@pytest.mark.parametrize("kind", ["atom", "bond", "self"])
+def test_boundary_sweeps_keep_reverse_edges(kind):
+    """Pairs stepped ulp by ulp across the 6 A and 3 A cutoffs (through a
+    lattice translation, and an atom's own images): every edge has its
+    reverse, the bonds are closed under reversal, and the edge set equals a
+    scalar brute force. The sweep includes pairs whose two one-orientation
+    evaluations fall on opposite sides of the cutoff, so a test in one
+    orientation only would fail here."""
+    b = synth.boundary_batch(kind)
+    g = graph.build_graph(b.atom_ptr, b.pos, b.lattice)
+    _assert_reverse_total(g)
+    assert _edge_tuples(g) == sorted(_scalar_bruteforce(b.atom_ptr, b.pos, b.lattice, 6.0, reach=2))
+    rc2 = np.float32(9.0 if kind == "bond" else 36.0)
+    split = 0
+    for s in range(b.n_struct):
+        a0, a1 = b.atom_ptr[s], b.atom_ptr[s + 1]
+        for i in range(a0, a1):
+            for j in range(a0, a1):
+                n = np.array([[1, 0, 0]])
+                fwd = graph.fp32_d2(b.pos[i], b.pos[j][None], n, b.lattice[s])[0]
+                bwd = graph.fp32_d2(b.pos[j], b.pos[i][None], -n, b.lattice[s])[0]
+                split += (fwd < rc2) != (bwd < rc2)
+    assert split > 0
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_random_cells_reverse_total(seed):
+    """No guard band: random triclinic cells, every edge has its reverse."""
+    b = synth.random_crystals(seed=300 + seed, n_struct=4, n_lo=2, n_hi=24, rho=(0.06, 0.12))
+    _assert_reverse_total(graph.build_graph(b.atom_ptr, b.pos, b.lattice))
