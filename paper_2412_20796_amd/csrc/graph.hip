@@ -27,7 +27,7 @@ constexpr float kMaxCoord = 1.0e4f;   // max |Cartesian coordinate|
 constexpr int kMaxEdgesPerAtom = 8192;
 constexpr int kImgBias = 512;         // image components stored as n + 512 in 10 bits
 
-enum ErrBits { ERR_Z = 1, ERR_DET = 2, ERR_THIN = 4, ERR_FAR = 8, ERR_REV = 16, ERR_PTR = 32 };
+enum ErrBits { ERR_Z = 1, ERR_DET = 2, ERR_THIN = 4, ERR_FAR = 8, ERR_PTR = 32 };
 
 struct StructInfo {
   double Linv[9];
@@ -45,17 +45,27 @@ struct GraphInfo {
 };
 
 // ---------------------------------------------------------------------------
-// The exact fp32 cutoff expression: one rounding per operation, no FMA.
+// The exact fp32 cutoff expression: one rounding per operation, no FMA,
+// evaluated in the canonical orientation of the pair {(i, j, n), (j, i, -n)}
+// (i < j, or i = j with n lexicographically positive). (r_j + s) - r_i and
+// (r_i - s) - r_j round differently, so without a fixed orientation an edge
+// near the cutoff could pass while its reverse fails; with it both directions
+// get the same D2 and every edge has its reverse.
 // ---------------------------------------------------------------------------
-__device__ __forceinline__ float pair_d2(const float* ri, const float* rj, int n1, int n2, int n3, const float* L) {
+__device__ __forceinline__ float pair_d2(int i, int j, const float* ri, const float* rj, int n1, int n2, int n3,
+                                         const float* L) {
 #pragma clang fp contract(off)
-  const float f1 = (float)n1, f2 = (float)n2, f3 = (float)n3;
+  const bool canon = i < j || (i == j && (n1 > 0 || (n1 == 0 && (n2 > 0 || (n2 == 0 && n3 > 0)))));
+  const float sg = canon ? 1.0f : -1.0f;  // exact: m = sg * n
+  const float f1 = sg * (float)n1, f2 = sg * (float)n2, f3 = sg * (float)n3;
   const float sx = (f1 * L[0] + f2 * L[3]) + f3 * L[6];
   const float sy = (f1 * L[1] + f2 * L[4]) + f3 * L[7];
   const float sz = (f1 * L[2] + f2 * L[5]) + f3 * L[8];
-  const float dx = (rj[0] + sx) - ri[0];
-  const float dy = (rj[1] + sy) - ri[1];
-  const float dz = (rj[2] + sz) - ri[2];
+  const float px = canon ? ri[0] : rj[0], py = canon ? ri[1] : rj[1], pz = canon ? ri[2] : rj[2];
+  const float qx = canon ? rj[0] : ri[0], qy = canon ? rj[1] : ri[1], qz = canon ? rj[2] : ri[2];
+  const float dx = (qx + sx) - px;
+  const float dy = (qy + sy) - py;
+  const float dz = (qz + sz) - pz;
   return (dx * dx + dy * dy) + dz * dz;
 }
 
@@ -312,7 +322,7 @@ __device__ __forceinline__ void block_search(const SearchArgs& A, int i, SearchS
       const int n2 = sh.m[lo][1] - A.atom_wrap[j * 3 + 1] + wi[1];
       const int n3 = sh.m[lo][2] - A.atom_wrap[j * 3 + 2] + wi[2];
       const float rj[3] = {A.pos[j * 3 + 0], A.pos[j * 3 + 1], A.pos[j * 3 + 2]};
-      const float dd = pair_d2(ri, rj, n1, n2, n3, L);
+      const float dd = pair_d2(i, j, ri, rj, n1, n2, n3, L);
       if (dd < A.rc2_atom && !(j == i && n1 == 0 && n2 == 0 && n3 == 0)) f(j, n1, n2, n3, dd);
     }
     __syncthreads();
@@ -466,9 +476,13 @@ __global__ void __launch_bounds__(kSearchThreads) k_fill(SearchArgs A, int sort_
   }
 }
 
-// Reverse map: binary search of (i, -n) in the sorted edge list of j.
+// Reverse map: binary search of (i, -n) in the sorted edge list of j. The
+// search always succeeds: D2 is the same number in both directions (see
+// pair_d2), and the cell list of j holds i at -n whenever that of i holds j
+// at n (both cover every pair closer than r + kMargin, while D2 < r^2 implies
+// a separation within fp32 rounding of r). The fallback value is never used.
 __device__ __forceinline__ void rev_atoms(int blk, int N, const int* __restrict__ edge_ptr, const int* __restrict__ edge_dst,
-                                          const int* __restrict__ edge_img, int* __restrict__ edge_rev, GraphInfo* ginfo) {
+                                          const int* __restrict__ edge_img, int* __restrict__ edge_rev) {
   const int i = blk * 4 + (threadIdx.x >> 6);
   if (i >= N) return;
   const int lane = threadIdx.x & 63;
@@ -484,7 +498,6 @@ __device__ __forceinline__ void rev_atoms(int blk, int N, const int* __restrict_
       if (cmp == 0) { found = mid; break; }
       if (cmp < 0) lo = mid + 1; else hi = mid - 1;
     }
-    if (found < 0) atomicOr(&ginfo->err, ERR_REV);
     edge_rev[e] = found < 0 ? e : found;
   }
 }
@@ -513,12 +526,11 @@ __device__ __forceinline__ void angle_atoms(int blk, int N, const int* __restric
 // reverse edges of atoms 4 b .. 4 b + 3, blocks [nb, 2 nb) their angle lists.
 __global__ void __launch_bounds__(256) k_rev_angles(int N, const int* __restrict__ edge_ptr,
                                                     const int* __restrict__ edge_dst, const int* __restrict__ edge_img,
-                                                    int* __restrict__ edge_rev, GraphInfo* ginfo,
-                                                    const int* __restrict__ bond_ptr,
+                                                    int* __restrict__ edge_rev, const int* __restrict__ bond_ptr,
                                                     const long long* __restrict__ angle_base, int* __restrict__ angle_ptr,
                                                     int* __restrict__ angle_b2) {
   const int nb = (N + 3) / 4;
-  if ((int)blockIdx.x < nb) rev_atoms(blockIdx.x, N, edge_ptr, edge_dst, edge_img, edge_rev, ginfo);
+  if ((int)blockIdx.x < nb) rev_atoms(blockIdx.x, N, edge_ptr, edge_dst, edge_img, edge_rev);
   else angle_atoms(blockIdx.x - nb, N, bond_ptr, angle_base, angle_ptr, angle_b2);
 }
 
@@ -649,7 +661,7 @@ int build_graph(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_grap
   KLAUNCH(st, "k_fill", k_fill<<<N, kSearchThreads, sizeof(unsigned long long) * sort_size, st>>>(A, sort_size, graph->edge_ptr, graph->bond_ptr,
                                                                 graph->edge_dst, graph->edge_img, graph->bond_edge));
   KLAUNCH(st, "k_rev_angles", k_rev_angles<<<2 * cdiv(N, 4), 256, 0, st>>>(N, graph->edge_ptr, graph->edge_dst, graph->edge_img,
-                                                                       graph->edge_rev, g.ginfo, graph->bond_ptr, g.angle_base,
+                                                                       graph->edge_rev, graph->bond_ptr, g.angle_base,
                                                                        graph->angle_ptr, graph->angle_b2));
   return CHGNET_OK;
 }

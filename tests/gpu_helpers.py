@@ -1,4 +1,7 @@
 """Shared helpers of the GPU parity tests (no model arithmetic here)."""
+import json
+import os
+
 import numpy as np
 
 GRAPH_KEYS = ("edge_ptr", "edge_dst", "edge_img", "edge_rev", "bond_ptr", "bond_edge", "angle_ptr", "angle_b2")
@@ -39,3 +42,13 @@ def subset_batch(batch, structs):
         lat.append(batch.lattice[s])
         ptr.append(ptr[-1] + a1 - a0)
     return Batch(np.asarray(ptr, np.int32), np.concatenate(pos), np.stack(lat), np.concatenate(Z))
+
+
+def golden_reverse_pair_cell():
+    """The two-atom cell of tests/golden/reverse_pair_cell.json as a batch."""
+    from paper_2412_20796_amd.synth import Batch
+
+    with open(os.path.join(os.path.dirname(__file__), "golden", "reverse_pair_cell.json")) as f:
+        c = json.load(f)
+    L = (np.eye(3, dtype=np.float32) * np.float32(c["lattice_a"]))[None]
+    return Batch(np.array([0, 2], np.int32), np.asarray(c["pos"], np.float32), L, np.array([8, 25], np.int32)), c

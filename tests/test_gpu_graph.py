@@ -3,7 +3,7 @@ arrays (canonical order), on the seeded workloads and on degenerate cells."""
 import numpy as np
 import pytest
 
-from gpu_helpers import assert_graph_equal, subset_batch
+from gpu_helpers import assert_graph_equal, golden_reverse_pair_cell, subset_batch
 from oracle import graph as og
 from paper_2412_20796_amd import synth
 
@@ -153,3 +153,29 @@ def test_build_is_deterministic(bd):
     g1, _ = gpu_graph(bd, b)
     g2, _ = gpu_graph(bd, b)
     assert_graph_equal(g1, g2)
+
+
+def test_reverse_pair_cell_bit_exact(bd):
+    """The pair whose one-orientation D2 is 36 - 1 ulp one way and 36 the other
+    (golden fixture): both directions are edges and each is the other's reverse."""
+    b, c = golden_reverse_pair_cell()
+    got, g = gpu_graph(bd, b)
+    ref = og.build_graph(b.atom_ptr, b.pos, b.lattice)
+    assert g.n_edges == c["edges"]
+    assert_graph_equal(got, ref)
+    src = np.repeat(np.arange(2), np.diff(got["edge_ptr"]))
+    img = got["edge_img"].reshape(-1, 3)
+    tup = [(int(src[e]), int(got["edge_dst"][e])) + tuple(int(x) for x in img[e]) for e in range(len(src))]
+    e0, e1 = tup.index(tuple(c["boundary_edges"][0])), tup.index(tuple(c["boundary_edges"][1]))
+    assert got["edge_rev"][e0] == e1 and got["edge_rev"][e1] == e0
+
+
+@pytest.mark.parametrize("kind", ["atom", "bond", "self"])
+def test_boundary_sweeps_bit_exact(bd, kind):
+    """Pairs stepped ulp by ulp across the 6 A and 3 A cutoffs: bit-exact
+    graphs, and every edge is the reverse of its reverse."""
+    b = synth.boundary_batch(kind)
+    got, _ = gpu_graph(bd, b)
+    assert_graph_equal(got, og.build_graph(b.atom_ptr, b.pos, b.lattice))
+    rev = got["edge_rev"]
+    assert (rev[rev] == np.arange(len(rev))).all()

@@ -4,7 +4,7 @@ loss and every parameter gradient; bitwise run-to-run reproducibility."""
 import numpy as np
 import pytest
 
-from gpu_helpers import assert_close, assert_graph_equal, subset_batch
+from gpu_helpers import assert_close, assert_graph_equal, golden_reverse_pair_cell, subset_batch
 from oracle import graph as og
 from oracle import model as om
 from paper_2412_20796_amd import synth
@@ -74,6 +74,24 @@ def test_step_parity_random_small_batches(bd):
         params = synth.make_params(64, 3, seed=(9, 1, seed))
         targets = synth.make_targets(b, seed=(9, 2, seed))
         _check_step(bd, b, params, targets, 64, 3, "random%d" % seed)
+
+
+def test_step_parity_cutoff_pairs(bd):
+    """Cells with a pair one fp32 ulp from the 6 A or 3 A cutoff (the golden
+    two-atom cell and ulp sweeps): step parity, and the net force of every
+    crystal is zero (Eq. 8 with the symmetrised edge scalars)."""
+    b0, _ = golden_reverse_pair_cell()
+    for name, b in [("reverse-pair", b0), ("sweep-atom", synth.boundary_batch("atom")),
+                    ("sweep-bond", synth.boundary_batch("bond"))]:
+        params = synth.make_params(64, 3, seed=(6, 1, len(name)))
+        _check_step(bd, b, params, synth.make_targets(b, seed=(6, 2, len(name))), 64, 3, name)
+        hp, db, g, ws = _setup(bd, b, 64, 3)
+        _, F, _ = bd.forward(hp, db, g, _dev(params), ws)
+        F = F.cpu().numpy().astype(np.float64)
+        for s in range(b.n_struct):
+            net = F[b.atom_ptr[s]:b.atom_ptr[s + 1]].sum(0)
+            scale = np.abs(F[b.atom_ptr[s]:b.atom_ptr[s + 1]]).max() + 1e-30
+            assert np.abs(net).max() <= 1e-5 * scale + 1e-6, (name, s, net)
 
 
 def test_step_parity_sparse_cells(bd):
