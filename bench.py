@@ -7,8 +7,9 @@ Inputs (positions, lattices, atomic numbers, targets, weights) are seeded and
 synthetic (the dataset is not available) and are resident in HBM before the
 timed region.
 
-Prints one JSON line (rank 0). Default workload: 40 random triclinic crystals
-with 8-64 atoms each, d = 64, 4 layers.
+Prints one JSON line (rank 0). Default workload: wide128, 128 random
+triclinic crystals with 8-128 atoms each (log-uniform), d = 128, 5 layers
+(the largest single-GPU configuration); the others are chosen by --workload.
 """
 from __future__ import annotations
 
@@ -30,7 +31,7 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="triclinic40")
+    ap.add_argument("--workload", default="wide128")
     ap.add_argument("--magmom", action="store_true", help="model variant: magnetic-moment head and its loss term")
     ap.add_argument("--huber", type=float, default=0.0, help="model variant: Huber loss with this delta (0 = MSE)")
     ap.add_argument("--sequential", action="store_true", help="model variant: the Eq. (10) interaction block")
@@ -39,7 +40,9 @@ def parse():
     ap.add_argument("--forward-only", action="store_true",
                     help="time inference (graph build + forward with the readout) instead of training steps")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-sample", type=int, default=0, help="structures in the CPU oracle sample (0 = auto)")
+    ap.add_argument("--cpu-sample", type=int, default=0,
+                    help="structures in the CPU oracle sample (0 = auto: the whole batch, or for wide128 four "
+                         "structures at evenly spaced size quantiles)")
     ap.add_argument("--no-roofline", action="store_true")
     ap.add_argument("--launch-timing-only", action="store_true",
                     help="warm-up and timed steps all with per-launch timing (the library's side stream then runs "
@@ -136,8 +139,9 @@ def main():
         ev[k + 1].record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
-    ms = ev[0].elapsed_time(ev[-1]) / args.steps
+    ms_mean = ev[0].elapsed_time(ev[-1]) / args.steps
     per_step = np.array([ev[k].elapsed_time(ev[k + 1]) for k in range(args.steps)])
+    ms = float(np.median(per_step))
     S = b.n_struct
     value = S / (ms * 1e-3)
 
@@ -155,6 +159,7 @@ def main():
         "vs_baseline": None,
         "dtype": "fp32",
         "data": "synthetic (seeded crystals shaped like the paper's training set; random-init weights)",
+        "timing": "median of per-step HIP events over the timed steps (mean in ms_per_step_mean)",
         "config": {"workload": args.workload, "structures": S, "atoms": b.n_atoms, "edges": E, "bonds": B,
                    "angles": A, "d": d, "layers": T, "parallelism": "single GPU",
                    "block": "Eq. 10 (sequential)" if args.sequential else "Eq. 11",
@@ -164,7 +169,7 @@ def main():
                    "step": "graph + forward" if args.forward_only else "graph + forward + loss + backward + Adam"},
         "edges_per_s": round(E / (ms * 1e-3), 1),
         "angles_per_s": round(A / (ms * 1e-3), 1),
-        "ms_per_step_median": round(float(np.median(per_step)), 4),
+        "ms_per_step_mean": round(ms_mean, 4),
         "ms_per_step_p10_p90": [round(float(np.percentile(per_step, 10)), 4),
                                 round(float(np.percentile(per_step, 90)), 4)],
         "wall_s_timed": round(wall, 3),
@@ -339,14 +344,41 @@ def algorithmic_cost(tag, z):
     return None, None
 
 
+def mandatory_cost(tag, z):
+    """The method's own memory traffic (the mandatory forward bytes per unit
+    and layer of the scope table: an edge reads e and e^a, 8d bytes; a bond
+    of the bond graph reads and writes e_b, 8d; an angle reads and writes a,
+    8d, plus 8 bytes of indices, or reads it only in the last layer, 4d + 8;
+    atoms are negligible), attributed to the gate launch of each layer; the
+    backward gate moves twice the forward (activations in, their gradients
+    out). Dense products keep their flop count (the split GEMMs are the
+    method's arithmetic). None where a kernel moves only this design's own
+    intermediates."""
+    bound, work = algorithmic_cost(tag, z)
+    if bound == "mfma":
+        return bound, work
+    N, E, B, A, D, T = z["N"], z["E"], z["B"], z["A"], z["D"], z["T"]
+    lay = E * 8 * D + B * 8 * D + A * (8 * D + 8)
+    last = E * 8 * D + B * 8 * D + A * (4 * D + 8)
+    if tag == "k_gate_fwd":
+        return "hbm", (T - 1) * lay + last
+    if tag == "k_gate_bwd":
+        return "hbm", 2 * ((T - 1) * lay + last)
+    return None, None
+
+
 # rocprofv3 kernel symbol of each launch tag that has an algorithmic cost
-TAG_SYMBOL = {
-    "gemm_z": "k_gemm<64, 1>",
-    "gemm_in_bwd": "k_gemm<64, 2>",
-    "tn_in": "k_tn<1>",
-    "k_gate_fwd": "k_gate_fwd_mm",
-    "k_gate_bwd": "k_gate_bwd_mm",
-}
+# (the gate kernels depend on the width: fused product-and-gate kernels at
+# d = 64, row-gate kernels after a separate product at d = 128)
+def tag_symbol(tag, d):
+    return {
+        "gemm_z": "k_gemm<64, 1>",
+        "gemm_in_bwd": "k_gemm<64, 2>",
+        "tn_in": "k_tn<1>",
+        "k_gate_fwd": "k_gate_fwd_mm" if d == 64 else "k_gate_fwd<128>",
+        "k_gate_bwd": "k_gate_bwd_mm" if d == 64 else "k_gate_bwd<128>",
+    }.get(tag)
+
 
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_%s.md")
 SOURCE_DIR = os.path.join(ROOT, "paper_2412_20796_amd", "csrc")
@@ -368,7 +400,9 @@ def measured_traffic(workload, tag):
     """HBM bytes per launch of `tag` from the committed counter summary, or
     None if there is none for this workload, the kernel, or these sources."""
     path = TRAFFIC_FILE % workload
-    sym = TAG_SYMBOL.get(tag)
+    from paper_2412_20796_amd import synth
+
+    sym = tag_symbol(tag, synth.WORKLOADS.get(workload, (0, 64, 0))[1])
     if sym is None or not os.path.exists(path):
         return None
     text = open(path).read()
@@ -427,9 +461,13 @@ def traffic_summary(fetch_csv, write_csv, workload, command):
 
 
 def roofline(prof, steps, z):
+    """Per-tag rates from the per-launch HIP events. `achieved` and `frac`
+    count the method's mandatory work (mandatory_cost); the design_* fields
+    count every array this implementation reads or writes (algorithmic_cost)."""
     rows = []
     for tag, (n, ms) in prof.items():
         bound, work = algorithmic_cost(tag, z)
+        mbound, mwork = mandatory_cost(tag, z)
         per_step_ms = ms / steps
         row = {"tag": tag, "launches_per_step": n / steps, "ms_per_step": round(per_step_ms, 4),
                "avg_launch_us": round(1e3 * ms / max(n, 1), 2)}
@@ -439,29 +477,41 @@ def roofline(prof, steps, z):
                 ach = work / sec / 1e12
                 row.update(bound="mfma", achieved=round(ach, 3), unit="TFLOP/s", frac=round(ach / FP32_PEAK_TFLOPS, 4))
             else:
-                ach = work / sec / 1e9
-                row.update(bound="hbm", achieved=round(ach, 1), unit="GB/s", frac=round(ach / HBM_PEAK_GBS, 4))
+                dach = work / sec / 1e9
+                row.update(bound="hbm", unit="GB/s", design_achieved=round(dach, 1),
+                           design_frac=round(dach / HBM_PEAK_GBS, 4))
+                if mbound:
+                    ach = mwork / sec / 1e9
+                    row.update(achieved=round(ach, 1), frac=round(ach / HBM_PEAK_GBS, 4))
         rows.append(row)
     rows.sort(key=lambda r: -r["ms_per_step"])
-    dom = next(r for r in rows if "bound" in r)
+    dom = next(r for r in rows if "frac" in r)
     bound, work = algorithmic_cost(dom["tag"], z)
+    _, mwork = mandatory_cost(dom["tag"], z)
     n_launch = dom["launches_per_step"]
-    per_launch = work / n_launch
     rl = {"kernel": dom["tag"], "bound": dom["bound"], "achieved": dom["achieved"],
           "peak": FP32_PEAK_TFLOPS if dom["bound"] == "mfma" else HBM_PEAK_GBS, "unit": dom["unit"],
           "frac": dom["frac"], "traffic": measured_traffic(z["workload"], dom["tag"]),
-          "work_per_launch": per_launch, "work_unit": "flop" if bound == "mfma" else "byte",
+          "work_per_launch": mwork / n_launch, "work_unit": "flop" if bound == "mfma" else "byte",
+          "work_basis": "the method's mandatory work per unit (split-GEMM flops; gate bytes: e, e^a, e_b, a "
+                        "per layer), times the units of one launch",
+          "design_work_per_launch": work / n_launch,
           "traffic_unit": "bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
           "avg_launch_us": dom["avg_launch_us"], "launches_per_step": n_launch,
           "timing": "HIP events around every launch of the kernel on the library's stream, %d steps" % steps}
-    return rl, rows[:14]
+    if dom["bound"] == "hbm":
+        rl.update(design_achieved=dom["design_achieved"], design_frac=dom["design_frac"])
+    return rl, rows[:16]
 
 
 def cpu_baseline(workload, sample, min_seconds=10.0, variant=None):
     """The CPU oracle (fp64 NumPy, untuned) on a bounded sample of the same
-    workload: graph build, forward, loss and backward of the first `sample`
-    structures (default: the whole batch), repeated until min_seconds of CPU
-    work; reported in structures per second."""
+    workload: graph build, forward, loss and backward of `sample` structures
+    taken at evenly spaced quantiles of the batch's size distribution (default:
+    the whole batch, or four structures for wide128, whose full batch takes the
+    oracle tens of minutes), repeated until min_seconds of CPU work and at
+    least three times on the small workloads; reported in structures per
+    second of that sample."""
     import numpy as np
 
     from oracle import model as om
@@ -470,13 +520,19 @@ def cpu_baseline(workload, sample, min_seconds=10.0, variant=None):
     mag = bool(variant and variant.magmom)
     b, params, targets, d, T = synth.workload_inputs(workload, magmom=mag)
     if sample <= 0:
-        sample = b.n_struct
+        sample = 4 if workload == "wide128" else b.n_struct
+    sample = min(sample, b.n_struct)
+    sizes = np.diff(b.atom_ptr)
+    order = np.argsort(sizes, kind="stable")
+    picks = sorted(int(order[min(b.n_struct - 1, int((q + 0.5) * b.n_struct / sample))]) for q in range(sample))
     ptr = [0]
-    for s in range(sample):
-        ptr.append(ptr[-1] + int(b.atom_ptr[s + 1] - b.atom_ptr[s]))
+    for s in picks:
+        ptr.append(ptr[-1] + int(sizes[s]))
     n = ptr[-1]
-    sb = synth.Batch(np.asarray(ptr, np.int32), b.pos[:n], b.lattice[:sample], b.Z[:n])
-    tgt = (targets[0][:sample], targets[1][:n], targets[2][:sample]) + ((targets[3][:n],) if mag else ())
+    atoms = np.concatenate([np.arange(b.atom_ptr[s], b.atom_ptr[s + 1]) for s in picks])
+    sb = synth.Batch(np.asarray(ptr, np.int32), b.pos[atoms], b.lattice[picks], b.Z[atoms])
+    tgt = (targets[0][picks], targets[1][atoms], targets[2][picks]) + ((targets[3][atoms],) if mag else ())
+    min_reps = 3 if workload in ("cubic8", "triclinic40", "heavytail64") else 1
     fwd = bool(variant and variant.forward_only)
     hp = om.HParams(d=d, n_layers=T, magmom=mag, sequential=bool(variant and variant.sequential),
                     conservative=bool(variant and variant.conservative))
@@ -502,7 +558,7 @@ def cpu_baseline(workload, sample, min_seconds=10.0, variant=None):
         n_edges = len(graph["edge_dst"])
         reps += 1
         dt = time.perf_counter() - t
-        if dt >= min_seconds or reps >= 20:
+        if (dt >= min_seconds and reps >= min_reps) or reps >= 20:
             break
     try:
         from threadpoolctl import threadpool_info
@@ -512,8 +568,8 @@ def cpu_baseline(workload, sample, min_seconds=10.0, variant=None):
         threads = 1
     return {"value": round(reps * sample / dt, 4), "unit": "structures/s", "cores": threads, "kind": "oracle",
             "host_cpus": len(os.sched_getaffinity(0)), "edges_per_s": round(reps * n_edges / dt, 1),
-            "sample": "%d of the %d structures (%d atoms), %d %s in %.1f s"
-                      % (sample, b.n_struct, n, reps, "inference(s) (graph, forward)" if fwd
+            "sample": "%d of the %d structures (%d atoms, %d edges; evenly spaced size quantiles), %d %s in %.1f s"
+                      % (sample, b.n_struct, n, n_edges, reps, "inference(s) (graph, forward)" if fwd
                          else "full step(s) (graph, forward, loss, backward through F = -dE/dr by autograd)"
                          if hp.conservative else "full step(s) (graph, forward, loss, backward)", dt)}
 
