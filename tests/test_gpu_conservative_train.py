@@ -11,15 +11,17 @@ gradients on a sample of structures against the oracle on those structures
 alone (crystals of a batch are independent and the gradient is linear in
 the output gradients). The Eq. (10) block is refused with CHGNET_EINVAL.
 
-Tolerance per parameter tensor: |gpu - ref| <= 5e-5 m + 1e-3 |ref|, with m
+Tolerance per parameter tensor: |gpu - ref| <= 3e-5 m + 1e-4 |ref|, with m
 the larger of the tensor's max|ref| and 1e-2 of the whole gradient's (a
 tensor whose exact gradient vanishes, such as the energy bias when the
 energy errors of a batch cancel, is held to rounding of the whole sum).
-The fp32 path forms each gradient term as a product of a first derivative
-(as accurate as the direct-head gradients, about 1e-5 relative) with
-tangents that pass through the same chain once more, and sums terms of both
-signs over every edge and angle; the bound allows about twenty times the
-first-order tests' relative error against the tensor's scale."""
+The relative term is the first-order tests' 1e-4. The fp32 path forms each
+gradient term as a product of a first derivative (as accurate as the
+direct-head gradients, about 1e-5 relative) with tangents that pass through
+the same chain once more, and sums terms of both signs over every edge and
+angle, so its absolute error scales with the tensor's largest entry rather
+than with each entry: measured at most 5e-6 of m on every tensor but one,
+and 1.8e-5 of m on the energy bias of a batch whose energy errors cancel."""
 import numpy as np
 import pytest
 
@@ -30,7 +32,7 @@ from paper_2412_20796_amd import synth
 
 pytestmark = pytest.mark.gpu
 
-ATOL_REL, RTOL = 5e-5, 1e-3
+ATOL_REL, RTOL = 3e-5, 1e-4
 
 
 @pytest.fixture(scope="module")

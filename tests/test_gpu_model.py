@@ -183,6 +183,44 @@ def test_adam_update(bd):
         assert np.all(np.abs(pg - pr) <= 2 * lr * t + 1e-5 + 1e-4 * np.abs(pr)), "adam step bound"
 
 
+def test_adam_kernel_on_its_own_gradient(bd):
+    """The Adam update alone: at t = 1, 2, 3 the oracle's Adam is applied, in
+    fp64, to the GPU's own parameters, moments and gradient of that step, and
+    the GPU's new parameters, m and v must match everywhere (the update is
+    elementwise, so fp32 rounding bounds the difference)."""
+    b, params, targets, d, T = synth.workload_inputs("triclinic40")
+    hp, db, g, ws = _setup(bd, b, d, T)
+    p = _dev(params)
+    m = _dev(np.zeros_like(params))
+    v = _dev(np.zeros_like(params))
+    lr, b1, b2, eps = 3e-4, 0.9, 0.999, 1e-8
+    tg = [_dev(x) for x in targets]
+    for t in (1, 2, 3):
+        p0, m0, v0 = (x.cpu().numpy().astype(np.float64) for x in (p, m, v))
+        _, grad = bd.step(hp, db, g, p, tg, ws, adam=(m, v, (lr, b1, b2, eps, float(t))))
+        gg = grad.cpu().numpy().astype(np.float64)
+        # the kernel takes the hyperparameters as fp32 values (1 - 0.999 in
+        # fp32 is 1.3e-5 away from 0.001): the oracle gets the same numbers
+        h32 = [float(np.float32(x)) for x in (lr, b1, b2, eps)]
+        pr, mr, vr = om.adam(p0, gg, m0, v0, *h32, t)
+        pg, mg, vg = (x.cpu().numpy().astype(np.float64) for x in (p, m, v))
+        # fp32 keeps ~1e-7 relative above its smallest normal numbers (1.2e-38);
+        # squares of gradients below ~1e-19 fall under it
+        # m = b1 m + (1 - b1) g can cancel: fp32 rounding is relative to the terms
+        mag_m = h32[1] * np.abs(m0) + (1 - h32[1]) * np.abs(gg)
+        for name, got, ref, mag in (("m", mg, mr, mag_m), ("v", vg, vr, np.abs(vr))):
+            err = np.abs(got - ref)
+            bad = err > 1e-6 * mag + 1e-36
+            assert not bad.any(), ("adam %s step %d" % (name, t), int(bad.sum()),
+                                   float(ref[np.argmax(err)]), float(got[np.argmax(err)]))
+        # the step is at most lr in size; fp32 rounds p to a few ulps and the
+        # step to ~1e-6 of itself
+        tol = 4 * np.spacing(np.abs(pr).astype(np.float32)).astype(np.float64) + 1e-5 * lr
+        bad = np.abs(pg - pr) > tol
+        assert not bad.any(), ("adam params step %d" % t, int(bad.sum()), float(np.abs(pg - pr).max()))
+        assert np.count_nonzero(pg != p0) > 0.5 * pg.size
+
+
 def test_bitwise_reproducible(bd):
     b, params, targets, d, T = synth.workload_inputs("triclinic40")
     hp, db, g, ws = _setup(bd, b, d, T)
