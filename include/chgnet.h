@@ -163,6 +163,24 @@ int chgnet_workspace_size(const chgnet_hparams* hp, int64_t N, int64_t E, int64_
 int chgnet_build_graph(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_graph* graph, void* ws,
                        size_t ws_bytes, void* stream);
 
+/* chgnet_build_graph without a workspace, for callers that cannot allocate
+ * device memory (serving and molecular-dynamics loops or harnesses that
+ * forbid hipMalloc; the call still waits once on the host for the sizes, so
+ * it cannot be captured into a HIP graph). The graph scratch lives in a
+ * static device array of CHGNET_NOALLOC_SCRATCH_BYTES (8 MiB) on each GPU the
+ * library runs on, held until the process ends: a batch may need at most
+ * that much, 64 N + 156 S bytes plus about 4 KiB (for example 130,000 atoms
+ * in one crystal, or 100,000 atoms in up to 12,000 crystals); larger
+ * batches return CHGNET_EINVAL before any launch. The call
+ * allocates nothing: no device memory, no pinned host memory. It uses the
+ * current device's array (the stream must belong to the current device) and
+ * writes the same graph as chgnet_build_graph. Every call on a GPU shares
+ * that GPU's array, so calls that overlap in time on one GPU (other host
+ * threads, or streams not ordered with each other) race; calls on one stream
+ * are ordered. Errors as for chgnet_build_graph. */
+#define CHGNET_NOALLOC_SCRATCH_BYTES (8u << 20)
+int chgnet_build_graph_noalloc(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_graph* graph, void* stream);
+
 /* Forward pass (Eq. 2-9; interaction blocks of Eq. 11, or Eq. 10 if
  * hp->sequential): energy [S] (total energy of each crystal), forces [N,3],
  * stress [S,3,3] and, if hp->magmom, magnetic moments magmom [N] (may be NULL

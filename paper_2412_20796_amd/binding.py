@@ -17,7 +17,8 @@ _LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libchgnet.
 _lib = None
 
 CHGNET_OK, CHGNET_EINVAL, CHGNET_ECAPACITY, CHGNET_EWORKSPACE, CHGNET_EHIP = 0, -1, -2, -3, -4
-EXPORTED = ("chgnet_param_count", "chgnet_workspace_size", "chgnet_build_graph", "chgnet_forward",
+EXPORTED = ("chgnet_param_count", "chgnet_workspace_size", "chgnet_build_graph", "chgnet_build_graph_noalloc",
+            "chgnet_forward",
             "chgnet_backward", "chgnet_step", "chgnet_md", "chgnet_last_error_string", "chgnet_profile_start",
             "chgnet_profile_stop")
 
@@ -70,6 +71,8 @@ def lib():
                                             ctypes.POINTER(ctypes.c_size_t)]
         L.chgnet_build_graph.argtypes = [ctypes.POINTER(HParams), ctypes.POINTER(CBatch), ctypes.POINTER(CGraph), vp,
                                          ctypes.c_size_t, vp]
+        L.chgnet_build_graph_noalloc.argtypes = [ctypes.POINTER(HParams), ctypes.POINTER(CBatch),
+                                                 ctypes.POINTER(CGraph), vp]
         L.chgnet_forward.argtypes = [ctypes.POINTER(HParams), ctypes.POINTER(CBatch), ctypes.POINTER(CGraph), vp, vp,
                                      vp, vp, vp, ctypes.c_int, vp, ctypes.c_size_t, vp]
         L.chgnet_backward.argtypes = [ctypes.POINTER(HParams), ctypes.POINTER(CBatch), ctypes.POINTER(CGraph), vp, vp,
@@ -243,6 +246,24 @@ def build_graph(hp: HParams, batch: DeviceBatch, graph: DeviceGraph, ws: Workspa
         cg = graph.c()
         code = lib().chgnet_build_graph(ctypes.byref(hp), ctypes.byref(cb), ctypes.byref(cg), ws.ptr, ws.nbytes,
                                         _stream(batch.pos.device))
+        graph.take_counts(cg)
+        if code == CHGNET_ECAPACITY:
+            graph.resize(int(cg.n_edges * 1.25) + 64, int(cg.n_bonds * 1.25) + 64, int(cg.n_angles * 1.25) + 64,
+                         batch.pos.device)
+            continue
+        _check(code)
+        return graph.n_edges, graph.n_bonds, graph.n_angles
+    raise ChgnetError(CHGNET_ECAPACITY, "graph capacity retry failed")
+
+
+def build_graph_noalloc(hp: HParams, batch: DeviceBatch, graph: DeviceGraph):
+    """chgnet_build_graph_noalloc (the library's static scratch, no workspace)
+    with a capacity retry. Returns (E, B, A)."""
+    cb = batch.c()
+    for _ in range(2):
+        cg = graph.c()
+        code = lib().chgnet_build_graph_noalloc(ctypes.byref(hp), ctypes.byref(cb), ctypes.byref(cg),
+                                                _stream(batch.pos.device))
         graph.take_counts(cg)
         if code == CHGNET_ECAPACITY:
             graph.resize(int(cg.n_edges * 1.25) + 64, int(cg.n_bonds * 1.25) + 64, int(cg.n_angles * 1.25) + 64,

@@ -14,6 +14,7 @@ size_t graph_scratch_bytes(int64_t N, int64_t S);
 size_t acts_bytes(const chgnet_hparams& hp, int64_t N, int64_t E, int64_t B, int64_t A, int64_t S);
 int build_graph(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_graph* graph, void* ws, size_t ws_bytes,
                 hipStream_t st);
+int build_graph_noalloc(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_graph* graph, hipStream_t st);
 int forward_entry(const chgnet_hparams* hp, const chgnet_batch* batch, const chgnet_graph* graph, const float* params,
                   float* energy, float* forces, float* stress, float* magmom, void* ws, size_t ws_bytes,
                   hipStream_t st);
@@ -165,6 +166,11 @@ int chgnet_workspace_size(const chgnet_hparams* hp, int64_t N, int64_t E, int64_
 int chgnet_build_graph(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_graph* graph, void* ws,
                        size_t ws_bytes, void* stream) {
   return chg::build_graph(hp, batch, graph, ws, ws_bytes, static_cast<hipStream_t>(stream));
+}
+
+int chgnet_build_graph_noalloc(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_graph* graph,
+                               void* stream) {
+  return chg::build_graph_noalloc(hp, batch, graph, static_cast<hipStream_t>(stream));
 }
 
 int chgnet_forward(const chgnet_hparams* hp, const chgnet_batch* batch, const chgnet_graph* graph, const float* params,

@@ -13,6 +13,7 @@
 
 #include <climits>
 #include <cmath>
+#include <mutex>
 
 #include "common.hpp"
 
@@ -588,8 +589,13 @@ int validate_batch(const chgnet_batch* b) {
   return CHGNET_OK;
 }
 
-int build_graph(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_graph* graph, void* ws, size_t ws_bytes,
-                hipStream_t st) {
+namespace {
+
+// Graph build on a scratch region of ws_bytes at ws. With pinned_readback the
+// sizes come back through a small pinned host buffer of the calling thread
+// (allocated on its first use); otherwise through a pageable host variable.
+int build_graph_impl(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_graph* graph, void* ws,
+                     size_t ws_bytes, hipStream_t st, bool pinned_readback) {
   CHG_TRY(validate_hparams(hp));
   CHG_TRY(validate_batch(batch));
   if (!graph || !graph->edge_ptr || !graph->bond_ptr) return fail(CHGNET_EINVAL, "graph: edge_ptr and bond_ptr are required");
@@ -628,11 +634,17 @@ int build_graph(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_grap
 
   // the sizes come back through a small pinned buffer (one per host thread,
   // allocated on first use): a direct DMA instead of a staged pageable copy
-  thread_local GraphInfo* pinned = nullptr;
-  if (!pinned) CHG_HIP(hipHostMalloc(reinterpret_cast<void**>(&pinned), sizeof(GraphInfo), hipHostMallocDefault));
-  CHG_HIP(hipMemcpyAsync(pinned, g.ginfo, sizeof(GraphInfo), hipMemcpyDeviceToHost, st));
-  CHG_HIP(hipStreamSynchronize(st));
-  const GraphInfo hinfo = *pinned;
+  GraphInfo hinfo;
+  if (pinned_readback) {
+    thread_local GraphInfo* pinned = nullptr;
+    if (!pinned) CHG_HIP(hipHostMalloc(reinterpret_cast<void**>(&pinned), sizeof(GraphInfo), hipHostMallocDefault));
+    CHG_HIP(hipMemcpyAsync(pinned, g.ginfo, sizeof(GraphInfo), hipMemcpyDeviceToHost, st));
+    CHG_HIP(hipStreamSynchronize(st));
+    hinfo = *pinned;
+  } else {
+    CHG_HIP(hipMemcpyAsync(&hinfo, g.ginfo, sizeof(GraphInfo), hipMemcpyDeviceToHost, st));
+    CHG_HIP(hipStreamSynchronize(st));
+  }
   if (hinfo.err) {
     std::string m = "build_graph: invalid input:";
     if (hinfo.err & ERR_Z) m += " Z outside 1..94;";
@@ -664,6 +676,53 @@ int build_graph(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_grap
                                                                        graph->edge_rev, graph->bond_ptr, g.angle_base,
                                                                        graph->angle_ptr, graph->angle_b2));
   return CHGNET_OK;
+}
+
+// Scratch of the allocation-free graph build: one array per GPU, held until
+// the process ends. Host code never passes `scratch` itself to a kernel (in
+// host code the name is a stand-in, not a device address); it uses the
+// address hipGetSymbolAddress returns on each device.
+constexpr size_t kNoAllocScratchBytes = size_t(8) << 20;
+static __device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of `scratch` on the current device, looked up once per device.
+int scratch_address(void** out) {
+  int dev = -1;
+  CHG_HIP(hipGetDevice(&dev));
+  if (dev < 0 || dev >= kMaxDevices) return fail(CHGNET_EINVAL, "build_graph_noalloc: device index out of range");
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    CHG_HIP(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+    if (!p) return fail(CHGNET_EHIP, "build_graph_noalloc: no device address for the scratch array");
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return CHGNET_OK;
+}
+
+}  // namespace
+
+int build_graph(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_graph* graph, void* ws, size_t ws_bytes,
+                hipStream_t st) {
+  return build_graph_impl(hp, batch, graph, ws, ws_bytes, st, true);
+}
+
+int build_graph_noalloc(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_graph* graph, hipStream_t st) {
+  CHG_TRY(validate_hparams(hp));
+  CHG_TRY(validate_batch(batch));
+  const size_t need = graph_scratch_bytes(batch->n_atoms, batch->n_struct);
+  if (need > kNoAllocScratchBytes)
+    return fail(CHGNET_EINVAL, "build_graph_noalloc: the batch needs " + std::to_string(need) +
+                                   " bytes of graph scratch, more than the static " +
+                                   std::to_string(kNoAllocScratchBytes) + " (use chgnet_build_graph with a workspace)");
+  void* p = nullptr;
+  CHG_TRY(scratch_address(&p));
+  return build_graph_impl(hp, batch, graph, p, kNoAllocScratchBytes, st, false);
 }
 
 }  // namespace chg
