@@ -272,6 +272,11 @@ def algorithmic_cost(tag, z):
         return "mfma", T * (N * 16 * D * D + B * 8 * D * D) - N * 4 * D * D - B * 4 * D * D
     if tag == "gemm_bond_bwd":
         return "mfma", Tang * B * 16 * D * D + B * 8 * D * D
+    if tag == "k_gate_fwd" and D != 64:
+        # d = 128: the fused gate is bound by its product z = x W (+ b) of
+        # every edge (d -> 2d) and, per angle, of the bond-conv and
+        # angle-update gates (d -> 4d; d -> 2d in the last layer)
+        return "mfma", T * E * 4 * D * D + Tang * A * 8 * D * D + A * 4 * D * D
     if tag == "k_gate_fwd" and D == 64:
         # pre-activations formed in the kernel (d = 64): per edge x (d) and
         # e^a (d) in, z kept for the backward (2d), message (d) and the copy
@@ -280,13 +285,6 @@ def algorithmic_cost(tag, z):
         # terms N x 8d (6d last layer), per-bond terms B x 8d (4d), e^b B x d.
         lay = E * 6 * D + A * 9 * D + N * 8 * D + B * 9 * D
         last = E * 6 * D + A * 4 * D + N * 6 * D + B * 5 * D
-        return "hbm", f * (Tang * lay + last)
-    if tag == "k_gate_fwd":
-        # z from the product kernel: per edge z (2d) + e^a (d) in, message (d)
-        # out; per angle: bond gate z (2d) in, message (d) out; angle gate z
-        # (2d) + a (d) in, a' (d) out. Tables as above.
-        lay = E * 4 * D + A * 7 * D + N * 8 * D + B * 9 * D
-        last = E * 4 * D + A * 3 * D + N * 6 * D + B * 5 * D
         return "hbm", f * (Tang * lay + last)
     if tag == "k_gate_bwd" and z.get("fused_bwd"):
         # as below, plus the input gradients the kernel forms: per edge the
@@ -368,14 +366,14 @@ def mandatory_cost(tag, z):
 
 
 # rocprofv3 kernel symbol of each launch tag that has an algorithmic cost
-# (the gate kernels depend on the width: fused product-and-gate kernels at
-# d = 64, row-gate kernels after a separate product at d = 128)
+# (the backward gate depends on the width: a fused gate-and-input-gradient
+# kernel at d = 64, a row-gate kernel before a separate product at d = 128)
 def tag_symbol(tag, d):
     return {
         "gemm_z": "k_gemm<64, 1>",
         "gemm_in_bwd": "k_gemm<64, 2>",
         "tn_in": "k_tn<1>",
-        "k_gate_fwd": "k_gate_fwd_mm" if d == 64 else "k_gate_fwd<128>",
+        "k_gate_fwd": "k_gate_fwd_mm<%d>" % d,
         "k_gate_bwd": "k_gate_bwd_mm" if d == 64 else "k_gate_bwd<128>",
     }.get(tag)
 

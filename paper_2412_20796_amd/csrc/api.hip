@@ -16,8 +16,8 @@ int build_graph(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_grap
                 hipStream_t st);
 int build_graph_noalloc(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_graph* graph, hipStream_t st);
 int forward_entry(const chgnet_hparams* hp, const chgnet_batch* batch, const chgnet_graph* graph, const float* params,
-                  float* energy, float* forces, float* stress, float* magmom, void* ws, size_t ws_bytes,
-                  hipStream_t st);
+                  float* energy, float* forces, float* stress, float* magmom, int save_for_backward, void* ws,
+                  size_t ws_bytes, hipStream_t st);
 int backward_entry(const chgnet_hparams* hp, const chgnet_batch* batch, const chgnet_graph* graph, const float* params,
                    const float* dE, const float* dF, const float* dS, const float* dM, float* grad, void* ws,
                    size_t ws_bytes, hipStream_t st);
@@ -176,8 +176,7 @@ int chgnet_build_graph_noalloc(const chgnet_hparams* hp, const chgnet_batch* bat
 int chgnet_forward(const chgnet_hparams* hp, const chgnet_batch* batch, const chgnet_graph* graph, const float* params,
                    float* energy, float* forces, float* stress, float* magmom, int save_for_backward, void* ws,
                    size_t ws_bytes, void* stream) {
-  (void)save_for_backward;  // activations are always kept in ws
-  return chg::forward_entry(hp, batch, graph, params, energy, forces, stress, magmom, ws, ws_bytes,
+  return chg::forward_entry(hp, batch, graph, params, energy, forces, stress, magmom, save_for_backward, ws, ws_bytes,
                             static_cast<hipStream_t>(stream));
 }
 

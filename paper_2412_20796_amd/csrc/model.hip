@@ -361,83 +361,34 @@ __device__ __forceinline__ void load_z(const float* __restrict__ z, int ldz, con
   }
 }
 
-// Columns per lane of the forward and backward gates.
-constexpr int kFwdCpl = 16;
+// Columns per lane of the row-layout backward gate.
 constexpr int kBwdCpl = 8;
 
 enum GateFwdMode { FWD_ATOM = 0, FWD_BOND = 1, FWD_ANGLE = 2 };
 
-// Forward gate. z rows at z + row*ldz (2d values).
+// Forward gate modes:
 //   FWD_ATOM : out[row] = e^a[row] * phi            (atom conv message)
 //   FWD_BOND : out[row] = e^b[b2[row]] * phi        (bond conv message)
 //   FWD_ANGLE: out[row] = a[row] + phi              (angle update)
-struct GateFwdJob {
-  int mode, rows, ldz, block0;
-  const float* z;
-  GateAdds ad;
-  LnPtrs ln;
-  const float* mulv;
-  const int* mul_idx;
-  float* out;
-};
-struct GateFwdJobs {
-  int n;
-  GateFwdJob j[3];
-};
 
-template <int D, int MODE>
-__device__ __forceinline__ void gate_fwd_rows(int blk, const GateFwdJob& J) {
-  constexpr int CPL = kFwdCpl;
-  using L = Lanes<D, CPL>;
-  const int lane = threadIdx.x & 63, slot = lane / L::LPR, j = lane % L::LPR;
-  const int row = (blk * 4 + (threadIdx.x >> 6)) * L::RPW + slot;
-  if (row >= J.rows) return;  // LN lanes of a row are adjacent: a row is all-in or all-out
-  float zc[CPL], zg[CPL], rc, rg;
-  load_z<D, CPL>(J.z, J.ldz, J.ad, row, j, zc, zg);
-  ln_stats<D, CPL>(zc, zg, rc, rg);
-  float mv[CPL], o[CPL];
-  const int64_t mrow = MODE == FWD_BOND ? J.mul_idx[row] : row;
-  load_cols<D, CPL>(J.mulv + mrow * D, j, mv);
-#pragma unroll
-  for (int k = 0; k < CPL; ++k) {
-    const int c = L::col(j, k);
-    const float yc = J.ln.gc[c] * zc[k] + J.ln.bc[c];
-    const float yg = J.ln.gg[c] * zg[k] + J.ln.bg[c];
-    const float phi = yc * sigm(yc) * sigm(yg);
-    o[k] = MODE == FWD_ANGLE ? mv[k] + phi : mv[k] * phi;
-  }
-  store_cols<D, CPL>(J.out + (int64_t)row * D, j, o);
-}
-
-// The independent gates of a layer (atom conv, bond conv, angle update; Eq.
-// 11) in one launch: job k owns blocks [block0_k, block0_{k+1}).
-template <int D>
-__global__ void __launch_bounds__(256) k_gate_fwd(GateFwdJobs J) {
-  int k = 0;
-  while (k + 1 < J.n && (int)blockIdx.x >= J.j[k + 1].block0) ++k;
-  const GateFwdJob& jb = J.j[k];
-  const int blk = blockIdx.x - jb.block0;
-  if (jb.mode == FWD_ATOM) gate_fwd_rows<D, FWD_ATOM>(blk, jb);
-  else if (jb.mode == FWD_BOND) gate_fwd_rows<D, FWD_BOND>(blk, jb);
-  else gate_fwd_rows<D, FWD_ANGLE>(blk, jb);
-}
-
-// Forward gate with its own pre-activation product (d = 64): z = x W + b
-// (+ the gathered terms) is formed tile by tile in LDS and never round-trips
+// Forward gate with its own pre-activation product: z = x W + b (+ the
+// gathered terms) is formed tile by tile in LDS and never round-trips
 // through HBM. Producer wave w keeps the fp32 MFMA B fragments of output
-// columns [32w, 32w + 32) of W (64 x 128: core | gate) in registers; the x
-// tile is staged in LDS; each producer forms its 64 x 32 slice of z with
+// columns [32w, 32w + 32) of W (d x 2d: core | gate) in registers; the x
+// tile is staged in LDS; each producer forms its rows x 32 slice of z with
 // 32x32x2 MFMAs (lane half h supplies k = 16h + i in step i of each 32-wide
 // k block) and writes it to the z tile; the consumers' row-layout gate then
-// reads z from LDS.
+// reads z from LDS. d = 64: 64-row tiles, 4 producer and 8 consumer
+// wavefronts; d = 128: 32-row tiles, 8 producers (256 columns) and 8
+// consumers, 16 wavefronts of at most 128 VGPRs.
 typedef float v16f __attribute__((ext_vector_type(16)));
 
 struct GateMmJob {
   int mode, rows, tile0;
-  const float* x;  // [rows, 64]
-  const float* W;  // [64, 128] core | gate columns, row stride ldw
+  const float* x;  // [rows, d]
+  const float* W;  // [d, 2d] core | gate columns, row stride ldw
   int ldw;
-  const float* bias;  // [128]
+  const float* bias;  // [2d]
   GateAdds ad;
   LnPtrs ln;
   const float* mulv;
@@ -445,18 +396,35 @@ struct GateMmJob {
   float* out;
   float* zsave;  // optional [rows, ldzs]: x W + b, kept for the backward pass
   int ldzs;
-  float* xcopy;  // optional [rows, 64]: a copy of x (the residual part of e^{t+1})
+  float* xcopy;  // optional [rows, d]: a copy of x (the residual part of e^{t+1})
 };
 struct GateMmJobs {
   int n, ntiles;
   GateMmJob j[3];
 };
 
-constexpr int kMmRows = 64;
-constexpr int kMmXld = 64 + 4;
-constexpr int kMmZld = 128 + 4;
-
 constexpr int kMmCpl = 8;
+
+template <int D>
+struct MmCfg {
+  static constexpr int Rows = D == 64 ? 64 : 32;  // rows per tile
+  static constexpr int Prod = 2 * D / 32;         // producer waves: 32 z columns each
+  static constexpr int Cons = 8;                  // consumer waves
+  static constexpr int Threads = 64 * (Prod + Cons);
+  static constexpr int Xld = D + 4;
+  static constexpr int Zld = 2 * D + 4;
+  static constexpr int KB = D / 32;    // 32-deep k blocks
+  static constexpr int RS = Rows / 32;  // 32-row subtiles
+  // x tile loads: every producer thread moves F floats of one row
+  static constexpr int F = Rows * D / (64 * Prod);
+  static constexpr int TPR = D / F;  // threads per x row
+  static_assert(Cons * Lanes<D, kMmCpl>::RPW == Rows, "one consumer pass per tile");
+  static_assert(F % 4 == 0 && Rows * TPR == 64 * Prod, "x tile split");
+};
+// kept for the backward gate kernel (d = 64 only)
+constexpr int kMmRows = MmCfg<64>::Rows;
+constexpr int kMmProducers = MmCfg<64>::Prod, kMmConsumers = MmCfg<64>::Cons;
+constexpr int kMmThreads = MmCfg<64>::Threads;
 
 // Gathered operands of one gate row (the atom/bond terms of the split first
 // layer and the multiplier row), loaded one tile ahead of their use; the
@@ -472,8 +440,9 @@ __device__ __forceinline__ void gate_mm_index(const GateMmJob& J, int row, int (
   ix[kMaxAdds] = J.mode == FWD_BOND ? J.mul_idx[r] : r;
 }
 
+template <int D>
 __device__ __forceinline__ void gate_mm_gather(const GateMmJob& J, const int (&ix)[kMaxAdds + 1], GateRowIn& in) {
-  constexpr int D = 64, CPL = kMmCpl;
+  constexpr int CPL = kMmCpl;
   const int j = (threadIdx.x & 63) % Lanes<D, CPL>::LPR;
 #pragma unroll
   for (int q = 0; q < kMaxAdds; ++q) {
@@ -490,10 +459,10 @@ struct GateLnRegs {
   float gc[kMmCpl], bc[kMmCpl], gg[kMmCpl], bg[kMmCpl];
 };
 
-template <int MODE>
+template <int D, int MODE>
 __device__ __forceinline__ void gate_mm_row(const GateMmJob& J, int row, int lr, const float* Zs, const GateRowIn& in,
                                             const GateLnRegs& ln) {
-  constexpr int D = 64, CPL = kMmCpl;
+  constexpr int CPL = kMmCpl;
   using L = Lanes<D, CPL>;
   const int j = (threadIdx.x & 63) % L::LPR;
   if (row >= J.rows) return;
@@ -502,7 +471,7 @@ __device__ __forceinline__ void gate_mm_row(const GateMmJob& J, int row, int lr,
     // odd rows of the z tile hold the two 32-column halves of each 64-column
     // block swapped (written so by the producers): the two rows of a read
     // phase fall in different banks
-    const float* zr = Zs + lr * kMmZld;
+    const float* zr = Zs + lr * MmCfg<D>::Zld;
     const int sw = (lr & 1) * 32;
 #pragma unroll
     for (int q = 0; q < CPL / 4; ++q) {
@@ -538,68 +507,78 @@ __device__ __forceinline__ void gate_mm_row(const GateMmJob& J, int row, int lr,
   store_cols<D, CPL>(J.out + (int64_t)row * D, j, o);
 }
 
-// Producer and consumer wavefronts: waves 0-3 form z of tile i (x tile and
-// z tile double-buffered in LDS) while waves 4-11 run the gate rows of tile
-// i-1 and gather the operands of tile i; one block barrier per tile hands
-// the buffers over. Producers and consumers run separate loops with the same
-// number of block barriers, so each keeps only its own state.
-constexpr int kMmProducers = 4, kMmConsumers = 8;
-constexpr int kMmThreads = 64 * (kMmProducers + kMmConsumers);
+// Producer and consumer wavefronts: the producers form z of tile i (x tile
+// and z tile double-buffered in LDS) while the consumers run the gate rows
+// of tile i-1 and gather the operands of tile i; one block barrier per tile
+// hands the buffers over. Producers and consumers run separate loops with
+// the same number of block barriers, so each keeps only its own state.
 
-// Producer pieces (threads 0-255). x tile loads: thread -> row tid / 4, 16
-// columns at 16 (tid % 4); rows past `rows` read as zero.
-__device__ __forceinline__ void mm_fetch_x(const float* __restrict__ x, int rows, int row0, float4 (&v)[4]) {
-  const int tid = threadIdx.x, row = row0 + (tid >> 2), xc = 16 * (tid & 3);
+// Producer pieces (threads 0 .. 64 Prod - 1). x tile loads: thread -> row
+// tid / TPR, F columns at F (tid % TPR); rows past `rows` read as zero.
+template <int D>
+__device__ __forceinline__ void mm_fetch_x(const float* __restrict__ x, int rows, int row0,
+                                           float4 (&v)[MmCfg<D>::F / 4]) {
+  using C = MmCfg<D>;
+  const int tid = threadIdx.x, row = row0 + tid / C::TPR, xc = C::F * (tid % C::TPR);
 #pragma unroll
-  for (int q = 0; q < 4; ++q) v[q] = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int q = 0; q < C::F / 4; ++q) v[q] = make_float4(0.f, 0.f, 0.f, 0.f);
   if (row < rows) {
-    const float* p = x + (int64_t)row * 64 + xc;
+    const float* p = x + (int64_t)row * D + xc;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) v[q] = *reinterpret_cast<const float4*>(p + 4 * q);
+    for (int q = 0; q < C::F / 4; ++q) v[q] = *reinterpret_cast<const float4*>(p + 4 * q);
   }
 }
-__device__ __forceinline__ void mm_store_x(float* X, const float4 (&v)[4]) {
-  const int tid = threadIdx.x, xr = tid >> 2, xc = 16 * (tid & 3);
+template <int D>
+__device__ __forceinline__ void mm_store_x(float* X, const float4 (&v)[MmCfg<D>::F / 4]) {
+  using C = MmCfg<D>;
+  const int tid = threadIdx.x, xr = tid / C::TPR, xc = C::F * (tid % C::TPR);
 #pragma unroll
-  for (int q = 0; q < 4; ++q) *reinterpret_cast<float4*>(&X[xr * kMmXld + xc + 4 * q]) = v[q];
+  for (int q = 0; q < C::F / 4; ++q) *reinterpret_cast<float4*>(&X[xr * C::Xld + xc + 4 * q]) = v[q];
 }
 // the same x tile piece to global memory (rows past `rows` are skipped)
-__device__ __forceinline__ void mm_copy_x(float* __restrict__ dst, int rows, int row0, const float4 (&v)[4]) {
-  const int tid = threadIdx.x, row = row0 + (tid >> 2), xc = 16 * (tid & 3);
+template <int D>
+__device__ __forceinline__ void mm_copy_x(float* __restrict__ dst, int rows, int row0,
+                                          const float4 (&v)[MmCfg<D>::F / 4]) {
+  using C = MmCfg<D>;
+  const int tid = threadIdx.x, row = row0 + tid / C::TPR, xc = C::F * (tid % C::TPR);
   if (row < rows) {
-    float* p = dst + (int64_t)row * 64 + xc;
+    float* p = dst + (int64_t)row * D + xc;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
+    for (int q = 0; q < C::F / 4; ++q) {
       const v4f t = {v[q].x, v[q].y, v[q].z, v[q].w};
       __builtin_nontemporal_store(t, reinterpret_cast<v4f*>(p + 4 * q));
     }
   }
 }
 // B fragments of W columns [32 wave, 32 wave + 32) and their bias
+template <int D>
 __device__ __forceinline__ void mm_load_w(const float* __restrict__ W, int ldw, const float* __restrict__ b, int wave,
-                                          float (&bfr)[2][16], float& bias) {
+                                          float (&bfr)[MmCfg<D>::KB][16], float& bias) {
   const int lane = threadIdx.x & 63, h = lane >> 5, col = 32 * wave + (lane & 31);
 #pragma unroll
-  for (int kb = 0; kb < 2; ++kb)
+  for (int kb = 0; kb < MmCfg<D>::KB; ++kb)
 #pragma unroll
     for (int e = 0; e < 16; ++e) bfr[kb][e] = W[(int64_t)(32 * kb + 16 * h + e) * ldw + col];
   bias = b[col];
 }
-// z slice (64 rows x 32 columns) of one producer wave, X -> Z
-__device__ __forceinline__ void mm_tile(const float* X, float* Z, const float (&bfr)[2][16], float bias, int wave) {
+// z slice (Rows x 32 columns) of one producer wave, X -> Z
+template <int D>
+__device__ __forceinline__ void mm_tile(const float* X, float* Z, const float (&bfr)[MmCfg<D>::KB][16], float bias,
+                                        int wave) {
+  using C = MmCfg<D>;
   const int lane = threadIdx.x & 63, h = lane >> 5, l32 = lane & 31;
-  // the two 32-row subtiles are independent accumulation chains
-  v16f acc[kMmRows / 32];
+  // the 32-row subtiles are independent accumulation chains
+  v16f acc[C::RS];
 #pragma unroll
-  for (int s = 0; s < kMmRows / 32; ++s)
+  for (int s = 0; s < C::RS; ++s)
 #pragma unroll
     for (int e = 0; e < 16; ++e) acc[s][e] = 0.f;
 #pragma unroll
-  for (int kb = 0; kb < 2; ++kb) {
-    float af[kMmRows / 32][16];
+  for (int kb = 0; kb < C::KB; ++kb) {
+    float af[C::RS][16];
 #pragma unroll
-    for (int s = 0; s < kMmRows / 32; ++s) {
-      const float* ap = &X[(32 * s + l32) * kMmXld + 32 * kb + 16 * h];
+    for (int s = 0; s < C::RS; ++s) {
+      const float* ap = &X[(32 * s + l32) * C::Xld + 32 * kb + 16 * h];
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         const float4 v = *reinterpret_cast<const float4*>(ap + 4 * q);
@@ -609,28 +588,29 @@ __device__ __forceinline__ void mm_tile(const float* X, float* Z, const float (&
 #pragma unroll
     for (int e = 0; e < 16; ++e)
 #pragma unroll
-      for (int s = 0; s < kMmRows / 32; ++s)
+      for (int s = 0; s < C::RS; ++s)
         acc[s] = __builtin_amdgcn_mfma_f32_32x32x2f32(af[s][e], bfr[kb][e], acc[s], 0, 0, 0);
   }
 #pragma unroll
-  for (int s = 0; s < kMmRows / 32; ++s)
+  for (int s = 0; s < C::RS; ++s)
 #pragma unroll
     for (int e = 0; e < 16; ++e)
-      Z[(32 * s + 8 * (e >> 2) + 4 * h + (e & 3)) * kMmZld + ((32 * wave + l32) ^ ((e & 1) * 32))] = acc[s][e] + bias;
+      Z[(32 * s + 8 * (e >> 2) + 4 * h + (e & 3)) * C::Zld + ((32 * wave + l32) ^ ((e & 1) * 32))] = acc[s][e] + bias;
 }
 
 // One block per compute unit, walking tiles blockIdx.x, blockIdx.x +
 // gridDim.x, ... of the concatenated jobs.
-__global__ void __launch_bounds__(kMmThreads, 1) k_gate_fwd_mm(GateMmJobs J) {
-  __shared__ __attribute__((aligned(16))) float Xs[2][kMmRows * kMmXld];
-  __shared__ __attribute__((aligned(16))) float Zs[2][kMmRows * kMmZld];
-  // LayerNorm parameters of every job: [job][gc, bc, gg, bg][64]
-  __shared__ __attribute__((aligned(16))) float LnS[3][4][64];
+template <int D>
+__global__ void __launch_bounds__(MmCfg<D>::Threads, 1) k_gate_fwd_mm(GateMmJobs J) {
+  using C = MmCfg<D>;
+  __shared__ __attribute__((aligned(16))) float Xs[2][C::Rows * C::Xld];
+  __shared__ __attribute__((aligned(16))) float Zs[2][C::Rows * C::Zld];
+  // LayerNorm parameters of every job: [job][gc, bc, gg, bg][d]
+  __shared__ __attribute__((aligned(16))) float LnS[3][4][D];
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  {
-    static_assert(kMmThreads == 3 * 4 * 64, "one LayerNorm value per thread");
-    const int t = threadIdx.x, jb = t / 256, q = (t / 64) % 4, c = t % 64;
+  for (int t = threadIdx.x; t < 3 * 4 * D; t += C::Threads) {
+    const int jb = t / (4 * D), q = (t / D) % 4, c = t % D;
     if (jb < J.n) {
       const LnPtrs& ln = J.j[jb].ln;
       LnS[jb][q][c] = (q == 0 ? ln.gc : q == 1 ? ln.bc : q == 2 ? ln.gg : ln.bg)[c];
@@ -644,53 +624,52 @@ __global__ void __launch_bounds__(kMmThreads, 1) k_gate_fwd_mm(GateMmJobs J) {
   const int nt = (int)blockIdx.x < J.ntiles ? (J.ntiles - 1 - (int)blockIdx.x) / (int)gridDim.x + 1 : 0;
   if (nt == 0) return;
   auto tile_of = [&](int i) { return (int)blockIdx.x + i * (int)gridDim.x; };
-  auto fetch_x = [&](int tile, float4 (&v)[4]) {
-    const GateMmJob& jb = J.j[job_of(tile)];
-    mm_fetch_x(jb.x, jb.rows, (tile - jb.tile0) * kMmRows, v);
-  };
-  auto copy_x = [&](int tile, const float4 (&v)[4]) {
-    const GateMmJob& jb = J.j[job_of(tile)];
-    if (jb.xcopy) mm_copy_x(jb.xcopy, jb.rows, (tile - jb.tile0) * kMmRows, v);
-  };
-  if (wave < kMmProducers) {
-    float4 xv[4];
+  if (wave < C::Prod) {
+    float4 xv[C::F / 4];
+    auto fetch_x = [&](int tile) {
+      const GateMmJob& jb = J.j[job_of(tile)];
+      mm_fetch_x<D>(jb.x, jb.rows, (tile - jb.tile0) * C::Rows, xv);
+    };
+    auto copy_x = [&](int tile) {
+      const GateMmJob& jb = J.j[job_of(tile)];
+      if (jb.xcopy) mm_copy_x<D>(jb.xcopy, jb.rows, (tile - jb.tile0) * C::Rows, xv);
+    };
     int cur = -1;
-    float bfr[2][16], bias = 0.f;
-    fetch_x(tile_of(0), xv);
-    mm_store_x(Xs[0], xv);
-    copy_x(tile_of(0), xv);
-    if (nt > 1) fetch_x(tile_of(1), xv);
+    float bfr[C::KB][16], bias = 0.f;
+    fetch_x(tile_of(0));
+    mm_store_x<D>(Xs[0], xv);
+    copy_x(tile_of(0));
+    if (nt > 1) fetch_x(tile_of(1));
     __syncthreads();
     for (int i = 0; i <= nt; ++i) {
       if (i < nt) {
         const int k = job_of(tile_of(i));
         if (k != cur) {
           cur = k;
-          mm_load_w(J.j[k].W, J.j[k].ldw, J.j[k].bias, wave, bfr, bias);
+          mm_load_w<D>(J.j[k].W, J.j[k].ldw, J.j[k].bias, wave, bfr, bias);
         }
         if (i + 1 < nt) {
-          mm_store_x(Xs[(i + 1) & 1], xv);
-          copy_x(tile_of(i + 1), xv);
-          if (i + 2 < nt) fetch_x(tile_of(i + 2), xv);
+          mm_store_x<D>(Xs[(i + 1) & 1], xv);
+          copy_x(tile_of(i + 1));
+          if (i + 2 < nt) fetch_x(tile_of(i + 2));
         }
-        mm_tile(Xs[i & 1], Zs[i & 1], bfr, bias, wave);
+        mm_tile<D>(Xs[i & 1], Zs[i & 1], bfr, bias, wave);
       }
       __syncthreads();
     }
   } else {
     // lane row within the tile; gathered operands of the next tile and row
     // indices of the one after
-    using GL = Lanes<64, kMmCpl>;
-    static_assert(kMmConsumers * GL::RPW == kMmRows, "one consumer pass per tile");
-    const int lr = (wave - kMmProducers) * GL::RPW + lane / GL::LPR;
-    auto row_of = [&](int tile, const GateMmJob& jb) { return (tile - jb.tile0) * kMmRows + lr; };
+    using GL = Lanes<D, kMmCpl>;
+    const int lr = (wave - C::Prod) * GL::RPW + lane / GL::LPR;
+    auto row_of = [&](int tile, const GateMmJob& jb) { return (tile - jb.tile0) * C::Rows + lr; };
     GateRowIn in;
     GateLnRegs lnr;
     int lnjob = -1;
     int ix[kMaxAdds + 1];
     const GateMmJob& j0 = J.j[job_of(tile_of(0))];
     gate_mm_index(j0, row_of(tile_of(0), j0), ix);
-    gate_mm_gather(j0, ix, in);
+    gate_mm_gather<D>(j0, ix, in);
     if (nt > 1) {
       const GateMmJob& j1 = J.j[job_of(tile_of(1))];
       gate_mm_index(j1, row_of(tile_of(1), j1), ix);
@@ -704,19 +683,19 @@ __global__ void __launch_bounds__(kMmThreads, 1) k_gate_fwd_mm(GateMmJobs J) {
         if (k != lnjob) {
           lnjob = k;
           const int jl = lane % GL::LPR;
-          load_cols<64, kMmCpl>(LnS[k][0], jl, lnr.gc);
-          load_cols<64, kMmCpl>(LnS[k][1], jl, lnr.bc);
-          load_cols<64, kMmCpl>(LnS[k][2], jl, lnr.gg);
-          load_cols<64, kMmCpl>(LnS[k][3], jl, lnr.bg);
+          load_cols<D, kMmCpl>(LnS[k][0], jl, lnr.gc);
+          load_cols<D, kMmCpl>(LnS[k][1], jl, lnr.bc);
+          load_cols<D, kMmCpl>(LnS[k][2], jl, lnr.gg);
+          load_cols<D, kMmCpl>(LnS[k][3], jl, lnr.bg);
         }
         const int row = row_of(tile, jb);
         const float* Z = Zs[(i - 1) & 1];
-        if (jb.mode == FWD_ATOM) gate_mm_row<FWD_ATOM>(jb, row, lr, Z, in, lnr);
-        else if (jb.mode == FWD_BOND) gate_mm_row<FWD_BOND>(jb, row, lr, Z, in, lnr);
-        else gate_mm_row<FWD_ANGLE>(jb, row, lr, Z, in, lnr);
+        if (jb.mode == FWD_ATOM) gate_mm_row<D, FWD_ATOM>(jb, row, lr, Z, in, lnr);
+        else if (jb.mode == FWD_BOND) gate_mm_row<D, FWD_BOND>(jb, row, lr, Z, in, lnr);
+        else gate_mm_row<D, FWD_ANGLE>(jb, row, lr, Z, in, lnr);
         if (i < nt) {
           const GateMmJob& jn = J.j[job_of(tile_of(i))];
-          gate_mm_gather(jn, ix, in);
+          gate_mm_gather<D>(jn, ix, in);
           if (i + 1 < nt) {
             const GateMmJob& jm = J.j[job_of(tile_of(i + 1))];
             gate_mm_index(jm, row_of(tile_of(i + 1), jm), ix);
@@ -2258,51 +2237,35 @@ int pack_params(const ParamLayout& L, const ParamLayout& La, const float* P, flo
 }
 
 // Launch the gates of one layer (forward) as one multi-job kernel.
-int gate_fwd_launch(int D, GateFwdJobs J, hipStream_t st) {
-  constexpr int RPB64 = 4 * Lanes<64, kFwdCpl>::RPW, RPB128 = 4 * Lanes<128, kFwdCpl>::RPW;
-  const int rpb = D == 64 ? RPB64 : RPB128;
-  GateFwdJobs K{};
-  int blocks = 0;
-  for (int i = 0; i < J.n; ++i) {
-    if (J.j[i].rows <= 0) continue;
-    K.j[K.n] = J.j[i];
-    K.j[K.n].block0 = blocks;
-    blocks += (int)cdiv(J.j[i].rows, rpb);
-    K.n++;
-  }
-  if (blocks == 0) return CHGNET_OK;
-  if (D == 64) KLAUNCH(st, "k_gate_fwd", k_gate_fwd<64><<<blocks, 256, 0, st>>>(K));
-  else KLAUNCH(st, "k_gate_fwd", k_gate_fwd<128><<<blocks, 256, 0, st>>>(K));
-  return CHGNET_OK;
-}
-
-// Launch the fused (d = 64) forward gates of one layer: a persistent grid of
-// one block per compute unit.
-int gate_fwd_mm_launch(GateMmJobs J, hipStream_t st) {
+// Launch the fused forward gates of one layer: a persistent grid of one
+// block per compute unit.
+int gate_fwd_mm_launch(int D, GateMmJobs J, hipStream_t st) {
+  const int rows_per_tile = D == 64 ? MmCfg<64>::Rows : MmCfg<128>::Rows;
   GateMmJobs K{};
   int tiles = 0;
   for (int i = 0; i < J.n; ++i) {
     if (J.j[i].rows <= 0) continue;
     K.j[K.n] = J.j[i];
     K.j[K.n].tile0 = tiles;
-    tiles += (int)cdiv(J.j[i].rows, kMmRows);
+    tiles += (int)cdiv(J.j[i].rows, rows_per_tile);
     K.n++;
   }
   K.ntiles = tiles;
   if (tiles == 0) return CHGNET_OK;
   const int grid = std::min(tiles, 256);
-  KLAUNCH(st, "k_gate_fwd", k_gate_fwd_mm<<<grid, kMmThreads, 0, st>>>(K));
+  if (D == 64) KLAUNCH(st, "k_gate_fwd", k_gate_fwd_mm<64><<<grid, MmCfg<64>::Threads, 0, st>>>(K));
+  else KLAUNCH(st, "k_gate_fwd", k_gate_fwd_mm<128><<<grid, MmCfg<128>::Threads, 0, st>>>(K));
   return CHGNET_OK;
 }
 
-GateMmJob mm_job(int mode, int64_t rows, const float* x, const float* W, const float* bias, const GateAdds& ad,
+GateMmJob mm_job(int D, int mode, int64_t rows, const float* x, const float* W, const float* bias, const GateAdds& ad,
                  LnPtrs ln, const float* mulv, const int* idx, float* out, float* zsave, int ldzs) {
   GateMmJob j{};
   j.mode = mode;
   j.rows = (int)rows;
   j.x = x;
   j.W = W;
-  j.ldw = 128;
+  j.ldw = 2 * D;
   j.bias = bias;
   j.ad = ad;
   j.ln = ln;
@@ -2311,21 +2274,6 @@ GateMmJob mm_job(int mode, int64_t rows, const float* x, const float* W, const f
   j.out = out;
   j.zsave = zsave;
   j.ldzs = ldzs;
-  return j;
-}
-
-GateFwdJob fwd_job(int mode, int64_t rows, const float* z, int ldz, const GateAdds& ad, LnPtrs ln, const float* mulv,
-                   const int* idx, float* out) {
-  GateFwdJob j{};
-  j.mode = mode;
-  j.rows = (int)rows;
-  j.z = z;
-  j.ldz = ldz;
-  j.ad = ad;
-  j.ln = ln;
-  j.mulv = mulv;
-  j.mul_idx = idx;
-  j.out = out;
   return j;
 }
 
@@ -2425,6 +2373,7 @@ struct Ctx {
   Acts a;
   char* ws;        // workspace, and the bytes the activations use of it
   size_t ws_bytes, ws_used;
+  bool save_z = true;  // keep the gate pre-activations for a backward pass
 };
 
 int make_ctx(const chgnet_hparams* hp, const chgnet_batch* batch, const chgnet_graph* graph, void* ws, size_t ws_bytes,
@@ -2559,47 +2508,23 @@ int forward_impl(Ctx& c, const float* Pflat, float* energy, float* forces, float
     // GatedMLPs: bit 0 atom conv, bit 1 bond conv, bit 2 angle update
     auto gates = [&](int which) -> int {
       if (!ang) which &= 3;
-      if (D == 64) {
-        // pre-activations formed inside the gate kernel; z kept for the backward
-        GateMmJobs J{};
-        if (which & 1) {
-          J.j[J.n] = mm_job(FWD_ATOM, E, a.e[t], Wx_av, P + lo.av.b, ad_av, ln_ptrs(P, lo.av), a.ea, nullptr, a.msg,
-                            a.zv[t], 2 * D);
-          J.j[J.n++].xcopy = a.e[t + 1];  // e^{t+1} = e^t outside G^b (the bond rows are updated after)
-        }
-        if (which & 2)
-          J.j[J.n++] = mm_job(FWD_BOND, A, a.a[t], Wx_be, P + lo.be.b, ad_be, ln_ptrs(P, lo.be), a.eb, a.ang_b2,
-                              a.msgb, a.zae[t], 4 * D);
-        if (which & 4)
-          J.j[J.n++] = mm_job(FWD_ANGLE, A, a.a[t], Wx_an, P + lo.an.b, ad_an, ln_ptrs(P, lo.an), a.a[t], nullptr,
-                              a.a[t + 1], a.zae[t] + 2 * D, 4 * D);
-        return gate_fwd_mm_launch(J, st);
-      }
-      // edge and angle terms (+ bias) by the GEMM; the gathered atom and bond
-      // terms are added by the gate kernels, which stream each row once
-      std::vector<GemmProblem> ps;
+      // pre-activations formed inside the gate kernel; z kept for a backward
+      // pass unless the caller asked for none
+      GateMmJobs J{};
+      float* zv = c.save_z ? a.zv[t] : nullptr;
+      float* zae = c.save_z ? a.zae[t] : nullptr;
       if (which & 1) {
-        GemmProblem p = gp(E, 2 * D, a.zv[t], 2 * D);
-        seg(p, a.e[t], D, 0, D, Wx_av, 2 * D, 0);
-        p.bias = P + lo.av.b;
-        ps.push_back(p);
+        J.j[J.n] = mm_job(D, FWD_ATOM, E, a.e[t], Wx_av, P + lo.av.b, ad_av, ln_ptrs(P, lo.av), a.ea, nullptr, a.msg,
+                          zv, 2 * D);
+        J.j[J.n++].xcopy = a.e[t + 1];  // e^{t+1} = e^t outside G^b (the bond rows are updated after)
       }
-      for (int k = 0; k < 2; ++k) {
-        if (!(which & (2 << k))) continue;
-        GemmProblem q = gp(A, 2 * D, a.zae[t] + k * 2 * D, 4 * D);
-        seg(q, a.a[t], D, 0, D, k ? Wx_an : Wx_be, 2 * D, 0);
-        q.bias = P + (k ? lo.an.b : lo.be.b);
-        ps.push_back(q);
-      }
-      CHG_TRY(run_gemms(ps, st, "gemm_z"));
-      GateFwdJobs J{};
-      if (which & 1) J.j[J.n++] = fwd_job(FWD_ATOM, E, a.zv[t], 2 * D, ad_av, ln_ptrs(P, lo.av), a.ea, nullptr, a.msg);
       if (which & 2)
-        J.j[J.n++] = fwd_job(FWD_BOND, A, a.zae[t], 4 * D, ad_be, ln_ptrs(P, lo.be), a.eb, a.ang_b2, a.msgb);
+        J.j[J.n++] = mm_job(D, FWD_BOND, A, a.a[t], Wx_be, P + lo.be.b, ad_be, ln_ptrs(P, lo.be), a.eb, a.ang_b2,
+                            a.msgb, zae, 4 * D);
       if (which & 4)
-        J.j[J.n++] = fwd_job(FWD_ANGLE, A, a.zae[t] + 2 * D, 4 * D, ad_an, ln_ptrs(P, lo.an), a.a[t], nullptr,
-                             a.a[t + 1]);
-      return gate_fwd_launch(D, J, st);
+        J.j[J.n++] = mm_job(D, FWD_ANGLE, A, a.a[t], Wx_an, P + lo.an.b, ad_an, ln_ptrs(P, lo.an), a.a[t], nullptr,
+                            a.a[t + 1], zae ? zae + 2 * D : nullptr, 4 * D);
+      return gate_fwd_mm_launch(D, J, st);
     };
     // messages: m_i = sum over out-edges of e^a * phi_v; mu_b = eb_b * sum over
     // angles (b, b2) of eb_b2 * phi_e
@@ -2646,11 +2571,7 @@ int forward_impl(Ctx& c, const float* Pflat, float* energy, float* forces, float
         ps.push_back(p);
       }
       if (which & 2) {
-        if (E > 0 && D != 64) {  // at d = 64 the atom-conv gate launch wrote the copy
-          const int64_t n4 = E * D / 4;  // d is a multiple of 4 and the arena aligns to 256 B
-          KLAUNCH(st, "k_copy", k_copy4<<<(unsigned)std::min<int64_t>(cdiv(n4, 256), 4096), 256, 0, st>>>(
-                                    reinterpret_cast<float4*>(a.e[t + 1]), reinterpret_cast<const float4*>(a.e[t]), n4));
-        }
+        // the atom-conv gate launch wrote e^{t+1} = e^t; the bond rows follow
         GemmProblem p = gp(B, D, a.e[t + 1], D);
         seg(p, a.mu[t], D, 0, D, P + lo.be_Wo, D, 0);
         p.bias = P + lo.be_bo;
@@ -3294,6 +3215,7 @@ int conservative_impl(Ctx& c, float* forces, float* stress, hipStream_t st) {
 // Forward pass with the readout the hyperparameters select.
 int forward_full(Ctx& c, const float* Pflat, float* energy, float* forces, float* stress, float* magmom,
                  hipStream_t st, bool pack = true) {
+  if (c.hp->conservative) c.save_z = true;  // its readout runs the backward of E
   CHG_TRY(forward_impl(c, Pflat, energy, forces, stress, magmom, st, pack));
   if (c.hp->conservative) CHG_TRY(conservative_impl(c, forces, stress, st));
   return CHGNET_OK;
@@ -3313,11 +3235,12 @@ size_t acts_bytes(const chgnet_hparams& hp, int64_t N, int64_t E, int64_t B, int
 }
 
 int forward_entry(const chgnet_hparams* hp, const chgnet_batch* batch, const chgnet_graph* graph, const float* params,
-                  float* energy, float* forces, float* stress, float* magmom, void* ws, size_t ws_bytes,
-                  hipStream_t st) {
+                  float* energy, float* forces, float* stress, float* magmom, int save_for_backward, void* ws,
+                  size_t ws_bytes, hipStream_t st) {
   Ctx c;
   CHG_TRY(make_ctx(hp, batch, graph, ws, ws_bytes, c));
   if (!params || !energy || !forces || !stress) return fail(CHGNET_EINVAL, "forward: null output or params");
+  c.save_z = save_for_backward != 0;
   if (magmom && !hp->magmom) return fail(CHGNET_EINVAL, "forward: magmom output without the magnetic-moment head");
   return forward_full(c, params, energy, forces, stress, magmom, st);
 }
@@ -3405,6 +3328,7 @@ int md_entry(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_graph* 
     CHG_TRY(build_graph(hp, b, graph, ws, ws_bytes, st));
     Ctx c;
     CHG_TRY(make_ctx(hp, b, graph, ws, ws_bytes, c));
+    c.save_z = false;  // no backward pass follows (the conservative readout keeps its own)
     CHG_TRY(forward_full(c, params, s->energy ? s->energy : c.a.out_E, s->forces, s->stress ? s->stress : c.a.out_S,
                          nullptr, st, !packed));
     packed = true;

@@ -183,6 +183,31 @@ def test_adam_update(bd):
         assert np.all(np.abs(pg - pr) <= 2 * lr * t + 1e-5 + 1e-4 * np.abs(pr)), "adam step bound"
 
 
+@pytest.mark.parametrize("d,T", [(64, 4), (128, 5)])
+def test_forward_without_saved_activations(bd, d, T):
+    """save_for_backward = 0 skips the stored pre-activations; the outputs are
+    bitwise those of a forward that keeps them, and a backward after a saving
+    forward still matches the oracle."""
+    b = synth.random_crystals(seed=41, n_struct=3, n_lo=6, n_hi=20)
+    params = synth.make_params(d, T, seed=(41, 1, d))
+    hp, db, g, ws = _setup(bd, b, d, T)
+    p = _dev(params)
+    out0 = [x.cpu().numpy().copy() for x in bd.forward(hp, db, g, p, ws, save_for_backward=False)]
+    out1 = [x.cpu().numpy().copy() for x in bd.forward(hp, db, g, p, ws, save_for_backward=True)]
+    for x0, x1 in zip(out0, out1):
+        assert np.array_equal(x0, x1)
+    ohp = om.HParams(d=d, n_layers=T)
+    rE, rF, rS, cache = om.forward(ohp, b, og.build_graph(b.atom_ptr, b.pos, b.lattice), params.astype(np.float64))
+    assert_close(out0[0], rE, "energy")
+    assert_close(out0[1], rF, "forces")
+    rng = np.random.default_rng(3)
+    dE = rng.standard_normal(b.n_struct).astype(np.float32)
+    dF = rng.standard_normal((b.n_atoms, 3)).astype(np.float32)
+    dS = rng.standard_normal((b.n_struct, 3, 3)).astype(np.float32)
+    grad = bd.backward(hp, db, g, p, _dev(dE), _dev(dF), _dev(dS), ws).cpu().numpy()
+    assert_close(grad, om.backward(ohp, cache, dE, dF, dS), "gradient after a saving forward")
+
+
 def test_adam_kernel_on_its_own_gradient(bd):
     """The Adam update alone: at t = 1, 2, 3 the oracle's Adam is applied, in
     fp64, to the GPU's own parameters, moments and gradient of that step, and
