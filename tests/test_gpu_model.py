@@ -157,6 +157,39 @@ def test_super4096_forward(bd):
     assert_close(S.cpu().numpy(), rS, "super4096 stress")
 
 
+def test_super4096_training_step(bd):
+    """One full training step on the 4096-atom supercell (graph, forward,
+    loss, backward) against the oracle's step stored in
+    tests/golden/super4096_step.npz (written by make_super4096_step.py, which
+    calls only the oracle; the oracle needs several minutes and ~16 GB for
+    this cell). The stored inputs' digest must match the seeded inputs."""
+    import importlib.util
+    import os
+
+    gdir = os.path.join(os.path.dirname(__file__), "golden")
+    spec = importlib.util.spec_from_file_location("mk4096", os.path.join(gdir, "make_super4096_step.py"))
+    mk = importlib.util.module_from_spec(spec)
+    spec.loader.exec_module(mk)
+    ref = np.load(os.path.join(gdir, "super4096_step.npz"), allow_pickle=False)
+    b, params, targets, d, T = synth.workload_inputs("super4096")
+    assert str(ref["inputs_sha256"]) == mk.input_digest(b, params, targets), "golden made from other inputs"
+    hp, db, g, ws = _setup(bd, b, d, T)
+    p = _dev(params)
+    E, F, S = bd.forward(hp, db, g, p, ws)
+    assert g.n_edges == int(ref["n_edges"])
+    assert_close(E.cpu().numpy(), ref["energy"], "super4096 energy")
+    assert_close(F.cpu().numpy(), ref["forces"], "super4096 forces")
+    assert_close(S.cpu().numpy(), ref["stress"], "super4096 stress")
+    loss, grad = bd.step(hp, db, g, p, [_dev(x) for x in targets], ws)
+    assert_close(loss.cpu().numpy(), [float(ref["loss"])], "super4096 loss")
+    gg = grad.cpu().numpy()
+    rg = ref["grad"].astype(np.float64)
+    lay, _ = om.layout(om.HParams(d=d, n_layers=T))
+    for tname, (off, shape) in lay.items():
+        n = int(np.prod(shape))
+        assert_close(gg[off:off + n], rg[off:off + n], "super4096 grad " + tname)
+
+
 def test_adam_update(bd):
     b, params, targets, d, T = synth.workload_inputs("cubic8")
     hp, db, g, ws = _setup(bd, b, d, T)
