@@ -31,7 +31,7 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="wide128")
+    ap.add_argument("--workload", default=None, help="default: wide128 (training, inference), cubic8 (--md)")
     ap.add_argument("--magmom", action="store_true", help="model variant: magnetic-moment head and its loss term")
     ap.add_argument("--huber", type=float, default=0.0, help="model variant: Huber loss with this delta (0 = MSE)")
     ap.add_argument("--sequential", action="store_true", help="model variant: the Eq. (10) interaction block")
@@ -52,9 +52,14 @@ def parse():
     ap.add_argument("--md", action="store_true",
                     help="time velocity-Verlet molecular dynamics (forward only) instead of training steps")
     ap.add_argument("--md-replicas", type=int, default=1, help="independent copies of the crystal stepped together")
+    ap.add_argument("--md-skin", type=float, default=0.0,
+                    help="MD neighbour-list reuse: Verlet skin in A (0 = full graph search every step)")
     ap.add_argument("--traffic-summary", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="no GPU: reduce two rocprofv3 counter CSVs (FETCH_SIZE, WRITE_SIZE) to a markdown summary")
-    return ap.parse_args()
+    args = ap.parse_args()
+    if args.workload is None and not args.md:
+        args.workload = "wide128"
+    return args
 
 
 def main():
@@ -198,7 +203,7 @@ def md_bench(args, bd, synth, dev):
     import numpy as np
     import torch
 
-    workload = args.workload if args.workload != "triclinic40" else "cubic8"
+    workload = args.workload or "cubic8"
     b0, params, _, d, T = synth.workload_inputs(workload)
     R = max(1, args.md_replicas)
     if R > 1:
@@ -217,14 +222,22 @@ def md_bench(args, bd, synth, dev):
     vel = torch.tensor((rng.standard_normal((b.n_atoms, 3)) * 0.01).astype(np.float32), device=dev)
     inv_m = torch.tensor((1.0 / rng.uniform(6.0, 60.0, b.n_atoms)).astype(np.float32), device=dev)
     dt = 0.5
-    F, E, S = bd.md(hp, db, g, p, vel, inv_m, dt, max(args.warmup, 1), ws)
+    skin = args.md_skin
+    cand = bd.MdList(b.n_atoms, 4096, dev) if skin > 0 else None
+    # a stream of its own (default priority): on it chgnet_md captures and
+    # replays the forward pass of steps whose graph sizes repeat
     torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    wall0 = time.perf_counter()
-    e0.record()
-    bd.md(hp, db, g, p, vel, inv_m, dt, args.steps, ws, forces=F, energy=E, stress=S)
-    e1.record()
-    torch.cuda.synchronize()
+    side = torch.cuda.Stream(dev)
+    with torch.cuda.stream(side):
+        F, E, S = bd.md(hp, db, g, p, vel, inv_m, dt, max(args.warmup, 1), ws, skin=skin, cand=cand)
+        torch.cuda.synchronize()
+        builds0 = cand.n_builds if cand else 0
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        wall0 = time.perf_counter()
+        e0.record()
+        bd.md(hp, db, g, p, vel, inv_m, dt, args.steps, ws, forces=F, energy=E, stress=S, skin=skin, cand=cand)
+        e1.record()
+        torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
     ms = e0.elapsed_time(e1) / args.steps
     return {
@@ -235,6 +248,8 @@ def md_bench(args, bd, synth, dev):
         "config": {"workload": "md-" + workload, "structures": b.n_struct, "atoms": b.n_atoms,
                    "replicas": R, "edges": g.n_edges, "bonds": g.n_bonds, "angles": g.n_angles, "d": d,
                    "layers": T, "integrator": "velocity Verlet, dt %.1f fs" % dt,
+                   "neighbour_list": ("candidates within r + %.2f A, rebuilt %d times in the timed steps"
+                                      % (skin, cand.n_builds - builds0)) if skin > 0 else "full search every step",
                    "block": "Eq. 10 (sequential)" if args.sequential else "Eq. 11",
                    "readout": "conservative (F = -dE/dr)" if args.conservative else "direct force/stress heads"},
         "atom_steps_per_s": round(b.n_atoms * 1e3 / ms, 1),

@@ -217,7 +217,15 @@ int chgnet_step(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_grap
                 const chgnet_loss* loss_cfg, float* loss, float* grad, float* adam_m, float* adam_v,
                 const float* adam_hp, void* ws, size_t ws_bytes, void* stream);
 
-/* Molecular-dynamics state of a batch (device arrays; Sec. V, Table 2). */
+/* Molecular-dynamics state of a batch (device arrays unless noted; Sec. V,
+ * Table 2). Neighbour-list reuse (Verlet skin): with skin > 0 the call keeps
+ * a candidate list of every pair within r_atom + skin of the positions at its
+ * build (in the caller's cand_* arrays) and, at each step, filters it with
+ * the exact cutoff test of chgnet_graph at the new positions, which gives the
+ * same graph as a full search as long as no atom has moved more than
+ * (skin - 0.01 A) / 2 since the list was built; the list is rebuilt (cell-list
+ * search at r_atom + skin) at the first step of a call and whenever that no
+ * longer holds. */
 typedef struct {
   float* pos;            /* [N,3] positions, A (the batch's pos array); updated   */
   float* vel;            /* [N,3] velocities, A/fs; updated                       */
@@ -226,6 +234,15 @@ typedef struct {
                             written at the end                                    */
   float* energy;         /* [S] energies at the final positions, eV (or NULL)     */
   float* stress;         /* [S,3,3] stresses at the final positions (or NULL)     */
+  float skin;            /* host: 0 = full search every step, else in (0.02, 2] A */
+  int64_t cap_cand;      /* host in: capacity of cand_dst / cand_img              */
+  int64_t n_cand;        /* host out: pairs on the last list built (also when
+                            CHGNET_ECAPACITY reports the list too long)           */
+  int32_t* cand_ptr;     /* [N+1] CSR offsets of the list by source atom          */
+  int32_t* cand_dst;     /* [cap_cand] destination atom of each candidate         */
+  int32_t* cand_img;     /* [cap_cand,3] lattice translation of each candidate    */
+  float* ref_pos;        /* [N,3] positions at the last list build                */
+  int32_t n_builds;      /* host out: lists built during the call                 */
 } chgnet_md_state;
 
 /* n_steps of NVE velocity-Verlet molecular dynamics with the model's direct
@@ -233,14 +250,19 @@ typedef struct {
  * forward at the new x; v += dt/2 a, with a = F / m * 0.0096485332157 A/fs^2
  * per eV/(A u) (dt in fs). batch->pos must equal state->pos. If forces_valid
  * is 0 the forces at the initial positions are computed first. Every step
- * rebuilds the graph (one wait for its sizes, as chgnet_build_graph);
- * positions are not wrapped into the cell. *steps_done (host) receives the
+ * forms the graph at the new positions, by a full search or from the
+ * candidate list (see chgnet_md_state), with one wait for its sizes; once two
+ * consecutive steps have graphs of the same sizes, the forward pass and the
+ * second half-kick are captured into a HIP graph (on a non-null stream, with
+ * the direct heads) and replayed while the sizes stay the same. Positions
+ * are not wrapped into the cell. With skin > 0, CHGNET_ECAPACITY may also
+ * mean that cap_cand < n_cand: grow the list and call again. *steps_done (host) receives the
  * number of completed steps: on CHGNET_ECAPACITY the state is that of the
  * last completed step with valid forces; grow the graph and call again for
  * the remaining steps with forces_valid = 1. The model variant of hp applies
  * (conservative forces included; magmom is not returned). Errors as for chgnet_build_graph. */
 int chgnet_md(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_graph* graph, const float* params,
-              const chgnet_md_state* state, float dt, int n_steps, int forces_valid, int* steps_done, void* ws,
+              chgnet_md_state* state, float dt, int n_steps, int forces_valid, int* steps_done, void* ws,
               size_t ws_bytes, void* stream);
 
 /* Text of the last error on the calling thread ("" if none). */

@@ -43,7 +43,10 @@ class LossCfg(ctypes.Structure):
 
 class MdState(ctypes.Structure):
     _fields_ = [("pos", ctypes.c_void_p), ("vel", ctypes.c_void_p), ("inv_mass", ctypes.c_void_p),
-                ("forces", ctypes.c_void_p), ("energy", ctypes.c_void_p), ("stress", ctypes.c_void_p)]
+                ("forces", ctypes.c_void_p), ("energy", ctypes.c_void_p), ("stress", ctypes.c_void_p),
+                ("skin", ctypes.c_float), ("cap_cand", ctypes.c_int64), ("n_cand", ctypes.c_int64),
+                ("cand_ptr", ctypes.c_void_p), ("cand_dst", ctypes.c_void_p), ("cand_img", ctypes.c_void_p),
+                ("ref_pos", ctypes.c_void_p), ("n_builds", ctypes.c_int32)]
 
 
 class CBatch(ctypes.Structure):
@@ -343,10 +346,29 @@ def step(hp, batch, graph, params, targets, ws, loss_w=(2.0, 1.5, 0.1, 0.1), hub
     raise ChgnetError(CHGNET_ECAPACITY, "graph capacity retry failed")
 
 
-def md(hp, batch, graph, params, vel, inv_mass, dt, n_steps, ws, forces=None, energy=None, stress=None):
-    """n_steps of velocity-Verlet MD (chgnet_md) on batch.pos and vel in place, growing the graph when
-    its capacity runs out. forces: [N,3] forces at batch.pos (computed first if None). Returns
-    (forces, energy, stress) at the final positions."""
+class MdList:
+    """Device arrays of chgnet_md's candidate list (Verlet skin)."""
+
+    def __init__(self, n_atoms, cap, device="cuda"):
+        self.cap = int(cap)
+        self.ptr = torch.zeros(n_atoms + 1, dtype=torch.int32, device=device)
+        self.dst = torch.zeros(max(self.cap, 1), dtype=torch.int32, device=device)
+        self.img = torch.zeros(max(self.cap, 1), 3, dtype=torch.int32, device=device)
+        self.ref = torch.zeros(n_atoms, 3, dtype=torch.float32, device=device)
+        self.n_builds = 0
+        self.n_cand = 0
+
+    def grow(self, n, device):
+        self.cap = int(n * 1.25) + 64
+        self.dst = torch.zeros(self.cap, dtype=torch.int32, device=device)
+        self.img = torch.zeros(self.cap, 3, dtype=torch.int32, device=device)
+
+
+def md(hp, batch, graph, params, vel, inv_mass, dt, n_steps, ws, forces=None, energy=None, stress=None, skin=0.0,
+       cand=None):
+    """n_steps of velocity-Verlet MD (chgnet_md) on batch.pos and vel in place, growing the graph (and the
+    candidate list with skin > 0) when its capacity runs out. forces: [N,3] forces at batch.pos (computed
+    first if None). cand: an MdList to use (one is made if None). Returns (forces, energy, stress)."""
     dev = batch.pos.device
     S, N = batch.n_struct, batch.n_atoms
     valid = forces is not None
@@ -356,12 +378,17 @@ def md(hp, batch, graph, params, vel, inv_mass, dt, n_steps, ws, forces=None, en
         energy = torch.empty(S, dtype=torch.float32, device=dev)
     if stress is None:
         stress = torch.empty(S, 3, 3, dtype=torch.float32, device=dev)
-    st = MdState(_ptr(batch.pos).value, _ptr(vel).value, _ptr(inv_mass).value, _ptr(forces).value,
-                 _ptr(energy).value, _ptr(stress).value)
+    if skin > 0 and cand is None:
+        cand = MdList(N, 1024, dev)
     cb = batch.c()
     left = n_steps
-    for _ in range(8):
+    for _ in range(12):
         ensure_ws(hp, batch, graph, ws)
+        st = MdState(_ptr(batch.pos).value, _ptr(vel).value, _ptr(inv_mass).value, _ptr(forces).value,
+                     _ptr(energy).value, _ptr(stress).value, float(skin))
+        if skin > 0:
+            st.cap_cand, st.cand_ptr, st.cand_dst = cand.cap, _ptr(cand.ptr).value, _ptr(cand.dst).value
+            st.cand_img, st.ref_pos = _ptr(cand.img).value, _ptr(cand.ref).value
         cg = graph.c()
         done = ctypes.c_int(0)
         code = lib().chgnet_md(ctypes.byref(hp), ctypes.byref(cb), ctypes.byref(cg), _ptr(params), ctypes.byref(st),
@@ -369,8 +396,15 @@ def md(hp, batch, graph, params, vel, inv_mass, dt, n_steps, ws, forces=None, en
         graph.take_counts(cg)
         left -= done.value
         valid = valid or done.value > 0
+        if skin > 0:
+            cand.n_builds += st.n_builds
+            cand.n_cand = st.n_cand
         if code == CHGNET_ECAPACITY:
-            graph.resize(int(cg.n_edges * 1.25) + 64, int(cg.n_bonds * 1.25) + 64, int(cg.n_angles * 1.25) + 64, dev)
+            if skin > 0 and st.n_cand > cand.cap:
+                cand.grow(st.n_cand, dev)
+            else:
+                graph.resize(int(cg.n_edges * 1.25) + 64, int(cg.n_bonds * 1.25) + 64, int(cg.n_angles * 1.25) + 64,
+                             dev)
             continue
         _check(code)
         return forces, energy, stress

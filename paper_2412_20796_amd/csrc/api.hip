@@ -26,7 +26,7 @@ int step_entry(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_graph
                float* loss, float* grad, float* adam_m, float* adam_v, const float* adam_hp, void* ws,
                size_t ws_bytes, hipStream_t st);
 int md_entry(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_graph* graph, const float* params,
-             const chgnet_md_state* s, float dt, int n_steps, int forces_valid, int* steps_done, void* ws,
+             chgnet_md_state* s, float dt, int n_steps, int forces_valid, int* steps_done, void* ws,
              size_t ws_bytes, hipStream_t st);
 
 namespace {
@@ -196,7 +196,7 @@ int chgnet_step(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_grap
 }
 
 int chgnet_md(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_graph* graph, const float* params,
-              const chgnet_md_state* state, float dt, int n_steps, int forces_valid, int* steps_done, void* ws,
+              chgnet_md_state* state, float dt, int n_steps, int forces_valid, int* steps_done, void* ws,
               size_t ws_bytes, void* stream) {
   return chg::md_entry(hp, batch, graph, params, state, dt, n_steps, forces_valid, steps_done, ws, ws_bytes,
                        static_cast<hipStream_t>(stream));

@@ -13,6 +13,7 @@
 
 #include <climits>
 #include <cmath>
+#include <cstring>
 #include <mutex>
 
 #include "common.hpp"
@@ -43,6 +44,8 @@ struct GraphInfo {
   long long n_edges, n_bonds, n_angles;
   int max_count;
   int err;
+  unsigned int max_disp2;  // MD neighbour-list reuse: largest squared displacement (fp32 bits)
+  int pad;
 };
 
 // ---------------------------------------------------------------------------
@@ -595,7 +598,7 @@ namespace {
 // sizes come back through a small pinned host buffer of the calling thread
 // (allocated on its first use); otherwise through a pageable host variable.
 int build_graph_impl(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_graph* graph, void* ws,
-                     size_t ws_bytes, hipStream_t st, bool pinned_readback) {
+                     size_t ws_bytes, hipStream_t st, bool pinned_readback, bool candidates = false) {
   CHG_TRY(validate_hparams(hp));
   CHG_TRY(validate_batch(batch));
   if (!graph || !graph->edge_ptr || !graph->bond_ptr) return fail(CHGNET_EINVAL, "graph: edge_ptr and bond_ptr are required");
@@ -620,7 +623,7 @@ int build_graph_impl(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet
   SearchArgs A;
   A.N = N;
   A.rc2_atom = hp->r_atom * hp->r_atom;
-  A.rc2_bond = hp->r_bond * hp->r_bond;
+  A.rc2_bond = candidates ? -1.0f : hp->r_bond * hp->r_bond;  // a candidate list has no bonds
   A.pos = batch->pos;
   A.info = g.info;
   A.atom_struct = g.atom_struct;
@@ -663,6 +666,15 @@ int build_graph_impl(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet
     return fail(CHGNET_EINVAL, "build_graph: graph larger than 2^31 entries");
   if (hinfo.n_edges > graph->cap_edges || hinfo.n_bonds > graph->cap_bonds || hinfo.n_angles > graph->cap_angles)
     return fail(CHGNET_ECAPACITY, "build_graph: capacity too small (required sizes written to the graph)");
+  if (candidates) {
+    if (hinfo.n_edges > 0 && (!graph->edge_dst || !graph->edge_img))
+      return fail(CHGNET_EINVAL, "md: candidate arrays are required");
+    int sort_size = 64;
+    while (sort_size < hinfo.max_count) sort_size <<= 1;
+    KLAUNCH(st, "k_fill", k_fill<<<N, kSearchThreads, sizeof(unsigned long long) * sort_size, st>>>(
+                              A, sort_size, graph->edge_ptr, graph->bond_ptr, graph->edge_dst, graph->edge_img, nullptr));
+    return CHGNET_OK;
+  }
   if (hinfo.n_edges > 0 && (!graph->edge_dst || !graph->edge_img || !graph->edge_rev))
     return fail(CHGNET_EINVAL, "graph: edge arrays are required");
   if (!graph->angle_ptr || (hinfo.n_bonds > 0 && !graph->bond_edge))
@@ -676,6 +688,112 @@ int build_graph_impl(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet
                                                                        graph->edge_rev, graph->bond_ptr, g.angle_base,
                                                                        graph->angle_ptr, graph->angle_b2));
   return CHGNET_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Molecular dynamics: reuse of a candidate list (Verlet skin). The list holds
+// every pair within r + skin of the positions at its build, in the canonical
+// (j, n) order of each source atom. While no atom has moved more than
+// (skin - 0.01 A) / 2 since then, every pair now within r is on the list, and
+// filtering it with the exact cutoff test at the current positions gives the
+// same graph, in the same order, as a full search.
+// ---------------------------------------------------------------------------
+__global__ void __launch_bounds__(256) k_md_disp(int n, const float* __restrict__ pos, const float* __restrict__ ref,
+                                                 GraphInfo* ginfo) {
+  __shared__ float red[4];
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  float d2 = 0.f;
+  if (i < n) {
+    const float dx = pos[3 * i] - ref[3 * i], dy = pos[3 * i + 1] - ref[3 * i + 1], dz = pos[3 * i + 2] - ref[3 * i + 2];
+    d2 = dx * dx + dy * dy + dz * dz;
+  }
+  for (int off = 32; off > 0; off >>= 1) d2 = fmaxf(d2, __shfl_xor(d2, off, 64));
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = d2;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const float m = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+    atomicMax(&ginfo->max_disp2, __float_as_uint(m));  // non-negative floats order as their bits
+  }
+}
+
+struct CandArgs {
+  int N, S;
+  float rc2_atom, rc2_bond;
+  const int* atom_ptr;
+  const float* pos;
+  const float* lattice;
+  const int* cand_ptr;
+  const int* cand_dst;
+  const int* cand_img;
+};
+
+// Cutoff test of candidate c of atom i at the current positions.
+__device__ __forceinline__ float cand_d2(const CandArgs& A, int i, const float* L, const float (&ri)[3], int c,
+                                         int& j) {
+  j = A.cand_dst[c];
+  const float rj[3] = {A.pos[3 * j], A.pos[3 * j + 1], A.pos[3 * j + 2]};
+  return pair_d2(i, j, ri, rj, A.cand_img[3 * c], A.cand_img[3 * c + 1], A.cand_img[3 * c + 2], L);
+}
+
+// Edges and bonds of each atom among its candidates; one wavefront per atom.
+__global__ void __launch_bounds__(256) k_cand_count(CandArgs A, int* __restrict__ edge_count, int* __restrict__ bond_count) {
+  const int i = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (i >= A.N) return;
+  const int s = find_struct(A.atom_ptr, A.S, i);
+  float L[9];
+  for (int k = 0; k < 9; ++k) L[k] = A.lattice[9 * s + k];
+  const float ri[3] = {A.pos[3 * i], A.pos[3 * i + 1], A.pos[3 * i + 2]};
+  int ne = 0, nb = 0;
+  for (int c = A.cand_ptr[i] + lane; c < A.cand_ptr[i + 1]; c += 64) {
+    int j;
+    const float dd = cand_d2(A, i, L, ri, c, j);
+    ne += dd < A.rc2_atom ? 1 : 0;
+    nb += dd < A.rc2_bond ? 1 : 0;
+  }
+  for (int off = 32; off > 0; off >>= 1) {
+    ne += __shfl_xor(ne, off, 64);
+    nb += __shfl_xor(nb, off, 64);
+  }
+  if (lane == 0) {
+    edge_count[i] = ne;
+    bond_count[i] = nb;
+  }
+}
+
+// The kept candidates of each atom in list order (one wavefront per atom,
+// 64 candidates per round, compacted by ballot): edge arrays and bond list.
+__global__ void __launch_bounds__(256) k_cand_fill(CandArgs A, const int* __restrict__ edge_ptr,
+                                                   const int* __restrict__ bond_ptr, int* __restrict__ edge_dst,
+                                                   int* __restrict__ edge_img, int* __restrict__ bond_edge) {
+  const int i = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (i >= A.N) return;
+  const int s = find_struct(A.atom_ptr, A.S, i);
+  float L[9];
+  for (int k = 0; k < 9; ++k) L[k] = A.lattice[9 * s + k];
+  const float ri[3] = {A.pos[3 * i], A.pos[3 * i + 1], A.pos[3 * i + 2]};
+  int e = edge_ptr[i], b = bond_ptr[i];
+  const unsigned long long below = (1ull << lane) - 1ull;
+  for (int c0 = A.cand_ptr[i]; c0 < A.cand_ptr[i + 1]; c0 += 64) {
+    const int c = c0 + lane;
+    bool keep = false, bond = false;
+    int j = 0;
+    if (c < A.cand_ptr[i + 1]) {
+      const float dd = cand_d2(A, i, L, ri, c, j);
+      keep = dd < A.rc2_atom;
+      bond = dd < A.rc2_bond;
+    }
+    const unsigned long long mk = __ballot(keep), mb = __ballot(bond);
+    if (keep) {
+      const int k = e + __popcll(mk & below);
+      edge_dst[k] = j;
+      edge_img[3 * k] = A.cand_img[3 * c];
+      edge_img[3 * k + 1] = A.cand_img[3 * c + 1];
+      edge_img[3 * k + 2] = A.cand_img[3 * c + 2];
+      if (bond) bond_edge[b + __popcll(mb & below)] = k;
+    }
+    e += __popcll(mk);
+    b += __popcll(mb);
+  }
 }
 
 // Scratch of the allocation-free graph build: one array per GPU, held until
@@ -723,6 +841,79 @@ int build_graph_noalloc(const chgnet_hparams* hp, const chgnet_batch* batch, chg
   void* p = nullptr;
   CHG_TRY(scratch_address(&p));
   return build_graph_impl(hp, batch, graph, p, kNoAllocScratchBytes, st, false);
+}
+
+// Candidate list of every pair within r_atom + skin of the batch's current
+// positions into s->cand_* (bonds are not kept), and those positions into
+// s->ref_pos. graph->bond_ptr serves as scratch.
+int md_build_candidates(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_md_state* s, chgnet_graph* graph,
+                        void* ws, size_t ws_bytes, hipStream_t st) {
+  chgnet_hparams hc = *hp;
+  hc.r_atom = hp->r_atom + s->skin;
+  hc.r_bond = hc.r_atom;
+  chgnet_graph cg{};
+  cg.cap_edges = s->cap_cand;
+  cg.edge_ptr = s->cand_ptr;
+  cg.edge_dst = s->cand_dst;
+  cg.edge_img = s->cand_img;
+  cg.bond_ptr = graph->bond_ptr;
+  const int code = build_graph_impl(&hc, batch, &cg, ws, ws_bytes, st, true, true);
+  s->n_cand = cg.n_edges;
+  if (code != CHGNET_OK) return code;
+  CHG_HIP(hipMemcpyAsync(s->ref_pos, batch->pos, sizeof(float) * 3 * batch->n_atoms, hipMemcpyDeviceToDevice, st));
+  s->n_builds += 1;
+  return CHGNET_OK;
+}
+
+// The graph of the batch's current positions from the candidate list. Sets
+// *stale (and builds nothing) when some atom has moved too far since the
+// list was built; otherwise as chgnet_build_graph (one wait for the sizes).
+int md_filter_graph(const chgnet_hparams* hp, const chgnet_batch* batch, const chgnet_md_state* s,
+                    chgnet_graph* graph, void* ws, size_t ws_bytes, hipStream_t st, bool* stale) {
+  *stale = false;
+  const int N = batch->n_atoms, S = batch->n_struct;
+  Arena ar{static_cast<char*>(ws), ws_bytes, 0};
+  GraphScratch g;
+  carve(ar, N, S, g);
+  if (!ws || !ar.ok()) return fail(CHGNET_EWORKSPACE, "workspace too small for the graph build");
+  KLAUNCH(st, "k_zero_scratch", k_zero_scratch<<<1, 256, 0, st>>>(g.ginfo, g.bin_count, g.bin_cursor, 1));
+  KLAUNCH(st, "k_md_disp", k_md_disp<<<(unsigned)cdiv(N, 256), 256, 0, st>>>(N, batch->pos, s->ref_pos, g.ginfo));
+  CandArgs A{N, S, hp->r_atom * hp->r_atom, hp->r_bond * hp->r_bond, batch->atom_ptr, batch->pos, batch->lattice,
+             s->cand_ptr, s->cand_dst, s->cand_img};
+  KLAUNCH(st, "k_cand_count", k_cand_count<<<(unsigned)cdiv(N, 4), 256, 0, st>>>(A, g.edge_count, g.bond_count));
+  KLAUNCH(st, "k_scan_counts", k_scan_counts<<<1, 1024, 0, st>>>(N, g.edge_count, g.bond_count, graph->edge_ptr,
+                                                                   graph->bond_ptr, g.angle_base, g.ginfo));
+  thread_local GraphInfo* pinned = nullptr;
+  if (!pinned) CHG_HIP(hipHostMalloc(reinterpret_cast<void**>(&pinned), sizeof(GraphInfo), hipHostMallocDefault));
+  CHG_HIP(hipMemcpyAsync(pinned, g.ginfo, sizeof(GraphInfo), hipMemcpyDeviceToHost, st));
+  CHG_HIP(hipStreamSynchronize(st));
+  const GraphInfo hinfo = *pinned;
+  // the list covers every pair within r of the current positions while twice
+  // the largest displacement stays below the skin (0.01 A spares fp32
+  // rounding of coordinates up to 10^4 A)
+  const float half = 0.5f * (s->skin - 0.01f);
+  float md2;
+  std::memcpy(&md2, &hinfo.max_disp2, sizeof(float));
+  if (!(md2 < half * half)) {
+    *stale = true;
+    return CHGNET_OK;
+  }
+  graph->n_edges = hinfo.n_edges;
+  graph->n_bonds = hinfo.n_bonds;
+  graph->n_angles = hinfo.n_angles;
+  if (hinfo.max_count > kMaxEdgesPerAtom) return fail(CHGNET_EINVAL, "build_graph: more than 8192 edges on one atom");
+  if (hinfo.n_edges >= INT_MAX || hinfo.n_angles >= INT_MAX)
+    return fail(CHGNET_EINVAL, "build_graph: graph larger than 2^31 entries");
+  if (hinfo.n_edges > graph->cap_edges || hinfo.n_bonds > graph->cap_bonds || hinfo.n_angles > graph->cap_angles)
+    return fail(CHGNET_ECAPACITY, "build_graph: capacity too small (required sizes written to the graph)");
+  KLAUNCH(st, "k_cand_fill", k_cand_fill<<<(unsigned)cdiv(N, 4), 256, 0, st>>>(A, graph->edge_ptr, graph->bond_ptr,
+                                                                              graph->edge_dst, graph->edge_img,
+                                                                              graph->bond_edge));
+  KLAUNCH(st, "k_rev_angles", k_rev_angles<<<2 * cdiv(N, 4), 256, 0, st>>>(N, graph->edge_ptr, graph->edge_dst,
+                                                                            graph->edge_img, graph->edge_rev,
+                                                                            graph->bond_ptr, g.angle_base,
+                                                                            graph->angle_ptr, graph->angle_b2));
+  return CHGNET_OK;
 }
 
 }  // namespace chg

@@ -3308,8 +3308,29 @@ int step_entry(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_graph
   return CHGNET_OK;
 }
 
+int md_build_candidates(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_md_state* s, chgnet_graph* graph,
+                        void* ws, size_t ws_bytes, hipStream_t st);
+int md_filter_graph(const chgnet_hparams* hp, const chgnet_batch* batch, const chgnet_md_state* s,
+                    chgnet_graph* graph, void* ws, size_t ws_bytes, hipStream_t st, bool* stale);
+
+// Ends a stream capture begun by the caller and turns it into an executable
+// graph (nullptr and the error of `code` if the captured work failed).
+int end_capture(hipStream_t st, int code, hipGraphExec_t* exec) {
+  hipGraph_t g = nullptr;
+  const hipError_t e = hipStreamEndCapture(st, &g);
+  if (code != CHGNET_OK) {
+    if (g) (void)hipGraphDestroy(g);
+    return code;
+  }
+  if (e != hipSuccess) return fail(CHGNET_EHIP, std::string("hipStreamEndCapture: ") + hipGetErrorString(e));
+  const hipError_t e2 = hipGraphInstantiate(exec, g, nullptr, nullptr, 0);
+  (void)hipGraphDestroy(g);
+  if (e2 != hipSuccess) return fail(CHGNET_EHIP, std::string("hipGraphInstantiate: ") + hipGetErrorString(e2));
+  return CHGNET_OK;
+}
+
 int md_entry(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_graph* graph, const float* params,
-             const chgnet_md_state* s, float dt, int n_steps, int forces_valid, int* steps_done, void* ws,
+             chgnet_md_state* s, float dt, int n_steps, int forces_valid, int* steps_done, void* ws,
              size_t ws_bytes, hipStream_t st) {
   if (steps_done) *steps_done = 0;
   CHG_TRY(validate_hparams(hp));
@@ -3317,15 +3338,37 @@ int md_entry(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_graph* 
   if (!s->pos || !s->vel || !s->inv_mass || !s->forces || s->pos != batch->pos)
     return fail(CHGNET_EINVAL, "md: state arrays missing or state->pos != batch->pos");
   if (!(dt > 0.f) || !std::isfinite(dt) || n_steps < 0) return fail(CHGNET_EINVAL, "md: need dt > 0 and n_steps >= 0");
+  const bool reuse = s->skin != 0.f;
+  if (reuse && (!(s->skin > 0.02f) || !(s->skin <= 2.0f) || !(hp->r_atom + s->skin <= 20.0f)))
+    return fail(CHGNET_EINVAL, "md: the skin must be 0 or in (0.02, 2] A with r_atom + skin <= 20");
+  if (reuse && (!s->cand_ptr || !s->ref_pos || s->cap_cand < 0 || (s->cap_cand > 0 && (!s->cand_dst || !s->cand_img))))
+    return fail(CHGNET_EINVAL, "md: the candidate list needs cand_ptr, cand_dst, cand_img and ref_pos");
+  s->n_builds = 0;
   // 1 eV / (A u) in A / fs^2: e / u * 1e10 m/s^2 = e / u * 1e-10 A/fs^2 (CODATA 2018 e and u)
   constexpr double kAccel = 1.602176634e-19 / 1.66053906660e-27 * 1e-10;
   const float h = (float)(0.5 * (double)dt * kAccel);
   const int n3 = 3 * batch->n_atoms;
   const unsigned nb = (unsigned)cdiv(n3, 256);
   chgnet_batch trial = *batch;
-  bool packed = false;
-  auto forces_at = [&](const chgnet_batch* b) -> int {
-    CHG_TRY(build_graph(hp, b, graph, ws, ws_bytes, st));
+  bool packed = false, have_list = false;
+  // the graph at b's positions: a full search, or the filtered candidate list
+  // (rebuilt at the first step of the call and whenever an atom has moved
+  // too far since its build)
+  auto graph_at = [&](const chgnet_batch* b) -> int {
+    if (!reuse) return build_graph(hp, b, graph, ws, ws_bytes, st);
+    for (int attempt = 0; attempt < 2; ++attempt) {
+      if (!have_list) {
+        CHG_TRY(md_build_candidates(hp, b, s, graph, ws, ws_bytes, st));
+        have_list = true;
+      }
+      bool stale = false;
+      CHG_TRY(md_filter_graph(hp, b, s, graph, ws, ws_bytes, st, &stale));
+      if (!stale) return CHGNET_OK;
+      have_list = false;
+    }
+    return fail(CHGNET_EHIP, "md: a fresh candidate list was reported stale");
+  };
+  auto forward_at = [&](const chgnet_batch* b) -> int {
     Ctx c;
     CHG_TRY(make_ctx(hp, b, graph, ws, ws_bytes, c));
     c.save_z = false;  // no backward pass follows (the conservative readout keeps its own)
@@ -3334,7 +3377,10 @@ int md_entry(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_graph* 
     packed = true;
     return CHGNET_OK;
   };
-  if (!forces_valid) CHG_TRY(forces_at(batch));
+  if (!forces_valid) {
+    CHG_TRY(graph_at(batch));
+    CHG_TRY(forward_at(batch));
+  }
   // trial positions and velocities sit in the workspace at an address that
   // does not depend on the graph sizes; a step that runs out of graph
   // capacity leaves the caller's state at the last completed step
@@ -3350,14 +3396,52 @@ int md_entry(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_graph* 
     pos2 = a.md_pos;
     vel2 = a.md_vel;
   }
-  for (int k = 0; k < n_steps; ++k) {
-    KLAUNCH(st, "k_md", k_md_kick_drift<<<nb, 256, 0, st>>>(n3, s->pos, s->vel, s->forces, s->inv_mass, h, dt, pos2, vel2));
-    trial.pos = pos2;
-    CHG_TRY(forces_at(&trial));
+  // The forward pass and the second half-kick of a step depend on the graph
+  // only through its sizes (the arrays are read from memory, the workspace
+  // layout follows the sizes), so once two consecutive steps have the same
+  // sizes that part is captured into a HIP graph and replayed while they
+  // stay the same. Not with the conservative readout (its backward forks a
+  // second stream), a null stream or per-launch timing.
+  const bool can_capture = st != nullptr && !prof_active() && !hp->conservative;
+  hipGraphExec_t exec = nullptr;
+  int64_t exec_sizes[3] = {-1, -1, -1}, prev[3] = {-1, -1, -1};
+  auto commit = [&]() -> int {
     KLAUNCH(st, "k_md", k_md_kick_commit<<<nb, 256, 0, st>>>(n3, pos2, vel2, s->forces, s->inv_mass, h, s->pos, s->vel));
-    *steps_done = k + 1;
-  }
-  return CHGNET_OK;
+    return CHGNET_OK;
+  };
+  auto run_steps = [&]() -> int {
+    for (int k = 0; k < n_steps; ++k) {
+      KLAUNCH(st, "k_md", k_md_kick_drift<<<nb, 256, 0, st>>>(n3, s->pos, s->vel, s->forces, s->inv_mass, h, dt, pos2, vel2));
+      trial.pos = pos2;
+      CHG_TRY(graph_at(&trial));
+      const int64_t sz[3] = {graph->n_edges, graph->n_bonds, graph->n_angles};
+      const bool same_prev = sz[0] == prev[0] && sz[1] == prev[1] && sz[2] == prev[2];
+      const bool same_exec = exec && sz[0] == exec_sizes[0] && sz[1] == exec_sizes[1] && sz[2] == exec_sizes[2];
+      if (can_capture && packed && !same_exec && same_prev) {
+        if (exec) {
+          CHG_HIP(hipGraphExecDestroy(exec));
+          exec = nullptr;
+        }
+        CHG_HIP(hipStreamBeginCapture(st, hipStreamCaptureModeThreadLocal));
+        int code = forward_at(&trial);
+        if (code == CHGNET_OK) code = commit();
+        CHG_TRY(end_capture(st, code, &exec));
+        for (int q = 0; q < 3; ++q) exec_sizes[q] = sz[q];
+        CHG_HIP(hipGraphLaunch(exec, st));
+      } else if (can_capture && same_exec) {
+        CHG_HIP(hipGraphLaunch(exec, st));
+      } else {
+        CHG_TRY(forward_at(&trial));
+        CHG_TRY(commit());
+      }
+      for (int q = 0; q < 3; ++q) prev[q] = sz[q];
+      *steps_done = k + 1;
+    }
+    return CHGNET_OK;
+  };
+  const int code = run_steps();
+  if (exec) (void)hipGraphExecDestroy(exec);
+  return code;
 }
 
 }  // namespace chg

@@ -1,7 +1,9 @@
 """GPU molecular dynamics (chgnet_md: velocity Verlet with the direct force
 head) against the oracle's integrator and forward pass: positions,
 velocities, forces, energies and stresses after several steps within
-|gpu - oracle| <= 1e-5 + 1e-4 |oracle|. The trajectories are chosen so that no
+|gpu - oracle| <= 1e-5 + 1e-4 |oracle|; the candidate-list (Verlet skin)
+graph and the captured forward pass bitwise against a full search every step
+and against eager one-step calls. The trajectories are chosen so that no
 atom pair comes within 1e-4 A of either cutoff, where fp32 and fp64 positions
 could disagree on the graph."""
 import numpy as np
@@ -122,3 +124,78 @@ def test_md_zero_steps_gives_forward_forces(bd):
     assert np.array_equal(F.cpu().numpy(), F2.cpu().numpy())
     assert np.array_equal(E.cpu().numpy(), E2.cpu().numpy())
     assert np.array_equal(db.pos.cpu().numpy(), b.pos)
+
+
+def _md_on_stream(bd, b, params, v0, inv_m, dt, calls, d, T, skin=0.0, cand_cap=1024, cap=(64, 16, 64)):
+    """MD through `calls` (a list of step counts, one chgnet_md call each) on
+    a non-default stream, where chgnet_md may capture and replay its forward
+    pass. Returns the final state and the candidate list used."""
+    import torch
+
+    hp = bd.hparams(d=d, n_layers=T)
+    db = bd.DeviceBatch.from_host(b)
+    ws = bd.Workspace()
+    g = bd.DeviceGraph(b.n_atoms, *cap)
+    vel, im, p = _dev(v0), _dev(inv_m), _dev(params)
+    cand = bd.MdList(b.n_atoms, cand_cap) if skin > 0 else None
+    torch.cuda.synchronize()
+    s = torch.cuda.Stream()
+    F = E = S = None
+    with torch.cuda.stream(s):
+        for n in calls:
+            F, E, S = bd.md(hp, db, g, p, vel, im, dt, n, ws, forces=F, skin=skin, cand=cand)
+    torch.cuda.synchronize()
+    return (db.pos.cpu().numpy(), vel.cpu().numpy(), F.cpu().numpy(), E.cpu().numpy(), S.cpu().numpy()), cand
+
+
+def _md_inputs(b, seed):
+    rng = np.random.default_rng(seed)
+    v0 = (rng.standard_normal((b.n_atoms, 3)) * 0.02).astype(np.float32)
+    inv_m = (1.0 / rng.uniform(6.0, 60.0, b.n_atoms)).astype(np.float32)
+    return v0, inv_m
+
+
+@pytest.mark.parametrize("skin", [0.0, 0.5])
+def test_md_captured_steps_match_single_steps(bd, skin):
+    """Twelve steps in one call (the forward pass captured once graph sizes
+    repeat, then replayed, with the eager graph work and a host wait between
+    replays) against twelve one-step calls (never captured): bitwise equal
+    after 4, 8 and 12 steps."""
+    b, params, _, d, T = synth.workload_inputs("cubic8")
+    v0, inv_m = _md_inputs(b, 5)
+    for n in (4, 8, 12):
+        one, _ = _md_on_stream(bd, b, params, v0, inv_m, 0.5, [n], d, T, skin=skin)
+        many, _ = _md_on_stream(bd, b, params, v0, inv_m, 0.5, [1] * n, d, T, skin=skin)
+        for x, y, what in zip(one, many, ("pos", "vel", "forces", "energy", "stress")):
+            assert np.array_equal(x, y), (skin, n, what)
+
+
+def test_md_verlet_skin_is_exact(bd):
+    """The candidate list filtered every step gives the same trajectory,
+    bitwise, as a full search every step: slow atoms with a generous skin
+    (one list for the whole run), fast atoms (~0.05 A per step) with a
+    generous and a tight skin (rebuilt as atoms move; more often for the
+    tight one), and a list that starts with no capacity (regrown)."""
+    b, params, _, d, T = synth.workload_inputs("cubic8")
+    v0, inv_m = _md_inputs(b, 8)
+    big = (4096, 1024, 8192)  # graph room for one chgnet_md call (each call builds its own list)
+    builds = {}
+    for speed, skin, cap in ((1.0, 1.0, 4096), (5.0, 1.0, 4096), (5.0, 0.1, 4096), (5.0, 0.5, 1)):
+        ref, _ = _md_on_stream(bd, b, params, v0 * speed, inv_m, 0.5, [16], d, T, cap=big)
+        got, cand = _md_on_stream(bd, b, params, v0 * speed, inv_m, 0.5, [16], d, T, skin=skin, cand_cap=cap, cap=big)
+        print("speed", speed, "skin", skin, "list builds", cand.n_builds, "pairs", cand.n_cand, flush=True)
+        for x, y, what in zip(got, ref, ("pos", "vel", "forces", "energy", "stress")):
+            assert np.array_equal(x, y), (speed, skin, what)
+        builds[speed, skin] = cand.n_builds
+    assert builds[1.0, 1.0] == 1
+    assert 1 < builds[5.0, 1.0] < builds[5.0, 0.1]
+
+
+def test_md_replica_batch_with_skin(bd):
+    """Three crystals stepped together with the candidate list, against the
+    oracle's trajectory."""
+    full, params, _, d, T = synth.workload_inputs("triclinic40")
+    b = subset_batch(full, [0, 5, 11])
+    v0, inv_m, ref = _guarded_case(b, params, d, T, 3, 2.0, range(60, 80))
+    got, cand = _md_on_stream(bd, b, params, v0, inv_m, 2.0, [3], d, T, skin=0.4)
+    _compare(got, ref, "replicas md with skin")
