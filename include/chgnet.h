@@ -24,7 +24,9 @@
  *    that the library creates, with a few events, once per host thread and
  *    device; it forks from and joins back into `stream`, so the call still
  *    behaves as work enqueued on `stream`. Results are bitwise reproducible
- *    run to run (no floating-point atomics).
+ *    run to run: every floating-point sum runs in a fixed order (no
+ *    floating-point atomics). chgnet_build_graph keeps a small pinned host
+ *    buffer per host thread for the size readback (allocated on first use).
  *  - Return value: CHGNET_OK (0) or a negative error code below; the text of
  *    the last error of the calling thread is chgnet_last_error_string().
  *

@@ -598,25 +598,43 @@ __global__ void __launch_bounds__(256) kd_bwd_bonds(int64_t n, const float* __re
   dst[i] = ds.t;
 }
 
-// per angle (b1, b2): d phi = d s_b1 * e^b_b2; d e^b_b2 += d s_b1 * phi
+// per angle (b1, b2): d phi = d s_b1 * e^b_b2
 __global__ void __launch_bounds__(256) kd_bwd_angles(int64_t n, int D, const int* __restrict__ b1,
                                                      const int* __restrict__ b2, const float* __restrict__ dsv,
                                                      const float* __restrict__ dst, const float* __restrict__ ebv,
-                                                     const float* __restrict__ ebt, const float* __restrict__ pv,
-                                                     const float* __restrict__ pt, float* __restrict__ dpv,
-                                                     float* __restrict__ dpt, float* __restrict__ debv,
-                                                     float* __restrict__ debt) {
+                                                     const float* __restrict__ ebt, float* __restrict__ dpv,
+                                                     float* __restrict__ dpt) {
   const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (i >= n) return;
   const int64_t a = i / D, c = i % D;
   const int64_t o1 = (int64_t)b1[a] * D + c, o2 = (int64_t)b2[a] * D + c;
-  const Dn ds{dsv[o1], dst[o1]};
-  const Dn dp = ds * Dn{ebv[o2], ebt[o2]};
-  const Dn g = ds * Dn{pv[i], pt[i]};
+  const Dn dp = Dn{dsv[o1], dst[o1]} * Dn{ebv[o2], ebt[o2]};
   dpv[i] = dp.v;
   dpt[i] = dp.t;
-  atomicAdd(debv + o2, g.v);
-  atomicAdd(debt + o2, g.t);
+}
+
+// per bond q: d e^b_q += sum over the angles (p, q) whose second bond is q of
+// d s_p * phi_(p,q). The angles of a centre atom with bonds b0 .. b0 + k - 1
+// form one block, bond p's row listing the other bonds in order, so (p, q)
+// sits at angle_ptr[p] + (q - b0) - (q > p); the sum runs over p in order
+// (no atomics, the same result every run).
+__global__ void __launch_bounds__(256) kd_bwd_b2(int64_t n, int D, const int* __restrict__ bond_src,
+                                                 const int* __restrict__ bond_ptr, const int* __restrict__ angle_ptr,
+                                                 const float* __restrict__ dsv, const float* __restrict__ dst,
+                                                 const float* __restrict__ pv, const float* __restrict__ pt,
+                                                 float* __restrict__ debv, float* __restrict__ debt) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= n) return;
+  const int q = (int)(i / D), c = (int)(i % D);
+  const int ctr = bond_src[q], b0 = bond_ptr[ctr], b1 = bond_ptr[ctr + 1];
+  Dn acc{0.f, 0.f};
+  for (int p = b0; p < b1; ++p) {
+    if (p == q) continue;
+    const int64_t a = (int64_t)angle_ptr[p] + (q - b0) - (q > p ? 1 : 0);
+    acc = acc + Dn{dsv[(int64_t)p * D + c], dst[(int64_t)p * D + c]} * Dn{pv[a * D + c], pt[a * D + c]};
+  }
+  debv[i] += acc.v;
+  debt[i] += acc.t;
 }
 
 // ---------------------------------------------------------------------------
@@ -658,14 +676,6 @@ __global__ void __launch_bounds__(256) kd_act_bwd(int64_t n, const float* __rest
   const Dn g = Dn{dv[i], dt[i]} * dn_dsilu(Dn{hv[i], ht[i]});
   dv[i] = g.v;
   dt[i] = g.t;
-}
-
-// element table rows: g[Z_i - 1] += d v0_i (tangent)
-__global__ void __launch_bounds__(256) kd_wz(int64_t n, int D, const int* __restrict__ Z, const float* __restrict__ dvt,
-                                             float* __restrict__ g) {
-  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (i >= n) return;
-  atomicAdd(g + (int64_t)(Z[i / D] - 1) * D + i % D, dvt[i]);
 }
 
 // tangent of d sRBF / d rbf_n * d sRBF_n / d f_n per row (edge, or bond through its edge)
@@ -1068,10 +1078,15 @@ int cons_grad_impl(Ctx& c, const float* dE, const float* dF, const float* dS, co
                                                                                d.ss[t][1], a.eb, d.eb_t, d.deb[0],
                                                                                d.deb[1], d.dss[0], d.dss[1]));
     if (A > 0)
+    {
       KLAUNCH(st, "kd_msg_bwd", kd_bwd_angles<<<dn_blocks(A * D), 256, 0, st>>>(A * D, D, a.ang_b1, a.ang_b2, d.dss[0],
-                                                                                d.dss[1], a.eb, d.eb_t, d.pbe[t][0],
-                                                                                d.pbe[t][1], d.dpbe[0], d.dpbe[1],
-                                                                                d.deb[0], d.deb[1]));
+                                                                                d.dss[1], a.eb, d.eb_t, d.dpbe[0],
+                                                                                d.dpbe[1]));
+      KLAUNCH(st, "kd_msg_bwd", kd_bwd_b2<<<dn_blocks(B * D), 256, 0, st>>>(B * D, D, a.bond_src, g.bond_ptr,
+                                                                            g.angle_ptr, d.dss[0], d.dss[1],
+                                                                            d.pbe[t][0], d.pbe[t][1], d.deb[0],
+                                                                            d.deb[1]));
+    }
     // gates
     {
       DnGates J{};
@@ -1174,7 +1189,8 @@ int cons_grad_impl(Ctx& c, const float* dE, const float* dF, const float* dS, co
   }
 
   // embedding (Eq. 2) and sRBF frequencies
-  KLAUNCH(st, "kd_embed", kd_wz<<<dn_blocks(ND), 256, 0, st>>>(ND, D, bt.Z, d.dv[1], gB + Lg.W_Z));
+  // element table rows: g[Z_i - 1] += d v0_i (tangent), summed per element in atom order
+  KLAUNCH(st, "kd_embed", k_embed_bwd_Z<<<24, 256, 0, st>>>((int)N, D, bt.Z, d.dv[1], gB + Lg.W_Z));
   cross(E, R, D, a.rbf_a, d.rbfa_t, R, nullptr, d.de, D, nullptr, Lg.W_e, 2 * D);
   colsum(E, D, d.de[1], D, nullptr, Lg.b_e0);
   cross(E, R, D, a.rbf_a, d.rbfa_t, R, nullptr, d.dea, D, nullptr, Lg.W_e + D, 2 * D);

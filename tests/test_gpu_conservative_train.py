@@ -201,3 +201,18 @@ def test_eq10_block_refused(bd):
     with pytest.raises(bd.ChgnetError) as e:
         bd.step(hp, db, g, _dev(params), [_dev(x) for x in targets], ws)
     assert e.value.code == bd.CHGNET_EINVAL
+
+
+def test_step_bitwise_reproducible(bd):
+    """Training through the conservative readout twice on the same inputs:
+    the loss and every gradient entry are bitwise equal (every sum of the
+    dual-number path runs in a fixed order)."""
+    b, params, targets, d, T = synth.workload_inputs("triclinic40")
+    hp, db, g, ws = _setup(bd, b, d, T)
+    p = _dev(params)
+    tg = [_dev(x) for x in targets]
+    l1, g1 = bd.step(hp, db, g, p, tg, ws)
+    l1, g1 = l1.cpu().numpy().copy(), g1.cpu().numpy().copy()
+    l2, g2 = bd.step(hp, db, g, p, tg, ws)
+    assert np.array_equal(l1, l2.cpu().numpy())
+    assert np.array_equal(g1, g2.cpu().numpy())
