@@ -75,8 +75,8 @@ typedef struct {
                          tangent of the weight gradient along the
                          displacement -dL/dF and the strain rate
                          (dL/dsigma)/V (forward-over-reverse in dual
-                         numbers); with sequential = 1 both return EINVAL.
-                         The workspace then holds the dual-number buffers
+                         numbers), with either block. The workspace then
+                         holds the dual-number buffers
                          as well (chgnet_workspace_size includes them).     */
 } chgnet_hparams;
 
@@ -201,7 +201,7 @@ int chgnet_forward(const chgnet_hparams* hp, const chgnet_batch* batch, const ch
  * batch, graph and params. Positions and lattices are not differentiated.
  * d|x|/dx is taken as 0 at x = 0. With hp->conservative the forces and
  * stresses are the derivatives of the energy, and their terms differentiate
- * those derivatives (second derivatives; the Eq. (10) block: EINVAL). */
+ * those derivatives (second derivatives). */
 int chgnet_backward(const chgnet_hparams* hp, const chgnet_batch* batch, const chgnet_graph* graph,
                     const float* params, const float* dE, const float* dF, const float* dS, const float* dM,
                     float* grad, void* ws, size_t ws_bytes, void* stream);

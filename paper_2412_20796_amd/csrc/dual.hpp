@@ -167,7 +167,7 @@ __global__ void __launch_bounds__(256) kd_angles(int A, int K, const int* __rest
 // over the angles centred on i of dz_be | of dz_an]; the four wavefronts
 // take every fourth row and their sums are added in a fixed order.
 constexpr int kDzMaxCols = 4;  // 2d / 64 columns a lane
-__global__ void __launch_bounds__(256) kd_dz_atoms(int N, int D, int nblk, const int* __restrict__ ep,
+__global__ void __launch_bounds__(256) kd_dz_atoms(int N, int D, int q0, int nblk, const int* __restrict__ ep,
                                                    const int* __restrict__ rev, const int* __restrict__ bp,
                                                    const int* __restrict__ ap, const float* __restrict__ zav,
                                                    const float* __restrict__ zat, const float* __restrict__ zbv,
@@ -177,7 +177,7 @@ __global__ void __launch_bounds__(256) kd_dz_atoms(int N, int D, int nblk, const
   __shared__ float red[4][2][kDzMaxCols * 64];
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
   const int64_t i = blockIdx.x / nblk;
-  const int q = blockIdx.x % nblk;
+  const int q = q0 + (int)(blockIdx.x % nblk);
   const int W2 = 2 * D, nc = W2 / 64;
   int64_t r0, r1;
   const float *xv, *xt;
@@ -222,7 +222,7 @@ __global__ void __launch_bounds__(256) kd_dz_atoms(int N, int D, int nblk, const
 // of bond p lists the other k - 1 bonds in increasing order, so the angle
 // (p, q) is the reverse of (q, p) and sits at position q - b0 (minus one if q
 // > p) of p's block: the second-bond sums read the reverses of b's own angles.
-__global__ void __launch_bounds__(256) kd_dz_bonds(int B, int D, int ang, const int* __restrict__ ap,
+__global__ void __launch_bounds__(256) kd_dz_bonds(int B, int D, int which, const int* __restrict__ ap,
                                                    const int* __restrict__ bsrc, const int* __restrict__ bp,
                                                    const int* __restrict__ b2, const float* __restrict__ zbv,
                                                    const float* __restrict__ zbt, const float* __restrict__ znv,
@@ -238,11 +238,13 @@ __global__ void __launch_bounds__(256) kd_dz_bonds(int B, int D, int ang, const 
     for (int64_t a = ap[w]; a < ap[w + 1]; ++a) {
       const int64_t p = b2[a], pp = p - b0;
       const int64_t o = a * W2 + c, o2 = (ap[p] + (qq < pp ? qq : qq - 1)) * W2 + c;
-      s[0] += zbv[o];
-      s[1] += zbt[o];
-      s[2] += zbv[o2];
-      s[3] += zbt[o2];
-      if (ang) {
+      if (which & 1) {
+        s[0] += zbv[o];
+        s[1] += zbt[o];
+        s[2] += zbv[o2];
+        s[3] += zbt[o2];
+      }
+      if (which & 2) {
         s[4] += znv[o];
         s[5] += znt[o];
         s[6] += znv[o2];
@@ -252,6 +254,7 @@ __global__ void __launch_bounds__(256) kd_dz_bonds(int B, int D, int ang, const 
     const int64_t o = w * 4 * W2 + c;
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
+      if (!(which & (k < 2 ? 1 : 2))) continue;
       tv[o + k * W2] = s[2 * k];
       tt[o + k * W2] = s[2 * k + 1];
     }
@@ -799,7 +802,6 @@ unsigned dn_blocks(int64_t n) { return (unsigned)cdiv(std::max<int64_t>(n, 1), 2
 // activations of forward_impl with the same weights (a.Pal) and positions.
 int cons_grad_impl(Ctx& c, const float* dE, const float* dF, const float* dS, const float* dM, float* G,
                    hipStream_t st) {
-  if (c.hp->sequential) return fail(CHGNET_EINVAL, "conservative readout: weight gradients need the Eq. (11) block");
   const Dims& m = c.dm;
   Acts& a = c.a;
   const ParamLayout& L = c.La;
@@ -867,54 +869,66 @@ int cons_grad_impl(Ctx& c, const float* dE, const float* dF, const float* dS, co
     return CHGNET_OK;
   };
   const int64_t WB = (int64_t)D * 2 * D;  // one d-row input block of a gate's first layer
+  const bool seq = c.hp->sequential != 0;
+  // Modules of a layer, by bit: 1 atom conv (Eq. 4), 2 bond conv (Eq. 5), 4
+  // angle update (Eq. 6). Under Eq. (11) all three read layer-t features and
+  // run together; under Eq. (10) they run in order, the bond conv reading
+  // v^{t+1} and the angle update v^{t+1} and e^{t+1}.
   for (int t = 0; t < m.T; ++t) {
     const LayerOffsets& lo = L.layer[t];
     const bool ang = lo.has_angle;
     const float *Wav = P + lo.av.W, *Wbe = P + lo.be.W, *Wan = P + lo.an.W;
-    // projections of the atom blocks (v W_av0 | v W_av1 | v W_be0 | v W_an0)
-    // and bond blocks (e_b W_be1 | e_b W_be2 | e_b W_an1 | e_b W_an2); the
-    // edge and angle blocks with the bias into z
-    {
+    // projections of the modules' atom blocks (v W_av0 | v W_av1 | v W_be0 |
+    // v W_an0, from vin) and bond blocks (e_b W_be1 | e_b W_be2 | e_b W_an1 |
+    // e_b W_an2, from ein); the edge and angle blocks with the bias into z
+    auto project = [&](int which, const float* vv, const float* vt, const float* ev, const float* et) -> int {
       std::vector<GemmProblem> ps;
       const float* Wa[4] = {Wav, Wav + WB, Wbe, Wan};
-      for (int k = 0; k < (ang ? 4 : 3); ++k) {
+      for (int k = 0; k < 4; ++k) {
+        if (!(which & (k < 2 ? 1 : k == 2 ? 2 : 4))) continue;
         GemmProblem p = gp(N, 2 * D, d.PA[0] + k * 2 * D, 8 * D);
-        seg(p, a.v[t], D, 0, D, Wa[k], 2 * D, 0);
+        seg(p, vv, D, 0, D, Wa[k], 2 * D, 0);
         ps.push_back(p);
-        ps.push_back(tangent_of(p, {d.v_t[t]}, d.PA[1] + k * 2 * D, nullptr));
+        ps.push_back(tangent_of(p, {vt}, d.PA[1] + k * 2 * D, nullptr));
       }
       const float* Wb[4] = {Wbe + WB, Wbe + 2 * WB, Wan + WB, Wan + 2 * WB};
-      for (int k = 0; k < (ang ? 4 : 2); ++k) {
+      for (int k = 0; k < 4; ++k) {
+        if (!(which & (k < 2 ? 2 : 4))) continue;
         GemmProblem p = gp(B, 2 * D, d.PB[0] + k * 2 * D, 8 * D);
         p.a_rows = g.bond_edge;
-        seg(p, a.e[t], D, 0, D, Wb[k], 2 * D, 0);
+        seg(p, ev, D, 0, D, Wb[k], 2 * D, 0);
         ps.push_back(p);
-        ps.push_back(tangent_of(p, {d.e_t[t]}, d.PB[1] + k * 2 * D, nullptr));
+        ps.push_back(tangent_of(p, {et}, d.PB[1] + k * 2 * D, nullptr));
       }
-      GemmProblem p = gp(E, 2 * D, d.zav[t][0], 2 * D);
-      seg(p, a.e[t], D, 0, D, Wav + 2 * WB, 2 * D, 0);
-      p.bias = P + lo.av.b;
-      ps.push_back(p);
-      ps.push_back(tangent_of(p, {d.e_t[t]}, d.zav[t][1], nullptr));
-      p = gp(A, 2 * D, d.zbe[t][0], 2 * D);
-      seg(p, a.a[t], D, 0, D, Wbe + 3 * WB, 2 * D, 0);
-      p.bias = P + lo.be.b;
-      ps.push_back(p);
-      ps.push_back(tangent_of(p, {d.a_t[t]}, d.zbe[t][1], nullptr));
-      if (ang) {
-        p = gp(A, 2 * D, d.zan[t][0], 2 * D);
+      if (which & 1) {
+        GemmProblem p = gp(E, 2 * D, d.zav[t][0], 2 * D);
+        seg(p, a.e[t], D, 0, D, Wav + 2 * WB, 2 * D, 0);
+        p.bias = P + lo.av.b;
+        ps.push_back(p);
+        ps.push_back(tangent_of(p, {d.e_t[t]}, d.zav[t][1], nullptr));
+      }
+      if (which & 2) {
+        GemmProblem p = gp(A, 2 * D, d.zbe[t][0], 2 * D);
+        seg(p, a.a[t], D, 0, D, Wbe + 3 * WB, 2 * D, 0);
+        p.bias = P + lo.be.b;
+        ps.push_back(p);
+        ps.push_back(tangent_of(p, {d.a_t[t]}, d.zbe[t][1], nullptr));
+      }
+      if (which & 4) {
+        GemmProblem p = gp(A, 2 * D, d.zan[t][0], 2 * D);
         seg(p, a.a[t], D, 0, D, Wan + 3 * WB, 2 * D, 0);
         p.bias = P + lo.an.b;
         ps.push_back(p);
         ps.push_back(tangent_of(p, {d.a_t[t]}, d.zan[t][1], nullptr));
       }
-      CHG_TRY(run_gemms(ps, st, "kd_gemm"));
-    }
-    {
+      return run_gemms(ps, st, "kd_gemm");
+    };
+    auto gates_fwd = [&](int which) -> int {
       DnGates J{};
       const GatedOffsets* go[3] = {&lo.av, &lo.be, &lo.an};
       float* zs[3][2] = {{d.zav[t][0], d.zav[t][1]}, {d.zbe[t][0], d.zbe[t][1]}, {d.zan[t][0], d.zan[t][1]}};
-      for (int k = 0; k < (ang ? 3 : 2); ++k) {
+      for (int k = 0; k < 3; ++k) {
+        if (!(which & (1 << k))) continue;
         DnGate& q = J.j[J.n++];
         q.rows = k == 0 ? E : A;
         q.zv = zs[k][0];
@@ -946,36 +960,63 @@ int cons_grad_impl(Ctx& c, const float* dE, const float* dF, const float* dS, co
           q.res_t = d.a_t[t];
         }
       }
-      CHG_TRY(gates(J, true));
-    }
-    if (N > 0)
-      KLAUNCH(st, "kd_msg", kd_msg_atoms<<<(unsigned)N, 256, 0, st>>>((int)N, D, g.edge_ptr, a.ea, d.ea_t,
-                                                                              d.pav[t][0], d.pav[t][1], d.m[t][0], d.m[t][1]));
-    if (B > 0)
-      KLAUNCH(st, "kd_msg", kd_msg_bonds<<<(unsigned)cdiv(B, 4), 256, 0, st>>>((int)B, D, g.angle_ptr, a.ang_b2, a.eb, d.eb_t,
-                                                                              d.pbe[t][0], d.pbe[t][1], d.ss[t][0],
-                                                                              d.ss[t][1], d.mu[t][0], d.mu[t][1]));
+      return gates(J, true);
+    };
+    auto messages = [&](int which) -> int {
+      if ((which & 1) && N > 0)
+        KLAUNCH(st, "kd_msg", kd_msg_atoms<<<(unsigned)N, 256, 0, st>>>((int)N, D, g.edge_ptr, a.ea, d.ea_t, d.pav[t][0],
+                                                                        d.pav[t][1], d.m[t][0], d.m[t][1]));
+      if ((which & 2) && B > 0)
+        KLAUNCH(st, "kd_msg", kd_msg_bonds<<<(unsigned)cdiv(B, 4), 256, 0, st>>>((int)B, D, g.angle_ptr, a.ang_b2, a.eb,
+                                                                                 d.eb_t, d.pbe[t][0], d.pbe[t][1],
+                                                                                 d.ss[t][0], d.ss[t][1], d.mu[t][0],
+                                                                                 d.mu[t][1]));
+      return CHGNET_OK;
+    };
     // v' = v + m Wo + bo; e' = e, bonds e'_b = e_b + mu Wo + bo (tangents)
-    if (E > 0) {
-      const int64_t n4 = E * D / 4;
-      KLAUNCH(st, "k_copy", k_copy4<<<(unsigned)std::min<int64_t>(cdiv(n4, 256), 4096), 256, 0, st>>>(
-                                reinterpret_cast<float4*>(d.e_t[t + 1]), reinterpret_cast<const float4*>(d.e_t[t]), n4));
-    }
-    {
+    auto updates = [&](int which) -> int {
+      if ((which & 2) && E > 0) {
+        const int64_t n4 = E * D / 4;
+        KLAUNCH(st, "k_copy", k_copy4<<<(unsigned)std::min<int64_t>(cdiv(n4, 256), 4096), 256, 0, st>>>(
+                                  reinterpret_cast<float4*>(d.e_t[t + 1]), reinterpret_cast<const float4*>(d.e_t[t]), n4));
+      }
       std::vector<GemmProblem> ps;
-      GemmProblem p = gp(N, D, d.v_t[t + 1], D);
-      seg(p, d.m[t][1], D, 0, D, P + lo.av_Wo, D, 0);
-      p.res = d.v_t[t];
-      p.res_ld = D;
-      ps.push_back(p);
-      p = gp(B, D, d.e_t[t + 1], D);
-      seg(p, d.mu[t][1], D, 0, D, P + lo.be_Wo, D, 0);
-      p.res = d.e_t[t];
-      p.res_ld = D;
-      p.res_rows = g.bond_edge;
-      p.c_rows = g.bond_edge;
-      ps.push_back(p);
-      CHG_TRY(run_gemms(ps, st, "kd_gemm"));
+      if (which & 1) {
+        GemmProblem p = gp(N, D, d.v_t[t + 1], D);
+        seg(p, d.m[t][1], D, 0, D, P + lo.av_Wo, D, 0);
+        p.res = d.v_t[t];
+        p.res_ld = D;
+        ps.push_back(p);
+      }
+      if (which & 2) {
+        GemmProblem p = gp(B, D, d.e_t[t + 1], D);
+        seg(p, d.mu[t][1], D, 0, D, P + lo.be_Wo, D, 0);
+        p.res = d.e_t[t];
+        p.res_ld = D;
+        p.res_rows = g.bond_edge;
+        p.c_rows = g.bond_edge;
+        ps.push_back(p);
+      }
+      return run_gemms(ps, st, "kd_gemm");
+    };
+    if (!seq) {
+      CHG_TRY(project(ang ? 7 : 3, a.v[t], d.v_t[t], a.e[t], d.e_t[t]));
+      CHG_TRY(gates_fwd(ang ? 7 : 3));
+      CHG_TRY(messages(3));
+      CHG_TRY(updates(3));
+    } else {
+      CHG_TRY(project(1, a.v[t], d.v_t[t], a.e[t], d.e_t[t]));
+      CHG_TRY(gates_fwd(1));
+      CHG_TRY(messages(1));
+      CHG_TRY(updates(1));
+      CHG_TRY(project(2, a.v[t + 1], d.v_t[t + 1], a.e[t], d.e_t[t]));
+      CHG_TRY(gates_fwd(2));
+      CHG_TRY(messages(2));
+      CHG_TRY(updates(2));
+      if (ang) {
+        CHG_TRY(project(4, a.v[t + 1], d.v_t[t + 1], a.e[t + 1], d.e_t[t + 1]));
+        CHG_TRY(gates_fwd(4));
+      }
     }
   }
 
@@ -1060,42 +1101,58 @@ int cons_grad_impl(Ctx& c, const float* dE, const float* dF, const float* dS, co
     const LayerOffsets& lo = L.layer[t];
     const LayerOffsets& lg = Lg.layer[t];
     const bool ang = lo.has_angle;
-    // output linears: dm = dv Wo^T, dmu = de_b Wo^T
-    CHG_TRY(gemm2(N, D, d.dm, D, d.dv, D, D, P + lo.av_Wo, D, 1, nullptr));
-    if (B > 0) CHG_TRY(gemm2(B, D, d.dmu, D, d.de, D, D, P + lo.be_Wo, D, 1, g.bond_edge));
-    cross(N, D, D, d.m[t][0], d.m[t][1], D, nullptr, d.dv, D, nullptr, lg.av_Wo, D);
-    colsum(N, D, d.dv[1], D, nullptr, lg.av_bo);
-    cross(B, D, D, d.mu[t][0], d.mu[t][1], D, nullptr, d.de, D, g.bond_edge, lg.be_Wo, D);
-    colsum(B, D, d.de[1], D, g.bond_edge, lg.be_bo);
-    CHG_TRY(flush());
-    // messages
-    if (E > 0)
-      KLAUNCH(st, "kd_msg_bwd", kd_bwd_atoms<<<dn_blocks(E * D), 256, 0, st>>>(E * D, D, a.edge_src, d.dm[0], d.dm[1], a.ea,
-                                                                               d.ea_t, d.pav[t][0], d.pav[t][1], d.dpav[0],
-                                                                               d.dpav[1], d.dea[0], d.dea[1]));
-    if (B > 0)
-      KLAUNCH(st, "kd_msg_bwd", kd_bwd_bonds<<<dn_blocks(B * D), 256, 0, st>>>(B * D, d.dmu[0], d.dmu[1], d.ss[t][0],
-                                                                               d.ss[t][1], a.eb, d.eb_t, d.deb[0],
-                                                                               d.deb[1], d.dss[0], d.dss[1]));
-    if (A > 0)
-    {
-      KLAUNCH(st, "kd_msg_bwd", kd_bwd_angles<<<dn_blocks(A * D), 256, 0, st>>>(A * D, D, a.ang_b1, a.ang_b2, d.dss[0],
-                                                                                d.dss[1], a.eb, d.eb_t, d.dpbe[0],
-                                                                                d.dpbe[1]));
-      KLAUNCH(st, "kd_msg_bwd", kd_bwd_b2<<<dn_blocks(B * D), 256, 0, st>>>(B * D, D, a.bond_src, g.bond_ptr,
-                                                                            g.angle_ptr, d.dss[0], d.dss[1],
-                                                                            d.pbe[t][0], d.pbe[t][1], d.deb[0],
-                                                                            d.deb[1]));
-    }
-    // gates
-    {
+    const float *Wav = P + lo.av.W, *Wbe = P + lo.be.W, *Wan = P + lo.an.W;
+    // inputs the modules read: under Eq. (10) the bond conv and the angle
+    // update read v^{t+1}, and the angle update e^{t+1}
+    const float* vbv = seq ? a.v[t + 1] : a.v[t];
+    const float* vbt = seq ? d.v_t[t + 1] : d.v_t[t];
+    const float* env = seq ? a.e[t + 1] : a.e[t];
+    const float* ent = seq ? d.e_t[t + 1] : d.e_t[t];
+    // output linears (bit 1 atom conv: dm = dv Wo^T; bit 2 bond conv:
+    // dmu = de_b Wo^T) and their weight terms
+    auto out_linears = [&](int which) -> int {
+      if (which & 1) {
+        CHG_TRY(gemm2(N, D, d.dm, D, d.dv, D, D, P + lo.av_Wo, D, 1, nullptr));
+        cross(N, D, D, d.m[t][0], d.m[t][1], D, nullptr, d.dv, D, nullptr, lg.av_Wo, D);
+        colsum(N, D, d.dv[1], D, nullptr, lg.av_bo);
+      }
+      if (which & 2) {
+        if (B > 0) CHG_TRY(gemm2(B, D, d.dmu, D, d.de, D, D, P + lo.be_Wo, D, 1, g.bond_edge));
+        cross(B, D, D, d.mu[t][0], d.mu[t][1], D, nullptr, d.de, D, g.bond_edge, lg.be_Wo, D);
+        colsum(B, D, d.de[1], D, g.bond_edge, lg.be_bo);
+      }
+      return flush();
+    };
+    auto messages_bwd = [&](int which) -> int {
+      if ((which & 1) && E > 0)
+        KLAUNCH(st, "kd_msg_bwd", kd_bwd_atoms<<<dn_blocks(E * D), 256, 0, st>>>(E * D, D, a.edge_src, d.dm[0], d.dm[1],
+                                                                                 a.ea, d.ea_t, d.pav[t][0], d.pav[t][1],
+                                                                                 d.dpav[0], d.dpav[1], d.dea[0],
+                                                                                 d.dea[1]));
+      if ((which & 2) && B > 0)
+        KLAUNCH(st, "kd_msg_bwd", kd_bwd_bonds<<<dn_blocks(B * D), 256, 0, st>>>(B * D, d.dmu[0], d.dmu[1], d.ss[t][0],
+                                                                                 d.ss[t][1], a.eb, d.eb_t, d.deb[0],
+                                                                                 d.deb[1], d.dss[0], d.dss[1]));
+      if ((which & 2) && A > 0) {
+        KLAUNCH(st, "kd_msg_bwd", kd_bwd_angles<<<dn_blocks(A * D), 256, 0, st>>>(A * D, D, a.ang_b1, a.ang_b2, d.dss[0],
+                                                                                  d.dss[1], a.eb, d.eb_t, d.dpbe[0],
+                                                                                  d.dpbe[1]));
+        KLAUNCH(st, "kd_msg_bwd", kd_bwd_b2<<<dn_blocks(B * D), 256, 0, st>>>(B * D, D, a.bond_src, g.bond_ptr,
+                                                                              g.angle_ptr, d.dss[0], d.dss[1],
+                                                                              d.pbe[t][0], d.pbe[t][1], d.deb[0],
+                                                                              d.deb[1]));
+      }
+      return CHGNET_OK;
+    };
+    auto gates_bwd = [&](int which) -> int {
       DnGates J{};
       const GatedOffsets* go[3] = {&lo.av, &lo.be, &lo.an};
       float* zs[3][2] = {{d.zav[t][0], d.zav[t][1]}, {d.zbe[t][0], d.zbe[t][1]}, {d.zan[t][0], d.zan[t][1]}};
       float* dp[3][2] = {{d.dpav[0], d.dpav[1]}, {d.dpbe[0], d.dpbe[1]}, {d.da[0], d.da[1]}};
       float* dz[3][2] = {{d.dzav[0], d.dzav[1]}, {d.dzbe[0], d.dzbe[1]}, {d.dzan[0], d.dzan[1]}};
       float* lnp[3] = {d.lnav, d.lnbe, d.lnan};
-      for (int k = 0; k < (ang ? 3 : 2); ++k) {
+      for (int k = 0; k < 3; ++k) {
+        if (!(which & (1 << k))) continue;
         DnGate& q = J.j[J.n++];
         q.rows = k == 0 ? E : A;
         q.zv = zs[k][0];
@@ -1110,57 +1167,76 @@ int cons_grad_impl(Ctx& c, const float* dE, const float* dF, const float* dS, co
         q.dzt = dz[k][1];
         q.lnp = lnp[k];
       }
-      CHG_TRY(gates(J, false));
-    }
-    // pre-activation gradients summed per atom (S) and per bond (T)
-    if (N > 0)
-      KLAUNCH(st, "kd_dz_sum", kd_dz_atoms<<<(unsigned)(N * (ang ? 4 : 3)), 256, 0, st>>>((int)N, D, ang ? 4 : 3, g.edge_ptr, g.edge_rev,
-                                                                                g.bond_ptr, g.angle_ptr, d.dzav[0], d.dzav[1],
-                                                                                d.dzbe[0], d.dzbe[1], d.dzan[0], d.dzan[1],
-                                                                                d.S[0], d.S[1]));
-    if (B > 0)
-      KLAUNCH(st, "kd_dz_sum", kd_dz_bonds<<<(unsigned)cdiv(B, 4), 256, 0, st>>>((int)B, D, ang, g.angle_ptr, a.bond_src,
-                                                                                g.bond_ptr, a.ang_b2, d.dzbe[0], d.dzbe[1],
-                                                                                d.dzan[0], d.dzan[1], d.T[0], d.T[1]));
-    // input gradients of v^t, e^t and a^t (accumulated): atoms from S, edges
-    // from dz_av, angles from dz_be, dz_an; then the bond rows of e from T
-    {
-      const float *Wav = P + lo.av.W, *Wbe = P + lo.be.W, *Wan = P + lo.an.W;
+      return gates(J, false);
+    };
+    // pre-activation gradients summed per atom (S blocks: 0, 1 atom conv v_i,
+    // v_j; 2 bond-conv centre; 3 angle-update centre) and per bond (T blocks:
+    // 0, 1 bond-conv first and second bond; 2, 3 angle update)
+    auto dz_sums = [&](int which) -> int {
+      const int q0 = (which & 1) ? 0 : (which & 2) ? 2 : 3;
+      const int q1 = (which & 4) ? 4 : (which & 2) ? 3 : 2;
+      if (N > 0 && q1 > q0)
+        KLAUNCH(st, "kd_dz_sum", kd_dz_atoms<<<(unsigned)(N * (q1 - q0)), 256, 0, st>>>(
+                                     (int)N, D, q0, q1 - q0, g.edge_ptr, g.edge_rev, g.bond_ptr, g.angle_ptr, d.dzav[0],
+                                     d.dzav[1], d.dzbe[0], d.dzbe[1], d.dzan[0], d.dzan[1], d.S[0], d.S[1]));
+      if (B > 0 && (which & 6))
+        KLAUNCH(st, "kd_dz_sum", kd_dz_bonds<<<(unsigned)cdiv(B, 4), 256, 0, st>>>((int)B, D, (which >> 1) & 3,
+                                                                                  g.angle_ptr, a.bond_src, g.bond_ptr,
+                                                                                  a.ang_b2, d.dzbe[0], d.dzbe[1],
+                                                                                  d.dzan[0], d.dzan[1], d.T[0], d.T[1]));
+      return CHGNET_OK;
+    };
+    // input gradients of the modules in `which` (accumulated): atoms from S,
+    // edges from dz_av, angles from dz_be, dz_an; then the bond rows of e
+    // from T
+    auto input_grads = [&](int which) -> int {
       std::vector<GemmProblem> ps;
       GemmProblem p = gp(N, D, d.dv[0], D);
       p.accumulate = 1;
-      seg(p, d.S[0], 8 * D, 0, 2 * D, Wav, 2 * D, 1);
-      seg(p, d.S[0], 8 * D, 2 * D, 2 * D, Wav + WB, 2 * D, 1);
-      seg(p, d.S[0], 8 * D, 4 * D, 2 * D, Wbe, 2 * D, 1);
-      if (ang) seg(p, d.S[0], 8 * D, 6 * D, 2 * D, Wan, 2 * D, 1);
+      if (which & 1) {
+        seg(p, d.S[0], 8 * D, 0, 2 * D, Wav, 2 * D, 1);
+        seg(p, d.S[0], 8 * D, 2 * D, 2 * D, Wav + WB, 2 * D, 1);
+      }
+      if (which & 2) seg(p, d.S[0], 8 * D, 4 * D, 2 * D, Wbe, 2 * D, 1);
+      if (which & 4) seg(p, d.S[0], 8 * D, 6 * D, 2 * D, Wan, 2 * D, 1);
       ps.push_back(p);
       ps.push_back(tangent_of(p, {d.S[1], d.S[1], d.S[1], d.S[1]}, d.dv[1], nullptr));
-      p = gp(E, D, d.de[0], D);
-      p.accumulate = 1;
-      seg(p, d.dzav[0], 2 * D, 0, 2 * D, Wav + 2 * WB, 2 * D, 1);
-      ps.push_back(p);
-      ps.push_back(tangent_of(p, {d.dzav[1]}, d.de[1], nullptr));
-      p = gp(A, D, d.da[0], D);
-      p.accumulate = 1;
-      seg(p, d.dzbe[0], 2 * D, 0, 2 * D, Wbe + 3 * WB, 2 * D, 1);
-      if (ang) seg(p, d.dzan[0], 2 * D, 0, 2 * D, Wan + 3 * WB, 2 * D, 1);
-      ps.push_back(p);
-      ps.push_back(tangent_of(p, {d.dzbe[1], d.dzan[1]}, d.da[1], nullptr));
-      CHG_TRY(run_gemms(ps, st, "kd_gemm"));
-      ps.clear();
-      p = gp(B, D, d.de[0], D);
-      p.accumulate = 1;
-      p.c_rows = g.bond_edge;
-      seg(p, d.T[0], 8 * D, 0, 2 * D, Wbe + WB, 2 * D, 1);
-      seg(p, d.T[0], 8 * D, 2 * D, 2 * D, Wbe + 2 * WB, 2 * D, 1);
-      if (ang) {
-        seg(p, d.T[0], 8 * D, 4 * D, 2 * D, Wan + WB, 2 * D, 1);
-        seg(p, d.T[0], 8 * D, 6 * D, 2 * D, Wan + 2 * WB, 2 * D, 1);
+      if (which & 1) {
+        p = gp(E, D, d.de[0], D);
+        p.accumulate = 1;
+        seg(p, d.dzav[0], 2 * D, 0, 2 * D, Wav + 2 * WB, 2 * D, 1);
+        ps.push_back(p);
+        ps.push_back(tangent_of(p, {d.dzav[1]}, d.de[1], nullptr));
       }
-      ps.push_back(p);
-      ps.push_back(tangent_of(p, {d.T[1], d.T[1], d.T[1], d.T[1]}, d.de[1], nullptr));
+      if (which & 6) {
+        p = gp(A, D, d.da[0], D);
+        p.accumulate = 1;
+        if (which & 2) seg(p, d.dzbe[0], 2 * D, 0, 2 * D, Wbe + 3 * WB, 2 * D, 1);
+        if (which & 4) seg(p, d.dzan[0], 2 * D, 0, 2 * D, Wan + 3 * WB, 2 * D, 1);
+        ps.push_back(p);
+        ps.push_back(which == 4 ? tangent_of(p, {d.dzan[1]}, d.da[1], nullptr)
+                                : tangent_of(p, {d.dzbe[1], d.dzan[1]}, d.da[1], nullptr));
+      }
       CHG_TRY(run_gemms(ps, st, "kd_gemm"));
-    }
+      if (which & 6) {
+        ps.clear();
+        p = gp(B, D, d.de[0], D);
+        p.accumulate = 1;
+        p.c_rows = g.bond_edge;
+        if (which & 2) {
+          seg(p, d.T[0], 8 * D, 0, 2 * D, Wbe + WB, 2 * D, 1);
+          seg(p, d.T[0], 8 * D, 2 * D, 2 * D, Wbe + 2 * WB, 2 * D, 1);
+        }
+        if (which & 4) {
+          seg(p, d.T[0], 8 * D, 4 * D, 2 * D, Wan + WB, 2 * D, 1);
+          seg(p, d.T[0], 8 * D, 6 * D, 2 * D, Wan + 2 * WB, 2 * D, 1);
+        }
+        ps.push_back(p);
+        ps.push_back(tangent_of(p, {d.T[1], d.T[1], d.T[1], d.T[1]}, d.de[1], nullptr));
+        CHG_TRY(run_gemms(ps, st, "kd_gemm"));
+      }
+      return CHGNET_OK;
+    };
     // weight terms of the gates, block by block: atom blocks over atoms
     // against S, bond blocks over bonds against T, edge and angle blocks over
     // their rows against dz
@@ -1172,9 +1248,11 @@ int cons_grad_impl(Ctx& c, const float* dE, const float* dF, const float* dS, co
         crossc(E, D, 2 * D, a.e[t], d.e_t[t], D, nullptr, dz, 2 * D, 0, nullptr, og.W + 2 * WB, 2 * D);
       } else {
         const int sc = gi == 1 ? 4 * D : 6 * D, tc = gi == 1 ? 0 : 4 * D;
-        crossc(N, D, 2 * D, a.v[t], d.v_t[t], D, nullptr, d.S, 8 * D, sc, nullptr, og.W, 2 * D);
-        crossc(B, D, 2 * D, a.e[t], d.e_t[t], D, g.bond_edge, d.T, 8 * D, tc, nullptr, og.W + WB, 2 * D);
-        crossc(B, D, 2 * D, a.e[t], d.e_t[t], D, g.bond_edge, d.T, 8 * D, tc + 2 * D, nullptr, og.W + 2 * WB, 2 * D);
+        const float* ev = gi == 1 ? a.e[t] : env;
+        const float* et = gi == 1 ? d.e_t[t] : ent;
+        crossc(N, D, 2 * D, vbv, vbt, D, nullptr, d.S, 8 * D, sc, nullptr, og.W, 2 * D);
+        crossc(B, D, 2 * D, ev, et, D, g.bond_edge, d.T, 8 * D, tc, nullptr, og.W + WB, 2 * D);
+        crossc(B, D, 2 * D, ev, et, D, g.bond_edge, d.T, 8 * D, tc + 2 * D, nullptr, og.W + 2 * WB, 2 * D);
         crossc(A, D, 2 * D, a.a[t], d.a_t[t], D, nullptr, dz, 2 * D, 0, nullptr, og.W + 3 * WB, 2 * D);
       }
       colsum(rows, 2 * D, dz[1], 2 * D, nullptr, og.b);
@@ -1182,10 +1260,43 @@ int cons_grad_impl(Ctx& c, const float* dE, const float* dF, const float* dS, co
       ts.push_back(split_out(tp(kDnGateWaves, 1, 4 * D, nullptr, 0, 0, nullptr, lnp, 4 * D, 0, nullptr, gB + og.g_c, D), D,
                              gB + og.b_c, gB + og.g_g, gB + og.b_g));
     };
-    gate_terms(0, d.dzav, d.lnav, lg.av);
-    gate_terms(1, d.dzbe, d.lnbe, lg.be);
-    if (ang) gate_terms(2, d.dzan, d.lnan, lg.an);
-    CHG_TRY(flush());
+    auto module_terms = [&](int which) -> int {
+      if (which & 1) gate_terms(0, d.dzav, d.lnav, lg.av);
+      if (which & 2) gate_terms(1, d.dzbe, d.lnbe, lg.be);
+      if (which & 4) gate_terms(2, d.dzan, d.lnan, lg.an);
+      return flush();
+    };
+    if (!seq) {
+      const int all = ang ? 7 : 3;
+      CHG_TRY(out_linears(3));
+      CHG_TRY(messages_bwd(3));
+      CHG_TRY(gates_bwd(all));
+      CHG_TRY(dz_sums(all));
+      CHG_TRY(input_grads(all));
+      CHG_TRY(module_terms(all));
+    } else {
+      // Eq. (10) in reverse: the angle update (upstream da^{t+1}; gradients
+      // into v^{t+1}, e^{t+1} and a^t), the bond conv (upstream de^{t+1};
+      // into v^{t+1}, e^t, a^t), then the atom conv (upstream dv^{t+1})
+      if (ang) {
+        CHG_TRY(gates_bwd(4));
+        CHG_TRY(dz_sums(4));
+        CHG_TRY(input_grads(4));
+        CHG_TRY(module_terms(4));
+      }
+      CHG_TRY(out_linears(2));
+      CHG_TRY(messages_bwd(2));
+      CHG_TRY(gates_bwd(2));
+      CHG_TRY(dz_sums(2));
+      CHG_TRY(input_grads(2));
+      CHG_TRY(module_terms(2));
+      CHG_TRY(out_linears(1));
+      CHG_TRY(messages_bwd(1));
+      CHG_TRY(gates_bwd(1));
+      CHG_TRY(dz_sums(1));
+      CHG_TRY(input_grads(1));
+      CHG_TRY(module_terms(1));
+    }
   }
 
   // embedding (Eq. 2) and sRBF frequencies

@@ -3265,8 +3265,6 @@ int step_entry(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_graph
                size_t ws_bytes, hipStream_t st) {
   if (!params || !E_t || !F_t || !S_t || !loss_cfg || !loss || !grad) return fail(CHGNET_EINVAL, "step: null argument");
   CHG_TRY(validate_hparams(hp));
-  if (hp->conservative && hp->sequential)
-    return fail(CHGNET_EINVAL, "step: the conservative readout is trained with the Eq. (11) block");
   if ((M_t != nullptr) != (hp->magmom != 0))
     return fail(CHGNET_EINVAL, "step: M_target is required with the magnetic-moment head and only with it");
   if (!std::isfinite(loss_cfg->huber_delta)) return fail(CHGNET_EINVAL, "step: huber_delta is not finite");

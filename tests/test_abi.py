@@ -83,18 +83,3 @@ def test_null_arguments_rejected(L):
     assert lib.chgnet_md(ctypes.byref(hp), None, None, None, None, 1.0, 1, 0, ctypes.byref(done), None, 0,
                          None) == L.CHGNET_EINVAL
     assert done.value == 0
-
-
-def test_conservative_training_with_the_eq10_block_refused(L):
-    """chgnet_step refuses training through the conservative readout with the
-    Eq. (10) block before it touches any array (host stand-ins for the device
-    pointers are never read)."""
-    hp = L.hparams(conservative=True, sequential=True)
-    lib = L.lib()
-    buf = (ctypes.c_float * 16)()
-    p = ctypes.cast(buf, ctypes.c_void_p)
-    lw = L.LossCfg(2.0, 1.5, 0.1, 0.1, 0.0)
-    code = lib.chgnet_step(ctypes.byref(hp), None, None, p, p, p, p, None, ctypes.byref(lw), p, p, None, None, None,
-                           None, 0, None)
-    assert code == L.CHGNET_EINVAL
-    assert b"Eq. (11)" in lib.chgnet_last_error_string()

@@ -9,7 +9,8 @@ is first order) and sparse cells (no bonds, no angles, no edges); at the
 full triclinic40 (d = 64, T = 4) and wide128 (d = 128, T = 5) sizes, output
 gradients on a sample of structures against the oracle on those structures
 alone (crystals of a batch are independent and the gradient is linear in
-the output gradients). The Eq. (10) block is refused with CHGNET_EINVAL.
+the output gradients); the reference block of Eq. (10) on cubic8, random
+batches, the moment head and d = 128, and through chgnet_backward.
 
 Tolerance per parameter tensor: |gpu - ref| <= 3e-5 m + 1e-4 |ref|, with m
 the larger of the tensor's max|ref| and 1e-2 of the whole gradient's (a
@@ -195,12 +196,59 @@ def test_full_size_sampled_structures(bd, workload, sample):
     _assert_grad(grad.cpu().numpy(), rg.numpy(), ohp, workload + " sampled conservative backward")
 
 
-def test_eq10_block_refused(bd):
+def _check_step_seq(bd, b, params, targets, d, T, name, delta=None, magmom=False):
+    ohp = om.HParams(d=d, n_layers=T, conservative=True, magmom=magmom, sequential=True)
+    graph = og.build_graph(b.atom_ptr, b.pos, b.lattice)
+    rl, rg = autodiff.loss_and_grad(ohp, b, graph, params.astype(np.float64), targets, delta=delta)
+    hp, db, g, ws = _setup(bd, b, d, T, magmom=magmom, sequential=True)
+    loss, grad = bd.step(hp, db, g, _dev(params), [_dev(x) for x in targets], ws, huber_delta=delta or 0.0)
+    lv = float(loss.cpu().numpy()[0])
+    assert abs(lv - rl) <= 1e-5 + 1e-4 * abs(rl), (name, lv, rl)
+    _assert_grad(grad.cpu().numpy(), rg, ohp, name)
+
+
+def test_eq10_block_step(bd):
+    """Training through the conservative readout with the reference block of
+    Eq. (10) (bond conv on v^{t+1}, angle update on v^{t+1} and e^{t+1}):
+    cubic8, random batches (one with Huber), the moment head and d = 128."""
     b, params, targets, d, T = synth.workload_inputs("cubic8")
+    _check_step_seq(bd, b, params, targets, d, T, "cubic8 eq10 conservative step")
+    for seed in (0, 1):
+        br = synth.random_crystals(seed=520 + seed, n_struct=2 + seed, n_lo=2, n_hi=12, rho=(0.06, 0.12))
+        _check_step_seq(bd, br, synth.make_params(64, 3, seed=(13, 1, seed)), synth.make_targets(br, seed=(13, 2, seed)),
+                        64, 3, "random%d eq10 conservative step" % seed, delta=0.1 if seed else None)
+    bm = synth.random_crystals(seed=23, n_struct=2, n_lo=3, n_hi=10)
+    _check_step_seq(bd, bm, synth.make_params(64, 2, seed=(13, 1, 7), magmom=True),
+                    synth.make_targets(bm, seed=(13, 2, 7), magmom=True), 64, 2, "magmom eq10 conservative step",
+                    magmom=True)
+    _check_step_seq(bd, bm, synth.make_params(128, 2, seed=(13, 1, 9)), synth.make_targets(bm, seed=(13, 2, 9)), 128, 2,
+                    "d128 eq10 conservative step")
+
+
+def test_eq10_block_backward_random_output_gradients(bd):
+    """chgnet_backward with the Eq. (10) block and random output gradients
+    against autograd's second derivatives of sum(dE E) + sum(dF F) + sum(dS sigma)."""
+    import torch
+
+    b = synth.random_crystals(seed=31, n_struct=2, n_lo=4, n_hi=12)
+    d, T = 64, 3
+    params = synth.make_params(d, T, seed=(14, 1, 0))
+    ohp = om.HParams(d=d, n_layers=T, conservative=True, sequential=True)
+    rng = np.random.default_rng(4)
+    dE = rng.standard_normal(b.n_struct)
+    dF = rng.standard_normal((b.n_atoms, 3))
+    dS = rng.standard_normal((b.n_struct, 3, 3))
+    graph = og.build_graph(b.atom_ptr, b.pos, b.lattice)
+    p64 = torch.tensor(params.astype(np.float64), requires_grad=True)
+    E, F, S, _, _ = autodiff.outputs(ohp, b, graph, p64, create_graph=True)
+    tot = (E * torch.tensor(dE)).sum() + (F * torch.tensor(dF)).sum() + (S * torch.tensor(dS)).sum()
+    (rg,) = torch.autograd.grad(tot, p64)
     hp, db, g, ws = _setup(bd, b, d, T, sequential=True)
-    with pytest.raises(bd.ChgnetError) as e:
-        bd.step(hp, db, g, _dev(params), [_dev(x) for x in targets], ws)
-    assert e.value.code == bd.CHGNET_EINVAL
+    p = _dev(params)
+    bd.forward(hp, db, g, p, ws)
+    f32 = lambda x: _dev(x.astype(np.float32))
+    grad = bd.backward(hp, db, g, p, f32(dE), f32(dF), f32(dS), ws)
+    _assert_grad(grad.cpu().numpy(), rg.numpy(), ohp, "eq10 conservative backward")
 
 
 def test_step_bitwise_reproducible(bd):
