@@ -1,11 +1,13 @@
 // fp32 MFMA GEMMs for the per-atom, per-edge and per-angle linear layers.
 //
-// Each wavefront owns a 32x32 block of C built from four 16x16x4 fp32 MFMA
-// tiles; a 256-thread workgroup covers 64x64, with the K dimension streamed
-// through LDS in chunks of 16. Operand rows may be gathered through an index
-// array (edge -> source atom, bond -> edge, angle -> bond), so the
-// concatenated GatedMLP inputs of Eq. (4)-(6) never exist in memory: the
-// products of their blocks are summed in the epilogue.
+// k_gemm: a 256-thread workgroup owns a 128 x 64 tile of C, each wavefront
+// 32 rows x 64 columns as two 32x32 fp32 MFMA (32x32x2) accumulators, with
+// the K dimension streamed through LDS in chunks of 32. k_gemm_w: direct-load
+// 32 x 64 wave tiles with k split over wavefronts, for few rows or a long k.
+// k_tn: split-K weight-gradient products X^T Y. Operand rows may be gathered
+// through an index array (edge -> source atom, bond -> edge, angle -> bond),
+// so the concatenated GatedMLP inputs of Eq. (4)-(6) never exist in memory:
+// the products of their blocks are summed in the epilogue.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
