@@ -126,7 +126,7 @@ def main():
         prof = bd.profile_stop()
         E, B, A = g.n_edges, g.n_bonds, g.n_angles
         rl, rows = roofline(prof, n, dict(N=b.n_atoms, E=E, B=B, A=A, S=b.n_struct, D=d, T=T,
-                                          fused_bwd=d == 64 and not args.sequential, workload=args.workload,
+                                          fused_bwd=not args.sequential, workload=args.workload,
                                           R=hp.n_rbf, K=hp.n_fourier))
         print(json.dumps({"launch_timing_steps": n, "roofline": rl, "kernels": rows}), flush=True)
         return
@@ -187,7 +187,7 @@ def main():
         torch.cuda.synchronize()
         prof = bd.profile_stop()
         out["roofline"], out["kernels"] = roofline(prof, args.steps, dict(N=b.n_atoms, E=E, B=B, A=A, S=S, D=d, T=T,
-                                                                            fused_bwd=d == 64 and not args.sequential,
+                                                                            fused_bwd=not args.sequential,
                                                                             workload=args.workload, R=hp.n_rbf,
                                                                             K=hp.n_fourier))
     if not args.no_cpu_baseline:
@@ -381,15 +381,13 @@ def mandatory_cost(tag, z):
 
 
 # rocprofv3 kernel symbol of each launch tag that has an algorithmic cost
-# (the backward gate depends on the width: a fused gate-and-input-gradient
-# kernel at d = 64, a row-gate kernel before a separate product at d = 128)
 def tag_symbol(tag, d):
     return {
         "gemm_z": "k_gemm<64, 1>",
         "gemm_in_bwd": "k_gemm<64, 2>",
         "tn_in": "k_tn<1>",
         "k_gate_fwd": "k_gate_fwd_mm<%d>" % d,
-        "k_gate_bwd": "k_gate_bwd_mm" if d == 64 else "k_gate_bwd<128>",
+        "k_gate_bwd": "k_gate_bwd_mm" if d == 64 else "k_gate_bwd_mm128",
     }.get(tag)
 
 

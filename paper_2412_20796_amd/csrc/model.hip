@@ -950,10 +950,10 @@ __device__ __forceinline__ void bwd_mm_ln_add(const float (&p)[32], float* wsum)
   }
 }
 
-template <int MODE>
+template <int D, int MODE>
 __device__ __forceinline__ void gate_bwd_mm_row(const GateBwdJob& J, int row, const BwdMmIdx& x, int j,
                                                 const float* lnS, float (&lp)[4 * kMmCpl], float* zrow) {
-  constexpr int D = 64, CPL = kMmCpl;
+  constexpr int CPL = kMmCpl;
   constexpr int LPR = Lanes<D, CPL>::LPR;
   float zc[CPL], zg[CPL], rc, rg;
   load_cols_nt<D, CPL>(J.z + (int64_t)row * J.ldz, j, zc);
@@ -1009,9 +1009,9 @@ __device__ __forceinline__ void gate_bwd_mm_row(const GateBwdJob& J, int row, co
   ln_stats<D, CPL>(zc, zg, rc, rg);
   float gc[CPL], bc[CPL], gg[CPL], bg[CPL];
   load_cols<D, CPL>(lnS, j, gc);
-  load_cols<D, CPL>(lnS + 64, j, bc);
-  load_cols<D, CPL>(lnS + 128, j, gg);
-  load_cols<D, CPL>(lnS + 192, j, bg);
+  load_cols<D, CPL>(lnS + D, j, bc);
+  load_cols<D, CPL>(lnS + 2 * D, j, gg);
+  load_cols<D, CPL>(lnS + 3 * D, j, bg);
   float dyc[CPL], dyg[CPL], side[CPL];
   float s1c = 0.f, s2c = 0.f, s1g = 0.f, s2g = 0.f;
 #pragma unroll
@@ -1218,9 +1218,9 @@ __global__ void __launch_bounds__(kMmThreads, 1) k_gate_bwd_mm(GateBwdMmJobs J) 
           if (row < jb.rows) {
             const float* lnS = &LnS[k][g][0][0];
             float* zrow = Zs[i & 1] + lr * kBmLd + 128 * g;
-            if (gj.mode == BWD_ATOM) gate_bwd_mm_row<BWD_ATOM>(gj, row, xi[g], j, lnS, lp, zrow);
-            else if (gj.mode == BWD_BOND) gate_bwd_mm_row<BWD_BOND>(gj, row, xi[g], j, lnS, lp, zrow);
-            else gate_bwd_mm_row<BWD_ANGLE>(gj, row, xi[g], j, lnS, lp, zrow);
+            if (gj.mode == BWD_ATOM) gate_bwd_mm_row<64, BWD_ATOM>(gj, row, xi[g], j, lnS, lp, zrow);
+            else if (gj.mode == BWD_BOND) gate_bwd_mm_row<64, BWD_BOND>(gj, row, xi[g], j, lnS, lp, zrow);
+            else gate_bwd_mm_row<64, BWD_ANGLE>(gj, row, xi[g], j, lnS, lp, zrow);
           }
           bwd_mm_ln_add(lp, Wsum[jb.gid[g]][cw]);
         }
@@ -1237,6 +1237,181 @@ __global__ void __launch_bounds__(kMmThreads, 1) k_gate_bwd_mm(GateBwdMmJobs J) 
     float s = 0.f;
     for (int w = 0; w < kMmConsumers; ++w) s += Wsum[gid][w][c];
     J.lnpart[gid][(int64_t)blockIdx.x * 256 + c] = s;
+  }
+}
+
+// LayerNorm parameter partials of one pass at d = 128 (4 sums x 8 columns
+// per lane, rows in the wavefront's 4 row slots, lane bits 4-5) summed over
+// the slots and added to this wavefront's LDS slot wsum[4][128]: the
+// lane-half swaps reduce over bit 5 and then bit 4, after which lane
+// (j, b4, b5) holds, for m = 0..7, sum m / 2 of column 64 (m % 2) + 4 j +
+// 2 b4 + b5 and is that slot's only writer (fixed order, no atomics).
+__device__ __forceinline__ void bwd_mm_ln_add128(const float (&p)[32], float* wsum) {
+  const int lane = threadIdx.x & 63;
+  float w[16];
+#pragma unroll
+  for (int m = 0; m < 16; ++m) w[m] = pl_sum32(p[2 * m], p[2 * m + 1]);
+  const int base = 4 * (lane & 15) + 2 * ((lane >> 4) & 1) + ((lane >> 5) & 1);
+#pragma unroll
+  for (int m = 0; m < 8; ++m) wsum[(m >> 1) * 128 + 64 * (m & 1) + base] += pl_sum16(w[2 * m], w[2 * m + 1]);
+}
+
+// Fused backward gate at d = 128: the gate backward of a layer (dz, the
+// LayerNorm parameter partials, d e^a / t2) and the input gradients of its
+// own rows dX = sum_g dz_g W_g^T + residual in one launch, one 1024-thread
+// block per compute unit. A tile is 32 rows; a pipeline stage ("unit") is
+// one gate of a tile: the eight consumer wavefronts form its dz (4 rows
+// each, 16 lanes a row), store it for the weight gradients and segmented
+// sums and into an LDS tile, while the eight producer wavefronts multiply
+// the previous unit's tile: each owns 16 output columns of all 32 rows
+// (fp32 MFMA 16x16x4, two 16-row subtiles), accumulating over the gates of
+// a tile; the weights W_g^T (256 x 128 per gate) do not fit on chip beside
+// the tiles, so each producer streams its 16 columns from L2 in quarters of
+// 64 k, one quarter ahead of the MFMAs.
+constexpr int kBm2Rows = 32, kBm2Ld = 256 + 4, kBm2Threads = 1024, kBm2Prod = 8, kBm2Cons = 8;
+
+__global__ void __launch_bounds__(kBm2Threads, 1) k_gate_bwd_mm128(GateBwdMmJobs J) {
+  constexpr int D = 128;
+  __shared__ __attribute__((aligned(16))) float Zs[2][kBm2Rows * kBm2Ld];
+  __shared__ __attribute__((aligned(16))) float LnS[2][2][4][D];
+  __shared__ __attribute__((aligned(16))) float Wsum[3][kBm2Cons][4 * D];
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  for (int t = threadIdx.x; t < 2 * 2 * 4 * D; t += kBm2Threads) {
+    const int jb = t / (8 * D), g = (t / (4 * D)) % 2, q = (t / D) % 4, c = t % D;
+    float v = 0.f;
+    if (jb < J.n && g < J.j[jb].ngates) {
+      const LnPtrs& ln = J.j[jb].g[g].ln;
+      v = (q == 0 ? ln.gc : q == 1 ? ln.bc : q == 2 ? ln.gg : ln.bg)[c];
+    }
+    LnS[jb][g][q][c] = v;
+  }
+  for (int t = threadIdx.x; t < 3 * kBm2Cons * 4 * D; t += kBm2Threads) (&Wsum[0][0][0])[t] = 0.f;
+  auto job_of = [&](int tile) {
+    int k = 0;
+    while (k + 1 < J.n && tile >= J.j[k + 1].tile0) ++k;
+    return k;
+  };
+  // the grid never exceeds the tile count: every block has a tile
+  const int nt = (J.ntiles - 1 - (int)blockIdx.x) / (int)gridDim.x + 1;
+  auto tile_of = [&](int i) { return (int)blockIdx.x + i * (int)gridDim.x; };
+  __syncthreads();
+  if (wave < kBm2Prod) {
+    const int n = lane & 15, q4 = lane >> 4, col = 16 * wave + n;
+    int units = 0;  // stages consumed so far (one block barrier each)
+    for (int i = 0; i < nt; ++i) {
+      const int tile = tile_of(i);
+      const int k = job_of(tile);
+      const GateBwdMmJob& jb = J.j[k];
+      const int row0 = (tile - jb.tile0) * kBm2Rows;
+      float rv[2][4];
+#pragma unroll
+      for (int rt = 0; rt < 2; ++rt)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const int row = row0 + 16 * rt + 4 * q4 + v;
+          rv[rt][v] = (jb.res && row < jb.rows) ? jb.res[(int64_t)row * D + col] : 0.f;
+        }
+      v4f acc[2];
+#pragma unroll
+      for (int rt = 0; rt < 2; ++rt) acc[rt] = v4f{0.f, 0.f, 0.f, 0.f};
+      for (int g = 0; g < jb.ngates; ++g) {
+        // quarter qt of the k range of gate g: lane quad q4 supplies k =
+        // 64 qt + 16 q4 + s in MFMA step s (the same map for A and B)
+        const float* wr = jb.W[g] + (int64_t)col * (2 * D) + 16 * q4;
+        float bq[2][16];
+        auto load_q = [&](int qt, float (&b)[16]) {
+#pragma unroll
+          for (int u = 0; u < 4; ++u) {
+            const float4 v = *reinterpret_cast<const float4*>(wr + 64 * qt + 4 * u);
+            b[4 * u] = v.x; b[4 * u + 1] = v.y; b[4 * u + 2] = v.z; b[4 * u + 3] = v.w;
+          }
+        };
+        load_q(0, bq[0]);
+        __syncthreads();  // the consumers have written this unit's dz tile
+        const float* Z = Zs[units & 1];
+        ++units;
+#pragma unroll
+        for (int qt = 0; qt < 4; ++qt) {
+          if (qt + 1 < 4) load_q(qt + 1, bq[(qt + 1) & 1]);
+#pragma unroll
+          for (int s4 = 0; s4 < 4; ++s4) {
+            float4 a4[2];
+#pragma unroll
+            for (int rt = 0; rt < 2; ++rt)
+              a4[rt] = *reinterpret_cast<const float4*>(Z + (16 * rt + n) * kBm2Ld +
+                                                        ((64 * qt + 16 * q4 + 4 * s4) ^ ((n & 1) * 32)));
+            const float* b = &bq[qt & 1][4 * s4];
+#pragma unroll
+            for (int rt = 0; rt < 2; ++rt) acc[rt] = __builtin_amdgcn_mfma_f32_16x16x4f32(a4[rt].x, b[0], acc[rt], 0, 0, 0);
+#pragma unroll
+            for (int rt = 0; rt < 2; ++rt) acc[rt] = __builtin_amdgcn_mfma_f32_16x16x4f32(a4[rt].y, b[1], acc[rt], 0, 0, 0);
+#pragma unroll
+            for (int rt = 0; rt < 2; ++rt) acc[rt] = __builtin_amdgcn_mfma_f32_16x16x4f32(a4[rt].z, b[2], acc[rt], 0, 0, 0);
+#pragma unroll
+            for (int rt = 0; rt < 2; ++rt) acc[rt] = __builtin_amdgcn_mfma_f32_16x16x4f32(a4[rt].w, b[3], acc[rt], 0, 0, 0);
+          }
+        }
+      }
+#pragma unroll
+      for (int rt = 0; rt < 2; ++rt)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const int row = row0 + 16 * rt + 4 * q4 + v;
+          if (row < jb.rows) jb.dx[(int64_t)row * D + col] = acc[rt][v] + rv[rt][v];
+        }
+    }
+    __syncthreads();  // matches the consumers' final barrier
+  } else {
+    using GL = Lanes<D, kMmCpl>;
+    const int cw = wave - kBm2Prod, j = lane % GL::LPR, slot = lane / GL::LPR;
+    const int lr = GL::RPW * cw + slot;  // row of the tile
+    int units = 0;
+    // row indices of a unit, loaded one unit ahead
+    auto unit_idx = [&](int i, int g, BwdMmIdx& x) {
+      if (i >= nt) return;
+      const int tile = tile_of(i);
+      const GateBwdMmJob& jb = J.j[job_of(tile)];
+      const int row = (tile - jb.tile0) * kBm2Rows + lr;
+      if (row < jb.rows) bwd_mm_index(jb.g[g], row, x);
+    };
+    BwdMmIdx xcur{}, xnext{};
+    unit_idx(0, 0, xcur);
+    for (int i = 0; i < nt; ++i) {
+      const int tile = tile_of(i);
+      const int k = __builtin_amdgcn_readfirstlane(job_of(tile));
+      const GateBwdMmJob& jb = J.j[k];
+      const int row = (tile - jb.tile0) * kBm2Rows + lr;
+      for (int g = 0; g < jb.ngates; ++g) {
+        const GateBwdJob& gj = jb.g[g];
+        if (g + 1 < jb.ngates) unit_idx(i, g + 1, xnext);
+        else unit_idx(i + 1, 0, xnext);
+        float lp[4 * kMmCpl];
+#pragma unroll
+        for (int q = 0; q < 4 * kMmCpl; ++q) lp[q] = 0.f;
+        if (row < jb.rows) {
+          const BwdMmIdx x = xcur;
+          const float* lnS = &LnS[k][g][0][0];
+          float* zrow = Zs[units & 1] + lr * kBm2Ld;
+          if (gj.mode == BWD_ATOM) gate_bwd_mm_row<D, BWD_ATOM>(gj, row, x, j, lnS, lp, zrow);
+          else if (gj.mode == BWD_BOND) gate_bwd_mm_row<D, BWD_BOND>(gj, row, x, j, lnS, lp, zrow);
+          else gate_bwd_mm_row<D, BWD_ANGLE>(gj, row, x, j, lnS, lp, zrow);
+        }
+        bwd_mm_ln_add128(lp, Wsum[jb.gid[g]][cw]);
+        xcur = xnext;
+        __syncthreads();  // this unit's dz tile is complete
+        ++units;
+      }
+    }
+    __syncthreads();  // the producers have read the last tile
+  }
+  __syncthreads();
+  for (int t = threadIdx.x; t < 3 * 4 * D; t += kBm2Threads) {
+    const int gid = t / (4 * D), c = t % (4 * D);
+    if (!J.lnpart[gid]) continue;
+    float s = 0.f;
+    for (int w = 0; w < kBm2Cons; ++w) s += Wsum[gid][w][c];
+    J.lnpart[gid][(int64_t)blockIdx.x * 4 * D + c] = s;
   }
 }
 
@@ -2321,35 +2496,37 @@ int gate_bwd_launch(int D, GateBwdJobs J, float* const* ln_grad, const int* slot
   return CHGNET_OK;
 }
 
-// Launch the fused (d = 64) backward gates and their input-gradient products
-// of one layer: a persistent grid of at most one block per compute unit.
+// Launch the fused backward gates and their input-gradient products of one
+// layer: a persistent grid of at most one block per compute unit.
 // slot[gid] is the lnpart slot of gate id gid (0 atom conv, 1 bond conv, 2
 // angle update); with ln_grad, each used slot's reduction into ln_grad[gid]
 // is appended to `defer`.
-int gate_bwd_mm_launch(GateBwdMmJobs J, float* const* ln_grad, const int* slot, const Acts& a,
+int gate_bwd_mm_launch(int D, GateBwdMmJobs J, float* const* ln_grad, const int* slot, const Acts& a,
                        std::vector<ReduceJob>& defer, hipStream_t st) {
   GateBwdMmJobs K{};
   int tiles = 0;
   bool used[3] = {false, false, false};
+  const int rows_per_tile = D == 64 ? kMmRows : kBm2Rows;
   for (int i = 0; i < J.n; ++i) {
     if (J.j[i].rows <= 0) continue;
     K.j[K.n] = J.j[i];
     K.j[K.n].tile0 = tiles;
-    tiles += (int)cdiv(J.j[i].rows, kMmRows);
+    tiles += (int)cdiv(J.j[i].rows, rows_per_tile);
     for (int g = 0; g < J.j[i].ngates; ++g) used[J.j[i].gid[g]] = true;
     K.n++;
   }
   K.ntiles = tiles;
   if (tiles == 0) return CHGNET_OK;
   const int grid = std::min(tiles, 256);
-  if ((int64_t)grid * 4 * 64 > a.lnpart_stride) return fail(CHGNET_EINVAL, "gate_bwd_mm: LayerNorm partial slots too small");
+  if ((int64_t)grid * 4 * D > a.lnpart_stride) return fail(CHGNET_EINVAL, "gate_bwd_mm: LayerNorm partial slots too small");
   for (int gid = 0; gid < 3; ++gid) {
     K.lnpart[gid] = nullptr;
     if (!used[gid] || !ln_grad) continue;
     K.lnpart[gid] = a.lnpart + (int64_t)slot[gid] * a.lnpart_stride;
-    defer.push_back(ReduceJob{K.lnpart[gid], grid, 4 * 64, 4 * 64, ln_grad[gid]});
+    defer.push_back(ReduceJob{K.lnpart[gid], grid, 4 * D, 4 * D, ln_grad[gid]});
   }
-  KLAUNCH(st, "k_gate_bwd", k_gate_bwd_mm<<<grid, kMmThreads, 0, st>>>(K));
+  if (D == 64) KLAUNCH(st, "k_gate_bwd", k_gate_bwd_mm<<<grid, kMmThreads, 0, st>>>(K));
+  else KLAUNCH(st, "k_gate_bwd", k_gate_bwd_mm128<<<grid, kBm2Threads, 0, st>>>(K));
   return CHGNET_OK;
 }
 
@@ -2830,9 +3007,9 @@ int backward_impl(Ctx& c, const float* Pflat, bool repack, const float* dE, cons
 
   // interaction blocks in reverse
   const bool seq = c.hp->sequential != 0;
-  // at d = 64 (Eq. 11 block) the gate backward also forms the input gradients
-  // of the edge and angle rows (k_gate_bwd_mm)
-  const bool fused = D == 64 && !seq;
+  // with the Eq. 11 block the gate backward also forms the input gradients
+  // of the edge and angle rows (k_gate_bwd_mm, k_gate_bwd_mm128)
+  const bool fused = !seq;
   for (int t = m.T - 1; t >= 0; --t) {
     const LayerOffsets& lo = L.layer[t];
     const LayerOffsets& lg = Lg.layer[t];
@@ -2879,7 +3056,7 @@ int backward_impl(Ctx& c, const float* Pflat, bool repack, const float* dE, cons
       }
       return gate_bwd_launch(D, J, wg ? lg_out : nullptr, slot, a, reduce_jobs, st);
     };
-    // fused gate backward and edge/angle input gradients (d = 64): edges
+    // fused gate backward and edge/angle input gradients: edges
     // de(e^t) = de(e^{t+1}) + dz_v W_av,e^T; angles da(a^t) = da(a^{t+1}) +
     // dz_b W_be,a^T + dz_a W_an,a^T (no angle update in the last layer)
     auto gates_mm = [&]() -> int {
@@ -2914,9 +3091,9 @@ int backward_impl(Ctx& c, const float* Pflat, bool repack, const float* dE, cons
         q.dx = a.da[nx];
       }
       const int slot[3] = {3 * t + 1, 3 * t, 3 * t + 2};
-      if (!wg) return gate_bwd_mm_launch(J, nullptr, slot, a, reduce_jobs, st);
+      if (!wg) return gate_bwd_mm_launch(D, J, nullptr, slot, a, reduce_jobs, st);
       float* lg_out[3] = {G + lg.av.g_c, G + lg.be.g_c, G + lg.an.g_c};
-      return gate_bwd_mm_launch(J, lg_out, slot, a, reduce_jobs, st);
+      return gate_bwd_mm_launch(D, J, lg_out, slot, a, reduce_jobs, st);
     };
     // per-bond sums of dz over the bond's two angle roles (DZ12) from `ncols`
     // columns of dzae starting at col0; with_deb also forms d e^b
