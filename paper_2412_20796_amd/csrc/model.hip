@@ -1267,7 +1267,7 @@ __device__ __forceinline__ void bwd_mm_ln_add128(const float (&p)[32], float* ws
 // (fp32 MFMA 16x16x4, two 16-row subtiles), accumulating over the gates of
 // a tile; the weights W_g^T (256 x 128 per gate) do not fit on chip beside
 // the tiles, so each producer streams its 16 columns from L2 in quarters of
-// 64 k, one quarter ahead of the MFMAs.
+// 64 k, two quarters ahead of the MFMAs.
 constexpr int kBm2Rows = 32, kBm2Ld = 256 + 4, kBm2Threads = 1024, kBm2Prod = 8, kBm2Cons = 8;
 
 __global__ void __launch_bounds__(kBm2Threads, 1) k_gate_bwd_mm128(GateBwdMmJobs J) {
@@ -1298,6 +1298,27 @@ __global__ void __launch_bounds__(kBm2Threads, 1) k_gate_bwd_mm128(GateBwdMmJobs
   __syncthreads();
   if (wave < kBm2Prod) {
     const int n = lane & 15, q4 = lane >> 4, col = 16 * wave + n;
+    // W^T columns of this lane for a unit (tile i, gate g): lane quad q4
+    // supplies k = 64 qt + 16 q4 + s in MFMA step s of quarter qt (the same
+    // map for A and B). The quarters of successive units form one stream,
+    // loaded two quarters ahead through a ring of four register buffers.
+    auto unit_w = [&](int i, int g) -> const float* {
+      const GateBwdMmJob& jb = J.j[job_of(tile_of(i))];
+      return jb.W[g] + (int64_t)col * (2 * D) + 16 * q4;
+    };
+    float bq[4][16];
+    auto load_q = [&](const float* wr, int qt, float (&b)[16]) {
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const float4 v = *reinterpret_cast<const float4*>(wr + 64 * qt + 4 * u);
+        b[4 * u] = v.x; b[4 * u + 1] = v.y; b[4 * u + 2] = v.z; b[4 * u + 3] = v.w;
+      }
+    };
+    {
+      const float* w0 = unit_w(0, 0);
+      load_q(w0, 0, bq[0]);
+      load_q(w0, 1, bq[1]);
+    }
     int units = 0;  // stages consumed so far (one block barrier each)
     for (int i = 0; i < nt; ++i) {
       const int tile = tile_of(i);
@@ -1316,24 +1337,17 @@ __global__ void __launch_bounds__(kBm2Threads, 1) k_gate_bwd_mm128(GateBwdMmJobs
 #pragma unroll
       for (int rt = 0; rt < 2; ++rt) acc[rt] = v4f{0.f, 0.f, 0.f, 0.f};
       for (int g = 0; g < jb.ngates; ++g) {
-        // quarter qt of the k range of gate g: lane quad q4 supplies k =
-        // 64 qt + 16 q4 + s in MFMA step s (the same map for A and B)
-        const float* wr = jb.W[g] + (int64_t)col * (2 * D) + 16 * q4;
-        float bq[2][16];
-        auto load_q = [&](int qt, float (&b)[16]) {
-#pragma unroll
-          for (int u = 0; u < 4; ++u) {
-            const float4 v = *reinterpret_cast<const float4*>(wr + 64 * qt + 4 * u);
-            b[4 * u] = v.x; b[4 * u + 1] = v.y; b[4 * u + 2] = v.z; b[4 * u + 3] = v.w;
-          }
-        };
-        load_q(0, bq[0]);
+        const float* wcur = jb.W[g] + (int64_t)col * (2 * D) + 16 * q4;
+        const float* wnext = g + 1 < jb.ngates ? jb.W[g + 1] + (int64_t)col * (2 * D) + 16 * q4
+                             : i + 1 < nt     ? unit_w(i + 1, 0)
+                                              : nullptr;
         __syncthreads();  // the consumers have written this unit's dz tile
         const float* Z = Zs[units & 1];
         ++units;
 #pragma unroll
         for (int qt = 0; qt < 4; ++qt) {
-          if (qt + 1 < 4) load_q(qt + 1, bq[(qt + 1) & 1]);
+          if (qt < 2) load_q(wcur, qt + 2, bq[qt + 2]);
+          else if (wnext) load_q(wnext, qt - 2, bq[qt - 2]);
 #pragma unroll
           for (int s4 = 0; s4 < 4; ++s4) {
             float4 a4[2];
@@ -1341,7 +1355,7 @@ __global__ void __launch_bounds__(kBm2Threads, 1) k_gate_bwd_mm128(GateBwdMmJobs
             for (int rt = 0; rt < 2; ++rt)
               a4[rt] = *reinterpret_cast<const float4*>(Z + (16 * rt + n) * kBm2Ld +
                                                         ((64 * qt + 16 * q4 + 4 * s4) ^ ((n & 1) * 32)));
-            const float* b = &bq[qt & 1][4 * s4];
+            const float* b = &bq[qt][4 * s4];
 #pragma unroll
             for (int rt = 0; rt < 2; ++rt) acc[rt] = __builtin_amdgcn_mfma_f32_16x16x4f32(a4[rt].x, b[0], acc[rt], 0, 0, 0);
 #pragma unroll
