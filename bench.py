@@ -301,6 +301,12 @@ def algorithmic_cost(tag, z):
         lay = E * 6 * D + A * 9 * D + N * 8 * D + B * 9 * D
         last = E * 6 * D + A * 4 * D + N * 6 * D + B * 5 * D
         return "hbm", f * (Tang * lay + last)
+    if tag == "k_gate_bwd" and z.get("fused_bwd") and D != 64:
+        # d = 128: the fused backward gate is bound by its input-gradient
+        # product dX = dz W^T of every edge (2d -> d) and, per angle, of the
+        # bond-conv and angle-update gates (2 x 2d -> d; one gate in the last
+        # layer): the same flops as the forward product
+        return "mfma", T * E * 4 * D * D + Tang * A * 8 * D * D + A * 4 * D * D
     if tag == "k_gate_bwd" and z.get("fused_bwd"):
         # as below, plus the input gradients the kernel forms: per edge the
         # residual (d) in and de (d) out; per angle da (d) out and, in layers
