@@ -894,9 +894,9 @@ struct GateBwdMmJob {
   int rows, tile0, ngates;
   int gid[2];  // LayerNorm partial slot of each gate: 0 atom conv, 1 bond conv, 2 angle update
   GateBwdJob g[2];
-  const float* W[2];  // rows of each gate's first-layer weight for this input block: [64][128]
-  const float* res;   // [rows, 64] added to dX, or nullptr
-  float* dx;          // [rows, 64]
+  const float* W[2];  // rows of each gate's first-layer weight for this input block: [D][2D]
+  const float* res;   // [rows, D] added to dX, or nullptr
+  float* dx;          // [rows, D]
 };
 struct GateBwdMmJobs {
   int n, ntiles;
@@ -1259,95 +1259,89 @@ __device__ __forceinline__ void bwd_mm_ln_add128(const float (&p)[32], float* ws
 // Fused backward gate at d = 128: the gate backward of a layer (dz, the
 // LayerNorm parameter partials, d e^a / t2) and the input gradients of its
 // own rows dX = sum_g dz_g W_g^T + residual in one launch, one 1024-thread
-// block per compute unit. A tile is 32 rows; a pipeline stage ("unit") is
-// one gate of a tile: the eight consumer wavefronts form its dz (4 rows
-// each, 16 lanes a row), store it for the weight gradients and segmented
-// sums and into an LDS tile, while the eight producer wavefronts multiply
-// the previous unit's tile: each owns 16 output columns of all 32 rows
-// (fp32 MFMA 16x16x4, two 16-row subtiles), accumulating over the gates of
-// a tile; the weights W_g^T (256 x 128 per gate) do not fit on chip beside
-// the tiles, so each producer streams its 16 columns from L2 in quarters of
-// 64 k, two quarters ahead of the MFMAs.
+// block per compute unit. Every gate is a job of its own over 32-row tiles
+// (atom conv over the edges; bond conv, then angle update over the angles);
+// a block takes the row tiles r = blockIdx.x + k gridDim.x of every job, job
+// by job, so it runs the angle update's tile r after the bond conv's tile r,
+// and the angle update adds its product to the bond conv's dX of those rows
+// (written and read back by the same lanes). Per tile the eight consumer
+// wavefronts form dz (4 rows each, 16 lanes a row), store it for the weight
+// gradients and segmented sums and into an LDS tile, while the eight
+// producer wavefronts multiply the previous tile: each owns 16 output
+// columns of all 32 rows (fp32 MFMA 16x16x4, two 16-row subtiles) and holds
+// its 16 columns of the job's W^T (256 x 128) in registers, loaded once per
+// job.
 constexpr int kBm2Rows = 32, kBm2Ld = 256 + 4, kBm2Threads = 1024, kBm2Prod = 8, kBm2Cons = 8;
 
-__global__ void __launch_bounds__(kBm2Threads, 1) k_gate_bwd_mm128(GateBwdMmJobs J) {
+struct GateBwd128Job {
+  int rows, ntiles, gid;  // gid: LayerNorm partial slot (0 atom conv, 1 bond conv, 2 angle update)
+  GateBwdJob g;
+  const float* W;    // [128, 256]: rows of the gate's first-layer weight for this input block
+  const float* res;  // [rows, 128] added to dX, or nullptr
+  float* dx;         // [rows, 128]
+};
+struct GateBwd128Jobs {
+  int n;
+  GateBwd128Job j[3];
+  float* lnpart[3];  // by slot: [gridDim.x][4 * 128], or nullptr
+};
+
+__global__ void __launch_bounds__(kBm2Threads, 1) k_gate_bwd_mm128(GateBwd128Jobs J) {
   constexpr int D = 128;
   __shared__ __attribute__((aligned(16))) float Zs[2][kBm2Rows * kBm2Ld];
-  __shared__ __attribute__((aligned(16))) float LnS[2][2][4][D];
+  __shared__ __attribute__((aligned(16))) float LnS[3][4][D];
   __shared__ __attribute__((aligned(16))) float Wsum[3][kBm2Cons][4 * D];
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  for (int t = threadIdx.x; t < 2 * 2 * 4 * D; t += kBm2Threads) {
-    const int jb = t / (8 * D), g = (t / (4 * D)) % 2, q = (t / D) % 4, c = t % D;
+  for (int t = threadIdx.x; t < 3 * 4 * D; t += kBm2Threads) {
+    const int jb = t / (4 * D), q = (t / D) % 4, c = t % D;
     float v = 0.f;
-    if (jb < J.n && g < J.j[jb].ngates) {
-      const LnPtrs& ln = J.j[jb].g[g].ln;
+    if (jb < J.n) {
+      const LnPtrs& ln = J.j[jb].g.ln;
       v = (q == 0 ? ln.gc : q == 1 ? ln.bc : q == 2 ? ln.gg : ln.bg)[c];
     }
-    LnS[jb][g][q][c] = v;
+    LnS[jb][q][c] = v;
   }
   for (int t = threadIdx.x; t < 3 * kBm2Cons * 4 * D; t += kBm2Threads) (&Wsum[0][0][0])[t] = 0.f;
-  auto job_of = [&](int tile) {
-    int k = 0;
-    while (k + 1 < J.n && tile >= J.j[k + 1].tile0) ++k;
-    return k;
-  };
-  // the grid never exceeds the tile count: every block has a tile
-  const int nt = (J.ntiles - 1 - (int)blockIdx.x) / (int)gridDim.x + 1;
-  auto tile_of = [&](int i) { return (int)blockIdx.x + i * (int)gridDim.x; };
+  const int b0 = (int)blockIdx.x, G = (int)gridDim.x;
   __syncthreads();
   if (wave < kBm2Prod) {
     const int n = lane & 15, q4 = lane >> 4, col = 16 * wave + n;
-    // W^T columns of this lane for a unit (tile i, gate g): lane quad q4
-    // supplies k = 64 qt + 16 q4 + s in MFMA step s of quarter qt (the same
-    // map for A and B). The quarters of successive units form one stream,
-    // loaded two quarters ahead through a ring of four register buffers.
-    auto unit_w = [&](int i, int g) -> const float* {
-      const GateBwdMmJob& jb = J.j[job_of(tile_of(i))];
-      return jb.W[g] + (int64_t)col * (2 * D) + 16 * q4;
-    };
-    float bq[4][16];
-    auto load_q = [&](const float* wr, int qt, float (&b)[16]) {
+    int units = 0;  // tiles consumed so far (one block barrier each)
+    for (int k = 0; k < J.n; ++k) {
+      const GateBwd128Job& jb = J.j[k];
+      if (b0 >= jb.ntiles) continue;
+      // this lane's W^T entries: lane quad q4 supplies k = 64 qt + 16 q4 + s
+      // in MFMA step s of quarter qt (the same map for A and B)
+      float bq[4][16];
+      {
+        const float* wr = jb.W + (int64_t)col * (2 * D) + 16 * q4;
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const float4 v = *reinterpret_cast<const float4*>(wr + 64 * qt + 4 * u);
-        b[4 * u] = v.x; b[4 * u + 1] = v.y; b[4 * u + 2] = v.z; b[4 * u + 3] = v.w;
+        for (int qt = 0; qt < 4; ++qt)
+#pragma unroll
+          for (int u = 0; u < 4; ++u) {
+            const float4 v = *reinterpret_cast<const float4*>(wr + 64 * qt + 4 * u);
+            bq[qt][4 * u] = v.x; bq[qt][4 * u + 1] = v.y; bq[qt][4 * u + 2] = v.z; bq[qt][4 * u + 3] = v.w;
+          }
       }
-    };
-    {
-      const float* w0 = unit_w(0, 0);
-      load_q(w0, 0, bq[0]);
-      load_q(w0, 1, bq[1]);
-    }
-    int units = 0;  // stages consumed so far (one block barrier each)
-    for (int i = 0; i < nt; ++i) {
-      const int tile = tile_of(i);
-      const int k = job_of(tile);
-      const GateBwdMmJob& jb = J.j[k];
-      const int row0 = (tile - jb.tile0) * kBm2Rows;
-      float rv[2][4];
+      for (int r = b0; r < jb.ntiles; r += G) {
+        const int row0 = r * kBm2Rows;
+        float rv[2][4];
 #pragma unroll
-      for (int rt = 0; rt < 2; ++rt)
+        for (int rt = 0; rt < 2; ++rt)
 #pragma unroll
-        for (int v = 0; v < 4; ++v) {
-          const int row = row0 + 16 * rt + 4 * q4 + v;
-          rv[rt][v] = (jb.res && row < jb.rows) ? jb.res[(int64_t)row * D + col] : 0.f;
-        }
-      v4f acc[2];
+          for (int v = 0; v < 4; ++v) {
+            const int row = row0 + 16 * rt + 4 * q4 + v;
+            rv[rt][v] = (jb.res && row < jb.rows) ? jb.res[(int64_t)row * D + col] : 0.f;
+          }
+        v4f acc[2];
 #pragma unroll
-      for (int rt = 0; rt < 2; ++rt) acc[rt] = v4f{0.f, 0.f, 0.f, 0.f};
-      for (int g = 0; g < jb.ngates; ++g) {
-        const float* wcur = jb.W[g] + (int64_t)col * (2 * D) + 16 * q4;
-        const float* wnext = g + 1 < jb.ngates ? jb.W[g + 1] + (int64_t)col * (2 * D) + 16 * q4
-                             : i + 1 < nt     ? unit_w(i + 1, 0)
-                                              : nullptr;
-        __syncthreads();  // the consumers have written this unit's dz tile
+        for (int rt = 0; rt < 2; ++rt) acc[rt] = v4f{0.f, 0.f, 0.f, 0.f};
+        __syncthreads();  // the consumers have written this tile's dz
         const float* Z = Zs[units & 1];
         ++units;
 #pragma unroll
-        for (int qt = 0; qt < 4; ++qt) {
-          if (qt < 2) load_q(wcur, qt + 2, bq[qt + 2]);
-          else if (wnext) load_q(wnext, qt - 2, bq[qt - 2]);
+        for (int qt = 0; qt < 4; ++qt)
 #pragma unroll
           for (int s4 = 0; s4 < 4; ++s4) {
             float4 a4[2];
@@ -1365,57 +1359,66 @@ __global__ void __launch_bounds__(kBm2Threads, 1) k_gate_bwd_mm128(GateBwdMmJobs
 #pragma unroll
             for (int rt = 0; rt < 2; ++rt) acc[rt] = __builtin_amdgcn_mfma_f32_16x16x4f32(a4[rt].w, b[3], acc[rt], 0, 0, 0);
           }
-        }
+#pragma unroll
+        for (int rt = 0; rt < 2; ++rt)
+#pragma unroll
+          for (int v = 0; v < 4; ++v) {
+            const int row = row0 + 16 * rt + 4 * q4 + v;
+            if (row < jb.rows) jb.dx[(int64_t)row * D + col] = acc[rt][v] + rv[rt][v];
+          }
       }
-#pragma unroll
-      for (int rt = 0; rt < 2; ++rt)
-#pragma unroll
-        for (int v = 0; v < 4; ++v) {
-          const int row = row0 + 16 * rt + 4 * q4 + v;
-          if (row < jb.rows) jb.dx[(int64_t)row * D + col] = acc[rt][v] + rv[rt][v];
-        }
     }
     __syncthreads();  // matches the consumers' final barrier
   } else {
     using GL = Lanes<D, kMmCpl>;
     const int cw = wave - kBm2Prod, j = lane % GL::LPR, slot = lane / GL::LPR;
     const int lr = GL::RPW * cw + slot;  // row of the tile
-    int units = 0;
-    // row indices of a unit, loaded one unit ahead
-    auto unit_idx = [&](int i, int g, BwdMmIdx& x) {
-      if (i >= nt) return;
-      const int tile = tile_of(i);
-      const GateBwdMmJob& jb = J.j[job_of(tile)];
-      const int row = (tile - jb.tile0) * kBm2Rows + lr;
-      if (row < jb.rows) bwd_mm_index(jb.g[g], row, x);
-    };
-    BwdMmIdx xcur{}, xnext{};
-    unit_idx(0, 0, xcur);
-    for (int i = 0; i < nt; ++i) {
-      const int tile = tile_of(i);
-      const int k = __builtin_amdgcn_readfirstlane(job_of(tile));
-      const GateBwdMmJob& jb = J.j[k];
-      const int row = (tile - jb.tile0) * kBm2Rows + lr;
-      for (int g = 0; g < jb.ngates; ++g) {
-        const GateBwdJob& gj = jb.g[g];
-        if (g + 1 < jb.ngates) unit_idx(i, g + 1, xnext);
-        else unit_idx(i + 1, 0, xnext);
-        float lp[4 * kMmCpl];
-#pragma unroll
-        for (int q = 0; q < 4 * kMmCpl; ++q) lp[q] = 0.f;
-        if (row < jb.rows) {
-          const BwdMmIdx x = xcur;
-          const float* lnS = &LnS[k][g][0][0];
-          float* zrow = Zs[units & 1] + lr * kBm2Ld;
-          if (gj.mode == BWD_ATOM) gate_bwd_mm_row<D, BWD_ATOM>(gj, row, x, j, lnS, lp, zrow);
-          else if (gj.mode == BWD_BOND) gate_bwd_mm_row<D, BWD_BOND>(gj, row, x, j, lnS, lp, zrow);
-          else gate_bwd_mm_row<D, BWD_ANGLE>(gj, row, x, j, lnS, lp, zrow);
-        }
-        bwd_mm_ln_add128(lp, Wsum[jb.gid[g]][cw]);
-        xcur = xnext;
-        __syncthreads();  // this unit's dz tile is complete
-        ++units;
+    // the block's tiles in order: (job k, tile r); row indices loaded one
+    // tile ahead
+    auto next_unit = [&](int& k, int& r) {
+      r += G;
+      while (k < J.n && r >= J.j[k].ntiles) {
+        ++k;
+        r = b0;
       }
+    };
+    auto unit_idx = [&](int k, int r, BwdMmIdx& x) {
+      if (k >= J.n) return;
+      const int row = r * kBm2Rows + lr;
+      if (row < J.j[k].rows) bwd_mm_index(J.j[k].g, row, x);
+    };
+    int k = 0, r = b0;
+    while (k < J.n && r >= J.j[k].ntiles) {
+      ++k;
+      r = b0;
+    }
+    BwdMmIdx xcur{}, xnext{};
+    unit_idx(k, r, xcur);
+    int units = 0;
+    while (k < J.n) {
+      int kn = k, rn = r;
+      next_unit(kn, rn);
+      unit_idx(kn, rn, xnext);
+      const GateBwd128Job& jb = J.j[k];
+      const GateBwdJob& gj = jb.g;
+      const int row = r * kBm2Rows + lr;
+      float lp[4 * kMmCpl];
+#pragma unroll
+      for (int q = 0; q < 4 * kMmCpl; ++q) lp[q] = 0.f;
+      if (row < jb.rows) {
+        const BwdMmIdx x = xcur;
+        const float* lnS = &LnS[k][0][0];
+        float* zrow = Zs[units & 1] + lr * kBm2Ld;
+        if (gj.mode == BWD_ATOM) gate_bwd_mm_row<D, BWD_ATOM>(gj, row, x, j, lnS, lp, zrow);
+        else if (gj.mode == BWD_BOND) gate_bwd_mm_row<D, BWD_BOND>(gj, row, x, j, lnS, lp, zrow);
+        else gate_bwd_mm_row<D, BWD_ANGLE>(gj, row, x, j, lnS, lp, zrow);
+      }
+      bwd_mm_ln_add128(lp, Wsum[jb.gid][cw]);
+      xcur = xnext;
+      k = kn;
+      r = rn;
+      __syncthreads();  // this tile's dz is complete
+      ++units;
     }
     __syncthreads();  // the producers have read the last tile
   }
@@ -2517,30 +2520,60 @@ int gate_bwd_launch(int D, GateBwdJobs J, float* const* ln_grad, const int* slot
 // is appended to `defer`.
 int gate_bwd_mm_launch(int D, GateBwdMmJobs J, float* const* ln_grad, const int* slot, const Acts& a,
                        std::vector<ReduceJob>& defer, hipStream_t st) {
+  bool used[3] = {false, false, false};
+  auto ln_slots = [&](int grid, float** lnpart) -> int {
+    if ((int64_t)grid * 4 * D > a.lnpart_stride)
+      return fail(CHGNET_EINVAL, "gate_bwd_mm: LayerNorm partial slots too small");
+    for (int gid = 0; gid < 3; ++gid) {
+      lnpart[gid] = nullptr;
+      if (!used[gid] || !ln_grad) continue;
+      lnpart[gid] = a.lnpart + (int64_t)slot[gid] * a.lnpart_stride;
+      defer.push_back(ReduceJob{lnpart[gid], grid, 4 * D, 4 * D, ln_grad[gid]});
+    }
+    return CHGNET_OK;
+  };
+  if (D == 128) {
+    // one job per gate; a job's later gates add to the dX its first wrote
+    GateBwd128Jobs K{};
+    int maxt = 0;
+    for (int i = 0; i < J.n; ++i) {
+      const GateBwdMmJob& q = J.j[i];
+      if (q.rows <= 0) continue;
+      for (int g = 0; g < q.ngates; ++g) {
+        if (K.n == 3) return fail(CHGNET_EINVAL, "gate_bwd_mm: more than three gates");
+        GateBwd128Job& k = K.j[K.n++];
+        k.rows = q.rows;
+        k.ntiles = (int)cdiv(q.rows, kBm2Rows);
+        k.gid = q.gid[g];
+        k.g = q.g[g];
+        k.W = q.W[g];
+        k.res = g == 0 ? q.res : q.dx;
+        k.dx = q.dx;
+        used[k.gid] = true;
+        maxt = std::max(maxt, k.ntiles);
+      }
+    }
+    if (maxt == 0) return CHGNET_OK;
+    const int grid = std::min(maxt, 256);
+    if (int rc = ln_slots(grid, K.lnpart)) return rc;
+    KLAUNCH(st, "k_gate_bwd", k_gate_bwd_mm128<<<grid, kBm2Threads, 0, st>>>(K));
+    return CHGNET_OK;
+  }
   GateBwdMmJobs K{};
   int tiles = 0;
-  bool used[3] = {false, false, false};
-  const int rows_per_tile = D == 64 ? kMmRows : kBm2Rows;
   for (int i = 0; i < J.n; ++i) {
     if (J.j[i].rows <= 0) continue;
     K.j[K.n] = J.j[i];
     K.j[K.n].tile0 = tiles;
-    tiles += (int)cdiv(J.j[i].rows, rows_per_tile);
+    tiles += (int)cdiv(J.j[i].rows, kMmRows);
     for (int g = 0; g < J.j[i].ngates; ++g) used[J.j[i].gid[g]] = true;
     K.n++;
   }
   K.ntiles = tiles;
   if (tiles == 0) return CHGNET_OK;
   const int grid = std::min(tiles, 256);
-  if ((int64_t)grid * 4 * D > a.lnpart_stride) return fail(CHGNET_EINVAL, "gate_bwd_mm: LayerNorm partial slots too small");
-  for (int gid = 0; gid < 3; ++gid) {
-    K.lnpart[gid] = nullptr;
-    if (!used[gid] || !ln_grad) continue;
-    K.lnpart[gid] = a.lnpart + (int64_t)slot[gid] * a.lnpart_stride;
-    defer.push_back(ReduceJob{K.lnpart[gid], grid, 4 * D, 4 * D, ln_grad[gid]});
-  }
-  if (D == 64) KLAUNCH(st, "k_gate_bwd", k_gate_bwd_mm<<<grid, kMmThreads, 0, st>>>(K));
-  else KLAUNCH(st, "k_gate_bwd", k_gate_bwd_mm128<<<grid, kBm2Threads, 0, st>>>(K));
+  if (int rc = ln_slots(grid, K.lnpart)) return rc;
+  KLAUNCH(st, "k_gate_bwd", k_gate_bwd_mm<<<grid, kMmThreads, 0, st>>>(K));
   return CHGNET_OK;
 }
 
