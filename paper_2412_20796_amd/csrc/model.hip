@@ -405,6 +405,13 @@ struct GateMmJobs {
 
 constexpr int kMmCpl = 8;
 
+// Wave priority of the consumer wavefronts in the fused gate kernels. The
+// consumers' chains of dependent loads set the pace of a tile; ahead of the
+// producers' MFMA stream in instruction issue they finish sooner (measured
+// at d = 128: backward 1.34 -> 1.14 ms and forward 1.01 -> 0.96 ms per layer
+// launch), while the producers, with a tile of slack, lose nothing.
+constexpr int kConsumerPrio = 2;
+
 template <int D>
 struct MmCfg {
   static constexpr int Rows = D == 64 ? 64 : 32;  // rows per tile
@@ -658,6 +665,7 @@ __global__ void __launch_bounds__(MmCfg<D>::Threads, 1) k_gate_fwd_mm(GateMmJobs
       __syncthreads();
     }
   } else {
+    __builtin_amdgcn_s_setprio(kConsumerPrio);
     // lane row within the tile; gathered operands of the next tile and row
     // indices of the one after
     using GL = Lanes<D, kMmCpl>;
@@ -1184,6 +1192,7 @@ __global__ void __launch_bounds__(kMmThreads, 1) k_gate_bwd_mm(GateBwdMmJobs J) 
       __syncthreads();
     }
   } else {
+    __builtin_amdgcn_s_setprio(kConsumerPrio);
     using GL = Lanes<64, kMmCpl>;
     const int cw = wave - kMmProducers, j = lane % GL::LPR, slot = lane / GL::LPR;
     // Every wavefront covers the same 8 rows of each of the tile's gates
@@ -1370,6 +1379,7 @@ __global__ void __launch_bounds__(kBm2Threads, 1) k_gate_bwd_mm128(GateBwd128Job
     }
     __syncthreads();  // matches the consumers' final barrier
   } else {
+    __builtin_amdgcn_s_setprio(kConsumerPrio);
     using GL = Lanes<D, kMmCpl>;
     const int cw = wave - kBm2Prod, j = lane % GL::LPR, slot = lane / GL::LPR;
     const int lr = GL::RPW * cw + slot;  // row of the tile
