@@ -448,10 +448,22 @@ struct TnLaunch {
 // layer whose weight gradient is X^T Y).
 // ROLE only names the instantiation (1: interaction-block weight gradients).
 constexpr int kTnRed = 2 * 64 * 64 + 4 * 64;
+// Rows per split-K chunk at most: the eight output tiles of a chunk stream
+// the same rows on one XCD, and a chunk of 2048 rows of 384 floats (3 MB)
+// stays in that XCD's 4 MB L2 while they do (4480-row chunks measured 1.30
+// ms per wide128 layer launch against 1.01 ms).
+constexpr int kTnMaxChunkRows = 2048;
+// rows of one wavefront's range (a quarter of a chunk): the size of its
+// LDS row-index tables
+constexpr int kTnWaveRows = kTnMaxChunkRows / 4;
 
-template <int VX, int VY, bool XFULL, bool YFULL, bool HASX = true>
+// RIDX: the problem gathers X or Y rows through an index array. The wave
+// first copies its range's row indices to LDS (ridx: [2][kTnWaveRows]), so
+// the fragment loads depend on no other global load and the loads of the
+// groups ahead stay in flight.
+template <int VX, int VY, bool XFULL, bool YFULL, bool HASX, bool RIDX>
 __device__ __forceinline__ void tn_wave(const TnPlan& Q, int chunk, int m0, int n0, bool colsum, float* red,
-                                        float* __restrict__ part) {
+                                        int* ridx, float* __restrict__ part) {
   // MFMA k-steps (row pairs) per register buffer: 2, or 1 where two-column
   // fragments are loaded one element at a time (partial or unaligned tiles,
   // not on the common shapes)
@@ -480,6 +492,12 @@ __device__ __forceinline__ void tn_wave(const TnPlan& Q, int chunk, int m0, int 
   // range are cancelled by a 0/1 mask on the Y values, applied when the
   // group is consumed, so that every load of a group is in flight at once.
   float rmask[NB][KS];
+  if (RIDX) {
+    for (int r = rlo + lane; r < rhi; r += 64) {
+      ridx[r - rlo] = P.x_rows ? P.x_rows[r] : r;
+      ridx[kTnWaveRows + r - rlo] = P.y_rows ? P.y_rows[r] : r;
+    }
+  }
   auto fetch = [&](int g, int b) {
     int xr[KS], yr[KS];
 #pragma unroll
@@ -487,12 +505,12 @@ __device__ __forceinline__ void tn_wave(const TnPlan& Q, int chunk, int m0, int 
       xr[i] = yr[i] = min(g + KS * h + i, rhi - 1);
       rmask[b][i] = g + KS * h + i < rhi ? 1.f : 0.f;
     }
-    if (P.x_rows)
+    if (RIDX)
 #pragma unroll
-      for (int i = 0; i < KS; ++i) xr[i] = P.x_rows[xr[i]];
-    if (P.y_rows)
-#pragma unroll
-      for (int i = 0; i < KS; ++i) yr[i] = P.y_rows[yr[i]];
+      for (int i = 0; i < KS; ++i) {
+        xr[i] = ridx[xr[i] - rlo];
+        yr[i] = ridx[kTnWaveRows + yr[i] - rlo];
+      }
 #pragma unroll
     for (int i = 0; i < KS; ++i) {
       if (HASX) {
@@ -620,9 +638,34 @@ __device__ __forceinline__ void tn_wave(const TnPlan& Q, int chunk, int m0, int 
   }
 }
 
+template <bool RIDX>
+__device__ __forceinline__ void tn_dispatch(const TnPlan& Q, int chunk, int m0, int n0, bool colsum, bool xf, bool yf,
+                                            float* red, int* ridx, float* __restrict__ part) {
+  if (Q.tiles_m == 0) {
+    // column sums only
+    if (yf) tn_wave<1, 2, false, true, false, RIDX>(Q, chunk, m0, n0, colsum, red, ridx, part);
+    else if (Q.vy == 2) tn_wave<1, 2, false, false, false, RIDX>(Q, chunk, m0, n0, colsum, red, ridx, part);
+    else tn_wave<1, 1, false, false, false, RIDX>(Q, chunk, m0, n0, colsum, red, ridx, part);
+  } else if (Q.vx == 2 && Q.vy == 2) {
+    if (xf && yf) tn_wave<2, 2, true, true, true, RIDX>(Q, chunk, m0, n0, colsum, red, ridx, part);
+    else if (xf) tn_wave<2, 2, true, false, true, RIDX>(Q, chunk, m0, n0, colsum, red, ridx, part);
+    else if (yf) tn_wave<2, 2, false, true, true, RIDX>(Q, chunk, m0, n0, colsum, red, ridx, part);
+    else tn_wave<2, 2, false, false, true, RIDX>(Q, chunk, m0, n0, colsum, red, ridx, part);
+  } else if (Q.vx == 2) {
+    if (xf) tn_wave<2, 1, true, false, true, RIDX>(Q, chunk, m0, n0, colsum, red, ridx, part);
+    else tn_wave<2, 1, false, false, true, RIDX>(Q, chunk, m0, n0, colsum, red, ridx, part);
+  } else if (Q.vy == 2) {
+    if (yf) tn_wave<1, 2, false, true, true, RIDX>(Q, chunk, m0, n0, colsum, red, ridx, part);
+    else tn_wave<1, 2, false, false, true, RIDX>(Q, chunk, m0, n0, colsum, red, ridx, part);
+  } else {
+    tn_wave<1, 1, false, false, true, RIDX>(Q, chunk, m0, n0, colsum, red, ridx, part);
+  }
+}
+
 template <int ROLE>
 __global__ void __launch_bounds__(256, 3) k_tn(TnLaunch L, float* __restrict__ part) {
   __shared__ float red[kTnRed];
+  __shared__ int ridx_all[4][2][kTnWaveRows];
   int k = 0;
   while (k + 1 < L.n && (int)blockIdx.x >= L.q[k + 1].block0) ++k;
   const TnPlan& Q = L.q[k];
@@ -649,25 +692,9 @@ __global__ void __launch_bounds__(256, 3) k_tn(TnLaunch L, float* __restrict__ p
   const TnProblem& P = Q.p;
   const bool xf = Q.vx == 2 && P.X && ((P.ldx | P.x_col) & 1) == 0 && ((uintptr_t)P.X & 7) == 0 && m0 + 64 <= P.M;
   const bool yf = Q.vy == 2 && ((P.ldy | P.y_col) & 1) == 0 && ((uintptr_t)P.Y & 7) == 0 && n0 + 64 <= P.N;
-  if (Q.tiles_m == 0) {
-    // column sums only
-    if (yf) tn_wave<1, 2, false, true, false>(Q, chunk, m0, n0, colsum, red, part);
-    else if (Q.vy == 2) tn_wave<1, 2, false, false, false>(Q, chunk, m0, n0, colsum, red, part);
-    else tn_wave<1, 1, false, false, false>(Q, chunk, m0, n0, colsum, red, part);
-  } else if (Q.vx == 2 && Q.vy == 2) {
-    if (xf && yf) tn_wave<2, 2, true, true>(Q, chunk, m0, n0, colsum, red, part);
-    else if (xf) tn_wave<2, 2, true, false>(Q, chunk, m0, n0, colsum, red, part);
-    else if (yf) tn_wave<2, 2, false, true>(Q, chunk, m0, n0, colsum, red, part);
-    else tn_wave<2, 2, false, false>(Q, chunk, m0, n0, colsum, red, part);
-  } else if (Q.vx == 2) {
-    if (xf) tn_wave<2, 1, true, false>(Q, chunk, m0, n0, colsum, red, part);
-    else tn_wave<2, 1, false, false>(Q, chunk, m0, n0, colsum, red, part);
-  } else if (Q.vy == 2) {
-    if (yf) tn_wave<1, 2, false, true>(Q, chunk, m0, n0, colsum, red, part);
-    else tn_wave<1, 2, false, false>(Q, chunk, m0, n0, colsum, red, part);
-  } else {
-    tn_wave<1, 1, false, false>(Q, chunk, m0, n0, colsum, red, part);
-  }
+  int* ridx = &ridx_all[threadIdx.x >> 6][0][0];
+  if (P.x_rows || P.y_rows) tn_dispatch<true>(Q, chunk, m0, n0, colsum, xf, yf, red, ridx, part);
+  else tn_dispatch<false>(Q, chunk, m0, n0, colsum, xf, yf, red, ridx, part);
 }
 
 // Ordered column sums of chunk partials: 16 wavefronts per block, wave w
@@ -816,11 +843,6 @@ int gemm_launch(const GemmBatch& b, hipStream_t st, const char* tag) {
   return CHGNET_OK;
 }
 
-// Rows per split-K chunk at most: the eight output tiles of a chunk stream
-// the same rows on one XCD, and a chunk of 2048 rows of 384 floats (3 MB)
-// stays in that XCD's 4 MB L2 while they do (4480-row chunks measured 1.30
-// ms per wide128 layer launch against 1.01 ms).
-constexpr int kTnMaxChunkRows = 2048;
 
 int tn_launch(const TnBatch& b, float* part, int64_t part_cap, hipStream_t st, const char* tag) {
   if (b.n == 0) return CHGNET_OK;
