@@ -342,23 +342,10 @@ struct GateAdds {
 };
 
 template <int D, int CPL>
-__device__ __forceinline__ void load_z(const float* __restrict__ z, int ldz, const GateAdds& ad, int row, int j,
-                                       float (&zc)[CPL], float (&zg)[CPL]) {
+__device__ __forceinline__ void load_z(const float* __restrict__ z, int ldz, int row, int j, float (&zc)[CPL],
+                                       float (&zg)[CPL]) {
   load_cols_nt<D, CPL>(z + (int64_t)row * ldz, j, zc);
   load_cols_nt<D, CPL>(z + (int64_t)row * ldz + D, j, zg);
-#pragma unroll
-  for (int q = 0; q < kMaxAdds; ++q) {
-    if (q >= ad.n) break;
-    const float* r = ad.p[q] + (int64_t)ad.idx[q][row] * ad.ld[q];
-    float uc[CPL], ug[CPL];
-    load_cols<D, CPL>(r, j, uc);
-    load_cols<D, CPL>(r + D, j, ug);
-#pragma unroll
-    for (int k = 0; k < CPL; ++k) {
-      zc[k] += uc[k];
-      zg[k] += ug[k];
-    }
-  }
 }
 
 // Columns per lane of the row-layout backward gate.
@@ -394,7 +381,7 @@ struct GateMmJob {
   const float* mulv;
   const int* mul_idx;
   float* out;
-  float* zsave;  // optional [rows, ldzs]: x W + b, kept for the backward pass
+  float* zsave;  // optional [rows, ldzs]: the whole pre-activation z, kept for the backward pass
   int ldzs;
   float* xcopy;  // optional [rows, d]: a copy of x (the residual part of e^{t+1})
 };
@@ -489,10 +476,6 @@ __device__ __forceinline__ void gate_mm_row(const GateMmJob& J, int row, int lr,
       zg[4 * q] = b.x; zg[4 * q + 1] = b.y; zg[4 * q + 2] = b.z; zg[4 * q + 3] = b.w;
     }
   }
-  if (J.zsave) {
-    store_cols_nt<D, CPL>(J.zsave + (int64_t)row * J.ldzs, j, zc);
-    store_cols_nt<D, CPL>(J.zsave + (int64_t)row * J.ldzs + D, j, zg);
-  }
 #pragma unroll
   for (int q = 0; q < kMaxAdds; ++q) {
     if (q >= J.ad.n) break;
@@ -501,6 +484,10 @@ __device__ __forceinline__ void gate_mm_row(const GateMmJob& J, int row, int lr,
       zc[k] += in.ac[q][k];
       zg[k] += in.ag[q][k];
     }
+  }
+  if (J.zsave) {
+    store_cols_nt<D, CPL>(J.zsave + (int64_t)row * J.ldzs, j, zc);
+    store_cols_nt<D, CPL>(J.zsave + (int64_t)row * J.ldzs + D, j, zg);
   }
   ln_stats<D, CPL>(zc, zg, rc, rg);
   float o[CPL];
@@ -726,8 +713,7 @@ enum GateBwdMode { BWD_ATOM = 0, BWD_BOND = 1, BWD_ANGLE = 2 };
 constexpr int kGateRows = 128;
 struct GateBwdJob {
   int mode, rows, ldz, lddz, block0;
-  const float* z;
-  GateAdds ad;
+  const float* z;  // the saved pre-activations [rows, ldz]
   LnPtrs ln;
   const float *up, *eb;
   const int *up_idx, *b2_idx;
@@ -752,7 +738,6 @@ template <int D, int MODE>
 __device__ __forceinline__ void gate_bwd_rows(int blk, const GateBwdJob& J, float* red) {
   const int rows = J.rows, ldz = J.ldz, lddz = J.lddz;
   const float* __restrict__ z = J.z;
-  const GateAdds& ad = J.ad;
   const LnPtrs& ln = J.ln;
   const float* __restrict__ up = J.up;
   const int* __restrict__ up_idx = J.up_idx;
@@ -774,7 +759,7 @@ __device__ __forceinline__ void gate_bwd_rows(int blk, const GateBwdJob& J, floa
     const int row = blk * kGateRows + (it * 4 + wave) * RPW + slot;
     if (row >= rows) continue;
     float zc[CPL], zg[CPL], rc, rg;
-    load_z<D, CPL>(z, ldz, ad, row, j, zc, zg);
+    load_z<D, CPL>(z, ldz, row, j, zc, zg);
     ln_stats<D, CPL>(zc, zg, rc, rg);
     float u[CPL], w[CPL], dphi[CPL];
     if (MODE == BWD_ANGLE) {
@@ -913,14 +898,12 @@ struct GateBwdMmJobs {
 };
 constexpr int kBmLd = 256 + 4;
 
-// Row indices of a consumer row: the gathered terms' rows, the upstream row
-// and (bond gate) the second bond.
+// Row indices of a consumer row: the upstream row and (bond gate) the second
+// bond.
 struct BwdMmIdx {
-  int a0, a1, up, b2;
+  int up, b2;
 };
 __device__ __forceinline__ void bwd_mm_index(const GateBwdJob& J, int row, BwdMmIdx& x) {
-  x.a0 = J.ad.n > 0 ? J.ad.idx[0][row] : 0;
-  x.a1 = J.ad.n > 1 ? J.ad.idx[1][row] : 0;
   x.up = J.mode == BWD_ANGLE ? row : J.up_idx[row];
   x.b2 = J.mode == BWD_BOND ? J.b2_idx[row] : 0;
 }
@@ -966,29 +949,6 @@ __device__ __forceinline__ void gate_bwd_mm_row(const GateBwdJob& J, int row, co
   float zc[CPL], zg[CPL], rc, rg;
   load_cols_nt<D, CPL>(J.z + (int64_t)row * J.ldz, j, zc);
   load_cols_nt<D, CPL>(J.z + (int64_t)row * J.ldz + D, j, zg);
-  static_assert(kMaxAdds == 2, "two gathered terms");
-  if (J.ad.n > 0) {
-    float uc[CPL], ug[CPL];
-    const float* r = J.ad.p[0] + (int64_t)x.a0 * J.ad.ld[0];
-    load_cols<D, CPL>(r, j, uc);
-    load_cols<D, CPL>(r + D, j, ug);
-#pragma unroll
-    for (int k = 0; k < CPL; ++k) {
-      zc[k] += uc[k];
-      zg[k] += ug[k];
-    }
-  }
-  if (J.ad.n > 1) {
-    float uc[CPL], ug[CPL];
-    const float* r = J.ad.p[1] + (int64_t)x.a1 * J.ad.ld[1];
-    load_cols<D, CPL>(r, j, uc);
-    load_cols<D, CPL>(r + D, j, ug);
-#pragma unroll
-    for (int k = 0; k < CPL; ++k) {
-      zc[k] += uc[k];
-      zg[k] += ug[k];
-    }
-  }
   // the running sum d e^a of this edge, loaded with the row's other inputs
   // (after the dz stores the load could not be moved ahead of them)
   float de[CPL];
@@ -2479,14 +2439,13 @@ GateMmJob mm_job(int D, int mode, int64_t rows, const float* x, const float* W, 
   return j;
 }
 
-GateBwdJob bwd_job(int mode, int64_t rows, const float* z, int ldz, const GateAdds& ad, LnPtrs ln, const float* up,
+GateBwdJob bwd_job(int mode, int64_t rows, const float* z, int ldz, LnPtrs ln, const float* up,
                    const int* up_idx, const float* eb, const int* b2_idx, float* aux, float* dz, int lddz) {
   GateBwdJob j{};
   j.mode = mode;
   j.rows = (int)rows;
   j.z = z;
   j.ldz = ldz;
-  j.ad = ad;
   j.ln = ln;
   j.up = up;
   j.up_idx = up_idx;
@@ -3083,9 +3042,6 @@ int backward_impl(Ctx& c, const float* Pflat, bool repack, const float* dE, cons
     const int nx = 1 - cur, enx = (ecur + 1) % 3;
     std::vector<GemmProblem> ps;
     std::vector<TnProblem> ts;
-    const GateAdds ad_av = adds(2, a.Xa[t], 8 * D, a.edge_src, a.Xa[t] + 2 * D, 8 * D, g.edge_dst);
-    const GateAdds ad_be = adds(2, a.Xb[t], 8 * D, a.ang_b1, a.Xb[t] + 4 * D, 8 * D, a.ang_b2);
-    const GateAdds ad_an = adds(2, a.Xb[t] + 2 * D, 8 * D, a.ang_b1, a.Xb[t] + 6 * D, 8 * D, a.ang_b2);
     // GatedMLP backward: bit 0 atom conv, bit 1 bond conv, bit 2 angle update
     auto gates = [&](int which) -> int {
       if (!ang) which &= 3;
@@ -3095,20 +3051,20 @@ int backward_impl(Ctx& c, const float* Pflat, bool repack, const float* dE, cons
       if (which & 2) {
         slot[J.n] = 3 * t;
         lg_out[J.n] = G + lg.be.g_c;
-        J.j[J.n++] = bwd_job(BWD_BOND, A, a.zae[t], 4 * D, ad_be, ln_ptrs(P, lo.be), a.dmu, a.ang_b1, a.eb, a.ang_b2,
+        J.j[J.n++] = bwd_job(BWD_BOND, A, a.zae[t], 4 * D, ln_ptrs(P, lo.be), a.dmu, a.ang_b1, a.eb, a.ang_b2,
                              a.t2, a.dzae, 4 * D);
       }
       if (which & 1) {
         slot[J.n] = 3 * t + 1;
         lg_out[J.n] = G + lg.av.g_c;
-        J.j[J.n++] = bwd_job(BWD_ATOM, E, a.zv[t], 2 * D, ad_av, ln_ptrs(P, lo.av), a.dm, a.edge_src, a.ea, nullptr,
+        J.j[J.n++] = bwd_job(BWD_ATOM, E, a.zv[t], 2 * D, ln_ptrs(P, lo.av), a.dm, a.edge_src, a.ea, nullptr,
                              a.dea, a.dzv, 2 * D);
         J.j[J.n - 1].aux_acc = t < m.T - 1;  // the first layer of the backward starts d e^a
       }
       if (which & 4) {
         slot[J.n] = 3 * t + 2;
         lg_out[J.n] = G + lg.an.g_c;
-        J.j[J.n++] = bwd_job(BWD_ANGLE, A, a.zae[t] + 2 * D, 4 * D, ad_an, ln_ptrs(P, lo.an), a.da[cur], nullptr,
+        J.j[J.n++] = bwd_job(BWD_ANGLE, A, a.zae[t] + 2 * D, 4 * D, ln_ptrs(P, lo.an), a.da[cur], nullptr,
                              nullptr, nullptr, nullptr, a.dzae + 2 * D, 4 * D);
       }
       return gate_bwd_launch(D, J, wg ? lg_out : nullptr, slot, a, reduce_jobs, st);
@@ -3123,7 +3079,7 @@ int backward_impl(Ctx& c, const float* Pflat, bool repack, const float* dE, cons
         q.rows = (int)E;
         q.ngates = 1;
         q.gid[0] = 0;
-        q.g[0] = bwd_job(BWD_ATOM, E, a.zv[t], 2 * D, ad_av, ln_ptrs(P, lo.av), a.dm, a.edge_src, a.ea, nullptr, a.dea,
+        q.g[0] = bwd_job(BWD_ATOM, E, a.zv[t], 2 * D, ln_ptrs(P, lo.av), a.dm, a.edge_src, a.ea, nullptr, a.dea,
                          a.dzv, 2 * D);
         q.g[0].aux_acc = t < m.T - 1;  // the first layer of the backward starts d e^a
         q.W[0] = Wav + 2 * D * 2 * D;
@@ -3135,12 +3091,12 @@ int backward_impl(Ctx& c, const float* Pflat, bool repack, const float* dE, cons
         q.rows = (int)A;
         q.ngates = ang ? 2 : 1;
         q.gid[0] = 1;
-        q.g[0] = bwd_job(BWD_BOND, A, a.zae[t], 4 * D, ad_be, ln_ptrs(P, lo.be), a.dmu, a.ang_b1, a.eb, a.ang_b2, a.t2,
+        q.g[0] = bwd_job(BWD_BOND, A, a.zae[t], 4 * D, ln_ptrs(P, lo.be), a.dmu, a.ang_b1, a.eb, a.ang_b2, a.t2,
                          a.dzae, 4 * D);
         q.W[0] = Wbe + 3 * D * 2 * D;
         if (ang) {
           q.gid[1] = 2;
-          q.g[1] = bwd_job(BWD_ANGLE, A, a.zae[t] + 2 * D, 4 * D, ad_an, ln_ptrs(P, lo.an), a.da[cur], nullptr, nullptr,
+          q.g[1] = bwd_job(BWD_ANGLE, A, a.zae[t] + 2 * D, 4 * D, ln_ptrs(P, lo.an), a.da[cur], nullptr, nullptr,
                            nullptr, nullptr, a.dzae + 2 * D, 4 * D);
           q.W[1] = Wan + 3 * D * 2 * D;
           q.res = a.da[cur];
