@@ -1537,6 +1537,7 @@ __global__ void __launch_bounds__(256, 2) k_head_mlp(HeadJobs J) {
 struct SegJob {
   int nseg, ncb, width, ld_in, ld_out, ld_mul, ld_out2, accumulate, block0;
   int wps;  // wavefronts per (segment, column block): 4 for long segments, 1 for short
+  int lpr;  // set by the launch: 0, one column a lane; else lanes per row, four columns a lane
   // optional output linear of the update (64-wide rows only): with y the
   // segment's result (out2 if set, else out), upd[urow(s)] = res[urow(s)]
   // + y Wo + bo, urow = upd_rows ? upd_rows[s] : s
@@ -1558,7 +1559,7 @@ struct SegJobs {
 };
 
 template <int WPS>
-__device__ __forceinline__ void segsum_block(const SegJob& S) {
+__device__ __forceinline__ void segsum_block(const SegJob& S, float (*red)[64]) {
   constexpr int SPB = 4 / WPS;  // (segment, column block) units per block
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int unit = (blockIdx.x - S.block0) * SPB + wave / WPS, w = wave % WPS;
@@ -1581,7 +1582,6 @@ __device__ __forceinline__ void segsum_block(const SegJob& S) {
   }
   float acc = (a0 + a1) + (a2 + a3);
   if (WPS > 1) {
-    __shared__ float red[4][64];
     red[wave][lane] = acc;
     __syncthreads();
     if (w != 0) return;
@@ -1612,13 +1612,122 @@ __device__ __forceinline__ void segsum_block(const SegJob& S) {
   }
 }
 
+// The same sums with four columns a lane (16-byte loads and stores): LPR
+// lanes cover a row's column block of 4 LPR columns and a load instruction
+// covers 64 / LPR rows. A wave takes groups of U instructions' rows; rows
+// are clamped into the segment (the surplus is loaded and weighted 0), so
+// every load of a group is issued at once, and with IDX the row indices of
+// the wave's next group are loaded while the current group's rows are.
+template <int WPS, int LPR, int U, bool IDX>
+__device__ __forceinline__ void segsum_block4(const SegJob& S, float4 (*red4)[64]) {
+  constexpr int SPB = 4 / WPS, RPI = 64 / LPR, G = U * RPI;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int unit = (blockIdx.x - S.block0) * SPB + wave / WPS, w = wave % WPS;
+  const int s = unit / S.ncb, sub = lane / LPR;
+  const int c = (unit % S.ncb) * 4 * LPR + 4 * (lane % LPR);
+  const bool ok = s < S.nseg && c < S.width;
+  float4 a[U];
+#pragma unroll
+  for (int u = 0; u < U; ++u) a[u] = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (ok) {
+    const int lo = S.ptr[s], hi = S.ptr[s + 1];
+    const float* __restrict__ vals = S.vals + c;
+    int ix[U];
+    auto rows_of = [&](int g) {
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int r = min(g + u * RPI + sub, hi - 1);
+        ix[u] = IDX ? S.idx[r] : r;
+      }
+    };
+    int g = lo + G * w;
+    if (g < hi) rows_of(g);
+    for (; g < hi; g += G * WPS) {
+      int cur[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) cur[u] = ix[u];
+      rows_of(g + G * WPS);
+      float4 x[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) x[u] = *reinterpret_cast<const float4*>(vals + (int64_t)cur[u] * S.ld_in);
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const float m = g + u * RPI + sub < hi ? 1.f : 0.f;
+        a[u].x += m * x[u].x;
+        a[u].y += m * x[u].y;
+        a[u].z += m * x[u].z;
+        a[u].w += m * x[u].w;
+      }
+    }
+  }
+  // fixed-order sums: the U partials, the lane groups of the other rows of an
+  // instruction, then the WPS wavefronts
+  float4 acc = a[0];
+#pragma unroll
+  for (int u = 1; u < U; ++u) {
+    acc.x += a[u].x;
+    acc.y += a[u].y;
+    acc.z += a[u].z;
+    acc.w += a[u].w;
+  }
+#pragma unroll
+  for (int m = LPR; m < 64; m *= 2) {
+    acc.x += __shfl_xor(acc.x, m);
+    acc.y += __shfl_xor(acc.y, m);
+    acc.z += __shfl_xor(acc.z, m);
+    acc.w += __shfl_xor(acc.w, m);
+  }
+  if (WPS > 1) {
+    red4[wave][lane] = acc;
+    __syncthreads();
+    if (w != 0) return;
+    for (int q = 1; q < WPS; ++q) {
+      const float4 t = red4[wave + q][lane];
+      acc.x += t.x;
+      acc.y += t.y;
+      acc.z += t.z;
+      acc.w += t.w;
+    }
+  }
+  if (!ok || sub != 0) return;
+  float4* o = reinterpret_cast<float4*>(S.out + (int64_t)s * S.ld_out + c);
+  if (S.accumulate) {
+    const float4 t = *o;
+    acc.x += t.x;
+    acc.y += t.y;
+    acc.z += t.z;
+    acc.w += t.w;
+  }
+  *o = acc;
+  if (S.out2) {
+    const float4 m = *reinterpret_cast<const float4*>(S.mul + (int64_t)s * S.ld_mul + c);
+    *reinterpret_cast<float4*>(S.out2 + (int64_t)s * S.ld_out2 + c) =
+        make_float4(m.x * acc.x, m.y * acc.y, m.z * acc.z, m.w * acc.w);
+  }
+}
+
+template <int WPS, int U>
+__device__ __forceinline__ void segsum_job(const SegJob& S, float4 (*red4)[64]) {
+  if (S.lpr == 0) segsum_block<WPS>(S, reinterpret_cast<float (*)[64]>(red4));
+  else if (S.idx) {
+    if (S.lpr == 64) segsum_block4<WPS, 64, U, true>(S, red4);
+    else if (S.lpr == 32) segsum_block4<WPS, 32, U, true>(S, red4);
+    else segsum_block4<WPS, 16, U, true>(S, red4);
+  } else {
+    if (S.lpr == 64) segsum_block4<WPS, 64, U, false>(S, red4);
+    else if (S.lpr == 32) segsum_block4<WPS, 32, U, false>(S, red4);
+    else segsum_block4<WPS, 16, U, false>(S, red4);
+  }
+}
+
 // Jobs of either segment length in one launch; each block runs its job's
 // variant (the choice is uniform over the block).
 __global__ void __launch_bounds__(256) k_segsum(SegJobs J) {
+  __shared__ float4 red4[4][64];  // wavefront partials (WPS > 1)
   int k = 0;
   while (k + 1 < J.n && (int)blockIdx.x >= J.j[k + 1].block0) ++k;
-  if (J.j[k].wps == 4) segsum_block<4>(J.j[k]);
-  else segsum_block<1>(J.j[k]);
+  if (J.j[k].wps == 4) segsum_job<4, 8>(J.j[k], red4);
+  else segsum_job<1, 4>(J.j[k], red4);
 }
 
 // Per bond b (centre i, local index q among k bonds): DZ1 = sum over the
@@ -2366,14 +2475,24 @@ SegJob seg_job(int64_t nseg, const int* ptr, const int* idx, const float* vals, 
 int segsum_launch(SegJobs J, int wps, hipStream_t st) {
   SegJobs K{};
   int blocks = 0;
+  auto al16 = [](const void* p, int ld) { return ((uintptr_t)p & 15) == 0 && (ld & 3) == 0; };
   for (int i = 0; i < J.n; ++i) {
     if (J.j[i].nseg <= 0) continue;
-    K.j[K.n] = J.j[i];
-    K.j[K.n].block0 = blocks;
-    if (K.j[K.n].wps != 1 && K.j[K.n].wps != 4) K.j[K.n].wps = wps;
-    if (K.j[K.n].Wo && (K.j[K.n].width != 64 || K.j[K.n].ncb != 1))
+    SegJob& q = K.j[K.n];
+    q = J.j[i];
+    q.block0 = blocks;
+    if (q.wps != 1 && q.wps != 4) q.wps = wps;
+    if (q.Wo && (q.width != 64 || q.ncb != 1))
       return fail(CHGNET_EINVAL, "segsum: the fused output linear needs 64-wide rows");
-    blocks += (int)cdiv((int64_t)J.j[i].nseg * J.j[i].ncb, 4 / K.j[K.n].wps);
+    // four columns a lane where rows and pointers allow 16-byte accesses
+    q.lpr = 0;
+    const bool vec = !q.Wo && q.width % 4 == 0 && al16(q.vals, q.ld_in) && al16(q.out, q.ld_out) &&
+                     (!q.out2 || (al16(q.out2, q.ld_out2) && al16(q.mul, q.ld_mul)));
+    if (vec && (q.width >= 256 || 256 % q.width == 0) && q.width >= 64) {
+      q.lpr = std::min(64, q.width / 4);
+      q.ncb = (int)cdiv(q.width, 4 * q.lpr);
+    }
+    blocks += (int)cdiv((int64_t)q.nseg * q.ncb, 4 / q.wps);
     K.n++;
   }
   if (blocks == 0) return CHGNET_OK;
