@@ -45,8 +45,9 @@ def parse():
                          "structures at evenly spaced size quantiles)")
     ap.add_argument("--no-roofline", action="store_true")
     ap.add_argument("--launch-timing-only", action="store_true",
-                    help="warm-up and timed steps all with per-launch timing (the library's side stream then runs "
-                         "serialized, as in the roofline pass); prints the per-kernel figures only, for profiling runs")
+                    help="after the warm-up steps, the timed steps with per-launch timing only (the library's side "
+                         "stream then runs serialized, as in the roofline pass); prints the per-kernel figures only, "
+                         "for profiling runs")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="first run a plain 256 MiB device copy (reference for HBM traffic counters)")
     ap.add_argument("--md", action="store_true",
@@ -118,7 +119,12 @@ def main():
         torch.cuda.synchronize()
         del src, dst
     if args.launch_timing_only:
-        n = max(args.warmup, 1) + args.steps
+        # warm-up steps unprofiled (their first launches include one-time
+        # costs), then `steps` steps with every launch timed
+        for _ in range(max(args.warmup, 1)):
+            one_step()
+        torch.cuda.synchronize()
+        n = args.steps
         bd.profile_start(400 * n + 1000)
         for _ in range(n):
             one_step()
