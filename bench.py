@@ -278,8 +278,6 @@ def algorithmic_cost(tag, z):
     N, E, B, A, D, T = z["N"], z["E"], z["B"], z["A"], z["D"], z["T"]
     Tang = T - 1  # layers with an angle update
     f = 4  # bytes per fp32
-    if tag == "gemm_z":
-        return "mfma", T * E * 4 * D * D + Tang * A * 8 * D * D + A * 4 * D * D
     if tag == "gemm_in_bwd" and z.get("fused_bwd"):
         # the edge and angle rows are formed by the fused gate backward; this
         # launch holds the atom rows and the bond rows (k = 8d, 6d last layer)
@@ -395,8 +393,7 @@ def mandatory_cost(tag, z):
 # rocprofv3 kernel symbol of each launch tag that has an algorithmic cost
 def tag_symbol(tag, d):
     return {
-        "gemm_z": "k_gemm<64, 1>",
-        "gemm_in_bwd": "k_gemm<64, 2>",
+        "gemm_in_bwd": "k_gemm<64, 2, 4>",
         "tn_in": "k_tn<1>",
         "k_gate_fwd": "k_gate_fwd_mm<%d>" % d,
         "k_gate_bwd": "k_gate_bwd_mm" if d == 64 else "k_gate_bwd_mm128",

@@ -277,9 +277,9 @@ const char* chgnet_last_error_string(void);
  * chgnet_profile_stop waits for the recorded events, disables timing and
  * writes one line per launch tag into buf (host memory, buflen bytes):
  * "<tag> <launches> <total milliseconds>\n". Tags are kernel names, or the
- * role of a GEMM launch (gemm_z: edge and angle GatedMLP pre-activations;
- * gemm_in_bwd: input gradients of the interaction block; tn_in: weight
- * gradients of the interaction block; ...). Returns CHGNET_EINVAL if buf is
+ * role of a GEMM launch (gemm_proj: per-atom and per-bond terms of the split
+ * first layers; gemm_in_bwd: input gradients of the interaction block;
+ * tn_in: weight gradients of the interaction block; ...). Returns CHGNET_EINVAL if buf is
  * too small and CHGNET_EWORKSPACE if more than max_launches launches ran. */
 int chgnet_profile_start(int max_launches);
 int chgnet_profile_stop(char* buf, size_t buflen);
