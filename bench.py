@@ -390,13 +390,15 @@ def mandatory_cost(tag, z):
     return None, None
 
 
-# rocprofv3 kernel symbol of each launch tag that has an algorithmic cost
-def tag_symbol(tag, d):
+# rocprofv3 kernel symbols of each launch tag that has an algorithmic cost
+# (a tag's call may launch several kernels: tn_in launches its 64 x 128 and
+# its 64 x 64 wave-tile plans separately)
+def tag_symbols(tag, d):
     return {
-        "gemm_in_bwd": "k_gemm<64, 2, 4>",
-        "tn_in": "k_tn<1>",
-        "k_gate_fwd": "k_gate_fwd_mm<%d>" % d,
-        "k_gate_bwd": "k_gate_bwd_mm" if d == 64 else "k_gate_bwd_mm128",
+        "gemm_in_bwd": ["k_gemm<64, 2, 4>"],
+        "tn_in": ["k_tn<1, true>", "k_tn<1, false>"],
+        "k_gate_fwd": ["k_gate_fwd_mm<%d>" % d],
+        "k_gate_bwd": ["k_gate_bwd_mm" if d == 64 else "k_gate_bwd_mm128"],
     }.get(tag)
 
 
@@ -422,8 +424,8 @@ def measured_traffic(workload, tag):
     path = TRAFFIC_FILE % workload
     from paper_2412_20796_amd import synth
 
-    sym = tag_symbol(tag, synth.WORKLOADS.get(workload, (0, 64, 0))[1])
-    if sym is None or not os.path.exists(path):
+    syms = tag_symbols(tag, synth.WORKLOADS.get(workload, (0, 64, 0))[1])
+    if syms is None or not os.path.exists(path):
         return None
     text = open(path).read()
     start = text.find("```json")
@@ -432,8 +434,10 @@ def measured_traffic(workload, tag):
     data = json.loads(text[start + 7:text.index("```", start + 7)])
     if data.get("source_sha256") != source_digest():
         return None
-    k = data["kernels"].get(sym)
-    return None if k is None else k["fetch_bytes"] + k["write_bytes"]
+    # each kernel of the tag is launched once per call (those of a plan kind
+    # the workload has no product for are absent)
+    ks = [data["kernels"][s] for s in syms if s in data["kernels"]]
+    return sum(k["fetch_bytes"] + k["write_bytes"] for k in ks) if ks else None
 
 
 def traffic_summary(fetch_csv, write_csv, workload, command):

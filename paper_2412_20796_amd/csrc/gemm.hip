@@ -445,13 +445,16 @@ struct TnLaunch {
 // of a group of 2 KS rows, lane half h supplies row KS h + i; lane c = lane % 32
 // holds columns vx c + v (v < vx) of the X row and vy c + u of the Y row, so
 // wave tile v of X and u of Y are column-interleaved and the fragment loads
-// are 4- or 8-byte vectors. The next group's fragments are loaded while the
+// are 4-, 8- or 16-byte vectors (vy = 4: 64 x 128 wave tiles, in a launch of
+// their own at two blocks per compute unit). The next group's fragments are loaded while the
 // current group's MFMAs run. The four wavefronts of a block take consecutive
 // quarters of the block's rows; their tiles are added in wave order in LDS.
 // A problem with a bias row also sums the Y columns (the bias gradient of a
 // layer whose weight gradient is X^T Y).
 // ROLE only names the instantiation (1: interaction-block weight gradients).
-constexpr int kTnRed = 2 * 64 * 64 + 4 * 64;
+// reduction buffer: two wave tiles and four wavefronts' column sums
+template <bool WIDE>
+constexpr int tn_red_floats() { return WIDE ? 2 * 64 * 128 + 4 * 128 : 2 * 64 * 64 + 4 * 64; }
 // Rows per split-K chunk at most: the eight output tiles of a chunk stream
 // the same rows on one XCD, and a chunk of 2048 rows of 384 floats (3 MB)
 // stays in that XCD's 4 MB L2 while they do (4480-row chunks measured 1.30
@@ -460,18 +463,25 @@ constexpr int kTnMaxChunkRows = 2048;
 // rows of one wavefront's range (a quarter of a chunk): the size of its
 // LDS row-index tables
 constexpr int kTnWaveRows = kTnMaxChunkRows / 4;
+// 64-row units of a launch (summed over its products and 64 x 64 wave tiles)
+// from which it takes 64 x 128 wave tiles where N allows (enough work that
+// 64 x 64 tiles would fill every block slot with kTnMaxChunkRows-row
+// chunks). Measured per training step:
+// wide128 -0.4 ms; triclinic40 (below the bound) 0.06 ms slower with them.
+constexpr int kTnWideUnits = 3 * 256 * (kTnMaxChunkRows / 64);
 
 // RIDX: the problem gathers X or Y rows through an index array. The wave
-// first copies its range's row indices to LDS (ridx: [2][kTnWaveRows]), so
-// the fragment loads depend on no other global load and the loads of the
-// groups ahead stay in flight.
+// first copies its range's row indices to LDS (ridx: [2][kTnWaveRows], in the
+// reduction buffer, which the block takes over once every wave is past its
+// rows), so the fragment loads depend on no other global load and the loads
+// of the groups ahead stay in flight.
 template <int VX, int VY, bool XFULL, bool YFULL, bool HASX, bool RIDX>
 __device__ __forceinline__ void tn_wave(const TnPlan& Q, int chunk, int m0, int n0, bool colsum, float* red,
                                         int* ridx, float* __restrict__ part) {
   // MFMA k-steps (row pairs) per register buffer: 2, or 1 where two-column
   // fragments are loaded one element at a time (partial or unaligned tiles,
   // not on the common shapes)
-  constexpr int KS = ((VX == 2 && HASX && !XFULL) || (VY == 2 && !YFULL)) ? 1 : 2;
+  constexpr int KS = ((VX == 2 && HASX && !XFULL) || (VY >= 2 && !YFULL)) ? 1 : 2;
   const TnProblem& P = Q.p;
   const int lane = threadIdx.x & 63, c = lane & 31, h = lane >> 5;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // uniform: scalar row range
@@ -529,7 +539,13 @@ __device__ __forceinline__ void tn_wave(const TnPlan& Q, int chunk, int m0, int 
         }
       }
       const float* yp = P.Y + (int64_t)yr[i] * P.ldy + P.y_col;
-      if (YFULL) {
+      if (YFULL && VY == 4) {
+        const float4 t = *reinterpret_cast<const float4*>(yp + yn);
+        yf[b][i][0] = t.x;
+        yf[b][i][1 % VY] = t.y;
+        yf[b][i][2 % VY] = t.z;
+        yf[b][i][VY - 1] = t.w;
+      } else if (YFULL) {
         const float2 t = *reinterpret_cast<const float2*>(yp + yn);
         yf[b][i][0] = t.x;
         yf[b][i][VY - 1] = t.y;
@@ -578,13 +594,16 @@ __device__ __forceinline__ void tn_wave(const TnPlan& Q, int chunk, int m0, int 
       compute(b);
     }
   }
+  // the row-index tables share this LDS: every wavefront is past its rows
+  if (RIDX) __syncthreads();
+  constexpr int TILE = VX * VY * 16 * 64, CS = 32 * VY;  // a wave tile; a wavefront's column sums
   // column sums: the two lane halves hold different rows of the same column
   if (colsum) {
 #pragma unroll
     for (int u = 0; u < VY; ++u) ysum[u] += __shfl_xor(ysum[u], 32);
     if (h == 0) {
 #pragma unroll
-      for (int u = 0; u < VY; ++u) red[2 * 64 * 64 + wave * 64 + u * 32 + c] = ysum[u];
+      for (int u = 0; u < VY; ++u) red[2 * TILE + wave * CS + u * 32 + c] = ysum[u];
     }
   }
   // wave tiles added in the order (w0 + w1) + (w2 + w3)
@@ -605,10 +624,10 @@ __device__ __forceinline__ void tn_wave(const TnPlan& Q, int chunk, int m0, int 
         for (int j = 0; j < 16; ++j) acc[v][u][j] += src[((v * VY + u) * 16 + j) * 64 + lane];
   };
   if (wave == 1) put(red);
-  if (wave == 3) put(red + 64 * 64);
+  if (wave == 3) put(red + TILE);
   __syncthreads();
   if (wave == 0) add(red);
-  if (wave == 2) add(red + 64 * 64);
+  if (wave == 2) add(red + TILE);
   __syncthreads();
   if (wave == 2) put(red);
   __syncthreads();
@@ -631,11 +650,11 @@ __device__ __forceinline__ void tn_wave(const TnPlan& Q, int chunk, int m0, int 
       }
   }
   if (colsum && h == 0) {
-    const float* ys = red + 2 * 64 * 64;
+    const float* ys = red + 2 * TILE;
 #pragma unroll
     for (int u = 0; u < VY; ++u) {
       const int k = u * 32 + c;
-      const float s = (ys[k] + ys[64 + k]) + (ys[128 + k] + ys[192 + k]);
+      const float s = (ys[k] + ys[CS + k]) + (ys[2 * CS + k] + ys[3 * CS + k]);
       const int n = yn + u;
       if (n < P.N) out[(int64_t)P.M * P.N + n] = s;
     }
@@ -666,14 +685,17 @@ __device__ __forceinline__ void tn_dispatch(const TnPlan& Q, int chunk, int m0, 
   }
 }
 
-template <int ROLE>
-__global__ void __launch_bounds__(256, 3) k_tn(TnLaunch L, float* __restrict__ part) {
-  __shared__ float red[kTnRed];
-  __shared__ int ridx_all[4][2][kTnWaveRows];
+// WIDE: the launch of the plans with 64 x 128 wave tiles (their blocks come
+// first); b0 is the launch's first block.
+template <int ROLE, bool WIDE>
+__global__ void __launch_bounds__(256, WIDE ? 2 : 3) k_tn(TnLaunch L, int b0, float* __restrict__ part) {
+  __shared__ float red[tn_red_floats<WIDE>()];
+  static_assert(4 * 2 * kTnWaveRows <= tn_red_floats<false>(), "row-index tables fit in the reduction buffer");
+  const int bid = b0 + (int)blockIdx.x;
   int k = 0;
-  while (k + 1 < L.n && (int)blockIdx.x >= L.q[k + 1].block0) ++k;
+  while (k + 1 < L.n && bid >= L.q[k + 1].block0) ++k;
   const TnPlan& Q = L.q[k];
-  const int lb = blockIdx.x - Q.block0;
+  const int lb = bid - Q.block0;
   const int tiles = max(Q.tiles_m, 1) * Q.tiles_n;
   // The tiles of a row chunk sit 8 block indices apart, so that they run on
   // one XCD (blocks are dealt to the 8 XCDs in turn) and share its L2 for the
@@ -695,10 +717,21 @@ __global__ void __launch_bounds__(256, 3) k_tn(TnLaunch L, float* __restrict__ p
   // the rows are 8-byte aligned
   const TnProblem& P = Q.p;
   const bool xf = Q.vx == 2 && P.X && ((P.ldx | P.x_col) & 1) == 0 && ((uintptr_t)P.X & 7) == 0 && m0 + 64 <= P.M;
-  const bool yf = Q.vy == 2 && ((P.ldy | P.y_col) & 1) == 0 && ((uintptr_t)P.Y & 7) == 0 && n0 + 64 <= P.N;
-  int* ridx = &ridx_all[threadIdx.x >> 6][0][0];
-  if (P.x_rows || P.y_rows) tn_dispatch<true>(Q, chunk, m0, n0, colsum, xf, yf, red, ridx, part);
-  else tn_dispatch<false>(Q, chunk, m0, n0, colsum, xf, yf, red, ridx, part);
+  int* ridx = reinterpret_cast<int*>(red) + (threadIdx.x >> 6) * 2 * kTnWaveRows;
+  if constexpr (WIDE) {
+    const bool yf = ((P.ldy | P.y_col) & 3) == 0 && ((uintptr_t)P.Y & 15) == 0 && n0 + 128 <= P.N;
+    if (P.x_rows || P.y_rows) {
+      if (xf && yf) tn_wave<2, 4, true, true, true, true>(Q, chunk, m0, n0, colsum, red, ridx, part);
+      else tn_wave<2, 4, false, false, true, true>(Q, chunk, m0, n0, colsum, red, ridx, part);
+    } else {
+      if (xf && yf) tn_wave<2, 4, true, true, true, false>(Q, chunk, m0, n0, colsum, red, ridx, part);
+      else tn_wave<2, 4, false, false, true, false>(Q, chunk, m0, n0, colsum, red, ridx, part);
+    }
+  } else {
+    const bool yf = Q.vy == 2 && ((P.ldy | P.y_col) & 1) == 0 && ((uintptr_t)P.Y & 7) == 0 && n0 + 64 <= P.N;
+    if (P.x_rows || P.y_rows) tn_dispatch<true>(Q, chunk, m0, n0, colsum, xf, yf, red, ridx, part);
+    else tn_dispatch<false>(Q, chunk, m0, n0, colsum, xf, yf, red, ridx, part);
+  }
 }
 
 // Ordered column sums of chunk partials: 16 wavefronts per block, wave w
@@ -901,11 +934,26 @@ int tn_launch(const TnBatch& b, float* part, int64_t part_cap, hipStream_t st, c
     q.tiles_n = (int)cdiv(q.p.N, 32 * q.vy);
     units += cdiv(std::max(q.p.R, 0), 64) * std::max(q.tiles_m, 1) * q.tiles_n;
   }
+  // 64 x 128 wave tiles (half the Y fragment loads and row-index reads per
+  // MFMA; two 4-wave blocks per compute unit) for the large launches
+  if (units >= kTnWideUnits) {
+    units = 0;
+    for (int i = 0; i < L.n; ++i) {
+      TnPlan& q = L.q[i];
+      if (q.p.X && q.p.M > 32 && q.p.N % 128 == 0) {
+        q.vy = 4;
+        q.tiles_n = q.p.N / 128;
+      }
+      units += cdiv(std::max(q.p.R, 0), 64) * std::max(q.tiles_m, 1) * q.tiles_n;
+    }
+  }
   // about one block per resident slot (three 4-wave blocks per compute
   // unit): fewer, longer blocks measured faster than several rounds
   const int64_t per = std::max<int64_t>(1, cdiv(units, 3 * 256));
   const int rpc = (int)std::min<int64_t>(64 * per, kTnMaxChunkRows);
-  int64_t off = 0, blocks = 0, maxmn = 0;
+  // the wide plans first: their blocks are the first launch's
+  std::stable_partition(L.q, L.q + L.n, [](const TnPlan& q) { return q.vy == 4; });
+  int64_t off = 0, blocks = 0, maxmn = 0, wide_blocks = 0;
   for (int i = 0; i < L.n; ++i) {
     TnPlan& q = L.q[i];
     q.rpc = rpc;
@@ -916,12 +964,20 @@ int tn_launch(const TnBatch& b, float* part, int64_t part_cap, hipStream_t st, c
     off += (int64_t)q.nchunks * mn;
     blocks += (int64_t)q.nchunks * std::max(q.tiles_m, 1) * q.tiles_n;
     maxmn = std::max(maxmn, mn);
+    if (q.vy == 4) wide_blocks = blocks;
   }
   if (off > part_cap) return fail(CHGNET_EWORKSPACE, "split-K partial buffer too small");
   if (blocks > 0x7fffffff) return fail(CHGNET_EINVAL, "tn: too many blocks");
   if (blocks > 0) {
-    if (std::string(tag) == "tn_in") KLAUNCH(st, tag, k_tn<1><<<(unsigned)blocks, 256, 0, st>>>(L, part));
-    else KLAUNCH(st, tag, k_tn<0><<<(unsigned)blocks, 256, 0, st>>>(L, part));
+    // the wide and the 64 x 64 plans' launches are timed as one under `tag`
+    const bool in = std::string(tag) == "tn_in";
+    const unsigned wb = (unsigned)wide_blocks, nb = (unsigned)(blocks - wide_blocks);
+    KLAUNCH(st, tag, {
+      if (wb > 0 && in) k_tn<1, true><<<wb, 256, 0, st>>>(L, 0, part);
+      if (wb > 0 && !in) k_tn<0, true><<<wb, 256, 0, st>>>(L, 0, part);
+      if (nb > 0 && in) k_tn<1, false><<<nb, 256, 0, st>>>(L, (int)wb, part);
+      if (nb > 0 && !in) k_tn<0, false><<<nb, 256, 0, st>>>(L, (int)wb, part);
+    });
     KLAUNCH(st, "k_tn_reduce", k_tn_reduce<<<dim3((unsigned)cdiv(maxmn, 64), L.n), 1024, 0, st>>>(L, part));
   }
   return CHGNET_OK;
