@@ -872,14 +872,21 @@ int gemm_launch(const GemmBatch& b, hipStream_t st, const char* tag) {
   // multiples of 8 (one per XCD, see k_gemm)
   const int per_problem = std::max(1, 2048 / (gy * b.n));
   const dim3 grid((unsigned)(cdiv(std::min(gx, per_problem), 8) * 8), gy, b.n);
-  // four wavefronts per SIMD where no problem has an activation epilogue and
-  // every segment is at least 128 deep (measured on wide128: the projection,
-  // update and input-gradient launches 4-17 % faster; the SiLU / SiLU'
-  // launches of the heads 17-25 % and the 31-deep embeddings 3 % slower)
+  // four wavefronts per SIMD where no problem has an activation epilogue,
+  // every segment is at least 128 deep and no problem has both more than
+  // 65,536 rows and k > 128 (measured on wide128: the projection, update and
+  // input-gradient launches 4-17 % faster; the SiLU / SiLU' launches of the
+  // heads 17-25 % and the 31-deep embeddings 3 % slower; the Eq. 10 block's
+  // edge and angle input gradients, k = 2d and 4d, 664 against 511 us)
   bool plain = true;
   for (int i = 0; i < b.n; ++i) {
     plain = plain && b.p[i].act == ACT_NONE;
-    for (int s = 0; s < b.p[i].nseg; ++s) plain = plain && b.p[i].seg[s].K >= 128;
+    int k = 0;
+    for (int s = 0; s < b.p[i].nseg; ++s) {
+      plain = plain && b.p[i].seg[s].K >= 128;
+      k += b.p[i].seg[s].K;
+    }
+    plain = plain && !(b.p[i].M > 65536 && k > 128);
   }
   const bool in_bwd = std::string(tag) == "gemm_in_bwd";
   if (in_bwd && plain) KLAUNCH(st, tag, k_gemm<64, 2, 4><<<grid, 256, 0, st>>>(b));
