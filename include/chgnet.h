@@ -29,6 +29,11 @@
  *    buffer per host thread for the size readback (allocated on first use).
  *  - Return value: CHGNET_OK (0) or a negative error code below; the text of
  *    the last error of the calling thread is chgnet_last_error_string().
+ *  - Environment: CHGNET_TN_WIDE_MIN_UNITS (a non-negative integer, read on
+ *    every weight-gradient launch) sets the launch size, in units of 64 rows
+ *    times 64 x 64 output tiles, from which the weight-gradient products use
+ *    64 x 128 wave tiles (default 24576). It changes only the kernel
+ *    schedule, not what is computed; unset is the measured default.
  *
  * Hyperparameters (Sec. IV): feature width d (64; 128 supported), layers T,
  * 31 radial and 31 angular basis functions, envelope exponent p = 8, atom

@@ -11,6 +11,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <cstdlib>
 #include <string>
 
 #include "common.hpp"
@@ -469,6 +470,18 @@ constexpr int kTnWaveRows = kTnMaxChunkRows / 4;
 // chunks). Measured per training step:
 // wide128 -0.4 ms; triclinic40 (below the bound) 0.06 ms slower with them.
 constexpr int kTnWideUnits = 3 * 256 * (kTnMaxChunkRows / 64);
+// The bound in force: CHGNET_TN_WIDE_MIN_UNITS (a non-negative integer,
+// read on every launch) overrides kTnWideUnits, so that the wide tiles can
+// also be run, and checked, on small batches.
+int64_t tn_wide_min_units() {
+  const char* e = std::getenv("CHGNET_TN_WIDE_MIN_UNITS");
+  if (e != nullptr && *e != 0) {
+    char* end = nullptr;
+    const long long v = std::strtoll(e, &end, 10);
+    if (*end == 0 && v >= 0) return v;
+  }
+  return kTnWideUnits;
+}
 
 // RIDX: the problem gathers X or Y rows through an index array. The wave
 // first copies its range's row indices to LDS (ridx: [2][kTnWaveRows], in the
@@ -943,7 +956,7 @@ int tn_launch(const TnBatch& b, float* part, int64_t part_cap, hipStream_t st, c
   }
   // 64 x 128 wave tiles (half the Y fragment loads and row-index reads per
   // MFMA; two 4-wave blocks per compute unit) for the large launches
-  if (units >= kTnWideUnits) {
+  if (units >= tn_wide_min_units()) {
     units = 0;
     for (int i = 0; i < L.n; ++i) {
       TnPlan& q = L.q[i];

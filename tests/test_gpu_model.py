@@ -68,6 +68,19 @@ def test_step_parity_workloads(bd, name):
     _check_step(bd, b, params, targets, d, T, name)
 
 
+def test_step_parity_wide_weight_gradient_tiles(bd, monkeypatch):
+    """The 64 x 128 wave tiles of the weight-gradient products, which the
+    library takes only for large launches, forced on small batches (d = 64
+    and d = 128, gathered and plain rows, bias column sums): full step
+    parity against the oracle."""
+    monkeypatch.setenv("CHGNET_TN_WIDE_MIN_UNITS", "0")
+    b, params, targets, d, T = synth.workload_inputs("triclinic40")
+    _check_step(bd, b, params, targets, d, T, "triclinic40-wide")
+    b = synth.random_crystals(seed=11, n_struct=3, n_lo=4, n_hi=12)
+    _check_step(bd, b, synth.make_params(128, 2, seed=(7, 1, 2)), synth.make_targets(b, seed=(7, 2, 2)), 128, 2,
+                "d128-wide")
+
+
 def test_step_parity_random_small_batches(bd):
     for seed in range(4):
         b = synth.random_crystals(seed=300 + seed, n_struct=1 + seed, n_lo=2, n_hi=14, rho=(0.06, 0.12))
