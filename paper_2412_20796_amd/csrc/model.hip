@@ -1538,6 +1538,9 @@ struct SegJob {
   int nseg, ncb, width, ld_in, ld_out, ld_mul, ld_out2, accumulate, block0;
   int wps;  // wavefronts per (segment, column block): 4 for long segments, 1 for short
   int lpr;  // set by the launch: 0, one column a lane; else lanes per row, four columns a lane
+  // set by the launch on the first job of a pair: the pair's block count (a
+  // multiple of 8); the two jobs' blocks are interleaved (see k_segsum)
+  int pair;
   // optional output linear of the update (64-wide rows only): with y the
   // segment's result (out2 if set, else out), upd[urow(s)] = res[urow(s)]
   // + y Wo + bo, urow = upd_rows ? upd_rows[s] : s
@@ -1559,10 +1562,10 @@ struct SegJobs {
 };
 
 template <int WPS>
-__device__ __forceinline__ void segsum_block(const SegJob& S, float (*red)[64]) {
+__device__ __forceinline__ void segsum_block(const SegJob& S, float (*red)[64], int lb) {
   constexpr int SPB = 4 / WPS;  // (segment, column block) units per block
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int unit = (blockIdx.x - S.block0) * SPB + wave / WPS, w = wave % WPS;
+  const int unit = lb * SPB + wave / WPS, w = wave % WPS;
   const int s = unit / S.ncb, c = (unit % S.ncb) * 64 + lane;
   const bool ok = s < S.nseg && c < S.width;
   float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
@@ -1619,10 +1622,10 @@ __device__ __forceinline__ void segsum_block(const SegJob& S, float (*red)[64]) 
 // every load of a group is issued at once, and with IDX the row indices of
 // the wave's next group are loaded while the current group's rows are.
 template <int WPS, int LPR, int U, bool IDX>
-__device__ __forceinline__ void segsum_block4(const SegJob& S, float4 (*red4)[64]) {
+__device__ __forceinline__ void segsum_block4(const SegJob& S, float4 (*red4)[64], int lb) {
   constexpr int SPB = 4 / WPS, RPI = 64 / LPR, G = U * RPI;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int unit = (blockIdx.x - S.block0) * SPB + wave / WPS, w = wave % WPS;
+  const int unit = lb * SPB + wave / WPS, w = wave % WPS;
   const int s = unit / S.ncb, sub = lane / LPR;
   const int c = (unit % S.ncb) * 4 * LPR + 4 * (lane % LPR);
   const bool ok = s < S.nseg && c < S.width;
@@ -1707,16 +1710,16 @@ __device__ __forceinline__ void segsum_block4(const SegJob& S, float4 (*red4)[64
 }
 
 template <int WPS, int U>
-__device__ __forceinline__ void segsum_job(const SegJob& S, float4 (*red4)[64]) {
-  if (S.lpr == 0) segsum_block<WPS>(S, reinterpret_cast<float (*)[64]>(red4));
+__device__ __forceinline__ void segsum_job(const SegJob& S, float4 (*red4)[64], int lb) {
+  if (S.lpr == 0) segsum_block<WPS>(S, reinterpret_cast<float (*)[64]>(red4), lb);
   else if (S.idx) {
-    if (S.lpr == 64) segsum_block4<WPS, 64, U, true>(S, red4);
-    else if (S.lpr == 32) segsum_block4<WPS, 32, U, true>(S, red4);
-    else segsum_block4<WPS, 16, U, true>(S, red4);
+    if (S.lpr == 64) segsum_block4<WPS, 64, U, true>(S, red4, lb);
+    else if (S.lpr == 32) segsum_block4<WPS, 32, U, true>(S, red4, lb);
+    else segsum_block4<WPS, 16, U, true>(S, red4, lb);
   } else {
-    if (S.lpr == 64) segsum_block4<WPS, 64, U, false>(S, red4);
-    else if (S.lpr == 32) segsum_block4<WPS, 32, U, false>(S, red4);
-    else segsum_block4<WPS, 16, U, false>(S, red4);
+    if (S.lpr == 64) segsum_block4<WPS, 64, U, false>(S, red4, lb);
+    else if (S.lpr == 32) segsum_block4<WPS, 32, U, false>(S, red4, lb);
+    else segsum_block4<WPS, 16, U, false>(S, red4, lb);
   }
 }
 
@@ -1726,8 +1729,20 @@ __global__ void __launch_bounds__(256) k_segsum(SegJobs J) {
   __shared__ float4 red4[4][64];  // wavefront partials (WPS > 1)
   int k = 0;
   while (k + 1 < J.n && (int)blockIdx.x >= J.j[k + 1].block0) ++k;
-  if (J.j[k].wps == 4) segsum_job<4, 8>(J.j[k], red4);
-  else segsum_job<1, 4>(J.j[k], red4);
+  int lb = (int)blockIdx.x - J.j[k].block0;
+  if (J.j[k].pair) {
+    // a pair of sums over the same rows (a segment's out-edges, then its
+    // in-edges through the reverse map): XCD x (blocks are dealt to the 8
+    // XCDs in turn) takes the x-th eighth of the pair's blocks, in which the
+    // two jobs alternate unit by unit, so a row read by its source atom's
+    // block is read again by its destination atom's block, on the same XCD
+    // and at about the same time
+    const int l = (lb & 7) * (J.j[k].pair >> 3) + (lb >> 3);
+    k += l & 1;
+    lb = l >> 1;
+  }
+  if (J.j[k].wps == 4) segsum_job<4, 8>(J.j[k], red4, lb);
+  else segsum_job<1, 4>(J.j[k], red4, lb);
 }
 
 // Per bond b (centre i, local index q among k bonds): DZ1 = sum over the
@@ -2500,6 +2515,28 @@ int segsum_launch(SegJobs J, int wps, hipStream_t st) {
     }
     blocks += (int)cdiv((int64_t)q.nseg * q.ncb, 4 / q.wps);
     K.n++;
+  }
+  // pairs: a plain job and the next over the same rows through an index
+  // (the reverse map) share one interleaved block range
+  blocks = 0;
+  for (int i = 0; i < K.n; ++i) {
+    SegJob& q = K.j[i];
+    q.block0 = blocks;
+    q.pair = 0;
+    const int nb = (int)cdiv((int64_t)q.nseg * q.ncb, 4 / q.wps);
+    if (i + 1 < K.n && blocks % 8 == 0) {
+      const SegJob& r = K.j[i + 1];
+      if (!q.idx && r.idx && r.ptr == q.ptr && r.vals == q.vals && r.nseg == q.nseg && r.ncb == q.ncb &&
+          r.wps == q.wps && r.lpr == q.lpr && !q.Wo && !r.Wo) {
+        q.pair = (int)(8 * cdiv(2 * (int64_t)nb, 8));
+        blocks += q.pair;
+        K.j[i + 1].block0 = blocks;
+        K.j[i + 1].pair = 0;
+        ++i;
+        continue;
+      }
+    }
+    blocks += nb;
   }
   if (blocks == 0) return CHGNET_OK;
   KLAUNCH(st, "k_segsum", k_segsum<<<blocks, 256, 0, st>>>(K));
