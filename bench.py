@@ -326,8 +326,10 @@ def algorithmic_cost(tag, z):
         lay = E * 7 * D + A * 10 * D + N * 9 * D + B * 10 * D
         last = E * 7 * D + A * 5 * D + N * 7 * D + B * 6 * D
         return "hbm", f * (Tang * lay + last)
-    if tag == "k_bond_bwd_reduce":  # read dz twice (both roles), t2; write DZ12
-        return "hbm", f * (Tang * A * (8 * D + D) + A * (4 * D + D) + T * B * 8 * D)
+    if tag == "k_bond_bwd_reduce":
+        # dz read once from HBM (a row's second read, by its other bond, is
+        # scheduled to hit L2), t2 read; DZ12 written
+        return "hbm", f * (Tang * A * (4 * D + D) + A * (2 * D + D) + T * B * 8 * D)
     # training through the conservative readout: the dual-number pass (value
     # and tangent parts; a linear map costs twice its flops, the tangent-only
     # maps once)
