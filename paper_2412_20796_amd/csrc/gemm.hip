@@ -837,10 +837,143 @@ __global__ void __launch_bounds__(256) k_reduce_rows2(ReduceJobs J, int groups_m
   if (w == 0 && k < count) R.out[k] = (float)((double)R.out[k] + (((red[0][lane] + red[1][lane]) + red[2][lane]) + red[3][lane]));
 }
 
+
+// Linear + SiLU layers of the d = 128 readout MLPs (C = A W + b, C2 =
+// silu(C), k = N = 128, more than 32768 rows): each wavefront of a 4-wave
+// block owns 32 output columns and holds its B fragments (64 floats a lane)
+// in registers for the whole launch (reloaded when the problem changes);
+// blocks walk the 32-row tiles of the batch's problems. The A tile of tile
+// i + 1 goes from registers to the other LDS buffer and the A loads of tile
+// i + 2 are issued before the MFMAs of tile i; one block barrier per tile.
+// The epilogue works from the accumulators: lane (h, c) holds column c of
+// rows 8 (j / 4) + 4 h + j % 4, so each store writes two 128-byte row
+// pieces. Measured on wide128: 0.27 -> 0.22 ms per head launch against the
+// LDS-tiled GEMM (which re-reads the weights for every tile); with gathered
+// residuals, scattered outputs or SiLU' factors it was slower and is not
+// used for them.
+struct SiluTiles {
+  int tile0[kMaxGemmProblems + 1];
+};
+constexpr int kSiluRows = 32, kSiluK = 128, kSiluWaves = 4;
+
+__global__ void __launch_bounds__(64 * kSiluWaves, 4) k_gemm_silu(GemmBatch batch, SiluTiles T) {
+  constexpr int R = kSiluRows, K = kSiluK, NW = kSiluWaves, LD = K + 4, F = R * K / (64 * NW), TPR = K / F,
+                KB = K / 32;
+  static_assert(F % 4 == 0 && R * TPR == 64 * NW, "A tile split");
+  __shared__ __attribute__((aligned(16))) float As[2][R * LD];
+  const int tid = threadIdx.x, lane = tid & 63, h = lane >> 5, l32 = lane & 31;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int ntiles = T.tile0[batch.n];
+  const int nt = (int)blockIdx.x < ntiles ? (ntiles - 1 - (int)blockIdx.x) / (int)gridDim.x + 1 : 0;
+  if (nt == 0) return;
+  auto prob_of = [&](int tile) {
+    int k = 0;
+    while (k + 1 < batch.n && tile >= T.tile0[k + 1]) ++k;
+    return k;
+  };
+  auto tile_of = [&](int i) { return (int)blockIdx.x + i * (int)gridDim.x; };
+  // A tile: thread -> row tid / TPR, F columns at F (tid % TPR); rows past M read as zero
+  float4 av[F / 4];
+  auto fetch = [&](int tile) {
+    const int k = prob_of(tile);
+    const GemmProblem& P = batch.p[k];
+    const GemmSeg& S = P.seg[0];
+    const int row = (tile - T.tile0[k]) * R + tid / TPR, ac = F * (tid % TPR);
+#pragma unroll
+    for (int q = 0; q < F / 4; ++q) av[q] = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (row < P.M) {
+      const int64_t ar = P.a_rows ? P.a_rows[row] : row;
+      const float* src = S.A + ar * S.lda + S.a_col + ac;
+#pragma unroll
+      for (int q = 0; q < F / 4; ++q) av[q] = *reinterpret_cast<const float4*>(src + 4 * q);
+    }
+  };
+  auto store = [&](float* X) {
+    const int xr = tid / TPR, ac = F * (tid % TPR);
+#pragma unroll
+    for (int q = 0; q < F / 4; ++q) *reinterpret_cast<float4*>(&X[xr * LD + ac + 4 * q]) = av[q];
+  };
+  // B fragments: MFMA k-step e of k block kb takes k = 32 kb + 16 h + e
+  float bfr[KB][16];
+  int cur = -1;
+  fetch(tile_of(0));
+  store(As[0]);
+  if (nt > 1) fetch(tile_of(1));
+  __syncthreads();
+  for (int i = 0; i < nt; ++i) {
+    const int tile = tile_of(i);
+    const int k = prob_of(tile);
+    const GemmProblem& P = batch.p[k];
+    const int col = 32 * wave + l32;
+    if (k != cur) {
+      cur = k;
+      const GemmSeg& S = P.seg[0];
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int kk = 32 * kb + 16 * h + e;
+          bfr[kb][e] = S.trans ? S.B[(int64_t)col * S.ldb + kk] : S.B[(int64_t)kk * S.ldb + col];
+        }
+    }
+    if (i + 1 < nt) {
+      store(As[(i + 1) & 1]);
+      if (i + 2 < nt) fetch(tile_of(i + 2));
+    }
+    const float* X = As[i & 1];
+    v16f acc;
+#pragma unroll
+    for (int j = 0; j < 16; ++j) acc[j] = 0.f;
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb) {
+      float af[16];
+      const float* ap = &X[l32 * LD + 32 * kb + 16 * h];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const float4 v = *reinterpret_cast<const float4*>(ap + 4 * q);
+        af[4 * q] = v.x; af[4 * q + 1] = v.y; af[4 * q + 2] = v.z; af[4 * q + 3] = v.w;
+      }
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc = __builtin_amdgcn_mfma_f32_32x32x2f32(af[e], bfr[kb][e], acc, 0, 0, 0);
+    }
+    const int r0 = (tile - T.tile0[k]) * R;
+    const float bias = P.bias ? P.bias[col] : 0.f;
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      const int row = r0 + 8 * (j >> 2) + 4 * h + (j & 3);
+      if (row < P.M) {
+        const float x = acc[j] + bias;
+        P.C[(int64_t)row * P.ldc + col] = x;
+        P.C2[(int64_t)row * P.ldc2 + col] = x * sigm(x);
+      }
+    }
+    __syncthreads();
+  }
+}
+
 }  // namespace
 
 int gemm_launch(const GemmBatch& b, hipStream_t st, const char* tag) {
   if (b.n == 0) return CHGNET_OK;
+  {
+    // the Linear + SiLU layers of the d = 128 heads (see k_gemm_silu)
+    bool silu = true;
+    int maxM = 0;
+    SiluTiles T{};
+    for (int i = 0; i < b.n && silu; ++i) {
+      const GemmProblem& P = b.p[i];
+      const GemmSeg& S = P.seg[0];
+      silu = P.nseg == 1 && S.K == kSiluK && P.N == 32 * kSiluWaves && P.act == ACT_SILU_OUT && !P.res &&
+             !P.c_rows && !P.accumulate && ((S.lda | S.a_col) & 3) == 0 && ((uintptr_t)S.A & 15) == 0;
+      maxM = std::max(maxM, P.M);
+      T.tile0[i + 1] = T.tile0[i] + (int)cdiv(std::max(P.M, 0), kSiluRows);
+    }
+    if (silu && maxM > 32768) {
+      const unsigned grid = (unsigned)std::min(T.tile0[b.n], 4 * 256);
+      KLAUNCH(st, tag, k_gemm_silu<<<grid, 64 * kSiluWaves, 0, st>>>(b, T));
+      return CHGNET_OK;
+    }
+  }
   // 64-column tiles: a 128-column variant needs ~170 VGPRs (2 waves per
   // SIMD) and measured slower on every shape used here
   const int BN = 64;
