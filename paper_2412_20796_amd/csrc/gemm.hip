@@ -733,7 +733,16 @@ __global__ void __launch_bounds__(256, WIDE ? 2 : 3) k_tn(TnLaunch L, int b0, fl
   int* ridx = reinterpret_cast<int*>(red) + (threadIdx.x >> 6) * 2 * kTnWaveRows;
   if constexpr (WIDE) {
     const bool yf = ((P.ldy | P.y_col) & 3) == 0 && ((uintptr_t)P.Y & 15) == 0 && n0 + 128 <= P.N;
-    if (P.x_rows || P.y_rows) {
+    if (Q.tiles_m == 0) {
+      // column sums only
+      if (P.x_rows || P.y_rows) {
+        if (yf) tn_wave<1, 4, false, true, false, true>(Q, chunk, m0, n0, colsum, red, ridx, part);
+        else tn_wave<1, 4, false, false, false, true>(Q, chunk, m0, n0, colsum, red, ridx, part);
+      } else {
+        if (yf) tn_wave<1, 4, false, true, false, false>(Q, chunk, m0, n0, colsum, red, ridx, part);
+        else tn_wave<1, 4, false, false, false, false>(Q, chunk, m0, n0, colsum, red, ridx, part);
+      }
+    } else if (P.x_rows || P.y_rows) {
       if (xf && yf) tn_wave<2, 4, true, true, true, true>(Q, chunk, m0, n0, colsum, red, ridx, part);
       else tn_wave<2, 4, false, false, true, true>(Q, chunk, m0, n0, colsum, red, ridx, part);
     } else {
@@ -1088,12 +1097,14 @@ int tn_launch(const TnBatch& b, float* part, int64_t part_cap, hipStream_t st, c
     units += cdiv(std::max(q.p.R, 0), 64) * std::max(q.tiles_m, 1) * q.tiles_n;
   }
   // 64 x 128 wave tiles (half the Y fragment loads and row-index reads per
-  // MFMA; two 4-wave blocks per compute unit) for the large launches
+  // MFMA; two 4-wave blocks per compute unit) for the large launches, and
+  // the column sums of bias-only problems with them (no launch of 64 x 64
+  // tiles is left for those)
   if (units >= tn_wide_min_units()) {
     units = 0;
     for (int i = 0; i < L.n; ++i) {
       TnPlan& q = L.q[i];
-      if (q.p.X && q.p.M > 32 && q.p.N % 128 == 0) {
+      if (q.p.N % 128 == 0 && (!q.p.X || q.p.M > 32)) {
         q.vy = 4;
         q.tiles_n = q.p.N / 128;
       }
