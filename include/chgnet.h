@@ -284,8 +284,11 @@ const char* chgnet_last_error_string(void);
  * "<tag> <launches> <total milliseconds>\n". Tags are kernel names, or the
  * role of a GEMM launch (gemm_proj: per-atom and per-bond terms of the split
  * first layers; gemm_in_bwd: input gradients of the interaction block;
- * tn_in: weight gradients of the interaction block; ...). Returns CHGNET_EINVAL if buf is
- * too small and CHGNET_EWORKSPACE if more than max_launches launches ran. */
+ * tn_in: weight gradients of the interaction block; ...); a call that
+ * launches several kernels under one tag (the weight gradients' 64 x 128
+ * and 64 x 64 wave-tile launches) is timed as one launch. Returns
+ * CHGNET_EINVAL if buf is too small and CHGNET_EWORKSPACE if more than
+ * max_launches launches ran. */
 int chgnet_profile_start(int max_launches);
 int chgnet_profile_stop(char* buf, size_t buflen);
 
