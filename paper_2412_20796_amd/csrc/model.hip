@@ -1767,11 +1767,11 @@ __global__ void __launch_bounds__(256) k_bond_bwd_reduce(int B, int D, const int
   const int b = blk * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   if (b >= B) return;
   const int i = bond_src[b], k0 = bond_ptr[i], k = bond_ptr[i + 1] - k0, q = b - k0;
-  const int lo = angle_ptr[b];
+  // the angles of the centre's bond p are rows angle_ptr[k0] + p (k - 1) ..,
+  // one per other bond in order (the graph's angle order)
+  const int64_t ap0 = angle_ptr[k0], lo = ap0 + (int64_t)q * (k - 1);
   const int64_t ld = 4 * D;
   const int c = lane * CPL;
-  // first angle row of each of the centre's bonds, one per lane (k <= 64)
-  const int apl = lane < k ? angle_ptr[k0 + lane] : 0;
   float s1[2][CPL], s2[2][CPL], tt[2][TPL];
 #pragma unroll
   for (int u = 0; u < 2; ++u) {
@@ -1790,7 +1790,7 @@ __global__ void __launch_bounds__(256) k_bond_bwd_reduce(int B, int D, const int
     j2 = j2 == 0 ? k - 1 : j2 - 1;
     const int u = t & 1;
     const int64_t r1 = lo + (j1 < q ? j1 : j1 - 1);
-    const int64_t r2 = (int64_t)(k <= 64 ? __builtin_amdgcn_readlane(apl, j2) : angle_ptr[k0 + j2]) + (q < j2 ? q : q - 1);
+    const int64_t r2 = ap0 + (int64_t)j2 * (k - 1) + (q < j2 ? q : q - 1);
 #pragma unroll
     for (int x = 0; x < CPL; ++x) {
       s1[u][x] += dzae[r1 * ld + c + x];
