@@ -1766,10 +1766,12 @@ __global__ void __launch_bounds__(256) k_bond_bwd_reduce(int B, int D, const int
   const int blk = (blockIdx.x & 7) * per + (blockIdx.x >> 3);
   const int b = blk * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   if (b >= B) return;
-  const int i = bond_src[b], k0 = bond_ptr[i], k = bond_ptr[i + 1] - k0, q = b - k0;
   // the angles of the centre's bond p are rows angle_ptr[k0] + p (k - 1) ..,
-  // one per other bond in order (the graph's angle order)
-  const int64_t ap0 = angle_ptr[k0], lo = ap0 + (int64_t)q * (k - 1);
+  // one per other bond in order (the graph's angle order); angle_ptr[b] is
+  // loaded beside bond_src[b], not after the centre's bond range
+  const int64_t lo = angle_ptr[b];
+  const int i = bond_src[b], k0 = bond_ptr[i], k = bond_ptr[i + 1] - k0, q = b - k0;
+  const int64_t ap0 = lo - (int64_t)q * (k - 1);
   const int64_t ld = 4 * D;
   const int c = lane * CPL;
   float s1[2][CPL], s2[2][CPL], tt[2][TPL];
