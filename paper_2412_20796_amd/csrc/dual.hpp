@@ -177,6 +177,7 @@ __global__ void __launch_bounds__(256) kd_dz_atoms(int N, int D, int q0, int nbl
   __shared__ float red[4][2][kDzMaxCols * 64];
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
   const int64_t i = blockIdx.x / nblk;
+  if (i >= N) return;  // uniform over the block
   const int q = q0 + (int)(blockIdx.x % nblk);
   const int W2 = 2 * D, nc = W2 / 64;
   int64_t r0, r1;
@@ -517,6 +518,7 @@ __global__ void __launch_bounds__(256) kd_msg_atoms(int N, int D, const int* __r
   __shared__ float red[4][2][kDnMaxV * 64];
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
   const int64_t i = blockIdx.x;
+  if (i >= N) return;  // uniform over the block
   float sv[kDnMaxV] = {}, st[kDnMaxV] = {};
   for (int64_t e = ep[i] + wv; e < ep[i + 1]; e += 4) {
 #pragma unroll

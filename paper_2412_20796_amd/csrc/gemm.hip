@@ -309,7 +309,7 @@ __global__ void __launch_bounds__(512, 2) k_gemm_w(GemmBatch batch) {
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int tl = wave / WK, kp = wave % WK;
   const int r0 = (blockIdx.x * TPB + tl) * 32, n0 = blockIdx.y * 64;
-  if (blockIdx.x * TPB * 32 >= P.M || n0 >= P.N) return;  // uniform over the block
+  if ((int)blockIdx.x * TPB * 32 >= P.M || n0 >= P.N) return;  // uniform over the block
   int groups = 0;
   for (int s = 0; s < P.nseg; ++s) groups += (P.seg[s].K + 7) / 8;
   const int g_lo = kp * groups / WK, g_hi = (kp + 1) * groups / WK;

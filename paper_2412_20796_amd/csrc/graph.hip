@@ -222,7 +222,7 @@ __global__ void k_scan_single(int n, const int* __restrict__ in, int* __restrict
     part[threadIdx.x] = v;
     __syncthreads();
     for (int off = 1; off < (int)blockDim.x; off <<= 1) {
-      int t = threadIdx.x >= off ? part[threadIdx.x - off] : 0;
+      int t = (int)threadIdx.x >= off ? part[threadIdx.x - off] : 0;
       __syncthreads();
       part[threadIdx.x] += t;
       __syncthreads();
@@ -385,7 +385,7 @@ __global__ void k_scan_counts(int N, const int* __restrict__ edge_count, const i
     __syncthreads();
     for (int off = 1; off < (int)blockDim.x; off <<= 1) {
       long long te = 0, tb = 0, ta = 0;
-      if (threadIdx.x >= off) { te = pe[threadIdx.x - off]; tb = pb[threadIdx.x - off]; ta = pa[threadIdx.x - off]; }
+      if ((int)threadIdx.x >= off) { te = pe[threadIdx.x - off]; tb = pb[threadIdx.x - off]; ta = pa[threadIdx.x - off]; }
       __syncthreads();
       pe[threadIdx.x] += te; pb[threadIdx.x] += tb; pa[threadIdx.x] += ta;
       __syncthreads();

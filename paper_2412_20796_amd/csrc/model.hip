@@ -1833,6 +1833,7 @@ __global__ void __launch_bounds__(256) k_struct_heads(int S, const int* __restri
                                                       const float* __restrict__ oE, const float* __restrict__ oS,
                                                       float* __restrict__ energy, float* __restrict__ stress) {
   const int s = blockIdx.x;
+  if (s >= S) return;  // uniform over the block
   __shared__ double red[10][256];
   double acc[10];
   for (int k = 0; k < 10; ++k) acc[k] = 0.0;
@@ -2058,7 +2059,7 @@ __global__ void __launch_bounds__(256) k_rbf_fgrad(int rows, const int* __restri
   if (np == 32) acc += __shfl_xor(acc, 32);
   if (lane < np) red[wave][lane] = acc;
   __syncthreads();
-  if (threadIdx.x < R)
+  if ((int)threadIdx.x < R)
     part[(int64_t)blockIdx.x * R + threadIdx.x] = ((red[0][threadIdx.x] + red[1][threadIdx.x]) + red[2][threadIdx.x]) + red[3][threadIdx.x];
 }
 
@@ -2201,6 +2202,7 @@ __global__ void __launch_bounds__(256) k_cons_stress(int S, const int* __restric
                                                      const float* __restrict__ xhat, const float* __restrict__ gvec,
                                                      const float* __restrict__ lattice, float* __restrict__ stress) {
   const int s = blockIdx.x;
+  if (s >= S) return;  // uniform over the block
   __shared__ double red[9][256];
   double acc[9];
   for (int k = 0; k < 9; ++k) acc[k] = 0.0;
@@ -2773,7 +2775,7 @@ int forward_impl(Ctx& c, const float* Pflat, float* energy, float* forces, float
   const float* P = a.Pal;
   const chgnet_graph& g = *c.graph;
   const chgnet_batch& bt = *c.batch;
-  const int D = m.D, V = D / 64;
+  const int D = m.D;
   const int64_t N = m.N, S = m.S, E = m.E, B = m.B, A = m.A;
 
   // geometry, bases and v0 (Eq. 2)
@@ -3084,7 +3086,7 @@ int backward_impl(Ctx& c, const float* Pflat, bool repack, const float* dE, cons
   const float* P = a.Pal;
   const chgnet_graph& g = *c.graph;
   const chgnet_batch& bt = *c.batch;
-  const int D = m.D, V = D / 64;
+  const int D = m.D;
   const int64_t N = m.N, E = m.E, B = m.B, A = m.A;
 
   const bool wg = G != nullptr;
