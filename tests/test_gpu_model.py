@@ -302,3 +302,26 @@ def test_bitwise_reproducible(bd):
     l2, g2 = bd.step(hp, db, g, p, tg, ws)
     assert np.array_equal(l1, l2.cpu().numpy())
     assert np.array_equal(g1, g2.cpu().numpy())
+
+
+@pytest.mark.parametrize("wide", ["default", "0"])
+def test_profile_counts_launches_by_tag(bd, monkeypatch, wide):
+    """chgnet_profile_start/stop: one training step of T layers reports the
+    fused gate launches, one weight-gradient launch per layer under tn_in
+    (also where the 64 x 128 and 64 x 64 wave-tile kernels both run) and
+    positive times; profiling changes no result."""
+    if wide != "default":
+        monkeypatch.setenv("CHGNET_TN_WIDE_MIN_UNITS", wide)
+    b, params, targets, d, T = synth.workload_inputs("triclinic40")
+    hp, db, g, ws = _setup(bd, b, d, T)
+    p = _dev(params)
+    tg = [_dev(x) for x in targets]
+    loss0, grad0 = bd.step(hp, db, g, p, tg, ws)
+    grad0 = grad0.cpu().numpy()
+    bd.profile_start()
+    loss1, grad1 = bd.step(hp, db, g, p, tg, ws)
+    prof = bd.profile_stop()
+    assert np.array_equal(grad1.cpu().numpy(), grad0)
+    assert prof["k_gate_fwd"][0] == T and prof["k_gate_bwd"][0] == T
+    assert prof["tn_in"][0] == T
+    assert all(n > 0 and ms > 0 for n, ms in prof.values())
