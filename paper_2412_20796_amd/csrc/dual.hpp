@@ -1303,7 +1303,7 @@ int cons_grad_impl(Ctx& c, const float* dE, const float* dF, const float* dS, co
 
   // embedding (Eq. 2) and sRBF frequencies
   // element table rows: g[Z_i - 1] += d v0_i (tangent), summed per element in atom order
-  KLAUNCH(st, "kd_embed", k_embed_bwd_Z<<<24, 256, 0, st>>>((int)N, D, bt.Z, d.dv[1], gB + Lg.W_Z));
+  KLAUNCH(st, "kd_embed", k_embed_bwd_Z<<<94, 64 * kEmbZWaves, 0, st>>>((int)N, D, bt.Z, d.dv[1], gB + Lg.W_Z));
   cross(E, R, D, a.rbf_a, d.rbfa_t, R, nullptr, d.de, D, nullptr, Lg.W_e, 2 * D);
   colsum(E, D, d.de[1], D, nullptr, Lg.b_e0);
   cross(E, R, D, a.rbf_a, d.rbfa_t, R, nullptr, d.dea, D, nullptr, Lg.W_e + D, 2 * D);

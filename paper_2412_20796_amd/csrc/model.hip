@@ -2010,24 +2010,67 @@ __global__ void k_seed_edges2(int E, const int* __restrict__ edge_rev, const flo
   if (e < E) doF[e] = 0.5f * (dn[e] + dn[edge_rev[e]]);
 }
 
-// dW_Z[z] = sum over atoms with Z_i = z+1 of dv0_i, in atom order. One
-// wavefront per element: lanes scan 64 atoms at a time, then the matching
-// rows are added in order (lanes over columns).
-__global__ void __launch_bounds__(256) k_embed_bwd_Z(int N, int D, const int* __restrict__ Z, const float* __restrict__ dv0,
-                                                     float* __restrict__ gWZ) {
-  const int z = blockIdx.x * 4 + (threadIdx.x >> 6) + 1, lane = threadIdx.x & 63;
-  if (z > 94) return;
+// Gradient of the element table W_Z: row z - 1 gets the sum of dv0 over the
+// atoms with Z = z. One block per element; wavefront w scans the w-th eighth
+// of the atoms (Z of 8 x 64 atoms loaded at once) and adds the rows of its
+// matches in atom order, up to 8 rows' loads issued together; the eight
+// partial sums are added in wavefront order.
+constexpr int kEmbZWaves = 8;
+__global__ void __launch_bounds__(64 * kEmbZWaves) k_embed_bwd_Z(int N, int D, const int* __restrict__ Z,
+                                                                 const float* __restrict__ dv0, float* __restrict__ gWZ) {
+  __shared__ float red[kEmbZWaves][2][64];
+  const int z = blockIdx.x + 1, lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int lo = (int)((int64_t)N * w / kEmbZWaves), hi = (int)((int64_t)N * (w + 1) / kEmbZWaves);
   float acc0 = 0.f, acc1 = 0.f;
-  for (int base = 0; base < N; base += 64) {
-    const int i = base + lane;
-    unsigned long long m = __ballot(i < N && Z[i] == z);
-    while (m) {
-      const int b = __ffsll(m) - 1;
-      m &= m - 1;
-      const int64_t row = (int64_t)(base + b) * D;
-      acc0 += dv0[row + lane];
-      if (D > 64) acc1 += dv0[row + 64 + lane];
+  for (int base = lo; base < hi; base += 512) {
+    int zz[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int i = base + 64 * u + lane;
+      zz[u] = i < hi ? Z[i] : 0;
     }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      unsigned long long m = __ballot(zz[u] == z);
+      const int b0 = base + 64 * u;
+      while (m) {
+        int rows[8];
+        int nr = 0;
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+          rows[q] = 0;
+          if (m) {
+            rows[q] = b0 + __ffsll(m) - 1;
+            m &= m - 1;
+            nr = q + 1;
+          }
+        }
+        float v0[8], v1[8];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+          v0[q] = v1[q] = 0.f;
+          if (q < nr) {
+            const int64_t row = (int64_t)rows[q] * D;
+            v0[q] = dv0[row + lane];
+            if (D > 64) v1[q] = dv0[row + 64 + lane];
+          }
+        }
+#pragma unroll
+        for (int q = 0; q < 8; ++q)
+          if (q < nr) {
+            acc0 += v0[q];
+            if (D > 64) acc1 += v1[q];
+          }
+      }
+    }
+  }
+  red[w][0][lane] = acc0;
+  red[w][1][lane] = acc1;
+  __syncthreads();
+  if (w != 0) return;
+  for (int q = 1; q < kEmbZWaves; ++q) {
+    acc0 += red[q][0][lane];
+    acc1 += red[q][1][lane];
   }
   gWZ[(int64_t)(z - 1) * D + lane] += acc0;
   if (D > 64) gWZ[(int64_t)(z - 1) * D + 64 + lane] += acc1;
@@ -3475,7 +3518,7 @@ int backward_impl(Ctx& c, const float* Pflat, bool repack, const float* dE, cons
   }
 
   // embeddings
-  if (wg) KLAUNCH(st, "k_embed_bwd_Z", k_embed_bwd_Z<<<24, 256, 0, st>>>((int)N, D, bt.Z, a.dv[cur], G + Lg.W_Z));
+  if (wg) KLAUNCH(st, "k_embed_bwd_Z", k_embed_bwd_Z<<<94, 64 * kEmbZWaves, 0, st>>>((int)N, D, bt.Z, a.dv[cur], G + Lg.W_Z));
   {
     std::vector<TnProblem> ts;
     ts.push_back(tp(E, m.R, D, a.rbf_a, m.R, 0, nullptr, a.de[ecur], D, 0, nullptr, G + Lg.W_e, 2 * D));
