@@ -1933,31 +1933,33 @@ __device__ __forceinline__ double rho(double r, double delta, double& g) {
 
 // Loss (weighted mean errors, per-atom energy) and its gradient; one block,
 // fp64 accumulation in a fixed order.
-__global__ void __launch_bounds__(256) k_loss(int S, int N, const int* __restrict__ atom_ptr, const float* __restrict__ energy,
+// one block; per-thread partial sums, then a fixed-order tree over the threads
+constexpr int kLossThreads = 1024;
+__global__ void __launch_bounds__(kLossThreads) k_loss(int S, int N, const int* __restrict__ atom_ptr, const float* __restrict__ energy,
                                               const float* __restrict__ forces, const float* __restrict__ stress,
                                               const float* __restrict__ om, const float* __restrict__ Et,
                                               const float* __restrict__ Ft, const float* __restrict__ St,
                                               const float* __restrict__ Mt, chgnet_loss lw, float* __restrict__ loss,
                                               float* __restrict__ dE, float* __restrict__ dF, float* __restrict__ dS,
                                               float* __restrict__ dM) {
-  __shared__ double red[4][256];
+  __shared__ double red[4][kLossThreads];
   const double delta = lw.huber_delta;
   double le = 0.0, lf = 0.0, ls = 0.0, lm = 0.0, g;
-  for (int s = threadIdx.x; s < S; s += 256) {
+  for (int s = threadIdx.x; s < S; s += kLossThreads) {
     const double n = (double)(atom_ptr[s + 1] - atom_ptr[s]);
     le += rho((double)energy[s] / n - (double)Et[s], delta, g);
     dE[s] = (float)(lw.w_energy * g / n / S);
   }
-  for (int k = threadIdx.x; k < 3 * N; k += 256) {
+  for (int k = threadIdx.x; k < 3 * N; k += kLossThreads) {
     lf += rho((double)forces[k] - (double)Ft[k], delta, g);
     dF[k] = (float)(lw.w_force * g / (3.0 * N));
   }
-  for (int k = threadIdx.x; k < 9 * S; k += 256) {
+  for (int k = threadIdx.x; k < 9 * S; k += kLossThreads) {
     ls += rho((double)stress[k] - (double)St[k], delta, g);
     dS[k] = (float)(lw.w_stress * g / (9.0 * S));
   }
   if (om)
-    for (int k = threadIdx.x; k < N; k += 256) {
+    for (int k = threadIdx.x; k < N; k += kLossThreads) {
       lm += rho(fabs((double)om[k]) - (double)Mt[k], delta, g);
       dM[k] = (float)(lw.w_magmom * g / N);
     }
@@ -1966,7 +1968,7 @@ __global__ void __launch_bounds__(256) k_loss(int S, int N, const int* __restric
   red[2][threadIdx.x] = ls;
   red[3][threadIdx.x] = lm;
   __syncthreads();
-  for (int off = 128; off > 0; off >>= 1) {
+  for (int off = kLossThreads / 2; off > 0; off >>= 1) {
     if ((int)threadIdx.x < off)
       for (int k = 0; k < 4; ++k) red[k][threadIdx.x] += red[k][threadIdx.x + off];
     __syncthreads();
@@ -3692,7 +3694,7 @@ int step_entry(const chgnet_hparams* hp, const chgnet_batch* batch, chgnet_graph
   CHG_TRY(forward_impl(c, params, e_out, f_out, s_out, nullptr, st, false));
   if (hp->conservative) CHG_TRY(conservative_impl(c, f_out, s_out, st));
   const bool mag = hp->magmom != 0;
-  KLAUNCH(st, "k_loss", k_loss<<<1, 256, 0, st>>>((int)c.dm.S, (int)c.dm.N, batch->atom_ptr, e_out, f_out, s_out,
+  KLAUNCH(st, "k_loss", k_loss<<<1, kLossThreads, 0, st>>>((int)c.dm.S, (int)c.dm.N, batch->atom_ptr, e_out, f_out, s_out,
                                                    mag ? c.a.oM : nullptr, E_t, F_t, S_t, M_t, *loss_cfg, loss, c.a.dE,
                                                    c.a.dF, c.a.dS, c.a.dM));
   if (hp->conservative) CHG_TRY(cons_grad_impl(c, c.a.dE, c.a.dF, c.a.dS, mag ? c.a.dM : nullptr, grad, st));
