@@ -210,27 +210,59 @@ __global__ void k_atom_bin(int N, int S, const int* __restrict__ atom_ptr, const
   atomicAdd(&bin_count[bin], 1);
 }
 
-// Exclusive scan of n ints with one block (any n). out[n] = total.
-__global__ void k_scan_single(int n, const int* __restrict__ in, int* __restrict__ out) {
-  __shared__ int part[1024];
-  __shared__ int carry;
-  if (threadIdx.x == 0) carry = 0;
+// Scans in a fixed order: a wavefront's inclusive scan by lane shuffles,
+// and a block's exclusive scan from its wavefronts' totals (sh: 17 slots of
+// shared memory; every thread of the block takes part).
+template <class T>
+__device__ __forceinline__ T wave_incl_scan(T v, int lane) {
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const T t = __shfl_up(v, d, 64);
+    if (lane >= d) v += t;
+  }
+  return v;
+}
+template <class T>
+__device__ __forceinline__ T block_excl_scan(T v, T* sh, T& total) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, nw = (int)(blockDim.x + 63) >> 6;
+  const T inc = wave_incl_scan(v, lane);
+  if (lane == 63) sh[w] = inc;
   __syncthreads();
-  for (int base = 0; base < n; base += blockDim.x) {
-    int idx = base + threadIdx.x;
-    int v = idx < n ? in[idx] : 0;
-    part[threadIdx.x] = v;
-    __syncthreads();
-    for (int off = 1; off < (int)blockDim.x; off <<= 1) {
-      int t = (int)threadIdx.x >= off ? part[threadIdx.x - off] : 0;
-      __syncthreads();
-      part[threadIdx.x] += t;
-      __syncthreads();
+  if (w == 0) {
+    const T t = lane < nw ? sh[lane] : T(0);
+    const T ti = wave_incl_scan(t, lane);
+    if (lane < nw) sh[lane] = ti - t;
+    if (lane == nw - 1) sh[16] = ti;
+  }
+  __syncthreads();
+  const T r = sh[w] + inc - v;
+  total = sh[16];
+  __syncthreads();
+  return r;
+}
+
+// Exclusive scan of n ints with one 1024-thread block (any n), 8 consecutive
+// values a thread per pass. out[n] = total.
+constexpr int kScanPer = 8;
+__global__ void __launch_bounds__(1024) k_scan_single(int n, const int* __restrict__ in, int* __restrict__ out) {
+  __shared__ int sh[17];
+  int carry = 0;
+  for (int base = 0; base < n; base += (int)blockDim.x * kScanPer) {
+    const int i0 = base + (int)threadIdx.x * kScanPer;
+    int v[kScanPer], sum = 0;
+#pragma unroll
+    for (int q = 0; q < kScanPer; ++q) {
+      v[q] = i0 + q < n ? in[i0 + q] : 0;
+      sum += v[q];
     }
-    if (idx < n) out[idx] = carry + part[threadIdx.x] - v;
-    __syncthreads();
-    if (threadIdx.x == blockDim.x - 1) carry += part[threadIdx.x];
-    __syncthreads();
+    int total;
+    int run = carry + block_excl_scan(sum, sh, total);
+#pragma unroll
+    for (int q = 0; q < kScanPer; ++q) {
+      if (i0 + q < n) out[i0 + q] = run;
+      run += v[q];
+    }
+    carry += total;
   }
   if (threadIdx.x == 0) out[n] = carry;
 }
@@ -363,42 +395,46 @@ __global__ void __launch_bounds__(kSearchThreads) k_count(SearchArgs A, int* __r
 }
 
 // Exclusive scans of edge counts, bond counts and k(k-1); totals into ginfo.
-__global__ void k_scan_counts(int N, const int* __restrict__ edge_count, const int* __restrict__ bond_count,
-                              int* __restrict__ edge_ptr, int* __restrict__ bond_ptr, long long* __restrict__ angle_base,
-                              GraphInfo* ginfo) {
-  __shared__ long long pe[1024], pb[1024], pa[1024];
-  __shared__ long long ce, cb, ca;
+__global__ void __launch_bounds__(1024) k_scan_counts(int N, const int* __restrict__ edge_count,
+                                                     const int* __restrict__ bond_count, int* __restrict__ edge_ptr,
+                                                     int* __restrict__ bond_ptr, long long* __restrict__ angle_base,
+                                                     GraphInfo* ginfo) {
+  __shared__ long long sh[17];
   __shared__ int mx[1024];
-  if (threadIdx.x == 0) { ce = cb = ca = 0; }
+  long long ce = 0, cb = 0, ca = 0;
   int my_max = 0;
-  __syncthreads();
-  for (int base = 0; base < N; base += blockDim.x) {
-    const int idx = base + threadIdx.x;
-    long long ve = 0, vb = 0, va = 0;
-    if (idx < N) {
-      ve = edge_count[idx];
-      vb = bond_count[idx];
-      va = vb * (vb - 1);
-      my_max = max(my_max, (int)ve);
+  for (int base = 0; base < N; base += (int)blockDim.x * kScanPer) {
+    const int i0 = base + (int)threadIdx.x * kScanPer;
+    int ve[kScanPer], vb[kScanPer];
+    long long se = 0, sb = 0, sa = 0;
+#pragma unroll
+    for (int q = 0; q < kScanPer; ++q) {
+      const bool in = i0 + q < N;
+      ve[q] = in ? edge_count[i0 + q] : 0;
+      vb[q] = in ? bond_count[i0 + q] : 0;
+      se += ve[q];
+      sb += vb[q];
+      sa += (long long)vb[q] * (vb[q] - 1);
+      my_max = max(my_max, ve[q]);
     }
-    pe[threadIdx.x] = ve; pb[threadIdx.x] = vb; pa[threadIdx.x] = va;
-    __syncthreads();
-    for (int off = 1; off < (int)blockDim.x; off <<= 1) {
-      long long te = 0, tb = 0, ta = 0;
-      if ((int)threadIdx.x >= off) { te = pe[threadIdx.x - off]; tb = pb[threadIdx.x - off]; ta = pa[threadIdx.x - off]; }
-      __syncthreads();
-      pe[threadIdx.x] += te; pb[threadIdx.x] += tb; pa[threadIdx.x] += ta;
-      __syncthreads();
+    long long te, tb, ta;
+    long long e0 = ce + block_excl_scan(se, sh, te);
+    long long b0 = cb + block_excl_scan(sb, sh, tb);
+    long long a0 = ca + block_excl_scan(sa, sh, ta);
+#pragma unroll
+    for (int q = 0; q < kScanPer; ++q) {
+      if (i0 + q < N) {
+        edge_ptr[i0 + q] = (int)(e0 < INT_MAX ? e0 : INT_MAX);
+        bond_ptr[i0 + q] = (int)(b0 < INT_MAX ? b0 : INT_MAX);
+        angle_base[i0 + q] = a0;
+      }
+      e0 += ve[q];
+      b0 += vb[q];
+      a0 += (long long)vb[q] * (vb[q] - 1);
     }
-    if (idx < N) {
-      long long e0 = ce + pe[threadIdx.x] - ve, b0 = cb + pb[threadIdx.x] - vb, a0 = ca + pa[threadIdx.x] - va;
-      edge_ptr[idx] = (int)(e0 < INT_MAX ? e0 : INT_MAX);
-      bond_ptr[idx] = (int)(b0 < INT_MAX ? b0 : INT_MAX);
-      angle_base[idx] = a0;
-    }
-    __syncthreads();
-    if (threadIdx.x == blockDim.x - 1) { ce += pe[threadIdx.x]; cb += pb[threadIdx.x]; ca += pa[threadIdx.x]; }
-    __syncthreads();
+    ce += te;
+    cb += tb;
+    ca += ta;
   }
   mx[threadIdx.x] = my_max;
   __syncthreads();
