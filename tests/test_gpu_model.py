@@ -292,8 +292,12 @@ def test_adam_kernel_on_its_own_gradient(bd):
         assert np.count_nonzero(pg != p0) > 0.5 * pg.size
 
 
-def test_bitwise_reproducible(bd):
-    b, params, targets, d, T = synth.workload_inputs("triclinic40")
+@pytest.mark.parametrize("name", ["triclinic40", "wide128"])
+def test_bitwise_reproducible(bd, name):
+    """Two steps on the same inputs give bitwise the same loss and gradient
+    (every sum in a fixed order; wide128 runs the d = 128 kernels, the
+    64 x 128 weight-gradient tiles and the SiLU head GEMM)."""
+    b, params, targets, d, T = synth.workload_inputs(name)
     hp, db, g, ws = _setup(bd, b, d, T)
     p = _dev(params)
     tg = [_dev(x) for x in targets]
