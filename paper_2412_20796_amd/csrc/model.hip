@@ -161,40 +161,50 @@ __global__ void __launch_bounds__(256) k_geom(GeomArgs g) {
     return;
   }
   blk -= g.nb_edges;
-  const int al = blk * 256 + tid;
-  if (al >= g.A) return;
-  const int b1 = upper_bound_idx(g.angle_ptr, g.B + 1, al);
-  const int i = upper_bound_idx(g.bond_ptr, g.N + 1, b1);
-  const int k0 = g.bond_ptr[i];
-  const int p = b1 - k0;
-  const int q0 = al - g.angle_ptr[b1];
-  const int b2 = k0 + (q0 < p ? q0 : q0 + 1);
-  g.ang_b1[al] = b1;
-  g.ang_b2[al] = b2;
-  g.ang_ctr[al] = i;
-  const float* L = g.lattice + 9 * upper_bound_idx(g.atom_ptr, g.S + 1, i);
-  double r[2][3];
-  const int es[2] = {g.bond_edge[b1], g.bond_edge[b2]};
-  for (int s = 0; s < 2; ++s) edge_vector(i, g.edge_dst[es[s]], g.edge_img + 3 * es[s], L, g.pos, r[s]);
-  const double dot = r[0][0] * r[1][0] + r[0][1] * r[1][1] + r[0][2] * r[1][2];
-  const double cx = r[0][1] * r[1][2] - r[0][2] * r[1][1];
-  const double cy = r[0][2] * r[1][0] - r[0][0] * r[1][2];
-  const double cz = r[0][0] * r[1][1] - r[0][1] * r[1][0];
-  const double cr = sqrt(cx * cx + cy * cy + cz * cz);
-  const double h = sqrt(dot * dot + cr * cr);
-  const double c1 = dot / h, s1 = cr / h;
-  const int M = (g.K - 1) / 2;
-  float* o = g.ft + (int64_t)al * g.K;
-  const double inv_sqrt_pi = 0.56418958354775628695;
-  o[0] = (float)(inv_sqrt_pi * 0.70710678118654752440);
-  double cm = 1.0, sm = 0.0;
-  for (int m = 1; m <= M; ++m) {
-    const double cn = cm * c1 - sm * s1, sn = sm * c1 + cm * s1;
-    cm = cn;
-    sm = sn;
-    o[m] = (float)(cm * inv_sqrt_pi);
-    o[M + m] = (float)(sm * inv_sqrt_pi);
+  const int a0 = blk * 256, al = a0 + tid;
+  const int na = min(256, g.A - a0);
+  // the block's Fourier rows go through LDS, so that they are written as
+  // one contiguous run
+  __shared__ float fts[256 * 32];
+  if (al < g.A) {
+    const int b1 = upper_bound_idx(g.angle_ptr, g.B + 1, al);
+    const int i = upper_bound_idx(g.bond_ptr, g.N + 1, b1);
+    const int k0 = g.bond_ptr[i];
+    const int p = b1 - k0;
+    const int q0 = al - g.angle_ptr[b1];
+    const int b2 = k0 + (q0 < p ? q0 : q0 + 1);
+    g.ang_b1[al] = b1;
+    g.ang_b2[al] = b2;
+    g.ang_ctr[al] = i;
+    const float* L = g.lattice + 9 * upper_bound_idx(g.atom_ptr, g.S + 1, i);
+    double r[2][3];
+    const int es[2] = {g.bond_edge[b1], g.bond_edge[b2]};
+    for (int s = 0; s < 2; ++s) edge_vector(i, g.edge_dst[es[s]], g.edge_img + 3 * es[s], L, g.pos, r[s]);
+    const double dot = r[0][0] * r[1][0] + r[0][1] * r[1][1] + r[0][2] * r[1][2];
+    const double cx = r[0][1] * r[1][2] - r[0][2] * r[1][1];
+    const double cy = r[0][2] * r[1][0] - r[0][0] * r[1][2];
+    const double cz = r[0][0] * r[1][1] - r[0][1] * r[1][0];
+    const double cr = sqrt(cx * cx + cy * cy + cz * cz);
+    const double h = sqrt(dot * dot + cr * cr);
+    const double c1 = dot / h, s1 = cr / h;
+    const int M = (g.K - 1) / 2;
+    // n_fourier up to 32 is staged (the default 31); longer rows go straight out
+    float* o = g.K <= 32 ? fts + tid * g.K : g.ft + (int64_t)al * g.K;
+    const double inv_sqrt_pi = 0.56418958354775628695;
+    o[0] = (float)(inv_sqrt_pi * 0.70710678118654752440);
+    double cm = 1.0, sm = 0.0;
+    for (int m = 1; m <= M; ++m) {
+      const double cn = cm * c1 - sm * s1, sn = sm * c1 + cm * s1;
+      cm = cn;
+      sm = sn;
+      o[m] = (float)(cm * inv_sqrt_pi);
+      o[M + m] = (float)(sm * inv_sqrt_pi);
+    }
   }
+  if (g.K > 32) return;  // uniform over the block
+  __syncthreads();
+  float* out = g.ft + (int64_t)a0 * g.K;
+  for (int t = tid; t < na * g.K; t += 256) out[t] = fts[t];
 }
 
 // Per bond (256 a block): source atom and the block's sRBF rows at the bond
