@@ -179,3 +179,15 @@ def test_boundary_sweeps_bit_exact(bd, kind):
     assert_graph_equal(got, og.build_graph(b.atom_ptr, b.pos, b.lattice))
     rev = got["edge_rev"]
     assert (rev[rev] == np.arange(len(rev))).all()
+
+
+def test_graph_more_atoms_than_one_scan_pass(bd):
+    """Over 8192 atoms and bins: the count and bin scans run several passes
+    (8 x 1024 values a pass) and carry between them; the graph stays
+    bit-exact."""
+    b = synth.random_crystals(seed=77, n_struct=240, n_lo=30, n_hi=46, rho=(0.07, 0.10))
+    assert b.n_atoms > 8192
+    got, g = gpu_graph(bd, b)
+    ref = og.build_graph(b.atom_ptr, b.pos, b.lattice)
+    print("N", b.n_atoms, "E", g.n_edges, "B", g.n_bonds, "A", g.n_angles)
+    assert_graph_equal(got, ref)
